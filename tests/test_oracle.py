@@ -1,0 +1,383 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these tests compares the oracle with itself: they use hand-derived
+worked examples (tests/golden/hand_cases.json), closed forms, central finite
+differences, PyTorch-CPU autograd and torch.optim.Adam in float64 (library
+routines, used here only), brute force on tiny inputs, and invariances.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle as O
+from ffinputs import make_data, make_weights, random_labels, random_matrix
+
+GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "hand_cases.json")))
+
+
+def _layer(case):
+    return np.array(case["W"], float), np.array(case["b"], float)
+
+
+# ---------------------------------------------------------------- worked examples
+@pytest.mark.parametrize("name", ["layer_identity_34", "layer_asymmetric"])
+def test_forward_hand(name):
+    c = GOLD[name]
+    W, b = _layer(c)
+    xh, z, h, g = O.layer_forward(W, b, np.array(c["x"]), c["norm_eps"])
+    np.testing.assert_allclose(xh, c["x_hat"], rtol=0, atol=1e-15)
+    np.testing.assert_allclose(h, c["h"], rtol=0, atol=1e-14)
+    np.testing.assert_allclose(g, c["g"], rtol=0, atol=1e-14)
+
+
+@pytest.mark.parametrize("name", ["norm_eps_placement", "zero_row"])
+def test_normalise_hand(name):
+    c = GOLD[name]
+    np.testing.assert_allclose(O.l2_normalise(np.array(c["x"]), c["norm_eps"]), c["x_hat"],
+                               rtol=0, atol=1e-15)
+
+
+@pytest.mark.parametrize("name", ["loss_at_threshold", "loss_log3", "loss_half_means"])
+def test_loss_hand(name):
+    c = GOLD[name]
+    loss, dg = O.ff_loss(np.array(c["g"]), c["n_pos"], c["theta"])
+    assert abs(loss - c["loss"]) < 1e-14
+    np.testing.assert_allclose(dg, c["dLdg"], rtol=0, atol=1e-14)
+
+
+def test_adam_hand():
+    c = GOLD["adam_two_steps"]
+    p, m, v = np.array([c["p0"]]), np.zeros(1), np.zeros(1)
+    for t, (gr, want) in enumerate(zip(c["grads"], c["p"]), start=1):
+        p, m, v = O.adam(p, m, v, np.array([gr]), t, c["lr"], c["beta1"], c["beta2"], c["eps"])
+        assert abs(p[0] - want) < 1e-16
+
+
+def test_embed_hand():
+    c = GOLD["embed"]
+    x = O.embed_labels(np.array(c["x_base"]), np.array(c["labels"]), c["n_classes"])
+    np.testing.assert_array_equal(x, c["x"])
+
+
+def test_grad_hand():
+    c = GOLD["grad_one_unit"]
+    W, b = _layer(c)
+    xh, _, h, g = O.layer_forward(W, b, np.array(c["x"]), c["norm_eps"])
+    np.testing.assert_allclose(g, c["g"], atol=1e-15)
+    loss, dg = O.ff_loss(g, c["n_pos"], c["theta"])
+    assert abs(loss - c["loss"]) < 1e-14
+    dW, db = O.layer_grads(xh, h, dg)
+    np.testing.assert_allclose(dW, c["dW"], atol=1e-15)
+    np.testing.assert_allclose(db, c["db"], atol=1e-15)
+
+
+# ---------------------------------------------------------------- closed forms
+def test_goodness_is_squared_norm_of_relu():
+    rng = np.random.default_rng(5)
+    z = rng.normal(size=(7, 11))
+    h = np.maximum(z, 0)
+    g = O.goodness(h)
+    for r in range(7):
+        assert abs(g[r] - sum(v * v for v in z[r] if v > 0)) < 1e-12
+
+
+def test_loss_derivative_is_logistic():
+    """d/dg softplus(theta-g) = -sigma(theta-g); d/dg softplus(g-theta) = sigma(g-theta)."""
+    theta = 2.0
+    g = np.array([-3.0, 0.1, 1.9, 2.0, 2.5, 40.0, 3.0, -1.0])
+    n_pos = 4
+    _, dg = O.ff_loss(g, n_pos, theta)
+    e = 1e-6
+    for r in range(len(g)):
+        gp, gm = g.copy(), g.copy()
+        gp[r] += e
+        gm[r] -= e
+        num = (O.ff_loss(gp, n_pos, theta)[0] - O.ff_loss(gm, n_pos, theta)[0]) / (2 * e)
+        assert abs(num - dg[r]) < 1e-8
+    # the logistic closed form, independently of the oracle's sigmoid
+    for r in range(len(g)):
+        sgn, n = (-1, n_pos) if r < n_pos else (1, len(g) - n_pos)
+        want = sgn / (1.0 + math.exp(-sgn * (g[r] - theta))) / n
+        assert abs(dg[r] - want) < 1e-15
+
+
+def test_softplus_sigmoid_extremes():
+    x = np.array([-800.0, -30.0, 0.0, 30.0, 800.0])
+    sp = O.softplus(x)
+    assert np.all(np.isfinite(sp))
+    assert sp[-1] == 800.0 and sp[0] == 0.0
+    assert abs(sp[2] - math.log(2)) < 1e-15
+    s = O.sigmoid(x)
+    assert s[0] == 0.0 and s[-1] == 1.0 and s[2] == 0.5
+
+
+def test_normalise_unit_and_scale_invariant():
+    x = random_matrix(3, 9, 37, 0, 1, p_zero=0.5).astype(float)
+    xh = O.l2_normalise(x, 1e-8)
+    np.testing.assert_allclose(np.linalg.norm(xh, axis=1), 1.0, atol=1e-7)
+    np.testing.assert_allclose(O.l2_normalise(7.5 * x, 1e-8), xh, atol=1e-8)
+
+
+def test_adam_first_step_closed_form():
+    rng = np.random.default_rng(9)
+    g = rng.normal(size=50) * 10.0 ** rng.integers(-6, 2, 50)
+    p0 = rng.normal(size=50)
+    p, _, _ = O.adam(p0, np.zeros(50), np.zeros(50), g, 1, 0.03, 0.9, 0.999, 1e-8)
+    np.testing.assert_allclose(p, p0 - 0.03 * g / (np.abs(g) + 1e-8), rtol=0, atol=1e-15)
+
+
+def test_bf16_round_matches_torch():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(2)
+    v = np.concatenate([rng.normal(size=4000) * 10.0 ** rng.integers(-8, 8, 4000),
+                        np.array([1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -(1.0 + 2 ** -8), 0.0])])
+    v32 = v.astype(np.float32)
+    want = torch.from_numpy(v32).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(O.bf16_round(v32), want)
+
+
+# ---------------------------------------------------------------- finite differences
+def _tiny_problem(seed, d_in=5, d_out=3, n_pos=2, n_neg=2):
+    rng = np.random.default_rng(seed)
+    for _ in range(100):
+        W = rng.normal(size=(d_out, d_in))
+        b = rng.normal(size=d_out) * 0.1
+        x = rng.uniform(0, 1, (n_pos + n_neg, d_in))
+        z = O.layer_forward(W, b, x, 1e-8)[1]
+        if np.min(np.abs(z)) > 1e-3:
+            return W, b, x
+    raise RuntimeError("no kink-free draw")
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_grads_finite_difference(seed):
+    W, b, x = _tiny_problem(seed)
+    n_pos, theta = 2, 0.7
+
+    def loss_of(Wp, bp):
+        return O.ff_loss(O.layer_forward(Wp, bp, x, 1e-8)[3], n_pos, theta)[0]
+
+    xh, _, h, g = O.layer_forward(W, b, x, 1e-8)
+    dW, db = O.layer_grads(xh, h, O.ff_loss(g, n_pos, theta)[1])
+    e = 1e-6
+    num = np.zeros_like(W)
+    for i in range(W.shape[0]):
+        for j in range(W.shape[1]):
+            Wp, Wm = W.copy(), W.copy()
+            Wp[i, j] += e
+            Wm[i, j] -= e
+            num[i, j] = (loss_of(Wp, b) - loss_of(Wm, b)) / (2 * e)
+    numb = np.zeros_like(b)
+    for i in range(b.shape[0]):
+        bp, bm = b.copy(), b.copy()
+        bp[i] += e
+        bm[i] -= e
+        numb[i] = (loss_of(W, bp) - loss_of(W, bm)) / (2 * e)
+    assert np.max(np.abs(num - dW)) <= 1e-6 * max(1.0, np.max(np.abs(dW)))
+    assert np.max(np.abs(numb - db)) <= 1e-6 * max(1.0, np.max(np.abs(db)))
+
+
+# ---------------------------------------------------------------- PyTorch fp64 cross-check
+def test_layer_steps_match_torch_autograd_adam():
+    torch = pytest.importorskip("torch")
+    x_base = random_matrix(11, 24, 40, 0, 1, p_zero=0.6)
+    y, y_neg = random_labels(12, 24)
+    (W0, b0), = make_weights(13, (40, 17))
+    b0 = b0 + np.linspace(-0.05, 0.05, 17).astype(np.float32)
+    hp = O.HParams(theta=2.0, lr=0.03)
+    x = np.concatenate([O.embed_labels(x_base, y, 10), O.embed_labels(x_base, y_neg, 10)])
+    n_pos = 24
+
+    Wt = torch.tensor(W0, dtype=torch.float64, requires_grad=True)
+    bt = torch.tensor(b0, dtype=torch.float64, requires_grad=True)
+    opt = torch.optim.Adam([Wt, bt], lr=hp.lr, betas=(hp.beta1, hp.beta2), eps=hp.adam_eps)
+    xt = torch.tensor(x, dtype=torch.float64)
+    L = O.Layer.from_params(W0, b0)
+    for step in range(4):
+        xh = xt / (xt.norm(dim=1, keepdim=True) + hp.norm_eps)
+        h = torch.relu(xh @ Wt.T + bt)
+        g = (h * h).sum(1)
+        loss = (torch.nn.functional.softplus(hp.theta - g[:n_pos]).mean()
+                + torch.nn.functional.softplus(g[n_pos:] - hp.theta).mean())
+        opt.zero_grad()
+        loss.backward()
+        r = O.layer_step(L, x, n_pos, hp)
+        assert abs(r.loss - loss.item()) < 1e-12
+        np.testing.assert_allclose(r.g, g.detach().numpy(), rtol=1e-12, atol=1e-14)
+        np.testing.assert_allclose(r.dW, Wt.grad.numpy(), rtol=1e-10, atol=1e-14)
+        np.testing.assert_allclose(r.db, bt.grad.numpy(), rtol=1e-10, atol=1e-14)
+        opt.step()
+        np.testing.assert_allclose(L.W, Wt.detach().numpy(), rtol=1e-11, atol=1e-13)
+        np.testing.assert_allclose(L.b, bt.detach().numpy(), rtol=1e-11, atol=1e-13)
+
+
+# ---------------------------------------------------------------- scoring
+def test_score_hand_designed_net():
+    """One layer whose unit k sees label feature k plus data feature k.
+
+    For label c and data d >= 0 (C features after the label area), with
+    s = 1/(||(e_c, d)|| + eps) the same for every c:
+    g(c) = s^2 sum_k (delta_kc + d_k)^2 = s^2 (||d_{:C}||^2 + 2 d_c + 1),
+    so the predicted label is argmax_c d_c.
+    """
+    C = 10
+    rng = np.random.default_rng(4)
+    data = rng.uniform(0, 1, (8, C))
+    x_base = np.concatenate([rng.uniform(0, 1, (8, C)), data], axis=1)
+    W = np.zeros((C, 2 * C))
+    W[np.arange(C), np.arange(C)] = 1.0
+    W[np.arange(C), C + np.arange(C)] = 1.0
+    L = O.Layer.from_params(W, np.zeros(C))
+    S, pred = O.score_labels([L], x_base, C, O.HParams())
+    np.testing.assert_array_equal(pred, np.argmax(data, axis=1))
+    s2 = 1.0 / (np.sqrt(1.0 + np.sum(data ** 2, 1)) + 1e-8) ** 2
+    want = s2[:, None] * (np.sum(data ** 2, 1)[:, None] + 2 * data + 1)
+    np.testing.assert_allclose(S, want, rtol=1e-12)
+
+
+def test_score_brute_force_and_first_layer_skip():
+    x_base, _, _ = make_data(3, 8, 30)
+    layers = [O.Layer.from_params(W, b) for W, b in make_weights(4, (30, 12, 9))]
+    hp = O.HParams()
+    S0, p0 = O.score_labels(layers, x_base, 10, hp, 0)
+    S1, p1 = O.score_labels(layers, x_base, 10, hp, 1)
+    for n in range(8):
+        tot0, tot1 = [], []
+        for c in range(10):
+            a = x_base[n].astype(float).copy()
+            a[:10] = 0
+            a[c] = 1
+            gs = []
+            for L in layers:
+                a = a / (math.sqrt(float(a @ a)) + 1e-8)
+                a = np.maximum(L.W @ a + L.b, 0)
+                gs.append(float(a @ a))
+            tot0.append(sum(gs))
+            tot1.append(sum(gs[1:]))
+        np.testing.assert_allclose(S0[n], tot0, rtol=1e-12)
+        np.testing.assert_allclose(S1[n], tot1, rtol=1e-12)
+        assert p0[n] == int(np.argmax(tot0)) and p1[n] == int(np.argmax(tot1))
+
+
+def test_score_ties_go_to_lowest_label():
+    C = 10
+    x_base = np.ones((3, 25))
+    W = np.zeros((4, 25))
+    W[:, C:] = 1.0  # ignores the label area entirely: all labels tie
+    L = O.Layer.from_params(W, np.zeros(4))
+    _, pred = O.score_labels([L], x_base, C, O.HParams())
+    np.testing.assert_array_equal(pred, 0)
+
+
+def test_score_hidden_permutation_invariance():
+    x_base, _, _ = make_data(6, 10, 30)
+    (W1, b1), (W2, b2) = make_weights(7, (30, 16, 8))
+    b1 = b1 + 0.01
+    perm = np.random.default_rng(8).permutation(16)
+    hp = O.HParams()
+    A = [O.Layer.from_params(W1, b1), O.Layer.from_params(W2, b2)]
+    B = [O.Layer.from_params(W1[perm], b1[perm]), O.Layer.from_params(W2[:, perm], b2)]
+    SA, pa = O.score_labels(A, x_base, 10, hp)
+    SB, pb = O.score_labels(B, x_base, 10, hp)
+    np.testing.assert_allclose(SA, SB, rtol=1e-12)
+    np.testing.assert_array_equal(pa, pb)
+
+
+# ---------------------------------------------------------------- schedules
+def _net(seed, dims):
+    return [O.Layer.from_params(W, b) for W, b in make_weights(seed, dims)]
+
+
+def test_pipelined_equals_sequential_for_one_layer():
+    x_base, y, y_neg = make_data(21, 50, 24)
+    hp = O.HParams(lr=0.03)
+    A, B = _net(22, (24, 9)), _net(22, (24, 9))
+    ta = O.train_sequential(A, x_base, y, y_neg, 10, 16, 2, hp)
+    tb = O.train_pipelined(B, x_base, y, y_neg, 10, 16, 2, hp)
+    np.testing.assert_array_equal(ta, tb)
+    np.testing.assert_array_equal(A[0].W, B[0].W)
+
+
+def test_pipelined_order_invariance():
+    x_base, y, y_neg = make_data(23, 45, 20)
+    hp = O.HParams(lr=0.05)
+    res = []
+    for order in ["chunk_major", "layer_major", "wavefront"]:
+        net = _net(24, (20, 12, 10, 8))
+        tr = O.train_pipelined(net, x_base, y, y_neg, 10, 8, 1, hp, order=order)
+        res.append((tr, [L.W for L in net]))
+    for tr, Ws in res[1:]:
+        np.testing.assert_array_equal(tr, res[0][0])
+        for a, b in zip(Ws, res[0][1]):
+            np.testing.assert_array_equal(a, b)
+
+
+def test_schedules_agree_when_weights_frozen():
+    """With lr=0 pre- and post-update activities coincide, so both schedules see the
+    same inputs; each chunk loss then equals the loss of a plain forward pass."""
+    x_base, y, y_neg = make_data(25, 30, 20)
+    hp = O.HParams(lr=0.0)
+    A, B = _net(26, (20, 12, 10)), _net(26, (20, 12, 10))
+    ta = O.train_sequential(A, x_base, y, y_neg, 10, 8, 1, hp)
+    tb = O.train_pipelined(B, x_base, y, y_neg, 10, 8, 1, hp)
+    np.testing.assert_allclose(ta, tb, rtol=1e-13)
+    for ci, (s, b) in enumerate(O.chunk_bounds(30, 8)):
+        xs = x_base[s:s + b]
+        a = np.concatenate([O.embed_labels(xs, y[s:s + b], 10), O.embed_labels(xs, y_neg[s:s + b], 10)])
+        for li, L in enumerate(A):
+            a = np.maximum(O.l2_normalise(a, 1e-8) @ L.W.T + L.b, 0)
+            g = np.sum(a * a, 1)
+            want = (np.mean(np.log1p(np.exp(2.0 - g[:b]))) + np.mean(np.log1p(np.exp(g[b:] - 2.0))))
+            assert abs(ta[li, ci] - want) < 1e-12
+
+
+def test_sequential_hands_over_final_weights():
+    """Layer 2 of the sequential schedule trains on layer 1's output under its *final* weights."""
+    x_base, y, y_neg = make_data(27, 12, 16)
+    hp = O.HParams(lr=0.05)
+    A = _net(28, (16, 10, 6))
+    O.train_sequential(A, x_base, y, y_neg, 10, 12, 3, hp)
+    B = _net(28, (16, 10, 6))
+    x = np.concatenate([O.embed_labels(x_base, y, 10), O.embed_labels(x_base, y_neg, 10)])
+    for _ in range(3):
+        O.layer_step(B[0], x, 12, hp)
+    h = np.maximum(O.l2_normalise(x, 1e-8) @ B[0].W.T + B[0].b, 0)  # final layer-1 weights
+    for _ in range(3):
+        O.layer_step(B[1], h, 12, hp)
+    np.testing.assert_array_equal(A[1].W, B[1].W)
+
+
+def test_pipelined_hands_over_pre_update_activities():
+    x_base, y, y_neg = make_data(29, 6, 16)
+    hp = O.HParams(lr=0.05)
+    A = _net(30, (16, 10, 6))
+    O.train_pipelined(A, x_base, y, y_neg, 10, 6, 1, hp)
+    B = _net(30, (16, 10, 6))
+    x = np.concatenate([O.embed_labels(x_base, y, 10), O.embed_labels(x_base, y_neg, 10)])
+    h = np.maximum(O.l2_normalise(x, 1e-8) @ B[0].W.T + B[0].b, 0)  # weights before the step
+    O.layer_step(B[0], x, 6, hp)
+    O.layer_step(B[1], h, 6, hp)
+    np.testing.assert_array_equal(A[1].W, B[1].W)
+
+
+def test_chunking_ragged_tail():
+    assert O.chunk_bounds(60000, 1024)[-1] == (59392, 608)
+    assert len(O.chunk_bounds(60000, 1024)) == 59
+    assert O.chunk_bounds(50000, 2048)[-1] == (49152, 848)
+    assert len(O.chunk_bounds(50000, 2048)) == 25
+
+
+# ---------------------------------------------------------------- bf16 emulation points
+def test_bf16_mode_rounds_operands_only():
+    x_base, y, y_neg = make_data(31, 6, 40)
+    (W, b), = make_weights(32, (40, 8))
+    x = O.embed_labels(x_base, y, 10)
+    xh, z, h, g = O.layer_forward(W, b, x, 1e-8, bf16=True)
+    xr = O.bf16_round(O.l2_normalise(x, 1e-8))
+    np.testing.assert_array_equal(xh, xr)
+    np.testing.assert_allclose(z, xr @ O.bf16_round(W).T + b, rtol=1e-14)
+    _, z32, _, _ = O.layer_forward(W, b, x, 1e-8)
+    assert np.max(np.abs(z - z32)) < 2 ** -7 * np.max(np.abs(z32)) * 4
