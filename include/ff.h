@@ -1,0 +1,173 @@
+/*
+ * ff.h -- C ABI of the MI355X (gfx950) Forward-Forward library, libff.so.
+ *
+ * The library computes the layer-local Forward-Forward (FF) training step and
+ * goodness label scoring of "Going Forward-Forward in Distributed Deep
+ * Learning" (Aktemur et al., arXiv 2404.08573), and the one-GPU emulation of
+ * its Single-Layer pipeline (one HIP stream per layer).
+ *
+ * Conventions shared by every entry point:
+ *  - Pointers marked (device) are HIP device pointers, (host) are host memory.
+ *    Matrices are row-major with no padding: a [rows][cols] float matrix has
+ *    its element (r, c) at offset r*cols + c.  Device buffers must be 16-byte
+ *    aligned (any hipMalloc/PyTorch allocation is).
+ *  - The caller allocates and owns every buffer, including the workspace
+ *    (`ws`, device, 256-byte aligned, size from the matching *_workspace_size
+ *    call) and the Adam state.  The library allocates no device memory.
+ *  - `stream` arguments are hipStream_t values passed as void* (NULL is the
+ *    default stream).  Calls enqueue asynchronously and return without
+ *    synchronising; device-side faults surface at the caller's next sync.
+ *  - Errors are returned as ff_status; argument errors are detected on the
+ *    host before anything is enqueued, so no state changes (in particular
+ *    ff_layer.step is not incremented).  ff_last_error() gives the reason.
+ *  - Feature counts (d_in, d_out, d) must be multiples of 4 (16-byte rows).
+ *  - Reentrant across distinct layers and streams; one ff_layer must not be
+ *    stepped on two streams at once.
+ */
+#ifndef FF_H
+#define FF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FF_OK = 0,
+  FF_ERR_INVALID_ARG = -1,   /* bad pointer, size or shape                    */
+  FF_ERR_UNSUPPORTED = -2,   /* valid request outside what the kernels handle */
+  FF_ERR_WORKSPACE = -3,     /* ws NULL or smaller than required              */
+  FF_ERR_HIP = -4            /* a HIP runtime call or kernel launch failed    */
+} ff_status;
+
+/* Operand type of the matrix products; accumulation is always fp32.  In
+ * FF_BF16 mode three values are rounded to bfloat16 (round to nearest even)
+ * before they enter a product: R1 the normalised layer input, R2 the weight
+ * shadow W_bf16, R3 the gradient rows dZ = 2 dL/dg * h.  Everything else
+ * (activities, goodness, loss, master weights, Adam moments) stays fp32. */
+typedef enum { FF_F32 = 0, FF_BF16 = 1 } ff_dtype;
+
+/* Training schedule of ff_pipeline_epoch. */
+typedef enum { FF_SEQUENTIAL = 0, FF_PIPELINED = 1 } ff_schedule;
+
+/* One dense ReLU FF layer, h = max(x_hat W^T + b, 0) (Sec. 3, Sec. 5.1).
+ * All buffers are caller-owned device memory. */
+typedef struct {
+  int32_t d_in, d_out;
+  float *W;          /* (device) [d_out][d_in] fp32 master weights           */
+  float *b;          /* (device) [d_out]                                      */
+  float *mW, *vW;    /* (device) [d_out][d_in] Adam moments, zero at start    */
+  float *mb, *vb;    /* (device) [d_out]       Adam moments, zero at start    */
+  uint16_t *W_bf16;  /* (device) [d_out][d_in] bf16 shadow of W; required when
+                        dtype == FF_BF16 (kept in sync by every update, see
+                        ff_refresh_bf16_shadow), ignored otherwise            */
+  int64_t step;      /* (host) Adam step count t; an update increments it
+                        before use, so the first update runs with t = 1       */
+} ff_layer;
+
+/* Hyper-parameters.  theta: goodness threshold of Eq. 1.  lr, beta1, beta2,
+ * adam_eps: Adam (Sec. 5.1) with bias correction, eps added to sqrt(v_hat),
+ * no weight decay.  norm_eps: each layer input row is scaled by
+ * 1/(||x||_2 + norm_eps).  dtype: an ff_dtype. */
+typedef struct {
+  float theta, lr, beta1, beta2, adam_eps, norm_eps;
+  int32_t dtype;
+} ff_hparams;
+
+/* Human-readable name of a status code (static string). */
+const char *ff_status_string(int32_t status);
+
+/* Reason for the last error returned on the calling thread (static buffer). */
+const char *ff_last_error(void);
+
+/* Label embedding (Sec. 3, "Negative Data"): out[r] = x_base[r] with features
+ * 0..n_classes-1 replaced by the one-hot code of labels[r].
+ *   x_base (device) [rows][d] fp32; labels (device) [rows] int32 in
+ *   [0, n_classes); out (device) [rows][d] fp32, may alias x_base.
+ *   Requires n_classes <= d.  rows == 0 is a no-op. */
+ff_status ff_embed_labels(const float *x_base, const int32_t *labels, int32_t rows, int32_t d,
+                          int32_t n_classes, float *out, void *stream);
+
+/* Workspace bytes for ff_layer_forward / ff_layer_step on up to `rows` rows. */
+size_t ff_step_workspace_size(int32_t rows, int32_t d_in, int32_t d_out, int32_t dtype);
+
+/* Forward pass of one layer without update (Sec. 3, Eq. 1):
+ *   x_hat = x / (||x|| + norm_eps) (skipped when x_normalised != 0),
+ *   h = max(x_hat W^T + b, 0), g_r = sum_j h_rj^2.
+ *   x (device) [rows][d_in]; h_out (device) [rows][d_out] or NULL;
+ *   goodness (device) [rows] or NULL.  rows == 0 is a no-op. */
+ff_status ff_layer_forward(const ff_layer *L, const ff_hparams *hp, const float *x, int32_t rows,
+                           int32_t x_normalised, float *h_out, float *goodness, void *ws,
+                           size_t ws_bytes, void *stream);
+
+/* One FF training step of one layer, trainLayer(idx, batch) of Alg. 1/2,
+ * on R = n_pos + n_neg concatenated rows (positives first, as the
+ * concatenated dataset x of Sec. 4):
+ *   forward as ff_layer_forward;
+ *   loss = mean_{pos} softplus(theta - g) + mean_{neg} softplus(g - theta)
+ *          (negative log-likelihood of Eq. 1, each half averaged over its rows);
+ *   dZ_rj = 2 dL/dg_r h_rj;  dW = dZ^T x_hat;  db = sum_r dZ_r
+ *          (local gradient only: FF needs no input gradient);
+ *   one Adam update of W and b with t = ++L->step.
+ *   x (device) [R][d_in]; h_out (device) [R][d_out] or NULL: the activities,
+ *   computed with the weights before the update; goodness (device) [R] or
+ *   NULL; loss (device) [1] or NULL.  Requires n_pos >= 1 and n_neg >= 1. */
+ff_status ff_layer_step(ff_layer *L, const ff_hparams *hp, const float *x, int32_t n_pos,
+                        int32_t n_neg, int32_t x_normalised, float *h_out, float *goodness,
+                        float *loss, void *ws, size_t ws_bytes, void *stream);
+
+/* Rewrite W_bf16 = bf16(W) (round to nearest even).  Call once after
+ * initialising W in FF_BF16 mode; updates keep the shadow in sync after that. */
+ff_status ff_refresh_bf16_shadow(const ff_layer *L, void *stream);
+
+/* Workspace bytes for ff_score_labels. */
+size_t ff_score_workspace_size(const ff_layer *layers, int32_t n_layers, int32_t n,
+                               int32_t n_classes, int32_t dtype);
+
+/* Goodness prediction (Sec. 3 "Prediction"): every input n is run under each
+ * label c, embedded as in ff_embed_labels, through all layers;
+ *   S[n][c] = sum_{l >= first_scored_layer} g_l(n, c),  pred[n] = argmax_c S[n][c]
+ * with the lowest c winning exact ties.  The paper sums "all but the first
+ * hidden layer" (first_scored_layer = 1); 0 sums every layer.
+ *   layers (host) [n_layers], chained (d_in of l+1 == d_out of l);
+ *   x_base (device) [n][layers[0].d_in]; scores (device) [n][n_classes] or
+ *   NULL; pred (device) [n] int32.  n == 0 is a no-op. */
+ff_status ff_score_labels(const ff_layer *layers, int32_t n_layers, int32_t first_scored_layer,
+                          const ff_hparams *hp, const float *x_base, int32_t n, int32_t n_classes,
+                          float *scores, int32_t *pred, void *ws, size_t ws_bytes, void *stream);
+
+/* Workspace bytes for ff_pipeline_epoch. */
+size_t ff_pipeline_workspace_size(const ff_layer *layers, int32_t n_layers, int32_t n,
+                                  int32_t chunk_pairs, int32_t schedule, int32_t dtype);
+
+/* Layer-local FF training of a layer stack over the chunks
+ * [c*chunk_pairs, min((c+1)*chunk_pairs, n)) of x_base, in order, `epochs`
+ * times.  Chunk c's rows are its positives (labels y_pos) then its negatives
+ * (labels y_neg), embedded as in ff_embed_labels.
+ *   FF_SEQUENTIAL (Sec. 3 sequential training): layer l takes all its steps,
+ *     then one forward pass with its final weights gives layer l+1's input
+ *     (the "x <- layer(x)" step of Alg. 2).  Everything runs on streams[0].
+ *   FF_PIPELINED (Single-Layer PFF, Sec. 4.1 / Alg. 1, at the per-batch
+ *     exchange granularity proposed in Sec. 6): layer l runs on streams[l];
+ *     its step on chunk c starts once layer l-1 has emitted the activities of
+ *     chunk c (computed with its weights before that step's update) and
+ *     layer l has finished chunk c-1.  The result depends only on these
+ *     dependencies, not on how the streams interleave.
+ *   layers (host) [n_layers] chained; x_base (device) [n][layers[0].d_in];
+ *   y_pos, y_neg (device) [n] int32; streams (host) [n_layers] (only [0] is
+ *   read for FF_SEQUENTIAL); loss_trace (device) [n_layers][epochs*n_chunks]
+ *   or NULL.  The caller must not touch the layers or ws until all streams
+ *   have drained. */
+ff_status ff_pipeline_epoch(ff_layer *layers, int32_t n_layers, const ff_hparams *hp,
+                            const float *x_base, const int32_t *y_pos, const int32_t *y_neg,
+                            int32_t n, int32_t n_classes, int32_t chunk_pairs, int32_t epochs,
+                            int32_t schedule, void *const *streams, float *loss_trace, void *ws,
+                            size_t ws_bytes);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FF_H */

@@ -207,6 +207,8 @@ class StepResult:
     loss: float
     dW: np.ndarray       # gradient applied by the update
     db: np.ndarray
+    xh: np.ndarray       # [R, d_in] normalised input (bf16-rounded in bf16 mode)
+    dLdg: np.ndarray     # [R] derivative of the loss with respect to each goodness
 
 
 def layer_step(L: Layer, x: np.ndarray, n_pos: int, hp: HParams,
@@ -223,7 +225,7 @@ def layer_step(L: Layer, x: np.ndarray, n_pos: int, hp: HParams,
     L.t += 1
     L.W, L.mW, L.vW = adam(L.W, L.mW, L.vW, dW, L.t, hp.lr, hp.beta1, hp.beta2, hp.adam_eps)
     L.b, L.mb, L.vb = adam(L.b, L.mb, L.vb, db, L.t, hp.lr, hp.beta1, hp.beta2, hp.adam_eps)
-    return StepResult(h, g, loss, dW, db)
+    return StepResult(h, g, loss, dW, db, xh, dg)
 
 
 # ----------------------------------------------------------------------------

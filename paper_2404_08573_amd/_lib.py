@@ -1,0 +1,276 @@
+"""ctypes binding of libff.so (include/ff.h).  Argument marshalling only.
+
+Every function here has the name of the C entry point it calls and does no
+arithmetic of the method: it checks tensor devices/dtypes/shapes, passes raw
+device pointers and the current HIP stream, and raises ``FFError`` on a
+non-OK status.  PyTorch provides device memory and streams.  The library must
+have been built (``__graft_entry__.build()``); importing without it raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+from ctypes import POINTER, c_float, c_int32, c_int64, c_size_t, c_void_p
+from typing import List, Optional, Sequence
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libff.so")
+
+FF_OK, FF_ERR_INVALID_ARG, FF_ERR_UNSUPPORTED, FF_ERR_WORKSPACE, FF_ERR_HIP = 0, -1, -2, -3, -4
+FF_F32, FF_BF16 = 0, 1
+FF_SEQUENTIAL, FF_PIPELINED = 0, 1
+
+EXPORTS = ["ff_status_string", "ff_last_error", "ff_embed_labels", "ff_step_workspace_size",
+           "ff_layer_forward", "ff_layer_step", "ff_refresh_bf16_shadow",
+           "ff_score_workspace_size", "ff_score_labels", "ff_pipeline_workspace_size",
+           "ff_pipeline_epoch"]
+
+
+class FFError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{LIB.ff_status_string(status).decode()}: {msg}")
+        self.status = status
+
+
+class ff_layer(ctypes.Structure):
+    _fields_ = [("d_in", c_int32), ("d_out", c_int32), ("W", c_void_p), ("b", c_void_p),
+                ("mW", c_void_p), ("vW", c_void_p), ("mb", c_void_p), ("vb", c_void_p),
+                ("W_bf16", c_void_p), ("step", c_int64)]
+
+
+class ff_hparams(ctypes.Structure):
+    _fields_ = [("theta", c_float), ("lr", c_float), ("beta1", c_float), ("beta2", c_float),
+                ("adam_eps", c_float), ("norm_eps", c_float), ("dtype", c_int32)]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                          "(python -m paper_2404_08573_amd.build); there is no fallback path")
+    lib = ctypes.CDLL(LIB_PATH)
+    P = c_void_p
+    sig = {
+        "ff_status_string": (ctypes.c_char_p, [c_int32]),
+        "ff_last_error": (ctypes.c_char_p, []),
+        "ff_embed_labels": (c_int32, [P, P, c_int32, c_int32, c_int32, P, P]),
+        "ff_step_workspace_size": (c_size_t, [c_int32, c_int32, c_int32, c_int32]),
+        "ff_layer_forward": (c_int32, [POINTER(ff_layer), POINTER(ff_hparams), P, c_int32, c_int32,
+                                       P, P, P, c_size_t, P]),
+        "ff_layer_step": (c_int32, [POINTER(ff_layer), POINTER(ff_hparams), P, c_int32, c_int32,
+                                    c_int32, P, P, P, P, c_size_t, P]),
+        "ff_refresh_bf16_shadow": (c_int32, [POINTER(ff_layer), P]),
+        "ff_score_workspace_size": (c_size_t, [POINTER(ff_layer), c_int32, c_int32, c_int32,
+                                               c_int32]),
+        "ff_score_labels": (c_int32, [POINTER(ff_layer), c_int32, c_int32, POINTER(ff_hparams), P,
+                                      c_int32, c_int32, P, P, P, c_size_t, P]),
+        "ff_pipeline_workspace_size": (c_size_t, [POINTER(ff_layer), c_int32, c_int32, c_int32,
+                                                  c_int32, c_int32]),
+        "ff_pipeline_epoch": (c_int32, [POINTER(ff_layer), c_int32, POINTER(ff_hparams), P, P, P,
+                                        c_int32, c_int32, c_int32, c_int32, c_int32,
+                                        POINTER(c_void_p), P, P, c_size_t]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype, f.argtypes = res, args
+    return lib
+
+
+LIB = _load()
+
+
+def _check(status: int):
+    if status != FF_OK:
+        raise FFError(status, LIB.ff_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor], dtype=None, numel=None, name="tensor"):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name} has {t.numel()} elements, needs {numel}")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream if isinstance(s, torch.cuda.Stream) else int(s)
+
+
+@dataclasses.dataclass
+class HParams:
+    theta: float = 2.0
+    lr: float = 0.03
+    beta1: float = 0.9
+    beta2: float = 0.999
+    adam_eps: float = 1e-8
+    norm_eps: float = 1e-8
+    dtype: int = FF_F32
+
+    def c(self) -> ff_hparams:
+        return ff_hparams(self.theta, self.lr, self.beta1, self.beta2, self.adam_eps,
+                          self.norm_eps, self.dtype)
+
+
+class Layer:
+    """Device buffers of one FF layer (fp32 master W, b, Adam moments, optional bf16 shadow)."""
+
+    def __init__(self, W: torch.Tensor, b: torch.Tensor, bf16_shadow: bool = False):
+        dev = W.device
+        self.W = W.detach().to(dev, torch.float32).contiguous().clone()
+        self.b = b.detach().to(dev, torch.float32).contiguous().clone()
+        self.mW = torch.zeros_like(self.W)
+        self.vW = torch.zeros_like(self.W)
+        self.mb = torch.zeros_like(self.b)
+        self.vb = torch.zeros_like(self.b)
+        self.W_bf16 = torch.empty(self.W.shape, dtype=torch.int16, device=dev) if bf16_shadow else None
+        self.step = 0
+        self.d_out, self.d_in = self.W.shape
+        if bf16_shadow:
+            ff_refresh_bf16_shadow(self)
+
+    def c(self) -> ff_layer:
+        return ff_layer(self.d_in, self.d_out, self.W.data_ptr(), self.b.data_ptr(),
+                        self.mW.data_ptr(), self.vW.data_ptr(), self.mb.data_ptr(),
+                        self.vb.data_ptr(),
+                        self.W_bf16.data_ptr() if self.W_bf16 is not None else None, self.step)
+
+
+def _layers_c(layers: Sequence[Layer]):
+    arr = (ff_layer * len(layers))(*[L.c() for L in layers])
+    return arr
+
+
+def workspace(nbytes: int, device="cuda") -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+# ----------------------------------------------------------------------------- entry points
+def ff_embed_labels(x_base: torch.Tensor, labels: torch.Tensor, n_classes: int,
+                    out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    rows, d = x_base.shape
+    out = torch.empty_like(x_base) if out is None else out
+    _check(LIB.ff_embed_labels(_ptr(x_base, torch.float32, name="x_base"),
+                                _ptr(labels, torch.int32, rows, "labels"), rows, d, n_classes,
+                                _ptr(out, torch.float32, rows * d, "out"), _stream(stream)))
+    return out
+
+
+def ff_step_workspace_size(rows: int, d_in: int, d_out: int, dtype: int = FF_F32) -> int:
+    return LIB.ff_step_workspace_size(rows, d_in, d_out, dtype)
+
+
+def ff_layer_forward(layer: Layer, hp: HParams, x: torch.Tensor, x_normalised: bool = False,
+                     h_out: Optional[torch.Tensor] = None, goodness: Optional[torch.Tensor] = None,
+                     ws: Optional[torch.Tensor] = None, stream=None):
+    rows = x.shape[0]
+    if ws is None:
+        ws = workspace(ff_step_workspace_size(max(rows, 1), layer.d_in, layer.d_out, hp.dtype),
+                       x.device)
+    Lc = layer.c()
+    _check(LIB.ff_layer_forward(ctypes.byref(Lc), ctypes.byref(hp.c()),
+                                 _ptr(x, torch.float32, rows * layer.d_in, "x"), rows,
+                                 int(x_normalised), _ptr(h_out, torch.float32, rows * layer.d_out,
+                                                         "h_out"),
+                                 _ptr(goodness, torch.float32, rows, "goodness"),
+                                 _ptr(ws, torch.uint8), ws.numel(), _stream(stream)))
+    return h_out, goodness
+
+
+def ff_layer_step(layer: Layer, hp: HParams, x: torch.Tensor, n_pos: int, n_neg: int,
+                  x_normalised: bool = False, h_out: Optional[torch.Tensor] = None,
+                  goodness: Optional[torch.Tensor] = None, loss: Optional[torch.Tensor] = None,
+                  ws: Optional[torch.Tensor] = None, stream=None):
+    R = n_pos + n_neg
+    if ws is None:
+        ws = workspace(ff_step_workspace_size(max(R, 1), layer.d_in, layer.d_out, hp.dtype),
+                       x.device)
+    Lc = layer.c()
+    st = LIB.ff_layer_step(ctypes.byref(Lc), ctypes.byref(hp.c()),
+                            _ptr(x, torch.float32, R * layer.d_in, "x"), n_pos, n_neg,
+                            int(x_normalised), _ptr(h_out, torch.float32, R * layer.d_out, "h_out"),
+                            _ptr(goodness, torch.float32, R, "goodness"),
+                            _ptr(loss, torch.float32, 1, "loss"), _ptr(ws, torch.uint8),
+                            ws.numel(), _stream(stream))
+    layer.step = Lc.step
+    _check(st)
+    return h_out, goodness, loss
+
+
+def ff_refresh_bf16_shadow(layer: Layer, stream=None):
+    Lc = layer.c()
+    _check(LIB.ff_refresh_bf16_shadow(ctypes.byref(Lc), _stream(stream)))
+
+
+def ff_score_workspace_size(layers: Sequence[Layer], n: int, n_classes: int,
+                            dtype: int = FF_F32) -> int:
+    return LIB.ff_score_workspace_size(_layers_c(layers), len(layers), n, n_classes, dtype)
+
+
+def ff_score_labels(layers: Sequence[Layer], hp: HParams, x_base: torch.Tensor, n_classes: int,
+                    first_scored_layer: int = 0, scores: Optional[torch.Tensor] = None,
+                    pred: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                    stream=None):
+    n = x_base.shape[0]
+    dev = x_base.device
+    pred = torch.empty(n, dtype=torch.int32, device=dev) if pred is None else pred
+    if ws is None:
+        ws = workspace(ff_score_workspace_size(layers, max(n, 1), n_classes, hp.dtype), dev)
+    arr = _layers_c(layers)
+    _check(LIB.ff_score_labels(arr, len(layers), first_scored_layer, ctypes.byref(hp.c()),
+                                _ptr(x_base, torch.float32, n * layers[0].d_in, "x_base"), n,
+                                n_classes, _ptr(scores, torch.float32, n * n_classes, "scores"),
+                                _ptr(pred, torch.int32, n, "pred"), _ptr(ws, torch.uint8),
+                                ws.numel(), _stream(stream)))
+    return scores, pred
+
+
+def ff_pipeline_workspace_size(layers: Sequence[Layer], n: int, chunk_pairs: int, schedule: int,
+                               dtype: int = FF_F32) -> int:
+    return LIB.ff_pipeline_workspace_size(_layers_c(layers), len(layers), n, chunk_pairs,
+                                           schedule, dtype)
+
+
+def ff_pipeline_epoch(layers: List[Layer], hp: HParams, x_base: torch.Tensor, y_pos: torch.Tensor,
+                      y_neg: torch.Tensor, n_classes: int, chunk_pairs: int, epochs: int = 1,
+                      schedule: int = FF_SEQUENTIAL, streams: Optional[Sequence] = None,
+                      loss_trace: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None):
+    """Enqueue the epoch(s).  With streams=None, per-layer streams are created and
+    joined back into the current stream before returning (still asynchronous to
+    the host)."""
+    n = x_base.shape[0]
+    dev = x_base.device
+    nc = (n + chunk_pairs - 1) // chunk_pairs
+    if ws is None:
+        ws = workspace(ff_pipeline_workspace_size(layers, n, chunk_pairs, schedule, hp.dtype), dev)
+    own = streams is None
+    cur = torch.cuda.current_stream(dev)
+    if own:
+        streams = [cur] + [torch.cuda.Stream(dev) for _ in range(len(layers) - 1)]
+        for s in streams[1:]:
+            s.wait_stream(cur)
+    sarr = (c_void_p * len(layers))(*[_stream(s) for s in streams])
+    arr = _layers_c(layers)
+    st = LIB.ff_pipeline_epoch(arr, len(layers), ctypes.byref(hp.c()),
+                                _ptr(x_base, torch.float32, n * layers[0].d_in, "x_base"),
+                                _ptr(y_pos, torch.int32, n, "y_pos"),
+                                _ptr(y_neg, torch.int32, n, "y_neg"), n, n_classes, chunk_pairs,
+                                epochs, schedule, sarr,
+                                _ptr(loss_trace, torch.float32, len(layers) * nc * epochs,
+                                     "loss_trace"), _ptr(ws, torch.uint8), ws.numel())
+    for L, Lc in zip(layers, arr):
+        L.step = Lc.step
+    if own:
+        for s in streams[1:]:
+            cur.wait_stream(s)
+        for s in streams[1:]:  # the side streams used ws: keep it until they finish
+            ws.record_stream(s)
+    _check(st)
+    return loss_trace

@@ -1,0 +1,534 @@
+// Host side of the C ABI declared in include/ff.h: argument validation,
+// workspace carving, launch sequencing, and the one-stream-per-layer pipeline
+// scheduler (Single-Layer PFF, Sec. 4.1 / Alg. 1, emulated on one GPU).
+#include <hip/hip_runtime_api.h>
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "../../include/ff.h"
+#include "ff_internal.h"
+
+namespace {
+
+thread_local char g_msg[512] = "";
+
+ff_status fail(ff_status st, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_msg, sizeof g_msg, fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+#define FF_HIP(expr)                                                                   \
+  do {                                                                                 \
+    hipError_t e_ = (expr);                                                            \
+    if (e_ != hipSuccess)                                                              \
+      return fail(FF_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));          \
+  } while (0)
+
+#define FF_TRY(expr)                 \
+  do {                               \
+    ff_status s_ = (expr);           \
+    if (s_ != FF_OK) return s_;      \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+
+// Carves aligned regions out of a workspace; with base == nullptr it only
+// measures, so size queries and real carving share one code path.
+struct Carver {
+  char *base;
+  size_t off = 0;
+  explicit Carver(void *b) : base(static_cast<char *>(b)) {}
+  void *take(size_t bytes) {
+    off = (off + kAlign - 1) / kAlign * kAlign;
+    void *p = base ? base + off : nullptr;
+    off += bytes;
+    return p;
+  }
+};
+
+inline size_t elem_bytes(int dtype) { return dtype == FF_BF16 ? 2 : 4; }
+
+// Scratch of one layer step.  Pointers the caller supplied are not carved.
+struct StepScratch {
+  void *xhat = nullptr;   // [rows][d_in], fp32 or bf16
+  float *h = nullptr;     // [rows][d_out]
+  float *gpart = nullptr; // [col tiles][rows]
+  float *g = nullptr;     // [rows]
+  float *c = nullptr;     // [rows]
+  float *loss = nullptr;  // [1]
+};
+
+void carve_step(Carver &cv, StepScratch &s, int rows, int d_in, int d_out, int dtype, bool need_h,
+                bool need_g, bool need_loss) {
+  s.xhat = cv.take((size_t)rows * d_in * elem_bytes(dtype));
+  if (need_h) s.h = static_cast<float *>(cv.take((size_t)rows * d_out * 4));
+  s.gpart = static_cast<float *>(cv.take((size_t)ffk::fwd_col_tiles(d_out, dtype) * rows * 4));
+  if (need_g) s.g = static_cast<float *>(cv.take((size_t)rows * 4));
+  s.c = static_cast<float *>(cv.take((size_t)rows * 4));
+  if (need_loss) s.loss = static_cast<float *>(cv.take(4));
+}
+
+size_t step_ws_bytes(int rows, int d_in, int d_out, int dtype, bool need_h) {
+  Carver cv(nullptr);
+  StepScratch s;
+  carve_step(cv, s, rows, d_in, d_out, dtype, need_h, true, true);
+  return cv.off + kAlign;
+}
+
+ff_status check_hp(const ff_hparams *hp) {
+  if (!hp) return fail(FF_ERR_INVALID_ARG, "hp is NULL");
+  if (hp->dtype != FF_F32 && hp->dtype != FF_BF16)
+    return fail(FF_ERR_INVALID_ARG, "dtype %d is not FF_F32 or FF_BF16", hp->dtype);
+  if (!(hp->norm_eps >= 0.f) || !(hp->adam_eps >= 0.f) || !(hp->lr >= 0.f) ||
+      !(hp->beta1 >= 0.f && hp->beta1 < 1.f) || !(hp->beta2 >= 0.f && hp->beta2 < 1.f) ||
+      !isfinite(hp->theta))
+    return fail(FF_ERR_INVALID_ARG, "hyper-parameter out of range");
+  return FF_OK;
+}
+
+ff_status check_layer(const ff_layer *L, const ff_hparams *hp, bool for_update, int idx) {
+  if (!L) return fail(FF_ERR_INVALID_ARG, "layer %d is NULL", idx);
+  if (L->d_in <= 0 || L->d_out <= 0)
+    return fail(FF_ERR_INVALID_ARG, "layer %d: d_in=%d d_out=%d must be positive", idx, L->d_in,
+                L->d_out);
+  if (L->d_in % 4 || L->d_out % 4)
+    return fail(FF_ERR_UNSUPPORTED, "layer %d: d_in=%d d_out=%d must be multiples of 4", idx,
+                L->d_in, L->d_out);
+  if (!L->W || !L->b) return fail(FF_ERR_INVALID_ARG, "layer %d: W or b is NULL", idx);
+  if (for_update && (!L->mW || !L->vW || !L->mb || !L->vb))
+    return fail(FF_ERR_INVALID_ARG, "layer %d: Adam moment buffer is NULL", idx);
+  if (hp && hp->dtype == FF_BF16 && !L->W_bf16)
+    return fail(FF_ERR_INVALID_ARG, "layer %d: FF_BF16 needs the W_bf16 shadow", idx);
+  return FF_OK;
+}
+
+ff_status check_stack(const ff_layer *layers, int n_layers, const ff_hparams *hp,
+                      bool for_update) {
+  if (!layers || n_layers <= 0) return fail(FF_ERR_INVALID_ARG, "no layers");
+  for (int l = 0; l < n_layers; ++l) {
+    FF_TRY(check_layer(&layers[l], hp, for_update, l));
+    if (l > 0 && layers[l].d_in != layers[l - 1].d_out)
+      return fail(FF_ERR_INVALID_ARG, "layer %d: d_in=%d does not match d_out=%d of layer %d", l,
+                  layers[l].d_in, layers[l - 1].d_out, l - 1);
+  }
+  return FF_OK;
+}
+
+inline const void *weight_operand(const ff_layer *L, int dtype) {
+  return dtype == FF_BF16 ? static_cast<const void *>(L->W_bf16) : static_cast<const void *>(L->W);
+}
+
+// Normalised operand rows for a layer: fp32 rows may be used in place when
+// already normalised; otherwise (and always for bf16) the embed/normalise
+// kernel writes them into scratch.
+ff_status stage_input(const ffk::RowMap &src, int rows, int d_in, bool normalised, int dtype,
+                      float norm_eps, void *scratch, const void **operand, hipStream_t st) {
+  const bool bf16 = dtype == FF_BF16;
+  if (normalised && !bf16 && src.mode == ffk::ROWS) {
+    *operand = src.base;
+    return FF_OK;
+  }
+  FF_HIP(ffk::launch_embed_norm(src, rows, d_in, norm_eps, !normalised, bf16, scratch, st));
+  *operand = scratch;
+  return FF_OK;
+}
+
+// Forward of one layer on rows described by `src`.
+ff_status forward_core(const ff_layer *L, const ff_hparams *hp, const ffk::RowMap &src, int rows,
+                       bool normalised, float *h_out, float *goodness, StepScratch &s,
+                       hipStream_t st) {
+  const void *xop = nullptr;
+  FF_TRY(stage_input(src, rows, L->d_in, normalised, hp->dtype, hp->norm_eps, s.xhat, &xop, st));
+  FF_HIP(ffk::launch_fwd(hp->dtype, xop, weight_operand(L, hp->dtype), L->b, rows, L->d_out,
+                         L->d_in, h_out, s.gpart, st));
+  if (goodness)
+    FF_HIP(ffk::launch_goodness(s.gpart, ffk::fwd_col_tiles(L->d_out, hp->dtype), rows, goodness,
+                                nullptr, 0, st));
+  return FF_OK;
+}
+
+// One training step on rows described by `src` (n_pos positives first).
+ff_status step_core(ff_layer *L, const ff_hparams *hp, const ffk::RowMap &src, int n_pos,
+                    int n_neg, bool normalised, float *h_out, float *goodness, float *loss,
+                    StepScratch &s, hipStream_t st) {
+  const int R = n_pos + n_neg;
+  const void *xop = nullptr;
+  FF_TRY(stage_input(src, R, L->d_in, normalised, hp->dtype, hp->norm_eps, s.xhat, &xop, st));
+  float *H = h_out ? h_out : s.h;
+  float *g = goodness ? goodness : s.g;
+  float *lo = loss ? loss : s.loss;
+  const int nt = ffk::fwd_col_tiles(L->d_out, hp->dtype);
+  FF_HIP(ffk::launch_fwd(hp->dtype, xop, weight_operand(L, hp->dtype), L->b, R, L->d_out, L->d_in,
+                         H, s.gpart, st));
+  FF_HIP(ffk::launch_loss(s.gpart, nt, R, n_pos, hp->theta, g, s.c, lo, st));
+  const int64_t t = ++L->step;
+  ffk::AdamArgs a;
+  a.lr = hp->lr;
+  a.beta1 = hp->beta1;
+  a.beta2 = hp->beta2;
+  a.eps = hp->adam_eps;
+  a.bc1 = (float)(1.0 - pow((double)hp->beta1, (double)t));
+  a.bc2 = (float)(1.0 - pow((double)hp->beta2, (double)t));
+  FF_HIP(ffk::launch_dw_adam(hp->dtype, H, s.c, xop, L->d_out, L->d_in, R, L->W, L->mW, L->vW,
+                             hp->dtype == FF_BF16 ? L->W_bf16 : nullptr, L->b, L->mb, L->vb, a,
+                             st));
+  return FF_OK;
+}
+
+ff_status check_ws(void *ws, size_t ws_bytes, size_t need) {
+  if (!ws) return fail(FF_ERR_WORKSPACE, "workspace is NULL (needs %zu bytes)", need);
+  if ((reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
+    return fail(FF_ERR_WORKSPACE, "workspace must be %zu-byte aligned", kAlign);
+  if (ws_bytes < need)
+    return fail(FF_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+  return FF_OK;
+}
+
+ffk::RowMap rows_of(const float *x) {
+  ffk::RowMap m{};
+  m.base = x;
+  m.mode = ffk::ROWS;
+  return m;
+}
+
+constexpr int kScoreBlockImages = 2048;  // images per scoring pass (rows = images * classes)
+
+}  // namespace
+
+extern "C" {
+
+const char *ff_status_string(int32_t status) {
+  switch (status) {
+    case FF_OK: return "FF_OK";
+    case FF_ERR_INVALID_ARG: return "FF_ERR_INVALID_ARG";
+    case FF_ERR_UNSUPPORTED: return "FF_ERR_UNSUPPORTED";
+    case FF_ERR_WORKSPACE: return "FF_ERR_WORKSPACE";
+    case FF_ERR_HIP: return "FF_ERR_HIP";
+    default: return "FF_UNKNOWN_STATUS";
+  }
+}
+
+const char *ff_last_error(void) { return g_msg; }
+
+ff_status ff_embed_labels(const float *x_base, const int32_t *labels, int32_t rows, int32_t d,
+                          int32_t n_classes, float *out, void *stream) {
+  if (rows < 0 || d <= 0 || n_classes <= 0) return fail(FF_ERR_INVALID_ARG, "bad sizes");
+  if (d % 4) return fail(FF_ERR_UNSUPPORTED, "d=%d must be a multiple of 4", d);
+  if (n_classes > d) return fail(FF_ERR_INVALID_ARG, "n_classes=%d exceeds d=%d", n_classes, d);
+  if (rows == 0) return FF_OK;
+  if (!x_base || !labels || !out) return fail(FF_ERR_INVALID_ARG, "NULL pointer");
+  ffk::RowMap m{};
+  m.base = x_base;
+  m.lab_a = labels;
+  m.lab_b = labels;
+  m.mode = ffk::PAIRS;
+  m.n_pos = rows;
+  m.base_off = 0;
+  m.n_classes = n_classes;
+  FF_HIP(ffk::launch_embed_norm(m, rows, d, 0.f, false, false, out,
+                                static_cast<hipStream_t>(stream)));
+  return FF_OK;
+}
+
+size_t ff_step_workspace_size(int32_t rows, int32_t d_in, int32_t d_out, int32_t dtype) {
+  if (rows <= 0 || d_in <= 0 || d_out <= 0) return 0;
+  return step_ws_bytes(rows, d_in, d_out, dtype, true);
+}
+
+ff_status ff_layer_forward(const ff_layer *L, const ff_hparams *hp, const float *x, int32_t rows,
+                           int32_t x_normalised, float *h_out, float *goodness, void *ws,
+                           size_t ws_bytes, void *stream) {
+  FF_TRY(check_hp(hp));
+  FF_TRY(check_layer(L, hp, false, 0));
+  if (rows < 0) return fail(FF_ERR_INVALID_ARG, "rows=%d", rows);
+  if (rows == 0) return FF_OK;
+  if (!x) return fail(FF_ERR_INVALID_ARG, "x is NULL");
+  FF_TRY(check_ws(ws, ws_bytes, step_ws_bytes(rows, L->d_in, L->d_out, hp->dtype, true)));
+  Carver cv(ws);
+  StepScratch s;
+  carve_step(cv, s, rows, L->d_in, L->d_out, hp->dtype, true, true, true);
+  return forward_core(L, hp, rows_of(x), rows, x_normalised != 0, h_out, goodness, s,
+                      static_cast<hipStream_t>(stream));
+}
+
+ff_status ff_layer_step(ff_layer *L, const ff_hparams *hp, const float *x, int32_t n_pos,
+                        int32_t n_neg, int32_t x_normalised, float *h_out, float *goodness,
+                        float *loss, void *ws, size_t ws_bytes, void *stream) {
+  FF_TRY(check_hp(hp));
+  FF_TRY(check_layer(L, hp, true, 0));
+  if (n_pos < 1 || n_neg < 1)
+    return fail(FF_ERR_INVALID_ARG, "n_pos=%d n_neg=%d: both halves need at least one row",
+                n_pos, n_neg);
+  if (!x) return fail(FF_ERR_INVALID_ARG, "x is NULL");
+  const int R = n_pos + n_neg;
+  FF_TRY(check_ws(ws, ws_bytes, step_ws_bytes(R, L->d_in, L->d_out, hp->dtype, true)));
+  Carver cv(ws);
+  StepScratch s;
+  carve_step(cv, s, R, L->d_in, L->d_out, hp->dtype, true, true, true);
+  return step_core(L, hp, rows_of(x), n_pos, n_neg, x_normalised != 0, h_out, goodness, loss, s,
+                   static_cast<hipStream_t>(stream));
+}
+
+ff_status ff_refresh_bf16_shadow(const ff_layer *L, void *stream) {
+  FF_TRY(check_layer(L, nullptr, false, 0));
+  if (!L->W_bf16) return fail(FF_ERR_INVALID_ARG, "W_bf16 is NULL");
+  FF_HIP(ffk::launch_bf16_shadow(L->W, L->W_bf16, (size_t)L->d_out * L->d_in,
+                                 static_cast<hipStream_t>(stream)));
+  return FF_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Goodness prediction
+// ---------------------------------------------------------------------------
+namespace {
+struct ScoreScratch {
+  void *x = nullptr;        // [rows][max d_in] operand rows
+  float *h = nullptr;       // [rows][max d_out]
+  float *gpart = nullptr;   // [max col tiles][rows]
+  float *scores = nullptr;  // [n][C] when the caller passes none
+};
+
+void carve_score(Carver &cv, ScoreScratch &s, const ff_layer *layers, int n_layers, int n, int C,
+                 int dtype, bool need_scores) {
+  const int nb = std::min(n, kScoreBlockImages);
+  const size_t rows = (size_t)nb * C;
+  int max_in = 0, max_out = 0, max_nt = 0;
+  for (int l = 0; l < n_layers; ++l) {
+    max_in = std::max(max_in, layers[l].d_in);
+    max_out = std::max(max_out, layers[l].d_out);
+    max_nt = std::max(max_nt, ffk::fwd_col_tiles(layers[l].d_out, dtype));
+  }
+  s.x = cv.take(rows * max_in * elem_bytes(dtype));
+  s.h = static_cast<float *>(cv.take(rows * max_out * 4));
+  s.gpart = static_cast<float *>(cv.take((size_t)max_nt * rows * 4));
+  if (need_scores) s.scores = static_cast<float *>(cv.take((size_t)n * C * 4));
+}
+}  // namespace
+
+size_t ff_score_workspace_size(const ff_layer *layers, int32_t n_layers, int32_t n,
+                               int32_t n_classes, int32_t dtype) {
+  if (!layers || n_layers <= 0 || n <= 0 || n_classes <= 0) return 0;
+  Carver cv(nullptr);
+  ScoreScratch s;
+  carve_score(cv, s, layers, n_layers, n, n_classes, dtype, true);
+  return cv.off + kAlign;
+}
+
+ff_status ff_score_labels(const ff_layer *layers, int32_t n_layers, int32_t first_scored_layer,
+                          const ff_hparams *hp, const float *x_base, int32_t n, int32_t n_classes,
+                          float *scores, int32_t *pred, void *ws, size_t ws_bytes, void *stream) {
+  FF_TRY(check_hp(hp));
+  FF_TRY(check_stack(layers, n_layers, hp, false));
+  if (first_scored_layer < 0 || first_scored_layer >= n_layers)
+    return fail(FF_ERR_INVALID_ARG, "first_scored_layer=%d outside [0, %d)", first_scored_layer,
+                n_layers);
+  if (n < 0 || n_classes <= 0) return fail(FF_ERR_INVALID_ARG, "n=%d n_classes=%d", n, n_classes);
+  if (n_classes > layers[0].d_in)
+    return fail(FF_ERR_INVALID_ARG, "n_classes=%d exceeds d_in=%d", n_classes, layers[0].d_in);
+  if (n == 0) return FF_OK;
+  if (!x_base || !pred) return fail(FF_ERR_INVALID_ARG, "x_base or pred is NULL");
+  if ((int64_t)n * n_classes > INT32_MAX) return fail(FF_ERR_UNSUPPORTED, "n too large");
+  Carver size_cv(nullptr);
+  ScoreScratch tmp;
+  carve_score(size_cv, tmp, layers, n_layers, n, n_classes, hp->dtype, scores == nullptr);
+  FF_TRY(check_ws(ws, ws_bytes, size_cv.off + kAlign));
+  Carver cv(ws);
+  ScoreScratch s;
+  carve_score(cv, s, layers, n_layers, n, n_classes, hp->dtype, scores == nullptr);
+  float *S = scores ? scores : s.scores;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const bool bf16 = hp->dtype == FF_BF16;
+  for (int n0 = 0; n0 < n; n0 += kScoreBlockImages) {
+    const int nb = std::min(kScoreBlockImages, n - n0);
+    const int rows = nb * n_classes;
+    ffk::RowMap m{};
+    m.base = x_base;
+    m.mode = ffk::EXPAND;
+    m.base_off = n0;
+    m.n_classes = n_classes;
+    FF_HIP(ffk::launch_embed_norm(m, rows, layers[0].d_in, hp->norm_eps, true, bf16, s.x, st));
+    for (int l = 0; l < n_layers; ++l) {
+      const ff_layer *L = &layers[l];
+      const bool last = l + 1 == n_layers;
+      FF_HIP(ffk::launch_fwd(hp->dtype, s.x, weight_operand(L, hp->dtype), L->b, rows, L->d_out,
+                             L->d_in, last ? nullptr : s.h, s.gpart, st));
+      if (l >= first_scored_layer)
+        FF_HIP(ffk::launch_goodness(s.gpart, ffk::fwd_col_tiles(L->d_out, hp->dtype), rows,
+                                    nullptr, S + (size_t)n0 * n_classes,
+                                    l > first_scored_layer ? 1 : 0, st));
+      if (!last)
+        FF_HIP(ffk::launch_embed_norm(rows_of(s.h), rows, L->d_out, hp->norm_eps, true, bf16,
+                                      s.x, st));
+    }
+  }
+  FF_HIP(ffk::launch_argmax(S, n, n_classes, pred, st));
+  return FF_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Training over chunks: sequential or one stream per layer
+// ---------------------------------------------------------------------------
+namespace {
+struct PipeScratch {
+  std::vector<StepScratch> step;    // per layer (pipelined) or one shared (sequential)
+  std::vector<float *> slot[2];     // pipelined: [l] input slots of layer l (l >= 1)
+  float *act[2] = {nullptr, nullptr};  // sequential: whole-set activations, ping-pong
+};
+
+void carve_pipe(Carver &cv, PipeScratch &p, const ff_layer *layers, int L, int n, int chunk,
+                int sched, int dtype) {
+  const int rows = 2 * std::min(chunk, n);
+  if (sched == FF_PIPELINED) {
+    p.step.assign(L, StepScratch());
+    p.slot[0].assign(L, nullptr);
+    p.slot[1].assign(L, nullptr);
+    for (int l = 0; l < L; ++l)
+      carve_step(cv, p.step[l], rows, layers[l].d_in, layers[l].d_out, dtype, l + 1 == L, false,
+                 false);
+    for (int l = 1; l < L; ++l)
+      for (int k = 0; k < 2; ++k)
+        p.slot[k][l] = static_cast<float *>(cv.take((size_t)rows * layers[l].d_in * 4));
+  } else {
+    int max_in = 0, max_out = 0;
+    for (int l = 0; l < L; ++l) {
+      max_in = std::max(max_in, layers[l].d_in);
+      max_out = std::max(max_out, layers[l].d_out);
+    }
+    p.step.assign(1, StepScratch());
+    carve_step(cv, p.step[0], rows, max_in, max_out, dtype, true, false, false);
+    int max_hidden = 0;
+    for (int l = 0; l + 1 < L; ++l) max_hidden = std::max(max_hidden, layers[l].d_out);
+    if (L > 1)
+      for (int k = 0; k < 2; ++k)
+        p.act[k] = static_cast<float *>(cv.take((size_t)2 * n * max_hidden * 4));
+  }
+}
+
+struct EventRing {
+  std::vector<hipEvent_t> ev;
+  ~EventRing() {
+    for (hipEvent_t e : ev)
+      if (e) (void)hipEventDestroy(e);
+  }
+};
+}  // namespace
+
+size_t ff_pipeline_workspace_size(const ff_layer *layers, int32_t n_layers, int32_t n,
+                                  int32_t chunk_pairs, int32_t schedule, int32_t dtype) {
+  if (!layers || n_layers <= 0 || n <= 0 || chunk_pairs <= 0) return 0;
+  Carver cv(nullptr);
+  PipeScratch p;
+  carve_pipe(cv, p, layers, n_layers, n, chunk_pairs, schedule, dtype);
+  return cv.off + kAlign;
+}
+
+ff_status ff_pipeline_epoch(ff_layer *layers, int32_t n_layers, const ff_hparams *hp,
+                            const float *x_base, const int32_t *y_pos, const int32_t *y_neg,
+                            int32_t n, int32_t n_classes, int32_t chunk_pairs, int32_t epochs,
+                            int32_t schedule, void *const *streams, float *loss_trace, void *ws,
+                            size_t ws_bytes) {
+  FF_TRY(check_hp(hp));
+  FF_TRY(check_stack(layers, n_layers, hp, true));
+  if (schedule != FF_SEQUENTIAL && schedule != FF_PIPELINED)
+    return fail(FF_ERR_INVALID_ARG, "schedule=%d", schedule);
+  if (n <= 0 || chunk_pairs <= 0 || epochs <= 0 || n_classes <= 0)
+    return fail(FF_ERR_INVALID_ARG, "n=%d chunk_pairs=%d epochs=%d n_classes=%d", n, chunk_pairs,
+                epochs, n_classes);
+  if (n_classes > layers[0].d_in)
+    return fail(FF_ERR_INVALID_ARG, "n_classes=%d exceeds d_in=%d", n_classes, layers[0].d_in);
+  if ((int64_t)2 * n > INT32_MAX) return fail(FF_ERR_UNSUPPORTED, "n too large");
+  if (!x_base || !y_pos || !y_neg || !streams)
+    return fail(FF_ERR_INVALID_ARG, "NULL pointer argument");
+  Carver size_cv(nullptr);
+  PipeScratch tmp;
+  carve_pipe(size_cv, tmp, layers, n_layers, n, chunk_pairs, schedule, hp->dtype);
+  FF_TRY(check_ws(ws, ws_bytes, size_cv.off + kAlign));
+  Carver cv(ws);
+  PipeScratch p;
+  carve_pipe(cv, p, layers, n_layers, n, chunk_pairs, schedule, hp->dtype);
+
+  const int nc = (n + chunk_pairs - 1) / chunk_pairs;
+  const int steps = nc * epochs;
+  auto chunk_map = [&](int c, int &start, int &b) {
+    start = c * chunk_pairs;
+    b = std::min(chunk_pairs, n - start);
+  };
+  auto pairs_map = [&](int start, int b) {
+    ffk::RowMap m{};
+    m.base = x_base;
+    m.lab_a = y_pos;
+    m.lab_b = y_neg;
+    m.mode = ffk::PAIRS;
+    m.n_pos = b;
+    m.base_off = start;
+    m.n_classes = n_classes;
+    return m;
+  };
+
+  if (schedule == FF_SEQUENTIAL) {
+    hipStream_t st = static_cast<hipStream_t>(streams[0]);
+    for (int l = 0; l < n_layers; ++l) {
+      ff_layer *L = &layers[l];
+      const float *in = l == 0 ? nullptr : p.act[(l - 1) & 1];
+      for (int q = 0; q < steps; ++q) {
+        int start, b;
+        chunk_map(q % nc, start, b);
+        const ffk::RowMap src = l == 0 ? pairs_map(start, b)
+                                       : rows_of(in + (size_t)2 * start * L->d_in);
+        FF_TRY(step_core(L, hp, src, b, b, false, nullptr, nullptr,
+                         loss_trace ? loss_trace + (size_t)l * steps + q : nullptr, p.step[0],
+                         st));
+      }
+      if (l + 1 < n_layers) {
+        float *out = p.act[l & 1];
+        for (int c = 0; c < nc; ++c) {
+          int start, b;
+          chunk_map(c, start, b);
+          const ffk::RowMap src = l == 0 ? pairs_map(start, b)
+                                         : rows_of(in + (size_t)2 * start * L->d_in);
+          FF_TRY(forward_core(L, hp, src, 2 * b, false, out + (size_t)2 * start * L->d_out,
+                              nullptr, p.step[0], st));
+        }
+      }
+    }
+    return FF_OK;
+  }
+
+  // Pipelined: done[l][q % kRing] marks layer l's step q complete.  Layer l's
+  // step q waits for layer l-1's step q (its input slot is filled) and, before
+  // it overwrites layer l+1's slot q%2, for layer l+1's step q-2 (the slot's
+  // previous reader).  Both waits are enqueued before the event is recorded
+  // again kRing steps later, so a ring of 4 events per layer suffices.
+  constexpr int kRing = 4;
+  EventRing ring;
+  ring.ev.assign((size_t)n_layers * kRing, nullptr);
+  for (auto &e : ring.ev) FF_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  for (int q = 0; q < steps; ++q) {
+    int start, b;
+    chunk_map(q % nc, start, b);
+    for (int l = 0; l < n_layers; ++l) {
+      ff_layer *L = &layers[l];
+      hipStream_t st = static_cast<hipStream_t>(streams[l]);
+      if (l > 0) FF_HIP(hipStreamWaitEvent(st, ring.ev[(size_t)(l - 1) * kRing + q % kRing], 0));
+      if (l + 1 < n_layers && q >= 2)
+        FF_HIP(hipStreamWaitEvent(st, ring.ev[(size_t)(l + 1) * kRing + (q - 2) % kRing], 0));
+      const ffk::RowMap src = l == 0 ? pairs_map(start, b) : rows_of(p.slot[q & 1][l]);
+      float *h_out = l + 1 < n_layers ? p.slot[q & 1][l + 1] : nullptr;
+      FF_TRY(step_core(L, hp, src, b, b, false, h_out, nullptr,
+                       loss_trace ? loss_trace + (size_t)l * steps + q : nullptr, p.step[l], st));
+      FF_HIP(hipEventRecord(ring.ev[(size_t)l * kRing + q % kRing], st));
+    }
+  }
+  return FF_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,69 @@
+// Internal interface between the host API (ff_api.cpp) and the gfx950 kernels
+// (ff_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ffk {
+
+// Where row r of a layer-0 input comes from.
+//   ROWS:     row r of `base` (already embedded or a hidden activity).
+//   PAIRS:    rows [0, n_pos) are base rows base_off+r with label lab_a[base_off+r];
+//             rows [n_pos, ..) are base rows base_off+r-n_pos with label lab_b[...]
+//             (a chunk's positives, then its negatives).
+//   EXPAND:   row r is base row base_off + r / n_classes under label r % n_classes
+//             (every candidate label of every input, for scoring).
+enum RowMode : int32_t { ROWS = 0, PAIRS = 1, EXPAND = 2 };
+
+struct RowMap {
+  const float *base;
+  const int32_t *lab_a;
+  const int32_t *lab_b;
+  int32_t mode;
+  int32_t n_pos;
+  int32_t base_off;
+  int32_t n_classes;
+};
+
+struct AdamArgs {
+  float lr, beta1, beta2, eps;
+  float bc1, bc2;  // 1 - beta1^t, 1 - beta2^t
+};
+
+// Row-tile and column-tile sizes of the forward product, which fix the
+// number of goodness partials per row (one per column tile).
+int fwd_col_tiles(int n_cols, int dtype);
+
+// Embedding (optional) + L2 normalisation (optional) into fp32 or bf16 rows.
+hipError_t launch_embed_norm(const RowMap &m, int rows, int d, float eps, bool normalise,
+                             bool bf16_out, void *out, hipStream_t s);
+
+// H = relu(X W^T + b) (optional store) and per-column-tile goodness partials
+// gpart[tile][M].  X: [M][K], W: [N][K]; fp32 or bf16 operands (dtype).
+hipError_t launch_fwd(int dtype, const void *X, const void *W, const float *bias, int M, int N,
+                      int K, float *H, float *gpart, hipStream_t s);
+
+// g_r = sum_t gpart[t][r]; loss and c_r = 2 dL/dg_r (single workgroup).
+hipError_t launch_loss(const float *gpart, int ntiles, int R, int n_pos, float theta, float *g,
+                       float *c, float *loss, hipStream_t s);
+
+// dW = (c . H)^T Xh contracted over the R rows, db = sum_r c_r H_r, then one
+// Adam update of W (and its bf16 shadow when Wb != nullptr) and of b.
+hipError_t launch_dw_adam(int dtype, const float *H, const float *c, const void *Xh, int M, int N,
+                          int K, float *W, float *mW, float *vW, uint16_t *Wb, float *b, float *mb,
+                          float *vb, const AdamArgs &a, hipStream_t s);
+
+// g_r = sum_t gpart[t][r] into g (any of the outputs may be null);
+// out[r] = g_r (accumulate == 0) or out[r] += g_r (accumulate == 1).
+hipError_t launch_goodness(const float *gpart, int ntiles, int R, float *g, float *out,
+                           int accumulate, hipStream_t s);
+
+// pred[n] = argmax_c scores[n][c], lowest c on ties.
+hipError_t launch_argmax(const float *scores, int n, int C, int32_t *pred, hipStream_t s);
+
+// Wb[i] = bf16(W[i]).
+hipError_t launch_bf16_shadow(const float *W, uint16_t *Wb, size_t count, hipStream_t s);
+
+}  // namespace ffk

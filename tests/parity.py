@@ -1,0 +1,88 @@
+"""Tolerances of the GPU-vs-oracle comparisons (shared by the GPU tests and the bench).
+
+fp32 path:
+  goodness, scores: |dg| <= 1e-4 |g_ref| + 1e-7 max|g_ref|
+  loss:             |dL| <= 1e-4 |L_ref|
+  activities h:     |dh| <= 1e-4 |h_ref| + 1e-5 max|h_ref| (fp32 contraction over
+                    d_in terms of unit-norm rows)
+  weights after k Adam steps: |dW| <= 1e-3 |W_ref| + 1e-6 outside the
+                    ill-conditioned set, i.e. elements whose oracle gradient had
+                    0 < |g| < 1e-5 sum|terms| at some step (Adam's first steps move
+                    by about lr*sign(g), so a gradient whose sum cancels down to
+                    rounding-noise level can flip its update in any fp32
+                    implementation); that set must be at most 1e-3 of the tensor.
+  labels:           bit-exact where the oracle's top-two gap is >= 1e-4 relative.
+bf16 path (compared with the bf16-emulating oracle): goodness, scores and loss
+  within 1e-2 relative, weights ||dW||_F <= 5e-2 ||W_ref||_F.
+"""
+import numpy as np
+
+
+def assert_goodness(g, ref, rel=1e-4, what="goodness"):
+    g = np.asarray(g, np.float64)
+    ref = np.asarray(ref, np.float64)
+    tol = rel * np.abs(ref) + 1e-7 * max(np.abs(ref).max(), 1e-30)
+    bad = np.abs(g - ref) > tol
+    assert not bad.any(), f"{what}: {bad.sum()} of {bad.size} off, worst rel " \
+                          f"{np.max(np.abs(g - ref) / (np.abs(ref) + 1e-30)):.3g}"
+
+
+def assert_loss(l, ref, rel=1e-4):
+    assert abs(float(l) - float(ref)) <= rel * abs(float(ref)), f"loss {l} vs {ref}"
+
+
+def assert_acts(h, ref, rel=1e-4):
+    h = np.asarray(h, np.float64)
+    tol = rel * np.abs(ref) + 1e-5 * max(np.abs(ref).max(), 1e-30)
+    bad = np.abs(h - ref) > tol
+    assert not bad.any(), f"activities: {bad.sum()} of {bad.size} off, max abs err " \
+                          f"{np.max(np.abs(h - ref)):.3g}"
+
+
+def grad_magnitudes(r):
+    """Sum of |terms| of every gradient element of an oracle step: (|dZ|^T |x_hat|, sum |dZ|)."""
+    dz = np.abs(2.0 * r.dLdg[:, None] * r.h)
+    return dz.T @ np.abs(r.xh), dz.sum(axis=0)
+
+
+def ill_conditioned(grads, mags):
+    """Elements whose gradient was ill-conditioned at some step.
+
+    A gradient element is a sum over the batch rows; rounding can change its
+    sign only when |sum| is tiny against sum(|terms|).  Flagged: 0 < |g| <
+    1e-5 sum(|terms|) (condition number above 1e5).  An exactly zero gradient
+    (a feature that is zero in every row) gives an exactly zero Adam update on
+    both sides and is not flagged."""
+    flag = np.zeros(np.shape(grads[0]), bool)
+    for gr, mg in zip(grads, mags):
+        a = np.abs(np.asarray(gr))
+        flag |= (a > 0) & (a < 1e-5 * np.asarray(mg))
+    return flag
+
+
+def assert_weights(W, ref, grads, mags, what="W", rel=1e-3):
+    W = np.asarray(W, np.float64)
+    flag = ill_conditioned(grads, mags)
+    assert flag.mean() <= 1e-3, f"{what}: ill-conditioned fraction {flag.mean():.2e} > 1e-3"
+    bad = (np.abs(W - ref) > rel * np.abs(ref) + 1e-6) & ~flag
+    assert not bad.any(), f"{what}: {bad.sum()} of {bad.size} off, worst abs " \
+                          f"{np.max(np.abs(W - ref)[~flag]):.3g}"
+
+
+def decided(S_ref, rel=1e-4):
+    """Rows whose oracle top-two score gap is at least `rel` relative."""
+    top2 = np.sort(S_ref, axis=1)[:, -2:]
+    return (top2[:, 1] - top2[:, 0]) >= rel * np.abs(top2[:, 1])
+
+
+def assert_labels(pred, S_ref, pred_ref):
+    ok = decided(S_ref)
+    pred = np.asarray(pred)
+    bad = (pred != pred_ref) & ok
+    assert not bad.any(), f"labels: {bad.sum()} decided rows differ"
+    return int(ok.sum())
+
+
+def assert_rel_fro(W, ref, rel):
+    d = np.linalg.norm(np.asarray(W, np.float64) - ref) / np.linalg.norm(ref)
+    assert d <= rel, f"relative Frobenius error {d:.3g} > {rel}"

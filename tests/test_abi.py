@@ -1,0 +1,155 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol that
+include/ff.h declares, and rejects bad arguments on the host before any launch."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ff.h")
+
+
+@pytest.fixture(scope="module")
+def P():
+    import paper_2404_08573_amd as P
+    P.LIB  # raises ImportError if libff.so is not built
+    return P
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ff_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_symbols()
+    for must in ["ff_layer_step", "ff_score_labels", "ff_pipeline_epoch", "ff_layer_forward",
+                 "ff_embed_labels", "ff_step_workspace_size", "ff_score_workspace_size",
+                 "ff_pipeline_workspace_size", "ff_status_string", "ff_last_error",
+                 "ff_refresh_bf16_shadow"]:
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol(P):
+    lib = ctypes.CDLL(P._lib.LIB_PATH)
+    for name in declared_symbols():
+        assert hasattr(lib, name), name
+    assert set(P._lib.EXPORTS) == set(declared_symbols())
+
+
+def test_status_strings(P):
+    L = P.LIB
+    assert L.ff_status_string(0) == b"FF_OK"
+    assert L.ff_status_string(-3) == b"FF_ERR_WORKSPACE"
+    assert L.ff_status_string(7) == b"FF_UNKNOWN_STATUS"
+
+
+def test_workspace_sizes(P):
+    a = P.ff_step_workspace_size(2048, 2000, 2000, P.FF_F32)
+    b = P.ff_step_workspace_size(1024, 2000, 2000, P.FF_F32)
+    c = P.ff_step_workspace_size(2048, 2000, 2000, P.FF_BF16)
+    assert a > b > 0 and a > c > 0
+    assert a >= 2048 * 2000 * 4 * 2  # normalised input + activities
+    assert P.ff_step_workspace_size(0, 10, 10, 0) == 0
+
+
+def _layer(P, d_in=16, d_out=8, bad=None):
+    fake = ctypes.c_void_p(256)  # never dereferenced: validation fails first
+    kw = dict(d_in=d_in, d_out=d_out, W=fake, b=fake, mW=fake, vW=fake, mb=fake, vb=fake,
+              W_bf16=None, step=0)
+    if bad:
+        kw.update(bad)
+    return P._lib.ff_layer(**kw)
+
+
+def _hp(P, **kw):
+    h = P.HParams(**kw)
+    return h.c()
+
+
+@pytest.mark.parametrize("case,status", [
+    ("n_pos0", -1), ("n_neg0", -1), ("x_null", -1), ("d_in_odd", -2), ("d_out0", -1),
+    ("no_moments", -1), ("bad_dtype", -1), ("bf16_no_shadow", -1), ("ws_null", -3),
+    ("ws_small", -3), ("beta_out_of_range", -1)])
+def test_layer_step_rejects_on_host(P, case, status):
+    L = _layer(P)
+    hp = _hp(P)
+    x = ctypes.c_void_p(4096)
+    n_pos, n_neg, ws, ws_bytes = 4, 4, ctypes.c_void_p(1 << 20), 1 << 30
+    if case == "n_pos0":
+        n_pos = 0
+    elif case == "n_neg0":
+        n_neg = 0
+    elif case == "x_null":
+        x = None
+    elif case == "d_in_odd":
+        L = _layer(P, d_in=15)
+    elif case == "d_out0":
+        L = _layer(P, d_out=0)
+    elif case == "no_moments":
+        L = _layer(P, bad=dict(mW=None))
+    elif case == "bad_dtype":
+        hp = _hp(P, dtype=5)
+    elif case == "bf16_no_shadow":
+        hp = _hp(P, dtype=P.FF_BF16)
+    elif case == "ws_null":
+        ws = None
+    elif case == "ws_small":
+        ws_bytes = 100
+    elif case == "beta_out_of_range":
+        hp = _hp(P, beta2=1.0)
+    st = P.LIB.ff_layer_step(ctypes.byref(L), ctypes.byref(hp), x, n_pos, n_neg, 0, None, None,
+                             None, ws, ws_bytes, None)
+    assert st == status, P.LIB.ff_last_error()
+    assert L.step == 0  # nothing enqueued, no state change
+    assert P.LIB.ff_last_error()
+
+
+def test_score_labels_rejects_on_host(P):
+    layers = (P._lib.ff_layer * 2)(_layer(P, 16, 8), _layer(P, 12, 8))  # does not chain
+    hp = _hp(P)
+    ws = ctypes.c_void_p(1 << 20)
+    st = P.LIB.ff_score_labels(layers, 2, 0, ctypes.byref(hp), ctypes.c_void_p(4096), 5, 10, None,
+                               ctypes.c_void_p(8192), ws, 1 << 30, None)
+    assert st == -1 and b"does not match" in P.LIB.ff_last_error()
+    layers = (P._lib.ff_layer * 2)(_layer(P, 16, 8), _layer(P, 8, 8))
+    st = P.LIB.ff_score_labels(layers, 2, 2, ctypes.byref(hp), ctypes.c_void_p(4096), 5, 10, None,
+                               ctypes.c_void_p(8192), ws, 1 << 30, None)
+    assert st == -1 and b"first_scored_layer" in P.LIB.ff_last_error()
+    st = P.LIB.ff_score_labels(layers, 2, 0, ctypes.byref(hp), ctypes.c_void_p(4096), 5, 17, None,
+                               ctypes.c_void_p(8192), ws, 1 << 30, None)
+    assert st == -1 and b"n_classes" in P.LIB.ff_last_error()
+    # n == 0 is a no-op that succeeds without touching the device
+    st = P.LIB.ff_score_labels(layers, 2, 0, ctypes.byref(hp), None, 0, 10, None, None, None, 0,
+                               None)
+    assert st == 0
+
+
+def test_pipeline_rejects_on_host(P):
+    layers = (P._lib.ff_layer * 2)(_layer(P, 16, 8), _layer(P, 8, 8))
+    hp = _hp(P)
+    streams = (ctypes.c_void_p * 2)(None, None)
+    args = [layers, 2, ctypes.byref(hp), ctypes.c_void_p(4096), ctypes.c_void_p(4096),
+            ctypes.c_void_p(4096), 100, 10, 32, 1, 1, streams, None, ctypes.c_void_p(1 << 20),
+            1 << 30]
+    bad_sched = list(args)
+    bad_sched[10] = 3
+    assert P.LIB.ff_pipeline_epoch(*bad_sched) == -1
+    zero_chunk = list(args)
+    zero_chunk[8] = 0
+    assert P.LIB.ff_pipeline_epoch(*zero_chunk) == -1
+    small_ws = list(args)
+    small_ws[14] = 10
+    assert P.LIB.ff_pipeline_epoch(*small_ws) == -3
+    assert layers[0].step == 0 and layers[1].step == 0
+
+
+def test_embed_rejects_on_host(P):
+    L = P.LIB
+    assert L.ff_embed_labels(ctypes.c_void_p(64), ctypes.c_void_p(64), 3, 8, 10,
+                             ctypes.c_void_p(64), None) == -1  # n_classes > d
+    assert L.ff_embed_labels(ctypes.c_void_p(64), ctypes.c_void_p(64), 3, 10, 4,
+                             ctypes.c_void_p(64), None) == -2  # d not a multiple of 4
+    assert L.ff_embed_labels(None, None, 0, 12, 10, None, None) == 0  # empty

@@ -1,0 +1,271 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle, same seeded inputs."""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import oracle as O  # noqa: E402
+from ffinputs import WORKLOADS, make_data, make_weights, random_labels, random_matrix  # noqa: E402
+from parity import (assert_acts, assert_goodness, assert_labels, assert_loss,  # noqa: E402
+                    assert_weights, grad_magnitudes)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def P():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2404_08573_amd as P
+    return P
+
+
+DEV = "cuda:0"
+
+
+def _t(a, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    if dtype is not None:
+        t = t.to(dtype)
+    return t.to(DEV)
+
+
+def _np(t):
+    torch.cuda.synchronize()
+    return t.detach().cpu().numpy()
+
+
+def _pair_rows(x_base, y, y_neg, C=10):
+    return np.concatenate([O.embed_labels(x_base, y, C), O.embed_labels(x_base, y_neg, C)])
+
+
+# ------------------------------------------------------------------ label embedding
+@pytest.mark.parametrize("rows,d,C", [(1, 12, 10), (77, 784, 10), (33, 16, 16)])
+def test_embed_labels_exact(P, rows, d, C):
+    x = random_matrix(rows + d, rows, d, 0, 1, 0.5)
+    lab = np.random.default_rng(rows).integers(0, C, rows).astype(np.int32)
+    out = P.ff_embed_labels(_t(x), _t(lab), C)
+    np.testing.assert_array_equal(_np(out), O.embed_labels(x, lab, C).astype(np.float32))
+
+
+# ------------------------------------------------------------------ forward
+FWD_SHAPES = [(1, 12, 8), (130, 44, 132), (300, 200, 260), (1024, 784, 500), (257, 784, 2000),
+              (129, 2000, 136)]
+
+
+@pytest.mark.parametrize("rows,d_in,d_out", FWD_SHAPES)
+def test_forward_parity(P, rows, d_in, d_out):
+    x = random_matrix(rows * 7 + d_in, rows, d_in, 0, 1, 0.6)
+    (W, b), = make_weights(d_out + 3, (d_in, d_out))
+    b = b + np.linspace(-0.02, 0.03, d_out).astype(np.float32)
+    L = P.Layer(_t(W), _t(b))
+    h = torch.empty(rows, d_out, device=DEV)
+    g = torch.empty(rows, device=DEV)
+    P.ff_layer_forward(L, P.HParams(), _t(x), h_out=h, goodness=g)
+    _, _, h_ref, g_ref = O.layer_forward(W, b, x, 1e-8)
+    assert_acts(_np(h), h_ref)
+    assert_goodness(_np(g), g_ref)
+
+
+def test_forward_prenormalised_input(P):
+    x = random_matrix(5, 200, 64, -1, 1)
+    xh = O.l2_normalise(x, 1e-8).astype(np.float32)
+    (W, b), = make_weights(6, (64, 40))
+    L = P.Layer(_t(W), _t(b))
+    g = torch.empty(200, device=DEV)
+    P.ff_layer_forward(L, P.HParams(), _t(xh), x_normalised=True, goodness=g)
+    assert_goodness(_np(g), O.layer_forward(W, b, xh, 0.0, normalised=True)[3])
+
+
+def test_forward_zero_rows_and_empty(P):
+    x = np.zeros((70, 32), np.float32)
+    x[::3] = random_matrix(1, 24, 32, 0, 1)[: len(x[::3])]
+    (W, b), = make_weights(2, (32, 24))
+    b = b + 0.1
+    L = P.Layer(_t(W), _t(b))
+    g = torch.empty(70, device=DEV)
+    P.ff_layer_forward(L, P.HParams(), _t(x), goodness=g)
+    assert_goodness(_np(g), O.layer_forward(W, b, x, 1e-8)[3])
+    P.ff_layer_forward(L, P.HParams(), _t(np.zeros((0, 32), np.float32)))  # no-op
+
+
+# ------------------------------------------------------------------ training step
+def _run_steps(P, x, n_pos, W, b, k, hp_kw, check_each=True):
+    hp, ohp = P.HParams(**hp_kw), O.HParams(**hp_kw)
+    L = P.Layer(_t(W), _t(b))
+    ref = O.Layer.from_params(W, b)
+    R, d_out = x.shape[0], W.shape[0]
+    xd = _t(x.astype(np.float32))
+    h = torch.empty(R, d_out, device=DEV)
+    g = torch.empty(R, device=DEV)
+    loss = torch.empty(1, device=DEV)
+    gW, gb, mW, mb = [], [], [], []
+    for _ in range(k):
+        P.ff_layer_step(L, hp, xd, n_pos, R - n_pos, h_out=h, goodness=g, loss=loss)
+        r = O.layer_step(ref, x, n_pos, ohp)
+        gW.append(r.dW)
+        gb.append(r.db)
+        a, c = grad_magnitudes(r)
+        mW.append(a)
+        mb.append(c)
+        if check_each:
+            assert_goodness(_np(g), r.g)
+            assert_loss(_np(loss)[0], r.loss)
+            assert_acts(_np(h), r.h)
+    assert L.step == k
+    assert_weights(_np(L.W), ref.W, gW, mW, "W")
+    assert_weights(_np(L.b), ref.b, gb, mb, "b")
+    assert_weights(_np(L.mW), ref.mW, gW, mW, "mW")
+    assert_weights(_np(L.vW), ref.vW, gW, mW, "vW", rel=2e-3)
+    return L, ref
+
+
+@pytest.mark.parametrize("n,d_in,d_out", [(16, 12, 8), (150, 200, 260), (512, 784, 500)])
+def test_step_parity(P, n, d_in, d_out):
+    x_base, y, y_neg = make_data(n + d_in, n, d_in)
+    (W, b), = make_weights(d_out, (d_in, d_out))
+    _run_steps(P, _pair_rows(x_base, y, y_neg), n, W, b, 1, dict(theta=2.0, lr=0.03))
+
+
+def test_step_parity_five_steps_tiny_config_layer1(P):
+    w = WORKLOADS["mnist_tiny_784_500x2"]
+    x_base, y, y_neg = make_data(w.seed_data, w.n, w.dims[0], w.p_zero)
+    (W, b), _ = make_weights(w.seed_w, w.dims)
+    _run_steps(P, _pair_rows(x_base, y, y_neg), w.n, W, b, 5, dict(theta=2.0, lr=0.03))
+
+
+def test_step_unequal_halves_and_hidden_input(P):
+    x = random_matrix(40, 253, 96, 0, 2, 0.3)  # unnormalised non-negative activities
+    (W, b), = make_weights(41, (96, 64))
+    _run_steps(P, x, 3, W, b, 3, dict(theta=0.5, lr=0.01))
+
+
+def test_step_full_size_2000x2000(P):
+    """One step at the 2000->2000 layer shape with 1024+1024 rows (the mnist chunk)."""
+    x = random_matrix(50, 2048, 2000, 0, 1, 0.5)
+    (W, b), = make_weights(51, (2000, 2000))
+    _run_steps(P, x, 1024, W, b, 1, dict(theta=2.0, lr=0.03))
+
+
+def test_step_workspace_too_small_changes_nothing(P):
+    (W, b), = make_weights(3, (16, 8))
+    L = P.Layer(_t(W), _t(b))
+    x = _t(random_matrix(4, 8, 16, 0, 1))
+    ws = torch.empty(64, dtype=torch.uint8, device=DEV)
+    with pytest.raises(P.FFError) as e:
+        P.ff_layer_step(L, P.HParams(), x, 4, 4, ws=ws)
+    assert e.value.status == P.FF_ERR_WORKSPACE
+    assert L.step == 0
+    np.testing.assert_array_equal(_np(L.W), W)
+
+
+# ------------------------------------------------------------------ label scoring
+@pytest.mark.parametrize("first", [0, 1])
+def test_score_parity_tiny_config(P, first):
+    w = WORKLOADS["mnist_tiny_784_500x2"]
+    x_base, _, _ = make_data(w.seed_data, w.n, w.dims[0], w.p_zero)
+    params = make_weights(w.seed_w, w.dims)
+    layers = [P.Layer(_t(W), _t(b)) for W, b in params]
+    S = torch.empty(w.n, 10, device=DEV)
+    _, pred = P.ff_score_labels(layers, P.HParams(), _t(x_base), 10, first, scores=S)
+    S_ref, p_ref = O.score_labels([O.Layer.from_params(W, b) for W, b in params], x_base, 10,
+                                  O.HParams(), first)
+    assert_goodness(_np(S), S_ref, what="scores")
+    assert_labels(_np(pred), S_ref, p_ref)
+
+
+def test_score_ragged_blocks_and_tiny(P):
+    """More images than one scoring pass holds (ragged last pass), odd label count."""
+    x_base, _, _ = make_data(60, 2100, 24, 0.5)
+    params = make_weights(61, (24, 36, 20))
+    layers = [P.Layer(_t(W), _t(b)) for W, b in params]
+    S = torch.empty(2100, 7, device=DEV)
+    _, pred = P.ff_score_labels(layers, P.HParams(), _t(x_base), 7, 0, scores=S)
+    S_ref, p_ref = O.score_labels([O.Layer.from_params(W, b) for W, b in params], x_base, 7,
+                                  O.HParams(), 0)
+    assert_goodness(_np(S), S_ref, what="scores")
+    assert_labels(_np(pred), S_ref, p_ref)
+    _, p1 = P.ff_score_labels(layers, P.HParams(), _t(x_base[:1]), 7, 1)
+    assert _np(p1)[0] == O.score_labels([O.Layer.from_params(W, b) for W, b in params],
+                                        x_base[:1], 7, O.HParams(), 1)[1][0]
+
+
+def test_score_full_size_sampled(P):
+    """All 10 000 inputs through 784->2000x4 on the GPU; the oracle checks a sample."""
+    w = WORKLOADS["mnist_score_784_2000x4"]
+    x_base, _, _ = make_data(w.seed_data, w.n, w.dims[0], w.p_zero)
+    params = make_weights(w.seed_w, w.dims)
+    layers = [P.Layer(_t(W), _t(b)) for W, b in params]
+    S = torch.empty(w.n, 10, device=DEV)
+    _, pred = P.ff_score_labels(layers, P.HParams(), _t(x_base), 10, 0, scores=S)
+    Sg, pg = _np(S), _np(pred)
+    # the device's own decision in its own precision: pred is the argmax of its scores
+    np.testing.assert_array_equal(pg, np.argmax(Sg, axis=1))
+    idx = np.random.default_rng(0).choice(w.n, 24, replace=False)
+    S_ref, p_ref = O.score_labels([O.Layer.from_params(W, b) for W, b in params], x_base[idx], 10,
+                                  O.HParams(), 0)
+    assert_goodness(Sg[idx], S_ref, what="scores")
+    assert_labels(pg[idx], S_ref, p_ref)
+
+
+# ------------------------------------------------------------------ schedules
+def _pipe(P, sched, n, dims, chunk, epochs, seed, hp_kw, streams=None):
+    x_base, y, y_neg = make_data(seed, n, dims[0])
+    params = make_weights(seed + 1, dims)
+    layers = [P.Layer(_t(W), _t(b)) for W, b in params]
+    nc = -(-n // chunk)
+    trace = torch.zeros(len(layers), nc * epochs, device=DEV)
+    P.ff_pipeline_epoch(layers, P.HParams(**hp_kw), _t(x_base), _t(y), _t(y_neg), 10, chunk,
+                        epochs, sched, streams=streams, loss_trace=trace)
+    torch.cuda.synchronize()
+    return layers, _np(trace), (x_base, y, y_neg, params)
+
+
+@pytest.mark.parametrize("sched", [0, 1])
+def test_pipeline_parity_small(P, sched):
+    hp_kw = dict(theta=2.0, lr=0.03)
+    dims = (64, 96, 80, 48)
+    layers, trace, (x_base, y, y_neg, params) = _pipe(P, sched, 300, dims, 64, 2, 70, hp_kw)
+    ref = [O.Layer.from_params(W, b) for W, b in params]
+    fn = O.train_sequential if sched == 0 else O.train_pipelined
+    tr_ref = fn(ref, x_base, y, y_neg, 10, 64, 2, O.HParams(**hp_kw))
+    np.testing.assert_allclose(trace, tr_ref, rtol=2e-4)
+    for L, R in zip(layers, ref):
+        assert L.step == tr_ref.shape[1]
+        np.testing.assert_allclose(_np(L.W), R.W, rtol=1e-3, atol=2e-4)
+
+
+def test_pipeline_schedule_invariance_bitwise(P):
+    """Same result with one stream per layer, run twice, and with every layer on one stream."""
+    hp_kw = dict(theta=2.0, lr=0.03)
+    dims = (784, 256, 256, 256)
+    a, ta, _ = _pipe(P, 1, 1500, dims, 256, 1, 80, hp_kw)
+    b, tb, _ = _pipe(P, 1, 1500, dims, 256, 1, 80, hp_kw)
+    s = torch.cuda.current_stream()
+    c, tc, _ = _pipe(P, 1, 1500, dims, 256, 1, 80, hp_kw, streams=[s] * len(dims[1:]))
+    np.testing.assert_array_equal(ta, tb)
+    np.testing.assert_array_equal(ta, tc)
+    for x, y, z in zip(a, b, c):
+        np.testing.assert_array_equal(_np(x.W), _np(y.W))
+        np.testing.assert_array_equal(_np(x.W), _np(z.W))
+
+
+def test_tiny_config_end_to_end(P):
+    """784->500->500, 512 pairs full batch, 5 steps per layer layer by layer, then scoring."""
+    w = WORKLOADS["mnist_tiny_784_500x2"]
+    x_base, y, y_neg = make_data(w.seed_data, w.n, w.dims[0], w.p_zero)
+    params = make_weights(w.seed_w, w.dims)
+    layers = [P.Layer(_t(W), _t(b)) for W, b in params]
+    hp_kw = dict(theta=w.theta, lr=w.lr)
+    trace = torch.zeros(2, 5, device=DEV)
+    P.ff_pipeline_epoch(layers, P.HParams(**hp_kw), _t(x_base), _t(y), _t(y_neg), 10, w.n,
+                        w.epochs, 0, loss_trace=trace)
+    S = torch.empty(w.n, 10, device=DEV)
+    _, pred = P.ff_score_labels(layers, P.HParams(**hp_kw), _t(x_base), 10, 0, scores=S)
+    ref = [O.Layer.from_params(W, b) for W, b in params]
+    tr_ref = O.train_sequential(ref, x_base, y, y_neg, 10, w.n, w.epochs, O.HParams(**hp_kw))
+    np.testing.assert_allclose(_np(trace), tr_ref, rtol=1e-4)
+    S_ref, p_ref = O.score_labels(ref, x_base, 10, O.HParams(**hp_kw))
+    assert_goodness(_np(S), S_ref, rel=1e-3, what="scores after training")
+    n_dec = assert_labels(_np(pred), S_ref, p_ref)
+    assert n_dec >= 0.9 * w.n
