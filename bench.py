@@ -1,0 +1,239 @@
+#!/usr/bin/env python
+"""Benchmark of the Forward-Forward hot path on one MI355X.
+
+One step = one pipelined training epoch of the 784->2000x4 FF net over the
+60 000-vector MNIST-shaped set in 1024+1024-row chunks (one HIP stream per
+layer; label embedding, normalisation, fused forward+goodness, loss, dW+Adam,
+activity handoff), followed by goodness label scoring of the 10 000-vector
+MNIST-shaped set under all 10 labels through a 784->2000x4 net.  Inputs are
+seeded synthetic data resident in HBM before the timed region.
+
+Prints one JSON line.  ``value`` is training pos+neg layer-step samples per
+second of whole step (training rows x layers / ms_per_step); the training and
+scoring parts are also reported on their own (HIP-event timed).  ``roofline``
+is the dominant kernel's algorithmic throughput from live per-launch HIP
+events; ``cpu_baseline`` is the CPU oracle timed on a bounded sample.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("FF train pos+neg samples/sec per layer-step and label-scored images/sec; "
+          "% MFMA peak")
+PEAK = {"f32": ("mfma", 157.3, "TFLOP/s"), "bf16": ("mfma", 2500.0, "TFLOP/s")}
+HBM_PEAK_GBS = 8000.0
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    with open(os.path.join(ROOT, "paper_2404_08573_amd", "csrc", "ff_kernels.hip"), "rb") as f:
+        h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel, workload):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if the kernel is unchanged."""
+    p = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        d = json.load(open(p))
+        e = d.get(workload, {}).get(kernel)
+        if not e or e.get("kernel_source_sha256_16") != kernel_source_hash():
+            return None
+        return e["bytes_per_launch"]
+    except Exception:
+        return None
+
+
+def cpu_baseline(w, x_base, y, y_neg, params, sw, sx, sparams, budget_s=12.0):
+    """The oracle as it stands, on a bounded sample of the same workload."""
+    import numpy as np
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count()
+    hp = O.HParams(theta=w.theta, lr=w.lr)
+    layers = [O.Layer.from_params(W, b) for W, b in params]
+    b = w.chunk_pairs
+    t0 = time.perf_counter()
+    steps = 0
+    rows = 0
+    # one chunk through every layer (each layer trains on the previous layer's
+    # activities, as in the pipeline), repeated while the time budget lasts
+    for c in range(len(w.chunks()) - 1):
+        s = c * b
+        x = O.chunk_input(x_base, y, y_neg, s, b, w.n_classes)
+        for L in layers:
+            r = O.layer_step(L, x, b, hp)
+            x = r.h
+            steps += 1
+            rows += 2 * b
+        if time.perf_counter() - t0 > budget_s * 0.6:
+            break
+    t_train = time.perf_counter() - t0
+    train_rate = rows / t_train  # layer-step samples per second
+    slayers = [O.Layer.from_params(W, b) for W, b in sparams]
+    n_img = 0
+    t1 = time.perf_counter()
+    while n_img < sw.n and time.perf_counter() - t1 < budget_s * 0.4:
+        O.score_labels(slayers, sx[n_img:n_img + 10], sw.n_classes, hp, 0)
+        n_img += 10
+    t_score = time.perf_counter() - t1
+    img_rate = n_img / t_score
+    # whole-step rate in the bench's unit: the same step on the CPU at these rates
+    step_rows = 2 * w.n * w.n_layers
+    step_time = step_rows / train_rate + sw.n / img_rate
+    return {"value": step_rows / step_time, "unit": "pos+neg samples/s per layer-step",
+            "cores": int(threads), "kind": "oracle",
+            "sample": f"{steps} layer-steps of {2 * b} rows (chunks 0..{steps // w.n_layers - 1} "
+                      f"through all {w.n_layers} layers, {t_train:.1f} s) and label scoring of "
+                      f"{n_img} inputs ({t_score:.1f} s); fp64 NumPy, extrapolated to the step",
+            "train_samples_per_s": train_rate, "images_per_s": img_rate}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="mnist_784_2000x4_pipelined")
+    ap.add_argument("--score-workload", default="mnist_score_784_2000x4")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this build has no multi-GPU path "
+              f"(--gpus {args.gpus} requested)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2404_08573_amd as P
+    from ffinputs import WORKLOADS, make_workload
+
+    w = WORKLOADS[args.workload]
+    sw = WORKLOADS[args.score_workload]
+    dtype = P.FF_BF16 if w.dtype == "bf16" else P.FF_F32
+    sched = P.FF_PIPELINED if w.schedule == "pipelined" else P.FF_SEQUENTIAL
+    dev = torch.device("cuda:0")
+    log(f"bench: generating {w.name} ({w.n} x {w.dims[0]}) and {sw.name} ({sw.n} x {sw.dims[0]})")
+    x_base, y, y_neg, params = make_workload(w)
+    sx, _, _, sparams = make_workload(sw)
+
+    xd = torch.from_numpy(x_base).to(dev)
+    yd = torch.from_numpy(y).to(dev)
+    ynd = torch.from_numpy(y_neg).to(dev)
+    sxd = torch.from_numpy(sx).to(dev)
+    bf16 = dtype == P.FF_BF16
+    layers = [P.Layer(torch.from_numpy(W).to(dev), torch.from_numpy(b).to(dev), bf16)
+              for W, b in params]
+    slayers = [P.Layer(torch.from_numpy(W).to(dev), torch.from_numpy(b).to(dev), bf16)
+               for W, b in sparams]
+    hp = P.HParams(theta=w.theta, lr=w.lr, beta1=w.beta1, beta2=w.beta2, adam_eps=w.adam_eps,
+                   norm_eps=w.norm_eps, dtype=dtype)
+    shp = P.HParams(theta=sw.theta, norm_eps=sw.norm_eps, dtype=dtype)
+    nc = len(w.chunks())
+    ws = P.workspace(P.ff_pipeline_workspace_size(layers, w.n, w.chunk_pairs, sched, dtype), dev)
+    sws = P.workspace(P.ff_score_workspace_size(slayers, sw.n, sw.n_classes, dtype), dev)
+    trace = torch.zeros(w.n_layers, nc, device=dev)
+    scores = torch.empty(sw.n, sw.n_classes, device=dev)
+    pred = torch.empty(sw.n, dtype=torch.int32, device=dev)
+    cur = torch.cuda.current_stream(dev)
+    side = [torch.cuda.Stream(dev) for _ in range(w.n_layers - 1)]
+    streams = [cur] + side
+
+    def step(ev=None):
+        for s in side:
+            s.wait_stream(cur)
+        if ev:
+            ev[0].record(cur)
+        P.ff_pipeline_epoch(layers, hp, xd, yd, ynd, w.n_classes, w.chunk_pairs, 1, sched,
+                            streams=streams, loss_trace=trace, ws=ws)
+        for s in side:
+            cur.wait_stream(s)
+        if ev:
+            ev[1].record(cur)
+        P.ff_score_labels(slayers, shp, sxd, sw.n_classes, 0, scores=scores, pred=pred, ws=sws)
+        if ev:
+            ev[2].record(cur)
+
+    log(f"bench: warmup {args.warmup} step(s)")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    launches_per_step = w.n_layers * nc * 4 + 4 * (sw.n // 2048 + 1) * 4 + 8
+    P.ff_profile_start(launches_per_step * args.steps + 64)
+    log(f"bench: timing {args.steps} step(s)")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(evs[k])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    kstats = P.ff_profile_stop()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    train_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+    score_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
+    step_rows = 2 * w.n * w.n_layers
+    assert torch.isfinite(trace).all().item(), "non-finite loss in the timed steps"
+
+    dname = "bf16" if bf16 else "f32"
+    bound, peak, punit = PEAK[dname]
+    gemms = {k: v for k, v in kstats.items() if k in ("forward", "dw_adam") and v["launches"]}
+    dom = max(gemms, key=lambda k: gemms[k]["total_ms"])
+    ds = gemms[dom]
+    achieved = ds["flops"] / (ds["total_ms"] * 1e-3) / 1e12
+    traffic = load_traffic(dom, w.name)
+    kernels = {}
+    for k, v in kstats.items():
+        if not v["launches"]:
+            continue
+        t = v["total_ms"] * 1e-3
+        kernels[k] = {"launches": v["launches"], "avg_us": v["total_ms"] * 1e3 / v["launches"],
+                      "share": v["total_ms"] / sum(x["total_ms"] for x in kstats.values()),
+                      "TFLOP/s": v["flops"] / t / 1e12 if v["flops"] else None,
+                      "GB/s": v["bytes"] / t / 1e9}
+    out = {
+        "metric": METRIC,
+        "value": step_rows / (ms_per_step * 1e-3),
+        "unit": "pos+neg samples/s per layer-step",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": dname, "data": "synthetic",
+        "config": {"workload": w.name, "rows_per_layer_step": 2 * w.chunk_pairs,
+                   "layers": list(w.dims), "samples": w.n, "chunks": nc,
+                   "schedule": w.schedule, "score_workload": sw.name, "score_images": sw.n,
+                   "score_layers": list(sw.dims)},
+        "train_ms_per_step": train_ms,
+        "train_samples_per_s": step_rows / (train_ms * 1e-3),
+        "score_ms_per_step": score_ms,
+        "images_per_s": sw.n / (score_ms * 1e-3),
+        "roofline": {"bound": bound, "kernel": dom, "achieved": achieved, "peak": peak,
+                     "unit": punit, "frac": achieved / peak,
+                     "traffic": traffic,
+                     "avg_launch_us": ds["total_ms"] * 1e3 / ds["launches"],
+                     "launches": ds["launches"]},
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        log("bench: timing the CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(w, x_base, y, y_neg, params, sw, sx, sparams)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

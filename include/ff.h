@@ -166,6 +166,35 @@ ff_status ff_pipeline_epoch(ff_layer *layers, int32_t n_layers, const ff_hparams
                             int32_t schedule, void *const *streams, float *loss_trace, void *ws,
                             size_t ws_bytes);
 
+/* ---- Kernel timing (tracing aid) -------------------------------------------
+ * Between ff_profile_start and ff_profile_stop every kernel the library
+ * launches (up to max_launches) is bracketed by a pair of hipEvents recorded on
+ * the stream it is launched on, and the algorithmic work of the launch is
+ * counted: flops of the matrix products (2*M*N*K) and the bytes that the
+ * operation must read and write at minimum.  ff_profile_stop waits for the
+ * recorded events, fills stats[FF_KERNEL_KINDS] and releases the events.
+ * Process-wide state; not reentrant with itself. */
+typedef enum {
+  FF_KERNEL_EMBED_NORM = 0,  /* label embedding + row normalisation          */
+  FF_KERNEL_FORWARD = 1,     /* fused forward product + bias/ReLU/goodness    */
+  FF_KERNEL_LOSS = 2,        /* goodness reduction, loss, row coefficients    */
+  FF_KERNEL_DW_ADAM = 3,     /* weight-gradient product + fused Adam          */
+  FF_KERNEL_GOODNESS = 4,    /* goodness reduction / score accumulation       */
+  FF_KERNEL_ARGMAX = 5,      /* label argmax                                  */
+  FF_KERNEL_SHADOW = 6,      /* bf16 weight shadow refresh                    */
+  FF_KERNEL_KINDS = 7
+} ff_kernel_kind;
+
+typedef struct {
+  int64_t launches;   /* launches timed                                      */
+  double total_ms;    /* sum of event-measured durations                     */
+  double flops;       /* algorithmic flops of those launches                 */
+  double bytes;       /* algorithmic HBM bytes of those launches             */
+} ff_kernel_stats;
+
+ff_status ff_profile_start(int32_t max_launches);
+ff_status ff_profile_stop(ff_kernel_stats *stats /* (host) [FF_KERNEL_KINDS] */);
+
 #ifdef __cplusplus
 }
 #endif

@@ -25,7 +25,9 @@ FF_SEQUENTIAL, FF_PIPELINED = 0, 1
 EXPORTS = ["ff_status_string", "ff_last_error", "ff_embed_labels", "ff_step_workspace_size",
            "ff_layer_forward", "ff_layer_step", "ff_refresh_bf16_shadow",
            "ff_score_workspace_size", "ff_score_labels", "ff_pipeline_workspace_size",
-           "ff_pipeline_epoch"]
+           "ff_pipeline_epoch", "ff_profile_start", "ff_profile_stop"]
+
+KERNEL_KINDS = ["embed_norm", "forward", "loss", "dw_adam", "goodness", "argmax", "bf16_shadow"]
 
 
 class FFError(RuntimeError):
@@ -38,6 +40,11 @@ class ff_layer(ctypes.Structure):
     _fields_ = [("d_in", c_int32), ("d_out", c_int32), ("W", c_void_p), ("b", c_void_p),
                 ("mW", c_void_p), ("vW", c_void_p), ("mb", c_void_p), ("vb", c_void_p),
                 ("W_bf16", c_void_p), ("step", c_int64)]
+
+
+class ff_kernel_stats(ctypes.Structure):
+    _fields_ = [("launches", c_int64), ("total_ms", ctypes.c_double), ("flops", ctypes.c_double),
+                ("bytes", ctypes.c_double)]
 
 
 class ff_hparams(ctypes.Structure):
@@ -70,6 +77,8 @@ def _load() -> ctypes.CDLL:
         "ff_pipeline_epoch": (c_int32, [POINTER(ff_layer), c_int32, POINTER(ff_hparams), P, P, P,
                                         c_int32, c_int32, c_int32, c_int32, c_int32,
                                         POINTER(c_void_p), P, P, c_size_t]),
+        "ff_profile_start": (c_int32, [c_int32]),
+        "ff_profile_stop": (c_int32, [POINTER(ff_kernel_stats)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -274,3 +283,15 @@ def ff_pipeline_epoch(layers: List[Layer], hp: HParams, x_base: torch.Tensor, y_
             ws.record_stream(s)
     _check(st)
     return loss_trace
+
+
+def ff_profile_start(max_launches: int = 65536):
+    _check(LIB.ff_profile_start(max_launches))
+
+
+def ff_profile_stop() -> dict:
+    """Per kernel kind: launches, total_ms, flops, bytes (event-timed on each launch's stream)."""
+    arr = (ff_kernel_stats * len(KERNEL_KINDS))()
+    _check(LIB.ff_profile_stop(arr))
+    return {k: dict(launches=a.launches, total_ms=a.total_ms, flops=a.flops, bytes=a.bytes)
+            for k, a in zip(KERNEL_KINDS, arr)}

@@ -9,6 +9,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "../../include/ff.h"
@@ -57,6 +58,45 @@ struct Carver {
 
 inline size_t elem_bytes(int dtype) { return dtype == FF_BF16 ? 2 : 4; }
 
+// ---------------------------------------------------------------------------
+// Kernel timing: event pairs around launches while a profile is active.
+// ---------------------------------------------------------------------------
+struct ProfRec {
+  int kind;
+  double flops, bytes;
+  hipEvent_t a, b;
+};
+struct Profiler {
+  std::mutex mu;
+  bool on = false;
+  std::vector<hipEvent_t> pool;
+  size_t used = 0;
+  std::vector<ProfRec> recs;
+};
+Profiler g_prof;
+
+// Launches `fn` (returning hipError_t), bracketed by timing events when a
+// profile is active and events remain.
+template <class F>
+hipError_t launch(int kind, double flops, double bytes, hipStream_t st, F fn) {
+  std::unique_lock<std::mutex> lk(g_prof.mu);
+  if (!g_prof.on || g_prof.used + 2 > g_prof.pool.size()) {
+    lk.unlock();
+    return fn();
+  }
+  hipEvent_t a = g_prof.pool[g_prof.used++], b = g_prof.pool[g_prof.used++];
+  hipError_t e = hipEventRecord(a, st);
+  if (e != hipSuccess) return e;
+  e = fn();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(b, st);
+  if (e == hipSuccess) g_prof.recs.push_back(ProfRec{kind, flops, bytes, a, b});
+  return e;
+}
+
+// Algorithmic work of the launches (what the operation must move or compute).
+inline double gemm_flops(long m, long n, long k) { return 2.0 * m * n * k; }
+
 // Scratch of one layer step.  Pointers the caller supplied are not carved.
 struct StepScratch {
   void *xhat = nullptr;   // [rows][d_in], fp32 or bf16
@@ -64,6 +104,7 @@ struct StepScratch {
   float *gpart = nullptr; // [col tiles][rows]
   float *g = nullptr;     // [rows]
   float *c = nullptr;     // [rows]
+  float *lpart = nullptr; // [loss blocks][2]
   float *loss = nullptr;  // [1]
 };
 
@@ -74,6 +115,7 @@ void carve_step(Carver &cv, StepScratch &s, int rows, int d_in, int d_out, int d
   s.gpart = static_cast<float *>(cv.take((size_t)ffk::fwd_col_tiles(d_out, dtype) * rows * 4));
   if (need_g) s.g = static_cast<float *>(cv.take((size_t)rows * 4));
   s.c = static_cast<float *>(cv.take((size_t)rows * 4));
+  s.lpart = static_cast<float *>(cv.take((size_t)ffk::loss_blocks(rows) * 2 * 4));
   if (need_loss) s.loss = static_cast<float *>(cv.take(4));
 }
 
@@ -130,6 +172,42 @@ inline const void *weight_operand(const ff_layer *L, int dtype) {
 // Normalised operand rows for a layer: fp32 rows may be used in place when
 // already normalised; otherwise (and always for bf16) the embed/normalise
 // kernel writes them into scratch.
+hipError_t embed_norm(const ffk::RowMap &src, int rows, int d, float eps, bool normalise,
+                      bool bf16, void *out, hipStream_t st) {
+  // unique source rows: a chunk's positives and negatives share base rows, and
+  // label expansion reads each base row once per label
+  const double src_rows = src.mode == ffk::PAIRS    ? (double)src.n_pos
+                          : src.mode == ffk::EXPAND ? (double)rows / src.n_classes
+                                                    : (double)rows;
+  const double bytes = src_rows * d * 4.0 + (double)rows * d * (bf16 ? 2 : 4);
+  return launch(FF_KERNEL_EMBED_NORM, 0.0, bytes, st, [&] {
+    return ffk::launch_embed_norm(src, rows, d, eps, normalise, bf16, out, st);
+  });
+}
+
+hipError_t fwd(int dtype, const void *X, const void *W, const float *bias, int M, int N, int K,
+               float *H, float *gpart, hipStream_t st) {
+  const double eb = (double)elem_bytes(dtype);
+  const double nt = ffk::fwd_col_tiles(N, dtype);
+  const double bytes = (double)M * K * eb + (double)N * K * eb + N * 4.0 +
+                       (H ? (double)M * N * 4.0 : 0.0) + nt * M * 4.0;
+  return launch(FF_KERNEL_FORWARD, gemm_flops(M, N, K), bytes, st, [&] {
+    return ffk::launch_fwd(dtype, X, W, bias, M, N, K, H, gpart, st);
+  });
+}
+
+hipError_t goodness_sum(const float *gpart, int nt, int R, float *g, float *out, int accumulate,
+                        hipStream_t st) {
+  const double bytes = (double)nt * R * 4.0 + (g ? R * 4.0 : 0.0) +
+                       (out ? R * 4.0 * (accumulate ? 2 : 1) : 0.0);
+  return launch(FF_KERNEL_GOODNESS, 0.0, bytes, st, [&] {
+    return ffk::launch_goodness(gpart, nt, R, g, out, accumulate, st);
+  });
+}
+
+// Normalised operand rows for a layer: fp32 rows may be used in place when
+// already normalised; otherwise (and always for bf16) the embed/normalise
+// kernel writes them into scratch.
 ff_status stage_input(const ffk::RowMap &src, int rows, int d_in, bool normalised, int dtype,
                       float norm_eps, void *scratch, const void **operand, hipStream_t st) {
   const bool bf16 = dtype == FF_BF16;
@@ -137,7 +215,7 @@ ff_status stage_input(const ffk::RowMap &src, int rows, int d_in, bool normalise
     *operand = src.base;
     return FF_OK;
   }
-  FF_HIP(ffk::launch_embed_norm(src, rows, d_in, norm_eps, !normalised, bf16, scratch, st));
+  FF_HIP(embed_norm(src, rows, d_in, norm_eps, !normalised, bf16, scratch, st));
   *operand = scratch;
   return FF_OK;
 }
@@ -148,11 +226,11 @@ ff_status forward_core(const ff_layer *L, const ff_hparams *hp, const ffk::RowMa
                        hipStream_t st) {
   const void *xop = nullptr;
   FF_TRY(stage_input(src, rows, L->d_in, normalised, hp->dtype, hp->norm_eps, s.xhat, &xop, st));
-  FF_HIP(ffk::launch_fwd(hp->dtype, xop, weight_operand(L, hp->dtype), L->b, rows, L->d_out,
-                         L->d_in, h_out, s.gpart, st));
+  FF_HIP(fwd(hp->dtype, xop, weight_operand(L, hp->dtype), L->b, rows, L->d_out, L->d_in, h_out,
+             s.gpart, st));
   if (goodness)
-    FF_HIP(ffk::launch_goodness(s.gpart, ffk::fwd_col_tiles(L->d_out, hp->dtype), rows, goodness,
-                                nullptr, 0, st));
+    FF_HIP(goodness_sum(s.gpart, ffk::fwd_col_tiles(L->d_out, hp->dtype), rows, goodness, nullptr,
+                        0, st));
   return FF_OK;
 }
 
@@ -167,9 +245,17 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const ffk::RowMap &src, i
   float *g = goodness ? goodness : s.g;
   float *lo = loss ? loss : s.loss;
   const int nt = ffk::fwd_col_tiles(L->d_out, hp->dtype);
-  FF_HIP(ffk::launch_fwd(hp->dtype, xop, weight_operand(L, hp->dtype), L->b, R, L->d_out, L->d_in,
-                         H, s.gpart, st));
-  FF_HIP(ffk::launch_loss(s.gpart, nt, R, n_pos, hp->theta, g, s.c, lo, st));
+  FF_HIP(fwd(hp->dtype, xop, weight_operand(L, hp->dtype), L->b, R, L->d_out, L->d_in, H, s.gpart,
+             st));
+  FF_HIP(launch(FF_KERNEL_LOSS, 0.0, (double)nt * R * 4.0 + R * (g ? 8.0 : 4.0), st, [&] {
+    return ffk::launch_loss(s.gpart, nt, R, n_pos, hp->theta, g, s.c, s.lpart, st);
+  }));
+  ffk::LossFinish lf;
+  lf.lpart = s.lpart;
+  lf.nblk = ffk::loss_blocks(R);
+  lf.n_pos = n_pos;
+  lf.n_neg = n_neg;
+  lf.loss = lo;
   const int64_t t = ++L->step;
   ffk::AdamArgs a;
   a.lr = hp->lr;
@@ -178,9 +264,17 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const ffk::RowMap &src, i
   a.eps = hp->adam_eps;
   a.bc1 = (float)(1.0 - pow((double)hp->beta1, (double)t));
   a.bc2 = (float)(1.0 - pow((double)hp->beta2, (double)t));
-  FF_HIP(ffk::launch_dw_adam(hp->dtype, H, s.c, xop, L->d_out, L->d_in, R, L->W, L->mW, L->vW,
-                             hp->dtype == FF_BF16 ? L->W_bf16 : nullptr, L->b, L->mb, L->vb, a,
-                             st));
+  {
+    const double eb = (double)elem_bytes(hp->dtype);
+    const double params = (double)L->d_out * L->d_in;
+    const double bytes = (double)R * L->d_out * 4.0 + (double)R * L->d_in * eb + R * 4.0 +
+                         params * (24.0 + (hp->dtype == FF_BF16 ? 2.0 : 0.0)) + L->d_out * 24.0;
+    FF_HIP(launch(FF_KERNEL_DW_ADAM, gemm_flops(L->d_out, L->d_in, R), bytes, st, [&] {
+      return ffk::launch_dw_adam(hp->dtype, H, s.c, xop, L->d_out, L->d_in, R, L->W, L->mW, L->vW,
+                                 hp->dtype == FF_BF16 ? L->W_bf16 : nullptr, L->b, L->mb, L->vb,
+                                 a, lf, st);
+    }));
+  }
   return FF_OK;
 }
 
@@ -234,8 +328,7 @@ ff_status ff_embed_labels(const float *x_base, const int32_t *labels, int32_t ro
   m.n_pos = rows;
   m.base_off = 0;
   m.n_classes = n_classes;
-  FF_HIP(ffk::launch_embed_norm(m, rows, d, 0.f, false, false, out,
-                                static_cast<hipStream_t>(stream)));
+  FF_HIP(embed_norm(m, rows, d, 0.f, false, false, out, static_cast<hipStream_t>(stream)));
   return FF_OK;
 }
 
@@ -281,8 +374,10 @@ ff_status ff_layer_step(ff_layer *L, const ff_hparams *hp, const float *x, int32
 ff_status ff_refresh_bf16_shadow(const ff_layer *L, void *stream) {
   FF_TRY(check_layer(L, nullptr, false, 0));
   if (!L->W_bf16) return fail(FF_ERR_INVALID_ARG, "W_bf16 is NULL");
-  FF_HIP(ffk::launch_bf16_shadow(L->W, L->W_bf16, (size_t)L->d_out * L->d_in,
-                                 static_cast<hipStream_t>(stream)));
+  const size_t count = (size_t)L->d_out * L->d_in;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  FF_HIP(launch(FF_KERNEL_SHADOW, 0.0, count * 6.0, st,
+                [&] { return ffk::launch_bf16_shadow(L->W, L->W_bf16, count, st); }));
   return FF_OK;
 }
 
@@ -355,22 +450,21 @@ ff_status ff_score_labels(const ff_layer *layers, int32_t n_layers, int32_t firs
     m.mode = ffk::EXPAND;
     m.base_off = n0;
     m.n_classes = n_classes;
-    FF_HIP(ffk::launch_embed_norm(m, rows, layers[0].d_in, hp->norm_eps, true, bf16, s.x, st));
+    FF_HIP(embed_norm(m, rows, layers[0].d_in, hp->norm_eps, true, bf16, s.x, st));
     for (int l = 0; l < n_layers; ++l) {
       const ff_layer *L = &layers[l];
       const bool last = l + 1 == n_layers;
-      FF_HIP(ffk::launch_fwd(hp->dtype, s.x, weight_operand(L, hp->dtype), L->b, rows, L->d_out,
-                             L->d_in, last ? nullptr : s.h, s.gpart, st));
+      FF_HIP(fwd(hp->dtype, s.x, weight_operand(L, hp->dtype), L->b, rows, L->d_out, L->d_in,
+                 last ? nullptr : s.h, s.gpart, st));
       if (l >= first_scored_layer)
-        FF_HIP(ffk::launch_goodness(s.gpart, ffk::fwd_col_tiles(L->d_out, hp->dtype), rows,
-                                    nullptr, S + (size_t)n0 * n_classes,
-                                    l > first_scored_layer ? 1 : 0, st));
+        FF_HIP(goodness_sum(s.gpart, ffk::fwd_col_tiles(L->d_out, hp->dtype), rows, nullptr,
+                            S + (size_t)n0 * n_classes, l > first_scored_layer ? 1 : 0, st));
       if (!last)
-        FF_HIP(ffk::launch_embed_norm(rows_of(s.h), rows, L->d_out, hp->norm_eps, true, bf16,
-                                      s.x, st));
+        FF_HIP(embed_norm(rows_of(s.h), rows, L->d_out, hp->norm_eps, true, bf16, s.x, st));
     }
   }
-  FF_HIP(ffk::launch_argmax(S, n, n_classes, pred, st));
+  FF_HIP(launch(FF_KERNEL_ARGMAX, 0.0, (double)n * n_classes * 4.0 + n * 4.0, st,
+                [&] { return ffk::launch_argmax(S, n, n_classes, pred, st); }));
   return FF_OK;
 }
 
@@ -529,6 +623,59 @@ ff_status ff_pipeline_epoch(ff_layer *layers, int32_t n_layers, const ff_hparams
     }
   }
   return FF_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Kernel timing
+// ---------------------------------------------------------------------------
+ff_status ff_profile_start(int32_t max_launches) {
+  if (max_launches <= 0) return fail(FF_ERR_INVALID_ARG, "max_launches=%d", max_launches);
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (g_prof.on) return fail(FF_ERR_INVALID_ARG, "a profile is already active");
+  g_prof.pool.assign((size_t)2 * max_launches, nullptr);
+  for (auto &e : g_prof.pool) {
+    hipError_t err = hipEventCreate(&e);
+    if (err != hipSuccess) {
+      for (auto &f : g_prof.pool)
+        if (f) (void)hipEventDestroy(f);
+      g_prof.pool.clear();
+      return fail(FF_ERR_HIP, "hipEventCreate failed: %s", hipGetErrorString(err));
+    }
+  }
+  g_prof.used = 0;
+  g_prof.recs.clear();
+  g_prof.on = true;
+  return FF_OK;
+}
+
+ff_status ff_profile_stop(ff_kernel_stats *stats) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (!g_prof.on) return fail(FF_ERR_INVALID_ARG, "no active profile");
+  g_prof.on = false;
+  ff_status st = FF_OK;
+  if (stats)
+    for (int k = 0; k < FF_KERNEL_KINDS; ++k) stats[k] = ff_kernel_stats{0, 0.0, 0.0, 0.0};
+  for (const ProfRec &r : g_prof.recs) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e != hipSuccess) {
+      st = fail(FF_ERR_HIP, "reading kernel timing events: %s", hipGetErrorString(e));
+      continue;
+    }
+    if (stats) {
+      ff_kernel_stats &k = stats[r.kind];
+      k.launches += 1;
+      k.total_ms += ms;
+      k.flops += r.flops;
+      k.bytes += r.bytes;
+    }
+  }
+  for (auto &e : g_prof.pool) (void)hipEventDestroy(e);
+  g_prof.pool.clear();
+  g_prof.recs.clear();
+  g_prof.used = 0;
+  return st;
 }
 
 }  // extern "C"

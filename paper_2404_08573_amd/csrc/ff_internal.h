@@ -32,6 +32,18 @@ struct AdamArgs {
   float bc1, bc2;  // 1 - beta1^t, 1 - beta2^t
 };
 
+// Loss scalar finished by the dW kernel from the per-workgroup partials of
+// the loss-rows kernel: loss = sum(pos partials)/n_pos + sum(neg partials)/n_neg.
+struct LossFinish {
+  const float *lpart;  // [nblk][2]
+  int32_t nblk;
+  int32_t n_pos, n_neg;
+  float *loss;         // null: not wanted
+};
+
+// Number of per-workgroup loss partial pairs for `rows` rows.
+int loss_blocks(int rows);
+
 // Row-tile and column-tile sizes of the forward product, which fix the
 // number of goodness partials per row (one per column tile).
 int fwd_col_tiles(int n_cols, int dtype);
@@ -45,15 +57,17 @@ hipError_t launch_embed_norm(const RowMap &m, int rows, int d, float eps, bool n
 hipError_t launch_fwd(int dtype, const void *X, const void *W, const float *bias, int M, int N,
                       int K, float *H, float *gpart, hipStream_t s);
 
-// g_r = sum_t gpart[t][r]; loss and c_r = 2 dL/dg_r (single workgroup).
+// g_r = sum_t gpart[t][r] (into g unless null), c_r = 2 dL/dg_r, and loss
+// partials lpart[loss_blocks(R)][2].
 hipError_t launch_loss(const float *gpart, int ntiles, int R, int n_pos, float theta, float *g,
-                       float *c, float *loss, hipStream_t s);
+                       float *c, float *lpart, hipStream_t s);
 
 // dW = (c . H)^T Xh contracted over the R rows, db = sum_r c_r H_r, then one
-// Adam update of W (and its bf16 shadow when Wb != nullptr) and of b.
+// Adam update of W (and its bf16 shadow when Wb != nullptr) and of b; also
+// finishes the loss scalar described by lf.
 hipError_t launch_dw_adam(int dtype, const float *H, const float *c, const void *Xh, int M, int N,
                           int K, float *W, float *mW, float *vW, uint16_t *Wb, float *b, float *mb,
-                          float *vb, const AdamArgs &a, hipStream_t s);
+                          float *vb, const AdamArgs &a, const LossFinish &lf, hipStream_t s);
 
 // g_r = sum_t gpart[t][r] into g (any of the outputs may be null);
 // out[r] = g_r (accumulate == 0) or out[r] += g_r (accumulate == 1).

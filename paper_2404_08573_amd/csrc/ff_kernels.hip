@@ -9,12 +9,13 @@
 //   k_fwd_f32      Z = X W^T on fp32 MFMA (v_mfma_f32_32x32x2f32), epilogue fuses
 //                  bias, ReLU, the H store and the per-row goodness partial sum over
 //                  the tile's columns (Eq. 1) through a lane butterfly and LDS.
-//   k_loss         goodness partials -> g, the Eq. 1 threshold loss and the per-row
-//                  gradient coefficient c_r = 2 dL/dg_r; one workgroup, fixed order.
+//   k_loss_rows    goodness partials -> g, the per-row gradient coefficient
+//                  c_r = 2 dL/dg_r and per-workgroup sums of the Eq. 1 loss terms.
 //   k_dw_adam_f32  dW = (c.H)^T X_hat on fp32 MFMA (contraction over the batch rows),
 //                  the row scale c applied while staging H, db summed from the same
 //                  staged rows, and the Adam update of W and b fused in the epilogue
-//                  (no split over rows, so every dW tile is final in one workgroup).
+//                  (no split over rows, so every dW tile is final in one workgroup);
+//                  its first thread also finishes the loss scalar in a fixed order.
 //   k_goodness, k_argmax, k_bf16_shadow: small row/elementwise kernels.
 //
 // Every reduction runs in a fixed order, so results are bitwise reproducible
@@ -138,10 +139,10 @@ __global__ __launch_bounds__(kBlock) void k_embed_norm(RowMap m, int rows, int d
 }
 
 // ---------------------------------------------------------------------------
-// Goodness row reduction of a 64x64 wave tile held as 2x2 32x32 MFMA blocks.
-// v[q], q = bi*16 + r, holds this lane's partial (over its columns) for the
-// accumulator row (bi, r).  A reduce-scatter butterfly over the 32 lanes of
-// each half-wave leaves lane l with the full sum of entry q = l & 31.
+// Goodness row reduction of a wave's 64-row accumulator tile held as two
+// 32x32 MFMA blocks.  v[q], q = bi*16 + r, holds this lane's partial (over its
+// columns) for accumulator row (bi, r).  A reduce-scatter butterfly over the 32
+// lanes of each half-wave leaves lane l with the full sum of entry q = l & 31.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float rowsum_scatter32(float (&v)[32], int lane) {
 #pragma unroll
@@ -157,33 +158,87 @@ __device__ __forceinline__ float rowsum_scatter32(float (&v)[32], int lane) {
   return v[0];
 }
 
-// Row (within the wave's 64-row tile) of 32x32 accumulator element (bi, r)
-// held by a lane with half-wave index kg: the v_mfma_f32_32x32x2f32 output
-// layout puts row 8*(r/4) + 4*kg + r%4 of block bi in register r.
-__device__ __forceinline__ int acc_row(int bi, int r, int kg) {
-  return bi * 32 + 8 * (r >> 2) + 4 * kg + (r & 3);
+// Row (within a 32x32 block) of accumulator register r held by a lane of
+// half-wave kg: the v_mfma_f32_32x32x2f32 output layout puts row
+// 8*(r/4) + 4*kg + r%4 in register r (column = lane % 32).
+__device__ __forceinline__ int acc_row(int r, int kg) { return 8 * (r >> 2) + 4 * kg + (r & 3); }
+
+// Software pipeline over nk k-tiles: LDS is double-buffered and the global
+// loads run two tiles ahead in two register stages, so a load has two tiles'
+// worth of MFMA work to land.  Tile t lives in LDS buffer t%2; the loop is
+// unrolled by two so the register stages are fixed.  Every LDS buffer is
+// rewritten only after the barrier that ends the computation reading it.
+template <class Load, class Store, class Compute, class Stage>
+__device__ __forceinline__ void kloop2(int nk, Load &gload, Store &sstore, Compute &compute,
+                                       Stage &s0, Stage &s1) {
+  gload(s0, 0);
+  if (nk > 1) gload(s1, 1);
+  sstore(s0, 0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; kt += 2) {
+    if (kt + 2 < nk) gload(s0, kt + 2);
+    compute(0);
+    if (kt + 1 < nk) sstore(s1, 1);
+    __syncthreads();
+    if (kt + 1 >= nk) break;
+    if (kt + 3 < nk) gload(s1, kt + 3);
+    compute(1);
+    if (kt + 2 < nk) sstore(s0, 0);
+    __syncthreads();
+  }
 }
+
+// One register stage: the loads of tile t+1 are issued before the MFMAs of
+// tile t and written to the other LDS buffer after them.
+template <class Load, class Store, class Compute, class Stage>
+__device__ __forceinline__ void kloop1(int nk, Load &gload, Store &sstore, Compute &compute,
+                                       Stage &s0) {
+  gload(s0, 0);
+  sstore(s0, 0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + 1 < nk) gload(s0, kt + 1);
+    compute(kt & 1);
+    if (kt + 1 < nk) sstore(s0, (kt + 1) & 1);
+    __syncthreads();
+  }
+}
+
+template <int PF, class Load, class Store, class Compute, class Stage>
+__device__ __forceinline__ void kloop(int nk, Load &gload, Store &sstore, Compute &compute,
+                                      Stage &s0, Stage &s1) {
+  if constexpr (PF == 2)
+    kloop2(nk, gload, sstore, compute, s0, s1);
+  else
+    kloop1(nk, gload, sstore, compute, s0);
+}
+
+constexpr int kPrefetch = 1;  // register stages of the GEMM pipelines
+
+constexpr int kGemm = 512;  // 8 waves: two per SIMD, so one wave's LDS/global waits hide behind the other's MFMAs
 
 // ---------------------------------------------------------------------------
 // Forward: H = relu(X W^T + b), gpart[tn][row] = sum over the tile's columns of H^2.
-// X [M][K], W [N][K] (both K-contiguous), fp32.  Tile 128x128, 4 waves in 2x2,
-// each wave 64x64 as 2x2 blocks of v_mfma_f32_32x32x2f32.  Within a BK slab the
-// two half-waves take the two halves of the slab's k range, so every lane reads
+// X [M][K], W [N][K] (both K-contiguous), fp32.  Tile 128x128; waves 2 (M) x 4 (N),
+// each 64x32 as two v_mfma_f32_32x32x2f32 blocks.  Within a BK slab the two
+// half-waves take the two halves of the slab's k range, so every lane reads
 // contiguous float4 runs from LDS for both operands (the k order inside the
 // contraction is a permutation of the plain order, the same for X and W).
+// Loads are branch-free: out-of-range rows read a clamped valid row whose
+// results are never stored; the k tail is zeroed.
 // ---------------------------------------------------------------------------
 template <int BK, bool STORE_H>
-__global__ __launch_bounds__(kBlock) void k_fwd_f32(const float *__restrict__ X,
-                                                    const float *__restrict__ W,
-                                                    const float *__restrict__ bias, int M, int N,
-                                                    int K, float *__restrict__ H,
-                                                    float *__restrict__ gpart) {
+__global__ __launch_bounds__(kGemm) void k_fwd_f32(const float *__restrict__ X,
+                                                   const float *__restrict__ W,
+                                                   const float *__restrict__ bias, int M, int N,
+                                                   int K, float *__restrict__ H,
+                                                   float *__restrict__ gpart) {
   constexpr int BM = 128, BN = 128;
   constexpr int LDK = BK + 4;   // padded row: conflict-free 16-byte reads
   constexpr int KF4 = BK / 4;   // float4 per tile row
-  constexpr int A_LD = BM * KF4 / kBlock;
-  constexpr int B_LD = BN * KF4 / kBlock;
-  static_assert(A_LD * kBlock == BM * KF4 && B_LD * kBlock == BN * KF4, "tile/threads");
+  constexpr int LD = BM * KF4 / kGemm;  // float4 loads per thread per operand
+  constexpr int RSTEP = kGemm / KF4;    // tile rows between a thread's loads
+  static_assert(LD * kGemm == BM * KF4, "tile/threads");
   __shared__ __attribute__((aligned(16))) float sm[2 * (BM + BN) * LDK];
   float *As = sm;                 // [2][BM][LDK]
   float *Bs = sm + 2 * BM * LDK;  // [2][BN][LDK]
@@ -192,168 +247,162 @@ __global__ __launch_bounds__(kBlock) void k_fwd_f32(const float *__restrict__ X,
   const int tn = blockIdx.x % nt, tm = blockIdx.x / nt;
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;
   const int li = lane & 31, kg = lane >> 5;
 
-  float4 ra[A_LD], rb[B_LD];
-  auto gload = [&](int kt) {
-    const int kb = kt * BK;
+  const int srow = tid / KF4, kc = (tid % KF4) * 4;
+  const float *pa[LD];
+  const float *pb[LD];
 #pragma unroll
-    for (int i = 0; i < A_LD; ++i) {
-      const int idx = tid + i * kBlock, row = idx / KF4, kc = (idx % KF4) * 4;
-      const int gr = m0 + row, gk = kb + kc;
-      ra[i] = (gr < M && gk < K) ? ld4(X + (size_t)gr * K + gk) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-#pragma unroll
-    for (int i = 0; i < B_LD; ++i) {
-      const int idx = tid + i * kBlock, row = idx / KF4, kc = (idx % KF4) * 4;
-      const int gr = n0 + row, gk = kb + kc;
-      rb[i] = (gr < N && gk < K) ? ld4(W + (size_t)gr * K + gk) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
+  for (int i = 0; i < LD; ++i) {
+    pa[i] = X + (size_t)min(m0 + srow + i * RSTEP, M - 1) * K + kc;
+    pb[i] = W + (size_t)min(n0 + srow + i * RSTEP, N - 1) * K + kc;
+  }
+  // Loaded values are only consumed when written to LDS, after the MFMAs of
+  // the current tile, so the loads overlap that work (the k-tail mask is
+  // applied at that point too, never right after the load).
+  struct Stage {
+    float4 a[LD], b[LD];
+    int kt;
   };
-  auto sstore = [&](int buf) {
+  Stage s0, s1;
+  auto gload = [&](Stage &st, int kt) {
+    const int kb = kt * BK;
+    const int ko = kb + kc < K ? kb : K - 4 - kc;  // clamped to a valid address when past K
 #pragma unroll
-    for (int i = 0; i < A_LD; ++i) {
-      const int idx = tid + i * kBlock, row = idx / KF4, kc = (idx % KF4) * 4;
-      st4(As + (buf * BM + row) * LDK + kc, ra[i]);
+    for (int i = 0; i < LD; ++i) {
+      st.a[i] = ld4(pa[i] + ko);
+      st.b[i] = ld4(pb[i] + ko);
     }
+    st.kt = kt;
+  };
+  auto sstore = [&](const Stage &st, int buf) {
+    const bool kok = st.kt * BK + kc < K;
+    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-    for (int i = 0; i < B_LD; ++i) {
-      const int idx = tid + i * kBlock, row = idx / KF4, kc = (idx % KF4) * 4;
-      st4(Bs + (buf * BN + row) * LDK + kc, rb[i]);
+    for (int i = 0; i < LD; ++i) {
+      st4(As + (buf * BM + srow + i * RSTEP) * LDK + kc, kok ? st.a[i] : z);
+      st4(Bs + (buf * BN + srow + i * RSTEP) * LDK + kc, kok ? st.b[i] : z);
     }
   };
 
-  floatx16 acc[2][2];
+  floatx16 acc[2];
 #pragma unroll
   for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
-    for (int bj = 0; bj < 2; ++bj)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[bi][bj][r] = 0.f;
+    for (int r = 0; r < 16; ++r) acc[bi][r] = 0.f;
 
   auto compute = [&](int buf) {
     const float *a0 = As + (buf * BM + wm * 64 + li) * LDK + kg * (BK / 2);
-    const float *b0 = Bs + (buf * BN + wn * 64 + li) * LDK + kg * (BK / 2);
+    const float *b0 = Bs + (buf * BN + wn * 32 + li) * LDK + kg * (BK / 2);
 #pragma unroll
     for (int s4 = 0; s4 < BK / 2; s4 += 4) {
-      float4 a[2], b[2];
-      a[0] = ld4(a0 + s4);
-      a[1] = ld4(a0 + 32 * LDK + s4);
-      b[0] = ld4(b0 + s4);
-      b[1] = ld4(b0 + 32 * LDK + s4);
+      const float4 a_0 = ld4(a0 + s4), a_1 = ld4(a0 + 32 * LDK + s4), b = ld4(b0 + s4);
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-          for (int bj = 0; bj < 2; ++bj)
-            acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x2f32(comp(a[bi], q), comp(b[bj], q),
-                                                               acc[bi][bj], 0, 0, 0);
+      for (int q = 0; q < 4; ++q) {
+        acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(comp(a_0, q), comp(b, q), acc[0], 0, 0, 0);
+        acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(comp(a_1, q), comp(b, q), acc[1], 0, 0, 0);
+      }
     }
   };
 
   const int nk = (K + BK - 1) / BK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
-    compute(cur);
-    if (kt + 1 < nk) sstore(cur ^ 1);
-    __syncthreads();
-  }
+  kloop<kPrefetch>(nk, gload, sstore, compute, s0, s1);
 
   // Epilogue: bias, ReLU, H store, goodness partials.
   float hsq[32];
+  const int col = n0 + wn * 32 + li;
+  const bool cok = col < N;
+  const float bv = cok ? bias[col] : 0.f;
 #pragma unroll
-  for (int q = 0; q < 32; ++q) hsq[q] = 0.f;
+  for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
-  for (int bj = 0; bj < 2; ++bj) {
-    const int col = n0 + wn * 64 + bj * 32 + li;
-    const bool cok = col < N;
-    const float bv = cok ? bias[col] : 0.f;
-#pragma unroll
-    for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float h = cok ? fmaxf(acc[bi][bj][r] + bv, 0.f) : 0.f;
-        if (STORE_H) {
-          const int row = m0 + wm * 64 + acc_row(bi, r, kg);
-          if (row < M && cok) H[(size_t)row * N + col] = h;
-        }
-        hsq[bi * 16 + r] += h * h;
+    for (int r = 0; r < 16; ++r) {
+      const float h = cok ? fmaxf(acc[bi][r] + bv, 0.f) : 0.f;
+      if (STORE_H) {
+        const int row = m0 + wm * 64 + bi * 32 + acc_row(r, kg);
+        if (row < M && cok) H[(size_t)row * N + col] = h;
       }
-  }
+      hsq[bi * 16 + r] = h * h;
+    }
   const float part = rowsum_scatter32(hsq, lane);
   const int q = lane & 31;
-  float *gs = sm;  // [2][BM], main-loop buffers are free after the last barrier
-  gs[wn * BM + wm * 64 + acc_row(q >> 4, q & 15, kg)] = part;
+  float *gs = sm;  // [4][BM]; the main-loop buffers are free after the last barrier
+  gs[wn * BM + wm * 64 + (q >> 4) * 32 + acc_row(q & 15, kg)] = part;
   __syncthreads();
   if (tid < BM) {
     const int row = m0 + tid;
-    if (row < M) gpart[(size_t)tn * M + row] = gs[tid] + gs[BM + tid];
+    if (row < M)
+      gpart[(size_t)tn * M + row] = (gs[tid] + gs[BM + tid]) + (gs[2 * BM + tid] + gs[3 * BM + tid]);
   }
 }
 
 // ---------------------------------------------------------------------------
-// Loss: one workgroup; g_r, c_r, and the Eq. 1 loss (mean over positives +
-// mean over negatives) with a fixed-order tree reduction.
+// Loss rows: g_r, c_r = 2 dL/dg_r, and per-workgroup partial sums of the Eq. 1
+// terms (positives and negatives apart); the dW kernel finishes the scalar.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(1024) void k_loss(const float *__restrict__ gpart, int nt, int R,
-                                               int n_pos, float theta, float *__restrict__ g,
-                                               float *__restrict__ c, float *__restrict__ loss) {
-  __shared__ float sp[1024], sn[1024];
-  const int n_neg = R - n_pos;
-  const float inv_p = 1.f / (float)n_pos, inv_n = 1.f / (float)n_neg;
+constexpr int kLossRows = 256;
+
+__global__ __launch_bounds__(kLossRows) void k_loss_rows(const float *__restrict__ gpart, int nt,
+                                                          int R, int n_pos, float theta,
+                                                          float *__restrict__ g,
+                                                          float *__restrict__ c,
+                                                          float *__restrict__ lpart) {
+  __shared__ float sp[kLossRows], sn[kLossRows];
+  const int r = blockIdx.x * kLossRows + threadIdx.x;
   float lp = 0.f, ln = 0.f;
-  for (int r = threadIdx.x; r < R; r += 1024) {
+  if (r < R) {
     float gv = 0.f;
     for (int t = 0; t < nt; ++t) gv += gpart[(size_t)t * R + r];
     if (g) g[r] = gv;
     if (r < n_pos) {
       const float x = theta - gv;
-      lp += softplus_f(x);
-      c[r] = -2.f * sigmoid_f(x) * inv_p;
+      lp = softplus_f(x);
+      c[r] = -2.f * sigmoid_f(x) / (float)n_pos;
     } else {
       const float x = gv - theta;
-      ln += softplus_f(x);
-      c[r] = 2.f * sigmoid_f(x) * inv_n;
+      ln = softplus_f(x);
+      c[r] = 2.f * sigmoid_f(x) / (float)(R - n_pos);
     }
   }
   sp[threadIdx.x] = lp;
   sn[threadIdx.x] = ln;
   __syncthreads();
-  for (int s = 512; s > 0; s >>= 1) {
+  for (int s = kLossRows / 2; s > 0; s >>= 1) {
     if ((int)threadIdx.x < s) {
       sp[threadIdx.x] += sp[threadIdx.x + s];
       sn[threadIdx.x] += sn[threadIdx.x + s];
     }
     __syncthreads();
   }
-  if (threadIdx.x == 0 && loss) loss[0] = sp[0] * inv_p + sn[0] * inv_n;
+  if (threadIdx.x == 0) {
+    lpart[2 * blockIdx.x] = sp[0];
+    lpart[2 * blockIdx.x + 1] = sn[0];
+  }
 }
 
 // ---------------------------------------------------------------------------
 // dW = (c.H)^T X_hat (+ db) with the Adam update fused.  M = d_out, N = d_in,
 // K = R batch rows.  Both operands arrive row-major over K (batch rows), so the
-// LDS tiles are [BK][BM] and [BK][BN]; each lane reads one float per operand
-// per MFMA.  Half-wave kg takes slab rows 2s+kg; the 32-float pad puts those
-// two rows on disjoint bank halves.
+// LDS tiles are [BK][BM] and [BK][BN].  Waves 2 (M) x 4 (N), each 64x32.  A lane
+// reads one float2 of the c.H tile per k: its two values are row 2i and 2i+1 of
+// the wave's 64 rows, feeding MFMA block 0 and block 1, so MFMA row i of block
+// bi is tile row 2i+bi.  Half-wave kg takes slab rows 2s+kg.  The H loads are
+// issued raw ahead of the MFMAs; the row scale c and the db sums are applied
+// when the registers are written to LDS.
 // ---------------------------------------------------------------------------
 template <int BK>
-__global__ __launch_bounds__(kBlock) void k_dw_adam_f32(
+__global__ __launch_bounds__(kGemm) void k_dw_adam_f32(
     const float *__restrict__ Hm, const float *__restrict__ cvec, const float *__restrict__ Xh,
     int M, int N, int K, float *__restrict__ W, float *__restrict__ mW, float *__restrict__ vW,
     uint16_t *__restrict__ Wb, float *__restrict__ bvec, float *__restrict__ mb,
-    float *__restrict__ vb, AdamArgs ad) {
+    float *__restrict__ vb, AdamArgs ad, LossFinish lf) {
   constexpr int BM = 128, BN = 128;
-  constexpr int LDM = BM + 32, LDN = BN + 32;
-  constexpr int MF4 = BM / 4, NF4 = BN / 4;
-  constexpr int A_LD = BK * MF4 / kBlock, B_LD = BK * NF4 / kBlock;
-  constexpr int RG = kBlock / MF4;  // row groups of the staging layout
-  static_assert(A_LD * kBlock == BK * MF4 && B_LD * kBlock == BK * NF4, "tile/threads");
+  constexpr int LDM = BM + 4, LDN = BN + 4;
+  constexpr int CF4 = BM / 4;            // float4 per tile row (both operands)
+  constexpr int KSTEP = kGemm / CF4;     // slab rows between a thread's loads (16)
+  constexpr int LD = BK / KSTEP;         // loads per thread per operand
+  static_assert(BM == BN && LD * KSTEP == BK, "tile/threads");
   __shared__ __attribute__((aligned(16))) float sm[2 * BK * (LDM + LDN)];
   float *As = sm;                  // [2][BK][LDM]
   float *Bs = sm + 2 * BK * LDM;   // [2][BK][LDN]
@@ -362,103 +411,94 @@ __global__ __launch_bounds__(kBlock) void k_dw_adam_f32(
   const int tn = blockIdx.x % nt, tm = blockIdx.x / nt;
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;
   const int li = lane & 31, kg = lane >> 5;
   const bool do_db = (tn == 0);
 
-  float4 ra[A_LD], rb[B_LD];
+  if (lf.loss && blockIdx.x == 0 && tid == 0) {
+    float sp = 0.f, sn = 0.f;
+    for (int i = 0; i < lf.nblk; ++i) {
+      sp += lf.lpart[2 * i];
+      sn += lf.lpart[2 * i + 1];
+    }
+    lf.loss[0] = sp / (float)lf.n_pos + sn / (float)lf.n_neg;
+  }
+
+  const int c4 = (tid % CF4) * 4, kr = tid / CF4;
+  const float *pa = Hm + (m0 + c4 < M ? m0 + c4 : 0);  // invalid columns: results never stored
+  const float *pb = Xh + (n0 + c4 < N ? n0 + c4 : 0);
+  // Loaded values are only consumed when written to LDS (scaled by c, masked
+  // past K, summed into db), after the MFMAs of the current tile.
+  struct Stage {
+    float4 a[LD], b[LD];
+    float c[LD];
+    int kt;
+  };
+  Stage s0, s1;
   float4 dbp = make_float4(0.f, 0.f, 0.f, 0.f);
-  auto gload = [&](int kt) {
-    const int kb = kt * BK;
+  auto gload = [&](Stage &st, int kt) {
 #pragma unroll
-    for (int i = 0; i < A_LD; ++i) {
-      const int idx = tid + i * kBlock, k = idx / MF4, c4 = (idx % MF4) * 4;
-      const int gr = kb + k, gc = m0 + c4;
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (gr < K && gc < M) {
-        v = ld4(Hm + (size_t)gr * M + gc);
-        const float cc = cvec[gr];
-        v.x *= cc;
-        v.y *= cc;
-        v.z *= cc;
-        v.w *= cc;
-      }
-      ra[i] = v;
+    for (int i = 0; i < LD; ++i) {
+      const int k = min(kt * BK + kr + i * KSTEP, K - 1);
+      st.a[i] = ld4(pa + (size_t)k * M);
+      st.b[i] = ld4(pb + (size_t)k * N);
+      st.c[i] = cvec[k];
+    }
+    st.kt = kt;
+  };
+  auto sstore = [&](const Stage &st, int buf) {
+#pragma unroll
+    for (int i = 0; i < LD; ++i) {
+      const float cc = st.kt * BK + kr + i * KSTEP < K ? st.c[i] : 0.f;  // rows past K add nothing
+      float4 v = st.a[i];
+      v.x *= cc;
+      v.y *= cc;
+      v.z *= cc;
+      v.w *= cc;
       if (do_db) {
         dbp.x += v.x;
         dbp.y += v.y;
         dbp.z += v.z;
         dbp.w += v.w;
       }
-    }
-#pragma unroll
-    for (int i = 0; i < B_LD; ++i) {
-      const int idx = tid + i * kBlock, k = idx / NF4, c4 = (idx % NF4) * 4;
-      const int gr = kb + k, gc = n0 + c4;
-      rb[i] = (gr < K && gc < N) ? ld4(Xh + (size_t)gr * N + gc) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < A_LD; ++i) {
-      const int idx = tid + i * kBlock, k = idx / MF4, c4 = (idx % MF4) * 4;
-      st4(As + (buf * BK + k) * LDM + c4, ra[i]);
-    }
-#pragma unroll
-    for (int i = 0; i < B_LD; ++i) {
-      const int idx = tid + i * kBlock, k = idx / NF4, c4 = (idx % NF4) * 4;
-      st4(Bs + (buf * BK + k) * LDN + c4, rb[i]);
+      st4(As + (buf * BK + kr + i * KSTEP) * LDM + c4, v);
+      st4(Bs + (buf * BK + kr + i * KSTEP) * LDN + c4, st.b[i]);
     }
   };
 
-  floatx16 acc[2][2];
+  floatx16 acc[2];
 #pragma unroll
   for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
-    for (int bj = 0; bj < 2; ++bj)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[bi][bj][r] = 0.f;
+    for (int r = 0; r < 16; ++r) acc[bi][r] = 0.f;
 
   auto compute = [&](int buf) {
-    const float *a0 = As + (buf * BK + kg) * LDM + wm * 64 + li;
-    const float *b0 = Bs + (buf * BK + kg) * LDN + wn * 64 + li;
+    const float *a0 = As + (buf * BK + kg) * LDM + wm * 64 + 2 * li;
+    const float *b0 = Bs + (buf * BK + kg) * LDN + wn * 32 + li;
 #pragma unroll
     for (int s = 0; s < BK / 2; ++s) {
-      const float a_0 = a0[2 * s * LDM], a_1 = a0[2 * s * LDM + 32];
-      const float b_0 = b0[2 * s * LDN], b_1 = b0[2 * s * LDN + 32];
-      acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a_0, b_0, acc[0][0], 0, 0, 0);
-      acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a_0, b_1, acc[0][1], 0, 0, 0);
-      acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a_1, b_0, acc[1][0], 0, 0, 0);
-      acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a_1, b_1, acc[1][1], 0, 0, 0);
+      const float2 a = *reinterpret_cast<const float2 *>(a0 + 2 * s * LDM);
+      const float b = b0[2 * s * LDN];
+      acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.x, b, acc[0], 0, 0, 0);
+      acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.y, b, acc[1], 0, 0, 0);
     }
   };
 
   const int nk = (K + BK - 1) / BK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
-    compute(cur);
-    if (kt + 1 < nk) sstore(cur ^ 1);
-    __syncthreads();
-  }
+  kloop<kPrefetch>(nk, gload, sstore, compute, s0, s1);
 
   // Adam on this workgroup's W tile.
-#pragma unroll
-  for (int bj = 0; bj < 2; ++bj) {
-    const int col = n0 + wn * 64 + bj * 32 + li;
-    if (col >= N) continue;
+  const int col = n0 + wn * 32 + li;
+  if (col < N) {
 #pragma unroll
     for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * 64 + acc_row(bi, r, kg);
+        const int row = m0 + wm * 64 + 2 * acc_row(r, kg) + bi;
         if (row >= M) continue;
         const size_t idx = (size_t)row * N + col;
         float p = W[idx], m = mW[idx], v = vW[idx];
-        adam_update(p, m, v, acc[bi][bj][r], ad);
+        adam_update(p, m, v, acc[bi][r], ad);
         W[idx] = p;
         mW[idx] = m;
         vW[idx] = v;
@@ -468,14 +508,13 @@ __global__ __launch_bounds__(kBlock) void k_dw_adam_f32(
 
   // db and Adam on b (column-tile 0 only).
   if (do_db) {
-    float *red = sm;  // [RG][BM]
-    const int rg = tid / MF4, c4 = (tid % MF4) * 4;
-    st4(red + rg * BM + c4, dbp);
+    float *red = sm;  // [KSTEP][BM]
+    st4(red + kr * BM + c4, dbp);
     __syncthreads();
     if (tid < BM && m0 + tid < M) {
       float s = 0.f;
 #pragma unroll
-      for (int g2 = 0; g2 < RG; ++g2) s += red[g2 * BM + tid];
+      for (int g2 = 0; g2 < KSTEP; ++g2) s += red[g2 * BM + tid];
       const int row = m0 + tid;
       float p = bvec[row], m = mb[row], v = vb[row];
       adam_update(p, m, v, s, ad);
@@ -530,6 +569,8 @@ inline unsigned cdiv(long a, long b) { return (unsigned)((a + b - 1) / b); }
 // ---------------------------------------------------------------------------
 int fwd_col_tiles(int n_cols, int /*dtype*/) { return (int)cdiv(n_cols, 128); }
 
+int loss_blocks(int rows) { return (int)cdiv(rows, kLossRows); }
+
 hipError_t launch_embed_norm(const RowMap &m, int rows, int d, float eps, bool normalise,
                              bool bf16_out, void *out, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
@@ -551,28 +592,28 @@ hipError_t launch_fwd(int dtype, const void *X, const void *W, const float *bias
   const float *x = static_cast<const float *>(X);
   const float *w = static_cast<const float *>(W);
   if (H)
-    hipLaunchKernelGGL((k_fwd_f32<32, true>), grid, dim3(kBlock), 0, s, x, w, bias, M, N, K, H,
+    hipLaunchKernelGGL((k_fwd_f32<32, true>), grid, dim3(kGemm), 0, s, x, w, bias, M, N, K, H,
                        gpart);
   else
-    hipLaunchKernelGGL((k_fwd_f32<32, false>), grid, dim3(kBlock), 0, s, x, w, bias, M, N, K, H,
+    hipLaunchKernelGGL((k_fwd_f32<32, false>), grid, dim3(kGemm), 0, s, x, w, bias, M, N, K, H,
                        gpart);
   return hipGetLastError();
 }
 
 hipError_t launch_loss(const float *gpart, int ntiles, int R, int n_pos, float theta, float *g,
-                       float *c, float *loss, hipStream_t s) {
-  hipLaunchKernelGGL(k_loss, dim3(1), dim3(1024), 0, s, gpart, ntiles, R, n_pos, theta, g, c,
-                     loss);
+                       float *c, float *lpart, hipStream_t s) {
+  hipLaunchKernelGGL(k_loss_rows, dim3(loss_blocks(R)), dim3(kLossRows), 0, s, gpart, ntiles, R,
+                     n_pos, theta, g, c, lpart);
   return hipGetLastError();
 }
 
 hipError_t launch_dw_adam(int dtype, const float *H, const float *c, const void *Xh, int M, int N,
                           int K, float *W, float *mW, float *vW, uint16_t *Wb, float *b, float *mb,
-                          float *vb, const AdamArgs &a, hipStream_t s) {
+                          float *vb, const AdamArgs &a, const LossFinish &lf, hipStream_t s) {
   if (dtype != 0) return hipErrorNotSupported;
   const dim3 grid(cdiv(M, 128) * cdiv(N, 128));
-  hipLaunchKernelGGL((k_dw_adam_f32<32>), grid, dim3(kBlock), 0, s, H, c,
-                     static_cast<const float *>(Xh), M, N, K, W, mW, vW, Wb, b, mb, vb, a);
+  hipLaunchKernelGGL((k_dw_adam_f32<32>), grid, dim3(kGemm), 0, s, H, c,
+                     static_cast<const float *>(Xh), M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf);
   return hipGetLastError();
 }
 
