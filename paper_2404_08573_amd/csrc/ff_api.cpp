@@ -112,7 +112,7 @@ void carve_step(Carver &cv, StepScratch &s, int rows, int d_in, int d_out, int d
                 bool need_g, bool need_loss) {
   s.xhat = cv.take((size_t)rows * d_in * elem_bytes(dtype));
   if (need_h) s.h = static_cast<float *>(cv.take((size_t)rows * d_out * 4));
-  s.gpart = static_cast<float *>(cv.take((size_t)ffk::fwd_col_tiles(d_out, dtype) * rows * 4));
+  s.gpart = static_cast<float *>(cv.take((size_t)ffk::fwd_col_tiles_max(d_out) * rows * 4));
   if (need_g) s.g = static_cast<float *>(cv.take((size_t)rows * 4));
   s.c = static_cast<float *>(cv.take((size_t)rows * 4));
   s.lpart = static_cast<float *>(cv.take((size_t)ffk::loss_blocks(rows) * 2 * 4));
@@ -188,7 +188,7 @@ hipError_t embed_norm(const ffk::RowMap &src, int rows, int d, float eps, bool n
 hipError_t fwd(int dtype, const void *X, const void *W, const float *bias, int M, int N, int K,
                float *H, float *gpart, hipStream_t st) {
   const double eb = (double)elem_bytes(dtype);
-  const double nt = ffk::fwd_col_tiles(N, dtype);
+  const double nt = ffk::fwd_col_tiles(M, N, dtype);
   const double bytes = (double)M * K * eb + (double)N * K * eb + N * 4.0 +
                        (H ? (double)M * N * 4.0 : 0.0) + nt * M * 4.0;
   return launch(FF_KERNEL_FORWARD, gemm_flops(M, N, K), bytes, st, [&] {
@@ -229,7 +229,7 @@ ff_status forward_core(const ff_layer *L, const ff_hparams *hp, const ffk::RowMa
   FF_HIP(fwd(hp->dtype, xop, weight_operand(L, hp->dtype), L->b, rows, L->d_out, L->d_in, h_out,
              s.gpart, st));
   if (goodness)
-    FF_HIP(goodness_sum(s.gpart, ffk::fwd_col_tiles(L->d_out, hp->dtype), rows, goodness, nullptr,
+    FF_HIP(goodness_sum(s.gpart, ffk::fwd_col_tiles(rows, L->d_out, hp->dtype), rows, goodness, nullptr,
                         0, st));
   return FF_OK;
 }
@@ -244,7 +244,7 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const ffk::RowMap &src, i
   float *H = h_out ? h_out : s.h;
   float *g = goodness ? goodness : s.g;
   float *lo = loss ? loss : s.loss;
-  const int nt = ffk::fwd_col_tiles(L->d_out, hp->dtype);
+  const int nt = ffk::fwd_col_tiles(R, L->d_out, hp->dtype);
   FF_HIP(fwd(hp->dtype, xop, weight_operand(L, hp->dtype), L->b, R, L->d_out, L->d_in, H, s.gpart,
              st));
   FF_HIP(launch(FF_KERNEL_LOSS, 0.0, (double)nt * R * 4.0 + R * (g ? 8.0 : 4.0), st, [&] {
@@ -400,7 +400,7 @@ void carve_score(Carver &cv, ScoreScratch &s, const ff_layer *layers, int n_laye
   for (int l = 0; l < n_layers; ++l) {
     max_in = std::max(max_in, layers[l].d_in);
     max_out = std::max(max_out, layers[l].d_out);
-    max_nt = std::max(max_nt, ffk::fwd_col_tiles(layers[l].d_out, dtype));
+    max_nt = std::max(max_nt, ffk::fwd_col_tiles_max(layers[l].d_out));
   }
   s.x = cv.take(rows * max_in * elem_bytes(dtype));
   s.h = static_cast<float *>(cv.take(rows * max_out * 4));
@@ -457,7 +457,7 @@ ff_status ff_score_labels(const ff_layer *layers, int32_t n_layers, int32_t firs
       FF_HIP(fwd(hp->dtype, s.x, weight_operand(L, hp->dtype), L->b, rows, L->d_out, L->d_in,
                  last ? nullptr : s.h, s.gpart, st));
       if (l >= first_scored_layer)
-        FF_HIP(goodness_sum(s.gpart, ffk::fwd_col_tiles(L->d_out, hp->dtype), rows, nullptr,
+        FF_HIP(goodness_sum(s.gpart, ffk::fwd_col_tiles(rows, L->d_out, hp->dtype), rows, nullptr,
                             S + (size_t)n0 * n_classes, l > first_scored_layer ? 1 : 0, st));
       if (!last)
         FF_HIP(embed_norm(rows_of(s.h), rows, L->d_out, hp->norm_eps, true, bf16, s.x, st));

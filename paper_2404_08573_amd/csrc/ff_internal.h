@@ -44,9 +44,11 @@ struct LossFinish {
 // Number of per-workgroup loss partial pairs for `rows` rows.
 int loss_blocks(int rows);
 
-// Row-tile and column-tile sizes of the forward product, which fix the
-// number of goodness partials per row (one per column tile).
-int fwd_col_tiles(int n_cols, int dtype);
+// Number of column tiles of the forward product on rows x n_cols, which is
+// the number of goodness partials per row (one per column tile), and its
+// upper bound over all row counts (for sizing scratch).
+int fwd_col_tiles(int rows, int n_cols, int dtype);
+int fwd_col_tiles_max(int n_cols);
 
 // Embedding (optional) + L2 normalisation (optional) into fp32 or bf16 rows.
 hipError_t launch_embed_norm(const RowMap &m, int rows, int d, float eps, bool normalise,

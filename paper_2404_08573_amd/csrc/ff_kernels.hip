@@ -23,6 +23,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "ff_internal.h"
 
 namespace ffk {
@@ -139,14 +141,18 @@ __global__ __launch_bounds__(kBlock) void k_embed_norm(RowMap m, int rows, int d
 }
 
 // ---------------------------------------------------------------------------
-// Goodness row reduction of a wave's 64-row accumulator tile held as two
-// 32x32 MFMA blocks.  v[q], q = bi*16 + r, holds this lane's partial (over its
-// columns) for accumulator row (bi, r).  A reduce-scatter butterfly over the 32
-// lanes of each half-wave leaves lane l with the full sum of entry q = l & 31.
+// Reduce-scatter of NV per-lane values over the 32 lanes of each half-wave
+// (butterfly: at each step a lane keeps one half of its array and adds the
+// partner's copy of that half).  On return, for NV >= 32, lane l holds in
+// v[j], j < NV/32, the full sum of entry j + (NV/32)*(l & 31); for NV == 16
+// it holds in v[0] the sum of entry (l & 31) >> 1 (lanes l and l^1 agree).
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ float rowsum_scatter32(float (&v)[32], int lane) {
+template <int NV>
+__device__ __forceinline__ void rowsum_scatter(float (&v)[NV], int lane) {
+  static_assert(NV == 16 || NV == 32 || NV == 64, "16, 32 or 64 values");
+  constexpr int kSteps = NV == 16 ? 4 : 5;
 #pragma unroll
-  for (int o = 16, half = 16; o >= 1; o >>= 1, half >>= 1) {
+  for (int st = 0, o = 16, half = NV / 2; st < kSteps; ++st, o >>= 1, half >>= 1) {
     const bool hi = (lane & o) != 0;
 #pragma unroll
     for (int q = 0; q < half; ++q) {
@@ -155,7 +161,7 @@ __device__ __forceinline__ float rowsum_scatter32(float (&v)[32], int lane) {
       v[q] = keep + __shfl_xor(send, o);
     }
   }
-  return v[0];
+  if (NV == 16) v[0] += __shfl_xor(v[0], 1);
 }
 
 // Row (within a 32x32 block) of accumulator register r held by a lane of
@@ -163,82 +169,67 @@ __device__ __forceinline__ float rowsum_scatter32(float (&v)[32], int lane) {
 // 8*(r/4) + 4*kg + r%4 in register r (column = lane % 32).
 __device__ __forceinline__ int acc_row(int r, int kg) { return 8 * (r >> 2) + 4 * kg + (r & 3); }
 
-// Software pipeline over nk k-tiles: LDS is double-buffered and the global
-// loads run two tiles ahead in two register stages, so a load has two tiles'
-// worth of MFMA work to land.  Tile t lives in LDS buffer t%2; the loop is
-// unrolled by two so the register stages are fixed.  Every LDS buffer is
-// rewritten only after the barrier that ends the computation reading it.
-template <class Load, class Store, class Compute, class Stage>
-__device__ __forceinline__ void kloop2(int nk, Load &gload, Store &sstore, Compute &compute,
-                                       Stage &s0, Stage &s1) {
-  gload(s0, 0);
-  if (nk > 1) gload(s1, 1);
-  sstore(s0, 0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; kt += 2) {
-    if (kt + 2 < nk) gload(s0, kt + 2);
-    compute(0);
-    if (kt + 1 < nk) sstore(s1, 1);
-    __syncthreads();
-    if (kt + 1 >= nk) break;
-    if (kt + 3 < nk) gload(s1, kt + 3);
-    compute(1);
-    if (kt + 2 < nk) sstore(s0, 0);
-    __syncthreads();
+// V consecutive floats from LDS (V = 1, 2 or 4) as an array.
+template <int V>
+__device__ __forceinline__ void lds_vec(const float *p, float (&out)[V]) {
+  if constexpr (V == 4) {
+    const float4 t = ld4(p);
+    out[0] = t.x;
+    out[1] = t.y;
+    out[2] = t.z;
+    out[3] = t.w;
+  } else if constexpr (V == 2) {
+    const float2 t = *reinterpret_cast<const float2 *>(p);
+    out[0] = t.x;
+    out[1] = t.y;
+  } else {
+    out[0] = p[0];
   }
 }
 
-// One register stage: the loads of tile t+1 are issued before the MFMAs of
-// tile t and written to the other LDS buffer after them.
+// Software pipeline over nk k-tiles with double-buffered LDS: the loads of
+// tile t+1 are issued before the MFMAs of tile t and written to the other LDS
+// buffer after them (load results are consumed only there, so the loads
+// overlap the MFMAs).  Each LDS buffer is rewritten only after the barrier
+// that ends the computation reading it.
 template <class Load, class Store, class Compute, class Stage>
-__device__ __forceinline__ void kloop1(int nk, Load &gload, Store &sstore, Compute &compute,
-                                       Stage &s0) {
-  gload(s0, 0);
-  sstore(s0, 0);
+__device__ __forceinline__ void kloop(int nk, Load &gload, Store &sstore, Compute &compute,
+                                      Stage &st) {
+  gload(st, 0);
+  sstore(st, 0);
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) gload(s0, kt + 1);
+    if (kt + 1 < nk) gload(st, kt + 1);
     compute(kt & 1);
-    if (kt + 1 < nk) sstore(s0, (kt + 1) & 1);
+    if (kt + 1 < nk) sstore(st, (kt + 1) & 1);
     __syncthreads();
   }
 }
-
-template <int PF, class Load, class Store, class Compute, class Stage>
-__device__ __forceinline__ void kloop(int nk, Load &gload, Store &sstore, Compute &compute,
-                                      Stage &s0, Stage &s1) {
-  if constexpr (PF == 2)
-    kloop2(nk, gload, sstore, compute, s0, s1);
-  else
-    kloop1(nk, gload, sstore, compute, s0);
-}
-
-constexpr int kPrefetch = 1;  // register stages of the GEMM pipelines
-
-constexpr int kGemm = 512;  // 8 waves: two per SIMD, so one wave's LDS/global waits hide behind the other's MFMAs
 
 // ---------------------------------------------------------------------------
 // Forward: H = relu(X W^T + b), gpart[tn][row] = sum over the tile's columns of H^2.
-// X [M][K], W [N][K] (both K-contiguous), fp32.  Tile 128x128; waves 2 (M) x 4 (N),
-// each 64x32 as two v_mfma_f32_32x32x2f32 blocks.  Within a BK slab the two
-// half-waves take the two halves of the slab's k range, so every lane reads
-// contiguous float4 runs from LDS for both operands (the k order inside the
-// contraction is a permutation of the plain order, the same for X and W).
-// Loads are branch-free: out-of-range rows read a clamped valid row whose
-// results are never stored; the k tail is zeroed.
+// X [M][K], W [N][K] (both K-contiguous), fp32.  Tile BM x BN, WM x WN waves,
+// each (BM/WM) x (BN/WN) as 32x32 v_mfma_f32_32x32x2f32 blocks.  Within a BK
+// slab the two half-waves take the two halves of the slab's k range, so every
+// lane reads contiguous float4 runs from LDS for both operands (the k order
+// inside the contraction is a permutation of the plain order, the same for X
+// and W).  Loads are branch-free: out-of-range rows read a clamped valid row
+// whose results are never stored; the k tail is zeroed when written to LDS.
 // ---------------------------------------------------------------------------
-template <int BK, bool STORE_H>
-__global__ __launch_bounds__(kGemm) void k_fwd_f32(const float *__restrict__ X,
-                                                   const float *__restrict__ W,
-                                                   const float *__restrict__ bias, int M, int N,
-                                                   int K, float *__restrict__ H,
-                                                   float *__restrict__ gpart) {
-  constexpr int BM = 128, BN = 128;
+template <int BM, int BN, int BK, int WM, int WN, bool STORE_H>
+__global__ __launch_bounds__(WM *WN * 64) void k_fwd_f32(const float *__restrict__ X,
+                                                         const float *__restrict__ W,
+                                                         const float *__restrict__ bias, int M,
+                                                         int N, int K, float *__restrict__ H,
+                                                         float *__restrict__ gpart) {
+  constexpr int NT = WM * WN * 64;
+  constexpr int TM = BM / WM, TN = BN / WN, MB = TM / 32, NB = TN / 32;
   constexpr int LDK = BK + 4;   // padded row: conflict-free 16-byte reads
   constexpr int KF4 = BK / 4;   // float4 per tile row
-  constexpr int LD = BM * KF4 / kGemm;  // float4 loads per thread per operand
-  constexpr int RSTEP = kGemm / KF4;    // tile rows between a thread's loads
-  static_assert(LD * kGemm == BM * KF4, "tile/threads");
+  constexpr int LDA = BM * KF4 / NT, LDB = BN * KF4 / NT;  // float4 loads per thread
+  constexpr int RSTEP = NT / KF4;                          // tile rows between them
+  static_assert(MB * 32 == TM && NB * 32 == TN, "wave tile is whole 32x32 blocks");
+  static_assert(LDA * NT == BM * KF4 && LDB * NT == BN * KF4, "tile/threads");
   __shared__ __attribute__((aligned(16))) float sm[2 * (BM + BN) * LDK];
   float *As = sm;                 // [2][BM][LDK]
   float *Bs = sm + 2 * BM * LDK;  // [2][BN][LDK]
@@ -247,93 +238,117 @@ __global__ __launch_bounds__(kGemm) void k_fwd_f32(const float *__restrict__ X,
   const int tn = blockIdx.x % nt, tm = blockIdx.x / nt;
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wm = wave / WN, wn = wave % WN;
   const int li = lane & 31, kg = lane >> 5;
 
   const int srow = tid / KF4, kc = (tid % KF4) * 4;
-  const float *pa[LD];
-  const float *pb[LD];
+  const float *pa[LDA];
+  const float *pb[LDB];
 #pragma unroll
-  for (int i = 0; i < LD; ++i) {
-    pa[i] = X + (size_t)min(m0 + srow + i * RSTEP, M - 1) * K + kc;
-    pb[i] = W + (size_t)min(n0 + srow + i * RSTEP, N - 1) * K + kc;
-  }
-  // Loaded values are only consumed when written to LDS, after the MFMAs of
-  // the current tile, so the loads overlap that work (the k-tail mask is
-  // applied at that point too, never right after the load).
+  for (int i = 0; i < LDA; ++i) pa[i] = X + (size_t)min(m0 + srow + i * RSTEP, M - 1) * K + kc;
+#pragma unroll
+  for (int i = 0; i < LDB; ++i) pb[i] = W + (size_t)min(n0 + srow + i * RSTEP, N - 1) * K + kc;
+
+  // Loaded values are consumed only when written to LDS, after the MFMAs of
+  // the current tile (the k-tail mask is applied there, never right after
+  // the load, which would make the wave wait for it).
   struct Stage {
-    float4 a[LD], b[LD];
+    float4 a[LDA], b[LDB];
     int kt;
-  };
-  Stage s0, s1;
-  auto gload = [&](Stage &st, int kt) {
+  } st;
+  auto gload = [&](Stage &g, int kt) {
     const int kb = kt * BK;
     const int ko = kb + kc < K ? kb : K - 4 - kc;  // clamped to a valid address when past K
 #pragma unroll
-    for (int i = 0; i < LD; ++i) {
-      st.a[i] = ld4(pa[i] + ko);
-      st.b[i] = ld4(pb[i] + ko);
-    }
-    st.kt = kt;
+    for (int i = 0; i < LDA; ++i) g.a[i] = ld4(pa[i] + ko);
+#pragma unroll
+    for (int i = 0; i < LDB; ++i) g.b[i] = ld4(pb[i] + ko);
+    g.kt = kt;
   };
-  auto sstore = [&](const Stage &st, int buf) {
-    const bool kok = st.kt * BK + kc < K;
+  auto sstore = [&](const Stage &g, int buf) {
+    const bool kok = g.kt * BK + kc < K;
     const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-    for (int i = 0; i < LD; ++i) {
-      st4(As + (buf * BM + srow + i * RSTEP) * LDK + kc, kok ? st.a[i] : z);
-      st4(Bs + (buf * BN + srow + i * RSTEP) * LDK + kc, kok ? st.b[i] : z);
-    }
+    for (int i = 0; i < LDA; ++i)
+      st4(As + (buf * BM + srow + i * RSTEP) * LDK + kc, kok ? g.a[i] : z);
+#pragma unroll
+    for (int i = 0; i < LDB; ++i)
+      st4(Bs + (buf * BN + srow + i * RSTEP) * LDK + kc, kok ? g.b[i] : z);
   };
 
-  floatx16 acc[2];
+  floatx16 acc[MB][NB];
 #pragma unroll
-  for (int bi = 0; bi < 2; ++bi)
+  for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[bi][r] = 0.f;
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.f;
 
   auto compute = [&](int buf) {
-    const float *a0 = As + (buf * BM + wm * 64 + li) * LDK + kg * (BK / 2);
-    const float *b0 = Bs + (buf * BN + wn * 32 + li) * LDK + kg * (BK / 2);
+    const float *a0 = As + (buf * BM + wm * TM + li) * LDK + kg * (BK / 2);
+    const float *b0 = Bs + (buf * BN + wn * TN + li) * LDK + kg * (BK / 2);
 #pragma unroll
     for (int s4 = 0; s4 < BK / 2; s4 += 4) {
-      const float4 a_0 = ld4(a0 + s4), a_1 = ld4(a0 + 32 * LDK + s4), b = ld4(b0 + s4);
+      float4 a[MB], b[NB];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(comp(a_0, q), comp(b, q), acc[0], 0, 0, 0);
-        acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(comp(a_1, q), comp(b, q), acc[1], 0, 0, 0);
-      }
+      for (int mb = 0; mb < MB; ++mb) a[mb] = ld4(a0 + mb * 32 * LDK + s4);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) b[nb] = ld4(b0 + nb * 32 * LDK + s4);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(comp(a[mb], q), comp(b[nb], q),
+                                                               acc[mb][nb], 0, 0, 0);
     }
   };
 
-  const int nk = (K + BK - 1) / BK;
-  kloop<kPrefetch>(nk, gload, sstore, compute, s0, s1);
+  kloop((K + BK - 1) / BK, gload, sstore, compute, st);
 
   // Epilogue: bias, ReLU, H store, goodness partials.
-  float hsq[32];
-  const int col = n0 + wn * 32 + li;
-  const bool cok = col < N;
-  const float bv = cok ? bias[col] : 0.f;
+  float hsq[MB * 16];
 #pragma unroll
-  for (int bi = 0; bi < 2; ++bi)
+  for (int q = 0; q < MB * 16; ++q) hsq[q] = 0.f;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const float h = cok ? fmaxf(acc[bi][r] + bv, 0.f) : 0.f;
-      if (STORE_H) {
-        const int row = m0 + wm * 64 + bi * 32 + acc_row(r, kg);
-        if (row < M && cok) H[(size_t)row * N + col] = h;
+  for (int nb = 0; nb < NB; ++nb) {
+    const int col = n0 + wn * TN + nb * 32 + li;
+    const bool cok = col < N;
+    const float bv = cok ? bias[col] : 0.f;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float h = cok ? fmaxf(acc[mb][nb][r] + bv, 0.f) : 0.f;
+        if (STORE_H) {
+          const int row = m0 + wm * TM + mb * 32 + acc_row(r, kg);
+          if (row < M && cok) H[(size_t)row * N + col] = h;
+        }
+        hsq[mb * 16 + r] += h * h;
       }
-      hsq[bi * 16 + r] = h * h;
+  }
+  rowsum_scatter(hsq, lane);
+  float *gs = sm;  // [WN][BM]; the main-loop buffers are free after the last barrier
+  if constexpr (MB == 1) {
+    const int q = (lane & 31) >> 1;
+    if ((lane & 1) == 0) gs[wn * BM + wm * TM + acc_row(q, kg)] = hsq[0];
+  } else {
+#pragma unroll
+    for (int j = 0; j < MB / 2; ++j) {
+      const int q = j + (MB / 2) * (lane & 31);
+      gs[wn * BM + wm * TM + (q >> 4) * 32 + acc_row(q & 15, kg)] = hsq[j];
     }
-  const float part = rowsum_scatter32(hsq, lane);
-  const int q = lane & 31;
-  float *gs = sm;  // [4][BM]; the main-loop buffers are free after the last barrier
-  gs[wn * BM + wm * 64 + (q >> 4) * 32 + acc_row(q & 15, kg)] = part;
+  }
   __syncthreads();
-  if (tid < BM) {
-    const int row = m0 + tid;
-    if (row < M)
-      gpart[(size_t)tn * M + row] = (gs[tid] + gs[BM + tid]) + (gs[2 * BM + tid] + gs[3 * BM + tid]);
+  for (int t = tid; t < BM; t += NT) {
+    const int row = m0 + t;
+    if (row < M) {
+      float g = 0.f;
+#pragma unroll
+      for (int w = 0; w < WN; ++w) g += gs[w * BM + t];
+      gpart[(size_t)tn * M + row] = g;
+    }
   }
 }
 
@@ -384,25 +399,29 @@ __global__ __launch_bounds__(kLossRows) void k_loss_rows(const float *__restrict
 // ---------------------------------------------------------------------------
 // dW = (c.H)^T X_hat (+ db) with the Adam update fused.  M = d_out, N = d_in,
 // K = R batch rows.  Both operands arrive row-major over K (batch rows), so the
-// LDS tiles are [BK][BM] and [BK][BN].  Waves 2 (M) x 4 (N), each 64x32.  A lane
-// reads one float2 of the c.H tile per k: its two values are row 2i and 2i+1 of
-// the wave's 64 rows, feeding MFMA block 0 and block 1, so MFMA row i of block
-// bi is tile row 2i+bi.  Half-wave kg takes slab rows 2s+kg.  The H loads are
-// issued raw ahead of the MFMAs; the row scale c and the db sums are applied
-// when the registers are written to LDS.
+// LDS tiles are [BK][BM] and [BK][BN].  WM x WN waves, each (BM/WM) x (BN/WN)
+// as MB x NB 32x32 blocks.  A lane reads MB consecutive floats of the c.H tile
+// per k and feeds one to each row block, so MFMA row i of block mb is wave-tile
+// row MB*i + mb; likewise NB consecutive X_hat floats give column NB*j + nb.
+// Half-wave kg takes slab rows 2s+kg.  The loads are issued raw ahead of the
+// MFMAs; the row scale c, the k-tail mask and the db sums are applied when the
+// registers are written to LDS.
 // ---------------------------------------------------------------------------
-template <int BK>
-__global__ __launch_bounds__(kGemm) void k_dw_adam_f32(
+template <int BM, int BN, int BK, int WM, int WN>
+__global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
     const float *__restrict__ Hm, const float *__restrict__ cvec, const float *__restrict__ Xh,
     int M, int N, int K, float *__restrict__ W, float *__restrict__ mW, float *__restrict__ vW,
-    uint16_t *__restrict__ Wb, float *__restrict__ bvec, float *__restrict__ mb,
-    float *__restrict__ vb, AdamArgs ad, LossFinish lf) {
-  constexpr int BM = 128, BN = 128;
+    uint16_t *__restrict__ Wb, float *__restrict__ bvec, float *__restrict__ mbv,
+    float *__restrict__ vbv, AdamArgs ad, LossFinish lf) {
+  constexpr int NT = WM * WN * 64;
+  constexpr int TM = BM / WM, TN = BN / WN, MB = TM / 32, NB = TN / 32;
   constexpr int LDM = BM + 4, LDN = BN + 4;
-  constexpr int CF4 = BM / 4;            // float4 per tile row (both operands)
-  constexpr int KSTEP = kGemm / CF4;     // slab rows between a thread's loads (16)
-  constexpr int LD = BK / KSTEP;         // loads per thread per operand
-  static_assert(BM == BN && LD * KSTEP == BK, "tile/threads");
+  constexpr int CFA = BM / 4, CFB = BN / 4;          // float4 per tile row
+  constexpr int KSA = NT / CFA, KSB = NT / CFB;      // slab rows between a thread's loads
+  constexpr int LDA = BK / KSA, LDB = BK / KSB;      // loads per thread
+  static_assert(MB * 32 == TM && NB * 32 == TN, "wave tile is whole 32x32 blocks");
+  static_assert(LDA * KSA == BK && LDB * KSB == BK && NT % CFA == 0 && NT % CFB == 0,
+                "tile/threads");
   __shared__ __attribute__((aligned(16))) float sm[2 * BK * (LDM + LDN)];
   float *As = sm;                  // [2][BK][LDM]
   float *Bs = sm + 2 * BK * LDM;   // [2][BK][LDN]
@@ -411,7 +430,7 @@ __global__ __launch_bounds__(kGemm) void k_dw_adam_f32(
   const int tn = blockIdx.x % nt, tm = blockIdx.x / nt;
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wm = wave / WN, wn = wave % WN;
   const int li = lane & 31, kg = lane >> 5;
   const bool do_db = (tn == 0);
 
@@ -424,33 +443,34 @@ __global__ __launch_bounds__(kGemm) void k_dw_adam_f32(
     lf.loss[0] = sp / (float)lf.n_pos + sn / (float)lf.n_neg;
   }
 
-  const int c4 = (tid % CF4) * 4, kr = tid / CF4;
-  const float *pa = Hm + (m0 + c4 < M ? m0 + c4 : 0);  // invalid columns: results never stored
-  const float *pb = Xh + (n0 + c4 < N ? n0 + c4 : 0);
-  // Loaded values are only consumed when written to LDS (scaled by c, masked
-  // past K, summed into db), after the MFMAs of the current tile.
+  const int ca = (tid % CFA) * 4, ka = tid / CFA;
+  const int cb = (tid % CFB) * 4, kb = tid / CFB;
+  const float *pa = Hm + (m0 + ca < M ? m0 + ca : 0);  // invalid columns: results never stored
+  const float *pb = Xh + (n0 + cb < N ? n0 + cb : 0);
+
   struct Stage {
-    float4 a[LD], b[LD];
-    float c[LD];
+    float4 a[LDA], b[LDB];
+    float c[LDA];
     int kt;
-  };
-  Stage s0, s1;
+  } st;
   float4 dbp = make_float4(0.f, 0.f, 0.f, 0.f);
-  auto gload = [&](Stage &st, int kt) {
+  auto gload = [&](Stage &g, int kt) {
 #pragma unroll
-    for (int i = 0; i < LD; ++i) {
-      const int k = min(kt * BK + kr + i * KSTEP, K - 1);
-      st.a[i] = ld4(pa + (size_t)k * M);
-      st.b[i] = ld4(pb + (size_t)k * N);
-      st.c[i] = cvec[k];
+    for (int i = 0; i < LDA; ++i) {
+      const int k = min(kt * BK + ka + i * KSA, K - 1);
+      g.a[i] = ld4(pa + (size_t)k * M);
+      g.c[i] = cvec[k];
     }
-    st.kt = kt;
-  };
-  auto sstore = [&](const Stage &st, int buf) {
 #pragma unroll
-    for (int i = 0; i < LD; ++i) {
-      const float cc = st.kt * BK + kr + i * KSTEP < K ? st.c[i] : 0.f;  // rows past K add nothing
-      float4 v = st.a[i];
+    for (int i = 0; i < LDB; ++i)
+      g.b[i] = ld4(pb + (size_t)min(kt * BK + kb + i * KSB, K - 1) * N);
+    g.kt = kt;
+  };
+  auto sstore = [&](const Stage &g, int buf) {
+#pragma unroll
+    for (int i = 0; i < LDA; ++i) {
+      const float cc = g.kt * BK + ka + i * KSA < K ? g.c[i] : 0.f;  // rows past K add nothing
+      float4 v = g.a[i];
       v.x *= cc;
       v.y *= cc;
       v.z *= cc;
@@ -461,44 +481,52 @@ __global__ __launch_bounds__(kGemm) void k_dw_adam_f32(
         dbp.z += v.z;
         dbp.w += v.w;
       }
-      st4(As + (buf * BK + kr + i * KSTEP) * LDM + c4, v);
-      st4(Bs + (buf * BK + kr + i * KSTEP) * LDN + c4, st.b[i]);
+      st4(As + (buf * BK + ka + i * KSA) * LDM + ca, v);
     }
+#pragma unroll
+    for (int i = 0; i < LDB; ++i) st4(Bs + (buf * BK + kb + i * KSB) * LDN + cb, g.b[i]);
   };
 
-  floatx16 acc[2];
+  floatx16 acc[MB][NB];
 #pragma unroll
-  for (int bi = 0; bi < 2; ++bi)
+  for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[bi][r] = 0.f;
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.f;
 
   auto compute = [&](int buf) {
-    const float *a0 = As + (buf * BK + kg) * LDM + wm * 64 + 2 * li;
-    const float *b0 = Bs + (buf * BK + kg) * LDN + wn * 32 + li;
+    const float *a0 = As + (buf * BK + kg) * LDM + wm * TM + MB * li;
+    const float *b0 = Bs + (buf * BK + kg) * LDN + wn * TN + NB * li;
 #pragma unroll
     for (int s = 0; s < BK / 2; ++s) {
-      const float2 a = *reinterpret_cast<const float2 *>(a0 + 2 * s * LDM);
-      const float b = b0[2 * s * LDN];
-      acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.x, b, acc[0], 0, 0, 0);
-      acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.y, b, acc[1], 0, 0, 0);
+      float a[MB], b[NB];
+      lds_vec<MB>(a0 + 2 * s * LDM, a);
+      lds_vec<NB>(b0 + 2 * s * LDN, b);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[mb], b[nb], acc[mb][nb], 0, 0, 0);
     }
   };
 
-  const int nk = (K + BK - 1) / BK;
-  kloop<kPrefetch>(nk, gload, sstore, compute, s0, s1);
+  kloop((K + BK - 1) / BK, gload, sstore, compute, st);
 
   // Adam on this workgroup's W tile.
-  const int col = n0 + wn * 32 + li;
-  if (col < N) {
 #pragma unroll
-    for (int bi = 0; bi < 2; ++bi)
+  for (int nb = 0; nb < NB; ++nb) {
+    const int col = n0 + wn * TN + NB * li + nb;
+    if (col >= N) continue;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * 64 + 2 * acc_row(r, kg) + bi;
+        const int row = m0 + wm * TM + MB * acc_row(r, kg) + mb;
         if (row >= M) continue;
         const size_t idx = (size_t)row * N + col;
         float p = W[idx], m = mW[idx], v = vW[idx];
-        adam_update(p, m, v, acc[bi][r], ad);
+        adam_update(p, m, v, acc[mb][nb][r], ad);
         W[idx] = p;
         mW[idx] = m;
         vW[idx] = v;
@@ -508,19 +536,20 @@ __global__ __launch_bounds__(kGemm) void k_dw_adam_f32(
 
   // db and Adam on b (column-tile 0 only).
   if (do_db) {
-    float *red = sm;  // [KSTEP][BM]
-    st4(red + kr * BM + c4, dbp);
+    float *red = sm;  // [KSA][BM]
+    st4(red + ka * BM + ca, dbp);
     __syncthreads();
-    if (tid < BM && m0 + tid < M) {
-      float s = 0.f;
+    for (int t = tid; t < BM; t += NT) {
+      const int row = m0 + t;
+      if (row >= M) continue;
+      float sum = 0.f;
 #pragma unroll
-      for (int g2 = 0; g2 < KSTEP; ++g2) s += red[g2 * BM + tid];
-      const int row = m0 + tid;
-      float p = bvec[row], m = mb[row], v = vb[row];
-      adam_update(p, m, v, s, ad);
+      for (int g2 = 0; g2 < KSA; ++g2) sum += red[g2 * BM + t];
+      float p = bvec[row], m = mbv[row], v = vbv[row];
+      adam_update(p, m, v, sum, ad);
       bvec[row] = p;
-      mb[row] = m;
-      vb[row] = v;
+      mbv[row] = m;
+      vbv[row] = v;
     }
   }
 }
@@ -567,7 +596,27 @@ inline unsigned cdiv(long a, long b) { return (unsigned)((a + b - 1) / b); }
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
-int fwd_col_tiles(int n_cols, int /*dtype*/) { return (int)cdiv(n_cols, 128); }
+// GEMM tile configurations: (BM, BN, BK, waves along M, waves along N),
+// measured on MI355X over the layer shapes of the workloads.  A launch takes
+// the large tile when its tiles alone fill every CU, else the small one.
+template <int BM, int BN, int BK, int WM, int WN>
+struct Tile {
+  static constexpr int bm = BM, bn = BN, bk = BK, wm = WM, wn = WN, threads = WM * WN * 64;
+  static long tiles(int m, int n) { return (long)cdiv(m, BM) * cdiv(n, BN); }
+};
+constexpr int kCUs = 256;
+using FwdBig = Tile<128, 128, 32, 4, 2>;
+using FwdSmall = Tile<64, 64, 32, 2, 2>;
+using DwBig = Tile<64, 128, 32, 2, 4>;
+using DwSmall = Tile<64, 64, 32, 2, 2>;
+
+inline bool fwd_big(int M, int N) { return FwdBig::tiles(M, N) >= kCUs; }
+inline bool dw_big(int M, int N) { return DwBig::tiles(M, N) >= kCUs; }
+
+int fwd_col_tiles(int rows, int n_cols, int /*dtype*/) {
+  return (int)cdiv(n_cols, fwd_big(rows, n_cols) ? FwdBig::bn : FwdSmall::bn);
+}
+int fwd_col_tiles_max(int n_cols) { return (int)cdiv(n_cols, std::min(FwdBig::bn, FwdSmall::bn)); }
 
 int loss_blocks(int rows) { return (int)cdiv(rows, kLossRows); }
 
@@ -584,19 +633,28 @@ hipError_t launch_embed_norm(const RowMap &m, int rows, int d, float eps, bool n
   return hipGetLastError();
 }
 
+template <class T>
+void fwd_launch(const float *x, const float *w, const float *bias, int M, int N, int K, float *H,
+                float *gpart, hipStream_t s) {
+  const dim3 grid(T::tiles(M, N));
+  if (H)
+    hipLaunchKernelGGL((k_fwd_f32<T::bm, T::bn, T::bk, T::wm, T::wn, true>), grid,
+                       dim3(T::threads), 0, s, x, w, bias, M, N, K, H, gpart);
+  else
+    hipLaunchKernelGGL((k_fwd_f32<T::bm, T::bn, T::bk, T::wm, T::wn, false>), grid,
+                       dim3(T::threads), 0, s, x, w, bias, M, N, K, H, gpart);
+}
+
 hipError_t launch_fwd(int dtype, const void *X, const void *W, const float *bias, int M, int N,
                       int K, float *H, float *gpart, hipStream_t s) {
   if (M <= 0) return hipSuccess;
   if (dtype != 0) return hipErrorNotSupported;
-  const dim3 grid(cdiv(M, 128) * cdiv(N, 128));
   const float *x = static_cast<const float *>(X);
   const float *w = static_cast<const float *>(W);
-  if (H)
-    hipLaunchKernelGGL((k_fwd_f32<32, true>), grid, dim3(kGemm), 0, s, x, w, bias, M, N, K, H,
-                       gpart);
+  if (fwd_big(M, N))
+    fwd_launch<FwdBig>(x, w, bias, M, N, K, H, gpart, s);
   else
-    hipLaunchKernelGGL((k_fwd_f32<32, false>), grid, dim3(kGemm), 0, s, x, w, bias, M, N, K, H,
-                       gpart);
+    fwd_launch<FwdSmall>(x, w, bias, M, N, K, H, gpart, s);
   return hipGetLastError();
 }
 
@@ -607,13 +665,23 @@ hipError_t launch_loss(const float *gpart, int ntiles, int R, int n_pos, float t
   return hipGetLastError();
 }
 
+template <class T>
+void dw_launch(const float *H, const float *c, const float *Xh, int M, int N, int K, float *W,
+               float *mW, float *vW, uint16_t *Wb, float *b, float *mb, float *vb,
+               const AdamArgs &a, const LossFinish &lf, hipStream_t s) {
+  hipLaunchKernelGGL((k_dw_adam_f32<T::bm, T::bn, T::bk, T::wm, T::wn>), dim3(T::tiles(M, N)),
+                     dim3(T::threads), 0, s, H, c, Xh, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf);
+}
+
 hipError_t launch_dw_adam(int dtype, const float *H, const float *c, const void *Xh, int M, int N,
                           int K, float *W, float *mW, float *vW, uint16_t *Wb, float *b, float *mb,
                           float *vb, const AdamArgs &a, const LossFinish &lf, hipStream_t s) {
   if (dtype != 0) return hipErrorNotSupported;
-  const dim3 grid(cdiv(M, 128) * cdiv(N, 128));
-  hipLaunchKernelGGL((k_dw_adam_f32<32>), grid, dim3(kGemm), 0, s, H, c,
-                     static_cast<const float *>(Xh), M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf);
+  const float *x = static_cast<const float *>(Xh);
+  if (dw_big(M, N))
+    dw_launch<DwBig>(H, c, x, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
+  else
+    dw_launch<DwSmall>(H, c, x, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
   return hipGetLastError();
 }
 

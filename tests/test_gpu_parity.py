@@ -49,8 +49,10 @@ def test_embed_labels_exact(P, rows, d, C):
 
 
 # ------------------------------------------------------------------ forward
+# small shapes take the 64x64 tile, the last two the 128x128 tile (ragged in rows,
+# columns and depth)
 FWD_SHAPES = [(1, 12, 8), (130, 44, 132), (300, 200, 260), (1024, 784, 500), (257, 784, 2000),
-              (129, 2000, 136)]
+              (129, 2000, 136), (2100, 788, 2004), (2048, 2000, 2000)]
 
 
 @pytest.mark.parametrize("rows,d_in,d_out", FWD_SHAPES)
@@ -145,6 +147,13 @@ def test_step_full_size_2000x2000(P):
     x = random_matrix(50, 2048, 2000, 0, 1, 0.5)
     (W, b), = make_weights(51, (2000, 2000))
     _run_steps(P, x, 1024, W, b, 1, dict(theta=2.0, lr=0.03))
+
+
+def test_step_large_tiles_ragged(P):
+    """Both products on their large tiles, ragged in every dimension (2060 rows, 2004 wide)."""
+    x = random_matrix(52, 2060, 2004, 0, 1, 0.5)
+    (W, b), = make_weights(53, (2004, 2004))
+    _run_steps(P, x, 1031, W, b, 2, dict(theta=2.0, lr=0.01))
 
 
 def test_step_workspace_too_small_changes_nothing(P):
