@@ -191,6 +191,10 @@ def main():
     step_rows = 2 * w.n * w.n_layers
     assert torch.isfinite(trace).all().item(), "non-finite loss in the timed steps"
 
+    # whole-step algorithmic flops of the training epoch (both products of every layer step)
+    train_flops = sum(4.0 * 2 * b * di * do for (_, b) in w.chunks()
+                      for di, do in zip(w.dims[:-1], w.dims[1:]))
+    kernel_ms = sum(v["total_ms"] for v in kstats.values())
     dname = "bf16" if bf16 else "f32"
     bound, peak, punit = PEAK[dname]
     gemms = {k: v for k, v in kstats.items() if k in ("forward", "dw_adam") and v["launches"]}
@@ -226,7 +230,12 @@ def main():
                      "unit": punit, "frac": achieved / peak,
                      "traffic": traffic,
                      "avg_launch_us": ds["total_ms"] * 1e3 / ds["launches"],
-                     "launches": ds["launches"]},
+                     "launches": ds["launches"],
+                     "note": "per-launch durations include time shared with the other layers' "
+                             "streams: kernel time summed over launches is `concurrency` times "
+                             "the step's wall time"},
+        "concurrency": kernel_ms / (ms_per_step * args.steps),
+        "train_mfma_frac": train_flops / (train_ms * 1e-3) / 1e12 / peak,
         "kernels": kernels,
     }
     if not args.no_cpu_baseline:
