@@ -150,6 +150,9 @@ ff_status check_layer(const ff_layer *L, const ff_hparams *hp, bool for_update, 
     return fail(FF_ERR_INVALID_ARG, "layer %d: Adam moment buffer is NULL", idx);
   if (hp && hp->dtype == FF_BF16 && !L->W_bf16)
     return fail(FF_ERR_INVALID_ARG, "layer %d: FF_BF16 needs the W_bf16 shadow", idx);
+  if (hp && hp->dtype == FF_BF16 && L->d_in % 8)
+    return fail(FF_ERR_UNSUPPORTED, "layer %d: FF_BF16 needs d_in=%d to be a multiple of 8", idx,
+                L->d_in);
   return FF_OK;
 }
 

@@ -6,9 +6,10 @@
 // Kernels
 //   k_embed_norm   label embedding (Sec. 3 "Negative Data") + row L2 normalisation;
 //                  one wave per row, float4 loads, HBM-bound.
-//   k_fwd_f32      Z = X W^T on fp32 MFMA (v_mfma_f32_32x32x2f32), epilogue fuses
-//                  bias, ReLU, the H store and the per-row goodness partial sum over
-//                  the tile's columns (Eq. 1) through a lane butterfly and LDS.
+//   k_fwd          Z = X W^T on MFMA (v_mfma_f32_32x32x2f32 for fp32 operands,
+//                  v_mfma_f32_32x32x16_bf16 for bf16), epilogue fuses bias, ReLU, the
+//                  H store and the per-row goodness partial sum over the tile's
+//                  columns (Eq. 1) through a lane butterfly and LDS.
 //   k_loss_rows    goodness partials -> g, the per-row gradient coefficient
 //                  c_r = 2 dL/dg_r and per-workgroup sums of the Eq. 1 loss terms.
 //   k_dw_adam_f32  dW = (c.H)^T X_hat on fp32 MFMA (contraction over the batch rows),
@@ -16,6 +17,8 @@
 //                  staged rows, and the Adam update of W and b fused in the epilogue
 //                  (no split over rows, so every dW tile is final in one workgroup);
 //                  its first thread also finishes the loss scalar in a fixed order.
+//   k_dw_adam_bf16 the same on v_mfma_f32_32x32x16_bf16: the staging transposes
+//                  row-major operands into k-contiguous LDS rows in registers.
 //   k_goodness, k_argmax, k_bf16_shadow: small row/elementwise kernels.
 //
 // Every reduction runs in a fixed order, so results are bitwise reproducible
@@ -31,6 +34,7 @@ namespace ffk {
 namespace {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kBlock = 256;  // 4 waves of 64 lanes
 
@@ -38,6 +42,13 @@ __device__ __forceinline__ float4 ld4(const float *p) {
   return *reinterpret_cast<const float4 *>(p);
 }
 __device__ __forceinline__ void st4(float *p, float4 v) { *reinterpret_cast<float4 *>(p) = v; }
+__device__ __forceinline__ uint4 ld16(const void *p) { return *reinterpret_cast<const uint4 *>(p); }
+__device__ __forceinline__ void st16(void *p, uint4 v) { *reinterpret_cast<uint4 *>(p) = v; }
+__device__ __forceinline__ float4 as_f4(uint4 u) {
+  return make_float4(__uint_as_float(u.x), __uint_as_float(u.y), __uint_as_float(u.z),
+                     __uint_as_float(u.w));
+}
+__device__ __forceinline__ bf16x8 as_bf8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
 __device__ __forceinline__ float comp(const float4 &v, int q) {
   return q == 0 ? v.x : (q == 1 ? v.y : (q == 2 ? v.z : v.w));
 }
@@ -208,31 +219,50 @@ __device__ __forceinline__ void kloop(int nk, Load &gload, Store &sstore, Comput
 
 // ---------------------------------------------------------------------------
 // Forward: H = relu(X W^T + b), gpart[tn][row] = sum over the tile's columns of H^2.
-// X [M][K], W [N][K] (both K-contiguous), fp32.  Tile BM x BN, WM x WN waves,
-// each (BM/WM) x (BN/WN) as 32x32 v_mfma_f32_32x32x2f32 blocks.  Within a BK
-// slab the two half-waves take the two halves of the slab's k range, so every
-// lane reads contiguous float4 runs from LDS for both operands (the k order
-// inside the contraction is a permutation of the plain order, the same for X
-// and W).  Loads are branch-free: out-of-range rows read a clamped valid row
-// whose results are never stored; the k tail is zeroed when written to LDS.
+// X [M][K], W [N][K] (both K-contiguous), fp32 or bf16 operands, fp32
+// accumulation.  Tile BM x BN, WM x WN waves, each (BM/WM) x (BN/WN) as 32x32
+// MFMA blocks: v_mfma_f32_32x32x2f32 (one fp32 per lane per instruction) or
+// v_mfma_f32_32x32x16_bf16 (eight bf16 per lane).  Within a BK slab the two
+// half-waves take the two halves of the slab's k range, so every lane reads
+// contiguous 16-byte runs from LDS for both operands (the k order inside the
+// contraction is a permutation of the plain order, the same for X and W).
+// Loads are branch-free: out-of-range rows read a clamped valid row whose
+// results are never stored; the k tail is zeroed when written to LDS.  BK is
+// in elements; K must be a multiple of the 16-byte vector (4 fp32 / 8 bf16).
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int BK, int WM, int WN, bool STORE_H>
-__global__ __launch_bounds__(WM *WN * 64) void k_fwd_f32(const float *__restrict__ X,
-                                                         const float *__restrict__ W,
-                                                         const float *__restrict__ bias, int M,
-                                                         int N, int K, float *__restrict__ H,
-                                                         float *__restrict__ gpart) {
+template <bool BF16>
+struct Operand;
+template <>
+struct Operand<false> {
+  using T = float;
+  static constexpr int kVec = 4;  // elements per 16 bytes
+};
+template <>
+struct Operand<true> {
+  using T = uint16_t;  // bf16 bits
+  static constexpr int kVec = 8;
+};
+
+template <bool BF16, int BM, int BN, int BK, int WM, int WN, bool STORE_H>
+__global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16>::T *__restrict__ X,
+                                                     const typename Operand<BF16>::T *__restrict__ W,
+                                                     const float *__restrict__ bias, int M, int N,
+                                                     int K, float *__restrict__ H,
+                                                     float *__restrict__ gpart) {
+  using T = typename Operand<BF16>::T;
+  constexpr int VE = Operand<BF16>::kVec;
   constexpr int NT = WM * WN * 64;
   constexpr int TM = BM / WM, TN = BN / WN, MB = TM / 32, NB = TN / 32;
-  constexpr int LDK = BK + 4;   // padded row: conflict-free 16-byte reads
-  constexpr int KF4 = BK / 4;   // float4 per tile row
-  constexpr int LDA = BM * KF4 / NT, LDB = BN * KF4 / NT;  // float4 loads per thread
-  constexpr int RSTEP = NT / KF4;                          // tile rows between them
+  constexpr int LDK = BK + VE;  // rows padded by 16 bytes: conflict-free 16-byte reads
+  constexpr int KCH = BK / VE;  // 16-byte chunks per tile row
+  constexpr int LDA = BM * KCH / NT, LDB = BN * KCH / NT;  // chunk loads per thread
+  constexpr int RSTEP = NT / KCH;                          // tile rows between them
   static_assert(MB * 32 == TM && NB * 32 == TN, "wave tile is whole 32x32 blocks");
-  static_assert(LDA * NT == BM * KF4 && LDB * NT == BN * KF4, "tile/threads");
-  __shared__ __attribute__((aligned(16))) float sm[2 * (BM + BN) * LDK];
-  float *As = sm;                 // [2][BM][LDK]
-  float *Bs = sm + 2 * BM * LDK;  // [2][BN][LDK]
+  static_assert(LDA * NT == BM * KCH && LDB * NT == BN * KCH, "tile/threads");
+  static_assert((BK / 2) % VE == 0, "half slab is whole vectors");
+  __shared__ __attribute__((aligned(16))) T sm[2 * (BM + BN) * LDK];
+  T *As = sm;                 // [2][BM][LDK]
+  T *Bs = sm + 2 * BM * LDK;  // [2][BN][LDK]
 
   const int nt = (N + BN - 1) / BN;
   const int tn = blockIdx.x % nt, tm = blockIdx.x / nt;
@@ -241,9 +271,9 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd_f32(const float *__restrict
   const int wm = wave / WN, wn = wave % WN;
   const int li = lane & 31, kg = lane >> 5;
 
-  const int srow = tid / KF4, kc = (tid % KF4) * 4;
-  const float *pa[LDA];
-  const float *pb[LDB];
+  const int srow = tid / KCH, kc = (tid % KCH) * VE;
+  const T *pa[LDA];
+  const T *pb[LDB];
 #pragma unroll
   for (int i = 0; i < LDA; ++i) pa[i] = X + (size_t)min(m0 + srow + i * RSTEP, M - 1) * K + kc;
 #pragma unroll
@@ -253,27 +283,27 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd_f32(const float *__restrict
   // the current tile (the k-tail mask is applied there, never right after
   // the load, which would make the wave wait for it).
   struct Stage {
-    float4 a[LDA], b[LDB];
+    uint4 a[LDA], b[LDB];
     int kt;
   } st;
   auto gload = [&](Stage &g, int kt) {
     const int kb = kt * BK;
-    const int ko = kb + kc < K ? kb : K - 4 - kc;  // clamped to a valid address when past K
+    const int ko = kb + kc < K ? kb : K - VE - kc;  // clamped to a valid address when past K
 #pragma unroll
-    for (int i = 0; i < LDA; ++i) g.a[i] = ld4(pa[i] + ko);
+    for (int i = 0; i < LDA; ++i) g.a[i] = ld16(pa[i] + ko);
 #pragma unroll
-    for (int i = 0; i < LDB; ++i) g.b[i] = ld4(pb[i] + ko);
+    for (int i = 0; i < LDB; ++i) g.b[i] = ld16(pb[i] + ko);
     g.kt = kt;
   };
   auto sstore = [&](const Stage &g, int buf) {
     const bool kok = g.kt * BK + kc < K;
-    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+    const uint4 z = make_uint4(0u, 0u, 0u, 0u);
 #pragma unroll
     for (int i = 0; i < LDA; ++i)
-      st4(As + (buf * BM + srow + i * RSTEP) * LDK + kc, kok ? g.a[i] : z);
+      st16(As + (buf * BM + srow + i * RSTEP) * LDK + kc, kok ? g.a[i] : z);
 #pragma unroll
     for (int i = 0; i < LDB; ++i)
-      st4(Bs + (buf * BN + srow + i * RSTEP) * LDK + kc, kok ? g.b[i] : z);
+      st16(Bs + (buf * BN + srow + i * RSTEP) * LDK + kc, kok ? g.b[i] : z);
   };
 
   floatx16 acc[MB][NB];
@@ -285,23 +315,32 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd_f32(const float *__restrict
       for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.f;
 
   auto compute = [&](int buf) {
-    const float *a0 = As + (buf * BM + wm * TM + li) * LDK + kg * (BK / 2);
-    const float *b0 = Bs + (buf * BN + wn * TN + li) * LDK + kg * (BK / 2);
+    const T *a0 = As + (buf * BM + wm * TM + li) * LDK + kg * (BK / 2);
+    const T *b0 = Bs + (buf * BN + wn * TN + li) * LDK + kg * (BK / 2);
 #pragma unroll
-    for (int s4 = 0; s4 < BK / 2; s4 += 4) {
-      float4 a[MB], b[NB];
+    for (int sv = 0; sv < BK / 2; sv += VE) {
+      uint4 a[MB], b[NB];
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) a[mb] = ld4(a0 + mb * 32 * LDK + s4);
+      for (int mb = 0; mb < MB; ++mb) a[mb] = ld16(a0 + mb * 32 * LDK + sv);
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) b[nb] = ld4(b0 + nb * 32 * LDK + s4);
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
+      for (int nb = 0; nb < NB; ++nb) b[nb] = ld16(b0 + nb * 32 * LDK + sv);
+      if constexpr (BF16) {
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb)
-            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(comp(a[mb], q), comp(b[nb], q),
-                                                               acc[mb][nb], 0, 0, 0);
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf8(a[mb]), as_bf8(b[nb]),
+                                                                  acc[mb][nb], 0, 0, 0);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+              acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                  comp(as_f4(a[mb]), q), comp(as_f4(b[nb]), q), acc[mb][nb], 0, 0, 0);
+      }
     }
   };
 
@@ -329,7 +368,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd_f32(const float *__restrict
       }
   }
   rowsum_scatter(hsq, lane);
-  float *gs = sm;  // [WN][BM]; the main-loop buffers are free after the last barrier
+  float *gs = reinterpret_cast<float *>(sm);  // [WN][BM]; the main-loop buffers are free now
   if constexpr (MB == 1) {
     const int q = (lane & 31) >> 1;
     if ((lane & 1) == 0) gs[wn * BM + wm * TM + acc_row(q, kg)] = hsq[0];
@@ -555,6 +594,229 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
 }
 
 // ---------------------------------------------------------------------------
+// bf16 dW = bf16(c.H)^T X_hat (+ db from the fp32 c.H) with the Adam update
+// fused.  M = d_out, N = d_in, K = R batch rows; H fp32 [K][M], X_hat bf16
+// [K][N].  v_mfma_f32_32x32x16_bf16 takes eight k-consecutive values per lane,
+// so the staging transposes: a thread loads an 8-row x 4-column block of each
+// operand (rows = batch rows), scales the H rows by c in fp32 (summing db
+// there), rounds to bf16, and writes four k-contiguous 16-byte rows to LDS.
+// LDS row p of an operand tile holds tile column 4*(p % G) + p / G (G = tile
+// width / 4), so the 32 threads that write one instruction's rows hit 32
+// consecutive rows (conflict-free) and the MFMA lanes read consecutive rows.
+// The epilogue writes the accumulators to an LDS tile in natural order, then
+// applies Adam with coalesced float4 accesses to W and its moments.
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int BK, int WM, int WN>
+__global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_bf16(
+    const float *__restrict__ Hm, const float *__restrict__ cvec,
+    const uint16_t *__restrict__ Xh, int M, int N, int K, float *__restrict__ W,
+    float *__restrict__ mW, float *__restrict__ vW, uint16_t *__restrict__ Wb,
+    float *__restrict__ bvec, float *__restrict__ mbv, float *__restrict__ vbv, AdamArgs ad,
+    LossFinish lf) {
+  constexpr int NT = WM * WN * 64;
+  constexpr int TM = BM / WM, TN = BN / WN, MB = TM / 32, NB = TN / 32;
+  constexpr int LDK = BK + 8;               // bf16 elements; rows padded by 16 bytes
+  constexpr int GA = BM / 4, GB = BN / 4;   // 4-column groups per tile
+  constexpr int KB8 = BK / 8;               // 8-row groups per slab
+  constexpr int APT = GA * KB8 / NT, BPT = GB * KB8 / NT;  // staging blocks per thread
+  constexpr int LDC = BN + 4;
+  static_assert(MB * 32 == TM && NB * 32 == TN, "wave tile is whole 32x32 blocks");
+  static_assert(APT * NT == GA * KB8 && BPT * NT == GB * KB8, "tile/threads");
+  static_assert(NT % GA == 0 && NT % GB == 0 && (BK / 2) % 8 == 0, "staging layout");
+  constexpr int kMainFloats = (2 * (BM + BN) * LDK) / 2;
+  constexpr int kSmFloats = kMainFloats > BM * LDC ? kMainFloats : BM * LDC;
+  __shared__ __attribute__((aligned(16))) float smf[kSmFloats];
+  uint16_t *As = reinterpret_cast<uint16_t *>(smf);  // [2][BM][LDK]
+  uint16_t *Bs = As + 2 * BM * LDK;                  // [2][BN][LDK]
+
+  const int nt = (N + BN - 1) / BN;
+  const int tn = blockIdx.x % nt, tm = blockIdx.x / nt;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int li = lane & 31, kg = lane >> 5;
+  const bool do_db = (tn == 0);
+
+  if (lf.loss && blockIdx.x == 0 && tid == 0) {
+    float sp = 0.f, sn = 0.f;
+    for (int i = 0; i < lf.nblk; ++i) {
+      sp += lf.lpart[2 * i];
+      sn += lf.lpart[2 * i + 1];
+    }
+    lf.loss[0] = sp / (float)lf.n_pos + sn / (float)lf.n_neg;
+  }
+
+  // Column groups are fixed per thread (NT is a multiple of the group counts).
+  // Groups past the matrix edge read a clamped valid group whose results are
+  // never stored.
+  const int ga = tid % GA, gb = tid % GB;
+  const float *pa = Hm + min(m0 + 4 * ga, M - 4);
+  const uint16_t *pb = Xh + min(n0 + 4 * gb, N - 4);
+
+  struct Stage {
+    float4 a[APT][8];
+    float c[APT][8];
+    uint2 b[BPT][8];
+    int kt;
+  } st;
+  float4 dbp = make_float4(0.f, 0.f, 0.f, 0.f);
+  auto gload = [&](Stage &g, int kt) {
+#pragma unroll
+    for (int i = 0; i < APT; ++i) {
+      const int k0 = kt * BK + 8 * ((tid + i * NT) / GA);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int k = min(k0 + j, K - 1);
+        g.a[i][j] = ld4(pa + (size_t)k * M);
+        g.c[i][j] = cvec[k];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < BPT; ++i) {
+      const int k0 = kt * BK + 8 * ((tid + i * NT) / GB);
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        g.b[i][j] = *reinterpret_cast<const uint2 *>(pb + (size_t)min(k0 + j, K - 1) * N);
+    }
+    g.kt = kt;
+  };
+  auto sstore = [&](const Stage &g, int buf) {
+#pragma unroll
+    for (int i = 0; i < APT; ++i) {
+      const int kb = (tid + i * NT) / GA;
+      const int k0 = g.kt * BK + 8 * kb;
+      float4 v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float cc = k0 + j < K ? g.c[i][j] : 0.f;  // rows past K add nothing
+        v[j] = make_float4(g.a[i][j].x * cc, g.a[i][j].y * cc, g.a[i][j].z * cc,
+                           g.a[i][j].w * cc);
+        if (do_db) {
+          dbp.x += v[j].x;
+          dbp.y += v[j].y;
+          dbp.z += v[j].z;
+          dbp.w += v[j].w;
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {  // tile column 4*ga + q, eight k values
+        uint4 row;
+        row.x = bf16_bits(comp(v[0], q)) | (bf16_bits(comp(v[1], q)) << 16);
+        row.y = bf16_bits(comp(v[2], q)) | (bf16_bits(comp(v[3], q)) << 16);
+        row.z = bf16_bits(comp(v[4], q)) | (bf16_bits(comp(v[5], q)) << 16);
+        row.w = bf16_bits(comp(v[6], q)) | (bf16_bits(comp(v[7], q)) << 16);
+        st16(As + (buf * BM + q * GA + ga) * LDK + 8 * kb, row);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < BPT; ++i) {
+      const int kb = (tid + i * NT) / GB;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {  // tile column 4*gb + q: the q-th bf16 of each row
+        const int sh = (q & 1) * 16;
+        uint32_t e[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) e[j] = ((q < 2 ? g.b[i][j].x : g.b[i][j].y) >> sh) & 0xFFFFu;
+        uint4 row;
+        row.x = e[0] | (e[1] << 16);
+        row.y = e[2] | (e[3] << 16);
+        row.z = e[4] | (e[5] << 16);
+        row.w = e[6] | (e[7] << 16);
+        st16(Bs + (buf * BN + q * GB + gb) * LDK + 8 * kb, row);
+      }
+    }
+  };
+
+  floatx16 acc[MB][NB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.f;
+
+  auto compute = [&](int buf) {
+    const uint16_t *a0 = As + (buf * BM + wm * TM + li) * LDK + kg * (BK / 2);
+    const uint16_t *b0 = Bs + (buf * BN + wn * TN + li) * LDK + kg * (BK / 2);
+#pragma unroll
+    for (int sv = 0; sv < BK / 2; sv += 8) {
+      uint4 a[MB], b[NB];
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) a[mb] = ld16(a0 + mb * 32 * LDK + sv);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) b[nb] = ld16(b0 + nb * 32 * LDK + sv);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf8(a[mb]), as_bf8(b[nb]),
+                                                                acc[mb][nb], 0, 0, 0);
+    }
+  };
+
+  kloop((K + BK - 1) / BK, gload, sstore, compute, st);
+
+  // Accumulators to a natural-order LDS tile (undoing the row permutation).
+  float *Cs = smf;  // [BM][LDC]; the main-loop buffers are free after the last barrier
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int q = wn * TN + nb * 32 + li;
+      const int n = 4 * (q % GB) + q / GB;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int p = wm * TM + mb * 32 + acc_row(r, kg);
+        Cs[(4 * (p % GA) + p / GA) * LDC + n] = acc[mb][nb][r];
+      }
+    }
+  __syncthreads();
+
+  // Adam on the tile, float4 along d_in.
+  for (int idx = tid; idx < BM * (BN / 4); idx += NT) {
+    const int m = idx / (BN / 4), n4 = (idx % (BN / 4)) * 4;
+    const int row = m0 + m, col = n0 + n4;
+    if (row >= M || col >= N) continue;
+    const size_t o = (size_t)row * N + col;
+    const float4 g4 = ld4(Cs + m * LDC + n4);
+    float4 p = ld4(W + o), m4 = ld4(mW + o), v4 = ld4(vW + o);
+    adam_update(p.x, m4.x, v4.x, g4.x, ad);
+    adam_update(p.y, m4.y, v4.y, g4.y, ad);
+    adam_update(p.z, m4.z, v4.z, g4.z, ad);
+    adam_update(p.w, m4.w, v4.w, g4.w, ad);
+    st4(W + o, p);
+    st4(mW + o, m4);
+    st4(vW + o, v4);
+    if (Wb) {
+      uint2 sh;
+      sh.x = bf16_bits(p.x) | (bf16_bits(p.y) << 16);
+      sh.y = bf16_bits(p.z) | (bf16_bits(p.w) << 16);
+      *reinterpret_cast<uint2 *>(Wb + o) = sh;
+    }
+  }
+
+  // db and Adam on b (column-tile 0 only).
+  if (do_db) {
+    __syncthreads();  // Cs reads are done
+    float *red = smf;  // [NT / GA][BM]
+    st4(red + (tid / GA) * BM + 4 * ga, dbp);
+    __syncthreads();
+    for (int t = tid; t < BM; t += NT) {
+      const int row = m0 + t;
+      if (row >= M) continue;
+      float sum = 0.f;
+#pragma unroll
+      for (int g2 = 0; g2 < NT / GA; ++g2) sum += red[g2 * BM + t];
+      float p = bvec[row], m = mbv[row], v = vbv[row];
+      adam_update(p, m, v, sum, ad);
+      bvec[row] = p;
+      mbv[row] = m;
+      vbv[row] = v;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Small kernels
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kBlock) void k_goodness(const float *__restrict__ gpart, int nt,
@@ -596,9 +858,10 @@ inline unsigned cdiv(long a, long b) { return (unsigned)((a + b - 1) / b); }
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
-// GEMM tile configurations: (BM, BN, BK, waves along M, waves along N),
-// measured on MI355X over the layer shapes of the workloads.  A launch takes
-// the large tile when its tiles alone fill every CU, else the small one.
+// GEMM tile configurations: (BM, BN, BK in elements, waves along M, waves
+// along N), measured on MI355X over the layer shapes of the workloads.  A
+// launch takes the large tile when its tiles alone fill every CU, else the
+// small one.
 template <int BM, int BN, int BK, int WM, int WN>
 struct Tile {
   static constexpr int bm = BM, bn = BN, bk = BK, wm = WM, wn = WN, threads = WM * WN * 64;
@@ -609,14 +872,27 @@ using FwdBig = Tile<128, 128, 32, 4, 2>;
 using FwdSmall = Tile<64, 64, 32, 2, 2>;
 using DwBig = Tile<64, 128, 32, 2, 4>;
 using DwSmall = Tile<64, 64, 32, 2, 2>;
+using FwdBigBf16 = Tile<128, 128, 64, 4, 2>;
+using FwdSmallBf16 = Tile<64, 64, 64, 2, 2>;
+using DwBigBf16 = Tile<128, 128, 64, 2, 2>;
+using DwSmallBf16 = Tile<64, 64, 128, 2, 2>;
 
-inline bool fwd_big(int M, int N) { return FwdBig::tiles(M, N) >= kCUs; }
-inline bool dw_big(int M, int N) { return DwBig::tiles(M, N) >= kCUs; }
-
-int fwd_col_tiles(int rows, int n_cols, int /*dtype*/) {
-  return (int)cdiv(n_cols, fwd_big(rows, n_cols) ? FwdBig::bn : FwdSmall::bn);
+inline bool fwd_big(int M, int N, int dtype) {
+  return (dtype ? FwdBigBf16::tiles(M, N) : FwdBig::tiles(M, N)) >= kCUs;
 }
-int fwd_col_tiles_max(int n_cols) { return (int)cdiv(n_cols, std::min(FwdBig::bn, FwdSmall::bn)); }
+inline bool dw_big(int M, int N, int dtype) {
+  return (dtype ? DwBigBf16::tiles(M, N) : DwBig::tiles(M, N)) >= kCUs;
+}
+
+int fwd_col_tiles(int rows, int n_cols, int dtype) {
+  const int bn = dtype ? (fwd_big(rows, n_cols, dtype) ? FwdBigBf16::bn : FwdSmallBf16::bn)
+                       : (fwd_big(rows, n_cols, dtype) ? FwdBig::bn : FwdSmall::bn);
+  return (int)cdiv(n_cols, bn);
+}
+int fwd_col_tiles_max(int n_cols) {
+  return (int)cdiv(n_cols, std::min(std::min(FwdBig::bn, FwdSmall::bn),
+                                    std::min(FwdBigBf16::bn, FwdSmallBf16::bn)));
+}
 
 int loss_blocks(int rows) { return (int)cdiv(rows, kLossRows); }
 
@@ -633,28 +909,36 @@ hipError_t launch_embed_norm(const RowMap &m, int rows, int d, float eps, bool n
   return hipGetLastError();
 }
 
-template <class T>
-void fwd_launch(const float *x, const float *w, const float *bias, int M, int N, int K, float *H,
+template <bool BF16, class T>
+void fwd_launch(const void *x, const void *w, const float *bias, int M, int N, int K, float *H,
                 float *gpart, hipStream_t s) {
+  using E = typename Operand<BF16>::T;
   const dim3 grid(T::tiles(M, N));
+  const E *xe = static_cast<const E *>(x);
+  const E *we = static_cast<const E *>(w);
   if (H)
-    hipLaunchKernelGGL((k_fwd_f32<T::bm, T::bn, T::bk, T::wm, T::wn, true>), grid,
-                       dim3(T::threads), 0, s, x, w, bias, M, N, K, H, gpart);
+    hipLaunchKernelGGL((k_fwd<BF16, T::bm, T::bn, T::bk, T::wm, T::wn, true>), grid,
+                       dim3(T::threads), 0, s, xe, we, bias, M, N, K, H, gpart);
   else
-    hipLaunchKernelGGL((k_fwd_f32<T::bm, T::bn, T::bk, T::wm, T::wn, false>), grid,
-                       dim3(T::threads), 0, s, x, w, bias, M, N, K, H, gpart);
+    hipLaunchKernelGGL((k_fwd<BF16, T::bm, T::bn, T::bk, T::wm, T::wn, false>), grid,
+                       dim3(T::threads), 0, s, xe, we, bias, M, N, K, H, gpart);
 }
 
 hipError_t launch_fwd(int dtype, const void *X, const void *W, const float *bias, int M, int N,
                       int K, float *H, float *gpart, hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  if (dtype != 0) return hipErrorNotSupported;
-  const float *x = static_cast<const float *>(X);
-  const float *w = static_cast<const float *>(W);
-  if (fwd_big(M, N))
-    fwd_launch<FwdBig>(x, w, bias, M, N, K, H, gpart, s);
-  else
-    fwd_launch<FwdSmall>(x, w, bias, M, N, K, H, gpart, s);
+  const bool big = fwd_big(M, N, dtype);
+  if (dtype == 0) {
+    if (big)
+      fwd_launch<false, FwdBig>(X, W, bias, M, N, K, H, gpart, s);
+    else
+      fwd_launch<false, FwdSmall>(X, W, bias, M, N, K, H, gpart, s);
+  } else {
+    if (big)
+      fwd_launch<true, FwdBigBf16>(X, W, bias, M, N, K, H, gpart, s);
+    else
+      fwd_launch<true, FwdSmallBf16>(X, W, bias, M, N, K, H, gpart, s);
+  }
   return hipGetLastError();
 }
 
@@ -665,23 +949,36 @@ hipError_t launch_loss(const float *gpart, int ntiles, int R, int n_pos, float t
   return hipGetLastError();
 }
 
-template <class T>
-void dw_launch(const float *H, const float *c, const float *Xh, int M, int N, int K, float *W,
+template <bool BF16, class T>
+void dw_launch(const float *H, const float *c, const void *Xh, int M, int N, int K, float *W,
                float *mW, float *vW, uint16_t *Wb, float *b, float *mb, float *vb,
                const AdamArgs &a, const LossFinish &lf, hipStream_t s) {
-  hipLaunchKernelGGL((k_dw_adam_f32<T::bm, T::bn, T::bk, T::wm, T::wn>), dim3(T::tiles(M, N)),
-                     dim3(T::threads), 0, s, H, c, Xh, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf);
+  if constexpr (BF16)
+    hipLaunchKernelGGL((k_dw_adam_bf16<T::bm, T::bn, T::bk, T::wm, T::wn>),
+                       dim3(T::tiles(M, N)), dim3(T::threads), 0, s, H, c,
+                       static_cast<const uint16_t *>(Xh), M, N, K, W, mW, vW, Wb, b, mb, vb, a,
+                       lf);
+  else
+    hipLaunchKernelGGL((k_dw_adam_f32<T::bm, T::bn, T::bk, T::wm, T::wn>), dim3(T::tiles(M, N)),
+                       dim3(T::threads), 0, s, H, c, static_cast<const float *>(Xh), M, N, K, W,
+                       mW, vW, Wb, b, mb, vb, a, lf);
 }
 
 hipError_t launch_dw_adam(int dtype, const float *H, const float *c, const void *Xh, int M, int N,
                           int K, float *W, float *mW, float *vW, uint16_t *Wb, float *b, float *mb,
                           float *vb, const AdamArgs &a, const LossFinish &lf, hipStream_t s) {
-  if (dtype != 0) return hipErrorNotSupported;
-  const float *x = static_cast<const float *>(Xh);
-  if (dw_big(M, N))
-    dw_launch<DwBig>(H, c, x, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
-  else
-    dw_launch<DwSmall>(H, c, x, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
+  const bool big = dw_big(M, N, dtype);
+  if (dtype == 0) {
+    if (big)
+      dw_launch<false, DwBig>(H, c, Xh, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
+    else
+      dw_launch<false, DwSmall>(H, c, Xh, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
+  } else {
+    if (big)
+      dw_launch<true, DwBigBf16>(H, c, Xh, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
+    else
+      dw_launch<true, DwSmallBf16>(H, c, Xh, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
+  }
   return hipGetLastError();
 }
 

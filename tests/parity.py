@@ -12,8 +12,11 @@ fp32 path:
                     rounding-noise level can flip its update in any fp32
                     implementation); that set must be at most 1e-3 of the tensor.
   labels:           bit-exact where the oracle's top-two gap is >= 1e-4 relative.
-bf16 path (compared with the bf16-emulating oracle): goodness, scores and loss
-  within 1e-2 relative, weights ||dW||_F <= 5e-2 ||W_ref||_F.
+bf16 path (compared with the bf16-emulating oracle, which rounds the same three
+  operands): goodness, scores and loss within 1e-3 relative; activities 1e-3
+  relative + 1e-3 max|h| (an operand within fp32 rounding of a bf16 rounding
+  boundary may round differently on the two sides); weights as fp32 with 2e-3;
+  and against the fp32 oracle ||dW||_F <= 5e-2 ||W_ref||_F (the workload's bar).
 """
 import numpy as np
 
@@ -31,9 +34,16 @@ def assert_loss(l, ref, rel=1e-4):
     assert abs(float(l) - float(ref)) <= rel * abs(float(ref)), f"loss {l} vs {ref}"
 
 
-def assert_acts(h, ref, rel=1e-4):
+def assert_acts(h, ref, rel=1e-4, floor=1e-5):
+    """|dh| <= rel |h_ref| + floor max|h_ref|.
+
+    bf16 operands: a value that lies within fp32 rounding of a bf16 rounding
+    boundary can round to neighbouring bf16 values on the two sides (the device
+    computes it in fp32, the oracle in fp64); one such operand moves z by one bf16
+    ulp (2^-8 relative) of one product term, about 1e-4 of max|h| at these
+    shapes, so the bf16 tests use floor = 1e-3."""
     h = np.asarray(h, np.float64)
-    tol = rel * np.abs(ref) + 1e-5 * max(np.abs(ref).max(), 1e-30)
+    tol = rel * np.abs(ref) + floor * max(np.abs(ref).max(), 1e-30)
     bad = np.abs(h - ref) > tol
     assert not bad.any(), f"activities: {bad.sum()} of {bad.size} off, max abs err " \
                           f"{np.max(np.abs(h - ref)):.3g}"
@@ -60,13 +70,25 @@ def ill_conditioned(grads, mags):
     return flag
 
 
-def assert_weights(W, ref, grads, mags, what="W", rel=1e-3):
+def assert_weights(W, ref, grads, mags, what="W", rel=1e-3, outliers=0.0, outlier_rel=0.0):
+    """Weights after k Adam steps (see the module docstring).
+
+    `outliers` (bf16 comparisons only): the fraction of elements allowed to
+    exceed `rel`, each still within `outlier_rel`.  With bf16 operands the two
+    sides may round one operand of a gradient sum one bf16 ulp apart (the value
+    sits within fp32 rounding of a bf16 rounding boundary), which moves that sum
+    by 2^-8 of one term; Adam's per-element normalisation can turn that into a
+    weight difference above the fp32 bar for the rare elements it touches."""
     W = np.asarray(W, np.float64)
     flag = ill_conditioned(grads, mags)
     assert flag.mean() <= 1e-3, f"{what}: ill-conditioned fraction {flag.mean():.2e} > 1e-3"
-    bad = (np.abs(W - ref) > rel * np.abs(ref) + 1e-6) & ~flag
-    assert not bad.any(), f"{what}: {bad.sum()} of {bad.size} off, worst abs " \
-                          f"{np.max(np.abs(W - ref)[~flag]):.3g}"
+    err = np.abs(W - ref)
+    bad = (err > rel * np.abs(ref) + 1e-6) & ~flag
+    n_ok = int(outliers * bad.size)
+    msg = f"{what}: {bad.sum()} of {bad.size} off, worst abs {np.max(err[~flag]):.3g}"
+    assert bad.sum() <= n_ok, msg
+    if bad.any():
+        assert np.all(err[bad] <= outlier_rel * np.abs(ref[bad]) + 1e-5), msg
 
 
 def decided(S_ref, rel=1e-4):

@@ -278,3 +278,96 @@ def test_tiny_config_end_to_end(P):
     assert_goodness(_np(S), S_ref, rel=1e-3, what="scores after training")
     n_dec = assert_labels(_np(pred), S_ref, p_ref)
     assert n_dec >= 0.9 * w.n
+
+
+# ------------------------------------------------------------------ bf16 operands
+BF16_FWD_SHAPES = [(1, 16, 8), (300, 200, 260), (2048, 784, 2000), (2100, 2000, 2004)]
+
+
+@pytest.mark.parametrize("rows,d_in,d_out", BF16_FWD_SHAPES)
+def test_forward_parity_bf16(P, rows, d_in, d_out):
+    x = random_matrix(rows + 3 * d_in, rows, d_in, 0, 1, 0.6)
+    (W, b), = make_weights(d_out + 5, (d_in, d_out))
+    b = b + np.linspace(-0.02, 0.03, d_out).astype(np.float32)
+    L = P.Layer(_t(W), _t(b), bf16_shadow=True)
+    h = torch.empty(rows, d_out, device=DEV)
+    g = torch.empty(rows, device=DEV)
+    P.ff_layer_forward(L, P.HParams(dtype=P.FF_BF16), _t(x), h_out=h, goodness=g)
+    _, _, h_ref, g_ref = O.layer_forward(W, b, x, 1e-8, bf16=True)
+    assert_goodness(_np(g), g_ref, rel=1e-3)
+    assert_acts(_np(h), h_ref, rel=1e-3, floor=1e-3)
+
+
+def _run_steps_bf16(P, x, n_pos, W, b, k, hp_kw):
+    hp = P.HParams(dtype=P.FF_BF16, **hp_kw)
+    ohp = O.HParams(bf16=True, **hp_kw)
+    L = P.Layer(_t(W), _t(b), bf16_shadow=True)
+    ref = O.Layer.from_params(W, b)
+    ref32 = O.Layer.from_params(W, b)
+    R = x.shape[0]
+    xd = _t(x.astype(np.float32))
+    g = torch.empty(R, device=DEV)
+    loss = torch.empty(1, device=DEV)
+    gW, mW = [], []
+    for _ in range(k):
+        P.ff_layer_step(L, hp, xd, n_pos, R - n_pos, goodness=g, loss=loss)
+        r = O.layer_step(ref, x, n_pos, ohp)
+        O.layer_step(ref32, x, n_pos, O.HParams(**hp_kw))
+        gW.append(r.dW)
+        mW.append(grad_magnitudes(r)[0])
+        assert_goodness(_np(g), r.g, rel=1e-3)
+        assert_loss(_np(loss)[0], r.loss, rel=1e-3)
+    assert_weights(_np(L.W), ref.W, gW, mW, "W (vs bf16-emulating oracle)", rel=2e-3,
+                   outliers=1e-5, outlier_rel=2e-2)
+    # the shadow is the rounded master
+    np.testing.assert_array_equal(
+        _np(L.W_bf16).view(np.uint16),
+        (_np(L.W).view(np.uint32).astype(np.uint64) + 0x7FFF
+         + ((_np(L.W).view(np.uint32) >> 16) & 1)).astype(np.uint32).__rshift__(16).astype(np.uint16))
+    # the workload's bar against the fp32 oracle
+    d = np.linalg.norm(_np(L.W) - ref32.W) / np.linalg.norm(ref32.W)
+    assert d <= 5e-2, f"bf16 weights vs fp32 oracle: relative error {d:.3g}"
+    return L
+
+
+@pytest.mark.parametrize("n,d_in,d_out,k", [(24, 16, 12, 2), (150, 200, 260, 3), (1024, 784, 2000, 2)])
+def test_step_parity_bf16(P, n, d_in, d_out, k):
+    x_base, y, y_neg = make_data(n + d_out, n, d_in)
+    (W, b), = make_weights(d_out + 1, (d_in, d_out))
+    _run_steps_bf16(P, _pair_rows(x_base, y, y_neg), n, W, b, k, dict(theta=2.0, lr=0.01))
+
+
+def test_step_parity_bf16_large_tiles_ragged(P):
+    x = random_matrix(54, 2060, 2008, 0, 1, 0.5)
+    (W, b), = make_weights(55, (2008, 2004))
+    _run_steps_bf16(P, x, 1031, W, b, 2, dict(theta=2.0, lr=0.01))
+
+
+def test_score_parity_bf16(P):
+    x_base, _, _ = make_data(62, 300, 64)
+    params = make_weights(63, (64, 96, 40))
+    layers = [P.Layer(_t(W), _t(b), bf16_shadow=True) for W, b in params]
+    S = torch.empty(300, 10, device=DEV)
+    _, pred = P.ff_score_labels(layers, P.HParams(dtype=P.FF_BF16), _t(x_base), 10, 0, scores=S)
+    S_ref, p_ref = O.score_labels([O.Layer.from_params(W, b) for W, b in params], x_base, 10,
+                                  O.HParams(bf16=True), 0)
+    assert_goodness(_np(S), S_ref, rel=1e-3, what="bf16 scores")
+    decided = (np.sort(S_ref, 1)[:, -1] - np.sort(S_ref, 1)[:, -2]) >= 1e-2 * np.sort(S_ref, 1)[:, -1]
+    np.testing.assert_array_equal(_np(pred)[decided], p_ref[decided])
+
+
+def test_pipeline_parity_bf16(P):
+    hp_kw = dict(theta=2.0, lr=0.01)
+    dims = (64, 96, 80)
+    x_base, y, y_neg = make_data(90, 200, 64)
+    params = make_weights(91, dims)
+    layers = [P.Layer(_t(W), _t(b), bf16_shadow=True) for W, b in params]
+    trace = torch.zeros(2, 4, device=DEV)
+    P.ff_pipeline_epoch(layers, P.HParams(dtype=P.FF_BF16, **hp_kw), _t(x_base), _t(y),
+                        _t(y_neg), 10, 50, 1, P.FF_PIPELINED, loss_trace=trace)
+    ref = [O.Layer.from_params(W, b) for W, b in params]
+    tr = O.train_pipelined(ref, x_base, y, y_neg, 10, 50, 1, O.HParams(bf16=True, **hp_kw))
+    np.testing.assert_allclose(_np(trace), tr, rtol=1e-3)
+    for L, R in zip(layers, ref):
+        d = np.linalg.norm(_np(L.W) - R.W) / np.linalg.norm(R.W)
+        assert d < 1e-3, d
