@@ -59,11 +59,16 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// fp32 -> bf16 bits, round to nearest even (inputs are finite).
-__device__ __forceinline__ uint32_t bf16_bits(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return u >> 16;
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// Two fp32 -> packed bf16 (a in the low half), round to nearest even; gfx950
+// does this in one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
+  const bf16x2_t v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
+}
+__device__ __forceinline__ uint16_t bf16_of(float a) {
+  return __builtin_bit_cast(uint16_t, (__bf16)a);
 }
 
 __device__ __forceinline__ float softplus_f(float x) {
@@ -142,8 +147,8 @@ __global__ __launch_bounds__(kBlock) void k_embed_norm(RowMap m, int rows, int d
     v.w *= scale;
     if (BF16OUT) {
       uint2 p;
-      p.x = bf16_bits(v.x) | (bf16_bits(v.y) << 16);
-      p.y = bf16_bits(v.z) | (bf16_bits(v.w) << 16);
+      p.x = pack_bf16(v.x, v.y);
+      p.y = pack_bf16(v.z, v.w);
       reinterpret_cast<uint2 *>(out)[(size_t)r * d4 + i] = p;
     } else {
       st4(reinterpret_cast<float *>(out) + (size_t)r * d + 4 * i, v);
@@ -569,7 +574,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
         W[idx] = p;
         mW[idx] = m;
         vW[idx] = v;
-        if (Wb) Wb[idx] = (uint16_t)bf16_bits(p);
+        if (Wb) Wb[idx] = bf16_of(p);
       }
   }
 
@@ -701,10 +706,10 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_bf16(
 #pragma unroll
       for (int q = 0; q < 4; ++q) {  // tile column 4*ga + q, eight k values
         uint4 row;
-        row.x = bf16_bits(comp(v[0], q)) | (bf16_bits(comp(v[1], q)) << 16);
-        row.y = bf16_bits(comp(v[2], q)) | (bf16_bits(comp(v[3], q)) << 16);
-        row.z = bf16_bits(comp(v[4], q)) | (bf16_bits(comp(v[5], q)) << 16);
-        row.w = bf16_bits(comp(v[6], q)) | (bf16_bits(comp(v[7], q)) << 16);
+        row.x = pack_bf16(comp(v[0], q), comp(v[1], q));
+        row.y = pack_bf16(comp(v[2], q), comp(v[3], q));
+        row.z = pack_bf16(comp(v[4], q), comp(v[5], q));
+        row.w = pack_bf16(comp(v[6], q), comp(v[7], q));
         st16(As + (buf * BM + q * GA + ga) * LDK + 8 * kb, row);
       }
     }
@@ -789,8 +794,8 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_bf16(
     st4(vW + o, v4);
     if (Wb) {
       uint2 sh;
-      sh.x = bf16_bits(p.x) | (bf16_bits(p.y) << 16);
-      sh.y = bf16_bits(p.z) | (bf16_bits(p.w) << 16);
+      sh.x = pack_bf16(p.x, p.y);
+      sh.y = pack_bf16(p.z, p.w);
       *reinterpret_cast<uint2 *>(Wb + o) = sh;
     }
   }
@@ -848,7 +853,7 @@ __global__ __launch_bounds__(kBlock) void k_argmax(const float *__restrict__ S, 
 __global__ __launch_bounds__(kBlock) void k_bf16_shadow(const float *__restrict__ W,
                                                         uint16_t *__restrict__ Wb, size_t count) {
   const size_t i = (size_t)blockIdx.x * kBlock + threadIdx.x;
-  if (i < count) Wb[i] = (uint16_t)bf16_bits(W[i]);
+  if (i < count) Wb[i] = bf16_of(W[i]);
 }
 
 inline unsigned cdiv(long a, long b) { return (unsigned)((a + b - 1) / b); }
