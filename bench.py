@@ -56,6 +56,72 @@ def load_traffic(kernel, workload):
         return None
 
 
+KIND_OF = [("k_fwd", "forward"), ("k_dw_adam", "dw_adam"), ("k_embed_norm", "embed_norm"),
+           ("k_loss_rows", "loss"), ("k_goodness", "goodness"), ("k_argmax", "argmax"),
+           ("k_bf16_shadow", "bf16_shadow")]
+
+
+def copy_calibration(nbytes):
+    """One plain device copy of nbytes (read nbytes, write nbytes): the reference
+    that scales the FETCH_SIZE / WRITE_SIZE counters to bytes."""
+    import torch
+    src = torch.ones(nbytes // 4, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": nbytes}))
+
+
+def _counter_per_dispatch(csv_path, counter):
+    """Mean value per dispatch of `counter`, by kernel kind and for the copy kernel."""
+    import csv
+    import collections
+    tot = collections.defaultdict(float)
+    n = collections.defaultdict(set)
+    for r in csv.DictReader(open(csv_path)):
+        if r["Counter_Name"] != counter:
+            continue
+        name = r["Kernel_Name"]
+        kind = next((k for pat, k in KIND_OF if pat in name), None)
+        if kind is None and ("copy" in name.lower() or "elementwise" in name):
+            kind = "copy"
+        if kind is None:
+            continue
+        tot[kind] += float(r["Counter_Value"])
+        n[kind].add(r["Dispatch_Id"])
+    return {k: tot[k] / len(n[k]) for k in tot}, {k: len(n[k]) for k in n}
+
+
+def _largest_dispatch(csv_path, counter):
+    """The copy run's largest single dispatch of `counter` (KiB): the calibration copy."""
+    import csv
+    return max(float(r["Counter_Value"]) for r in csv.DictReader(open(csv_path))
+               if r["Counter_Name"] == counter)
+
+
+def traffic_summary(fetch_csv, write_csv, cfetch_csv, cwrite_csv, workload, copy_bytes):
+    """HBM bytes per launch for each kernel kind, scaled by the copy calibration."""
+    f, nf = _counter_per_dispatch(fetch_csv, "FETCH_SIZE")
+    w, _ = _counter_per_dispatch(write_csv, "WRITE_SIZE")
+    kf = copy_bytes / (_largest_dispatch(cfetch_csv, "FETCH_SIZE") * 1024.0)
+    kw = copy_bytes / (_largest_dispatch(cwrite_csv, "WRITE_SIZE") * 1024.0)
+    out = {"_about": "HBM bytes per launch from rocprofv3 --pmc FETCH_SIZE and --pmc WRITE_SIZE "
+                     "(KiB per dispatch) scaled by the factor each counter reads for a plain "
+                     f"device copy of {copy_bytes} bytes; valid only for the kernel source hash",
+           "fetch_factor": kf, "write_factor": kw}
+    out[workload] = {k: {"bytes_per_launch": f[k] * 1024.0 * kf + w.get(k, 0.0) * 1024.0 * kw,
+                         "fetch_bytes_per_launch": f[k] * 1024.0 * kf,
+                         "write_bytes_per_launch": w.get(k, 0.0) * 1024.0 * kw,
+                         "dispatches": nf[k], "kernel_source_sha256_16": kernel_source_hash()}
+                     for k in f if k != "copy"}
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    old = json.load(open(path)) if os.path.exists(path) else {}
+    old.update(out)
+    json.dump(old, open(path, "w"), indent=1)
+    print(json.dumps(out, indent=1))
+
+
 def cpu_baseline(w, x_base, y, y_neg, params, sw, sx, sparams, budget_s=12.0):
     """The oracle as it stands, on a bounded sample of the same workload."""
     import numpy as np
@@ -112,7 +178,19 @@ def main():
     ap.add_argument("--workload", default="mnist_784_2000x4_pipelined")
     ap.add_argument("--score-workload", default="mnist_score_784_2000x4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, metavar="BYTES", default=0,
+                    help="run one plain device copy of BYTES (counter calibration) and exit")
+    ap.add_argument("--traffic-summary", nargs=4, metavar="CSV",
+                    help="FETCH, WRITE, copy FETCH, copy WRITE counter_collection.csv files: "
+                         "write profiles/traffic.json for --workload and exit")
+    ap.add_argument("--copy-bytes", type=int, default=1 << 30)
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
+    if args.traffic_summary:
+        traffic_summary(*args.traffic_summary, args.workload, args.copy_bytes)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this build has no multi-GPU path "
               f"(--gpus {args.gpus} requested)", file=sys.stderr)
@@ -202,6 +280,8 @@ def main():
     ds = gemms[dom]
     achieved = ds["flops"] / (ds["total_ms"] * 1e-3) / 1e12
     traffic = load_traffic(dom, w.name)
+    if traffic is not None:
+        traffic *= 1.0  # HBM bytes per launch of the dominant kernel (counter runs)
     kernels = {}
     for k, v in kstats.items():
         if not v["launches"]:

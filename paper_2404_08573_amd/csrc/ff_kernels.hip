@@ -180,6 +180,25 @@ __device__ __forceinline__ void rowsum_scatter(float (&v)[NV], int lane) {
   if (NV == 16) v[0] += __shfl_xor(v[0], 1);
 }
 
+// XCD-aware tile order.  Workgroups are dealt round-robin to the 8 XCDs, each
+// with its own L2, so consecutive workgroup ids land on different L2s.  Each
+// XCD is given a contiguous range of tiles instead, walked in groups of G row
+// panels (all column panels of a group before the next group), so the
+// workgroups sharing an L2 at a given time also share operand panels.  A
+// bijection of tile indices: results do not depend on it.
+__device__ __forceinline__ void tile_of(int bid, int mt, int nt, int &tm, int &tn) {
+  constexpr int kXcd = 8, G = 4;
+  const int T = mt * nt;
+  const int q = T / kXcd, r = T % kXcd;
+  const int x = bid % kXcd, j = bid / kXcd;
+  const int t = x * q + min(x, r) + j;
+  const int gsz = G * nt;
+  const int g = t / gsz, o = t % gsz;
+  const int rows = min(G, mt - g * G);
+  tm = g * G + o % rows;
+  tn = o / rows;
+}
+
 // Row (within a 32x32 block) of accumulator register r held by a lane of
 // half-wave kg: the v_mfma_f32_32x32x2f32 output layout puts row
 // 8*(r/4) + 4*kg + r%4 in register r (column = lane % 32).
@@ -203,22 +222,44 @@ __device__ __forceinline__ void lds_vec(const float *p, float (&out)[V]) {
   }
 }
 
-// Software pipeline over nk k-tiles with double-buffered LDS: the loads of
-// tile t+1 are issued before the MFMAs of tile t and written to the other LDS
-// buffer after them (load results are consumed only there, so the loads
-// overlap the MFMAs).  Each LDS buffer is rewritten only after the barrier
-// that ends the computation reading it.
-template <class Load, class Store, class Compute, class Stage>
+// Software pipeline over nk k-tiles with double-buffered LDS and PF register
+// stages: the loads of tile t+PF are issued before the MFMAs of tile t, and
+// tile t+1 is written from its register stage to the other LDS buffer after
+// them.  Load results are consumed only there, so each load has PF tiles of
+// MFMA work to land.  The steady-state body is straight-line code (loads and
+// LDS writes unconditional: loads past the last tile read clamped valid
+// addresses and are masked to zero, and their LDS buffer is never read), so
+// the compiler's wait counters track each stage separately instead of
+// draining every load at a control-flow join.  The loop is unrolled by
+// lcm(PF, 2) so that register stages and LDS buffers are fixed; each LDS
+// buffer is rewritten only after the barrier that ends the computation
+// reading it, and each register stage only after it has been written to LDS.
+template <int PF, class Load, class Store, class Compute, class Stage>
 __device__ __forceinline__ void kloop(int nk, Load &gload, Store &sstore, Compute &compute,
-                                      Stage &st) {
-  gload(st, 0);
-  sstore(st, 0);
+                                      Stage (&st)[PF]) {
+  constexpr int U = PF % 2 == 0 ? PF : 2 * PF;
+#pragma unroll
+  for (int j = 0; j < PF; ++j) gload(st[j], j);
+  sstore(st[0], 0);
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) gload(st, kt + 1);
-    compute(kt & 1);
-    if (kt + 1 < nk) sstore(st, (kt + 1) & 1);
-    __syncthreads();
+  int kt = 0;
+  for (; kt + U <= nk; kt += U) {
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      gload(st[j % PF], kt + j + PF);
+      compute(j % 2);
+      sstore(st[(j + 1) % PF], (j + 1) % 2);
+      __syncthreads();
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < U; ++j) {
+    if (kt + j < nk) {
+      gload(st[j % PF], kt + j + PF);
+      compute(j % 2);
+      sstore(st[(j + 1) % PF], (j + 1) % 2);
+      __syncthreads();
+    }
   }
 }
 
@@ -248,7 +289,7 @@ struct Operand<true> {
   static constexpr int kVec = 8;
 };
 
-template <bool BF16, int BM, int BN, int BK, int WM, int WN, bool STORE_H>
+template <bool BF16, int BM, int BN, int BK, int WM, int WN, int PF, bool STORE_H>
 __global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16>::T *__restrict__ X,
                                                      const typename Operand<BF16>::T *__restrict__ W,
                                                      const float *__restrict__ bias, int M, int N,
@@ -270,7 +311,8 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16
   T *Bs = sm + 2 * BM * LDK;  // [2][BN][LDK]
 
   const int nt = (N + BN - 1) / BN;
-  const int tn = blockIdx.x % nt, tm = blockIdx.x / nt;
+  int tm, tn;
+  tile_of(blockIdx.x, (M + BM - 1) / BM, nt, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
@@ -290,7 +332,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16
   struct Stage {
     uint4 a[LDA], b[LDB];
     int kt;
-  } st;
+  } st[PF];
   auto gload = [&](Stage &g, int kt) {
     const int kb = kt * BK;
     const int ko = kb + kc < K ? kb : K - VE - kc;  // clamped to a valid address when past K
@@ -349,7 +391,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16
     }
   };
 
-  kloop((K + BK - 1) / BK, gload, sstore, compute, st);
+  kloop<PF>((K + BK - 1) / BK, gload, sstore, compute, st);
 
   // Epilogue: bias, ReLU, H store, goodness partials.
   float hsq[MB * 16];
@@ -451,7 +493,7 @@ __global__ __launch_bounds__(kLossRows) void k_loss_rows(const float *__restrict
 // MFMAs; the row scale c, the k-tail mask and the db sums are applied when the
 // registers are written to LDS.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int BK, int WM, int WN>
+template <int BM, int BN, int BK, int WM, int WN, int PF>
 __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
     const float *__restrict__ Hm, const float *__restrict__ cvec, const float *__restrict__ Xh,
     int M, int N, int K, float *__restrict__ W, float *__restrict__ mW, float *__restrict__ vW,
@@ -471,7 +513,8 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
   float *Bs = sm + 2 * BK * LDM;   // [2][BK][LDN]
 
   const int nt = (N + BN - 1) / BN;
-  const int tn = blockIdx.x % nt, tm = blockIdx.x / nt;
+  int tm, tn;
+  tile_of(blockIdx.x, (M + BM - 1) / BM, nt, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
@@ -496,7 +539,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
     float4 a[LDA], b[LDB];
     float c[LDA];
     int kt;
-  } st;
+  } st[PF];
   float4 dbp = make_float4(0.f, 0.f, 0.f, 0.f);
   auto gload = [&](Stage &g, int kt) {
 #pragma unroll
@@ -555,7 +598,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
     }
   };
 
-  kloop((K + BK - 1) / BK, gload, sstore, compute, st);
+  kloop<PF>((K + BK - 1) / BK, gload, sstore, compute, st);
 
   // Adam on this workgroup's W tile.
 #pragma unroll
@@ -611,7 +654,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
 // The epilogue writes the accumulators to an LDS tile in natural order, then
 // applies Adam with coalesced float4 accesses to W and its moments.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int BK, int WM, int WN>
+template <int BM, int BN, int BK, int WM, int WN, int PF>
 __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_bf16(
     const float *__restrict__ Hm, const float *__restrict__ cvec,
     const uint16_t *__restrict__ Xh, int M, int N, int K, float *__restrict__ W,
@@ -635,7 +678,8 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_bf16(
   uint16_t *Bs = As + 2 * BM * LDK;                  // [2][BN][LDK]
 
   const int nt = (N + BN - 1) / BN;
-  const int tn = blockIdx.x % nt, tm = blockIdx.x / nt;
+  int tm, tn;
+  tile_of(blockIdx.x, (M + BM - 1) / BM, nt, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
@@ -663,7 +707,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_bf16(
     float c[APT][8];
     uint2 b[BPT][8];
     int kt;
-  } st;
+  } st[PF];
   float4 dbp = make_float4(0.f, 0.f, 0.f, 0.f);
   auto gload = [&](Stage &g, int kt) {
 #pragma unroll
@@ -759,7 +803,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_bf16(
     }
   };
 
-  kloop((K + BK - 1) / BK, gload, sstore, compute, st);
+  kloop<PF>((K + BK - 1) / BK, gload, sstore, compute, st);
 
   // Accumulators to a natural-order LDS tile (undoing the row permutation).
   float *Cs = smf;  // [BM][LDC]; the main-loop buffers are free after the last barrier
@@ -864,23 +908,24 @@ inline unsigned cdiv(long a, long b) { return (unsigned)((a + b - 1) / b); }
 // Launchers
 // ---------------------------------------------------------------------------
 // GEMM tile configurations: (BM, BN, BK in elements, waves along M, waves
-// along N), measured on MI355X over the layer shapes of the workloads.  A
-// launch takes the large tile when its tiles alone fill every CU, else the
-// small one.
-template <int BM, int BN, int BK, int WM, int WN>
+// along N, register stages of the load pipeline), measured on MI355X over
+// the layer shapes of the workloads.  A launch takes the large tile when its
+// tiles alone fill every CU, else the small one.
+template <int BM, int BN, int BK, int WM, int WN, int PF = 1>
 struct Tile {
-  static constexpr int bm = BM, bn = BN, bk = BK, wm = WM, wn = WN, threads = WM * WN * 64;
+  static constexpr int bm = BM, bn = BN, bk = BK, wm = WM, wn = WN, pf = PF,
+                       threads = WM * WN * 64;
   static long tiles(int m, int n) { return (long)cdiv(m, BM) * cdiv(n, BN); }
 };
 constexpr int kCUs = 256;
-using FwdBig = Tile<128, 128, 32, 4, 2>;
-using FwdSmall = Tile<64, 64, 32, 2, 2>;
-using DwBig = Tile<64, 128, 32, 2, 4>;
-using DwSmall = Tile<64, 64, 32, 2, 2>;
-using FwdBigBf16 = Tile<128, 128, 64, 4, 2>;
-using FwdSmallBf16 = Tile<64, 64, 64, 2, 2>;
-using DwBigBf16 = Tile<128, 128, 64, 2, 2>;
-using DwSmallBf16 = Tile<64, 64, 128, 2, 2>;
+using FwdBig = Tile<128, 128, 32, 4, 2, 2>;
+using FwdSmall = Tile<64, 64, 32, 2, 2, 2>;
+using DwBig = Tile<64, 128, 32, 2, 4, 3>;
+using DwSmall = Tile<64, 64, 32, 2, 2, 2>;
+using FwdBigBf16 = Tile<128, 128, 64, 4, 2, 2>;
+using FwdSmallBf16 = Tile<64, 64, 64, 2, 2, 2>;
+using DwBigBf16 = Tile<128, 128, 64, 2, 2, 1>;
+using DwSmallBf16 = Tile<64, 64, 128, 2, 2, 1>;
 
 inline bool fwd_big(int M, int N, int dtype) {
   return (dtype ? FwdBigBf16::tiles(M, N) : FwdBig::tiles(M, N)) >= kCUs;
@@ -922,10 +967,10 @@ void fwd_launch(const void *x, const void *w, const float *bias, int M, int N, i
   const E *xe = static_cast<const E *>(x);
   const E *we = static_cast<const E *>(w);
   if (H)
-    hipLaunchKernelGGL((k_fwd<BF16, T::bm, T::bn, T::bk, T::wm, T::wn, true>), grid,
+    hipLaunchKernelGGL((k_fwd<BF16, T::bm, T::bn, T::bk, T::wm, T::wn, T::pf, true>), grid,
                        dim3(T::threads), 0, s, xe, we, bias, M, N, K, H, gpart);
   else
-    hipLaunchKernelGGL((k_fwd<BF16, T::bm, T::bn, T::bk, T::wm, T::wn, false>), grid,
+    hipLaunchKernelGGL((k_fwd<BF16, T::bm, T::bn, T::bk, T::wm, T::wn, T::pf, false>), grid,
                        dim3(T::threads), 0, s, xe, we, bias, M, N, K, H, gpart);
 }
 
@@ -959,12 +1004,12 @@ void dw_launch(const float *H, const float *c, const void *Xh, int M, int N, int
                float *mW, float *vW, uint16_t *Wb, float *b, float *mb, float *vb,
                const AdamArgs &a, const LossFinish &lf, hipStream_t s) {
   if constexpr (BF16)
-    hipLaunchKernelGGL((k_dw_adam_bf16<T::bm, T::bn, T::bk, T::wm, T::wn>),
+    hipLaunchKernelGGL((k_dw_adam_bf16<T::bm, T::bn, T::bk, T::wm, T::wn, T::pf>),
                        dim3(T::tiles(M, N)), dim3(T::threads), 0, s, H, c,
                        static_cast<const uint16_t *>(Xh), M, N, K, W, mW, vW, Wb, b, mb, vb, a,
                        lf);
   else
-    hipLaunchKernelGGL((k_dw_adam_f32<T::bm, T::bn, T::bk, T::wm, T::wn>), dim3(T::tiles(M, N)),
+    hipLaunchKernelGGL((k_dw_adam_f32<T::bm, T::bn, T::bk, T::wm, T::wn, T::pf>), dim3(T::tiles(M, N)),
                        dim3(T::threads), 0, s, H, c, static_cast<const float *>(Xh), M, N, K, W,
                        mW, vW, Wb, b, mb, vb, a, lf);
 }
