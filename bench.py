@@ -122,6 +122,34 @@ def traffic_summary(fetch_csv, write_csv, cfetch_csv, cwrite_csv, workload, copy
     print(json.dumps(out, indent=1))
 
 
+def isolated_roofline(P, torch, w, dtype, kind, peak, punit, reps=20):
+    """The dominant kernel alone on one stream, at the largest layer shape of
+    the training step (its chunk rows x the widest layer), timed by the same
+    per-launch HIP events: the kernel's own efficiency, without the time it
+    shares with the other layers' streams in the pipelined step."""
+    from ffinputs import random_matrix, make_weights
+    dev = torch.device("cuda:0")
+    di, do = max(zip(w.dims[:-1], w.dims[1:]), key=lambda t: t[0] * t[1])
+    R = 2 * w.chunk_pairs
+    x = torch.from_numpy(random_matrix(7, R, di, 0, 1, 0.5)).to(dev)
+    (Wt, bt), = make_weights(8, (di, do))
+    L = P.Layer(torch.from_numpy(Wt).to(dev), torch.from_numpy(bt).to(dev),
+                dtype == P.FF_BF16)
+    hp = P.HParams(theta=w.theta, lr=w.lr, dtype=dtype)
+    ws = P.workspace(P.ff_step_workspace_size(R, di, do, dtype), dev)
+    for _ in range(3):
+        P.ff_layer_step(L, hp, x, R // 2, R - R // 2, ws=ws)
+    torch.cuda.synchronize()
+    P.ff_profile_start(reps * 8)
+    for _ in range(reps):
+        P.ff_layer_step(L, hp, x, R // 2, R - R // 2, ws=ws)
+    st = P.ff_profile_stop()[kind]
+    ach = st["flops"] / (st["total_ms"] * 1e-3) / 1e12
+    return {"kernel": kind, "shape": f"{R}x{di}->{do}", "achieved": ach, "peak": peak,
+            "unit": punit, "frac": ach / peak, "avg_launch_us": st["total_ms"] * 1e3 / reps,
+            "launches": st["launches"]}
+
+
 def cpu_baseline(w, x_base, y, y_neg, params, sw, sx, sparams, budget_s=12.0):
     """The oracle as it stands, on a bounded sample of the same workload."""
     import numpy as np
@@ -318,6 +346,7 @@ def main():
         "train_mfma_frac": train_flops / (train_ms * 1e-3) / 1e12 / peak,
         "kernels": kernels,
     }
+    out["roofline_isolated"] = isolated_roofline(P, torch, w, dtype, dom, peak, punit)
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(w, x_base, y, y_neg, params, sw, sx, sparams)

@@ -289,12 +289,22 @@ struct Operand<true> {
   static constexpr int kVec = 8;
 };
 
-template <bool BF16, int BM, int BN, int BK, int WM, int WN, int PF, bool STORE_H>
-__global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16>::T *__restrict__ X,
-                                                     const typename Operand<BF16>::T *__restrict__ W,
-                                                     const float *__restrict__ bias, int M, int N,
-                                                     int K, float *__restrict__ H,
-                                                     float *__restrict__ gpart) {
+// LDS elements of the NT main loop's double-buffered tiles.
+template <bool BF16, int BM, int BN, int BK>
+constexpr int nt_lds_elems() {
+  return 2 * (BM + BN) * (BK + Operand<BF16>::kVec);
+}
+
+// Main loop of C[m][n] = sum_k X[m][k] W[n][k] for the tile at (m0, n0), both
+// operands K-contiguous, into the wave's accumulators.  Shared by the forward
+// product and the bf16 weight-gradient product (whose operands are stored
+// transposed, k-contiguous, for it).
+template <bool BF16, int BM, int BN, int BK, int WM, int WN, int PF>
+__device__ __forceinline__ void nt_mainloop(const typename Operand<BF16>::T *__restrict__ X,
+                                            const typename Operand<BF16>::T *__restrict__ W,
+                                            int M, int N, int K, int m0, int n0,
+                                            typename Operand<BF16>::T *sm,
+                                            floatx16 (&acc)[BM / WM / 32][BN / WN / 32]) {
   using T = typename Operand<BF16>::T;
   constexpr int VE = Operand<BF16>::kVec;
   constexpr int NT = WM * WN * 64;
@@ -306,14 +316,8 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16
   static_assert(MB * 32 == TM && NB * 32 == TN, "wave tile is whole 32x32 blocks");
   static_assert(LDA * NT == BM * KCH && LDB * NT == BN * KCH, "tile/threads");
   static_assert((BK / 2) % VE == 0, "half slab is whole vectors");
-  __shared__ __attribute__((aligned(16))) T sm[2 * (BM + BN) * LDK];
   T *As = sm;                 // [2][BM][LDK]
   T *Bs = sm + 2 * BM * LDK;  // [2][BN][LDK]
-
-  const int nt = (N + BN - 1) / BN;
-  int tm, tn;
-  tile_of(blockIdx.x, (M + BM - 1) / BM, nt, tm, tn);
-  const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int li = lane & 31, kg = lane >> 5;
@@ -353,7 +357,6 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16
       st16(Bs + (buf * BN + srow + i * RSTEP) * LDK + kc, kok ? g.b[i] : z);
   };
 
-  floatx16 acc[MB][NB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -392,6 +395,28 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16
   };
 
   kloop<PF>((K + BK - 1) / BK, gload, sstore, compute, st);
+}
+
+template <bool BF16, int BM, int BN, int BK, int WM, int WN, int PF, bool STORE_H>
+__global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16>::T *__restrict__ X,
+                                                     const typename Operand<BF16>::T *__restrict__ W,
+                                                     const float *__restrict__ bias, int M, int N,
+                                                     int K, float *__restrict__ H,
+                                                     float *__restrict__ gpart) {
+  using T = typename Operand<BF16>::T;
+  constexpr int NT = WM * WN * 64;
+  constexpr int TM = BM / WM, TN = BN / WN, MB = TM / 32, NB = TN / 32;
+  __shared__ __attribute__((aligned(16))) T sm[nt_lds_elems<BF16, BM, BN, BK>()];
+  const int nt = (N + BN - 1) / BN;
+  int tm, tn;
+  tile_of(blockIdx.x, (M + BM - 1) / BM, nt, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int li = lane & 31, kg = lane >> 5;
+
+  floatx16 acc[MB][NB];
+  nt_mainloop<BF16, BM, BN, BK, WM, WN, PF>(X, W, M, N, K, m0, n0, sm, acc);
 
   // Epilogue: bias, ReLU, H store, goodness partials.
   float hsq[MB * 16];
