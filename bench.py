@@ -61,6 +61,25 @@ KIND_OF = [("k_fwd", "forward"), ("k_dw_adam", "dw_adam"), ("k_embed_norm", "emb
            ("k_bf16_shadow", "bf16_shadow")]
 
 
+def focus_steps(rows, d_in, d_out, bf16, steps=3):
+    """A few training steps of one layer shape on one stream, nothing else timed:
+    the workload of the per-kernel counter runs."""
+    import torch
+    import paper_2404_08573_amd as P
+    from ffinputs import random_matrix, make_weights
+    dev = torch.device("cuda:0")
+    dt = P.FF_BF16 if bf16 else P.FF_F32
+    x = torch.from_numpy(random_matrix(1, rows, d_in, 0, 1, 0.5)).to(dev)
+    (W, b), = make_weights(2, (d_in, d_out))
+    L = P.Layer(torch.from_numpy(W).to(dev), torch.from_numpy(b).to(dev), bool(bf16))
+    hp = P.HParams(dtype=dt, lr=0.01)
+    ws = P.workspace(P.ff_step_workspace_size(rows, d_in, d_out, dt), dev)
+    for _ in range(steps):
+        P.ff_layer_step(L, hp, x, rows // 2, rows - rows // 2, ws=ws)
+    torch.cuda.synchronize()
+    print(json.dumps({"focus": [rows, d_in, d_out, bf16], "steps": steps}))
+
+
 def copy_calibration(nbytes):
     """One plain device copy of nbytes (read nbytes, write nbytes): the reference
     that scales the FETCH_SIZE / WRITE_SIZE counters to bytes."""
@@ -212,7 +231,12 @@ def main():
                     help="FETCH, WRITE, copy FETCH, copy WRITE counter_collection.csv files: "
                          "write profiles/traffic.json for --workload and exit")
     ap.add_argument("--copy-bytes", type=int, default=1 << 30)
+    ap.add_argument("--focus", nargs=4, type=int, metavar=("ROWS", "D_IN", "D_OUT", "BF16"),
+                    help="run a few layer steps of one shape on one stream (for counter runs)")
     args = ap.parse_args()
+    if args.focus:
+        focus_steps(*args.focus)
+        return
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
         return
