@@ -138,6 +138,22 @@ ff_status ff_score_labels(const ff_layer *layers, int32_t n_layers, int32_t firs
                           const ff_hparams *hp, const float *x_base, int32_t n, int32_t n_classes,
                           float *scores, int32_t *pred, void *ws, size_t ws_bytes, void *stream);
 
+/* AdaptiveNEG negative labels (Sec. 5, after Hinton's FF paper): the wrong
+ * label the network currently scores highest,
+ *   y_neg[n] = argmax_{c != labels[n]} S[n][c]   (lowest c on exact ties),
+ * with S as in ff_score_labels (same first_scored_layer reading), so the
+ * caller can redraw the negatives of the training set between chapters.
+ *   labels (device) [n] int32, the true labels: a value outside
+ *   [0, n_classes) excludes nothing (not checked on the device);
+ *   scores (device) [n][n_classes] or NULL (the unmasked S);
+ *   y_neg (device) [n] int32, may not alias labels.
+ * n_classes >= 2.  Workspace: ff_score_workspace_size.  n == 0 is a no-op. */
+ff_status ff_adaptive_negatives(const ff_layer *layers, int32_t n_layers,
+                                int32_t first_scored_layer, const ff_hparams *hp,
+                                const float *x_base, const int32_t *labels, int32_t n,
+                                int32_t n_classes, float *scores, int32_t *y_neg, void *ws,
+                                size_t ws_bytes, void *stream);
+
 /* Workspace bytes for ff_pipeline_epoch. */
 size_t ff_pipeline_workspace_size(const ff_layer *layers, int32_t n_layers, int32_t n,
                                   int32_t chunk_pairs, int32_t schedule, int32_t dtype);

@@ -252,6 +252,27 @@ def score_labels(layers: Sequence[Layer], x_base: np.ndarray, n_classes: int,
     return S, np.argmax(S, axis=1).astype(np.int32)
 
 
+def adaptive_negatives(layers: Sequence[Layer], x_base: np.ndarray, labels: np.ndarray,
+                       n_classes: int, hp: HParams,
+                       first_scored_layer: int = 0) -> Tuple[np.ndarray, np.ndarray]:
+    """AdaptiveNEG (Sec. 5, the negative selection of Hinton's FF paper).
+
+    Each sample's negative label is the wrong label that the current network
+    predicts most strongly: the goodness prediction above is computed for every
+    label, the true label is set aside, and the best of the remaining labels is
+    taken (lowest index on ties).  Returns ``(S[n, C], y_neg[n])``.
+    """
+    S, _ = score_labels(layers, x_base, n_classes, hp, first_scored_layer)
+    y_neg = np.empty(S.shape[0], dtype=np.int32)
+    for i in range(S.shape[0]):
+        best = -1
+        for c in range(n_classes):
+            if c != labels[i] and (best < 0 or S[i, c] > S[i, best]):
+                best = c
+        y_neg[i] = best
+    return S, y_neg
+
+
 # ----------------------------------------------------------------------------
 # Training schedules over chunks (Sec. 3 sequential FF, Sec. 4.1 Alg. 1)
 # ----------------------------------------------------------------------------

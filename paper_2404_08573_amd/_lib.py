@@ -24,7 +24,8 @@ FF_SEQUENTIAL, FF_PIPELINED = 0, 1
 
 EXPORTS = ["ff_status_string", "ff_last_error", "ff_embed_labels", "ff_step_workspace_size",
            "ff_layer_forward", "ff_layer_step", "ff_refresh_bf16_shadow",
-           "ff_score_workspace_size", "ff_score_labels", "ff_pipeline_workspace_size",
+           "ff_score_workspace_size", "ff_score_labels", "ff_adaptive_negatives",
+           "ff_pipeline_workspace_size",
            "ff_pipeline_epoch", "ff_profile_start", "ff_profile_stop"]
 
 KERNEL_KINDS = ["embed_norm", "forward", "loss", "dw_adam", "goodness", "argmax", "bf16_shadow"]
@@ -72,6 +73,9 @@ def _load() -> ctypes.CDLL:
                                                c_int32]),
         "ff_score_labels": (c_int32, [POINTER(ff_layer), c_int32, c_int32, POINTER(ff_hparams), P,
                                       c_int32, c_int32, P, P, P, c_size_t, P]),
+        "ff_adaptive_negatives": (c_int32, [POINTER(ff_layer), c_int32, c_int32,
+                                            POINTER(ff_hparams), P, P, c_int32, c_int32, P, P, P,
+                                            c_size_t, P]),
         "ff_pipeline_workspace_size": (c_size_t, [POINTER(ff_layer), c_int32, c_int32, c_int32,
                                                   c_int32, c_int32]),
         "ff_pipeline_epoch": (c_int32, [POINTER(ff_layer), c_int32, POINTER(ff_hparams), P, P, P,
@@ -239,6 +243,27 @@ def ff_score_labels(layers: Sequence[Layer], hp: HParams, x_base: torch.Tensor, 
                                 _ptr(pred, torch.int32, n, "pred"), _ptr(ws, torch.uint8),
                                 ws.numel(), _stream(stream)))
     return scores, pred
+
+
+def ff_adaptive_negatives(layers: Sequence[Layer], hp: HParams, x_base: torch.Tensor,
+                          labels: torch.Tensor, n_classes: int, first_scored_layer: int = 0,
+                          scores: Optional[torch.Tensor] = None,
+                          y_neg: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                          stream=None):
+    """AdaptiveNEG: y_neg[n] = argmax over c != labels[n] of the goodness scores."""
+    n = x_base.shape[0]
+    dev = x_base.device
+    y_neg = torch.empty(n, dtype=torch.int32, device=dev) if y_neg is None else y_neg
+    if ws is None:
+        ws = workspace(ff_score_workspace_size(layers, max(n, 1), n_classes, hp.dtype), dev)
+    arr = _layers_c(layers)
+    _check(LIB.ff_adaptive_negatives(
+        arr, len(layers), first_scored_layer, ctypes.byref(hp.c()),
+        _ptr(x_base, torch.float32, n * layers[0].d_in, "x_base"),
+        _ptr(labels, torch.int32, n, "labels"), n, n_classes,
+        _ptr(scores, torch.float32, n * n_classes, "scores"), _ptr(y_neg, torch.int32, n, "y_neg"),
+        _ptr(ws, torch.uint8), ws.numel(), _stream(stream)))
+    return scores, y_neg
 
 
 def ff_pipeline_workspace_size(layers: Sequence[Layer], n: int, chunk_pairs: int, schedule: int,

@@ -421,9 +421,13 @@ size_t ff_score_workspace_size(const ff_layer *layers, int32_t n_layers, int32_t
   return cv.off + kAlign;
 }
 
-ff_status ff_score_labels(const ff_layer *layers, int32_t n_layers, int32_t first_scored_layer,
-                          const ff_hparams *hp, const float *x_base, int32_t n, int32_t n_classes,
-                          float *scores, int32_t *pred, void *ws, size_t ws_bytes, void *stream) {
+namespace {
+// Scores every input under every label, then takes the argmax (skipping
+// exclude[i] when exclude is given).
+ff_status score_core(const ff_layer *layers, int32_t n_layers, int32_t first_scored_layer,
+                     const ff_hparams *hp, const float *x_base, int32_t n, int32_t n_classes,
+                     const int32_t *exclude, float *scores, int32_t *pred, void *ws,
+                     size_t ws_bytes, void *stream) {
   FF_TRY(check_hp(hp));
   FF_TRY(check_stack(layers, n_layers, hp, false));
   if (first_scored_layer < 0 || first_scored_layer >= n_layers)
@@ -433,7 +437,7 @@ ff_status ff_score_labels(const ff_layer *layers, int32_t n_layers, int32_t firs
   if (n_classes > layers[0].d_in)
     return fail(FF_ERR_INVALID_ARG, "n_classes=%d exceeds d_in=%d", n_classes, layers[0].d_in);
   if (n == 0) return FF_OK;
-  if (!x_base || !pred) return fail(FF_ERR_INVALID_ARG, "x_base or pred is NULL");
+  if (!x_base || !pred) return fail(FF_ERR_INVALID_ARG, "x_base or the output labels are NULL");
   if ((int64_t)n * n_classes > INT32_MAX) return fail(FF_ERR_UNSUPPORTED, "n too large");
   Carver size_cv(nullptr);
   ScoreScratch tmp;
@@ -467,8 +471,27 @@ ff_status ff_score_labels(const ff_layer *layers, int32_t n_layers, int32_t firs
     }
   }
   FF_HIP(launch(FF_KERNEL_ARGMAX, 0.0, (double)n * n_classes * 4.0 + n * 4.0, st,
-                [&] { return ffk::launch_argmax(S, n, n_classes, pred, st); }));
+                [&] { return ffk::launch_argmax(S, n, n_classes, exclude, pred, st); }));
   return FF_OK;
+}
+}  // namespace
+
+ff_status ff_score_labels(const ff_layer *layers, int32_t n_layers, int32_t first_scored_layer,
+                          const ff_hparams *hp, const float *x_base, int32_t n, int32_t n_classes,
+                          float *scores, int32_t *pred, void *ws, size_t ws_bytes, void *stream) {
+  return score_core(layers, n_layers, first_scored_layer, hp, x_base, n, n_classes, nullptr,
+                    scores, pred, ws, ws_bytes, stream);
+}
+
+ff_status ff_adaptive_negatives(const ff_layer *layers, int32_t n_layers,
+                                int32_t first_scored_layer, const ff_hparams *hp,
+                                const float *x_base, const int32_t *labels, int32_t n,
+                                int32_t n_classes, float *scores, int32_t *y_neg, void *ws,
+                                size_t ws_bytes, void *stream) {
+  if (n > 0 && !labels) return fail(FF_ERR_INVALID_ARG, "labels is NULL");
+  if (n_classes < 2) return fail(FF_ERR_INVALID_ARG, "n_classes=%d: no wrong label", n_classes);
+  return score_core(layers, n_layers, first_scored_layer, hp, x_base, n, n_classes, labels,
+                    scores, y_neg, ws, ws_bytes, stream);
 }
 
 // ---------------------------------------------------------------------------

@@ -76,8 +76,10 @@ hipError_t launch_dw_adam(int dtype, const float *H, const float *c, const void 
 hipError_t launch_goodness(const float *gpart, int ntiles, int R, float *g, float *out,
                            int accumulate, hipStream_t s);
 
-// pred[n] = argmax_c scores[n][c], lowest c on ties.
-hipError_t launch_argmax(const float *scores, int n, int C, int32_t *pred, hipStream_t s);
+// pred[n] = argmax_c scores[n][c], lowest c on ties; with `exclude` (C >= 2),
+// c == exclude[n] is skipped.
+hipError_t launch_argmax(const float *scores, int n, int C, const int32_t *exclude, int32_t *pred,
+                         hipStream_t s);
 
 // Wb[i] = bf16(W[i]).
 hipError_t launch_bf16_shadow(const float *W, uint16_t *Wb, size_t count, hipStream_t s);

@@ -904,15 +904,19 @@ __global__ __launch_bounds__(kBlock) void k_goodness(const float *__restrict__ g
   if (out) out[r] = accumulate ? out[r] + gv : gv;
 }
 
+// pred[i] = argmax_c S[i][c], lowest c on ties.  With `exclude`, label
+// exclude[i] takes no part (an out-of-range label excludes nothing); C >= 2 then.
 __global__ __launch_bounds__(kBlock) void k_argmax(const float *__restrict__ S, int n, int C,
+                                                   const int32_t *__restrict__ exclude,
                                                    int32_t *__restrict__ pred) {
   const int i = blockIdx.x * kBlock + threadIdx.x;
   if (i >= n) return;
   const float *s = S + (size_t)i * C;
-  float best = s[0];
-  int arg = 0;
-  for (int c = 1; c < C; ++c)
-    if (s[c] > best) {
+  const int skip = exclude ? exclude[i] : -1;
+  int arg = skip == 0 ? 1 : 0;
+  float best = s[arg];
+  for (int c = arg + 1; c < C; ++c)
+    if (c != skip && s[c] > best) {
       best = s[c];
       arg = c;
     }
@@ -1065,9 +1069,11 @@ hipError_t launch_goodness(const float *gpart, int ntiles, int R, float *g, floa
   return hipGetLastError();
 }
 
-hipError_t launch_argmax(const float *scores, int n, int C, int32_t *pred, hipStream_t s) {
+hipError_t launch_argmax(const float *scores, int n, int C, const int32_t *exclude, int32_t *pred,
+                         hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_argmax, dim3(cdiv(n, kBlock)), dim3(kBlock), 0, s, scores, n, C, pred);
+  hipLaunchKernelGGL(k_argmax, dim3(cdiv(n, kBlock)), dim3(kBlock), 0, s, scores, n, C, exclude,
+                     pred);
   return hipGetLastError();
 }
 

@@ -55,23 +55,38 @@ def grad_magnitudes(r):
     return dz.T @ np.abs(r.xh), dz.sum(axis=0)
 
 
-def ill_conditioned(grads, mags):
+def ill_conditioned(grads, mags, lr=None, adam_eps=1e-8, tol=None):
     """Elements whose gradient was ill-conditioned at some step.
 
     A gradient element is a sum over the batch rows; rounding can change its
     sign only when |sum| is tiny against sum(|terms|).  Flagged: 0 < |g| <
     1e-5 sum(|terms|) (condition number above 1e5).  An exactly zero gradient
     (a feature that is zero in every row) gives an exactly zero Adam update on
-    both sides and is not flagged."""
+    both sides and is not flagged.
+
+    With `lr` (weights only), also flagged: elements whose Adam update
+    amplifies the same rounding allowance beyond half the weight tolerance
+    `tol`.  Adam's step g/(|g| + eps) has derivative eps/(|g| + eps)^2, so a
+    gradient near eps in size turns an error e in g into a weight error of up
+    to lr*eps*e/(|g| + eps)^2, with e = 1e-5 sum(|terms|) as above."""
     flag = np.zeros(np.shape(grads[0]), bool)
     for gr, mg in zip(grads, mags):
         a = np.abs(np.asarray(gr))
-        flag |= (a > 0) & (a < 1e-5 * np.asarray(mg))
+        mg = np.asarray(mg)
+        flag |= (a > 0) & (a < 1e-5 * mg)
+        if lr is not None:
+            amp = lr * adam_eps * 1e-5 * mg / (a + adam_eps) ** 2
+            flag |= (a > 0) & (amp > 0.5 * tol)
     return flag
 
 
-def assert_weights(W, ref, grads, mags, what="W", rel=1e-3, outliers=0.0, outlier_rel=0.0):
+def assert_weights(W, ref, grads, mags, what="W", rel=1e-3, outliers=0.0, outlier_rel=0.0,
+                   lr=None, adam_eps=1e-8):
     """Weights after k Adam steps (see the module docstring).
+
+    `lr`, `adam_eps`: pass them when W is a parameter updated by Adam with
+    those settings (not for the moments), so elements whose update amplifies
+    gradient rounding past the bar are set aside (see ill_conditioned).
 
     `outliers` (bf16 comparisons only): the fraction of elements allowed to
     exceed `rel`, each still within `outlier_rel`.  With bf16 operands the two
@@ -80,7 +95,7 @@ def assert_weights(W, ref, grads, mags, what="W", rel=1e-3, outliers=0.0, outlie
     by 2^-8 of one term; Adam's per-element normalisation can turn that into a
     weight difference above the fp32 bar for the rare elements it touches."""
     W = np.asarray(W, np.float64)
-    flag = ill_conditioned(grads, mags)
+    flag = ill_conditioned(grads, mags, lr, adam_eps, rel * np.abs(ref) + 1e-6)
     assert flag.mean() <= 1e-3, f"{what}: ill-conditioned fraction {flag.mean():.2e} > 1e-3"
     err = np.abs(W - ref)
     bad = (err > rel * np.abs(ref) + 1e-6) & ~flag
@@ -102,6 +117,24 @@ def assert_labels(pred, S_ref, pred_ref):
     pred = np.asarray(pred)
     bad = (pred != pred_ref) & ok
     assert not bad.any(), f"labels: {bad.sum()} decided rows differ"
+    return int(ok.sum())
+
+
+def assert_negatives(y_neg, S_ref, y_ref, labels):
+    """AdaptiveNEG labels: bit-exact where the oracle's two best wrong labels are
+    at least 1e-4 apart (relative); elsewhere any wrong label tied with the best
+    within that margin is valid."""
+    S = np.array(S_ref, np.float64)
+    n = np.arange(S.shape[0])
+    inr = (labels >= 0) & (labels < S.shape[1])
+    S[n[inr], labels[inr]] = -np.inf
+    y_neg = np.asarray(y_neg)
+    ok = decided(S)
+    bad = (y_neg != y_ref) & ok
+    assert not bad.any(), f"negatives: {bad.sum()} decided rows differ"
+    assert not np.any(inr & (y_neg == labels)), "a true label was chosen as negative"
+    best = S.max(axis=1)
+    assert np.all(S[n, y_neg] >= best - 1e-4 * np.abs(best)), "an undecided row chose a weak label"
     return int(ok.sum())
 
 

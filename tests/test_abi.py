@@ -28,7 +28,7 @@ def test_header_declares_the_entry_points():
     for must in ["ff_layer_step", "ff_score_labels", "ff_pipeline_epoch", "ff_layer_forward",
                  "ff_embed_labels", "ff_step_workspace_size", "ff_score_workspace_size",
                  "ff_pipeline_workspace_size", "ff_status_string", "ff_last_error",
-                 "ff_refresh_bf16_shadow"]:
+                 "ff_refresh_bf16_shadow", "ff_adaptive_negatives"]:
         assert must in names
 
 
@@ -128,6 +128,27 @@ def test_score_labels_rejects_on_host(P):
     assert st == 0
 
 
+def test_adaptive_negatives_rejects_on_host(P):
+    layers = (P._lib.ff_layer * 2)(_layer(P, 16, 8), _layer(P, 8, 8))
+    hp = _hp(P)
+    ws = ctypes.c_void_p(1 << 20)
+    args = [layers, 2, 0, ctypes.byref(hp), ctypes.c_void_p(4096), ctypes.c_void_p(4096), 5, 10,
+            None, ctypes.c_void_p(8192), ws, 1 << 30, None]
+    one = list(args)
+    one[7] = 1
+    assert P.LIB.ff_adaptive_negatives(*one) == -1
+    assert b"no wrong label" in P.LIB.ff_last_error()
+    nolab = list(args)
+    nolab[5] = None
+    assert P.LIB.ff_adaptive_negatives(*nolab) == -1
+    noout = list(args)
+    noout[9] = None
+    assert P.LIB.ff_adaptive_negatives(*noout) == -1
+    small = list(args)
+    small[11] = 16
+    assert P.LIB.ff_adaptive_negatives(*small) == -3
+
+
 def test_pipeline_rejects_on_host(P):
     layers = (P._lib.ff_layer * 2)(_layer(P, 16, 8), _layer(P, 8, 8))
     hp = _hp(P)
@@ -154,3 +175,15 @@ def test_embed_rejects_on_host(P):
     assert L.ff_embed_labels(ctypes.c_void_p(64), ctypes.c_void_p(64), 3, 10, 4,
                              ctypes.c_void_p(64), None) == -2  # d not a multiple of 4
     assert L.ff_embed_labels(None, None, 0, 12, 10, None, None) == 0  # empty
+
+
+def test_graft_build_entry_binds_exports(P, monkeypatch):
+    """__graft_entry__.build() after its compile step (stubbed here: the library
+    is already built) must load the library and bind every export."""
+    import importlib
+    import sys
+    sys.path.insert(0, ROOT)
+    import paper_2404_08573_amd.build as B
+    monkeypatch.setattr(B, "build", lambda *a, **k: None)
+    entry = importlib.import_module("__graft_entry__")
+    entry.build()

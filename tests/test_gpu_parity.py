@@ -7,7 +7,7 @@ torch = pytest.importorskip("torch")
 import oracle as O  # noqa: E402
 from ffinputs import WORKLOADS, make_data, make_weights, random_labels, random_matrix  # noqa: E402
 from parity import (assert_acts, assert_goodness, assert_labels, assert_loss,  # noqa: E402
-                    assert_weights, grad_magnitudes)
+                    assert_negatives, assert_weights, grad_magnitudes)
 
 pytestmark = pytest.mark.gpu
 
@@ -115,8 +115,8 @@ def _run_steps(P, x, n_pos, W, b, k, hp_kw, check_each=True):
             assert_loss(_np(loss)[0], r.loss)
             assert_acts(_np(h), r.h)
     assert L.step == k
-    assert_weights(_np(L.W), ref.W, gW, mW, "W")
-    assert_weights(_np(L.b), ref.b, gb, mb, "b")
+    assert_weights(_np(L.W), ref.W, gW, mW, "W", lr=ohp.lr, adam_eps=ohp.adam_eps)
+    assert_weights(_np(L.b), ref.b, gb, mb, "b", lr=ohp.lr, adam_eps=ohp.adam_eps)
     assert_weights(_np(L.mW), ref.mW, gW, mW, "mW")
     assert_weights(_np(L.vW), ref.vW, gW, mW, "vW", rel=2e-3)
     return L, ref
@@ -215,6 +215,68 @@ def test_score_full_size_sampled(P):
                                   O.HParams(), 0)
     assert_goodness(Sg[idx], S_ref, what="scores")
     assert_labels(pg[idx], S_ref, p_ref)
+
+
+# ------------------------------------------------------------------ AdaptiveNEG
+def _masked_argmax(S, labels):
+    S = np.array(S, np.float64)
+    inr = (labels >= 0) & (labels < S.shape[1])
+    S[np.arange(S.shape[0])[inr], labels[inr]] = -np.inf
+    return np.argmax(S, axis=1)
+
+
+@pytest.mark.parametrize("first", [0, 1])
+def test_adaptive_negatives_tiny_config(P, first):
+    w = WORKLOADS["mnist_tiny_784_500x2"]
+    x_base, y, _ = make_data(w.seed_data, w.n, w.dims[0], w.p_zero)
+    params = make_weights(w.seed_w, w.dims)
+    layers = [P.Layer(_t(W), _t(b)) for W, b in params]
+    S = torch.empty(w.n, 10, device=DEV)
+    _, y_neg = P.ff_adaptive_negatives(layers, P.HParams(), _t(x_base), _t(y), 10, first,
+                                       scores=S)
+    S_ref, n_ref = O.adaptive_negatives([O.Layer.from_params(W, b) for W, b in params], x_base,
+                                        y, 10, O.HParams(), first)
+    assert_goodness(_np(S), S_ref, what="scores")
+    assert assert_negatives(_np(y_neg), S_ref, n_ref, y) > 0.9 * w.n
+    np.testing.assert_array_equal(_np(y_neg), _masked_argmax(_np(S), y))
+
+
+def test_adaptive_negatives_edge_labels(P):
+    """Ragged scoring passes, 7 classes, true labels at both ends of the range,
+    out-of-range labels (nothing excluded: plain prediction), and 2 classes."""
+    x_base, _, _ = make_data(64, 2100, 24, 0.5)
+    params = make_weights(65, (24, 36, 20))
+    layers = [P.Layer(_t(W), _t(b)) for W, b in params]
+    O_layers = [O.Layer.from_params(W, b) for W, b in params]
+    labels = np.resize(np.array([0, 6, 3, -1, 7, 6, 0], np.int32), 2100)
+    _, y_neg = P.ff_adaptive_negatives(layers, P.HParams(), _t(x_base), _t(labels), 7, 0)
+    S_ref, n_ref = O.adaptive_negatives(O_layers, x_base, labels, 7, O.HParams(), 0)
+    assert_negatives(_np(y_neg), S_ref, n_ref, labels)
+    out = (labels < 0) | (labels >= 7)
+    _, pred = P.ff_score_labels(layers, P.HParams(), _t(x_base), 7, 0)
+    np.testing.assert_array_equal(_np(y_neg)[out], _np(pred)[out])
+    lab2 = (np.arange(50) % 2).astype(np.int32)
+    _, y2 = P.ff_adaptive_negatives(layers, P.HParams(), _t(x_base[:50]), _t(lab2), 2, 1)
+    np.testing.assert_array_equal(_np(y2), 1 - lab2)
+
+
+def test_adaptive_negatives_training_set_sampled(P):
+    """Negatives for all 60 000 training samples under 784->2000x4 (the labels a
+    chapter of AdaptiveNEG training would use); the oracle checks a sample."""
+    w = WORKLOADS["mnist_784_2000x4"]
+    x_base, y, _ = make_data(w.seed_data, w.n, w.dims[0], w.p_zero)
+    params = make_weights(w.seed_w, w.dims)
+    layers = [P.Layer(_t(W), _t(b)) for W, b in params]
+    S = torch.empty(w.n, 10, device=DEV)
+    _, y_neg = P.ff_adaptive_negatives(layers, P.HParams(), _t(x_base), _t(y), 10, 0, scores=S)
+    Sg, ng = _np(S), _np(y_neg)
+    np.testing.assert_array_equal(ng, _masked_argmax(Sg, y))
+    assert not np.any(ng == y)
+    idx = np.random.default_rng(1).choice(w.n, 16, replace=False)
+    S_ref, n_ref = O.adaptive_negatives([O.Layer.from_params(W, b) for W, b in params],
+                                        x_base[idx], y[idx], 10, O.HParams(), 0)
+    assert_goodness(Sg[idx], S_ref, what="scores")
+    assert_negatives(ng[idx], S_ref, n_ref, y[idx])
 
 
 # ------------------------------------------------------------------ schedules
@@ -318,7 +380,7 @@ def _run_steps_bf16(P, x, n_pos, W, b, k, hp_kw):
         assert_goodness(_np(g), r.g, rel=1e-3)
         assert_loss(_np(loss)[0], r.loss, rel=1e-3)
     assert_weights(_np(L.W), ref.W, gW, mW, "W (vs bf16-emulating oracle)", rel=2e-3,
-                   outliers=1e-5, outlier_rel=2e-2)
+                   outliers=1e-5, outlier_rel=2e-2, lr=ohp.lr, adam_eps=ohp.adam_eps)
     # the shadow is the rounded master
     np.testing.assert_array_equal(
         _np(L.W_bf16).view(np.uint16),

@@ -286,6 +286,53 @@ def test_score_hidden_permutation_invariance():
     np.testing.assert_array_equal(pa, pb)
 
 
+# ---------------------------------------------------------------- AdaptiveNEG
+def test_adaptive_negatives_hand_designed_net():
+    """With the hand-designed layer above, the score of label c rises with the
+    data feature d_c, so the hardest wrong label is the largest d_c over the
+    labels other than the true one: the runner-up when the true label is the
+    largest, else the largest."""
+    C = 10
+    rng = np.random.default_rng(5)
+    data = rng.uniform(0, 1, (40, C))
+    x_base = np.concatenate([rng.uniform(0, 1, (40, C)), data], axis=1)
+    W = np.zeros((C, 2 * C))
+    W[np.arange(C), np.arange(C)] = 1.0
+    W[np.arange(C), C + np.arange(C)] = 1.0
+    L = O.Layer.from_params(W, np.zeros(C))
+    order = np.argsort(-data, axis=1)
+    y = np.where(np.arange(40) % 2 == 0, order[:, 0], rng.integers(0, C, 40)).astype(np.int32)
+    _, y_neg = O.adaptive_negatives([L], x_base, y, C, O.HParams())
+    want = np.where(order[:, 0] == y, order[:, 1], order[:, 0])
+    np.testing.assert_array_equal(y_neg, want)
+
+
+def test_adaptive_negatives_ties_and_exclusion():
+    C = 10
+    x_base = np.ones((4, 25))
+    W = np.zeros((4, 25))
+    W[:, C:] = 1.0  # every label ties
+    L = O.Layer.from_params(W, np.zeros(4))
+    y = np.array([0, 1, 9, 3], np.int32)
+    _, y_neg = O.adaptive_negatives([L], x_base, y, C, O.HParams())
+    np.testing.assert_array_equal(y_neg, [1, 0, 0, 0])
+
+
+def test_adaptive_negatives_order_statistics():
+    """On a random net: the chosen label is never the true one and beats or ties
+    every other wrong label; a sort of each row by (-score, label) gives it."""
+    x_base, y, _ = make_data(12, 30, 40)
+    layers = _net(13, (40, 16, 12))
+    for first in (0, 1):
+        S, y_neg = O.adaptive_negatives(layers, x_base, y, 10, O.HParams(), first)
+        S2, _ = O.score_labels(layers, x_base, 10, O.HParams(), first)
+        np.testing.assert_array_equal(S, S2)
+        for n in range(30):
+            assert y_neg[n] != y[n]
+            ranked = sorted(range(10), key=lambda c: (-S[n, c], c))
+            assert y_neg[n] == next(c for c in ranked if c != y[n])
+
+
 # ---------------------------------------------------------------- schedules
 def _net(seed, dims):
     return [O.Layer.from_params(W, b) for W, b in make_weights(seed, dims)]

@@ -1,0 +1,122 @@
+"""The parity bars themselves (tests/parity.py), checked on the CPU.
+
+Two properties keep a bar honest: a correct implementation in fp32, with its
+own summation order, passes it; and the oracle with a plausible mistake
+planted in it fails it.  The fp32 step below is written here only for that
+purpose (NumPy float32, BLAS summation order); the mistakes are planted in
+copies of the oracle's step, never in the oracle itself.
+"""
+import numpy as np
+import pytest
+
+import oracle as O
+from ffinputs import make_data, make_weights
+from parity import assert_goodness, assert_weights, grad_magnitudes, ill_conditioned
+
+F32 = np.float32
+
+
+def _fp32_steps(W, b, x, n_pos, k, hp):
+    """k FF steps evaluated in float32 throughout."""
+    W, b = W.astype(F32), b.astype(F32)
+    mW, vW, mb, vb = (np.zeros_like(W), np.zeros_like(W), np.zeros_like(b), np.zeros_like(b))
+    x = x.astype(F32)
+    xh = x / (np.sqrt((x * x).sum(1, keepdims=True)) + F32(hp.norm_eps))
+    for t in range(1, k + 1):
+        h = np.maximum(xh @ W.T + b, F32(0))
+        g = (h * h).sum(1)
+        s = np.empty_like(g)
+        s[:n_pos] = -1.0 / (1.0 + np.exp(g[:n_pos] - hp.theta)) / n_pos
+        s[n_pos:] = 1.0 / (1.0 + np.exp(hp.theta - g[n_pos:])) / (len(g) - n_pos)
+        dz = (2 * s)[:, None].astype(F32) * h
+        for p, m, v, gr in ((W, mW, vW, dz.T @ xh), (b, mb, vb, dz.sum(0))):
+            m[...] = F32(hp.beta1) * m + F32(1 - hp.beta1) * gr
+            v[...] = F32(hp.beta2) * v + F32(1 - hp.beta2) * gr * gr
+            mh = m / F32(1 - hp.beta1 ** t)
+            vh = v / F32(1 - hp.beta2 ** t)
+            p -= F32(hp.lr) * mh / (np.sqrt(vh) + F32(hp.adam_eps))
+    return W, b, g
+
+
+def _oracle_steps(W, b, x, n_pos, k, hp, grads=None):
+    L = O.Layer.from_params(W, b)
+    gW, mW, gb, mb = [], [], [], []
+    for _ in range(k):
+        r = O.layer_step(L, x, n_pos, hp)
+        a, c = grad_magnitudes(r)
+        gW.append(r.dW), mW.append(a), gb.append(r.db), mb.append(c)
+    return L, r, gW, mW, gb, mb
+
+
+CASES = [  # (data seed, weight seed, rows per half, d_in, d_out, steps)
+    (7, 8, 96, 64, 136, 1),     # the smoke step
+    (0, 1, 512, 784, 500, 3),   # the 784->500 layer of the small training config
+    (30, 31, 150, 200, 260, 5),
+]
+
+
+@pytest.mark.parametrize("case", CASES)
+def test_fp32_implementation_passes(case):
+    sd, sw, n, d_in, d_out, k = case
+    x_base, y, y_neg = make_data(sd, n, d_in)
+    (W, b), = make_weights(sw, (d_in, d_out))
+    x = np.concatenate([O.embed_labels(x_base, y, 10), O.embed_labels(x_base, y_neg, 10)])
+    hp = O.HParams(theta=2.0, lr=0.03)
+    W32, b32, g32 = _fp32_steps(W, b, x, n, k, hp)
+    L, r, gW, mW, gb, mb = _oracle_steps(W, b, x, n, k, hp)
+    assert_goodness(g32, r.g)
+    assert_weights(W32, L.W, gW, mW, "W", lr=hp.lr, adam_eps=hp.adam_eps)
+    assert_weights(b32, L.b, gb, mb, "b", lr=hp.lr, adam_eps=hp.adam_eps)
+    assert ill_conditioned(gW, mW, hp.lr, hp.adam_eps, 1e-3 * np.abs(L.W) + 1e-6).mean() < 1e-3
+
+
+def test_smoke_step_needs_the_adam_amplification_rule():
+    """The smoke step has one weight whose gradient is 0.9e-8, next to Adam's
+    eps: g/(|g| + eps) there moves by lr/4 per unit of relative gradient error,
+    so rounding a correct fp32 implementation may make moves that weight past
+    1e-3 relative.  The rule sets aside that element and nothing else."""
+    x_base, y, y_neg = make_data(7, 96, 64)
+    (W, b), = make_weights(8, (64, 136))
+    x = np.concatenate([O.embed_labels(x_base, y, 10), O.embed_labels(x_base, y_neg, 10)])
+    hp = O.HParams(theta=2.0, lr=0.03)
+    L, r, gW, mW, _, _ = _oracle_steps(W, b, x, 96, 1, hp)
+    plain = ill_conditioned(gW, mW)
+    amp = ill_conditioned(gW, mW, hp.lr, hp.adam_eps, 1e-3 * np.abs(L.W) + 1e-6)
+    assert plain.sum() == 0
+    assert list(zip(*np.nonzero(amp))) == [(40, 25)]
+    assert abs(r.dW[40, 25]) < 2e-8
+
+
+@pytest.mark.parametrize("mistake", ["loss_all_rows", "neg_sign", "drop_bias", "no_bias_corr",
+                                     "no_normalise", "transposed_dz"])
+def test_planted_oracle_mistakes_fail(mistake):
+    x_base, y, y_neg = make_data(30, 150, 200)
+    (W, b), = make_weights(31, (200, 260))
+    b = b + 0.05
+    x = np.concatenate([O.embed_labels(x_base, y, 10), O.embed_labels(x_base, y_neg, 10)])
+    hp = O.HParams(theta=2.0, lr=0.03)
+    L, r, gW, mW, gb, mb = _oracle_steps(W, b, x, 150, 2, hp)
+
+    M = O.Layer.from_params(W, b)
+    for _ in range(2):
+        xh = x if mistake == "no_normalise" else O.l2_normalise(x, hp.norm_eps)
+        z = xh @ M.W.T + (0 if mistake == "drop_bias" else M.b)
+        h = np.maximum(z, 0)
+        g = (h * h).sum(1)
+        _, dg = O.ff_loss(g, 150, hp.theta)
+        if mistake == "loss_all_rows":
+            dg = dg / 2
+        if mistake == "neg_sign":
+            dg[150:] = -dg[150:]
+        dz = 2 * dg[:, None] * h
+        if mistake == "transposed_dz":
+            dz = dz[::-1]
+        M.t += 1
+        t = 1 if mistake == "no_bias_corr" else M.t
+        M.W, M.mW, M.vW = O.adam(M.W, M.mW, M.vW, dz.T @ xh, t, hp.lr, hp.beta1, hp.beta2,
+                                 hp.adam_eps)
+        M.b, M.mb, M.vb = O.adam(M.b, M.mb, M.vb, dz.sum(0), t, hp.lr, hp.beta1, hp.beta2,
+                                 hp.adam_eps)
+    with pytest.raises(AssertionError):
+        assert_weights(M.W, L.W, gW, mW, "W", lr=hp.lr, adam_eps=hp.adam_eps)
+        assert_weights(M.b, L.b, gb, mb, "b", lr=hp.lr, adam_eps=hp.adam_eps)
