@@ -188,23 +188,24 @@ hipError_t embed_norm(const ffk::RowMap &src, int rows, int d, float eps, bool n
   });
 }
 
-hipError_t fwd(int dtype, const void *X, const void *W, const float *bias, int M, int N, int K,
-               float *H, float *gpart, hipStream_t st) {
+hipError_t fwd(int dtype, const void *X, const void *W, const float *bias, const float *rowscale,
+               int M, int N, int K, float *H, float *gpart, hipStream_t st) {
   const double eb = (double)elem_bytes(dtype);
   const double nt = ffk::fwd_col_tiles(M, N, dtype);
   const double bytes = (double)M * K * eb + (double)N * K * eb + N * 4.0 +
-                       (H ? (double)M * N * 4.0 : 0.0) + nt * M * 4.0;
+                       (rowscale ? M * 4.0 : 0.0) + (H ? (double)M * N * 4.0 : 0.0) +
+                       nt * M * 4.0;
   return launch(FF_KERNEL_FORWARD, gemm_flops(M, N, K), bytes, st, [&] {
-    return ffk::launch_fwd(dtype, X, W, bias, M, N, K, H, gpart, st);
+    return ffk::launch_fwd(dtype, X, W, bias, rowscale, M, N, K, H, gpart, st);
   });
 }
 
 hipError_t goodness_sum(const float *gpart, int nt, int R, float *g, float *out, int accumulate,
-                        hipStream_t st) {
+                        float *s_out, float norm_eps, hipStream_t st) {
   const double bytes = (double)nt * R * 4.0 + (g ? R * 4.0 : 0.0) +
-                       (out ? R * 4.0 * (accumulate ? 2 : 1) : 0.0);
+                       (out ? R * 4.0 * (accumulate ? 2 : 1) : 0.0) + (s_out ? R * 4.0 : 0.0);
   return launch(FF_KERNEL_GOODNESS, 0.0, bytes, st, [&] {
-    return ffk::launch_goodness(gpart, nt, R, g, out, accumulate, st);
+    return ffk::launch_goodness(gpart, nt, R, g, out, accumulate, s_out, norm_eps, st);
   });
 }
 
@@ -223,36 +224,63 @@ ff_status stage_input(const ffk::RowMap &src, int rows, int d_in, bool normalise
   return FF_OK;
 }
 
-// Forward of one layer on rows described by `src`.
-ff_status forward_core(const ff_layer *L, const ff_hparams *hp, const ffk::RowMap &src, int rows,
-                       bool normalised, float *h_out, float *goodness, StepScratch &s,
+// Input rows of a layer.  `rowscale` (fp32 only) marks raw hidden-activity rows
+// (src.mode == ROWS) whose normalisation 1/(||x_r|| + eps) is already known
+// (from the producing layer's goodness, the squared norm of the row): the
+// products then take the raw rows and apply the scale themselves (the
+// forward to its accumulators, dW to the rows it stages), and no normalised
+// copy is written.
+struct LayerInput {
+  ffk::RowMap src{};
+  bool normalised = false;
+  const float *rowscale = nullptr;
+};
+
+LayerInput raw_rows(const float *x, const float *rowscale) {
+  LayerInput in;
+  in.src.base = x;
+  in.src.mode = ffk::ROWS;
+  in.rowscale = rowscale;
+  return in;
+}
+
+// Forward of one layer; `s_next` (optional) receives the output rows'
+// normalisation for the next layer.
+ff_status forward_core(const ff_layer *L, const ff_hparams *hp, const LayerInput &in, int rows,
+                       float *h_out, float *goodness, float *s_next, StepScratch &s,
                        hipStream_t st) {
-  const void *xop = nullptr;
-  FF_TRY(stage_input(src, rows, L->d_in, normalised, hp->dtype, hp->norm_eps, s.xhat, &xop, st));
-  FF_HIP(fwd(hp->dtype, xop, weight_operand(L, hp->dtype), L->b, rows, L->d_out, L->d_in, h_out,
-             s.gpart, st));
-  if (goodness)
-    FF_HIP(goodness_sum(s.gpart, ffk::fwd_col_tiles(rows, L->d_out, hp->dtype), rows, goodness, nullptr,
-                        0, st));
+  const void *xop = in.src.base;
+  if (!in.rowscale)
+    FF_TRY(stage_input(in.src, rows, L->d_in, in.normalised, hp->dtype, hp->norm_eps, s.xhat,
+                       &xop, st));
+  FF_HIP(fwd(hp->dtype, xop, weight_operand(L, hp->dtype), L->b, in.rowscale, rows, L->d_out,
+             L->d_in, h_out, s.gpart, st));
+  if (goodness || s_next)
+    FF_HIP(goodness_sum(s.gpart, ffk::fwd_col_tiles(rows, L->d_out, hp->dtype), rows, goodness,
+                        nullptr, 0, s_next, hp->norm_eps, st));
   return FF_OK;
 }
 
-// One training step on rows described by `src` (n_pos positives first).
-ff_status step_core(ff_layer *L, const ff_hparams *hp, const ffk::RowMap &src, int n_pos,
-                    int n_neg, bool normalised, float *h_out, float *goodness, float *loss,
+// One training step (n_pos positives first); `s_next` as in forward_core.
+ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int n_pos,
+                    int n_neg, float *h_out, float *goodness, float *loss, float *s_next,
                     StepScratch &s, hipStream_t st) {
   const int R = n_pos + n_neg;
-  const void *xop = nullptr;
-  FF_TRY(stage_input(src, R, L->d_in, normalised, hp->dtype, hp->norm_eps, s.xhat, &xop, st));
+  const void *xop = in.src.base;
+  if (!in.rowscale)
+    FF_TRY(stage_input(in.src, R, L->d_in, in.normalised, hp->dtype, hp->norm_eps, s.xhat, &xop,
+                       st));
   float *H = h_out ? h_out : s.h;
   float *g = goodness ? goodness : s.g;
   float *lo = loss ? loss : s.loss;
   const int nt = ffk::fwd_col_tiles(R, L->d_out, hp->dtype);
-  FF_HIP(fwd(hp->dtype, xop, weight_operand(L, hp->dtype), L->b, R, L->d_out, L->d_in, H, s.gpart,
-             st));
-  FF_HIP(launch(FF_KERNEL_LOSS, 0.0, (double)nt * R * 4.0 + R * (g ? 8.0 : 4.0), st, [&] {
-    return ffk::launch_loss(s.gpart, nt, R, n_pos, hp->theta, g, s.c, s.lpart, st);
-  }));
+  FF_HIP(fwd(hp->dtype, xop, weight_operand(L, hp->dtype), L->b, in.rowscale, R, L->d_out,
+             L->d_in, H, s.gpart, st));
+  FF_HIP(launch(FF_KERNEL_LOSS, 0.0,
+                (double)nt * R * 4.0 + R * (g ? 8.0 : 4.0) + (s_next ? R * 4.0 : 0.0), st, [&] {
+                  return ffk::launch_loss(s.gpart, nt, R, n_pos, hp->theta, g, s.c, s.lpart,
+                                          s_next, hp->norm_eps, st);
+                }));
   ffk::LossFinish lf;
   lf.lpart = s.lpart;
   lf.nblk = ffk::loss_blocks(R);
@@ -270,12 +298,13 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const ffk::RowMap &src, i
   {
     const double eb = (double)elem_bytes(hp->dtype);
     const double params = (double)L->d_out * L->d_in;
-    const double bytes = (double)R * L->d_out * 4.0 + (double)R * L->d_in * eb + R * 4.0 +
+    const double bytes = (double)R * L->d_out * 4.0 + (double)R * L->d_in * eb +
+                         R * (in.rowscale ? 8.0 : 4.0) +
                          params * (24.0 + (hp->dtype == FF_BF16 ? 2.0 : 0.0)) + L->d_out * 24.0;
     FF_HIP(launch(FF_KERNEL_DW_ADAM, gemm_flops(L->d_out, L->d_in, R), bytes, st, [&] {
-      return ffk::launch_dw_adam(hp->dtype, H, s.c, xop, L->d_out, L->d_in, R, L->W, L->mW, L->vW,
-                                 hp->dtype == FF_BF16 ? L->W_bf16 : nullptr, L->b, L->mb, L->vb,
-                                 a, lf, st);
+      return ffk::launch_dw_adam(hp->dtype, H, s.c, xop, in.rowscale, L->d_out, L->d_in, R, L->W,
+                                 L->mW, L->vW, hp->dtype == FF_BF16 ? L->W_bf16 : nullptr, L->b,
+                                 L->mb, L->vb, a, lf, st);
     }));
   }
   return FF_OK;
@@ -352,7 +381,10 @@ ff_status ff_layer_forward(const ff_layer *L, const ff_hparams *hp, const float 
   Carver cv(ws);
   StepScratch s;
   carve_step(cv, s, rows, L->d_in, L->d_out, hp->dtype, true, true, true);
-  return forward_core(L, hp, rows_of(x), rows, x_normalised != 0, h_out, goodness, s,
+  LayerInput in;
+  in.src = rows_of(x);
+  in.normalised = x_normalised != 0;
+  return forward_core(L, hp, in, rows, h_out, goodness, nullptr, s,
                       static_cast<hipStream_t>(stream));
 }
 
@@ -370,7 +402,10 @@ ff_status ff_layer_step(ff_layer *L, const ff_hparams *hp, const float *x, int32
   Carver cv(ws);
   StepScratch s;
   carve_step(cv, s, R, L->d_in, L->d_out, hp->dtype, true, true, true);
-  return step_core(L, hp, rows_of(x), n_pos, n_neg, x_normalised != 0, h_out, goodness, loss, s,
+  LayerInput in;
+  in.src = rows_of(x);
+  in.normalised = x_normalised != 0;
+  return step_core(L, hp, in, n_pos, n_neg, h_out, goodness, loss, nullptr, s,
                    static_cast<hipStream_t>(stream));
 }
 
@@ -388,11 +423,16 @@ ff_status ff_refresh_bf16_shadow(const ff_layer *L, void *stream) {
 // Goodness prediction
 // ---------------------------------------------------------------------------
 namespace {
+// fp32: layer 0 takes normalised rows from x; layer l > 0 takes the raw rows
+// h[(l-1) % 2] with their normalisation rs (written by layer l-1's goodness
+// pass).  bf16: every layer's input is normalised into x (bf16), and h[0]
+// holds each layer's output.
 struct ScoreScratch {
-  void *x = nullptr;        // [rows][max d_in] operand rows
-  float *h = nullptr;       // [rows][max d_out]
-  float *gpart = nullptr;   // [max col tiles][rows]
-  float *scores = nullptr;  // [n][C] when the caller passes none
+  void *x = nullptr;              // [rows][d_in of layer 0] fp32, or [rows][max d_in] bf16
+  float *h[2] = {nullptr, nullptr};  // [rows][max d_out]; h[1] for fp32 stacks of 3+ layers
+  float *rs = nullptr;            // [rows] fp32
+  float *gpart = nullptr;         // [max col tiles][rows]
+  float *scores = nullptr;        // [n][C] when the caller passes none
 };
 
 void carve_score(Carver &cv, ScoreScratch &s, const ff_layer *layers, int n_layers, int n, int C,
@@ -405,8 +445,11 @@ void carve_score(Carver &cv, ScoreScratch &s, const ff_layer *layers, int n_laye
     max_out = std::max(max_out, layers[l].d_out);
     max_nt = std::max(max_nt, ffk::fwd_col_tiles_max(layers[l].d_out));
   }
-  s.x = cv.take(rows * max_in * elem_bytes(dtype));
-  s.h = static_cast<float *>(cv.take(rows * max_out * 4));
+  const bool bf16 = dtype == FF_BF16;
+  s.x = cv.take(rows * (bf16 ? max_in : layers[0].d_in) * elem_bytes(dtype));
+  if (n_layers > 1) s.h[0] = static_cast<float *>(cv.take(rows * max_out * 4));
+  if (n_layers > 2 && !bf16) s.h[1] = static_cast<float *>(cv.take(rows * max_out * 4));
+  if (n_layers > 1 && !bf16) s.rs = static_cast<float *>(cv.take(rows * 4));
   s.gpart = static_cast<float *>(cv.take((size_t)max_nt * rows * 4));
   if (need_scores) s.scores = static_cast<float *>(cv.take((size_t)n * C * 4));
 }
@@ -461,13 +504,19 @@ ff_status score_core(const ff_layer *layers, int32_t n_layers, int32_t first_sco
     for (int l = 0; l < n_layers; ++l) {
       const ff_layer *L = &layers[l];
       const bool last = l + 1 == n_layers;
-      FF_HIP(fwd(hp->dtype, s.x, weight_operand(L, hp->dtype), L->b, rows, L->d_out, L->d_in,
-                 last ? nullptr : s.h, s.gpart, st));
-      if (l >= first_scored_layer)
+      const bool raw = l > 0 && !bf16;
+      const void *X = raw ? s.h[(l - 1) & 1] : s.x;
+      float *H = last ? nullptr : s.h[bf16 ? 0 : (l & 1)];
+      FF_HIP(fwd(hp->dtype, X, weight_operand(L, hp->dtype), L->b, raw ? s.rs : nullptr, rows,
+                 L->d_out, L->d_in, H, s.gpart, st));
+      const bool scored = l >= first_scored_layer;
+      float *s_next = !last && !bf16 ? s.rs : nullptr;
+      if (scored || s_next)
         FF_HIP(goodness_sum(s.gpart, ffk::fwd_col_tiles(rows, L->d_out, hp->dtype), rows, nullptr,
-                            S + (size_t)n0 * n_classes, l > first_scored_layer ? 1 : 0, st));
-      if (!last)
-        FF_HIP(embed_norm(rows_of(s.h), rows, L->d_out, hp->norm_eps, true, bf16, s.x, st));
+                            scored ? S + (size_t)n0 * n_classes : nullptr,
+                            l > first_scored_layer ? 1 : 0, s_next, hp->norm_eps, st));
+      if (!last && bf16)
+        FF_HIP(embed_norm(rows_of(H), rows, L->d_out, hp->norm_eps, true, true, s.x, st));
     }
   }
   FF_HIP(launch(FF_KERNEL_ARGMAX, 0.0, (double)n * n_classes * 4.0 + n * 4.0, st,
@@ -498,10 +547,14 @@ ff_status ff_adaptive_negatives(const ff_layer *layers, int32_t n_layers,
 // Training over chunks: sequential or one stream per layer
 // ---------------------------------------------------------------------------
 namespace {
+// fp32 hidden inputs travel raw, with their row normalisation beside them
+// (slot_s, act_s); bf16 layers normalise their input into their own scratch.
 struct PipeScratch {
   std::vector<StepScratch> step;    // per layer (pipelined) or one shared (sequential)
   std::vector<float *> slot[2];     // pipelined: [l] input slots of layer l (l >= 1)
-  float *act[2] = {nullptr, nullptr};  // sequential: whole-set activations, ping-pong
+  std::vector<float *> slot_s[2];   // pipelined, fp32: [l] row normalisation of slot[.][l]
+  float *act[2] = {nullptr, nullptr};    // sequential: whole-set activations, ping-pong
+  float *act_s[2] = {nullptr, nullptr};  // sequential, fp32: their row normalisation
 };
 
 void carve_pipe(Carver &cv, PipeScratch &p, const ff_layer *layers, int L, int n, int chunk,
@@ -509,14 +562,18 @@ void carve_pipe(Carver &cv, PipeScratch &p, const ff_layer *layers, int L, int n
   const int rows = 2 * std::min(chunk, n);
   if (sched == FF_PIPELINED) {
     p.step.assign(L, StepScratch());
-    p.slot[0].assign(L, nullptr);
-    p.slot[1].assign(L, nullptr);
+    for (int k = 0; k < 2; ++k) {
+      p.slot[k].assign(L, nullptr);
+      p.slot_s[k].assign(L, nullptr);
+    }
     for (int l = 0; l < L; ++l)
-      carve_step(cv, p.step[l], rows, layers[l].d_in, layers[l].d_out, dtype, l + 1 == L, false,
-                 false);
+      carve_step(cv, p.step[l], rows, l == 0 || dtype == FF_BF16 ? layers[l].d_in : 0,
+                 layers[l].d_out, dtype, l + 1 == L, false, false);
     for (int l = 1; l < L; ++l)
-      for (int k = 0; k < 2; ++k)
+      for (int k = 0; k < 2; ++k) {
         p.slot[k][l] = static_cast<float *>(cv.take((size_t)rows * layers[l].d_in * 4));
+        if (dtype == FF_F32) p.slot_s[k][l] = static_cast<float *>(cv.take((size_t)rows * 4));
+      }
   } else {
     int max_in = 0, max_out = 0;
     for (int l = 0; l < L; ++l) {
@@ -528,8 +585,10 @@ void carve_pipe(Carver &cv, PipeScratch &p, const ff_layer *layers, int L, int n
     int max_hidden = 0;
     for (int l = 0; l + 1 < L; ++l) max_hidden = std::max(max_hidden, layers[l].d_out);
     if (L > 1)
-      for (int k = 0; k < 2; ++k)
+      for (int k = 0; k < 2; ++k) {
         p.act[k] = static_cast<float *>(cv.take((size_t)2 * n * max_hidden * 4));
+        if (dtype == FF_F32) p.act_s[k] = static_cast<float *>(cv.take((size_t)2 * n * 4));
+      }
   }
 }
 
@@ -599,24 +658,32 @@ ff_status ff_pipeline_epoch(ff_layer *layers, int32_t n_layers, const ff_hparams
     for (int l = 0; l < n_layers; ++l) {
       ff_layer *L = &layers[l];
       const float *in = l == 0 ? nullptr : p.act[(l - 1) & 1];
+      const float *in_s = l == 0 ? nullptr : p.act_s[(l - 1) & 1];
+      auto input = [&](int start, int b) {
+        if (l == 0) {
+          LayerInput li;
+          li.src = pairs_map(start, b);
+          return li;
+        }
+        return raw_rows(in + (size_t)2 * start * L->d_in,
+                        in_s ? in_s + (size_t)2 * start : nullptr);
+      };
       for (int q = 0; q < steps; ++q) {
         int start, b;
         chunk_map(q % nc, start, b);
-        const ffk::RowMap src = l == 0 ? pairs_map(start, b)
-                                       : rows_of(in + (size_t)2 * start * L->d_in);
-        FF_TRY(step_core(L, hp, src, b, b, false, nullptr, nullptr,
-                         loss_trace ? loss_trace + (size_t)l * steps + q : nullptr, p.step[0],
-                         st));
+        FF_TRY(step_core(L, hp, input(start, b), b, b, nullptr, nullptr,
+                         loss_trace ? loss_trace + (size_t)l * steps + q : nullptr, nullptr,
+                         p.step[0], st));
       }
       if (l + 1 < n_layers) {
         float *out = p.act[l & 1];
+        float *out_s = p.act_s[l & 1];
         for (int c = 0; c < nc; ++c) {
           int start, b;
           chunk_map(c, start, b);
-          const ffk::RowMap src = l == 0 ? pairs_map(start, b)
-                                         : rows_of(in + (size_t)2 * start * L->d_in);
-          FF_TRY(forward_core(L, hp, src, 2 * b, false, out + (size_t)2 * start * L->d_out,
-                              nullptr, p.step[0], st));
+          FF_TRY(forward_core(L, hp, input(start, b), 2 * b, out + (size_t)2 * start * L->d_out,
+                              nullptr, out_s ? out_s + (size_t)2 * start : nullptr, p.step[0],
+                              st));
         }
       }
     }
@@ -641,10 +708,15 @@ ff_status ff_pipeline_epoch(ff_layer *layers, int32_t n_layers, const ff_hparams
       if (l > 0) FF_HIP(hipStreamWaitEvent(st, ring.ev[(size_t)(l - 1) * kRing + q % kRing], 0));
       if (l + 1 < n_layers && q >= 2)
         FF_HIP(hipStreamWaitEvent(st, ring.ev[(size_t)(l + 1) * kRing + (q - 2) % kRing], 0));
-      const ffk::RowMap src = l == 0 ? pairs_map(start, b) : rows_of(p.slot[q & 1][l]);
-      float *h_out = l + 1 < n_layers ? p.slot[q & 1][l + 1] : nullptr;
-      FF_TRY(step_core(L, hp, src, b, b, false, h_out, nullptr,
-                       loss_trace ? loss_trace + (size_t)l * steps + q : nullptr, p.step[l], st));
+      LayerInput in;
+      if (l == 0)
+        in.src = pairs_map(start, b);
+      else
+        in = raw_rows(p.slot[q & 1][l], p.slot_s[q & 1][l]);
+      const bool next = l + 1 < n_layers;
+      FF_TRY(step_core(L, hp, in, b, b, next ? p.slot[q & 1][l + 1] : nullptr, nullptr,
+                       loss_trace ? loss_trace + (size_t)l * steps + q : nullptr,
+                       next ? p.slot_s[q & 1][l + 1] : nullptr, p.step[l], st));
       FF_HIP(hipEventRecord(ring.ev[(size_t)l * kRing + q % kRing], st));
     }
   }

@@ -54,27 +54,35 @@ int fwd_col_tiles_max(int n_cols);
 hipError_t launch_embed_norm(const RowMap &m, int rows, int d, float eps, bool normalise,
                              bool bf16_out, void *out, hipStream_t s);
 
-// H = relu(X W^T + b) (optional store) and per-column-tile goodness partials
-// gpart[tile][M].  X: [M][K], W: [N][K]; fp32 or bf16 operands (dtype).
-hipError_t launch_fwd(int dtype, const void *X, const void *W, const float *bias, int M, int N,
-                      int K, float *H, float *gpart, hipStream_t s);
+// H = relu(diag(rowscale) X W^T + b) (optional store) and per-column-tile
+// goodness partials gpart[tile][M].  X: [M][K], W: [N][K]; fp32 or bf16
+// operands (dtype).  rowscale [M] or null (scale 1): the normalisation of raw
+// input rows, applied to the product.
+hipError_t launch_fwd(int dtype, const void *X, const void *W, const float *bias,
+                      const float *rowscale, int M, int N, int K, float *H, float *gpart,
+                      hipStream_t s);
 
 // g_r = sum_t gpart[t][r] (into g unless null), c_r = 2 dL/dg_r, and loss
-// partials lpart[loss_blocks(R)][2].
+// partials lpart[loss_blocks(R)][2]; s_out (unless null) gets the
+// normalisation 1/(sqrt(g_r) + norm_eps) of the activity rows as the next
+// layer's input (g_r is their squared norm).
 hipError_t launch_loss(const float *gpart, int ntiles, int R, int n_pos, float theta, float *g,
-                       float *c, float *lpart, hipStream_t s);
+                       float *c, float *lpart, float *s_out, float norm_eps, hipStream_t s);
 
 // dW = (c . H)^T Xh contracted over the R rows, db = sum_r c_r H_r, then one
 // Adam update of W (and its bf16 shadow when Wb != nullptr) and of b; also
-// finishes the loss scalar described by lf.
-hipError_t launch_dw_adam(int dtype, const float *H, const float *c, const void *Xh, int M, int N,
-                          int K, float *W, float *mW, float *vW, uint16_t *Wb, float *b, float *mb,
-                          float *vb, const AdamArgs &a, const LossFinish &lf, hipStream_t s);
+// finishes the loss scalar described by lf.  bscale [R] or null (fp32 only):
+// Xh rows are raw and x_hat_r = bscale[r] * Xh_r.
+hipError_t launch_dw_adam(int dtype, const float *H, const float *c, const void *Xh,
+                          const float *bscale, int M, int N, int K, float *W, float *mW,
+                          float *vW, uint16_t *Wb, float *b, float *mb, float *vb,
+                          const AdamArgs &a, const LossFinish &lf, hipStream_t s);
 
 // g_r = sum_t gpart[t][r] into g (any of the outputs may be null);
-// out[r] = g_r (accumulate == 0) or out[r] += g_r (accumulate == 1).
+// out[r] = g_r (accumulate == 0) or out[r] += g_r (accumulate == 1);
+// s_out[r] = 1/(sqrt(g_r) + norm_eps), the next layer's input normalisation.
 hipError_t launch_goodness(const float *gpart, int ntiles, int R, float *g, float *out,
-                           int accumulate, hipStream_t s);
+                           int accumulate, float *s_out, float norm_eps, hipStream_t s);
 
 // pred[n] = argmax_c scores[n][c], lowest c on ties; with `exclude` (C >= 2),
 // c == exclude[n] is skipped.

@@ -400,8 +400,9 @@ __device__ __forceinline__ void nt_mainloop(const typename Operand<BF16>::T *__r
 template <bool BF16, int BM, int BN, int BK, int WM, int WN, int PF, bool STORE_H>
 __global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16>::T *__restrict__ X,
                                                      const typename Operand<BF16>::T *__restrict__ W,
-                                                     const float *__restrict__ bias, int M, int N,
-                                                     int K, float *__restrict__ H,
+                                                     const float *__restrict__ bias,
+                                                     const float *__restrict__ rowscale, int M,
+                                                     int N, int K, float *__restrict__ H,
                                                      float *__restrict__ gpart) {
   using T = typename Operand<BF16>::T;
   constexpr int NT = WM * WN * 64;
@@ -418,10 +419,15 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16
   floatx16 acc[MB][NB];
   nt_mainloop<BF16, BM, BN, BK, WM, WN, PF>(X, W, M, N, K, m0, n0, sm, acc);
 
-  // Epilogue: bias, ReLU, H store, goodness partials.
-  float hsq[MB * 16];
+  // Epilogue: row scale (the input rows' normalisation, when the operand rows
+  // are raw), bias, ReLU, H store, goodness partials.
+  float hsq[MB * 16], rs[MB * 16];
 #pragma unroll
-  for (int q = 0; q < MB * 16; ++q) hsq[q] = 0.f;
+  for (int q = 0; q < MB * 16; ++q) {
+    hsq[q] = 0.f;
+    rs[q] = rowscale ? rowscale[min(m0 + wm * TM + (q >> 4) * 32 + acc_row(q & 15, kg), M - 1)]
+                     : 1.f;
+  }
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     const int col = n0 + wn * TN + nb * 32 + li;
@@ -431,7 +437,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float h = cok ? fmaxf(acc[mb][nb][r] + bv, 0.f) : 0.f;
+        const float h = cok ? fmaxf(fmaf(acc[mb][nb][r], rs[mb * 16 + r], bv), 0.f) : 0.f;
         if (STORE_H) {
           const int row = m0 + wm * TM + mb * 32 + acc_row(r, kg);
           if (row < M && cok) H[(size_t)row * N + col] = h;
@@ -473,7 +479,9 @@ __global__ __launch_bounds__(kLossRows) void k_loss_rows(const float *__restrict
                                                           int R, int n_pos, float theta,
                                                           float *__restrict__ g,
                                                           float *__restrict__ c,
-                                                          float *__restrict__ lpart) {
+                                                          float *__restrict__ lpart,
+                                                          float *__restrict__ s_out,
+                                                          float norm_eps) {
   __shared__ float sp[kLossRows], sn[kLossRows];
   const int r = blockIdx.x * kLossRows + threadIdx.x;
   float lp = 0.f, ln = 0.f;
@@ -481,6 +489,7 @@ __global__ __launch_bounds__(kLossRows) void k_loss_rows(const float *__restrict
     float gv = 0.f;
     for (int t = 0; t < nt; ++t) gv += gpart[(size_t)t * R + r];
     if (g) g[r] = gv;
+    if (s_out) s_out[r] = 1.f / (sqrtf(gv) + norm_eps);  // g is the row's squared norm
     if (r < n_pos) {
       const float x = theta - gv;
       lp = softplus_f(x);
@@ -516,12 +525,13 @@ __global__ __launch_bounds__(kLossRows) void k_loss_rows(const float *__restrict
 // row MB*i + mb; likewise NB consecutive X_hat floats give column NB*j + nb.
 // Half-wave kg takes slab rows 2s+kg.  The loads are issued raw ahead of the
 // MFMAs; the row scale c, the k-tail mask and the db sums are applied when the
-// registers are written to LDS.
+// registers are written to LDS.  With BS the X rows are raw and bscale holds
+// their normalisation (x_hat_k = bscale[k] * X_k), applied there too.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int BK, int WM, int WN, int PF>
+template <int BM, int BN, int BK, int WM, int WN, int PF, bool BS>
 __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
     const float *__restrict__ Hm, const float *__restrict__ cvec, const float *__restrict__ Xh,
-    int M, int N, int K, float *__restrict__ W, float *__restrict__ mW, float *__restrict__ vW,
+    const float *__restrict__ bscale, int M, int N, int K, float *__restrict__ W, float *__restrict__ mW, float *__restrict__ vW,
     uint16_t *__restrict__ Wb, float *__restrict__ bvec, float *__restrict__ mbv,
     float *__restrict__ vbv, AdamArgs ad, LossFinish lf) {
   constexpr int NT = WM * WN * 64;
@@ -562,7 +572,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
 
   struct Stage {
     float4 a[LDA], b[LDB];
-    float c[LDA];
+    float c[LDA], s[BS ? LDB : 1];
     int kt;
   } st[PF];
   float4 dbp = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -574,8 +584,11 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
       g.c[i] = cvec[k];
     }
 #pragma unroll
-    for (int i = 0; i < LDB; ++i)
-      g.b[i] = ld4(pb + (size_t)min(kt * BK + kb + i * KSB, K - 1) * N);
+    for (int i = 0; i < LDB; ++i) {
+      const int k = min(kt * BK + kb + i * KSB, K - 1);
+      g.b[i] = ld4(pb + (size_t)k * N);
+      if constexpr (BS) g.s[i] = bscale[k];
+    }
     g.kt = kt;
   };
   auto sstore = [&](const Stage &g, int buf) {
@@ -596,7 +609,16 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
       st4(As + (buf * BK + ka + i * KSA) * LDM + ca, v);
     }
 #pragma unroll
-    for (int i = 0; i < LDB; ++i) st4(Bs + (buf * BK + kb + i * KSB) * LDN + cb, g.b[i]);
+    for (int i = 0; i < LDB; ++i) {
+      float4 v = g.b[i];
+      if constexpr (BS) {
+        v.x *= g.s[i];
+        v.y *= g.s[i];
+        v.z *= g.s[i];
+        v.w *= g.s[i];
+      }
+      st4(Bs + (buf * BK + kb + i * KSB) * LDN + cb, v);
+    }
   };
 
   floatx16 acc[MB][NB];
@@ -895,12 +917,14 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_bf16(
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kBlock) void k_goodness(const float *__restrict__ gpart, int nt,
                                                      int R, float *__restrict__ g,
-                                                     float *__restrict__ out, int accumulate) {
+                                                     float *__restrict__ out, int accumulate,
+                                                     float *__restrict__ s_out, float norm_eps) {
   const int r = blockIdx.x * kBlock + threadIdx.x;
   if (r >= R) return;
   float gv = 0.f;
   for (int t = 0; t < nt; ++t) gv += gpart[(size_t)t * R + r];
   if (g) g[r] = gv;
+  if (s_out) s_out[r] = 1.f / (sqrtf(gv) + norm_eps);
   if (out) out[r] = accumulate ? out[r] + gv : gv;
 }
 
@@ -989,83 +1013,91 @@ hipError_t launch_embed_norm(const RowMap &m, int rows, int d, float eps, bool n
 }
 
 template <bool BF16, class T>
-void fwd_launch(const void *x, const void *w, const float *bias, int M, int N, int K, float *H,
-                float *gpart, hipStream_t s) {
+void fwd_launch(const void *x, const void *w, const float *bias, const float *rowscale, int M,
+                int N, int K, float *H, float *gpart, hipStream_t s) {
   using E = typename Operand<BF16>::T;
   const dim3 grid(T::tiles(M, N));
   const E *xe = static_cast<const E *>(x);
   const E *we = static_cast<const E *>(w);
   if (H)
     hipLaunchKernelGGL((k_fwd<BF16, T::bm, T::bn, T::bk, T::wm, T::wn, T::pf, true>), grid,
-                       dim3(T::threads), 0, s, xe, we, bias, M, N, K, H, gpart);
+                       dim3(T::threads), 0, s, xe, we, bias, rowscale, M, N, K, H, gpart);
   else
     hipLaunchKernelGGL((k_fwd<BF16, T::bm, T::bn, T::bk, T::wm, T::wn, T::pf, false>), grid,
-                       dim3(T::threads), 0, s, xe, we, bias, M, N, K, H, gpart);
+                       dim3(T::threads), 0, s, xe, we, bias, rowscale, M, N, K, H, gpart);
 }
 
-hipError_t launch_fwd(int dtype, const void *X, const void *W, const float *bias, int M, int N,
-                      int K, float *H, float *gpart, hipStream_t s) {
+hipError_t launch_fwd(int dtype, const void *X, const void *W, const float *bias,
+                      const float *rowscale, int M, int N, int K, float *H, float *gpart,
+                      hipStream_t s) {
   if (M <= 0) return hipSuccess;
   const bool big = fwd_big(M, N, dtype);
   if (dtype == 0) {
     if (big)
-      fwd_launch<false, FwdBig>(X, W, bias, M, N, K, H, gpart, s);
+      fwd_launch<false, FwdBig>(X, W, bias, rowscale, M, N, K, H, gpart, s);
     else
-      fwd_launch<false, FwdSmall>(X, W, bias, M, N, K, H, gpart, s);
+      fwd_launch<false, FwdSmall>(X, W, bias, rowscale, M, N, K, H, gpart, s);
   } else {
     if (big)
-      fwd_launch<true, FwdBigBf16>(X, W, bias, M, N, K, H, gpart, s);
+      fwd_launch<true, FwdBigBf16>(X, W, bias, rowscale, M, N, K, H, gpart, s);
     else
-      fwd_launch<true, FwdSmallBf16>(X, W, bias, M, N, K, H, gpart, s);
+      fwd_launch<true, FwdSmallBf16>(X, W, bias, rowscale, M, N, K, H, gpart, s);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_loss(const float *gpart, int ntiles, int R, int n_pos, float theta, float *g,
-                       float *c, float *lpart, hipStream_t s) {
+                       float *c, float *lpart, float *s_out, float norm_eps, hipStream_t s) {
   hipLaunchKernelGGL(k_loss_rows, dim3(loss_blocks(R)), dim3(kLossRows), 0, s, gpart, ntiles, R,
-                     n_pos, theta, g, c, lpart);
+                     n_pos, theta, g, c, lpart, s_out, norm_eps);
   return hipGetLastError();
 }
 
 template <bool BF16, class T>
-void dw_launch(const float *H, const float *c, const void *Xh, int M, int N, int K, float *W,
-               float *mW, float *vW, uint16_t *Wb, float *b, float *mb, float *vb,
-               const AdamArgs &a, const LossFinish &lf, hipStream_t s) {
+void dw_launch(const float *H, const float *c, const void *Xh, const float *bscale, int M, int N,
+               int K, float *W, float *mW, float *vW, uint16_t *Wb, float *b, float *mb,
+               float *vb, const AdamArgs &a, const LossFinish &lf, hipStream_t s) {
+  const dim3 grid(T::tiles(M, N)), block(T::threads);
   if constexpr (BF16)
-    hipLaunchKernelGGL((k_dw_adam_bf16<T::bm, T::bn, T::bk, T::wm, T::wn, T::pf>),
-                       dim3(T::tiles(M, N)), dim3(T::threads), 0, s, H, c,
-                       static_cast<const uint16_t *>(Xh), M, N, K, W, mW, vW, Wb, b, mb, vb, a,
-                       lf);
+    hipLaunchKernelGGL((k_dw_adam_bf16<T::bm, T::bn, T::bk, T::wm, T::wn, T::pf>), grid, block,
+                       0, s, H, c, static_cast<const uint16_t *>(Xh), M, N, K, W, mW, vW, Wb, b,
+                       mb, vb, a, lf);
+  else if (bscale)
+    hipLaunchKernelGGL((k_dw_adam_f32<T::bm, T::bn, T::bk, T::wm, T::wn, T::pf, true>), grid,
+                       block, 0, s, H, c, static_cast<const float *>(Xh), bscale, M, N, K, W, mW,
+                       vW, Wb, b, mb, vb, a, lf);
   else
-    hipLaunchKernelGGL((k_dw_adam_f32<T::bm, T::bn, T::bk, T::wm, T::wn, T::pf>), dim3(T::tiles(M, N)),
-                       dim3(T::threads), 0, s, H, c, static_cast<const float *>(Xh), M, N, K, W,
-                       mW, vW, Wb, b, mb, vb, a, lf);
+    hipLaunchKernelGGL((k_dw_adam_f32<T::bm, T::bn, T::bk, T::wm, T::wn, T::pf, false>), grid,
+                       block, 0, s, H, c, static_cast<const float *>(Xh), bscale, M, N, K, W, mW,
+                       vW, Wb, b, mb, vb, a, lf);
 }
 
-hipError_t launch_dw_adam(int dtype, const float *H, const float *c, const void *Xh, int M, int N,
-                          int K, float *W, float *mW, float *vW, uint16_t *Wb, float *b, float *mb,
-                          float *vb, const AdamArgs &a, const LossFinish &lf, hipStream_t s) {
+hipError_t launch_dw_adam(int dtype, const float *H, const float *c, const void *Xh,
+                          const float *bscale, int M, int N, int K, float *W, float *mW,
+                          float *vW, uint16_t *Wb, float *b, float *mb, float *vb,
+                          const AdamArgs &a, const LossFinish &lf, hipStream_t s) {
   const bool big = dw_big(M, N, dtype);
   if (dtype == 0) {
     if (big)
-      dw_launch<false, DwBig>(H, c, Xh, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
+      dw_launch<false, DwBig>(H, c, Xh, bscale, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
     else
-      dw_launch<false, DwSmall>(H, c, Xh, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
+      dw_launch<false, DwSmall>(H, c, Xh, bscale, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
   } else {
+    if (bscale) return hipErrorInvalidValue;  // bf16 operands arrive normalised
     if (big)
-      dw_launch<true, DwBigBf16>(H, c, Xh, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
+      dw_launch<true, DwBigBf16>(H, c, Xh, nullptr, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
     else
-      dw_launch<true, DwSmallBf16>(H, c, Xh, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
+      dw_launch<true, DwSmallBf16>(H, c, Xh, nullptr, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf,
+                                   s);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_goodness(const float *gpart, int ntiles, int R, float *g, float *out,
-                           int accumulate, hipStream_t s) {
+                           int accumulate, float *s_out, float norm_eps, hipStream_t s) {
   if (R <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_goodness, dim3(cdiv(R, kBlock)), dim3(kBlock), 0, s, gpart, ntiles, R, g,
-                     out, accumulate);
+                     out, accumulate, s_out, norm_eps);
   return hipGetLastError();
 }
 
