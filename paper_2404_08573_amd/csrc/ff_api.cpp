@@ -176,15 +176,16 @@ inline const void *weight_operand(const ff_layer *L, int dtype) {
 // already normalised; otherwise (and always for bf16) the embed/normalise
 // kernel writes them into scratch.
 hipError_t embed_norm(const ffk::RowMap &src, int rows, int d, float eps, bool normalise,
-                      bool bf16, void *out, hipStream_t st) {
+                      bool bf16, void *out, hipStream_t st, float *scale_out = nullptr) {
   // unique source rows: a chunk's positives and negatives share base rows, and
   // label expansion reads each base row once per label
   const double src_rows = src.mode == ffk::PAIRS    ? (double)src.n_pos
                           : src.mode == ffk::EXPAND ? (double)rows / src.n_classes
                                                     : (double)rows;
-  const double bytes = src_rows * d * 4.0 + (double)rows * d * (bf16 ? 2 : 4);
+  const double bytes = src_rows * d * 4.0 + (double)rows * d * (bf16 ? 2 : 4) +
+                       (scale_out ? rows * 4.0 : 0.0);
   return launch(FF_KERNEL_EMBED_NORM, 0.0, bytes, st, [&] {
-    return ffk::launch_embed_norm(src, rows, d, eps, normalise, bf16, out, st);
+    return ffk::launch_embed_norm(src, rows, d, eps, normalise, bf16, out, scale_out, st);
   });
 }
 
@@ -197,6 +198,21 @@ hipError_t fwd(int dtype, const void *X, const void *W, const float *bias, const
                        nt * M * 4.0;
   return launch(FF_KERNEL_FORWARD, gemm_flops(M, N, K), bytes, st, [&] {
     return ffk::launch_fwd(dtype, X, W, bias, rowscale, M, N, K, H, gpart, st);
+  });
+}
+
+// Shared-base layer-0 forward over M base rows expanded by ex (bytes: the
+// base rows, W, the expanded H and partials).
+hipError_t fwd_expand(int dtype, const void *X, const void *W, const float *bias,
+                      const ffk::LabelExpand &ex, int M, int N, int K, float *H, float *gpart,
+                      hipStream_t st) {
+  const double eb = (double)elem_bytes(dtype);
+  const double rows_out = (double)M * ex.n_exp;
+  const double nt = ffk::fwd_col_tiles(M, N, dtype);
+  const double bytes = (double)M * K * eb + (double)N * K * eb + N * 4.0 + M * 4.0 +
+                       (H ? rows_out * N * 4.0 : 0.0) + nt * rows_out * 4.0;
+  return launch(FF_KERNEL_FORWARD, gemm_flops(M, N, K), bytes, st, [&] {
+    return ffk::launch_fwd_expand(dtype, X, W, bias, ex, M, N, K, H, gpart, st);
   });
 }
 
@@ -427,8 +443,11 @@ namespace {
 // h[(l-1) % 2] with their normalisation rs (written by layer l-1's goodness
 // pass).  bf16: every layer's input is normalised into x (bf16), and h[0]
 // holds each layer's output.
+// With the shared-base layer 0 (n_classes <= kMaxExpand), x first holds the
+// normalised masked base rows [images][d_in of layer 0] and ls their scale.
 struct ScoreScratch {
   void *x = nullptr;              // [rows][d_in of layer 0] fp32, or [rows][max d_in] bf16
+  float *ls = nullptr;            // [images] shared-base scale
   float *h[2] = {nullptr, nullptr};  // [rows][max d_out]; h[1] for fp32 stacks of 3+ layers
   float *rs = nullptr;            // [rows] fp32
   float *gpart = nullptr;         // [max col tiles][rows]
@@ -446,7 +465,10 @@ void carve_score(Carver &cv, ScoreScratch &s, const ff_layer *layers, int n_laye
     max_nt = std::max(max_nt, ffk::fwd_col_tiles_max(layers[l].d_out));
   }
   const bool bf16 = dtype == FF_BF16;
-  s.x = cv.take(rows * (bf16 ? max_in : layers[0].d_in) * elem_bytes(dtype));
+  const bool shared = C <= ffk::kMaxExpand;
+  const size_t x_rows = bf16 && n_layers > 1 ? rows : (shared ? (size_t)nb : rows);
+  s.x = cv.take(x_rows * (bf16 ? max_in : layers[0].d_in) * elem_bytes(dtype));
+  if (shared) s.ls = static_cast<float *>(cv.take((size_t)nb * 4));
   if (n_layers > 1) s.h[0] = static_cast<float *>(cv.take(rows * max_out * 4));
   if (n_layers > 2 && !bf16) s.h[1] = static_cast<float *>(cv.take(rows * max_out * 4));
   if (n_layers > 1 && !bf16) s.rs = static_cast<float *>(cv.take(rows * 4));
@@ -495,24 +517,38 @@ ff_status score_core(const ff_layer *layers, int32_t n_layers, int32_t first_sco
   for (int n0 = 0; n0 < n; n0 += kScoreBlockImages) {
     const int nb = std::min(kScoreBlockImages, n - n0);
     const int rows = nb * n_classes;
+    const bool shared = n_classes <= ffk::kMaxExpand;
     ffk::RowMap m{};
     m.base = x_base;
-    m.mode = ffk::EXPAND;
+    m.mode = shared ? ffk::MASKED : ffk::EXPAND;
     m.base_off = n0;
     m.n_classes = n_classes;
-    FF_HIP(embed_norm(m, rows, layers[0].d_in, hp->norm_eps, true, bf16, s.x, st));
+    FF_HIP(embed_norm(m, shared ? nb : rows, layers[0].d_in, hp->norm_eps, true, bf16, s.x, st,
+                      shared ? s.ls : nullptr));
     for (int l = 0; l < n_layers; ++l) {
       const ff_layer *L = &layers[l];
       const bool last = l + 1 == n_layers;
       const bool raw = l > 0 && !bf16;
       const void *X = raw ? s.h[(l - 1) & 1] : s.x;
       float *H = last ? nullptr : s.h[bf16 ? 0 : (l & 1)];
-      FF_HIP(fwd(hp->dtype, X, weight_operand(L, hp->dtype), L->b, raw ? s.rs : nullptr, rows,
-                 L->d_out, L->d_in, H, s.gpart, st));
+      int nt = ffk::fwd_col_tiles(rows, L->d_out, hp->dtype);
+      if (l == 0 && shared) {
+        ffk::LabelExpand ex{};
+        ex.n_exp = n_classes;
+        ex.n_classes = n_classes;
+        ex.mode = ffk::EXPAND;
+        ex.scale = s.ls;
+        FF_HIP(fwd_expand(hp->dtype, X, weight_operand(L, hp->dtype), L->b, ex, nb, L->d_out,
+                          L->d_in, H, s.gpart, st));
+        nt = ffk::fwd_col_tiles(nb, L->d_out, hp->dtype);
+      } else {
+        FF_HIP(fwd(hp->dtype, X, weight_operand(L, hp->dtype), L->b, raw ? s.rs : nullptr, rows,
+                   L->d_out, L->d_in, H, s.gpart, st));
+      }
       const bool scored = l >= first_scored_layer;
       float *s_next = !last && !bf16 ? s.rs : nullptr;
       if (scored || s_next)
-        FF_HIP(goodness_sum(s.gpart, ffk::fwd_col_tiles(rows, L->d_out, hp->dtype), rows, nullptr,
+        FF_HIP(goodness_sum(s.gpart, nt, rows, nullptr,
                             scored ? S + (size_t)n0 * n_classes : nullptr,
                             l > first_scored_layer ? 1 : 0, s_next, hp->norm_eps, st));
       if (!last && bf16)

@@ -15,7 +15,10 @@ namespace ffk {
 //             (a chunk's positives, then its negatives).
 //   EXPAND:   row r is base row base_off + r / n_classes under label r % n_classes
 //             (every candidate label of every input, for scoring).
-enum RowMode : int32_t { ROWS = 0, PAIRS = 1, EXPAND = 2 };
+//   MASKED:   row r is base row base_off + r with the n_classes label features
+//             zeroed, normalised as if one label feature were 1: the part that
+//             every label embedding of the row shares (same norm for every label).
+enum RowMode : int32_t { ROWS = 0, PAIRS = 1, EXPAND = 2, MASKED = 3 };
 
 struct RowMap {
   const float *base;
@@ -26,6 +29,25 @@ struct RowMap {
   int32_t base_off;
   int32_t n_classes;
 };
+
+// Label expansion of a shared-base layer-0 product.  Base row r (normalised,
+// label features zeroed) gives E output rows, one per label: output row
+// r * E + e under label e (EXPAND), or e * M + r under label lab_e[base_off + r]
+// with lab_0 = lab_a, lab_1 = lab_b (PAIRS: a chunk's positives, then its
+// negatives).  The label feature of the normalised row is scale[r], so output
+// row (r, label) is relu(P_r + scale[r] * W[:, label] + b) with P = X W^T on
+// the masked rows.  PAIRS labels outside [0, n_classes) are clamped into it
+// (the result is then unspecified, but no access leaves W).
+struct LabelExpand {
+  int32_t n_exp;
+  int32_t n_classes;
+  int32_t mode;  // EXPAND or PAIRS
+  const int32_t *lab_a;
+  const int32_t *lab_b;
+  int32_t base_off;
+  const float *scale;  // [M]
+};
+constexpr int kMaxExpand = 16;  // label counts up to this take the shared-base path
 
 struct AdamArgs {
   float lr, beta1, beta2, eps;
@@ -51,8 +73,10 @@ int fwd_col_tiles(int rows, int n_cols, int dtype);
 int fwd_col_tiles_max(int n_cols);
 
 // Embedding (optional) + L2 normalisation (optional) into fp32 or bf16 rows.
+// scale_out [rows] (optional): each row's normalisation factor (rounded to
+// bf16 when bf16_out), i.e. the value a one-hot label feature takes.
 hipError_t launch_embed_norm(const RowMap &m, int rows, int d, float eps, bool normalise,
-                             bool bf16_out, void *out, hipStream_t s);
+                             bool bf16_out, void *out, float *scale_out, hipStream_t s);
 
 // H = relu(diag(rowscale) X W^T + b) (optional store) and per-column-tile
 // goodness partials gpart[tile][M].  X: [M][K], W: [N][K]; fp32 or bf16
@@ -61,6 +85,14 @@ hipError_t launch_embed_norm(const RowMap &m, int rows, int d, float eps, bool n
 hipError_t launch_fwd(int dtype, const void *X, const void *W, const float *bias,
                       const float *rowscale, int M, int N, int K, float *H, float *gpart,
                       hipStream_t s);
+
+// Shared-base layer-0 forward: X [M][K] normalised masked base rows, W [N][K],
+// H [M * ex.n_exp][N] (optional) and gpart[tile][M * ex.n_exp] for the
+// expanded rows (see LabelExpand); the number of goodness partials per row is
+// fwd_col_tiles(M, N, dtype) (tiles follow the base rows).
+hipError_t launch_fwd_expand(int dtype, const void *X, const void *W, const float *bias,
+                             const LabelExpand &ex, int M, int N, int K, float *H, float *gpart,
+                             hipStream_t s);
 
 // g_r = sum_t gpart[t][r] (into g unless null), c_r = 2 dL/dg_r, and loss
 // partials lpart[loss_blocks(R)][2]; s_out (unless null) gets the

@@ -70,6 +70,10 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
 __device__ __forceinline__ uint16_t bf16_of(float a) {
   return __builtin_bit_cast(uint16_t, (__bf16)a);
 }
+__device__ __forceinline__ float bf16_round_f(float a) { return (float)(__bf16)a; }
+__device__ __forceinline__ float bf16_bits_to_f(uint16_t b) {
+  return __uint_as_float((uint32_t)b << 16);
+}
 
 __device__ __forceinline__ float softplus_f(float x) {
   return fmaxf(x, 0.f) + log1pf(expf(-fabsf(x)));
@@ -103,25 +107,31 @@ __device__ __forceinline__ void map_row(const RowMap &m, int r, int &src, int &l
   } else if (m.mode == EXPAND) {
     src = m.base_off + r / m.n_classes;
     lab = r % m.n_classes;
+  } else if (m.mode == MASKED) {
+    src = m.base_off + r;
+    lab = m.n_classes;  // matches no label feature: all of them become 0
   } else {
     src = r;
     lab = -1;
   }
 }
 
+// Features [col, col+4) of a row under label `lab`: the first C features are
+// replaced by one-hot(lab) (all zero when lab >= C); lab < 0 leaves the row as is.
 __device__ __forceinline__ float4 embed4(float4 v, int col, int lab, int C) {
   if (lab >= 0 && col < C) {
-    v.x = (col + 0 == lab) ? 1.f : (col + 0 < C ? 0.f : v.x);
-    v.y = (col + 1 == lab) ? 1.f : (col + 1 < C ? 0.f : v.y);
-    v.z = (col + 2 == lab) ? 1.f : (col + 2 < C ? 0.f : v.z);
-    v.w = (col + 3 == lab) ? 1.f : (col + 3 < C ? 0.f : v.w);
+    v.x = col + 0 < C ? (col + 0 == lab ? 1.f : 0.f) : v.x;
+    v.y = col + 1 < C ? (col + 1 == lab ? 1.f : 0.f) : v.y;
+    v.z = col + 2 < C ? (col + 2 == lab ? 1.f : 0.f) : v.z;
+    v.w = col + 3 < C ? (col + 3 == lab ? 1.f : 0.f) : v.w;
   }
   return v;
 }
 
 template <bool BF16OUT>
 __global__ __launch_bounds__(kBlock) void k_embed_norm(RowMap m, int rows, int d, float eps,
-                                                       int normalise, void *out) {
+                                                       int normalise, void *out,
+                                                       float *scale_out) {
   const int lane = threadIdx.x & 63;
   const int r = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
   if (r >= rows) return;  // uniform per wave
@@ -137,8 +147,10 @@ __global__ __launch_bounds__(kBlock) void k_embed_norm(RowMap m, int rows, int d
       ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
     }
     ss = wave_sum(ss);
+    if (m.mode == MASKED) ss += 1.f;  // the one-hot label feature every embedding carries
     scale = 1.f / (sqrtf(ss) + eps);
   }
+  if (scale_out && lane == 0) scale_out[r] = BF16OUT ? bf16_round_f(scale) : scale;
   for (int i = lane; i < d4; i += 64) {
     float4 v = embed4(ld4(xr + 4 * i), 4 * i, lab, m.n_classes);
     v.x *= scale;
@@ -465,6 +477,136 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16
 #pragma unroll
       for (int w = 0; w < WN; ++w) g += gs[w * BM + t];
       gpart[(size_t)tn * M + row] = g;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Shared-base layer-0 forward.  Every label embedding of an input row has the
+// same norm (one label feature is 1), so with x_hat = s * (masked row + e_label)
+// the product splits into P = X_masked_hat W^T, computed once per base row on
+// the main loop above, plus s * W[:, label] per label.  The epilogue expands
+// each base row into its E labelled output rows: bias, ReLU, H store and the
+// goodness partials of each.  The tile's label columns of W are staged in LDS
+// (converted from bf16 bits in bf16 mode, where s is already bf16-rounded, so
+// s * W_label is exact in fp32).
+// ---------------------------------------------------------------------------
+template <bool BF16, int BM, int BN, int BK, int WM, int WN, int PF, bool STORE_H>
+__global__ __launch_bounds__(WM *WN * 64) void k_fwd_expand(
+    const typename Operand<BF16>::T *__restrict__ X, const typename Operand<BF16>::T *__restrict__ W,
+    const float *__restrict__ bias, LabelExpand ex, int M, int N, int K, float *__restrict__ H,
+    float *__restrict__ gpart) {
+  using T = typename Operand<BF16>::T;
+  constexpr int NT = WM * WN * 64;
+  constexpr int TM = BM / WM, TN = BN / WN, MB = TM / 32, NB = TN / 32;
+  constexpr int kMain = nt_lds_elems<BF16, BM, BN, BK>() * (int)sizeof(T) / 4;  // in floats
+  constexpr int kEpi = kMaxExpand * (WN * BM + BN);
+  __shared__ __attribute__((aligned(16))) float smf[kMain > kEpi ? kMain : kEpi];
+  const int nt = (N + BN - 1) / BN;
+  int tm, tn;
+  tile_of(blockIdx.x, (M + BM - 1) / BM, nt, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int li = lane & 31, kg = lane >> 5;
+  const int E = ex.n_exp;
+  const int C = ex.mode == EXPAND ? E : 0;  // label columns staged (EXPAND: labels 0..E-1)
+
+  floatx16 acc[MB][NB];
+  nt_mainloop<BF16, BM, BN, BK, WM, WN, PF>(X, W, M, N, K, m0, n0, reinterpret_cast<T *>(smf),
+                                            acc);
+
+  // LDS after the main loop: gs [E][WN][BM] goodness partials, wl [BN][kMaxExpand].
+  float *gs = smf;
+  float *wl = smf + kMaxExpand * WN * BM;
+  if (C > 0)
+    for (int i = tid; i < BN * C; i += NT) {
+      const int j = i / C, c = i % C;
+      const int col = min(n0 + j, N - 1);
+      if constexpr (BF16)
+        wl[j * kMaxExpand + c] = bf16_bits_to_f(W[(size_t)col * K + c]);
+      else
+        wl[j * kMaxExpand + c] = W[(size_t)col * K + c];
+    }
+  __syncthreads();
+
+  float sr[MB * 16];
+  int rows[MB * 16];
+#pragma unroll
+  for (int q = 0; q < MB * 16; ++q) {
+    rows[q] = m0 + wm * TM + (q >> 4) * 32 + acc_row(q & 15, kg);
+    sr[q] = ex.scale[min(rows[q], M - 1)];
+  }
+  float bv[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int col = n0 + wn * TN + nb * 32 + li;
+    bv[nb] = col < N ? bias[col] : 0.f;
+  }
+
+  for (int e = 0; e < E; ++e) {
+    float hsq[MB * 16];
+#pragma unroll
+    for (int q = 0; q < MB * 16; ++q) hsq[q] = 0.f;
+    int lab[MB * 16];
+    if (ex.mode != EXPAND) {
+      const int32_t *lp = e == 0 ? ex.lab_a : ex.lab_b;
+#pragma unroll
+      for (int q = 0; q < MB * 16; ++q)
+        lab[q] = min(max(lp[ex.base_off + min(rows[q], M - 1)], 0), ex.n_classes - 1);
+    }
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int cl = wn * TN + nb * 32 + li;
+      const int col = n0 + cl;
+      const bool cok = col < N;
+      const float we = C > 0 ? wl[cl * kMaxExpand + e] : 0.f;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int q = mb * 16 + r;
+          float wlab = we;
+          if (ex.mode != EXPAND) {
+            const size_t wi = (size_t)min(col, N - 1) * K + lab[q];
+            if constexpr (BF16)
+              wlab = bf16_bits_to_f(W[wi]);
+            else
+              wlab = W[wi];
+          }
+          const float h = cok ? fmaxf(acc[mb][nb][r] + fmaf(sr[q], wlab, bv[nb]), 0.f) : 0.f;
+          if (STORE_H && cok && rows[q] < M) {
+            const size_t orow = ex.mode == EXPAND ? (size_t)rows[q] * E + e
+                                                  : (size_t)e * M + rows[q];
+            H[orow * N + col] = h;
+          }
+          hsq[q] += h * h;
+        }
+    }
+    rowsum_scatter(hsq, lane);
+    float *g = gs + e * WN * BM;
+    if constexpr (MB == 1) {
+      const int q = (lane & 31) >> 1;
+      if ((lane & 1) == 0) g[wn * BM + wm * TM + acc_row(q, kg)] = hsq[0];
+    } else {
+#pragma unroll
+      for (int j = 0; j < MB / 2; ++j) {
+        const int q = j + (MB / 2) * (lane & 31);
+        g[wn * BM + wm * TM + (q >> 4) * 32 + acc_row(q & 15, kg)] = hsq[j];
+      }
+    }
+  }
+  __syncthreads();
+  const size_t MO = (size_t)M * E;
+  for (int i = tid; i < BM * E; i += NT) {
+    const int t = i % BM, e = i / BM;
+    const int row = m0 + t;
+    if (row < M) {
+      float g = 0.f;
+#pragma unroll
+      for (int w = 0; w < WN; ++w) g += gs[(e * WN + w) * BM + t];
+      const size_t orow = ex.mode == EXPAND ? (size_t)row * E + e : (size_t)e * M + row;
+      gpart[(size_t)tn * MO + orow] = g;
     }
   }
 }
@@ -1000,15 +1142,15 @@ int fwd_col_tiles_max(int n_cols) {
 int loss_blocks(int rows) { return (int)cdiv(rows, kLossRows); }
 
 hipError_t launch_embed_norm(const RowMap &m, int rows, int d, float eps, bool normalise,
-                             bool bf16_out, void *out, hipStream_t s) {
+                             bool bf16_out, void *out, float *scale_out, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   const dim3 grid(cdiv(rows, kBlock / 64));
   if (bf16_out)
     hipLaunchKernelGGL(k_embed_norm<true>, grid, dim3(kBlock), 0, s, m, rows, d, eps,
-                       (int)normalise, out);
+                       (int)normalise, out, scale_out);
   else
     hipLaunchKernelGGL(k_embed_norm<false>, grid, dim3(kBlock), 0, s, m, rows, d, eps,
-                       (int)normalise, out);
+                       (int)normalise, out, scale_out);
   return hipGetLastError();
 }
 
@@ -1042,6 +1184,44 @@ hipError_t launch_fwd(int dtype, const void *X, const void *W, const float *bias
       fwd_launch<true, FwdBigBf16>(X, W, bias, rowscale, M, N, K, H, gpart, s);
     else
       fwd_launch<true, FwdSmallBf16>(X, W, bias, rowscale, M, N, K, H, gpart, s);
+  }
+  return hipGetLastError();
+}
+
+template <bool BF16, class T>
+void fwd_expand_launch(const void *x, const void *w, const float *bias, const LabelExpand &ex,
+                       int M, int N, int K, float *H, float *gpart, hipStream_t s) {
+  using E = typename Operand<BF16>::T;
+  const dim3 grid(T::tiles(M, N));
+  const E *xe = static_cast<const E *>(x);
+  const E *we = static_cast<const E *>(w);
+  if (H)
+    hipLaunchKernelGGL((k_fwd_expand<BF16, T::bm, T::bn, T::bk, T::wm, T::wn, T::pf, true>),
+                       grid, dim3(T::threads), 0, s, xe, we, bias, ex, M, N, K, H, gpart);
+  else
+    hipLaunchKernelGGL((k_fwd_expand<BF16, T::bm, T::bn, T::bk, T::wm, T::wn, T::pf, false>),
+                       grid, dim3(T::threads), 0, s, xe, we, bias, ex, M, N, K, H, gpart);
+}
+
+hipError_t launch_fwd_expand(int dtype, const void *X, const void *W, const float *bias,
+                             const LabelExpand &ex, int M, int N, int K, float *H, float *gpart,
+                             hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (ex.n_exp < 1 || ex.n_exp > kMaxExpand || ex.n_classes < 1 || ex.n_classes > K ||
+      (ex.mode == EXPAND && ex.n_exp != ex.n_classes) || (ex.mode == PAIRS && ex.n_exp != 2) ||
+      (ex.mode != EXPAND && ex.mode != PAIRS))
+    return hipErrorInvalidValue;
+  const bool big = fwd_big(M, N, dtype);
+  if (dtype == 0) {
+    if (big)
+      fwd_expand_launch<false, FwdBig>(X, W, bias, ex, M, N, K, H, gpart, s);
+    else
+      fwd_expand_launch<false, FwdSmall>(X, W, bias, ex, M, N, K, H, gpart, s);
+  } else {
+    if (big)
+      fwd_expand_launch<true, FwdBigBf16>(X, W, bias, ex, M, N, K, H, gpart, s);
+    else
+      fwd_expand_launch<true, FwdSmallBf16>(X, W, bias, ex, M, N, K, H, gpart, s);
   }
   return hipGetLastError();
 }

@@ -199,6 +199,21 @@ def test_score_ragged_blocks_and_tiny(P):
                                         x_base[:1], 7, O.HParams(), 1)[1][0]
 
 
+@pytest.mark.parametrize("n_classes,first", [(16, 0), (17, 1), (20, 0)])
+def test_score_label_counts_around_shared_base_limit(P, n_classes, first):
+    """Up to 16 labels layer 0 runs once per input and expands per label in its
+    epilogue; above that every labelled row is embedded and multiplied."""
+    x_base, _, _ = make_data(66, 300, 40, 0.5)
+    params = make_weights(67, (40, 68, 24, 12))
+    layers = [P.Layer(_t(W), _t(b)) for W, b in params]
+    S = torch.empty(300, n_classes, device=DEV)
+    _, pred = P.ff_score_labels(layers, P.HParams(), _t(x_base), n_classes, first, scores=S)
+    S_ref, p_ref = O.score_labels([O.Layer.from_params(W, b) for W, b in params], x_base,
+                                  n_classes, O.HParams(), first)
+    assert_goodness(_np(S), S_ref, what="scores")
+    assert_labels(_np(pred), S_ref, p_ref)
+
+
 def test_score_full_size_sampled(P):
     """All 10 000 inputs through 784->2000x4 on the GPU; the oracle checks a sample."""
     w = WORKLOADS["mnist_score_784_2000x4"]
