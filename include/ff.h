@@ -172,7 +172,9 @@ size_t ff_pipeline_workspace_size(const ff_layer *layers, int32_t n_layers, int3
  *     layer l has finished chunk c-1.  The result depends only on these
  *     dependencies, not on how the streams interleave.
  *   layers (host) [n_layers] chained; x_base (device) [n][layers[0].d_in];
- *   y_pos, y_neg (device) [n] int32; streams (host) [n_layers] (only [0] is
+ *   y_pos, y_neg (device) [n] int32 in [0, n_classes) (other values give
+ *   unspecified results, without out-of-bounds accesses); streams (host)
+ *   [n_layers] (only [0] is
  *   read for FF_SEQUENTIAL); loss_trace (device) [n_layers][epochs*n_chunks]
  *   or NULL.  The caller must not touch the layers or ws until all streams
  *   have drained. */

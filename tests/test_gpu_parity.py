@@ -295,14 +295,14 @@ def test_adaptive_negatives_training_set_sampled(P):
 
 
 # ------------------------------------------------------------------ schedules
-def _pipe(P, sched, n, dims, chunk, epochs, seed, hp_kw, streams=None):
+def _pipe(P, sched, n, dims, chunk, epochs, seed, hp_kw, streams=None, n_classes=10):
     x_base, y, y_neg = make_data(seed, n, dims[0])
     params = make_weights(seed + 1, dims)
     layers = [P.Layer(_t(W), _t(b)) for W, b in params]
     nc = -(-n // chunk)
     trace = torch.zeros(len(layers), nc * epochs, device=DEV)
-    P.ff_pipeline_epoch(layers, P.HParams(**hp_kw), _t(x_base), _t(y), _t(y_neg), 10, chunk,
-                        epochs, sched, streams=streams, loss_trace=trace)
+    P.ff_pipeline_epoch(layers, P.HParams(**hp_kw), _t(x_base), _t(y), _t(y_neg), n_classes,
+                        chunk, epochs, sched, streams=streams, loss_trace=trace)
     torch.cuda.synchronize()
     return layers, _np(trace), (x_base, y, y_neg, params)
 
@@ -318,6 +318,22 @@ def test_pipeline_parity_small(P, sched):
     np.testing.assert_allclose(trace, tr_ref, rtol=2e-4)
     for L, R in zip(layers, ref):
         assert L.step == tr_ref.shape[1]
+        np.testing.assert_allclose(_np(L.W), R.W, rtol=1e-3, atol=2e-4)
+
+
+@pytest.mark.parametrize("sched", [0, 1])
+def test_pipeline_parity_many_labels(P, sched):
+    """17 label features: above the label count whose layer-0 products share the
+    pair's base row, so every labelled row is embedded and multiplied."""
+    hp_kw = dict(theta=2.0, lr=0.03)
+    dims = (64, 96, 48)
+    layers, trace, (x_base, y, y_neg, params) = _pipe(P, sched, 200, dims, 64, 1, 71, hp_kw,
+                                                      n_classes=17)
+    ref = [O.Layer.from_params(W, b) for W, b in params]
+    fn = O.train_sequential if sched == 0 else O.train_pipelined
+    tr_ref = fn(ref, x_base, y, y_neg, 17, 64, 1, O.HParams(**hp_kw))
+    np.testing.assert_allclose(trace, tr_ref, rtol=2e-4)
+    for L, R in zip(layers, ref):
         np.testing.assert_allclose(_np(L.W), R.W, rtol=1e-3, atol=2e-4)
 
 
