@@ -210,7 +210,9 @@ typedef struct {
   double bytes;       /* algorithmic HBM bytes of those launches             */
 } ff_kernel_stats;
 
-ff_status ff_profile_start(int32_t max_launches);
+/* kind_mask: bit k selects kernel kind k (0 selects every kind); launches of
+ * other kinds run without events. */
+ff_status ff_profile_start(int32_t max_launches, uint32_t kind_mask);
 ff_status ff_profile_stop(ff_kernel_stats *stats /* (host) [FF_KERNEL_KINDS] */);
 
 #ifdef __cplusplus

@@ -81,7 +81,7 @@ def _load() -> ctypes.CDLL:
         "ff_pipeline_epoch": (c_int32, [POINTER(ff_layer), c_int32, POINTER(ff_hparams), P, P, P,
                                         c_int32, c_int32, c_int32, c_int32, c_int32,
                                         POINTER(c_void_p), P, P, c_size_t]),
-        "ff_profile_start": (c_int32, [c_int32]),
+        "ff_profile_start": (c_int32, [c_int32, ctypes.c_uint32]),
         "ff_profile_stop": (c_int32, [POINTER(ff_kernel_stats)]),
     }
     for name, (res, args) in sig.items():
@@ -310,8 +310,10 @@ def ff_pipeline_epoch(layers: List[Layer], hp: HParams, x_base: torch.Tensor, y_
     return loss_trace
 
 
-def ff_profile_start(max_launches: int = 65536):
-    _check(LIB.ff_profile_start(max_launches))
+def ff_profile_start(max_launches: int = 65536, kinds=None):
+    """kinds: names from KERNEL_KINDS to time (None: every kind)."""
+    mask = 0 if kinds is None else sum(1 << KERNEL_KINDS.index(k) for k in kinds)
+    _check(LIB.ff_profile_start(max_launches, mask))
 
 
 def ff_profile_stop() -> dict:

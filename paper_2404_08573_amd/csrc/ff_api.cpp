@@ -69,6 +69,7 @@ struct ProfRec {
 struct Profiler {
   std::mutex mu;
   bool on = false;
+  uint32_t mask = ~0u;  // kinds timed while on
   std::vector<hipEvent_t> pool;
   size_t used = 0;
   std::vector<ProfRec> recs;
@@ -80,7 +81,7 @@ Profiler g_prof;
 template <class F>
 hipError_t launch(int kind, double flops, double bytes, hipStream_t st, F fn) {
   std::unique_lock<std::mutex> lk(g_prof.mu);
-  if (!g_prof.on || g_prof.used + 2 > g_prof.pool.size()) {
+  if (!g_prof.on || !((g_prof.mask >> kind) & 1u) || g_prof.used + 2 > g_prof.pool.size()) {
     lk.unlock();
     return fn();
   }
@@ -762,7 +763,7 @@ ff_status ff_pipeline_epoch(ff_layer *layers, int32_t n_layers, const ff_hparams
 // ---------------------------------------------------------------------------
 // Kernel timing
 // ---------------------------------------------------------------------------
-ff_status ff_profile_start(int32_t max_launches) {
+ff_status ff_profile_start(int32_t max_launches, uint32_t kind_mask) {
   if (max_launches <= 0) return fail(FF_ERR_INVALID_ARG, "max_launches=%d", max_launches);
   std::lock_guard<std::mutex> lk(g_prof.mu);
   if (g_prof.on) return fail(FF_ERR_INVALID_ARG, "a profile is already active");
@@ -778,6 +779,7 @@ ff_status ff_profile_start(int32_t max_launches) {
   }
   g_prof.used = 0;
   g_prof.recs.clear();
+  g_prof.mask = kind_mask ? kind_mask : ~0u;
   g_prof.on = true;
   return FF_OK;
 }

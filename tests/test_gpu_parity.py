@@ -464,3 +464,26 @@ def test_pipeline_parity_bf16(P):
     for L, R in zip(layers, ref):
         d = np.linalg.norm(_np(L.W) - R.W) / np.linalg.norm(R.W)
         assert d < 1e-3, d
+
+
+# ------------------------------------------------------------------ kernel timing
+def test_profile_counts_and_kind_mask(P):
+    """Every launch of a step is timed and its work counted; a kind mask times
+    only the selected kinds."""
+    (W, b), = make_weights(90, (64, 96))
+    L = P.Layer(_t(W), _t(b))
+    x = _t(random_matrix(91, 40, 64, 0, 1))
+    P.ff_layer_step(L, P.HParams(), x, 20, 20)
+    torch.cuda.synchronize()
+    P.ff_profile_start(64)
+    P.ff_layer_step(L, P.HParams(), x, 20, 20)
+    allk = P.ff_profile_stop()
+    for k in ("embed_norm", "forward", "loss", "dw_adam"):
+        assert allk[k]["launches"] == 1 and allk[k]["total_ms"] > 0, k
+    assert allk["forward"]["flops"] == 2.0 * 40 * 64 * 96
+    assert allk["dw_adam"]["flops"] == 2.0 * 96 * 64 * 40
+    P.ff_profile_start(64, kinds=["forward"])
+    P.ff_layer_step(L, P.HParams(), x, 20, 20)
+    only = P.ff_profile_stop()
+    assert only["forward"]["launches"] == 1
+    assert all(v["launches"] == 0 for k, v in only.items() if k != "forward")
