@@ -17,8 +17,8 @@
 //                  staged rows, and the Adam update of W and b fused in the epilogue
 //                  (no split over rows, so every dW tile is final in one workgroup);
 //                  its first thread also finishes the loss scalar in a fixed order.
-//   k_dw_adam_bf16 the same on v_mfma_f32_32x32x16_bf16: the staging transposes
-//                  row-major operands into k-contiguous LDS rows in registers.
+//   k_dw_adam_bf16 the same on v_mfma_f32_32x32x16_bf16: tiles staged in their
+//                  natural layout, MFMA fragments through LDS transpose reads.
 //   k_goodness, k_argmax, k_bf16_shadow: small row/elementwise kernels.
 //
 // Every reduction runs in a fixed order, so results are bitwise reproducible
@@ -830,18 +830,29 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
   }
 }
 
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+
+// gfx950 LDS transpose read (ds_read_b64_tr_b16).  Within each group of 16
+// lanes, lane j receives element j % 4 of the 8 bytes addressed by lane
+// 4e + j / 4 as its element e (e = 0..3): when lane s of the group addresses
+// row k0 + s / 4, columns c0 + 4 (s % 4) .. +3 of a row-major b16 tile, lane j
+// gets column c0 + j at rows k0 .. k0 + 3.  (Lane layout measured on MI355X.)
+__device__ __forceinline__ uint2 lds_read_tr(const uint16_t *p) {
+  const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4 *)(p));
+  return __builtin_bit_cast(uint2, v);
+}
+
 // ---------------------------------------------------------------------------
 // bf16 dW = bf16(c.H)^T X_hat (+ db from the fp32 c.H) with the Adam update
 // fused.  M = d_out, N = d_in, K = R batch rows; H fp32 [K][M], X_hat bf16
-// [K][N].  v_mfma_f32_32x32x16_bf16 takes eight k-consecutive values per lane,
-// so the staging transposes: a thread loads an 8-row x 4-column block of each
-// operand (rows = batch rows), scales the H rows by c in fp32 (summing db
-// there), rounds to bf16, and writes four k-contiguous 16-byte rows to LDS.
-// LDS row p of an operand tile holds tile column 4*(p % G) + p / G (G = tile
-// width / 4), so the 32 threads that write one instruction's rows hit 32
-// consecutive rows (conflict-free) and the MFMA lanes read consecutive rows.
-// The epilogue writes the accumulators to an LDS tile in natural order, then
-// applies Adam with coalesced float4 accesses to W and its moments.
+// [K][N], both row-major over the contraction index.  Both LDS tiles keep that
+// natural layout ([BK][BM] and [BK][BN], rows padded to 16 banks mod 64):
+// staging is a coalesced copy, with H rows scaled by c in fp32 (db summed
+// there) and rounded to bf16 (R3).  The MFMA fragments, eight k-consecutive
+// values per lane, come from two transposed LDS reads each.  The accumulators
+// go through an LDS tile so that the fused Adam reads and writes W and its
+// moments with float4 accesses.
 // ---------------------------------------------------------------------------
 template <int BM, int BN, int BK, int WM, int WN, int PF>
 __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_bf16(
@@ -852,19 +863,18 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_bf16(
     LossFinish lf) {
   constexpr int NT = WM * WN * 64;
   constexpr int TM = BM / WM, TN = BN / WN, MB = TM / 32, NB = TN / 32;
-  constexpr int LDK = BK + 8;               // bf16 elements; rows padded by 16 bytes
-  constexpr int GA = BM / 4, GB = BN / 4;   // 4-column groups per tile
-  constexpr int KB8 = BK / 8;               // 8-row groups per slab
-  constexpr int APT = GA * KB8 / NT, BPT = GB * KB8 / NT;  // staging blocks per thread
-  constexpr int LDC = BN + 4;
-  static_assert(MB * 32 == TM && NB * 32 == TN, "wave tile is whole 32x32 blocks");
-  static_assert(APT * NT == GA * KB8 && BPT * NT == GB * KB8, "tile/threads");
-  static_assert(NT % GA == 0 && NT % GB == 0 && (BK / 2) % 8 == 0, "staging layout");
-  constexpr int kMainFloats = (2 * (BM + BN) * LDK) / 2;
-  constexpr int kSmFloats = kMainFloats > BM * LDC ? kMainFloats : BM * LDC;
-  __shared__ __attribute__((aligned(16))) float smf[kSmFloats];
-  uint16_t *As = reinterpret_cast<uint16_t *>(smf);  // [2][BM][LDK]
-  uint16_t *Bs = As + 2 * BM * LDK;                  // [2][BN][LDK]
+  constexpr int LDA = BM + 32, LDB = BN + 32;  // row strides (bf16): 16 banks mod 64
+  constexpr int CA = BM / 4, CB = BN / 8;      // float4 (A) / 8-bf16 (B) chunks per row
+  constexpr int RA = NT / CA, RB = NT / CB;    // slab rows between a thread's chunks
+  constexpr int APT = BK / RA, BPT = BK / RB;
+  static_assert(MB * 32 == TM && NB * 32 == TN, "wave tile");
+  static_assert(APT * RA == BK && BPT * RB == BK && NT % CA == 0 && NT % CB == 0, "staging");
+  static_assert(BK % 16 == 0, "k16 steps");
+  constexpr int LDC = BN + 4;  // fp32 accumulator tile for the epilogue
+  constexpr int kMain = 2 * BK * (LDA + LDB), kEpi = 2 * BM * LDC;  // in bf16 elements
+  __shared__ __attribute__((aligned(16))) uint16_t sm[kMain > kEpi ? kMain : kEpi];
+  uint16_t *As = sm;                 // [2][BK][LDA]
+  uint16_t *Bs = sm + 2 * BK * LDA;  // [2][BK][LDB]
 
   const int nt = (N + BN - 1) / BN;
   int tm, tn;
@@ -884,85 +894,53 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_bf16(
     lf.loss[0] = sp / (float)lf.n_pos + sn / (float)lf.n_neg;
   }
 
-  // Column groups are fixed per thread (NT is a multiple of the group counts).
-  // Groups past the matrix edge read a clamped valid group whose results are
-  // never stored.
-  const int ga = tid % GA, gb = tid % GB;
-  const float *pa = Hm + min(m0 + 4 * ga, M - 4);
-  const uint16_t *pb = Xh + min(n0 + 4 * gb, N - 4);
+  const int ca = tid % CA, ra = tid / CA;
+  const int cb = tid % CB, rb = tid / CB;
+  const float *pa = Hm + min(m0 + 4 * ca, M - 4);
+  const uint16_t *pb = Xh + min(n0 + 8 * cb, N - 8);
 
   struct Stage {
-    float4 a[APT][8];
-    float c[APT][8];
-    uint2 b[BPT][8];
+    float4 a[APT];
+    float c[APT];
+    uint4 b[BPT];
     int kt;
   } st[PF];
   float4 dbp = make_float4(0.f, 0.f, 0.f, 0.f);
   auto gload = [&](Stage &g, int kt) {
 #pragma unroll
     for (int i = 0; i < APT; ++i) {
-      const int k0 = kt * BK + 8 * ((tid + i * NT) / GA);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int k = min(k0 + j, K - 1);
-        g.a[i][j] = ld4(pa + (size_t)k * M);
-        g.c[i][j] = cvec[k];
-      }
+      const int k = min(kt * BK + ra + i * RA, K - 1);
+      g.a[i] = ld4(pa + (size_t)k * M);
+      g.c[i] = cvec[k];
     }
 #pragma unroll
-    for (int i = 0; i < BPT; ++i) {
-      const int k0 = kt * BK + 8 * ((tid + i * NT) / GB);
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        g.b[i][j] = *reinterpret_cast<const uint2 *>(pb + (size_t)min(k0 + j, K - 1) * N);
-    }
+    for (int i = 0; i < BPT; ++i)
+      g.b[i] = ld16(pb + (size_t)min(kt * BK + rb + i * RB, K - 1) * N);
     g.kt = kt;
   };
   auto sstore = [&](const Stage &g, int buf) {
 #pragma unroll
     for (int i = 0; i < APT; ++i) {
-      const int kb = (tid + i * NT) / GA;
-      const int k0 = g.kt * BK + 8 * kb;
-      float4 v[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float cc = k0 + j < K ? g.c[i][j] : 0.f;  // rows past K add nothing
-        v[j] = make_float4(g.a[i][j].x * cc, g.a[i][j].y * cc, g.a[i][j].z * cc,
-                           g.a[i][j].w * cc);
-        if (do_db) {
-          dbp.x += v[j].x;
-          dbp.y += v[j].y;
-          dbp.z += v[j].z;
-          dbp.w += v[j].w;
-        }
+      const int r = ra + i * RA;
+      const float cc = g.kt * BK + r < K ? g.c[i] : 0.f;  // rows past K add nothing
+      float4 v = g.a[i];
+      v.x *= cc;
+      v.y *= cc;
+      v.z *= cc;
+      v.w *= cc;
+      if (do_db) {
+        dbp.x += v.x;
+        dbp.y += v.y;
+        dbp.z += v.z;
+        dbp.w += v.w;
       }
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {  // tile column 4*ga + q, eight k values
-        uint4 row;
-        row.x = pack_bf16(comp(v[0], q), comp(v[1], q));
-        row.y = pack_bf16(comp(v[2], q), comp(v[3], q));
-        row.z = pack_bf16(comp(v[4], q), comp(v[5], q));
-        row.w = pack_bf16(comp(v[6], q), comp(v[7], q));
-        st16(As + (buf * BM + q * GA + ga) * LDK + 8 * kb, row);
-      }
+      uint2 p;
+      p.x = pack_bf16(v.x, v.y);
+      p.y = pack_bf16(v.z, v.w);
+      *reinterpret_cast<uint2 *>(As + (buf * BK + r) * LDA + 4 * ca) = p;
     }
 #pragma unroll
-    for (int i = 0; i < BPT; ++i) {
-      const int kb = (tid + i * NT) / GB;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {  // tile column 4*gb + q: the q-th bf16 of each row
-        const int sh = (q & 1) * 16;
-        uint32_t e[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) e[j] = ((q < 2 ? g.b[i][j].x : g.b[i][j].y) >> sh) & 0xFFFFu;
-        uint4 row;
-        row.x = e[0] | (e[1] << 16);
-        row.y = e[2] | (e[3] << 16);
-        row.z = e[4] | (e[5] << 16);
-        row.w = e[6] | (e[7] << 16);
-        st16(Bs + (buf * BN + q * GB + gb) * LDK + 8 * kb, row);
-      }
-    }
+    for (int i = 0; i < BPT; ++i) st16(Bs + (buf * BK + rb + i * RB) * LDB + 8 * cb, g.b[i]);
   };
 
   floatx16 acc[MB][NB];
@@ -973,16 +951,32 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_bf16(
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.f;
 
+  // Transposed fragment reads: within each 16-lane group g of the wave, lane
+  // s reads row 8*(g/2) + 4*t + s/4 of the k16 step, columns 16*(g%2) + 4*(s%4)
+  // .. +3 of the 32-wide block; the transpose hands lane (g, j) the values of
+  // column 16*(g%2) + j at 4 consecutive k.  Two reads (t = 0, 1) give the 8
+  // k-consecutive values v_mfma_f32_32x32x16_bf16 takes per lane.
+  const int g4 = lane >> 4, s16 = lane & 15;
+  const int frow = 8 * (g4 >> 1) + (s16 >> 2);
+  const int fcol = 16 * (g4 & 1) + 4 * (s16 & 3);
   auto compute = [&](int buf) {
-    const uint16_t *a0 = As + (buf * BM + wm * TM + li) * LDK + kg * (BK / 2);
-    const uint16_t *b0 = Bs + (buf * BN + wn * TN + li) * LDK + kg * (BK / 2);
+    const uint16_t *a0 = As + (buf * BK + frow) * LDA + wm * TM + fcol;
+    const uint16_t *b0 = Bs + (buf * BK + frow) * LDB + wn * TN + fcol;
 #pragma unroll
-    for (int sv = 0; sv < BK / 2; sv += 8) {
+    for (int k16 = 0; k16 < BK; k16 += 16) {
       uint4 a[MB], b[NB];
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) a[mb] = ld16(a0 + mb * 32 * LDK + sv);
+      for (int mb = 0; mb < MB; ++mb) {
+        const uint2 lo = lds_read_tr(a0 + k16 * LDA + mb * 32);
+        const uint2 hi = lds_read_tr(a0 + (k16 + 4) * LDA + mb * 32);
+        a[mb] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+      }
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) b[nb] = ld16(b0 + nb * 32 * LDK + sv);
+      for (int nb = 0; nb < NB; ++nb) {
+        const uint2 lo = lds_read_tr(b0 + k16 * LDB + nb * 32);
+        const uint2 hi = lds_read_tr(b0 + (k16 + 4) * LDB + nb * 32);
+        b[nb] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+      }
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -994,23 +988,17 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_bf16(
 
   kloop<PF>((K + BK - 1) / BK, gload, sstore, compute, st);
 
-  // Accumulators to a natural-order LDS tile (undoing the row permutation).
-  float *Cs = smf;  // [BM][LDC]; the main-loop buffers are free after the last barrier
+  // Accumulators to an LDS tile in natural order, then Adam with float4
+  // accesses along d_in (the main-loop buffers are free after the last barrier).
+  float *Cs = reinterpret_cast<float *>(sm);  // [BM][LDC]
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int q = wn * TN + nb * 32 + li;
-      const int n = 4 * (q % GB) + q / GB;
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int p = wm * TM + mb * 32 + acc_row(r, kg);
-        Cs[(4 * (p % GA) + p / GA) * LDC + n] = acc[mb][nb][r];
-      }
-    }
+      for (int r = 0; r < 16; ++r)
+        Cs[(wm * TM + mb * 32 + acc_row(r, kg)) * LDC + wn * TN + nb * 32 + li] = acc[mb][nb][r];
   __syncthreads();
-
-  // Adam on the tile, float4 along d_in.
   for (int idx = tid; idx < BM * (BN / 4); idx += NT) {
     const int m = idx / (BN / 4), n4 = (idx % (BN / 4)) * 4;
     const int row = m0 + m, col = n0 + n4;
@@ -1033,18 +1021,17 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_bf16(
     }
   }
 
-  // db and Adam on b (column-tile 0 only).
   if (do_db) {
     __syncthreads();  // Cs reads are done
-    float *red = smf;  // [NT / GA][BM]
-    st4(red + (tid / GA) * BM + 4 * ga, dbp);
+    float *red = reinterpret_cast<float *>(sm);  // [RA][BM]
+    st4(red + ra * BM + 4 * ca, dbp);
     __syncthreads();
     for (int t = tid; t < BM; t += NT) {
       const int row = m0 + t;
       if (row >= M) continue;
       float sum = 0.f;
 #pragma unroll
-      for (int g2 = 0; g2 < NT / GA; ++g2) sum += red[g2 * BM + t];
+      for (int g2 = 0; g2 < RA; ++g2) sum += red[g2 * BM + t];
       float p = bvec[row], m = mbv[row], v = vbv[row];
       adam_update(p, m, v, sum, ad);
       bvec[row] = p;
@@ -1119,8 +1106,8 @@ using DwBig = Tile<64, 128, 32, 2, 4, 3>;
 using DwSmall = Tile<64, 64, 32, 2, 2, 2>;
 using FwdBigBf16 = Tile<128, 128, 64, 4, 2, 2>;
 using FwdSmallBf16 = Tile<64, 64, 64, 2, 2, 2>;
-using DwBigBf16 = Tile<128, 128, 64, 2, 2, 1>;
-using DwSmallBf16 = Tile<64, 64, 128, 2, 2, 1>;
+using DwBigBf16 = Tile<128, 128, 32, 4, 2, 2>;
+using DwSmallBf16 = Tile<64, 64, 64, 2, 2, 2>;
 
 inline bool fwd_big(int M, int N, int dtype) {
   return (dtype ? FwdBigBf16::tiles(M, N) : FwdBig::tiles(M, N)) >= kCUs;
