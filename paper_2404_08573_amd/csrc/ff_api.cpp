@@ -208,8 +208,8 @@ hipError_t fwd_expand(int dtype, const void *X, const void *W, const float *bias
                       const ffk::LabelExpand &ex, int M, int N, int K, float *H, float *gpart,
                       hipStream_t st) {
   const double eb = (double)elem_bytes(dtype);
-  const double rows_out = (double)M * ex.n_exp;
-  const double nt = ffk::fwd_col_tiles(M, N, dtype);
+  const double rows_out = (double)M * ex.n_classes;
+  const double nt = ffk::fwd_expand_col_tiles(M, N, dtype);
   const double bytes = (double)M * K * eb + (double)N * K * eb + N * 4.0 + M * 4.0 +
                        (H ? rows_out * N * 4.0 : 0.0) + nt * rows_out * 4.0;
   return launch(FF_KERNEL_FORWARD, gemm_flops(M, N, K), bytes, st, [&] {
@@ -535,13 +535,11 @@ ff_status score_core(const ff_layer *layers, int32_t n_layers, int32_t first_sco
       int nt = ffk::fwd_col_tiles(rows, L->d_out, hp->dtype);
       if (l == 0 && shared) {
         ffk::LabelExpand ex{};
-        ex.n_exp = n_classes;
         ex.n_classes = n_classes;
-        ex.mode = ffk::EXPAND;
         ex.scale = s.ls;
         FF_HIP(fwd_expand(hp->dtype, X, weight_operand(L, hp->dtype), L->b, ex, nb, L->d_out,
                           L->d_in, H, s.gpart, st));
-        nt = ffk::fwd_col_tiles(nb, L->d_out, hp->dtype);
+        nt = ffk::fwd_expand_col_tiles(nb, L->d_out, hp->dtype);
       } else {
         FF_HIP(fwd(hp->dtype, X, weight_operand(L, hp->dtype), L->b, raw ? s.rs : nullptr, rows,
                    L->d_out, L->d_in, H, s.gpart, st));

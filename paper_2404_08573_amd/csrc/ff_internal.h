@@ -30,21 +30,13 @@ struct RowMap {
   int32_t n_classes;
 };
 
-// Label expansion of a shared-base layer-0 product.  Base row r (normalised,
-// label features zeroed) gives E output rows, one per label: output row
-// r * E + e under label e (EXPAND), or e * M + r under label lab_e[base_off + r]
-// with lab_0 = lab_a, lab_1 = lab_b (PAIRS: a chunk's positives, then its
-// negatives).  The label feature of the normalised row is scale[r], so output
-// row (r, label) is relu(P_r + scale[r] * W[:, label] + b) with P = X W^T on
-// the masked rows.  PAIRS labels outside [0, n_classes) are clamped into it
-// (the result is then unspecified, but no access leaves W).
+// Label expansion of a shared-base layer-0 product (scoring).  Base row r
+// (normalised, label features zeroed) gives n_classes output rows, row
+// r * n_classes + c under label c.  The label feature of the normalised row is
+// scale[r], so output row (r, c) is relu(P_r + scale[r] * W[:, c] + b) with
+// P = X W^T on the masked rows.
 struct LabelExpand {
-  int32_t n_exp;
   int32_t n_classes;
-  int32_t mode;  // EXPAND or PAIRS
-  const int32_t *lab_a;
-  const int32_t *lab_b;
-  int32_t base_off;
   const float *scale;  // [M]
 };
 constexpr int kMaxExpand = 16;  // label counts up to this take the shared-base path
@@ -71,6 +63,7 @@ int loss_blocks(int rows);
 // upper bound over all row counts (for sizing scratch).
 int fwd_col_tiles(int rows, int n_cols, int dtype);
 int fwd_col_tiles_max(int n_cols);
+int fwd_expand_col_tiles(int rows, int n_cols, int dtype);
 
 // Embedding (optional) + L2 normalisation (optional) into fp32 or bf16 rows.
 // scale_out [rows] (optional): each row's normalisation factor (rounded to
@@ -87,9 +80,9 @@ hipError_t launch_fwd(int dtype, const void *X, const void *W, const float *bias
                       hipStream_t s);
 
 // Shared-base layer-0 forward: X [M][K] normalised masked base rows, W [N][K],
-// H [M * ex.n_exp][N] (optional) and gpart[tile][M * ex.n_exp] for the
+// H [M * ex.n_classes][N] (optional) and gpart[tile][M * ex.n_classes] for the
 // expanded rows (see LabelExpand); the number of goodness partials per row is
-// fwd_col_tiles(M, N, dtype) (tiles follow the base rows).
+// fwd_expand_col_tiles(M, N, dtype) (tiles follow the base rows).
 hipError_t launch_fwd_expand(int dtype, const void *X, const void *W, const float *bias,
                              const LabelExpand &ex, int M, int N, int K, float *H, float *gpart,
                              hipStream_t s);

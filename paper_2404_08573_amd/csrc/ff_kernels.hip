@@ -509,82 +509,56 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd_expand(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int li = lane & 31, kg = lane >> 5;
-  const int E = ex.n_exp;
-  const int C = ex.mode == EXPAND ? E : 0;  // label columns staged (EXPAND: labels 0..E-1)
+  const int C = ex.n_classes;
 
   floatx16 acc[MB][NB];
   nt_mainloop<BF16, BM, BN, BK, WM, WN, PF>(X, W, M, N, K, m0, n0, reinterpret_cast<T *>(smf),
                                             acc);
 
-  // LDS after the main loop: gs [E][WN][BM] goodness partials, wl [BN][kMaxExpand].
+  // LDS after the main loop: gs [C][WN][BM] goodness partials, wl [BN][kMaxExpand]
+  // the tile's label columns of W.
   float *gs = smf;
   float *wl = smf + kMaxExpand * WN * BM;
-  if (C > 0)
-    for (int i = tid; i < BN * C; i += NT) {
-      const int j = i / C, c = i % C;
-      const int col = min(n0 + j, N - 1);
-      if constexpr (BF16)
-        wl[j * kMaxExpand + c] = bf16_bits_to_f(W[(size_t)col * K + c]);
-      else
-        wl[j * kMaxExpand + c] = W[(size_t)col * K + c];
-    }
+  for (int i = tid; i < BN * C; i += NT) {
+    const int j = i / C, c = i % C;
+    const int col = min(n0 + j, N - 1);
+    if constexpr (BF16)
+      wl[j * kMaxExpand + c] = bf16_bits_to_f(W[(size_t)col * K + c]);
+    else
+      wl[j * kMaxExpand + c] = W[(size_t)col * K + c];
+  }
   __syncthreads();
 
+  const int rbase = m0 + wm * TM;
   float sr[MB * 16];
-  int rows[MB * 16];
 #pragma unroll
-  for (int q = 0; q < MB * 16; ++q) {
-    rows[q] = m0 + wm * TM + (q >> 4) * 32 + acc_row(q & 15, kg);
-    sr[q] = ex.scale[min(rows[q], M - 1)];
-  }
-  float bv[NB];
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const int col = n0 + wn * TN + nb * 32 + li;
-    bv[nb] = col < N ? bias[col] : 0.f;
-  }
+  for (int q = 0; q < MB * 16; ++q)
+    sr[q] = ex.scale[min(rbase + (q >> 4) * 32 + acc_row(q & 15, kg), M - 1)];
 
-  for (int e = 0; e < E; ++e) {
+  for (int c = 0; c < C; ++c) {
     float hsq[MB * 16];
 #pragma unroll
     for (int q = 0; q < MB * 16; ++q) hsq[q] = 0.f;
-    int lab[MB * 16];
-    if (ex.mode != EXPAND) {
-      const int32_t *lp = e == 0 ? ex.lab_a : ex.lab_b;
-#pragma unroll
-      for (int q = 0; q < MB * 16; ++q)
-        lab[q] = min(max(lp[ex.base_off + min(rows[q], M - 1)], 0), ex.n_classes - 1);
-    }
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       const int cl = wn * TN + nb * 32 + li;
       const int col = n0 + cl;
       const bool cok = col < N;
-      const float we = C > 0 ? wl[cl * kMaxExpand + e] : 0.f;
+      const float bv = cok ? bias[col] : 0.f;
+      const float wc = wl[cl * kMaxExpand + c];
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int q = mb * 16 + r;
-          float wlab = we;
-          if (ex.mode != EXPAND) {
-            const size_t wi = (size_t)min(col, N - 1) * K + lab[q];
-            if constexpr (BF16)
-              wlab = bf16_bits_to_f(W[wi]);
-            else
-              wlab = W[wi];
-          }
-          const float h = cok ? fmaxf(acc[mb][nb][r] + fmaf(sr[q], wlab, bv[nb]), 0.f) : 0.f;
-          if (STORE_H && cok && rows[q] < M) {
-            const size_t orow = ex.mode == EXPAND ? (size_t)rows[q] * E + e
-                                                  : (size_t)e * M + rows[q];
-            H[orow * N + col] = h;
-          }
+          const int row = rbase + mb * 32 + acc_row(r, kg);
+          const float h = cok ? fmaxf(acc[mb][nb][r] + fmaf(sr[q], wc, bv), 0.f) : 0.f;
+          if (STORE_H && cok && row < M) H[((size_t)row * C + c) * N + col] = h;
           hsq[q] += h * h;
         }
     }
     rowsum_scatter(hsq, lane);
-    float *g = gs + e * WN * BM;
+    float *g = gs + c * WN * BM;
     if constexpr (MB == 1) {
       const int q = (lane & 31) >> 1;
       if ((lane & 1) == 0) g[wn * BM + wm * TM + acc_row(q, kg)] = hsq[0];
@@ -597,16 +571,15 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd_expand(
     }
   }
   __syncthreads();
-  const size_t MO = (size_t)M * E;
-  for (int i = tid; i < BM * E; i += NT) {
-    const int t = i % BM, e = i / BM;
+  const size_t MO = (size_t)M * C;
+  for (int i = tid; i < BM * C; i += NT) {
+    const int t = i % BM, c = i / BM;
     const int row = m0 + t;
     if (row < M) {
       float g = 0.f;
 #pragma unroll
-      for (int w = 0; w < WN; ++w) g += gs[(e * WN + w) * BM + t];
-      const size_t orow = ex.mode == EXPAND ? (size_t)row * E + e : (size_t)e * M + row;
-      gpart[(size_t)tn * MO + orow] = g;
+      for (int w = 0; w < WN; ++w) g += gs[(c * WN + w) * BM + t];
+      gpart[(size_t)tn * MO + (size_t)row * C + c] = g;
     }
   }
 }
@@ -1091,8 +1064,8 @@ inline unsigned cdiv(long a, long b) { return (unsigned)((a + b - 1) / b); }
 // ---------------------------------------------------------------------------
 // GEMM tile configurations: (BM, BN, BK in elements, waves along M, waves
 // along N, register stages of the load pipeline), measured on MI355X over
-// the layer shapes of the workloads.  A launch takes the large tile when its
-// tiles alone fill every CU, else the small one.
+// the layer shapes of the workloads.  A weight-gradient launch takes the large
+// tile when its tiles alone fill every CU, else the small one.
 template <int BM, int BN, int BK, int WM, int WN, int PF = 1>
 struct Tile {
   static constexpr int bm = BM, bn = BN, bk = BK, wm = WM, wn = WN, pf = PF,
@@ -1100,30 +1073,72 @@ struct Tile {
   static long tiles(int m, int n) { return (long)cdiv(m, BM) * cdiv(n, BN); }
 };
 constexpr int kCUs = 256;
-using FwdBig = Tile<128, 128, 32, 4, 2, 2>;
-using FwdSmall = Tile<64, 64, 32, 2, 2, 2>;
 using DwBig = Tile<64, 128, 32, 2, 4, 3>;
 using DwSmall = Tile<64, 64, 32, 2, 2, 2>;
-using FwdBigBf16 = Tile<128, 128, 64, 4, 2, 2>;
-using FwdSmallBf16 = Tile<64, 64, 64, 2, 2, 2>;
 using DwBigBf16 = Tile<128, 128, 32, 4, 2, 2>;
 using DwSmallBf16 = Tile<64, 64, 64, 2, 2, 2>;
 
-inline bool fwd_big(int M, int N, int dtype) {
-  return (dtype ? FwdBigBf16::tiles(M, N) : FwdBig::tiles(M, N)) >= kCUs;
+// Forward tile ladder: a launch takes the largest tile whose grid still puts a
+// workgroup on every CU.  bf16 products need the larger tiles for operand
+// reuse (a 128x128 bf16 tile asks about as many operand bytes per cycle as a
+// CU can load at full MFMA rate); fp32 measured no faster above 128x128.
+template <bool BF16>
+struct FwdTiles;
+template <>
+struct FwdTiles<false> {
+  using Huge = Tile<128, 128, 32, 4, 2, 2>;
+  using Large = Huge;
+  using Big = Huge;
+  using Small = Tile<64, 64, 32, 2, 2, 2>;
+};
+template <>
+struct FwdTiles<true> {
+  using Huge = Tile<256, 256, 64, 4, 2, 2>;
+  using Large = Tile<256, 192, 64, 4, 2, 2>;
+  using Big = Tile<128, 128, 64, 4, 2, 2>;
+  using Small = Tile<64, 64, 64, 2, 2, 2>;
+};
+template <class T>
+struct TileTag {
+  using type = T;
+};
+// LARGE = false: the label-expanding forward, whose epilogue holds more per
+// row, stays on the 128x128 / 64x64 rungs.
+template <bool BF16, bool LARGE = true, class F>
+void fwd_tile(int M, int N, F &&f) {
+  using L = FwdTiles<BF16>;
+  if constexpr (LARGE) {
+    if (L::Huge::tiles(M, N) >= kCUs) return f(TileTag<typename L::Huge>{});
+    if (L::Large::tiles(M, N) >= kCUs) return f(TileTag<typename L::Large>{});
+  }
+  if (L::Big::tiles(M, N) >= kCUs) return f(TileTag<typename L::Big>{});
+  f(TileTag<typename L::Small>{});
 }
+
 inline bool dw_big(int M, int N, int dtype) {
   return (dtype ? DwBigBf16::tiles(M, N) : DwBig::tiles(M, N)) >= kCUs;
 }
 
 int fwd_col_tiles(int rows, int n_cols, int dtype) {
-  const int bn = dtype ? (fwd_big(rows, n_cols, dtype) ? FwdBigBf16::bn : FwdSmallBf16::bn)
-                       : (fwd_big(rows, n_cols, dtype) ? FwdBig::bn : FwdSmall::bn);
+  int bn = 0;
+  auto pick = [&](auto t) { bn = decltype(t)::type::bn; };
+  if (dtype)
+    fwd_tile<true>(rows, n_cols, pick);
+  else
+    fwd_tile<false>(rows, n_cols, pick);
+  return (int)cdiv(n_cols, bn);
+}
+int fwd_expand_col_tiles(int rows, int n_cols, int dtype) {
+  int bn = 0;
+  auto pick = [&](auto t) { bn = decltype(t)::type::bn; };
+  if (dtype)
+    fwd_tile<true, false>(rows, n_cols, pick);
+  else
+    fwd_tile<false, false>(rows, n_cols, pick);
   return (int)cdiv(n_cols, bn);
 }
 int fwd_col_tiles_max(int n_cols) {
-  return (int)cdiv(n_cols, std::min(std::min(FwdBig::bn, FwdSmall::bn),
-                                    std::min(FwdBigBf16::bn, FwdSmallBf16::bn)));
+  return (int)cdiv(n_cols, std::min(FwdTiles<false>::Small::bn, FwdTiles<true>::Small::bn));
 }
 
 int loss_blocks(int rows) { return (int)cdiv(rows, kLossRows); }
@@ -1160,18 +1175,14 @@ hipError_t launch_fwd(int dtype, const void *X, const void *W, const float *bias
                       const float *rowscale, int M, int N, int K, float *H, float *gpart,
                       hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  const bool big = fwd_big(M, N, dtype);
-  if (dtype == 0) {
-    if (big)
-      fwd_launch<false, FwdBig>(X, W, bias, rowscale, M, N, K, H, gpart, s);
-    else
-      fwd_launch<false, FwdSmall>(X, W, bias, rowscale, M, N, K, H, gpart, s);
-  } else {
-    if (big)
-      fwd_launch<true, FwdBigBf16>(X, W, bias, rowscale, M, N, K, H, gpart, s);
-    else
-      fwd_launch<true, FwdSmallBf16>(X, W, bias, rowscale, M, N, K, H, gpart, s);
-  }
+  if (dtype == 0)
+    fwd_tile<false>(M, N, [&](auto t) {
+      fwd_launch<false, typename decltype(t)::type>(X, W, bias, rowscale, M, N, K, H, gpart, s);
+    });
+  else
+    fwd_tile<true>(M, N, [&](auto t) {
+      fwd_launch<true, typename decltype(t)::type>(X, W, bias, rowscale, M, N, K, H, gpart, s);
+    });
   return hipGetLastError();
 }
 
@@ -1194,22 +1205,16 @@ hipError_t launch_fwd_expand(int dtype, const void *X, const void *W, const floa
                              const LabelExpand &ex, int M, int N, int K, float *H, float *gpart,
                              hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  if (ex.n_exp < 1 || ex.n_exp > kMaxExpand || ex.n_classes < 1 || ex.n_classes > K ||
-      (ex.mode == EXPAND && ex.n_exp != ex.n_classes) || (ex.mode == PAIRS && ex.n_exp != 2) ||
-      (ex.mode != EXPAND && ex.mode != PAIRS))
+  if (ex.n_classes < 1 || ex.n_classes > kMaxExpand || ex.n_classes > K)
     return hipErrorInvalidValue;
-  const bool big = fwd_big(M, N, dtype);
-  if (dtype == 0) {
-    if (big)
-      fwd_expand_launch<false, FwdBig>(X, W, bias, ex, M, N, K, H, gpart, s);
-    else
-      fwd_expand_launch<false, FwdSmall>(X, W, bias, ex, M, N, K, H, gpart, s);
-  } else {
-    if (big)
-      fwd_expand_launch<true, FwdBigBf16>(X, W, bias, ex, M, N, K, H, gpart, s);
-    else
-      fwd_expand_launch<true, FwdSmallBf16>(X, W, bias, ex, M, N, K, H, gpart, s);
-  }
+  if (dtype == 0)
+    fwd_tile<false, false>(M, N, [&](auto t) {
+      fwd_expand_launch<false, typename decltype(t)::type>(X, W, bias, ex, M, N, K, H, gpart, s);
+    });
+  else
+    fwd_tile<true, false>(M, N, [&](auto t) {
+      fwd_expand_launch<true, typename decltype(t)::type>(X, W, bias, ex, M, N, K, H, gpart, s);
+    });
   return hipGetLastError();
 }
 

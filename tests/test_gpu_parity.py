@@ -374,7 +374,10 @@ def test_tiny_config_end_to_end(P):
 
 
 # ------------------------------------------------------------------ bf16 operands
-BF16_FWD_SHAPES = [(1, 16, 8), (300, 200, 260), (2048, 784, 2000), (2100, 2000, 2004)]
+# The last two select the 256x256 and 256x192 bf16 tiles (grids of at least one
+# tile per CU), with ragged row, column and k tails.
+BF16_FWD_SHAPES = [(1, 16, 8), (300, 200, 260), (2048, 784, 2000), (2100, 2000, 2004),
+                   (4200, 72, 4100), (4100, 136, 3000)]
 
 
 @pytest.mark.parametrize("rows,d_in,d_out", BF16_FWD_SHAPES)
