@@ -274,6 +274,97 @@ def adaptive_negatives(layers: Sequence[Layer], x_base: np.ndarray, labels: np.n
 
 
 # ----------------------------------------------------------------------------
+# Softmax prediction head (Sec. 3 "Prediction", Sec. 5, Sec. 5.1)
+# ----------------------------------------------------------------------------
+NEUTRAL_LABEL = 0.1
+
+
+def embed_neutral(x_base: np.ndarray, n_classes: int) -> np.ndarray:
+    """Neutral label for Softmax prediction (Sec. 3): every label feature is 0.1."""
+    x = np.array(x_base, dtype=F64, copy=True)
+    x[:, :n_classes] = NEUTRAL_LABEL
+    return x
+
+
+@dataclasses.dataclass
+class Head:
+    """The softmax layer: ``W[C][D]``, ``b[C]`` and their Adam moments, float64."""
+    W: np.ndarray
+    b: np.ndarray
+    mW: np.ndarray
+    vW: np.ndarray
+    mb: np.ndarray
+    vb: np.ndarray
+    t: int = 0
+
+    @staticmethod
+    def from_params(W, b) -> "Head":
+        W = np.array(W, dtype=F64)
+        b = np.array(b, dtype=F64)
+        return Head(W, b, np.zeros_like(W), np.zeros_like(W), np.zeros_like(b),
+                    np.zeros_like(b))
+
+
+def head_features(layers: Sequence[Layer], x_base: np.ndarray, n_classes: int, hp: HParams,
+                  first_layer: int = 1) -> np.ndarray:
+    """Input of the softmax layer: one pass of the neutrally labelled input through
+    the FF layers (no update), keeping the activity vectors of the hidden layers
+    from ``first_layer`` on ("all but the first hidden layer": 1).  Reading: each
+    activity vector enters length-normalised, ``h / (||h|| + norm_eps)``, the form in
+    which the next layer receives it.  Returns ``A[n, sum of their widths]``.
+    """
+    a = embed_neutral(x_base, n_classes)
+    feats = []
+    for li, L in enumerate(layers):
+        _, _, a, _ = layer_forward(L.W, L.b, a, hp.norm_eps, False, hp.bf16)
+        if li >= first_layer:
+            feats.append(l2_normalise(a, hp.norm_eps))
+    return np.concatenate(feats, axis=1)
+
+
+def softmax_xent(logits: np.ndarray, y: np.ndarray) -> Tuple[float, np.ndarray, np.ndarray]:
+    """Mean cross-entropy of softmax(logits) against labels y, its gradient with
+    respect to the logits, and the probabilities.  Softmax is taken after
+    subtracting each row's maximum (the same value in exact arithmetic)."""
+    z = np.asarray(logits, dtype=F64)
+    z = z - z.max(axis=1, keepdims=True)
+    e = np.exp(z)
+    p = e / e.sum(axis=1, keepdims=True)
+    n = z.shape[0]
+    loss = float(np.mean(np.log(e.sum(axis=1)) - z[np.arange(n), y]))
+    d = p.copy()
+    d[np.arange(n), y] -= 1.0
+    return loss, d / n, p
+
+
+def head_step(head: Head, layers: Sequence[Layer], x_base: np.ndarray, y: np.ndarray,
+              n_classes: int, hp: HParams, head_hp: HParams, first_layer: int = 1):
+    """One training step of the softmax layer on a batch (Sec. 3: trained by
+    backpropagation, which stops at the softmax layer; Sec. 5.1: Adam).  The FF
+    layers are not changed.  Returns ``(loss, logits, dW, db)``; mutates ``head``."""
+    A = head_features(layers, x_base, n_classes, hp, first_layer)
+    logits = A @ head.W.T + head.b
+    loss, d, _ = softmax_xent(logits, np.asarray(y, dtype=np.int64))
+    dW = d.T @ A
+    db = d.sum(axis=0)
+    head.t += 1
+    head.W, head.mW, head.vW = adam(head.W, head.mW, head.vW, dW, head.t, head_hp.lr,
+                                    head_hp.beta1, head_hp.beta2, head_hp.adam_eps)
+    head.b, head.mb, head.vb = adam(head.b, head.mb, head.vb, db, head.t, head_hp.lr,
+                                    head_hp.beta1, head_hp.beta2, head_hp.adam_eps)
+    return loss, logits, dW, db
+
+
+def head_predict(head: Head, layers: Sequence[Layer], x_base: np.ndarray, n_classes: int,
+                 hp: HParams, first_layer: int = 1) -> Tuple[np.ndarray, np.ndarray]:
+    """Softmax prediction: a single pass, then the most probable class (the largest
+    logit; lowest class on ties).  Returns ``(logits[n, C], pred[n])``."""
+    A = head_features(layers, x_base, n_classes, hp, first_layer)
+    logits = A @ head.W.T + head.b
+    return logits, np.argmax(logits, axis=1).astype(np.int32)
+
+
+# ----------------------------------------------------------------------------
 # Training schedules over chunks (Sec. 3 sequential FF, Sec. 4.1 Alg. 1)
 # ----------------------------------------------------------------------------
 def chunk_bounds(n: int, chunk_pairs: int) -> List[Tuple[int, int]]:

@@ -333,6 +333,92 @@ def test_adaptive_negatives_order_statistics():
             assert y_neg[n] == next(c for c in ranked if c != y[n])
 
 
+# ---------------------------------------------------------------- softmax head
+def test_embed_neutral_hand():
+    x = np.arange(24, dtype=np.float32).reshape(2, 12) / 10
+    e = O.embed_neutral(x, 10)
+    np.testing.assert_array_equal(e[:, :10], 0.1)
+    np.testing.assert_array_equal(e[:, 10:], x[:, 10:])
+
+
+def test_softmax_xent_closed_forms_and_finite_differences():
+    C, n = 10, 4
+    loss, d, p = O.softmax_xent(np.zeros((n, C)), np.array([0, 3, 9, 3]))
+    assert abs(loss - math.log(C)) < 1e-15
+    want = np.full((n, C), 1.0 / C)
+    want[np.arange(n), [0, 3, 9, 3]] -= 1.0
+    np.testing.assert_allclose(d, want / n, atol=1e-16)
+    rng = np.random.default_rng(3)
+    z = rng.normal(0, 3, (5, 7))
+    y = rng.integers(0, 7, 5)
+    l0, d0, p0 = O.softmax_xent(z, y)
+    np.testing.assert_allclose(p0.sum(axis=1), 1.0, rtol=1e-14)
+    l1, _, _ = O.softmax_xent(z + 123.0, y)  # a shift of every logit changes nothing
+    assert abs(l1 - l0) < 1e-12
+    h = 1e-6
+    for i, j in [(0, 0), (2, 5), (4, int(y[4]))]:
+        zp, zm = z.copy(), z.copy()
+        zp[i, j] += h
+        zm[i, j] -= h
+        fd = (O.softmax_xent(zp, y)[0] - O.softmax_xent(zm, y)[0]) / (2 * h)
+        assert abs(fd - d0[i, j]) < 1e-8
+
+
+def test_head_features_brute_force():
+    x_base, _, _ = make_data(14, 6, 30)
+    layers = _net(15, (30, 12, 9, 8))
+    hp = O.HParams()
+    A = O.head_features(layers, x_base, 10, hp, 1)
+    assert A.shape == (6, 17)
+    for n in range(6):
+        a = [0.1] * 10 + [float(v) for v in x_base[n, 10:]]
+        feats = []
+        for li, L in enumerate(layers):
+            nrm = math.sqrt(sum(v * v for v in a))
+            a = [v / (nrm + 1e-8) for v in a]
+            a = [max(0.0, sum(L.W[j, k] * a[k] for k in range(len(a))) + L.b[j])
+                 for j in range(L.W.shape[0])]
+            if li >= 1:
+                nrm = math.sqrt(sum(v * v for v in a))
+                feats += [v / (nrm + 1e-8) for v in a]
+        np.testing.assert_allclose(A[n], feats, rtol=1e-12, atol=1e-15)
+
+
+def test_head_steps_match_torch_autograd_adam():
+    torch = pytest.importorskip("torch")
+    x_base, y, _ = make_data(16, 40, 30)
+    layers = _net(17, (30, 16, 12))
+    rng = np.random.default_rng(18)
+    W = rng.uniform(-0.2, 0.2, (10, 12))
+    b = rng.uniform(-0.1, 0.1, 10)
+    hp, hhp = O.HParams(), O.HParams(lr=1e-2)
+    head = O.Head.from_params(W, b)
+    A = torch.tensor(O.head_features(layers, x_base, 10, hp, 1))
+    Wt = torch.tensor(W, requires_grad=True)
+    bt = torch.tensor(b, requires_grad=True)
+    opt = torch.optim.Adam([Wt, bt], lr=1e-2, betas=(0.9, 0.999), eps=1e-8)
+    for _ in range(3):
+        loss, logits, dW, db = O.head_step(head, layers, x_base, y, 10, hp, hhp, 1)
+        opt.zero_grad()
+        lt = torch.nn.functional.cross_entropy(A @ Wt.T + bt, torch.tensor(y, dtype=torch.int64))
+        lt.backward()
+        assert abs(loss - lt.item()) < 1e-12
+        np.testing.assert_allclose(dW, Wt.grad.numpy(), rtol=1e-10, atol=1e-15)
+        np.testing.assert_allclose(db, bt.grad.numpy(), rtol=1e-10, atol=1e-15)
+        opt.step()
+        np.testing.assert_allclose(head.W, Wt.detach().numpy(), rtol=1e-11, atol=1e-14)
+        np.testing.assert_allclose(head.b, bt.detach().numpy(), rtol=1e-11, atol=1e-14)
+
+
+def test_head_predict_is_argmax_with_lowest_tie():
+    x_base, _, _ = make_data(19, 5, 30)
+    layers = _net(20, (30, 12, 9))
+    head = O.Head.from_params(np.zeros((10, 9)), np.array([0, 2, 2, 1, 0, 0, 0, 2, 0, 0.0]))
+    logits, pred = O.head_predict(head, layers, x_base, 10, O.HParams(), 1)
+    np.testing.assert_array_equal(pred, 1)
+    np.testing.assert_allclose(logits, np.tile(head.b, (5, 1)))
+
+
 # ---------------------------------------------------------------- schedules
 def _net(seed, dims):
     return [O.Layer.from_params(W, b) for W, b in make_weights(seed, dims)]
