@@ -225,6 +225,41 @@ def other_workloads(P, torch, names, reps=2):
     return out
 
 
+def softmax_head(P, torch, sw, sxd, slayers, reps=5):
+    """Softmax prediction (one neutral-label pass + the softmax layer over the
+    normalised activities of layers 1..) of the scoring set, and one training
+    step of the softmax layer on it, each HIP-event timed on its own."""
+    from ffinputs import make_data, random_matrix
+    dev = torch.device("cuda:0")
+    D = sum(sw.dims[2:])
+    Wh = torch.from_numpy(random_matrix(96, sw.n_classes, D, -0.05, 0.05)).to(dev)
+    head = P.Head(Wh, torch.zeros(sw.n_classes, device=dev))
+    _, y, _ = make_data(sw.seed_data, sw.n, sw.dims[0], sw.p_zero, sw.n_classes)
+    yd = torch.from_numpy(y).to(dev)
+    hp = P.HParams(norm_eps=sw.norm_eps)
+    hhp = P.HParams(lr=1e-4)
+    ws = P.workspace(P.ff_head_workspace_size(slayers, 1, sw.n, sw.n_classes), dev)
+    pred = torch.empty(sw.n, dtype=torch.int32, device=dev)
+    loss = torch.empty(1, device=dev)
+    out = {}
+    for name, fn in (("predict", lambda: P.ff_head_predict(slayers, hp, head, sxd, 1, pred=pred,
+                                                           ws=ws)),
+                     ("step", lambda: P.ff_head_step(slayers, hp, head, hhp, sxd, yd, 1,
+                                                     loss=loss, ws=ws))):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        out[name + "_ms"] = a.elapsed_time(b) / reps
+    out["images_per_s"] = sw.n / (out["predict_ms"] * 1e-3)
+    out["features"] = D
+    return out
+
+
 def cpu_baseline(w, x_base, y, y_neg, params, sw, sx, sparams, budget_s=12.0):
     """The oracle as it stands, on a bounded sample of the same workload."""
     import numpy as np
@@ -443,6 +478,7 @@ def main():
     }
     out["roofline_isolated"] = isolated_roofline(P, torch, w, dtype, dom, peak, punit)
     if not args.no_other_workloads:
+        out["softmax_head"] = softmax_head(P, torch, sw, sxd, slayers)
         others = other_workloads(P, torch, ["mnist_784_2000x4", "mnist_784_2000x4_bf16",
                                             "cifar_3072x4_bf16_pipelined"])
         out["other_workloads"] = others

@@ -154,6 +154,50 @@ ff_status ff_adaptive_negatives(const ff_layer *layers, int32_t n_layers,
                                 int32_t n_classes, float *scores, int32_t *y_neg, void *ws,
                                 size_t ws_bytes, void *stream);
 
+/* ---- Softmax prediction layer (Sec. 3 "Prediction": Softmax; Sec. 5.1) ------
+ * An input is labelled with the neutral label (0.1 in every label feature) and
+ * run once through the FF layers without updates.  The activity vectors of
+ * layers first_layer..n_layers-1 (the paper: all but the first hidden layer,
+ * first_layer = 1), each length-normalised h / (||h|| + norm_eps) as the next
+ * layer receives it, are concatenated into A[n][d_feat] and fed to a softmax
+ * layer: logits = A W^T + b.  The softmax layer is trained by backpropagation
+ * that stops at it (mean cross-entropy, Adam); the FF layers are not changed.
+ * Its arithmetic is fp32 in both dtypes (hp->dtype selects the FF layers'
+ * operand type only).  At most 8 layers feed it. */
+typedef struct {
+  int32_t d_feat;     /* sum of d_out over layers first_layer..n_layers-1      */
+  int32_t n_classes;  /* C, 2..16, at most layers[0].d_in                      */
+  float *W;           /* (device) [n_classes][d_feat]                          */
+  float *b;           /* (device) [n_classes]                                  */
+  float *mW, *vW;     /* (device) [n_classes][d_feat] Adam moments, zero at start */
+  float *mb, *vb;     /* (device) [n_classes]                                  */
+  int64_t step;       /* (host) Adam step count, incremented by ff_head_step   */
+} ff_head;
+
+/* Workspace bytes for ff_head_step / ff_head_predict on n inputs (it grows
+ * with n: every layer's activities for the n inputs are held). */
+size_t ff_head_workspace_size(const ff_layer *layers, int32_t n_layers, int32_t first_layer,
+                              int32_t n, int32_t n_classes, int32_t dtype);
+
+/* One training step of the softmax layer on a batch of n inputs: logits,
+ * mean cross-entropy against labels, its gradient, one Adam update of W and
+ * b (head_hp: lr, beta1, beta2, adam_eps; the paper's lr is 1e-4).
+ *   layers (host) [n_layers] chained; hp: norm_eps and dtype of the FF layers;
+ *   x_base (device) [n][layers[0].d_in]; labels (device) [n] int32 in
+ *   [0, n_classes) (others give unspecified results, no stray accesses);
+ *   loss (device) [1] or NULL.  n == 0 is a no-op. */
+ff_status ff_head_step(const ff_layer *layers, int32_t n_layers, int32_t first_layer,
+                       const ff_hparams *hp, ff_head *head, const ff_hparams *head_hp,
+                       const float *x_base, const int32_t *labels, int32_t n, float *loss,
+                       void *ws, size_t ws_bytes, void *stream);
+
+/* Softmax prediction: one pass, logits (device) [n][n_classes] or NULL and
+ * pred (device) [n] int32 = argmax of the logits (lowest class on ties). */
+ff_status ff_head_predict(const ff_layer *layers, int32_t n_layers, int32_t first_layer,
+                          const ff_hparams *hp, const ff_head *head, const float *x_base,
+                          int32_t n, float *logits, int32_t *pred, void *ws, size_t ws_bytes,
+                          void *stream);
+
 /* Workspace bytes for ff_pipeline_epoch. */
 size_t ff_pipeline_workspace_size(const ff_layer *layers, int32_t n_layers, int32_t n,
                                   int32_t chunk_pairs, int32_t schedule, int32_t dtype);
@@ -200,7 +244,8 @@ typedef enum {
   FF_KERNEL_GOODNESS = 4,    /* goodness reduction / score accumulation       */
   FF_KERNEL_ARGMAX = 5,      /* label argmax                                  */
   FF_KERNEL_SHADOW = 6,      /* bf16 weight shadow refresh                    */
-  FF_KERNEL_KINDS = 7
+  FF_KERNEL_HEAD = 7,        /* softmax layer: logits, gradient, Adam         */
+  FF_KERNEL_KINDS = 8
 } ff_kernel_kind;
 
 typedef struct {

@@ -25,10 +25,12 @@ FF_SEQUENTIAL, FF_PIPELINED = 0, 1
 EXPORTS = ["ff_status_string", "ff_last_error", "ff_embed_labels", "ff_step_workspace_size",
            "ff_layer_forward", "ff_layer_step", "ff_refresh_bf16_shadow",
            "ff_score_workspace_size", "ff_score_labels", "ff_adaptive_negatives",
+           "ff_head_workspace_size", "ff_head_step", "ff_head_predict",
            "ff_pipeline_workspace_size",
            "ff_pipeline_epoch", "ff_profile_start", "ff_profile_stop"]
 
-KERNEL_KINDS = ["embed_norm", "forward", "loss", "dw_adam", "goodness", "argmax", "bf16_shadow"]
+KERNEL_KINDS = ["embed_norm", "forward", "loss", "dw_adam", "goodness", "argmax", "bf16_shadow",
+                "head"]
 
 
 class FFError(RuntimeError):
@@ -41,6 +43,12 @@ class ff_layer(ctypes.Structure):
     _fields_ = [("d_in", c_int32), ("d_out", c_int32), ("W", c_void_p), ("b", c_void_p),
                 ("mW", c_void_p), ("vW", c_void_p), ("mb", c_void_p), ("vb", c_void_p),
                 ("W_bf16", c_void_p), ("step", c_int64)]
+
+
+class ff_head(ctypes.Structure):
+    _fields_ = [("d_feat", c_int32), ("n_classes", c_int32), ("W", c_void_p), ("b", c_void_p),
+                ("mW", c_void_p), ("vW", c_void_p), ("mb", c_void_p), ("vb", c_void_p),
+                ("step", c_int64)]
 
 
 class ff_kernel_stats(ctypes.Structure):
@@ -76,6 +84,13 @@ def _load() -> ctypes.CDLL:
         "ff_adaptive_negatives": (c_int32, [POINTER(ff_layer), c_int32, c_int32,
                                             POINTER(ff_hparams), P, P, c_int32, c_int32, P, P, P,
                                             c_size_t, P]),
+        "ff_head_workspace_size": (c_size_t, [POINTER(ff_layer), c_int32, c_int32, c_int32,
+                                              c_int32, c_int32]),
+        "ff_head_step": (c_int32, [POINTER(ff_layer), c_int32, c_int32, POINTER(ff_hparams),
+                                   POINTER(ff_head), POINTER(ff_hparams), P, P, c_int32, P, P,
+                                   c_size_t, P]),
+        "ff_head_predict": (c_int32, [POINTER(ff_layer), c_int32, c_int32, POINTER(ff_hparams),
+                                      POINTER(ff_head), P, c_int32, P, P, P, c_size_t, P]),
         "ff_pipeline_workspace_size": (c_size_t, [POINTER(ff_layer), c_int32, c_int32, c_int32,
                                                   c_int32, c_int32]),
         "ff_pipeline_epoch": (c_int32, [POINTER(ff_layer), c_int32, POINTER(ff_hparams), P, P, P,
@@ -154,6 +169,25 @@ class Layer:
                         self.mW.data_ptr(), self.vW.data_ptr(), self.mb.data_ptr(),
                         self.vb.data_ptr(),
                         self.W_bf16.data_ptr() if self.W_bf16 is not None else None, self.step)
+
+
+class Head:
+    """Device buffers of the softmax prediction layer: W [C][d_feat], b [C], Adam moments."""
+
+    def __init__(self, W: torch.Tensor, b: torch.Tensor):
+        self.W = W.detach().to(torch.float32).contiguous().clone()
+        self.b = b.detach().to(self.W.device, torch.float32).contiguous().clone()
+        self.mW = torch.zeros_like(self.W)
+        self.vW = torch.zeros_like(self.W)
+        self.mb = torch.zeros_like(self.b)
+        self.vb = torch.zeros_like(self.b)
+        self.step = 0
+        self.n_classes, self.d_feat = self.W.shape
+
+    def c(self) -> ff_head:
+        return ff_head(self.d_feat, self.n_classes, self.W.data_ptr(), self.b.data_ptr(),
+                       self.mW.data_ptr(), self.vW.data_ptr(), self.mb.data_ptr(),
+                       self.vb.data_ptr(), self.step)
 
 
 def _layers_c(layers: Sequence[Layer]):
@@ -264,6 +298,53 @@ def ff_adaptive_negatives(layers: Sequence[Layer], hp: HParams, x_base: torch.Te
         _ptr(scores, torch.float32, n * n_classes, "scores"), _ptr(y_neg, torch.int32, n, "y_neg"),
         _ptr(ws, torch.uint8), ws.numel(), _stream(stream)))
     return scores, y_neg
+
+
+def ff_head_workspace_size(layers: Sequence[Layer], first_layer: int, n: int, n_classes: int,
+                           dtype: int = FF_F32) -> int:
+    return LIB.ff_head_workspace_size(_layers_c(layers), len(layers), first_layer, n, n_classes,
+                                      dtype)
+
+
+def ff_head_step(layers: Sequence[Layer], hp: HParams, head: Head, head_hp: HParams,
+                 x_base: torch.Tensor, labels: torch.Tensor, first_layer: int = 1,
+                 loss: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                 stream=None):
+    """One Adam step of the softmax prediction layer on the batch x_base (labels)."""
+    n = x_base.shape[0]
+    if ws is None:
+        ws = workspace(ff_head_workspace_size(layers, first_layer, max(n, 1), head.n_classes,
+                                              hp.dtype), x_base.device)
+    Hc = head.c()
+    st = LIB.ff_head_step(_layers_c(layers), len(layers), first_layer, ctypes.byref(hp.c()),
+                          ctypes.byref(Hc), ctypes.byref(head_hp.c()),
+                          _ptr(x_base, torch.float32, n * layers[0].d_in, "x_base"),
+                          _ptr(labels, torch.int32, n, "labels"), n,
+                          _ptr(loss, torch.float32, 1, "loss"), _ptr(ws, torch.uint8),
+                          ws.numel(), _stream(stream))
+    head.step = Hc.step
+    _check(st)
+    return loss
+
+
+def ff_head_predict(layers: Sequence[Layer], hp: HParams, head: Head, x_base: torch.Tensor,
+                    first_layer: int = 1, logits: Optional[torch.Tensor] = None,
+                    pred: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                    stream=None):
+    """Softmax prediction: (logits or None, pred)."""
+    n = x_base.shape[0]
+    dev = x_base.device
+    pred = torch.empty(n, dtype=torch.int32, device=dev) if pred is None else pred
+    if ws is None:
+        ws = workspace(ff_head_workspace_size(layers, first_layer, max(n, 1), head.n_classes,
+                                              hp.dtype), dev)
+    _check(LIB.ff_head_predict(_layers_c(layers), len(layers), first_layer, ctypes.byref(hp.c()),
+                               ctypes.byref(head.c()),
+                               _ptr(x_base, torch.float32, n * layers[0].d_in, "x_base"), n,
+                               _ptr(logits, torch.float32, n * head.n_classes, "logits"),
+                               _ptr(pred, torch.int32, n, "pred"), _ptr(ws, torch.uint8),
+                               ws.numel(), _stream(stream)))
+    return logits, pred
 
 
 def ff_pipeline_workspace_size(layers: Sequence[Layer], n: int, chunk_pairs: int, schedule: int,

@@ -579,6 +579,201 @@ ff_status ff_adaptive_negatives(const ff_layer *layers, int32_t n_layers,
 }
 
 // ---------------------------------------------------------------------------
+// Softmax prediction layer
+// ---------------------------------------------------------------------------
+namespace {
+// Every layer's activities for the n inputs and their row normalisation (the
+// normalisation of layer l's output is both layer l+1's input scale, in fp32,
+// and the scale of the head's feature block l).
+struct HeadScratch {
+  void *x0 = nullptr;           // [n][d_in of layer 0] normalised neutral rows
+  void *xb = nullptr;           // bf16: [n][max hidden d_in] normalised bf16 rows
+  std::vector<float *> h, s;    // [l]: [n][d_out_l], [n]
+  float *gpart = nullptr;       // [max col tiles][n]
+  float *G = nullptr;           // [n][C]
+  float *lrow = nullptr;        // [n]
+  float *part = nullptr;        // [splits][C][d_feat]
+  float *loss = nullptr;        // [1]
+};
+
+int head_feat_width(const ff_layer *layers, int n_layers, int first) {
+  int d = 0;
+  for (int l = first; l < n_layers; ++l) d += layers[l].d_out;
+  return d;
+}
+
+void carve_head(Carver &cv, HeadScratch &hs, const ff_layer *layers, int L, int first, int n,
+                int C, int dtype) {
+  const bool bf16 = dtype == FF_BF16;
+  hs.x0 = cv.take((size_t)n * layers[0].d_in * elem_bytes(dtype));
+  int max_hidden_in = 0, max_nt = 0;
+  for (int l = 0; l < L; ++l) {
+    if (l > 0) max_hidden_in = std::max(max_hidden_in, layers[l].d_in);
+    max_nt = std::max(max_nt, ffk::fwd_col_tiles_max(layers[l].d_out));
+  }
+  if (bf16 && L > 1) hs.xb = cv.take((size_t)n * max_hidden_in * 2);
+  hs.h.assign(L, nullptr);
+  hs.s.assign(L, nullptr);
+  for (int l = 0; l < L; ++l) {
+    hs.h[l] = static_cast<float *>(cv.take((size_t)n * layers[l].d_out * 4));
+    hs.s[l] = static_cast<float *>(cv.take((size_t)n * 4));
+  }
+  hs.gpart = static_cast<float *>(cv.take((size_t)max_nt * n * 4));
+  hs.G = static_cast<float *>(cv.take((size_t)n * C * 4));
+  hs.lrow = static_cast<float *>(cv.take((size_t)n * 4));
+  hs.part = static_cast<float *>(cv.take((size_t)ffk::head_grad_splits(n) * C *
+                                         head_feat_width(layers, L, first) * 4));
+  hs.loss = static_cast<float *>(cv.take(4));
+}
+
+ff_status check_head(const ff_layer *layers, int n_layers, int first, const ff_hparams *hp,
+                     const ff_head *head, bool for_update) {
+  FF_TRY(check_hp(hp));
+  FF_TRY(check_stack(layers, n_layers, hp, false));
+  if (first < 0 || first >= n_layers)
+    return fail(FF_ERR_INVALID_ARG, "first_layer=%d outside [0, %d)", first, n_layers);
+  if (n_layers - first > ffk::kHeadMaxBlocks)
+    return fail(FF_ERR_UNSUPPORTED, "%d layers feed the softmax layer (at most %d)",
+                n_layers - first, ffk::kHeadMaxBlocks);
+  if (!head) return fail(FF_ERR_INVALID_ARG, "head is NULL");
+  if (head->d_feat != head_feat_width(layers, n_layers, first))
+    return fail(FF_ERR_INVALID_ARG, "head d_feat=%d, but layers %d.. give %d features",
+                head->d_feat, first, head_feat_width(layers, n_layers, first));
+  if (head->n_classes < 2 || head->n_classes > ffk::kHeadMaxClasses ||
+      head->n_classes > layers[0].d_in)
+    return fail(FF_ERR_INVALID_ARG, "head n_classes=%d outside [2, %d] or above d_in",
+                head->n_classes, ffk::kHeadMaxClasses);
+  if (!head->W || !head->b) return fail(FF_ERR_INVALID_ARG, "head W or b is NULL");
+  if (for_update && (!head->mW || !head->vW || !head->mb || !head->vb))
+    return fail(FF_ERR_INVALID_ARG, "head Adam moment buffer is NULL");
+  return FF_OK;
+}
+
+// The neutral pass through the FF layers; returns the head's feature blocks.
+ff_status head_features(const ff_layer *layers, int L, int first, const ff_hparams *hp,
+                        const float *x_base, int n, int C, HeadScratch &hs, hipStream_t st,
+                        ffk::HeadFeatures &f) {
+  const bool bf16 = hp->dtype == FF_BF16;
+  ffk::RowMap m{};
+  m.base = x_base;
+  m.mode = ffk::NEUTRAL;
+  m.n_classes = C;
+  FF_HIP(embed_norm(m, n, layers[0].d_in, hp->norm_eps, true, bf16, hs.x0, st));
+  for (int l = 0; l < L; ++l) {
+    const ff_layer *Ly = &layers[l];
+    const void *X = hs.x0;
+    const float *rs = nullptr;
+    if (l > 0 && bf16) {
+      FF_HIP(embed_norm(rows_of(hs.h[l - 1]), n, Ly->d_in, hp->norm_eps, true, true, hs.xb, st));
+      X = hs.xb;
+    } else if (l > 0) {
+      X = hs.h[l - 1];
+      rs = hs.s[l - 1];
+    }
+    FF_HIP(fwd(hp->dtype, X, weight_operand(Ly, hp->dtype), Ly->b, rs, n, Ly->d_out, Ly->d_in,
+               hs.h[l], hs.gpart, st));
+    FF_HIP(goodness_sum(hs.gpart, ffk::fwd_col_tiles(n, Ly->d_out, hp->dtype), n, nullptr,
+                        nullptr, 0, hs.s[l], hp->norm_eps, st));
+  }
+  f = ffk::HeadFeatures{};
+  f.n_blocks = L - first;
+  for (int l = first; l < L; ++l) {
+    f.h[l - first] = hs.h[l];
+    f.s[l - first] = hs.s[l];
+    f.d[l - first] = layers[l].d_out;
+  }
+  return FF_OK;
+}
+
+ff_status head_prepare(const ff_layer *layers, int L, int first, const ff_hparams *hp,
+                       const ff_head *head, int n, void *ws, size_t ws_bytes, HeadScratch &hs) {
+  Carver size_cv(nullptr);
+  HeadScratch tmp;
+  carve_head(size_cv, tmp, layers, L, first, n, head->n_classes, hp->dtype);
+  FF_TRY(check_ws(ws, ws_bytes, size_cv.off + kAlign));
+  Carver cv(ws);
+  carve_head(cv, hs, layers, L, first, n, head->n_classes, hp->dtype);
+  return FF_OK;
+}
+}  // namespace
+
+size_t ff_head_workspace_size(const ff_layer *layers, int32_t n_layers, int32_t first_layer,
+                              int32_t n, int32_t n_classes, int32_t dtype) {
+  if (!layers || n_layers <= 0 || first_layer < 0 || first_layer >= n_layers || n <= 0 ||
+      n_classes <= 0)
+    return 0;
+  Carver cv(nullptr);
+  HeadScratch hs;
+  carve_head(cv, hs, layers, n_layers, first_layer, n, n_classes, dtype);
+  return cv.off + kAlign;
+}
+
+ff_status ff_head_step(const ff_layer *layers, int32_t n_layers, int32_t first_layer,
+                       const ff_hparams *hp, ff_head *head, const ff_hparams *head_hp,
+                       const float *x_base, const int32_t *labels, int32_t n, float *loss,
+                       void *ws, size_t ws_bytes, void *stream) {
+  FF_TRY(check_head(layers, n_layers, first_layer, hp, head, true));
+  FF_TRY(check_hp(head_hp));
+  if (n < 0) return fail(FF_ERR_INVALID_ARG, "n=%d", n);
+  if (n == 0) return FF_OK;
+  if (!x_base || !labels) return fail(FF_ERR_INVALID_ARG, "x_base or labels is NULL");
+  HeadScratch hs;
+  FF_TRY(head_prepare(layers, n_layers, first_layer, hp, head, n, ws, ws_bytes, hs));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int C = head->n_classes, D = head->d_feat;
+  ffk::HeadFeatures f;
+  FF_TRY(head_features(layers, n_layers, first_layer, hp, x_base, n, C, hs, st, f));
+  const int splits = ffk::head_grad_splits(n);
+  const int64_t t = ++head->step;
+  ffk::AdamArgs a;
+  a.lr = head_hp->lr;
+  a.beta1 = head_hp->beta1;
+  a.beta2 = head_hp->beta2;
+  a.eps = head_hp->adam_eps;
+  a.bc1 = (float)(1.0 - pow((double)head_hp->beta1, (double)t));
+  a.bc2 = (float)(1.0 - pow((double)head_hp->beta2, (double)t));
+  const double feat_bytes = (double)n * D * 4.0 + (double)n * f.n_blocks * 4.0;
+  FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * n * C * D, feat_bytes + (double)C * D * 4.0 + n * C * 4.0,
+                st, [&] {
+                  return ffk::launch_head_logits(f, head->W, head->b, n, C, D, labels, nullptr,
+                                                 nullptr, hs.G, hs.lrow, st);
+                }));
+  FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * n * C * D,
+                feat_bytes + n * C * 4.0 + (double)splits * C * D * 4.0, st, [&] {
+                  return ffk::launch_head_grad(f, hs.G, n, C, D, splits, hs.part, st);
+                }));
+  FF_HIP(launch(FF_KERNEL_HEAD, 0.0, (double)splits * C * D * 4.0 + (double)C * D * 24.0, st,
+                [&] {
+                  return ffk::launch_head_adam(hs.part, splits, hs.G, hs.lrow, n, C, D,
+                                               head->W, head->mW, head->vW, head->b, head->mb,
+                                               head->vb, a, loss ? loss : hs.loss, st);
+                }));
+  return FF_OK;
+}
+
+ff_status ff_head_predict(const ff_layer *layers, int32_t n_layers, int32_t first_layer,
+                          const ff_hparams *hp, const ff_head *head, const float *x_base,
+                          int32_t n, float *logits, int32_t *pred, void *ws, size_t ws_bytes,
+                          void *stream) {
+  FF_TRY(check_head(layers, n_layers, first_layer, hp, head, false));
+  if (n < 0) return fail(FF_ERR_INVALID_ARG, "n=%d", n);
+  if (n == 0) return FF_OK;
+  if (!x_base || !pred) return fail(FF_ERR_INVALID_ARG, "x_base or pred is NULL");
+  HeadScratch hs;
+  FF_TRY(head_prepare(layers, n_layers, first_layer, hp, head, n, ws, ws_bytes, hs));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int C = head->n_classes, D = head->d_feat;
+  ffk::HeadFeatures f;
+  FF_TRY(head_features(layers, n_layers, first_layer, hp, x_base, n, C, hs, st, f));
+  FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * n * C * D,
+                (double)n * D * 4.0 + (double)C * D * 4.0 + n * (C + 1) * 4.0, st, [&] {
+                  return ffk::launch_head_logits(f, head->W, head->b, n, C, D, nullptr, logits,
+                                                 pred, nullptr, nullptr, st);
+                }));
+  return FF_OK;
+}
+
+// ---------------------------------------------------------------------------
 // Training over chunks: sequential or one stream per layer
 // ---------------------------------------------------------------------------
 namespace {

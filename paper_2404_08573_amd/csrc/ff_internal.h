@@ -18,7 +18,9 @@ namespace ffk {
 //   MASKED:   row r is base row base_off + r with the n_classes label features
 //             zeroed, normalised as if one label feature were 1: the part that
 //             every label embedding of the row shares (same norm for every label).
-enum RowMode : int32_t { ROWS = 0, PAIRS = 1, EXPAND = 2, MASKED = 3 };
+//   NEUTRAL:  row r is base row base_off + r with every label feature 0.1 (the
+//             neutral label of Softmax prediction).
+enum RowMode : int32_t { ROWS = 0, PAIRS = 1, EXPAND = 2, MASKED = 3, NEUTRAL = 4 };
 
 struct RowMap {
   const float *base;
@@ -54,6 +56,41 @@ struct LossFinish {
   int32_t n_pos, n_neg;
   float *loss;         // null: not wanted
 };
+
+// Features of the softmax prediction layer: the concatenation of layer blocks
+// A_l[r][j] = s_l[r] * H_l[r][j] (normalised activities), block l of width d[l].
+constexpr int kHeadMaxBlocks = 8;
+constexpr int kHeadMaxClasses = 16;
+struct HeadFeatures {
+  int32_t n_blocks;
+  const float *h[kHeadMaxBlocks];
+  const float *s[kHeadMaxBlocks];
+  int32_t d[kHeadMaxBlocks];
+};
+
+// Softmax head forward on n rows: logits = A W^T + b (W [C][D]), then the
+// softmax.  Writes logits [n][C] and pred [n] (argmax, lowest class on ties)
+// when non-null; with labels (training) also G[n][C] = (p - onehot) / n, the
+// gradient of the mean cross-entropy with respect to the logits, and the
+// per-row loss lrow [n].
+hipError_t launch_head_logits(const HeadFeatures &f, const float *W, const float *b, int n,
+                              int C, int D, const int32_t *labels, float *logits, int32_t *pred,
+                              float *G, float *lrow, hipStream_t s);
+
+// Row splits of the head's weight-gradient reduction.
+int head_grad_splits(int n);
+
+// Head weight gradient partials: part[split][C][D] = sum over the split's rows
+// of G[r][c] * A[r][f].
+hipError_t launch_head_grad(const HeadFeatures &f, const float *G, int n, int C, int D,
+                            int splits, float *part, hipStream_t s);
+
+// Sum of the partials (fixed order), db = sum_r G[r] and loss = mean of lrow
+// (fixed order), and one Adam update of W [C][D] and b [C].
+hipError_t launch_head_adam(const float *part, int splits, const float *G, const float *lrow,
+                            int n, int C, int D, float *W, float *mW, float *vW, float *b,
+                            float *mb, float *vb, const AdamArgs &a, float *loss,
+                            hipStream_t s);
 
 // Number of per-workgroup loss partial pairs for `rows` rows.
 int loss_blocks(int rows);

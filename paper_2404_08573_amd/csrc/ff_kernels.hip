@@ -95,6 +95,8 @@ __device__ __forceinline__ void adam_update(float &p, float &m, float &v, float 
 // ---------------------------------------------------------------------------
 // Row source mapping (label embedding) + L2 normalisation
 // ---------------------------------------------------------------------------
+constexpr int kNeutralLab = -2;
+
 __device__ __forceinline__ void map_row(const RowMap &m, int r, int &src, int &lab) {
   if (m.mode == PAIRS) {
     if (r < m.n_pos) {
@@ -110,6 +112,9 @@ __device__ __forceinline__ void map_row(const RowMap &m, int r, int &src, int &l
   } else if (m.mode == MASKED) {
     src = m.base_off + r;
     lab = m.n_classes;  // matches no label feature: all of them become 0
+  } else if (m.mode == NEUTRAL) {
+    src = m.base_off + r;
+    lab = kNeutralLab;
   } else {
     src = r;
     lab = -1;
@@ -117,9 +122,15 @@ __device__ __forceinline__ void map_row(const RowMap &m, int r, int &src, int &l
 }
 
 // Features [col, col+4) of a row under label `lab`: the first C features are
-// replaced by one-hot(lab) (all zero when lab >= C); lab < 0 leaves the row as is.
+// replaced by one-hot(lab) (all zero when lab >= C), or all set to the neutral
+// 0.1 (lab == kNeutralLab); other negative labels leave the row as is.
 __device__ __forceinline__ float4 embed4(float4 v, int col, int lab, int C) {
-  if (lab >= 0 && col < C) {
+  if (lab == kNeutralLab && col < C) {
+    v.x = col + 0 < C ? 0.1f : v.x;
+    v.y = col + 1 < C ? 0.1f : v.y;
+    v.z = col + 2 < C ? 0.1f : v.z;
+    v.w = col + 3 < C ? 0.1f : v.w;
+  } else if (lab >= 0 && col < C) {
     v.x = col + 0 < C ? (col + 0 == lab ? 1.f : 0.f) : v.x;
     v.y = col + 1 < C ? (col + 1 == lab ? 1.f : 0.f) : v.y;
     v.z = col + 2 < C ? (col + 2 == lab ? 1.f : 0.f) : v.z;
@@ -1015,6 +1026,183 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_bf16(
 }
 
 // ---------------------------------------------------------------------------
+// Softmax prediction layer (Sec. 3 "Prediction": Softmax).  Its 10 outputs
+// are far too few for MFMA tiles; the work is reading the feature rows once.
+// ---------------------------------------------------------------------------
+// Feature block and column of feature index f (blocks are contiguous).
+__device__ __forceinline__ int head_block(const HeadFeatures &hf, int f, int &j) {
+  int blk = 0, off = 0;
+  while (blk + 1 < hf.n_blocks && f >= off + hf.d[blk]) off += hf.d[blk++];
+  j = f - off;
+  return blk;
+}
+
+// One wave per row: the C dot products over the row's feature blocks, reduced
+// across the wave, then the softmax on lanes 0..C-1.
+__global__ __launch_bounds__(kBlock) void k_head_logits(HeadFeatures hf,
+                                                        const float *__restrict__ W,
+                                                        const float *__restrict__ bias, int n,
+                                                        int C, int D,
+                                                        const int32_t *__restrict__ labels,
+                                                        float *__restrict__ logits,
+                                                        int32_t *__restrict__ pred,
+                                                        float *__restrict__ G,
+                                                        float *__restrict__ lrow) {
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  if (r >= n) return;  // uniform per wave
+  float acc[kHeadMaxClasses];
+#pragma unroll
+  for (int c = 0; c < kHeadMaxClasses; ++c) acc[c] = 0.f;
+  int off = 0;
+  for (int blk = 0; blk < hf.n_blocks; ++blk) {
+    const int d = hf.d[blk];
+    const float *hr = hf.h[blk] + (size_t)r * d;
+    const float sr = hf.s[blk][r];
+    for (int i = lane; i < (d >> 2); i += 64) {
+      float4 a = ld4(hr + 4 * i);
+      a.x *= sr;
+      a.y *= sr;
+      a.z *= sr;
+      a.w *= sr;
+#pragma unroll
+      for (int c = 0; c < kHeadMaxClasses; ++c)
+        if (c < C) {
+          const float4 w = ld4(W + (size_t)c * D + off + 4 * i);
+          acc[c] += a.x * w.x + a.y * w.y + a.z * w.z + a.w * w.w;
+        }
+    }
+    off += d;
+  }
+  float z = 0.f, zmax = -INFINITY;
+  int arg = 0;
+#pragma unroll
+  for (int c = 0; c < kHeadMaxClasses; ++c)
+    if (c < C) {
+      const float v = wave_sum(acc[c]) + bias[c];
+      if (lane == c) z = v;
+      if (v > zmax) {
+        zmax = v;
+        arg = c;
+      }
+    }
+  const float e = lane < C ? expf(z - zmax) : 0.f;
+  const float esum = wave_sum(e);
+  // labels outside [0, C) are clamped into it (unspecified result, no stray access)
+  const int y = labels ? min(max(labels[r], 0), C - 1) : 0;
+  const float zy = __shfl(z, y);  // the true class's logit, from its lane (whole wave active)
+  if (lane < C) {
+    if (logits) logits[(size_t)r * C + lane] = z;
+    if (G) G[(size_t)r * C + lane] = (e / esum - (lane == y ? 1.f : 0.f)) / (float)n;
+  }
+  if (lane == 0) {
+    if (pred) pred[r] = arg;
+    if (lrow) lrow[r] = logf(esum) - (zy - zmax);  // -log p_y
+  }
+}
+
+// One thread per 4 consecutive features and split of rows: C x 4 partial sums.
+__global__ __launch_bounds__(kBlock) void k_head_grad(HeadFeatures hf,
+                                                      const float *__restrict__ G, int n, int C,
+                                                      int D, int rows_per_split,
+                                                      float *__restrict__ part) {
+  const int f = 4 * (blockIdx.x * kBlock + threadIdx.x);
+  if (f >= D) return;
+  int j;
+  const int blk = head_block(hf, f, j);
+  const int d = hf.d[blk];
+  const float *h = hf.h[blk] + j;
+  const float *sv = hf.s[blk];
+  const int r0 = blockIdx.y * rows_per_split, r1 = min(n, r0 + rows_per_split);
+  float4 acc[kHeadMaxClasses];
+#pragma unroll
+  for (int c = 0; c < kHeadMaxClasses; ++c) acc[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int r = r0; r < r1; ++r) {
+    float4 a = ld4(h + (size_t)r * d);
+    const float sr = sv[r];
+    a.x *= sr;
+    a.y *= sr;
+    a.z *= sr;
+    a.w *= sr;
+#pragma unroll
+    for (int c = 0; c < kHeadMaxClasses; ++c)
+      if (c < C) {
+        const float g = G[(size_t)r * C + c];
+        acc[c].x += g * a.x;
+        acc[c].y += g * a.y;
+        acc[c].z += g * a.z;
+        acc[c].w += g * a.w;
+      }
+  }
+#pragma unroll
+  for (int c = 0; c < kHeadMaxClasses; ++c)
+    if (c < C) st4(part + ((size_t)blockIdx.y * C + c) * D + f, acc[c]);
+}
+
+// Adam on the head.  Block 0 also reduces db and the loss over the rows: each
+// thread sums a fixed strided subset, then a fixed-order tree in LDS.
+__global__ __launch_bounds__(kBlock) void k_head_adam(const float *__restrict__ part, int splits,
+                                                      const float *__restrict__ G,
+                                                      const float *__restrict__ lrow, int n,
+                                                      int C, int D, float *__restrict__ W,
+                                                      float *__restrict__ mW,
+                                                      float *__restrict__ vW,
+                                                      float *__restrict__ bvec,
+                                                      float *__restrict__ mbv,
+                                                      float *__restrict__ vbv, AdamArgs ad,
+                                                      float *__restrict__ loss) {
+  const size_t i = 4 * ((size_t)blockIdx.x * kBlock + threadIdx.x);
+  const size_t total = (size_t)C * D;
+  if (i < total) {
+    float4 g = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int sp = 0; sp < splits; ++sp) {
+      const float4 v = ld4(part + (size_t)sp * total + i);
+      g.x += v.x;
+      g.y += v.y;
+      g.z += v.z;
+      g.w += v.w;
+    }
+    float4 p = ld4(W + i), m = ld4(mW + i), v = ld4(vW + i);
+    adam_update(p.x, m.x, v.x, g.x, ad);
+    adam_update(p.y, m.y, v.y, g.y, ad);
+    adam_update(p.z, m.z, v.z, g.z, ad);
+    adam_update(p.w, m.w, v.w, g.w, ad);
+    st4(W + i, p);
+    st4(mW + i, m);
+    st4(vW + i, v);
+  }
+  if (blockIdx.x != 0) return;
+  __shared__ float red[kHeadMaxClasses + 1][kBlock];
+  float acc[kHeadMaxClasses + 1];
+#pragma unroll
+  for (int c = 0; c <= kHeadMaxClasses; ++c) acc[c] = 0.f;
+  for (int r = threadIdx.x; r < n; r += kBlock) {
+#pragma unroll
+    for (int c = 0; c < kHeadMaxClasses; ++c)
+      if (c < C) acc[c] += G[(size_t)r * C + c];
+    if (lrow) acc[kHeadMaxClasses] += lrow[r];
+  }
+#pragma unroll
+  for (int c = 0; c <= kHeadMaxClasses; ++c) red[c][threadIdx.x] = acc[c];
+  __syncthreads();
+  for (int st = kBlock / 2; st > 0; st >>= 1) {
+    if ((int)threadIdx.x < st)
+#pragma unroll
+      for (int c = 0; c <= kHeadMaxClasses; ++c) red[c][threadIdx.x] += red[c][threadIdx.x + st];
+    __syncthreads();
+  }
+  if ((int)threadIdx.x < C) {
+    const int c = threadIdx.x;
+    float p = bvec[c], m = mbv[c], v = vbv[c];
+    adam_update(p, m, v, red[c][0], ad);
+    bvec[c] = p;
+    mbv[c] = m;
+    vbv[c] = v;
+  }
+  if (threadIdx.x == 0 && loss) loss[0] = red[kHeadMaxClasses][0] / (float)n;
+}
+
+// ---------------------------------------------------------------------------
 // Small kernels
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kBlock) void k_goodness(const float *__restrict__ gpart, int nt,
@@ -1278,6 +1466,41 @@ hipError_t launch_argmax(const float *scores, int n, int C, const int32_t *exclu
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_argmax, dim3(cdiv(n, kBlock)), dim3(kBlock), 0, s, scores, n, C, exclude,
                      pred);
+  return hipGetLastError();
+}
+
+hipError_t launch_head_logits(const HeadFeatures &f, const float *W, const float *b, int n,
+                              int C, int D, const int32_t *labels, float *logits, int32_t *pred,
+                              float *G, float *lrow, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (C < 1 || C > kHeadMaxClasses || C > 64 || f.n_blocks < 1 || f.n_blocks > kHeadMaxBlocks ||
+      ((G || lrow) && !labels))
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_head_logits, dim3(cdiv(n, kBlock / 64)), dim3(kBlock), 0, s, f, W, b, n, C,
+                     D, labels, logits, pred, G, lrow);
+  return hipGetLastError();
+}
+
+int head_grad_splits(int n) { return std::max(1, (int)cdiv(n, 128)); }
+
+hipError_t launch_head_grad(const HeadFeatures &f, const float *G, int n, int C, int D,
+                            int splits, float *part, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (C < 1 || C > kHeadMaxClasses || D % 4 || splits < 1) return hipErrorInvalidValue;
+  const int rps = (int)cdiv(n, splits);
+  hipLaunchKernelGGL(k_head_grad, dim3(cdiv(D / 4, kBlock), splits), dim3(kBlock), 0, s, f, G, n,
+                     C, D, rps, part);
+  return hipGetLastError();
+}
+
+hipError_t launch_head_adam(const float *part, int splits, const float *G, const float *lrow,
+                            int n, int C, int D, float *W, float *mW, float *vW, float *b,
+                            float *mb, float *vb, const AdamArgs &a, float *loss,
+                            hipStream_t s) {
+  if (C < 1 || C > kHeadMaxClasses || D % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_head_adam, dim3(std::max(1u, cdiv((long)C * D / 4, kBlock))),
+                     dim3(kBlock), 0, s, part, splits, G, lrow, n, C, D, W, mW, vW, b, mb, vb,
+                     a, loss);
   return hipGetLastError();
 }
 

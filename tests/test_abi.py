@@ -149,6 +149,44 @@ def test_adaptive_negatives_rejects_on_host(P):
     assert P.LIB.ff_adaptive_negatives(*small) == -3
 
 
+def test_head_rejects_on_host(P):
+    layers = (P._lib.ff_layer * 3)(_layer(P, 16, 12), _layer(P, 12, 8), _layer(P, 8, 8))
+    hp = _hp(P)
+    fake = ctypes.c_void_p(256)
+
+    def head(d_feat=16, C=10, **kw):
+        f = dict(d_feat=d_feat, n_classes=C, W=fake, b=fake, mW=fake, vW=fake, mb=fake, vb=fake,
+                 step=0)
+        f.update(kw)
+        return P._lib.ff_head(**f)
+
+    ws = ctypes.c_void_p(1 << 20)
+
+    def step(h, first=1, labels=ctypes.c_void_p(4096), n=5):
+        return P.LIB.ff_head_step(layers, 3, first, ctypes.byref(hp), ctypes.byref(h),
+                                  ctypes.byref(hp), ctypes.c_void_p(4096), labels, n, None, ws,
+                                  1 << 30, None)
+
+    # every case is rejected on the host before anything is enqueued
+    for h, first, status, msg in [(head(d_feat=12), 1, -1, b"d_feat"),
+                                  (head(), 3, -1, b"first_layer"),
+                                  (head(C=1), 1, -1, b"n_classes"),
+                                  (head(C=17), 1, -1, b"n_classes"),
+                                  (head(mW=None), 1, -1, b"moment")]:
+        assert step(h, first) == status, msg
+        assert msg in P.LIB.ff_last_error()
+    assert step(head(), labels=None) == -1
+    h = head()
+    assert P.LIB.ff_head_step(layers, 3, 1, ctypes.byref(hp), ctypes.byref(h), ctypes.byref(hp),
+                              ctypes.c_void_p(4096), ctypes.c_void_p(4096), 5, None, ws, 16,
+                              None) == -3
+    assert h.step == 0
+    assert P.LIB.ff_head_predict(layers, 3, 1, ctypes.byref(hp), ctypes.byref(head()),
+                                 ctypes.c_void_p(4096), 5, None, None, ws, 1 << 30, None) == -1
+    assert P.LIB.ff_head_workspace_size(layers, 3, 3, 5, 10, 0) == 0  # first_layer out of range
+    assert P.LIB.ff_head_workspace_size(layers, 3, 1, 5, 10, 0) > 5 * (12 + 8 + 8) * 4
+
+
 def test_pipeline_rejects_on_host(P):
     layers = (P._lib.ff_layer * 2)(_layer(P, 16, 8), _layer(P, 8, 8))
     hp = _hp(P)

@@ -490,3 +490,104 @@ def test_profile_counts_and_kind_mask(P):
     only = P.ff_profile_stop()
     assert only["forward"]["launches"] == 1
     assert all(v["launches"] == 0 for k, v in only.items() if k != "forward")
+
+
+# ------------------------------------------------------------------ softmax prediction layer
+def _head_case(seed, dims, C, n, first):
+    x_base, y, _ = make_data(seed, n, dims[0])
+    y = (y % C).astype(np.int32)
+    params = make_weights(seed + 1, dims)
+    D = sum(dims[1 + first:])
+    rng = np.random.default_rng(seed + 2)
+    Wh = rng.uniform(-0.3, 0.3, (C, D)).astype(np.float32)
+    bh = rng.uniform(-0.1, 0.1, C).astype(np.float32)
+    return x_base, y, params, Wh, bh
+
+
+@pytest.mark.parametrize("dims,C,n,first", [((784, 500, 500), 10, 512, 1),
+                                            ((64, 96, 80, 48), 10, 37, 1),
+                                            ((64, 96, 80, 48), 16, 300, 0),
+                                            ((24, 36, 20), 2, 130, 1)])
+def test_head_predict_parity(P, dims, C, n, first):
+    x_base, _, params, Wh, bh = _head_case(92, dims, C, n, first)
+    layers = [P.Layer(_t(W), _t(b)) for W, b in params]
+    head = P.Head(_t(Wh), _t(bh))
+    logits = torch.empty(n, C, device=DEV)
+    _, pred = P.ff_head_predict(layers, P.HParams(), head, _t(x_base), first, logits=logits)
+    ref_layers = [O.Layer.from_params(W, b) for W, b in params]
+    z_ref, p_ref = O.head_predict(O.Head.from_params(Wh, bh), ref_layers, x_base, C, O.HParams(),
+                                  first)
+    assert_acts(_np(logits), z_ref)  # logits can cancel to near 0: floor 1e-5 of the largest
+    assert_labels(_np(pred), z_ref, p_ref)
+    np.testing.assert_array_equal(_np(pred), np.argmax(_np(logits), axis=1))
+
+
+@pytest.mark.parametrize("dims,C,n,lr", [((784, 500, 500), 10, 512, 1e-4),
+                                         ((64, 96, 80, 48), 10, 300, 1e-2)])
+def test_head_steps_parity(P, dims, C, n, lr):
+    x_base, y, params, Wh, bh = _head_case(93, dims, C, n, 1)
+    layers = [P.Layer(_t(W), _t(b)) for W, b in params]
+    head = P.Head(_t(Wh), _t(bh))
+    ref_layers = [O.Layer.from_params(W, b) for W, b in params]
+    ref = O.Head.from_params(Wh, bh)
+    hp, ohp = P.HParams(), O.HParams()
+    hhp, ohhp = P.HParams(lr=lr), O.HParams(lr=lr)
+    loss = torch.empty(1, device=DEV)
+    A = O.head_features(ref_layers, x_base, C, ohp, 1)
+    gW, gb, mW, mb = [], [], [], []
+    for _ in range(3):
+        P.ff_head_step(layers, hp, head, hhp, _t(x_base), _t(y), 1, loss=loss)
+        l_ref, _, dW, db = O.head_step(ref, ref_layers, x_base, y, C, ohp, ohhp, 1)
+        assert_loss(_np(loss)[0], l_ref)
+        gW.append(dW)
+        gb.append(db)
+    # gradient magnitudes for the conditioning rule: sum of |terms| of each element
+    r0 = O.Head.from_params(Wh, bh)
+    for _ in range(3):
+        z = A @ r0.W.T + r0.b
+        _, d, _ = O.softmax_xent(z, y)
+        mW.append(np.abs(d).T @ np.abs(A))
+        mb.append(np.abs(d).sum(axis=0))
+        O.head_step(r0, ref_layers, x_base, y, C, ohp, ohhp, 1)
+    assert head.step == 3
+    assert_weights(_np(head.W), ref.W, gW, mW, "head W", lr=lr, adam_eps=1e-8)
+    assert_weights(_np(head.b), ref.b, gb, mb, "head b", lr=lr, adam_eps=1e-8)
+    # the FF layers are untouched
+    for L, (W, b) in zip(layers, params):
+        np.testing.assert_array_equal(_np(L.W), W)
+        assert L.step == 0
+
+
+def test_head_bf16_layers(P):
+    dims, C, n = (64, 96, 80, 48), 10, 200
+    x_base, y, params, Wh, bh = _head_case(94, dims, C, n, 1)
+    layers = [P.Layer(_t(W), _t(b), bf16_shadow=True) for W, b in params]
+    head = P.Head(_t(Wh), _t(bh))
+    logits = torch.empty(n, C, device=DEV)
+    P.ff_head_predict(layers, P.HParams(dtype=P.FF_BF16), head, _t(x_base), 1, logits=logits)
+    ref_layers = [O.Layer.from_params(W, b) for W, b in params]
+    z_ref, _ = O.head_predict(O.Head.from_params(Wh, bh), ref_layers, x_base, C,
+                              O.HParams(bf16=True), 1)
+    assert_acts(_np(logits), z_ref, rel=1e-3, floor=1e-3)
+
+
+def test_head_full_size_sampled(P):
+    """Softmax prediction of all 10 000 inputs through 784->2000x4 (6000 features)."""
+    w = WORKLOADS["mnist_score_784_2000x4"]
+    x_base, _, _ = make_data(w.seed_data, w.n, w.dims[0], w.p_zero)
+    params = make_weights(w.seed_w, w.dims)
+    rng = np.random.default_rng(95)
+    Wh = rng.uniform(-0.05, 0.05, (10, 6000)).astype(np.float32)
+    bh = np.zeros(10, np.float32)
+    layers = [P.Layer(_t(W), _t(b)) for W, b in params]
+    logits = torch.empty(w.n, 10, device=DEV)
+    _, pred = P.ff_head_predict(layers, P.HParams(), P.Head(_t(Wh), _t(bh)), _t(x_base), 1,
+                                logits=logits)
+    zg, pg = _np(logits), _np(pred)
+    np.testing.assert_array_equal(pg, np.argmax(zg, axis=1))
+    idx = np.random.default_rng(2).choice(w.n, 16, replace=False)
+    z_ref, p_ref = O.head_predict(O.Head.from_params(Wh, bh),
+                                  [O.Layer.from_params(W, b) for W, b in params], x_base[idx], 10,
+                                  O.HParams(), 1)
+    assert_acts(zg[idx], z_ref)
+    assert_labels(pg[idx], z_ref, p_ref)
