@@ -365,6 +365,73 @@ def head_predict(head: Head, layers: Sequence[Layer], x_base: np.ndarray, n_clas
 
 
 # ----------------------------------------------------------------------------
+# Performance-Optimised PFF (the PFF variant with a classification goodness)
+# ----------------------------------------------------------------------------
+def po_layer_step(L: Layer, head: Head, x: np.ndarray, y: np.ndarray, hp: HParams,
+                  head_hp: HParams, normalised: bool = False):
+    """One step of Performance-Optimised PFF on one layer (Sec. 4 "PFF with a new
+    goodness function"): a softmax classifier is attached to the layer, and both
+    are trained by backpropagation through those two layers only, on the mean
+    cross-entropy of the labels (no negative data).  Readings: the classifier
+    takes the layer's activities h as they are; the layer input is normalised
+    as for FF.  Returns ``(loss, h, logits, dW, db, dWc, dbc)``, where h (the
+    next layer's input) uses the weights before the update; mutates L and head.
+    """
+    xh, z, h, _ = layer_forward(L.W, L.b, x, hp.norm_eps, normalised, hp.bf16)
+    logits = h @ head.W.T + head.b
+    loss, d, _ = softmax_xent(logits, np.asarray(y, dtype=np.int64))
+    dWc = d.T @ h
+    dbc = d.sum(axis=0)
+    dh = d @ head.W
+    dz = dh * (z > 0)
+    dzc = bf16_round(dz) if hp.bf16 else dz
+    dW = dzc.T @ xh
+    db = dz.sum(axis=0)
+    L.t += 1
+    L.W, L.mW, L.vW = adam(L.W, L.mW, L.vW, dW, L.t, hp.lr, hp.beta1, hp.beta2, hp.adam_eps)
+    L.b, L.mb, L.vb = adam(L.b, L.mb, L.vb, db, L.t, hp.lr, hp.beta1, hp.beta2, hp.adam_eps)
+    head.t += 1
+    head.W, head.mW, head.vW = adam(head.W, head.mW, head.vW, dWc, head.t, head_hp.lr,
+                                    head_hp.beta1, head_hp.beta2, head_hp.adam_eps)
+    head.b, head.mb, head.vb = adam(head.b, head.mb, head.vb, dbc, head.t, head_hp.lr,
+                                    head_hp.beta1, head_hp.beta2, head_hp.adam_eps)
+    return loss, h, logits, dW, db, dWc, dbc
+
+
+def po_train_pipelined(layers: List[Layer], heads: List[Head], x_base, y, n_classes: int,
+                       chunk_pairs: int, epochs: int, hp: HParams, head_hp: HParams) -> np.ndarray:
+    """Performance-Optimised PFF over chunks in the layer-per-stage pipeline: layer
+    l trains chunk c on layer l-1's activities of chunk c (computed before that
+    step's update), as the FF pipeline does.  Layer 0 sees the neutrally
+    labelled input (a reading: no label is given to a network that predicts it).
+    Returns the loss trace ``[L, epochs * n_chunks]``."""
+    chunks = chunk_bounds(x_base.shape[0], chunk_pairs)
+    trace = np.zeros((len(layers), epochs * len(chunks)))
+    for e in range(epochs):
+        for ci, (s, b) in enumerate(chunks):
+            a = embed_neutral(x_base[s:s + b], n_classes)
+            for li, (L, Hd) in enumerate(zip(layers, heads)):
+                loss, a, *_ = po_layer_step(L, Hd, a, y[s:s + b], hp, head_hp)
+                trace[li, e * len(chunks) + ci] = loss
+    return trace
+
+
+def po_predict(layers: Sequence[Layer], heads: Sequence[Head], x_base: np.ndarray,
+               n_classes: int, hp: HParams, all_layers: bool = True):
+    """Prediction of a Performance-Optimised network: one neutral-label pass; the
+    last layer's classifier logits, or (reading for "all layers") the sum of every
+    layer's classifier logits.  Returns ``(logits[n, C], pred[n])``, lowest class
+    on ties."""
+    a = embed_neutral(x_base, n_classes)
+    total = np.zeros((x_base.shape[0], heads[0].W.shape[0]))
+    for li, (L, Hd) in enumerate(zip(layers, heads)):
+        _, _, a, _ = layer_forward(L.W, L.b, a, hp.norm_eps, False, hp.bf16)
+        z = a @ Hd.W.T + Hd.b
+        total = total + z if all_layers else z
+    return total, np.argmax(total, axis=1).astype(np.int32)
+
+
+# ----------------------------------------------------------------------------
 # Training schedules over chunks (Sec. 3 sequential FF, Sec. 4.1 Alg. 1)
 # ----------------------------------------------------------------------------
 def chunk_bounds(n: int, chunk_pairs: int) -> List[Tuple[int, int]]:

@@ -419,6 +419,115 @@ def test_head_predict_is_argmax_with_lowest_tie():
     np.testing.assert_allclose(logits, np.tile(head.b, (5, 1)))
 
 
+# ---------------------------------------------------------------- Performance-Optimised PFF
+def _po_case(seed, d_in=30, d_out=16, C=10, n=24):
+    x_base, y, _ = make_data(seed, n, d_in)
+    (W, b), = make_weights(seed + 1, (d_in, d_out))
+    b = b + np.linspace(-0.05, 0.1, d_out).astype(np.float32)
+    rng = np.random.default_rng(seed + 2)
+    Wc = rng.uniform(-0.3, 0.3, (C, d_out))
+    bc = rng.uniform(-0.1, 0.1, C)
+    return O.embed_neutral(x_base, C), y, W, b, Wc, bc
+
+
+def test_po_steps_match_torch_two_layer_backprop():
+    """Layer + classifier trained together by autograd through both, Adam on each
+    with its own learning rate (PyTorch fp64, library routines only here)."""
+    torch = pytest.importorskip("torch")
+    x, y, W, b, Wc, bc = _po_case(40)
+    hp, hhp = O.HParams(lr=0.03), O.HParams(lr=1e-2)
+    L, Hd = O.Layer.from_params(W, b), O.Head.from_params(Wc, bc)
+    xt = torch.tensor(O.l2_normalise(x, 1e-8))
+    P = [torch.tensor(v, dtype=torch.float64, requires_grad=True) for v in (W, b, Wc, bc)]
+    opt_l = torch.optim.Adam(P[:2], lr=0.03, betas=(0.9, 0.999), eps=1e-8)
+    opt_c = torch.optim.Adam(P[2:], lr=1e-2, betas=(0.9, 0.999), eps=1e-8)
+    for _ in range(3):
+        loss, h, logits, dW, db, dWc, dbc = O.po_layer_step(L, Hd, x, y, hp, hhp)
+        opt_l.zero_grad()
+        opt_c.zero_grad()
+        ht = torch.relu(xt @ P[0].T + P[1])
+        lt = torch.nn.functional.cross_entropy(ht @ P[2].T + P[3],
+                                               torch.tensor(y, dtype=torch.int64))
+        lt.backward()
+        assert abs(loss - lt.item()) < 1e-12
+        np.testing.assert_allclose(h, ht.detach().numpy(), rtol=1e-12, atol=1e-15)
+        for got, t in zip((dW, db, dWc, dbc), P):
+            np.testing.assert_allclose(got, t.grad.numpy(), rtol=1e-10, atol=1e-15)
+        opt_l.step()
+        opt_c.step()
+        for got, t in zip((L.W, L.b, Hd.W, Hd.b), P):
+            np.testing.assert_allclose(got, t.detach().numpy(), rtol=1e-11, atol=1e-14)
+
+
+def test_po_bf16_gradient_within_rounding_bound():
+    """In bf16 mode the weight gradient contracts bf16-rounded dZ and x_hat (R3,
+    R1); it differs from the exact one by at most the rounding of those operands:
+    |dW16 - dW| <= (2^-8 + 2^-8 + 2^-16) * sum |dz| |x_hat| elementwise."""
+    x, y, W, b, Wc, bc = _po_case(41)
+    hp16, hp = O.HParams(bf16=True), O.HParams()
+    r16 = O.po_layer_step(O.Layer.from_params(W, b), O.Head.from_params(Wc, bc), x, y, hp16, hp)
+    # the exact gradient on the same bf16 forward: dz from the same logits, unrounded
+    xh16 = O.bf16_round(O.l2_normalise(x, 1e-8))
+    z16 = xh16 @ O.bf16_round(W).T + b
+    h16 = np.maximum(z16, 0)
+    _, d, _ = O.softmax_xent(h16 @ Wc.T + bc, y)
+    dz = (d @ Wc) * (z16 > 0)
+    exact = dz.T @ xh16
+    bound = (2.0 ** -8 + 2.0 ** -8 + 2.0 ** -16) * (np.abs(dz).T @ np.abs(xh16))
+    assert np.all(np.abs(r16[3] - exact) <= bound + 1e-300)
+    assert np.any(r16[3] != exact)  # the rounding is applied
+
+
+def test_po_pipeline_layer_independence_and_one_layer():
+    """Layer l's loss trace depends only on layers 0..l; with one layer the
+    pipeline is the plain chunk-by-chunk sequence of steps."""
+    x_base, y, _ = make_data(42, 150, 30)
+    dims = (30, 20, 16, 12)
+    params = make_weights(43, dims)
+    rng = np.random.default_rng(44)
+    heads = [rng.uniform(-0.2, 0.2, (10, d)) for d in dims[1:]]
+    hp, hhp = O.HParams(lr=0.03), O.HParams(lr=1e-3)
+
+    def run(ps, hs):
+        Ls = [O.Layer.from_params(W, b) for W, b in ps]
+        Hs = [O.Head.from_params(Wc, np.zeros(10)) for Wc in hs]
+        return O.po_train_pipelined(Ls, Hs, x_base, y, 10, 64, 2, hp, hhp)
+
+    t = run(params, heads)
+    alt = list(params)
+    alt[2] = (params[2][0] * 0.5, params[2][1])
+    t2 = run(alt, heads[:2] + [heads[2] * 3.0])
+    np.testing.assert_array_equal(t[:2], t2[:2])
+    assert np.any(t[2] != t2[2])
+    L = O.Layer.from_params(*params[0])
+    Hd = O.Head.from_params(heads[0], np.zeros(10))
+    seq = []
+    for _ in range(2):
+        for s, b in O.chunk_bounds(150, 64):
+            seq.append(O.po_layer_step(L, Hd, O.embed_neutral(x_base[s:s + b], 10), y[s:s + b],
+                                       hp, hhp)[0])
+    np.testing.assert_array_equal(t[0], seq)
+
+
+def test_po_predict_last_and_all_layers():
+    x_base, _, _ = make_data(45, 20, 30)
+    params = make_weights(46, (30, 16, 12))
+    layers = [O.Layer.from_params(W, b) for W, b in params]
+    rng = np.random.default_rng(47)
+    heads = [O.Head.from_params(rng.normal(size=(10, d)), rng.normal(size=10)) for d in (16, 12)]
+    zl, pl = O.po_predict(layers, heads, x_base, 10, O.HParams(), all_layers=False)
+    za, pa = O.po_predict(layers, heads, x_base, 10, O.HParams(), all_layers=True)
+    a = O.embed_neutral(x_base, 10)
+    h1 = O.layer_forward(layers[0].W, layers[0].b, a, 1e-8)[2]
+    h2 = O.layer_forward(layers[1].W, layers[1].b, h1, 1e-8)[2]
+    z1 = h1 @ heads[0].W.T + heads[0].b
+    z2 = h2 @ heads[1].W.T + heads[1].b
+    np.testing.assert_allclose(zl, z2, rtol=1e-13)
+    np.testing.assert_allclose(za, z1 + z2, rtol=1e-13)
+    np.testing.assert_array_equal(pl, np.argmax(z2, axis=1))
+    np.testing.assert_array_equal(pa, np.argmax(z1 + z2, axis=1))
+
+
 # ---------------------------------------------------------------- schedules
 def _net(seed, dims):
     return [O.Layer.from_params(W, b) for W, b in make_weights(seed, dims)]
