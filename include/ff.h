@@ -228,6 +228,61 @@ ff_status ff_pipeline_epoch(ff_layer *layers, int32_t n_layers, const ff_hparams
                             int32_t schedule, void *const *streams, float *loss_trace, void *ws,
                             size_t ws_bytes);
 
+/* ---- Performance-Optimised PFF (Sec. 4, "PFF with a new goodness function") -
+ * Each layer l carries its own softmax classifier heads[l] (d_feat = d_out of
+ * layer l).  The layer and its classifier are trained together by
+ * backpropagation through those two layers only, on the mean cross-entropy of
+ * the labels; there is no negative data.  Readings: the classifier takes the
+ * layer's activities h as they are; layer 0 sees the neutrally labelled input
+ * (0.1 in every label feature); each layer input is normalised as for FF.
+ * Both the layer (hp: lr, betas, adam_eps) and the classifier (head_hp) take
+ * one Adam update per step.  In FF_BF16 mode the layer's products use bf16
+ * operands at R1/R2/R3 (R3: the gradient rows dZ); the classifier is fp32. */
+
+/* Workspace bytes for ff_po_layer_step on up to `rows` rows. */
+size_t ff_po_step_workspace_size(int32_t rows, int32_t d_in, int32_t d_out, int32_t n_classes,
+                                 int32_t dtype);
+
+/* One step on `rows` input rows x (device) [rows][d_in] with labels (device)
+ * [rows] int32 in [0, n_classes): h = relu(x_hat W^T + b), logits = h Wc^T +
+ * bc, loss = mean cross-entropy; dWc = G^T h, dZ = (G Wc) * [h > 0],
+ * dW = dZ^T x_hat (G = dloss/dlogits); Adam on W, b, Wc, bc.
+ *   h_out (device) [rows][d_out] or NULL: the activities before the update
+ *   (the next layer's input); loss (device) [1] or NULL. */
+ff_status ff_po_layer_step(ff_layer *L, ff_head *head, const ff_hparams *hp,
+                           const ff_hparams *head_hp, const float *x, const int32_t *labels,
+                           int32_t rows, int32_t x_normalised, float *h_out, float *loss, void *ws,
+                           size_t ws_bytes, void *stream);
+
+/* Workspace bytes for ff_po_epoch. */
+size_t ff_po_epoch_workspace_size(const ff_layer *layers, int32_t n_layers, int32_t n,
+                                  int32_t n_classes, int32_t chunk, int32_t schedule,
+                                  int32_t dtype);
+
+/* Performance-optimised training over the chunks [c*chunk, min((c+1)*chunk, n))
+ * of x_base, `epochs` times, with the schedules of ff_pipeline_epoch
+ * (sequential, or one stream per layer handing each chunk's activities on).
+ *   heads (host) [n_layers], all with n_classes classes; labels (device) [n];
+ *   loss_trace (device) [n_layers][epochs*n_chunks] or NULL. */
+ff_status ff_po_epoch(ff_layer *layers, ff_head *heads, int32_t n_layers, const ff_hparams *hp,
+                      const ff_hparams *head_hp, const float *x_base, const int32_t *labels,
+                      int32_t n, int32_t n_classes, int32_t chunk, int32_t epochs,
+                      int32_t schedule, void *const *streams, float *loss_trace, void *ws,
+                      size_t ws_bytes);
+
+/* Workspace bytes for ff_po_predict on n inputs. */
+size_t ff_po_predict_workspace_size(const ff_layer *layers, int32_t n_layers, int32_t n,
+                                    int32_t n_classes, int32_t dtype);
+
+/* Prediction of a performance-optimised network: one neutral-label pass; the
+ * logits of the last layer's classifier (all_layers == 0) or the sum of every
+ * layer's classifier logits (all_layers != 0, a reading of "all layers").
+ *   logits (device) [n][n_classes] or NULL; pred (device) [n] int32 (argmax,
+ *   lowest class on ties).  At most 8 layers. */
+ff_status ff_po_predict(const ff_layer *layers, const ff_head *heads, int32_t n_layers,
+                        const ff_hparams *hp, const float *x_base, int32_t n, int32_t all_layers,
+                        float *logits, int32_t *pred, void *ws, size_t ws_bytes, void *stream);
+
 /* ---- Kernel timing (tracing aid) -------------------------------------------
  * Between ff_profile_start and ff_profile_stop every kernel the library
  * launches (up to max_launches) is bracketed by a pair of hipEvents recorded on

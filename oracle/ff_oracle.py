@@ -416,6 +416,25 @@ def po_train_pipelined(layers: List[Layer], heads: List[Head], x_base, y, n_clas
     return trace
 
 
+def po_train_sequential(layers: List[Layer], heads: List[Head], x_base, y, n_classes: int,
+                        chunk_pairs: int, epochs: int, hp: HParams,
+                        head_hp: HParams) -> np.ndarray:
+    """Performance-Optimised training one layer after another (the sequential FF
+    schedule of Sec. 3): layer l takes all its steps over the chunks, then its
+    output with its final weights is the next layer's input.  Returns the loss
+    trace ``[L, epochs * n_chunks]``."""
+    chunks = chunk_bounds(x_base.shape[0], chunk_pairs)
+    trace = np.zeros((len(layers), epochs * len(chunks)))
+    a_all = embed_neutral(x_base, n_classes)
+    for li, (L, Hd) in enumerate(zip(layers, heads)):
+        for e in range(epochs):
+            for ci, (s, b) in enumerate(chunks):
+                trace[li, e * len(chunks) + ci] = po_layer_step(L, Hd, a_all[s:s + b], y[s:s + b],
+                                                                hp, head_hp)[0]
+        a_all = layer_forward(L.W, L.b, a_all, hp.norm_eps, False, hp.bf16)[2]
+    return trace
+
+
 def po_predict(layers: Sequence[Layer], heads: Sequence[Head], x_base: np.ndarray,
                n_classes: int, hp: HParams, all_layers: bool = True):
     """Prediction of a Performance-Optimised network: one neutral-label pass; the

@@ -26,6 +26,8 @@ EXPORTS = ["ff_status_string", "ff_last_error", "ff_embed_labels", "ff_step_work
            "ff_layer_forward", "ff_layer_step", "ff_refresh_bf16_shadow",
            "ff_score_workspace_size", "ff_score_labels", "ff_adaptive_negatives",
            "ff_head_workspace_size", "ff_head_step", "ff_head_predict",
+           "ff_po_step_workspace_size", "ff_po_layer_step", "ff_po_epoch_workspace_size",
+           "ff_po_epoch", "ff_po_predict_workspace_size", "ff_po_predict",
            "ff_pipeline_workspace_size",
            "ff_pipeline_epoch", "ff_profile_start", "ff_profile_stop"]
 
@@ -91,6 +93,21 @@ def _load() -> ctypes.CDLL:
                                    c_size_t, P]),
         "ff_head_predict": (c_int32, [POINTER(ff_layer), c_int32, c_int32, POINTER(ff_hparams),
                                       POINTER(ff_head), P, c_int32, P, P, P, c_size_t, P]),
+        "ff_po_step_workspace_size": (c_size_t, [c_int32] * 5),
+        "ff_po_layer_step": (c_int32, [POINTER(ff_layer), POINTER(ff_head), POINTER(ff_hparams),
+                                       POINTER(ff_hparams), P, P, c_int32, c_int32, P, P, P,
+                                       c_size_t, P]),
+        "ff_po_epoch_workspace_size": (c_size_t, [POINTER(ff_layer), c_int32, c_int32, c_int32,
+                                                  c_int32, c_int32, c_int32]),
+        "ff_po_epoch": (c_int32, [POINTER(ff_layer), POINTER(ff_head), c_int32,
+                                  POINTER(ff_hparams), POINTER(ff_hparams), P, P, c_int32,
+                                  c_int32, c_int32, c_int32, c_int32, POINTER(c_void_p), P, P,
+                                  c_size_t]),
+        "ff_po_predict_workspace_size": (c_size_t, [POINTER(ff_layer), c_int32, c_int32, c_int32,
+                                                    c_int32]),
+        "ff_po_predict": (c_int32, [POINTER(ff_layer), POINTER(ff_head), c_int32,
+                                    POINTER(ff_hparams), P, c_int32, c_int32, P, P, P, c_size_t,
+                                    P]),
         "ff_pipeline_workspace_size": (c_size_t, [POINTER(ff_layer), c_int32, c_int32, c_int32,
                                                   c_int32, c_int32]),
         "ff_pipeline_epoch": (c_int32, [POINTER(ff_layer), c_int32, POINTER(ff_hparams), P, P, P,
@@ -344,6 +361,87 @@ def ff_head_predict(layers: Sequence[Layer], hp: HParams, head: Head, x_base: to
                                _ptr(logits, torch.float32, n * head.n_classes, "logits"),
                                _ptr(pred, torch.int32, n, "pred"), _ptr(ws, torch.uint8),
                                ws.numel(), _stream(stream)))
+    return logits, pred
+
+
+def _heads_c(heads: Sequence[Head]):
+    return (ff_head * len(heads))(*[h.c() for h in heads])
+
+
+def ff_po_layer_step(layer: Layer, head: Head, hp: HParams, head_hp: HParams, x: torch.Tensor,
+                     labels: torch.Tensor, x_normalised: bool = False,
+                     h_out: Optional[torch.Tensor] = None, loss: Optional[torch.Tensor] = None,
+                     ws: Optional[torch.Tensor] = None, stream=None):
+    """One performance-optimised step of a layer and its classifier on x (labels)."""
+    rows = x.shape[0]
+    if ws is None:
+        ws = workspace(LIB.ff_po_step_workspace_size(max(rows, 1), layer.d_in, layer.d_out,
+                                                     head.n_classes, hp.dtype), x.device)
+    Lc, Hc = layer.c(), head.c()
+    st = LIB.ff_po_layer_step(ctypes.byref(Lc), ctypes.byref(Hc), ctypes.byref(hp.c()),
+                              ctypes.byref(head_hp.c()),
+                              _ptr(x, torch.float32, rows * layer.d_in, "x"),
+                              _ptr(labels, torch.int32, rows, "labels"), rows, int(x_normalised),
+                              _ptr(h_out, torch.float32, rows * layer.d_out, "h_out"),
+                              _ptr(loss, torch.float32, 1, "loss"), _ptr(ws, torch.uint8),
+                              ws.numel(), _stream(stream))
+    layer.step, head.step = Lc.step, Hc.step
+    _check(st)
+
+
+def ff_po_epoch(layers: List[Layer], heads: List[Head], hp: HParams, head_hp: HParams,
+                x_base: torch.Tensor, labels: torch.Tensor, n_classes: int, chunk: int,
+                epochs: int = 1, schedule: int = FF_PIPELINED, streams: Optional[Sequence] = None,
+                loss_trace: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None):
+    """Performance-optimised training epoch(s); streams as for ff_pipeline_epoch."""
+    n = x_base.shape[0]
+    dev = x_base.device
+    nc = (n + chunk - 1) // chunk
+    if ws is None:
+        ws = workspace(LIB.ff_po_epoch_workspace_size(_layers_c(layers), len(layers), n,
+                                                      n_classes, chunk, schedule, hp.dtype), dev)
+    own = streams is None
+    cur = torch.cuda.current_stream(dev)
+    if own:
+        streams = [cur] + [torch.cuda.Stream(dev) for _ in range(len(layers) - 1)]
+        for s in streams[1:]:
+            s.wait_stream(cur)
+    sarr = (c_void_p * len(layers))(*[_stream(s) for s in streams])
+    arr, harr = _layers_c(layers), _heads_c(heads)
+    st = LIB.ff_po_epoch(arr, harr, len(layers), ctypes.byref(hp.c()), ctypes.byref(head_hp.c()),
+                         _ptr(x_base, torch.float32, n * layers[0].d_in, "x_base"),
+                         _ptr(labels, torch.int32, n, "labels"), n, n_classes, chunk, epochs,
+                         schedule, sarr,
+                         _ptr(loss_trace, torch.float32, len(layers) * nc * epochs, "loss_trace"),
+                         _ptr(ws, torch.uint8), ws.numel())
+    for L, Lc in zip(layers, arr):
+        L.step = Lc.step
+    for h, hc in zip(heads, harr):
+        h.step = hc.step
+    if own:
+        for s in streams[1:]:
+            cur.wait_stream(s)
+    _check(st)
+
+
+def ff_po_predict(layers: Sequence[Layer], heads: Sequence[Head], hp: HParams,
+                  x_base: torch.Tensor, all_layers: bool = True,
+                  logits: Optional[torch.Tensor] = None, pred: Optional[torch.Tensor] = None,
+                  ws: Optional[torch.Tensor] = None, stream=None):
+    """Prediction of a performance-optimised network: (logits or None, pred)."""
+    n = x_base.shape[0]
+    dev = x_base.device
+    C = heads[0].n_classes
+    pred = torch.empty(n, dtype=torch.int32, device=dev) if pred is None else pred
+    if ws is None:
+        ws = workspace(LIB.ff_po_predict_workspace_size(_layers_c(layers), len(layers),
+                                                        max(n, 1), C, hp.dtype), dev)
+    _check(LIB.ff_po_predict(_layers_c(layers), _heads_c(heads), len(layers),
+                             ctypes.byref(hp.c()),
+                             _ptr(x_base, torch.float32, n * layers[0].d_in, "x_base"), n,
+                             int(all_layers), _ptr(logits, torch.float32, n * C, "logits"),
+                             _ptr(pred, torch.int32, n, "pred"), _ptr(ws, torch.uint8),
+                             ws.numel(), _stream(stream)))
     return logits, pred
 
 

@@ -107,10 +107,23 @@ struct StepScratch {
   float *c = nullptr;     // [rows]
   float *lpart = nullptr; // [loss blocks][2]
   float *loss = nullptr;  // [1]
+  // Performance-optimised steps (po_classes > 0): the classifier's logit
+  // gradient, per-row loss and weight-gradient partials, and the layer's dZ
+  float *G = nullptr;     // [rows][C]
+  float *lrow = nullptr;  // [rows]
+  float *part = nullptr;  // [head_grad_splits(rows)][C][d_out]
+  float *dz = nullptr;    // [rows][d_out]
 };
 
 void carve_step(Carver &cv, StepScratch &s, int rows, int d_in, int d_out, int dtype, bool need_h,
-                bool need_g, bool need_loss) {
+                bool need_g, bool need_loss, int po_classes = 0) {
+  if (po_classes > 0) {
+    s.G = static_cast<float *>(cv.take((size_t)rows * po_classes * 4));
+    s.lrow = static_cast<float *>(cv.take((size_t)rows * 4));
+    s.part = static_cast<float *>(
+        cv.take((size_t)ffk::head_grad_splits(rows) * po_classes * d_out * 4));
+    s.dz = static_cast<float *>(cv.take((size_t)rows * d_out * 4));
+  }
   s.xhat = cv.take((size_t)rows * d_in * elem_bytes(dtype));
   if (need_h) s.h = static_cast<float *>(cv.take((size_t)rows * d_out * 4));
   s.gpart = static_cast<float *>(cv.take((size_t)ffk::fwd_col_tiles_max(d_out) * rows * 4));
@@ -324,6 +337,77 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int
                                  L->mb, L->vb, a, lf, st);
     }));
   }
+  return FF_OK;
+}
+
+// Adam arguments of update t.
+ffk::AdamArgs adam_args(const ff_hparams *hp, int64_t t) {
+  ffk::AdamArgs a;
+  a.lr = hp->lr;
+  a.beta1 = hp->beta1;
+  a.beta2 = hp->beta2;
+  a.eps = hp->adam_eps;
+  a.bc1 = (float)(1.0 - pow((double)hp->beta1, (double)t));
+  a.bc2 = (float)(1.0 - pow((double)hp->beta2, (double)t));
+  return a;
+}
+
+// One performance-optimised step (R rows, labels): the layer and its softmax
+// classifier trained together by backprop through the two, no negatives.
+ff_status po_step_core(ff_layer *L, ff_head *head, const ff_hparams *hp, const ff_hparams *head_hp,
+                       const LayerInput &in, int R, const int32_t *labels, float *h_out,
+                       float *loss, float *s_next, StepScratch &s, hipStream_t st) {
+  const int C = head->n_classes, D = L->d_out;
+  const void *xop = in.src.base;
+  if (!in.rowscale)
+    FF_TRY(stage_input(in.src, R, L->d_in, in.normalised, hp->dtype, hp->norm_eps, s.xhat, &xop,
+                       st));
+  float *H = h_out ? h_out : s.h;
+  FF_HIP(fwd(hp->dtype, xop, weight_operand(L, hp->dtype), L->b, in.rowscale, R, D, L->d_in, H,
+             s.gpart, st));
+  if (s_next)
+    FF_HIP(goodness_sum(s.gpart, ffk::fwd_col_tiles(R, D, hp->dtype), R, nullptr, nullptr, 0,
+                        s_next, hp->norm_eps, st));
+  ffk::HeadFeatures f{};
+  f.n_blocks = 1;
+  f.h[0] = H;
+  f.d[0] = D;
+  f.w[0] = head->W;
+  f.ldw[0] = D;
+  f.n_bias = 1;
+  f.bias[0] = head->b;
+  const int splits = ffk::head_grad_splits(R);
+  const double hbytes = (double)R * D * 4.0;
+  FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * R * C * D, hbytes + (double)C * D * 4.0 + R * C * 8.0, st,
+                [&] {
+                  return ffk::launch_head_logits(f, R, C, labels, nullptr, nullptr, s.G, s.lrow,
+                                                 st);
+                }));
+  FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * R * C * D, 2.0 * hbytes + (double)C * D * 4.0, st, [&] {
+    return ffk::launch_po_dz(H, s.G, head->W, R, D, C, s.dz, s.c, st);
+  }));
+  FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * R * C * D, hbytes + (double)splits * C * D * 4.0, st, [&] {
+    return ffk::launch_head_grad(f, s.G, R, C, D, splits, s.part, st);
+  }));
+  const ffk::AdamArgs ah = adam_args(head_hp, ++head->step);
+  FF_HIP(launch(FF_KERNEL_HEAD, 0.0, (double)splits * C * D * 4.0 + (double)C * D * 24.0, st,
+                [&] {
+                  return ffk::launch_head_adam(s.part, splits, s.G, s.lrow, R, C, D, head->W,
+                                               head->mW, head->vW, head->b, head->mb, head->vb,
+                                               ah, loss ? loss : s.loss, st);
+                }));
+  // dW = dZ^T x_hat, db = sum dZ: the weight-gradient product with row scale 1
+  const ffk::AdamArgs a = adam_args(hp, ++L->step);
+  ffk::LossFinish lf{};
+  const double eb = (double)elem_bytes(hp->dtype);
+  const double params = (double)D * L->d_in;
+  const double bytes = hbytes + (double)R * L->d_in * eb + R * (in.rowscale ? 8.0 : 4.0) +
+                       params * (24.0 + (hp->dtype == FF_BF16 ? 2.0 : 0.0)) + D * 24.0;
+  FF_HIP(launch(FF_KERNEL_DW_ADAM, gemm_flops(D, L->d_in, R), bytes, st, [&] {
+    return ffk::launch_dw_adam(hp->dtype, s.dz, s.c, xop, in.rowscale, D, L->d_in, R, L->W,
+                               L->mW, L->vW, hp->dtype == FF_BF16 ? L->W_bf16 : nullptr, L->b,
+                               L->mb, L->vb, a, lf, st);
+  }));
   return FF_OK;
 }
 
@@ -685,6 +769,18 @@ ff_status head_features(const ff_layer *layers, int L, int first, const ff_hpara
   return FF_OK;
 }
 
+// The head's weights as per-block views of W [C][D] (row stride D), one bias.
+void head_weights(ffk::HeadFeatures &f, const float *W, const float *b, int D) {
+  int off = 0;
+  for (int i = 0; i < f.n_blocks; ++i) {
+    f.w[i] = W + off;
+    f.ldw[i] = D;
+    off += f.d[i];
+  }
+  f.n_bias = 1;
+  f.bias[0] = b;
+}
+
 ff_status head_prepare(const ff_layer *layers, int L, int first, const ff_hparams *hp,
                        const ff_head *head, int n, void *ws, size_t ws_bytes, HeadScratch &hs) {
   Carver size_cv(nullptr);
@@ -723,6 +819,7 @@ ff_status ff_head_step(const ff_layer *layers, int32_t n_layers, int32_t first_l
   const int C = head->n_classes, D = head->d_feat;
   ffk::HeadFeatures f;
   FF_TRY(head_features(layers, n_layers, first_layer, hp, x_base, n, C, hs, st, f));
+  head_weights(f, head->W, head->b, D);
   const int splits = ffk::head_grad_splits(n);
   const int64_t t = ++head->step;
   ffk::AdamArgs a;
@@ -735,8 +832,8 @@ ff_status ff_head_step(const ff_layer *layers, int32_t n_layers, int32_t first_l
   const double feat_bytes = (double)n * D * 4.0 + (double)n * f.n_blocks * 4.0;
   FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * n * C * D, feat_bytes + (double)C * D * 4.0 + n * C * 4.0,
                 st, [&] {
-                  return ffk::launch_head_logits(f, head->W, head->b, n, C, D, labels, nullptr,
-                                                 nullptr, hs.G, hs.lrow, st);
+                  return ffk::launch_head_logits(f, n, C, labels, nullptr, nullptr, hs.G,
+                                                 hs.lrow, st);
                 }));
   FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * n * C * D,
                 feat_bytes + n * C * 4.0 + (double)splits * C * D * 4.0, st, [&] {
@@ -765,10 +862,11 @@ ff_status ff_head_predict(const ff_layer *layers, int32_t n_layers, int32_t firs
   const int C = head->n_classes, D = head->d_feat;
   ffk::HeadFeatures f;
   FF_TRY(head_features(layers, n_layers, first_layer, hp, x_base, n, C, hs, st, f));
+  head_weights(f, head->W, head->b, D);
   FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * n * C * D,
                 (double)n * D * 4.0 + (double)C * D * 4.0 + n * (C + 1) * 4.0, st, [&] {
-                  return ffk::launch_head_logits(f, head->W, head->b, n, C, D, nullptr, logits,
-                                                 pred, nullptr, nullptr, st);
+                  return ffk::launch_head_logits(f, n, C, nullptr, logits, pred, nullptr,
+                                                 nullptr, st);
                 }));
   return FF_OK;
 }
@@ -787,9 +885,11 @@ struct PipeScratch {
   float *act_s[2] = {nullptr, nullptr};  // sequential, fp32: their row normalisation
 };
 
+// rpp: rows per sample in a chunk (2 for FF: a positive and a negative row;
+// 1 for the performance-optimised variant); po_classes > 0 adds its scratch.
 void carve_pipe(Carver &cv, PipeScratch &p, const ff_layer *layers, int L, int n, int chunk,
-                int sched, int dtype) {
-  const int rows = 2 * std::min(chunk, n);
+                int sched, int dtype, int rpp = 2, int po_classes = 0) {
+  const int rows = rpp * std::min(chunk, n);
   if (sched == FF_PIPELINED) {
     p.step.assign(L, StepScratch());
     for (int k = 0; k < 2; ++k) {
@@ -798,7 +898,7 @@ void carve_pipe(Carver &cv, PipeScratch &p, const ff_layer *layers, int L, int n
     }
     for (int l = 0; l < L; ++l)
       carve_step(cv, p.step[l], rows, l == 0 || dtype == FF_BF16 ? layers[l].d_in : 0,
-                 layers[l].d_out, dtype, l + 1 == L, false, false);
+                 layers[l].d_out, dtype, l + 1 == L, false, false, po_classes);
     for (int l = 1; l < L; ++l)
       for (int k = 0; k < 2; ++k) {
         p.slot[k][l] = static_cast<float *>(cv.take((size_t)rows * layers[l].d_in * 4));
@@ -811,13 +911,13 @@ void carve_pipe(Carver &cv, PipeScratch &p, const ff_layer *layers, int L, int n
       max_out = std::max(max_out, layers[l].d_out);
     }
     p.step.assign(1, StepScratch());
-    carve_step(cv, p.step[0], rows, max_in, max_out, dtype, true, false, false);
+    carve_step(cv, p.step[0], rows, max_in, max_out, dtype, true, false, false, po_classes);
     int max_hidden = 0;
     for (int l = 0; l + 1 < L; ++l) max_hidden = std::max(max_hidden, layers[l].d_out);
     if (L > 1)
       for (int k = 0; k < 2; ++k) {
-        p.act[k] = static_cast<float *>(cv.take((size_t)2 * n * max_hidden * 4));
-        if (dtype == FF_F32) p.act_s[k] = static_cast<float *>(cv.take((size_t)2 * n * 4));
+        p.act[k] = static_cast<float *>(cv.take((size_t)rpp * n * max_hidden * 4));
+        if (dtype == FF_F32) p.act_s[k] = static_cast<float *>(cv.take((size_t)rpp * n * 4));
       }
   }
 }
@@ -839,6 +939,90 @@ size_t ff_pipeline_workspace_size(const ff_layer *layers, int32_t n_layers, int3
   carve_pipe(cv, p, layers, n_layers, n, chunk_pairs, schedule, dtype);
   return cv.off + kAlign;
 }
+
+}  // extern "C"
+
+namespace {
+// Chunk-by-chunk training over `epochs` passes, sequential or one stream per
+// layer (see ff_pipeline_epoch).  input0(start, b) describes layer 0's rows of
+// the chunk of b samples at `start` (rpp rows per sample); step(l, in, start,
+// b, h_out, loss, s_next, scratch, stream) runs one training step of layer l.
+template <class Input0, class Step>
+ff_status epoch_core(ff_layer *layers, int n_layers, const ff_hparams *hp, int n, int chunk_pairs,
+                     int epochs, int schedule, void *const *streams, float *loss_trace,
+                     PipeScratch &p, int rpp, Input0 input0, Step step) {
+  const int nc = (n + chunk_pairs - 1) / chunk_pairs;
+  const int steps = nc * epochs;
+  auto chunk_map = [&](int c, int &start, int &b) {
+    start = c * chunk_pairs;
+    b = std::min(chunk_pairs, n - start);
+  };
+
+  if (schedule == FF_SEQUENTIAL) {
+    hipStream_t st = static_cast<hipStream_t>(streams[0]);
+    for (int l = 0; l < n_layers; ++l) {
+      ff_layer *L = &layers[l];
+      const float *in = l == 0 ? nullptr : p.act[(l - 1) & 1];
+      const float *in_s = l == 0 ? nullptr : p.act_s[(l - 1) & 1];
+      auto input = [&](int start, int b) {
+        if (l == 0) return input0(start, b);
+        return raw_rows(in + (size_t)rpp * start * L->d_in,
+                        in_s ? in_s + (size_t)rpp * start : nullptr);
+      };
+      for (int q = 0; q < steps; ++q) {
+        int start, b;
+        chunk_map(q % nc, start, b);
+        FF_TRY(step(l, input(start, b), start, b, nullptr,
+                    loss_trace ? loss_trace + (size_t)l * steps + q : nullptr, nullptr, p.step[0],
+                    st));
+      }
+      if (l + 1 < n_layers) {
+        float *out = p.act[l & 1];
+        float *out_s = p.act_s[l & 1];
+        for (int c = 0; c < nc; ++c) {
+          int start, b;
+          chunk_map(c, start, b);
+          FF_TRY(forward_core(L, hp, input(start, b), rpp * b,
+                              out + (size_t)rpp * start * L->d_out, nullptr,
+                              out_s ? out_s + (size_t)rpp * start : nullptr, p.step[0], st));
+        }
+      }
+    }
+    return FF_OK;
+  }
+
+  // Pipelined: done[l][q % kRing] marks layer l's step q complete.  Layer l's
+  // step q waits for layer l-1's step q (its input slot is filled) and, before
+  // it overwrites layer l+1's slot q%2, for layer l+1's step q-2 (the slot's
+  // previous reader).  Both waits are enqueued before the event is recorded
+  // again kRing steps later, so a ring of 4 events per layer suffices.
+  constexpr int kRing = 4;
+  EventRing ring;
+  ring.ev.assign((size_t)n_layers * kRing, nullptr);
+  for (auto &e : ring.ev) FF_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  for (int q = 0; q < steps; ++q) {
+    int start, b;
+    chunk_map(q % nc, start, b);
+    for (int l = 0; l < n_layers; ++l) {
+      ff_layer *L = &layers[l];
+      hipStream_t st = static_cast<hipStream_t>(streams[l]);
+      if (l > 0) FF_HIP(hipStreamWaitEvent(st, ring.ev[(size_t)(l - 1) * kRing + q % kRing], 0));
+      if (l + 1 < n_layers && q >= 2)
+        FF_HIP(hipStreamWaitEvent(st, ring.ev[(size_t)(l + 1) * kRing + (q - 2) % kRing], 0));
+      const LayerInput in = l == 0 ? input0(start, b)
+                                   : raw_rows(p.slot[q & 1][l], p.slot_s[q & 1][l]);
+      const bool next = l + 1 < n_layers;
+      FF_TRY(step(l, in, start, b, next ? p.slot[q & 1][l + 1] : nullptr,
+                  loss_trace ? loss_trace + (size_t)l * steps + q : nullptr,
+                  next ? p.slot_s[q & 1][l + 1] : nullptr, p.step[l], st));
+      FF_HIP(hipEventRecord(ring.ev[(size_t)l * kRing + q % kRing], st));
+    }
+  }
+  return FF_OK;
+}
+}  // namespace
+
+extern "C" {
 
 ff_status ff_pipeline_epoch(ff_layer *layers, int32_t n_layers, const ff_hparams *hp,
                             const float *x_base, const int32_t *y_pos, const int32_t *y_neg,
@@ -865,12 +1049,6 @@ ff_status ff_pipeline_epoch(ff_layer *layers, int32_t n_layers, const ff_hparams
   PipeScratch p;
   carve_pipe(cv, p, layers, n_layers, n, chunk_pairs, schedule, hp->dtype);
 
-  const int nc = (n + chunk_pairs - 1) / chunk_pairs;
-  const int steps = nc * epochs;
-  auto chunk_map = [&](int c, int &start, int &b) {
-    start = c * chunk_pairs;
-    b = std::min(chunk_pairs, n - start);
-  };
   auto pairs_map = [&](int start, int b) {
     ffk::RowMap m{};
     m.base = x_base;
@@ -882,74 +1060,176 @@ ff_status ff_pipeline_epoch(ff_layer *layers, int32_t n_layers, const ff_hparams
     m.n_classes = n_classes;
     return m;
   };
+  auto input0 = [&](int start, int b) {
+    LayerInput li;
+    li.src = pairs_map(start, b);
+    return li;
+  };
+  auto step = [&](int l, const LayerInput &in, int, int b, float *h_out, float *loss,
+                  float *s_next, StepScratch &sc, hipStream_t st) {
+    return step_core(&layers[l], hp, in, b, b, h_out, nullptr, loss, s_next, sc, st);
+  };
+  return epoch_core(layers, n_layers, hp, n, chunk_pairs, epochs, schedule, streams, loss_trace,
+                    p, 2, input0, step);
+}
 
-  if (schedule == FF_SEQUENTIAL) {
-    hipStream_t st = static_cast<hipStream_t>(streams[0]);
-    for (int l = 0; l < n_layers; ++l) {
-      ff_layer *L = &layers[l];
-      const float *in = l == 0 ? nullptr : p.act[(l - 1) & 1];
-      const float *in_s = l == 0 ? nullptr : p.act_s[(l - 1) & 1];
-      auto input = [&](int start, int b) {
-        if (l == 0) {
-          LayerInput li;
-          li.src = pairs_map(start, b);
-          return li;
-        }
-        return raw_rows(in + (size_t)2 * start * L->d_in,
-                        in_s ? in_s + (size_t)2 * start : nullptr);
-      };
-      for (int q = 0; q < steps; ++q) {
-        int start, b;
-        chunk_map(q % nc, start, b);
-        FF_TRY(step_core(L, hp, input(start, b), b, b, nullptr, nullptr,
-                         loss_trace ? loss_trace + (size_t)l * steps + q : nullptr, nullptr,
-                         p.step[0], st));
-      }
-      if (l + 1 < n_layers) {
-        float *out = p.act[l & 1];
-        float *out_s = p.act_s[l & 1];
-        for (int c = 0; c < nc; ++c) {
-          int start, b;
-          chunk_map(c, start, b);
-          FF_TRY(forward_core(L, hp, input(start, b), 2 * b, out + (size_t)2 * start * L->d_out,
-                              nullptr, out_s ? out_s + (size_t)2 * start : nullptr, p.step[0],
-                              st));
-        }
-      }
-    }
-    return FF_OK;
-  }
+// ---------------------------------------------------------------------------
+// Performance-optimised PFF
+// ---------------------------------------------------------------------------
+namespace {
+ff_status check_po_head(const ff_head *h, int d_out, int l) {
+  if (!h) return fail(FF_ERR_INVALID_ARG, "head %d is NULL", l);
+  if (h->d_feat != d_out)
+    return fail(FF_ERR_INVALID_ARG, "head %d: d_feat=%d, layer d_out=%d", l, h->d_feat, d_out);
+  if (h->n_classes < 2 || h->n_classes > ffk::kHeadMaxClasses)
+    return fail(FF_ERR_INVALID_ARG, "head %d: n_classes=%d outside [2, %d]", l, h->n_classes,
+                ffk::kHeadMaxClasses);
+  if (!h->W || !h->b || !h->mW || !h->vW || !h->mb || !h->vb)
+    return fail(FF_ERR_INVALID_ARG, "head %d: a buffer is NULL", l);
+  return FF_OK;
+}
+}  // namespace
 
-  // Pipelined: done[l][q % kRing] marks layer l's step q complete.  Layer l's
-  // step q waits for layer l-1's step q (its input slot is filled) and, before
-  // it overwrites layer l+1's slot q%2, for layer l+1's step q-2 (the slot's
-  // previous reader).  Both waits are enqueued before the event is recorded
-  // again kRing steps later, so a ring of 4 events per layer suffices.
-  constexpr int kRing = 4;
-  EventRing ring;
-  ring.ev.assign((size_t)n_layers * kRing, nullptr);
-  for (auto &e : ring.ev) FF_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
-  for (int q = 0; q < steps; ++q) {
-    int start, b;
-    chunk_map(q % nc, start, b);
-    for (int l = 0; l < n_layers; ++l) {
-      ff_layer *L = &layers[l];
-      hipStream_t st = static_cast<hipStream_t>(streams[l]);
-      if (l > 0) FF_HIP(hipStreamWaitEvent(st, ring.ev[(size_t)(l - 1) * kRing + q % kRing], 0));
-      if (l + 1 < n_layers && q >= 2)
-        FF_HIP(hipStreamWaitEvent(st, ring.ev[(size_t)(l + 1) * kRing + (q - 2) % kRing], 0));
-      LayerInput in;
-      if (l == 0)
-        in.src = pairs_map(start, b);
-      else
-        in = raw_rows(p.slot[q & 1][l], p.slot_s[q & 1][l]);
-      const bool next = l + 1 < n_layers;
-      FF_TRY(step_core(L, hp, in, b, b, next ? p.slot[q & 1][l + 1] : nullptr, nullptr,
-                       loss_trace ? loss_trace + (size_t)l * steps + q : nullptr,
-                       next ? p.slot_s[q & 1][l + 1] : nullptr, p.step[l], st));
-      FF_HIP(hipEventRecord(ring.ev[(size_t)l * kRing + q % kRing], st));
-    }
+size_t ff_po_step_workspace_size(int32_t rows, int32_t d_in, int32_t d_out, int32_t n_classes,
+                                 int32_t dtype) {
+  if (rows <= 0 || d_in <= 0 || d_out <= 0 || n_classes <= 0) return 0;
+  Carver cv(nullptr);
+  StepScratch s;
+  carve_step(cv, s, rows, d_in, d_out, dtype, true, false, true, n_classes);
+  return cv.off + kAlign;
+}
+
+ff_status ff_po_layer_step(ff_layer *L, ff_head *head, const ff_hparams *hp,
+                           const ff_hparams *head_hp, const float *x, const int32_t *labels,
+                           int32_t rows, int32_t x_normalised, float *h_out, float *loss, void *ws,
+                           size_t ws_bytes, void *stream) {
+  FF_TRY(check_hp(hp));
+  FF_TRY(check_hp(head_hp));
+  FF_TRY(check_layer(L, hp, true, 0));
+  FF_TRY(check_po_head(head, L->d_out, 0));
+  if (rows < 1) return fail(FF_ERR_INVALID_ARG, "rows=%d", rows);
+  if (!x || !labels) return fail(FF_ERR_INVALID_ARG, "x or labels is NULL");
+  const int C = head->n_classes;
+  Carver size_cv(nullptr);
+  StepScratch tmp;
+  carve_step(size_cv, tmp, rows, L->d_in, L->d_out, hp->dtype, true, false, true, C);
+  FF_TRY(check_ws(ws, ws_bytes, size_cv.off + kAlign));
+  Carver cv(ws);
+  StepScratch s;
+  carve_step(cv, s, rows, L->d_in, L->d_out, hp->dtype, true, false, true, C);
+  LayerInput in;
+  in.src = rows_of(x);
+  in.normalised = x_normalised != 0;
+  return po_step_core(L, head, hp, head_hp, in, rows, labels, h_out, loss, nullptr, s,
+                      static_cast<hipStream_t>(stream));
+}
+
+size_t ff_po_epoch_workspace_size(const ff_layer *layers, int32_t n_layers, int32_t n,
+                                  int32_t n_classes, int32_t chunk, int32_t schedule,
+                                  int32_t dtype) {
+  if (!layers || n_layers <= 0 || n <= 0 || chunk <= 0 || n_classes <= 0) return 0;
+  Carver cv(nullptr);
+  PipeScratch p;
+  carve_pipe(cv, p, layers, n_layers, n, chunk, schedule, dtype, 1, n_classes);
+  return cv.off + kAlign;
+}
+
+ff_status ff_po_epoch(ff_layer *layers, ff_head *heads, int32_t n_layers, const ff_hparams *hp,
+                      const ff_hparams *head_hp, const float *x_base, const int32_t *labels,
+                      int32_t n, int32_t n_classes, int32_t chunk, int32_t epochs,
+                      int32_t schedule, void *const *streams, float *loss_trace, void *ws,
+                      size_t ws_bytes) {
+  FF_TRY(check_hp(hp));
+  FF_TRY(check_hp(head_hp));
+  FF_TRY(check_stack(layers, n_layers, hp, true));
+  if (!heads) return fail(FF_ERR_INVALID_ARG, "heads is NULL");
+  for (int l = 0; l < n_layers; ++l) {
+    FF_TRY(check_po_head(&heads[l], layers[l].d_out, l));
+    if (heads[l].n_classes != n_classes)
+      return fail(FF_ERR_INVALID_ARG, "head %d: n_classes=%d, expected %d", l,
+                  heads[l].n_classes, n_classes);
   }
+  if (schedule != FF_SEQUENTIAL && schedule != FF_PIPELINED)
+    return fail(FF_ERR_INVALID_ARG, "schedule=%d", schedule);
+  if (n <= 0 || chunk <= 0 || epochs <= 0)
+    return fail(FF_ERR_INVALID_ARG, "n=%d chunk=%d epochs=%d", n, chunk, epochs);
+  if (n_classes > layers[0].d_in)
+    return fail(FF_ERR_INVALID_ARG, "n_classes=%d exceeds d_in=%d", n_classes, layers[0].d_in);
+  if (!x_base || !labels || !streams) return fail(FF_ERR_INVALID_ARG, "NULL pointer argument");
+  Carver size_cv(nullptr);
+  PipeScratch tmp;
+  carve_pipe(size_cv, tmp, layers, n_layers, n, chunk, schedule, hp->dtype, 1, n_classes);
+  FF_TRY(check_ws(ws, ws_bytes, size_cv.off + kAlign));
+  Carver cv(ws);
+  PipeScratch p;
+  carve_pipe(cv, p, layers, n_layers, n, chunk, schedule, hp->dtype, 1, n_classes);
+  auto input0 = [&](int start, int) {
+    LayerInput li;
+    li.src.base = x_base;
+    li.src.mode = ffk::NEUTRAL;
+    li.src.base_off = start;
+    li.src.n_classes = n_classes;
+    return li;
+  };
+  auto step = [&](int l, const LayerInput &in, int start, int b, float *h_out, float *loss,
+                  float *s_next, StepScratch &sc, hipStream_t st) {
+    return po_step_core(&layers[l], &heads[l], hp, head_hp, in, b, labels + start, h_out, loss,
+                        s_next, sc, st);
+  };
+  return epoch_core(layers, n_layers, hp, n, chunk, epochs, schedule, streams, loss_trace, p, 1,
+                    input0, step);
+}
+
+size_t ff_po_predict_workspace_size(const ff_layer *layers, int32_t n_layers, int32_t n,
+                                    int32_t n_classes, int32_t dtype) {
+  return ff_head_workspace_size(layers, n_layers, 0, n, n_classes, dtype);
+}
+
+ff_status ff_po_predict(const ff_layer *layers, const ff_head *heads, int32_t n_layers,
+                        const ff_hparams *hp, const float *x_base, int32_t n, int32_t all_layers,
+                        float *logits, int32_t *pred, void *ws, size_t ws_bytes, void *stream) {
+  FF_TRY(check_hp(hp));
+  FF_TRY(check_stack(layers, n_layers, hp, false));
+  if (!heads) return fail(FF_ERR_INVALID_ARG, "heads is NULL");
+  if (n_layers > ffk::kHeadMaxBlocks)
+    return fail(FF_ERR_UNSUPPORTED, "%d layers (at most %d)", n_layers, ffk::kHeadMaxBlocks);
+  const int C = heads[0].n_classes;
+  for (int l = 0; l < n_layers; ++l) {
+    if (!heads[l].W || !heads[l].b) return fail(FF_ERR_INVALID_ARG, "head %d: W or b is NULL", l);
+    if (heads[l].d_feat != layers[l].d_out || heads[l].n_classes != C || C < 2 ||
+        C > ffk::kHeadMaxClasses || C > layers[0].d_in)
+      return fail(FF_ERR_INVALID_ARG, "head %d: shape does not match", l);
+  }
+  if (n < 0) return fail(FF_ERR_INVALID_ARG, "n=%d", n);
+  if (n == 0) return FF_OK;
+  if (!x_base || !pred) return fail(FF_ERR_INVALID_ARG, "x_base or pred is NULL");
+  Carver size_cv(nullptr);
+  HeadScratch tmp;
+  carve_head(size_cv, tmp, layers, n_layers, 0, n, C, hp->dtype);
+  FF_TRY(check_ws(ws, ws_bytes, size_cv.off + kAlign));
+  Carver cv(ws);
+  HeadScratch hs;
+  carve_head(cv, hs, layers, n_layers, 0, n, C, hp->dtype);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  ffk::HeadFeatures all;
+  FF_TRY(head_features(layers, n_layers, 0, hp, x_base, n, C, hs, st, all));
+  // raw activities of every layer (or the last) against their own classifiers
+  ffk::HeadFeatures f{};
+  const int l0 = all_layers ? 0 : n_layers - 1;
+  for (int l = l0; l < n_layers; ++l) {
+    const int i = f.n_blocks++;
+    f.h[i] = all.h[l];
+    f.s[i] = nullptr;
+    f.d[i] = layers[l].d_out;
+    f.w[i] = heads[l].W;
+    f.ldw[i] = layers[l].d_out;
+    f.bias[f.n_bias++] = heads[l].b;
+  }
+  double D = 0;
+  for (int l = l0; l < n_layers; ++l) D += layers[l].d_out;
+  FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * n * C * D, (double)n * D * 4.0 + C * D * 4.0, st, [&] {
+    return ffk::launch_head_logits(f, n, C, nullptr, logits, pred, nullptr, nullptr, st);
+  }));
   return FF_OK;
 }
 

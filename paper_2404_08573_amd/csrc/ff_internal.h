@@ -57,8 +57,10 @@ struct LossFinish {
   float *loss;         // null: not wanted
 };
 
-// Features of the softmax prediction layer: the concatenation of layer blocks
-// A_l[r][j] = s_l[r] * H_l[r][j] (normalised activities), block l of width d[l].
+// Features of a softmax classifier: the concatenation of layer blocks
+// A_l[r][j] = s_l[r] * H_l[r][j], block l of width d[l] (s_l null: scale 1).
+// Block l's classifier weights are w[l] [C][d[l]] with row stride ldw[l];
+// logits = sum over blocks of A_l w_l^T + sum of the n_bias bias vectors.
 constexpr int kHeadMaxBlocks = 8;
 constexpr int kHeadMaxClasses = 16;
 struct HeadFeatures {
@@ -66,22 +68,31 @@ struct HeadFeatures {
   const float *h[kHeadMaxBlocks];
   const float *s[kHeadMaxBlocks];
   int32_t d[kHeadMaxBlocks];
+  const float *w[kHeadMaxBlocks];
+  int32_t ldw[kHeadMaxBlocks];
+  int32_t n_bias;
+  const float *bias[kHeadMaxBlocks];
 };
 
-// Softmax head forward on n rows: logits = A W^T + b (W [C][D]), then the
-// softmax.  Writes logits [n][C] and pred [n] (argmax, lowest class on ties)
-// when non-null; with labels (training) also G[n][C] = (p - onehot) / n, the
-// gradient of the mean cross-entropy with respect to the logits, and the
-// per-row loss lrow [n].
-hipError_t launch_head_logits(const HeadFeatures &f, const float *W, const float *b, int n,
-                              int C, int D, const int32_t *labels, float *logits, int32_t *pred,
-                              float *G, float *lrow, hipStream_t s);
+// Softmax classifier forward on n rows (C classes), then the softmax.  Writes
+// logits [n][C] and pred [n] (argmax, lowest class on ties) when non-null;
+// with labels (training) also G[n][C] = (p - onehot) / n, the gradient of the
+// mean cross-entropy with respect to the logits, and the per-row loss lrow [n].
+hipError_t launch_head_logits(const HeadFeatures &f, int n, int C, const int32_t *labels,
+                              float *logits, int32_t *pred, float *G, float *lrow,
+                              hipStream_t s);
+
+// Performance-optimised layer backprop through its classifier:
+// dZ[r][j] = [H[r][j] > 0] * sum_c G[r][c] Wc[c][j] (H [R][D], Wc [C][D]),
+// and ones[r] = 1 (the row scale of the weight-gradient product).
+hipError_t launch_po_dz(const float *H, const float *G, const float *Wc, int R, int D, int C,
+                        float *dZ, float *ones, hipStream_t s);
 
 // Row splits of the head's weight-gradient reduction.
 int head_grad_splits(int n);
 
-// Head weight gradient partials: part[split][C][D] = sum over the split's rows
-// of G[r][c] * A[r][f].
+// Classifier weight-gradient partials: part[split][C][D] = sum over the
+// split's rows of G[r][c] * A[r][f] (the weights in f are not read).
 hipError_t launch_head_grad(const HeadFeatures &f, const float *G, int n, int C, int D,
                             int splits, float *part, hipStream_t s);
 

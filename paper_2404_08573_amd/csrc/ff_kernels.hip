@@ -1039,10 +1039,7 @@ __device__ __forceinline__ int head_block(const HeadFeatures &hf, int f, int &j)
 
 // One wave per row: the C dot products over the row's feature blocks, reduced
 // across the wave, then the softmax on lanes 0..C-1.
-__global__ __launch_bounds__(kBlock) void k_head_logits(HeadFeatures hf,
-                                                        const float *__restrict__ W,
-                                                        const float *__restrict__ bias, int n,
-                                                        int C, int D,
+__global__ __launch_bounds__(kBlock) void k_head_logits(HeadFeatures hf, int n, int C,
                                                         const int32_t *__restrict__ labels,
                                                         float *__restrict__ logits,
                                                         int32_t *__restrict__ pred,
@@ -1054,11 +1051,11 @@ __global__ __launch_bounds__(kBlock) void k_head_logits(HeadFeatures hf,
   float acc[kHeadMaxClasses];
 #pragma unroll
   for (int c = 0; c < kHeadMaxClasses; ++c) acc[c] = 0.f;
-  int off = 0;
   for (int blk = 0; blk < hf.n_blocks; ++blk) {
-    const int d = hf.d[blk];
+    const int d = hf.d[blk], ldw = hf.ldw[blk];
     const float *hr = hf.h[blk] + (size_t)r * d;
-    const float sr = hf.s[blk][r];
+    const float *wb = hf.w[blk];
+    const float sr = hf.s[blk] ? hf.s[blk][r] : 1.f;
     for (int i = lane; i < (d >> 2); i += 64) {
       float4 a = ld4(hr + 4 * i);
       a.x *= sr;
@@ -1068,18 +1065,18 @@ __global__ __launch_bounds__(kBlock) void k_head_logits(HeadFeatures hf,
 #pragma unroll
       for (int c = 0; c < kHeadMaxClasses; ++c)
         if (c < C) {
-          const float4 w = ld4(W + (size_t)c * D + off + 4 * i);
+          const float4 w = ld4(wb + (size_t)c * ldw + 4 * i);
           acc[c] += a.x * w.x + a.y * w.y + a.z * w.z + a.w * w.w;
         }
     }
-    off += d;
   }
   float z = 0.f, zmax = -INFINITY;
   int arg = 0;
 #pragma unroll
   for (int c = 0; c < kHeadMaxClasses; ++c)
     if (c < C) {
-      const float v = wave_sum(acc[c]) + bias[c];
+      float v = wave_sum(acc[c]);
+      for (int k = 0; k < hf.n_bias; ++k) v += hf.bias[k][c];
       if (lane == c) z = v;
       if (v > zmax) {
         zmax = v;
@@ -1101,6 +1098,37 @@ __global__ __launch_bounds__(kBlock) void k_head_logits(HeadFeatures hf,
   }
 }
 
+// Backprop of a layer's classifier into the layer: one thread per 4
+// consecutive units of a row.
+__global__ __launch_bounds__(kBlock) void k_po_dz(const float *__restrict__ H,
+                                                  const float *__restrict__ G,
+                                                  const float *__restrict__ Wc, int R, int D,
+                                                  int C, float *__restrict__ dZ,
+                                                  float *__restrict__ ones) {
+  const int q = blockIdx.x * kBlock + threadIdx.x;
+  const int d4 = D >> 2;
+  if (q >= R * d4) return;
+  const int r = q / d4, j = 4 * (q % d4);
+  const float4 h = ld4(H + (size_t)r * D + j);
+  float4 g = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int c = 0; c < kHeadMaxClasses; ++c)
+    if (c < C) {
+      const float gc = G[(size_t)r * C + c];
+      const float4 w = ld4(Wc + (size_t)c * D + j);
+      g.x += gc * w.x;
+      g.y += gc * w.y;
+      g.z += gc * w.z;
+      g.w += gc * w.w;
+    }
+  g.x = h.x > 0.f ? g.x : 0.f;  // the ReLU derivative (h = 0 wherever z <= 0)
+  g.y = h.y > 0.f ? g.y : 0.f;
+  g.z = h.z > 0.f ? g.z : 0.f;
+  g.w = h.w > 0.f ? g.w : 0.f;
+  st4(dZ + (size_t)r * D + j, g);
+  if (j == 0) ones[r] = 1.f;
+}
+
 // One thread per 4 consecutive features and split of rows: C x 4 partial sums.
 __global__ __launch_bounds__(kBlock) void k_head_grad(HeadFeatures hf,
                                                       const float *__restrict__ G, int n, int C,
@@ -1112,14 +1140,14 @@ __global__ __launch_bounds__(kBlock) void k_head_grad(HeadFeatures hf,
   const int blk = head_block(hf, f, j);
   const int d = hf.d[blk];
   const float *h = hf.h[blk] + j;
-  const float *sv = hf.s[blk];
+  const float *sv = hf.s[blk];  // null: scale 1
   const int r0 = blockIdx.y * rows_per_split, r1 = min(n, r0 + rows_per_split);
   float4 acc[kHeadMaxClasses];
 #pragma unroll
   for (int c = 0; c < kHeadMaxClasses; ++c) acc[c] = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int r = r0; r < r1; ++r) {
     float4 a = ld4(h + (size_t)r * d);
-    const float sr = sv[r];
+    const float sr = sv ? sv[r] : 1.f;
     a.x *= sr;
     a.y *= sr;
     a.z *= sr;
@@ -1469,15 +1497,24 @@ hipError_t launch_argmax(const float *scores, int n, int C, const int32_t *exclu
   return hipGetLastError();
 }
 
-hipError_t launch_head_logits(const HeadFeatures &f, const float *W, const float *b, int n,
-                              int C, int D, const int32_t *labels, float *logits, int32_t *pred,
-                              float *G, float *lrow, hipStream_t s) {
+hipError_t launch_head_logits(const HeadFeatures &f, int n, int C, const int32_t *labels,
+                              float *logits, int32_t *pred, float *G, float *lrow,
+                              hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  if (C < 1 || C > kHeadMaxClasses || C > 64 || f.n_blocks < 1 || f.n_blocks > kHeadMaxBlocks ||
-      ((G || lrow) && !labels))
+  if (C < 1 || C > kHeadMaxClasses || f.n_blocks < 1 || f.n_blocks > kHeadMaxBlocks ||
+      f.n_bias < 0 || f.n_bias > kHeadMaxBlocks || ((G || lrow) && !labels))
     return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_head_logits, dim3(cdiv(n, kBlock / 64)), dim3(kBlock), 0, s, f, W, b, n, C,
-                     D, labels, logits, pred, G, lrow);
+  hipLaunchKernelGGL(k_head_logits, dim3(cdiv(n, kBlock / 64)), dim3(kBlock), 0, s, f, n, C,
+                     labels, logits, pred, G, lrow);
+  return hipGetLastError();
+}
+
+hipError_t launch_po_dz(const float *H, const float *G, const float *Wc, int R, int D, int C,
+                        float *dZ, float *ones, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  if (C < 1 || C > kHeadMaxClasses || D % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_po_dz, dim3(cdiv((long)R * (D / 4), kBlock)), dim3(kBlock), 0, s, H, G,
+                     Wc, R, D, C, dZ, ones);
   return hipGetLastError();
 }
 

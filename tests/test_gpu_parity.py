@@ -591,3 +591,107 @@ def test_head_full_size_sampled(P):
                                   O.HParams(), 1)
     assert_acts(zg[idx], z_ref)
     assert_labels(pg[idx], z_ref, p_ref)
+
+
+# ------------------------------------------------------------------ Performance-Optimised PFF
+def _po_case(seed, d_in, d_out, C, rows):
+    x_base, y, _ = make_data(seed, rows, d_in)
+    y = (y % C).astype(np.int32)
+    (W, b), = make_weights(seed + 1, (d_in, d_out))
+    b = b + np.linspace(-0.02, 0.05, d_out).astype(np.float32)
+    rng = np.random.default_rng(seed + 2)
+    Wc = rng.uniform(-0.2, 0.2, (C, d_out)).astype(np.float32)
+    bc = rng.uniform(-0.1, 0.1, C).astype(np.float32)
+    return O.embed_neutral(x_base, C).astype(np.float32), y, W, b, Wc, bc
+
+
+def _po_mags(L, Hd, x, y, hp):
+    """Sum of |terms| of every weight-gradient element at the oracle's current
+    weights (for the conditioning rule), before the step is taken."""
+    xh, z, h, _ = O.layer_forward(L.W, L.b, x, hp.norm_eps, False, hp.bf16)
+    _, d, _ = O.softmax_xent(h @ Hd.W.T + Hd.b, y)
+    dz = np.abs((d @ Hd.W) * (z > 0))
+    return (dz.T @ np.abs(xh), dz.sum(axis=0), np.abs(d).T @ np.abs(h), np.abs(d).sum(axis=0))
+
+
+@pytest.mark.parametrize("d_in,d_out,C,rows,bf16", [(64, 96, 10, 150, False),
+                                                    (784, 2000, 10, 1024, False),
+                                                    (200, 260, 16, 77, False),
+                                                    (64, 96, 10, 150, True)])
+def test_po_layer_steps_parity(P, d_in, d_out, C, rows, bf16):
+    x, y, W, b, Wc, bc = _po_case(100 + d_in, d_in, d_out, C, rows)
+    hp_kw = dict(lr=0.01)
+    hp = P.HParams(dtype=P.FF_BF16 if bf16 else P.FF_F32, **hp_kw)
+    ohp = O.HParams(bf16=bf16, **hp_kw)
+    hhp, ohhp = P.HParams(lr=1e-3), O.HParams(lr=1e-3)
+    L = P.Layer(_t(W), _t(b), bf16_shadow=bf16)
+    Hd = P.Head(_t(Wc), _t(bc))
+    ref, refh = O.Layer.from_params(W, b), O.Head.from_params(Wc, bc)
+    h = torch.empty(rows, d_out, device=DEV)
+    loss = torch.empty(1, device=DEV)
+    grads = {k: [] for k in ("W", "b", "Wc", "bc")}
+    mags = {k: [] for k in ("W", "b", "Wc", "bc")}
+    rel = 1e-3 if bf16 else 1e-4
+    for step in range(3):
+        for k, m in zip(("W", "b", "Wc", "bc"), _po_mags(ref, refh, x, y, ohp)):
+            mags[k].append(m)
+        P.ff_po_layer_step(L, Hd, hp, hhp, _t(x), _t(y), h_out=h, loss=loss)
+        l_ref, h_ref, _, dW, db, dWc, dbc = O.po_layer_step(ref, refh, x, y, ohp, ohhp)
+        for k, g in zip(("W", "b", "Wc", "bc"), (dW, db, dWc, dbc)):
+            grads[k].append(g)
+        assert_loss(_np(loss)[0], l_ref, rel=rel)
+        if step == 0:  # later, the weights agree only to the weight bar (Adam-amplified elements)
+            assert_acts(_np(h), h_ref, rel=rel, floor=1e-3 if bf16 else 1e-5)
+    assert L.step == 3 and Hd.step == 3
+    extra = dict(rel=2e-3, outliers=1e-5, outlier_rel=2e-2) if bf16 else {}
+    # first moments: linear in the gradients, so every gradient element is checked
+    assert_weights(_np(L.mW), ref.mW, grads["W"], mags["W"], "mW", **extra)
+    assert_weights(_np(Hd.mW), refh.mW, grads["Wc"], mags["Wc"], "mWc", **extra)
+    assert_weights(_np(L.W), ref.W, grads["W"], mags["W"], "W", lr=0.01, **extra)
+    assert_weights(_np(L.b), ref.b, grads["b"], mags["b"], "b", lr=0.01, **extra)
+    assert_weights(_np(Hd.W), refh.W, grads["Wc"], mags["Wc"], "Wc", lr=1e-3, **extra)
+    assert_weights(_np(Hd.b), refh.b, grads["bc"], mags["bc"], "bc", lr=1e-3, **extra)
+
+
+@pytest.mark.parametrize("sched", [0, 1])
+def test_po_epoch_parity(P, sched):
+    dims, C, n, chunk = (64, 96, 80, 48), 10, 300, 64
+    x_base, y, _ = make_data(110, n, dims[0])
+    params = make_weights(111, dims)
+    rng = np.random.default_rng(112)
+    hws = [rng.uniform(-0.2, 0.2, (C, d)).astype(np.float32) for d in dims[1:]]
+    layers = [P.Layer(_t(W), _t(b)) for W, b in params]
+    heads = [P.Head(_t(Wc), torch.zeros(C, device=DEV)) for Wc in hws]
+    nc = -(-n // chunk)
+    trace = torch.zeros(len(layers), 2 * nc, device=DEV)
+    P.ff_po_epoch(layers, heads, P.HParams(lr=0.01), P.HParams(lr=1e-3), _t(x_base), _t(y), C,
+                  chunk, 2, sched, loss_trace=trace)
+    torch.cuda.synchronize()
+    ref = [O.Layer.from_params(W, b) for W, b in params]
+    refh = [O.Head.from_params(Wc, np.zeros(C)) for Wc in hws]
+    fn = O.po_train_sequential if sched == 0 else O.po_train_pipelined
+    tr_ref = fn(ref, refh, x_base, y, C, chunk, 2, O.HParams(lr=0.01), O.HParams(lr=1e-3))
+    np.testing.assert_allclose(_np(trace), tr_ref, rtol=2e-4)
+    for L, R, Hd, RH in zip(layers, ref, heads, refh):
+        assert L.step == 2 * nc and Hd.step == 2 * nc
+        np.testing.assert_allclose(_np(L.W), R.W, rtol=1e-3, atol=2e-4)
+        np.testing.assert_allclose(_np(Hd.W), RH.W, rtol=1e-3, atol=2e-4)
+
+
+@pytest.mark.parametrize("all_layers", [False, True])
+def test_po_predict_parity(P, all_layers):
+    dims, C, n = (64, 96, 80, 48), 10, 203
+    x_base, _, _ = make_data(113, n, dims[0])
+    params = make_weights(114, dims)
+    rng = np.random.default_rng(115)
+    hw = [(rng.uniform(-0.3, 0.3, (C, d)).astype(np.float32),
+           rng.uniform(-0.1, 0.1, C).astype(np.float32)) for d in dims[1:]]
+    layers = [P.Layer(_t(W), _t(b)) for W, b in params]
+    heads = [P.Head(_t(W), _t(b)) for W, b in hw]
+    logits = torch.empty(n, C, device=DEV)
+    _, pred = P.ff_po_predict(layers, heads, P.HParams(), _t(x_base), all_layers, logits=logits)
+    z_ref, p_ref = O.po_predict([O.Layer.from_params(W, b) for W, b in params],
+                                [O.Head.from_params(W, b) for W, b in hw], x_base, C,
+                                O.HParams(), all_layers)
+    assert_acts(_np(logits), z_ref)
+    assert_labels(_np(pred), z_ref, p_ref)

@@ -509,6 +509,29 @@ def test_po_pipeline_layer_independence_and_one_layer():
     np.testing.assert_array_equal(t[0], seq)
 
 
+def test_po_schedules_agree_for_one_layer_and_when_frozen():
+    """One layer: sequential and pipelined are the same chunk sequence.  With
+    learning rates 0 (weights frozen) every layer sees the same activities in
+    both schedules, so the traces agree for all layers."""
+    x_base, y, _ = make_data(48, 130, 30)
+    dims = (30, 20, 16)
+    params = make_weights(49, dims)
+    rng = np.random.default_rng(50)
+    hw = [rng.uniform(-0.2, 0.2, (10, d)) for d in dims[1:]]
+
+    def run(fn, k, lr, hlr):
+        Ls = [O.Layer.from_params(W, b) for W, b in params[:k]]
+        Hs = [O.Head.from_params(W, np.zeros(10)) for W in hw[:k]]
+        return fn(Ls, Hs, x_base, y, 10, 64, 2, O.HParams(lr=lr), O.HParams(lr=hlr))
+
+    np.testing.assert_array_equal(run(O.po_train_sequential, 1, 0.03, 1e-3),
+                                  run(O.po_train_pipelined, 1, 0.03, 1e-3))
+    np.testing.assert_allclose(run(O.po_train_sequential, 2, 0.0, 0.0),
+                               run(O.po_train_pipelined, 2, 0.0, 0.0), rtol=1e-13)
+    assert np.any(run(O.po_train_sequential, 2, 0.03, 1e-3)[1]
+                  != run(O.po_train_pipelined, 2, 0.03, 1e-3)[1])
+
+
 def test_po_predict_last_and_all_layers():
     x_base, _, _ = make_data(45, 20, 30)
     params = make_weights(46, (30, 16, 12))

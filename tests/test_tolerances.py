@@ -120,3 +120,42 @@ def test_planted_oracle_mistakes_fail(mistake):
     with pytest.raises(AssertionError):
         assert_weights(M.W, L.W, gW, mW, "W", lr=hp.lr, adam_eps=hp.adam_eps)
         assert_weights(M.b, L.b, gb, mb, "b", lr=hp.lr, adam_eps=hp.adam_eps)
+
+
+@pytest.mark.parametrize("mistake", ["no_relu_mask", "grad_sign", "no_head_bias_grad",
+                                     "label_shift"])
+def test_planted_po_mistakes_fail(mistake):
+    """The performance-optimised bars (weights with the Adam-amplified set aside,
+    plus the first moments) catch mistakes planted in a copy of the step."""
+    x_base, y, _ = make_data(120, 150, 64)
+    x = O.embed_neutral(x_base, 10)
+    (W, b), = make_weights(121, (64, 96))
+    rng = np.random.default_rng(122)
+    Wc, bc = rng.uniform(-0.2, 0.2, (10, 96)), rng.uniform(-0.1, 0.1, 10)
+    hp, hhp = O.HParams(lr=0.01), O.HParams(lr=1e-3)
+    L, Hd = O.Layer.from_params(W, b), O.Head.from_params(Wc, bc)
+    M, MH = O.Layer.from_params(W, b), O.Head.from_params(Wc, bc)
+    gW, mW = [], []
+    for _ in range(2):
+        xh, z, h, _ = O.layer_forward(L.W, L.b, x, 1e-8)
+        _, d, _ = O.softmax_xent(h @ Hd.W.T + Hd.b, y)
+        mW.append(np.abs((d @ Hd.W) * (z > 0)).T @ np.abs(xh))
+        gW.append(O.po_layer_step(L, Hd, x, y, hp, hhp)[3])
+        # the copy with the mistake
+        xh, z, h, _ = O.layer_forward(M.W, M.b, x, 1e-8)
+        yy = (y + 1) % 10 if mistake == "label_shift" else y
+        _, d, _ = O.softmax_xent(h @ MH.W.T + MH.b, yy)
+        if mistake == "grad_sign":
+            d = -d
+        dz = d @ MH.W if mistake == "no_relu_mask" else (d @ MH.W) * (z > 0)
+        dbc = np.zeros(10) if mistake == "no_head_bias_grad" else d.sum(axis=0)
+        M.t += 1
+        MH.t += 1
+        M.W, M.mW, M.vW = O.adam(M.W, M.mW, M.vW, dz.T @ xh, M.t, 0.01, 0.9, 0.999, 1e-8)
+        M.b, M.mb, M.vb = O.adam(M.b, M.mb, M.vb, dz.sum(0), M.t, 0.01, 0.9, 0.999, 1e-8)
+        MH.W, MH.mW, MH.vW = O.adam(MH.W, MH.mW, MH.vW, d.T @ h, MH.t, 1e-3, 0.9, 0.999, 1e-8)
+        MH.b, MH.mb, MH.vb = O.adam(MH.b, MH.mb, MH.vb, dbc, MH.t, 1e-3, 0.9, 0.999, 1e-8)
+    with pytest.raises(AssertionError):
+        assert_weights(M.mW, L.mW, gW, mW, "mW")
+        assert_weights(M.W, L.W, gW, mW, "W", lr=0.01)
+        assert_weights(MH.b, Hd.b, [np.ones(10)], [np.ones(10)], "bc", lr=1e-3)
