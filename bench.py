@@ -260,6 +260,58 @@ def softmax_head(P, torch, sw, sxd, slayers, reps=5):
     return out
 
 
+def po_and_adaptive(P, torch, w, xd, yd, layers, reps=2):
+    """Performance-Optimised PFF: pipelined epochs of the training workload's
+    net and data (no negatives, a classifier per layer, classifier lr 1e-4).
+    AdaptiveNEG: the hardest wrong label of every training sample under the
+    trained net.  Each HIP-event timed on its own after one untimed call."""
+    from ffinputs import random_matrix
+    dev = torch.device("cuda:0")
+    bf16 = w.dtype == "bf16"
+    dtype = P.FF_BF16 if bf16 else P.FF_F32
+    hp = P.HParams(theta=w.theta, lr=w.lr, norm_eps=w.norm_eps, dtype=dtype)
+    hhp = P.HParams(lr=1e-4)
+    heads = [P.Head(torch.from_numpy(random_matrix(97 + l, w.n_classes, d, -0.05, 0.05)).to(dev),
+                    torch.zeros(w.n_classes, device=dev)) for l, d in enumerate(w.dims[1:])]
+    ws = P.workspace(P.LIB.ff_po_epoch_workspace_size(P._lib._layers_c(layers), len(layers), w.n,
+                                                      w.n_classes, w.chunk_pairs, P.FF_PIPELINED,
+                                                      dtype), dev)
+    cur = torch.cuda.current_stream(dev)
+    streams = [cur] + [torch.cuda.Stream(dev) for _ in range(len(layers) - 1)]
+
+    def po():
+        for s in streams[1:]:
+            s.wait_stream(cur)
+        P.ff_po_epoch(layers, heads, hp, hhp, xd, yd, w.n_classes, w.chunk_pairs, 1,
+                      P.FF_PIPELINED, streams=streams, ws=ws)
+        for s in streams[1:]:
+            cur.wait_stream(s)
+
+    sws = P.workspace(P.ff_score_workspace_size(layers, w.n, w.n_classes, dtype), dev)
+    yneg = torch.empty_like(yd)
+
+    def adaptive():
+        P.ff_adaptive_negatives(layers, hp, xd, yd, w.n_classes, 0, y_neg=yneg, ws=sws)
+
+    out = {}
+    for name, fn in (("po_epoch", po), ("adaptive_negatives", adaptive)):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(cur)
+        for _ in range(reps):
+            fn()
+        b.record(cur)
+        torch.cuda.synchronize()
+        out[name + "_ms"] = a.elapsed_time(b) / reps
+    flops = sum(4.0 * b * di * do for (_, b) in w.chunks()
+                for di, do in zip(w.dims[:-1], w.dims[1:]))
+    out["po_samples_per_s"] = w.n * w.n_layers / (out["po_epoch_ms"] * 1e-3)
+    out["po_mfma_frac"] = flops / (out["po_epoch_ms"] * 1e-3) / 1e12 / PEAK["bf16" if bf16 else "f32"][1]
+    out["adaptive_images_per_s"] = w.n / (out["adaptive_negatives_ms"] * 1e-3)
+    return out
+
+
 def cpu_baseline(w, x_base, y, y_neg, params, sw, sx, sparams, budget_s=12.0):
     """The oracle as it stands, on a bounded sample of the same workload."""
     import numpy as np
@@ -479,6 +531,8 @@ def main():
     out["roofline_isolated"] = isolated_roofline(P, torch, w, dtype, dom, peak, punit)
     if not args.no_other_workloads:
         out["softmax_head"] = softmax_head(P, torch, sw, sxd, slayers)
+        out["performance_optimised_and_adaptive_neg"] = po_and_adaptive(P, torch, w, xd, yd,
+                                                                        layers)
         others = other_workloads(P, torch, ["mnist_784_2000x4", "mnist_784_2000x4_bf16",
                                             "cifar_3072x4_bf16_pipelined"])
         out["other_workloads"] = others
