@@ -274,6 +274,60 @@ def adaptive_negatives(layers: Sequence[Layer], x_base: np.ndarray, labels: np.n
 
 
 # ----------------------------------------------------------------------------
+# Chapter schedules of Single-Layer / All-Layers PFF (Sec. 4.1, Alg. 1; Sec. 4.2, Alg. 2)
+# ----------------------------------------------------------------------------
+def cooldown_lr(lr0: float, epoch: int, epochs: int, cooldown_start: int) -> float:
+    """Learning rate of (0-based) global epoch ``epoch``.  The paper cools the rate
+    down after the 50th of 100 epochs without giving the shape; reading: constant
+    until ``cooldown_start``, then a linear decay that would reach 0 at ``epochs``."""
+    if epoch < cooldown_start or cooldown_start >= epochs:
+        return lr0
+    return lr0 * (epochs - epoch) / (epochs - cooldown_start)
+
+
+def chapter_train(layers: List[Layer], x_base, y, y_neg_chapters, n_classes: int,
+                  chunk_pairs: int, epochs: int, splits: int, cooldown_start: int,
+                  hp: HParams) -> np.ndarray:
+    """Chapter-granularity PFF training (Alg. 1 Single-Layer; Alg. 2 All-Layers).
+
+    The E epochs are split into S chapters of E/S epochs.  In chapter c, layer l
+    first takes as input the training set (positives with labels y, negatives
+    with this chapter's wrong labels: RandomNEG redraws them for every chapter,
+    they are inputs here) passed through layers 0..l-1 as published at the end
+    of their chapter c ("x <- layer(x)" with getLayer(k, chapter)); then it
+    trains for E/S epochs over the chunks, starting from its own weights after
+    chapter c-1, with the cooled-down learning rate of each epoch; then it is
+    published.  Single-Layer (one layer per node) and All-Layers (each node
+    trains the whole net for a chapter, handing each layer on) compute this same
+    dependency graph; they differ in which node does which (layer, chapter).
+    Returns the loss trace ``[L, E * n_chunks]``.
+    """
+    E, S = epochs, splits
+    assert E % S == 0
+    per = E // S
+    chunks = chunk_bounds(x_base.shape[0], chunk_pairs)
+    L = len(layers)
+    trace = np.zeros((L, E * len(chunks)))
+    for c in range(S):
+        published = []
+        for li, Ly in enumerate(layers):
+            # the chapter's input of this layer: every chunk through the published layers
+            inputs = []
+            for (s, b) in chunks:
+                a = chunk_input(x_base, y, y_neg_chapters[c], s, b, n_classes)
+                for P in published:
+                    a = layer_forward(P[0], P[1], a, hp.norm_eps, False, hp.bf16)[2]
+                inputs.append(a)
+            for m in range(per):
+                e = c * per + m
+                hp_e = dataclasses.replace(hp, lr=cooldown_lr(hp.lr, e, E, cooldown_start))
+                for q, (s, b) in enumerate(chunks):
+                    trace[li, e * len(chunks) + q] = layer_step(Ly, inputs[q], b, hp_e).loss
+            published.append((Ly.W.copy(), Ly.b.copy()))
+    return trace
+
+
+# ----------------------------------------------------------------------------
 # Softmax prediction head (Sec. 3 "Prediction", Sec. 5, Sec. 5.1)
 # ----------------------------------------------------------------------------
 NEUTRAL_LABEL = 0.1

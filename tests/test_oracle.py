@@ -333,6 +333,68 @@ def test_adaptive_negatives_order_statistics():
             assert y_neg[n] == next(c for c in ranked if c != y[n])
 
 
+# ---------------------------------------------------------------- chapter schedules
+def test_cooldown_closed_form():
+    assert O.cooldown_lr(0.03, 0, 100, 50) == 0.03
+    assert O.cooldown_lr(0.03, 49, 100, 50) == 0.03
+    assert O.cooldown_lr(0.03, 50, 100, 50) == 0.03
+    assert abs(O.cooldown_lr(0.03, 75, 100, 50) - 0.015) < 1e-18
+    assert abs(O.cooldown_lr(0.03, 99, 100, 50) - 0.0006) < 1e-17
+    assert O.cooldown_lr(0.03, 99, 100, 100) == 0.03  # no cooldown
+
+
+def test_chapters_with_one_split_are_the_sequential_schedule():
+    """S = 1 and no cooldown: every layer trains all its epochs on the final
+    output of the layers below, which is the sequential FF schedule."""
+    x_base, y, y_neg = make_data(60, 150, 30)
+    params = make_weights(61, (30, 20, 16))
+    a = [O.Layer.from_params(W, b) for W, b in params]
+    b = [O.Layer.from_params(W, b) for W, b in params]
+    hp = O.HParams(lr=0.03)
+    ta = O.chapter_train(a, x_base, y, [y_neg], 10, 64, 2, 1, 2, hp)
+    tb = O.train_sequential(b, x_base, y, y_neg, 10, 64, 2, hp)
+    np.testing.assert_allclose(ta, tb, rtol=1e-13)
+    for la, lb in zip(a, b):
+        np.testing.assert_allclose(la.W, lb.W, rtol=1e-13)
+
+
+def test_chapters_layer_major_order_and_negative_redraw():
+    """The result depends only on the (layer, chapter) dependencies: running the
+    same units layer-major, with every published version kept, agrees.  Each
+    chapter uses its own negatives: a different redraw changes the result."""
+    x_base, y, _ = make_data(62, 130, 30)
+    negs = [random_labels(63 + c, 130)[1] for c in range(3)]
+    params = make_weights(64, (30, 20, 16, 12))
+    hp = O.HParams(lr=0.03)
+    E, S, chunk = 3, 3, 64
+    ref = [O.Layer.from_params(W, b) for W, b in params]
+    t_ref = O.chapter_train(ref, x_base, y, negs, 10, chunk, E, S, 1, hp)
+    # layer-major: layer l runs all its chapters, keeping every chapter's version
+    layers = [O.Layer.from_params(W, b) for W, b in params]
+    versions = []  # versions[l][c] = (W, b) published after chapter c
+    chunks = O.chunk_bounds(130, chunk)
+    t = np.zeros_like(t_ref)
+    for li, L in enumerate(layers):
+        versions.append([])
+        for c in range(S):
+            ins = []
+            for (s0, b0) in chunks:
+                a = O.chunk_input(x_base, y, negs[c], s0, b0, 10)
+                for k in range(li):
+                    W, bb = versions[k][c]
+                    a = O.layer_forward(W, bb, a, 1e-8)[2]
+                ins.append(a)
+            for q, (s0, b0) in enumerate(chunks):
+                hp_e = O.HParams(lr=O.cooldown_lr(0.03, c, E, 1))
+                t[li, c * len(chunks) + q] = O.layer_step(L, ins[q], b0, hp_e).loss
+            versions[li].append((L.W.copy(), L.b.copy()))
+    np.testing.assert_allclose(t, t_ref, rtol=1e-13)
+    other = [O.Layer.from_params(W, b) for W, b in params]
+    t_other = O.chapter_train(other, x_base, y, [negs[0]] * 3, 10, chunk, E, S, 1, hp)
+    assert np.any(t_other[:, len(chunks):] != t_ref[:, len(chunks):])
+    np.testing.assert_array_equal(t_other[0, :len(chunks)], t_ref[0, :len(chunks)])
+
+
 # ---------------------------------------------------------------- softmax head
 def test_embed_neutral_hand():
     x = np.arange(24, dtype=np.float32).reshape(2, 12) / 10
