@@ -312,6 +312,46 @@ def po_and_adaptive(P, torch, w, xd, yd, layers, reps=2):
     return out
 
 
+def chapters(P, torch, w, xd, yd, ynd, params, epochs=2, splits=2):
+    """Chapter schedules (Alg. 1 Single-Layer on one stream per layer, Alg. 2
+    All-Layers on two worker streams) of the training workload: `epochs` epochs
+    in `splits` chapters, RandomNEG negatives redrawn per chapter, the rate
+    cooled down from the second chapter.  Each run starts from fresh weights."""
+    from ffinputs import random_labels
+    dev = torch.device("cuda:0")
+    bf16 = w.dtype == "bf16"
+    dtype = P.FF_BF16 if bf16 else P.FF_F32
+    hp = P.HParams(theta=w.theta, lr=w.lr, norm_eps=w.norm_eps, dtype=dtype)
+    negs = torch.stack([ynd] + [torch.from_numpy(random_labels(200 + c, w.n)[1]).to(dev)
+                                for c in range(1, splits)]).contiguous()
+    out = {}
+    for name, assignment, ns in (("single_layer", P.FF_SINGLE_LAYER, w.n_layers),
+                                 ("all_layers", P.FF_ALL_LAYERS, 2)):
+        layers = [P.Layer(torch.from_numpy(W).to(dev), torch.from_numpy(b).to(dev), bf16)
+                  for W, b in params]
+        ws = P.workspace(P.LIB.ff_chapter_workspace_size(P._lib._layers_c(layers), len(layers),
+                                                         w.n, w.chunk_pairs, ns, dtype), dev)
+        cur = torch.cuda.current_stream(dev)
+        streams = [torch.cuda.Stream(dev) for _ in range(ns)]
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(cur)
+        for s in streams:
+            s.wait_stream(cur)
+        P.ff_chapter_train(layers, hp, xd, yd, negs, w.n_classes, w.chunk_pairs, epochs, splits,
+                           epochs // splits, assignment, streams=streams, ws=ws)
+        for s in streams:
+            cur.wait_stream(s)
+        b.record(cur)
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b)
+        out[name] = {"ms": ms, "streams": ns,
+                     "samples_per_s": 2 * w.n * w.n_layers * epochs / (ms * 1e-3)}
+        del layers, ws
+    out["epochs"], out["splits"] = epochs, splits
+    return out
+
+
 def cpu_baseline(w, x_base, y, y_neg, params, sw, sx, sparams, budget_s=12.0):
     """The oracle as it stands, on a bounded sample of the same workload."""
     import numpy as np
@@ -533,6 +573,7 @@ def main():
         out["softmax_head"] = softmax_head(P, torch, sw, sxd, slayers)
         out["performance_optimised_and_adaptive_neg"] = po_and_adaptive(P, torch, w, xd, yd,
                                                                         layers)
+        out["chapter_schedules"] = chapters(P, torch, w, xd, yd, ynd, params)
         others = other_workloads(P, torch, ["mnist_784_2000x4", "mnist_784_2000x4_bf16",
                                             "cifar_3072x4_bf16_pipelined"])
         out["other_workloads"] = others

@@ -52,6 +52,11 @@ typedef enum { FF_F32 = 0, FF_BF16 = 1 } ff_dtype;
 /* Training schedule of ff_pipeline_epoch. */
 typedef enum { FF_SEQUENTIAL = 0, FF_PIPELINED = 1 } ff_schedule;
 
+/* Who trains what in ff_chapter_train: one layer per worker stream for every
+ * chapter (Single-Layer PFF, Alg. 1), or every layer of chapter c on worker
+ * c mod n_streams (All-Layers PFF, Alg. 2). */
+typedef enum { FF_SINGLE_LAYER = 0, FF_ALL_LAYERS = 1 } ff_assignment;
+
 /* One dense ReLU FF layer, h = max(x_hat W^T + b, 0) (Sec. 3, Sec. 5.1).
  * All buffers are caller-owned device memory. */
 typedef struct {
@@ -153,6 +158,34 @@ ff_status ff_adaptive_negatives(const ff_layer *layers, int32_t n_layers,
                                 const float *x_base, const int32_t *labels, int32_t n,
                                 int32_t n_classes, float *scores, int32_t *y_neg, void *ws,
                                 size_t ws_bytes, void *stream);
+
+/* ---- Chapter schedules (Sec. 4.1 Alg. 1 Single-Layer, Sec. 4.2 Alg. 2 All-Layers)
+ * The `epochs` of training are split into `splits` chapters of epochs/splits
+ * epochs.  In chapter c, layer l takes the training set (positives with
+ * y_pos, negatives with this chapter's wrong labels y_neg_chapters[c]: the
+ * RandomNEG redraw, or AdaptiveNEG labels from ff_adaptive_negatives) passed
+ * through layers 0..l-1 as published at the end of their chapter c; then it
+ * trains epochs/splits epochs over the chunks of chunk_pairs pairs, starting
+ * from its own weights after chapter c-1; then its weights are published.
+ * The learning rate of (0-based) epoch e is hp->lr until cooldown_start, then
+ * hp->lr * (epochs - e) / (epochs - cooldown_start) (the paper's cooldown
+ * after epoch 50; its shape is a reading); cooldown_start >= epochs disables it.
+ * Both assignments compute the same result: they differ only in which worker
+ * stream runs which (layer, chapter), as the nodes of Alg. 1 and Alg. 2 do.
+ *   y_neg_chapters (device) [splits][n]; streams (host) [n_streams]
+ *   (FF_SINGLE_LAYER: n_streams == n_layers); loss_trace (device)
+ *   [n_layers][epochs * n_chunks] or NULL.  epochs must be a multiple of
+ *   splits.  The caller must not touch the layers or ws until all streams
+ *   have drained. */
+size_t ff_chapter_workspace_size(const ff_layer *layers, int32_t n_layers, int32_t n,
+                                 int32_t chunk_pairs, int32_t n_streams, int32_t dtype);
+
+ff_status ff_chapter_train(ff_layer *layers, int32_t n_layers, const ff_hparams *hp,
+                           const float *x_base, const int32_t *y_pos,
+                           const int32_t *y_neg_chapters, int32_t n, int32_t n_classes,
+                           int32_t chunk_pairs, int32_t epochs, int32_t splits,
+                           int32_t cooldown_start, int32_t assignment, int32_t n_streams,
+                           void *const *streams, float *loss_trace, void *ws, size_t ws_bytes);
 
 /* ---- Softmax prediction layer (Sec. 3 "Prediction": Softmax; Sec. 5.1) ------
  * An input is labelled with the neutral label (0.1 in every label feature) and

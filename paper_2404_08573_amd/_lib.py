@@ -21,11 +21,13 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libff.so")
 FF_OK, FF_ERR_INVALID_ARG, FF_ERR_UNSUPPORTED, FF_ERR_WORKSPACE, FF_ERR_HIP = 0, -1, -2, -3, -4
 FF_F32, FF_BF16 = 0, 1
 FF_SEQUENTIAL, FF_PIPELINED = 0, 1
+FF_SINGLE_LAYER, FF_ALL_LAYERS = 0, 1
 
 EXPORTS = ["ff_status_string", "ff_last_error", "ff_embed_labels", "ff_step_workspace_size",
            "ff_layer_forward", "ff_layer_step", "ff_refresh_bf16_shadow",
            "ff_score_workspace_size", "ff_score_labels", "ff_adaptive_negatives",
            "ff_head_workspace_size", "ff_head_step", "ff_head_predict",
+           "ff_chapter_workspace_size", "ff_chapter_train",
            "ff_po_step_workspace_size", "ff_po_layer_step", "ff_po_epoch_workspace_size",
            "ff_po_epoch", "ff_po_predict_workspace_size", "ff_po_predict",
            "ff_pipeline_workspace_size",
@@ -93,6 +95,11 @@ def _load() -> ctypes.CDLL:
                                    c_size_t, P]),
         "ff_head_predict": (c_int32, [POINTER(ff_layer), c_int32, c_int32, POINTER(ff_hparams),
                                       POINTER(ff_head), P, c_int32, P, P, P, c_size_t, P]),
+        "ff_chapter_workspace_size": (c_size_t, [POINTER(ff_layer), c_int32, c_int32, c_int32,
+                                                 c_int32, c_int32]),
+        "ff_chapter_train": (c_int32, [POINTER(ff_layer), c_int32, POINTER(ff_hparams), P, P, P,
+                                       c_int32, c_int32, c_int32, c_int32, c_int32, c_int32,
+                                       c_int32, c_int32, POINTER(c_void_p), P, P, c_size_t]),
         "ff_po_step_workspace_size": (c_size_t, [c_int32] * 5),
         "ff_po_layer_step": (c_int32, [POINTER(ff_layer), POINTER(ff_head), POINTER(ff_hparams),
                                        POINTER(ff_hparams), P, P, c_int32, c_int32, P, P, P,
@@ -362,6 +369,45 @@ def ff_head_predict(layers: Sequence[Layer], hp: HParams, head: Head, x_base: to
                                _ptr(pred, torch.int32, n, "pred"), _ptr(ws, torch.uint8),
                                ws.numel(), _stream(stream)))
     return logits, pred
+
+
+def ff_chapter_train(layers: List[Layer], hp: HParams, x_base: torch.Tensor, y_pos: torch.Tensor,
+                     y_neg_chapters: torch.Tensor, n_classes: int, chunk_pairs: int, epochs: int,
+                     splits: int, cooldown_start: int, assignment: int = FF_SINGLE_LAYER,
+                     streams: Optional[Sequence] = None, n_streams: Optional[int] = None,
+                     loss_trace: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None):
+    """Chapter-granularity training (Alg. 1 / Alg. 2); y_neg_chapters [splits][n].  With
+    streams=None, worker streams are created (one per layer for FF_SINGLE_LAYER, n_streams
+    for FF_ALL_LAYERS) and joined back into the current stream before returning."""
+    n = x_base.shape[0]
+    dev = x_base.device
+    nc = (n + chunk_pairs - 1) // chunk_pairs
+    ns = len(layers) if assignment == FF_SINGLE_LAYER else (n_streams or len(layers))
+    own = streams is None
+    cur = torch.cuda.current_stream(dev)
+    if own:
+        streams = [torch.cuda.Stream(dev) for _ in range(ns)]
+        for s in streams:
+            s.wait_stream(cur)
+    if ws is None:
+        ws = workspace(LIB.ff_chapter_workspace_size(_layers_c(layers), len(layers), n,
+                                                     chunk_pairs, len(streams), hp.dtype), dev)
+    sarr = (c_void_p * len(streams))(*[_stream(s) for s in streams])
+    arr = _layers_c(layers)
+    st = LIB.ff_chapter_train(arr, len(layers), ctypes.byref(hp.c()),
+                              _ptr(x_base, torch.float32, n * layers[0].d_in, "x_base"),
+                              _ptr(y_pos, torch.int32, n, "y_pos"),
+                              _ptr(y_neg_chapters, torch.int32, splits * n, "y_neg_chapters"), n,
+                              n_classes, chunk_pairs, epochs, splits, cooldown_start, assignment,
+                              len(streams), sarr,
+                              _ptr(loss_trace, torch.float32, len(layers) * epochs * nc,
+                                   "loss_trace"), _ptr(ws, torch.uint8), ws.numel())
+    for L, Lc in zip(layers, arr):
+        L.step = Lc.step
+    if own:
+        for s in streams:
+            cur.wait_stream(s)
+    _check(st)
 
 
 def _heads_c(heads: Sequence[Head]):

@@ -1072,6 +1072,189 @@ ff_status ff_pipeline_epoch(ff_layer *layers, int32_t n_layers, const ff_hparams
   return epoch_core(layers, n_layers, hp, n, chunk_pairs, epochs, schedule, streams, loss_trace,
                     p, 2, input0, step);
 }
+// ---------------------------------------------------------------------------
+// Chapter schedules (Single-Layer / All-Layers PFF)
+// ---------------------------------------------------------------------------
+namespace {
+constexpr int kPubSlots = 2;  // published weight versions in flight per layer
+
+struct ChapterScratch {
+  std::vector<StepScratch> step;           // per stream
+  std::vector<float *> act[2], act_s[2];   // per stream: whole-set activities, ping-pong
+  std::vector<float *> pub_w, pub_b;       // [l * kPubSlots + slot]
+  std::vector<uint16_t *> pub_wb;          // bf16 shadows of the published weights
+};
+
+void carve_chapter(Carver &cv, ChapterScratch &c, const ff_layer *layers, int L, int n,
+                   int chunk, int n_streams, int dtype) {
+  const int rows = 2 * std::min(chunk, n);
+  int max_in = 0, max_out = 0, max_hidden = 0;
+  for (int l = 0; l < L; ++l) {
+    max_in = std::max(max_in, layers[l].d_in);
+    max_out = std::max(max_out, layers[l].d_out);
+    if (l + 1 < L) max_hidden = std::max(max_hidden, layers[l].d_out);
+  }
+  c.step.assign(n_streams, StepScratch());
+  for (int k = 0; k < 2; ++k) {
+    c.act[k].assign(n_streams, nullptr);
+    c.act_s[k].assign(n_streams, nullptr);
+  }
+  for (int s = 0; s < n_streams; ++s) {
+    carve_step(cv, c.step[s], rows, max_in, max_out, dtype, true, false, false);
+    if (L > 1)
+      for (int k = 0; k < 2; ++k) {
+        c.act[k][s] = static_cast<float *>(cv.take((size_t)2 * n * max_hidden * 4));
+        if (dtype == FF_F32) c.act_s[k][s] = static_cast<float *>(cv.take((size_t)2 * n * 4));
+      }
+  }
+  c.pub_w.assign((size_t)L * kPubSlots, nullptr);
+  c.pub_b.assign((size_t)L * kPubSlots, nullptr);
+  c.pub_wb.assign((size_t)L * kPubSlots, nullptr);
+  for (int l = 0; l + 1 < L; ++l)  // the last layer's versions are never read
+    for (int k = 0; k < kPubSlots; ++k) {
+      const size_t i = (size_t)l * kPubSlots + k;
+      c.pub_w[i] = static_cast<float *>(cv.take((size_t)layers[l].d_out * layers[l].d_in * 4));
+      c.pub_b[i] = static_cast<float *>(cv.take((size_t)layers[l].d_out * 4));
+      if (dtype == FF_BF16)
+        c.pub_wb[i] = static_cast<uint16_t *>(
+            cv.take((size_t)layers[l].d_out * layers[l].d_in * 2));
+    }
+}
+
+float cooldown(float lr0, int epoch, int epochs, int start) {
+  if (epoch < start || start >= epochs) return lr0;
+  return (float)((double)lr0 * (epochs - epoch) / (epochs - start));
+}
+}  // namespace
+
+size_t ff_chapter_workspace_size(const ff_layer *layers, int32_t n_layers, int32_t n,
+                                 int32_t chunk_pairs, int32_t n_streams, int32_t dtype) {
+  if (!layers || n_layers <= 0 || n <= 0 || chunk_pairs <= 0 || n_streams <= 0) return 0;
+  Carver cv(nullptr);
+  ChapterScratch c;
+  carve_chapter(cv, c, layers, n_layers, n, chunk_pairs, n_streams, dtype);
+  return cv.off + kAlign;
+}
+
+ff_status ff_chapter_train(ff_layer *layers, int32_t n_layers, const ff_hparams *hp,
+                           const float *x_base, const int32_t *y_pos,
+                           const int32_t *y_neg_chapters, int32_t n, int32_t n_classes,
+                           int32_t chunk_pairs, int32_t epochs, int32_t splits,
+                           int32_t cooldown_start, int32_t assignment, int32_t n_streams,
+                           void *const *streams, float *loss_trace, void *ws, size_t ws_bytes) {
+  FF_TRY(check_hp(hp));
+  FF_TRY(check_stack(layers, n_layers, hp, true));
+  if (n <= 0 || chunk_pairs <= 0 || splits <= 0 || epochs <= 0 || epochs % splits)
+    return fail(FF_ERR_INVALID_ARG, "n=%d chunk_pairs=%d epochs=%d splits=%d (epochs must be a "
+                "multiple of splits)", n, chunk_pairs, epochs, splits);
+  if (n_classes <= 0 || n_classes > layers[0].d_in)
+    return fail(FF_ERR_INVALID_ARG, "n_classes=%d", n_classes);
+  if (assignment != FF_SINGLE_LAYER && assignment != FF_ALL_LAYERS)
+    return fail(FF_ERR_INVALID_ARG, "assignment=%d", assignment);
+  if (assignment == FF_SINGLE_LAYER && n_streams != n_layers)
+    return fail(FF_ERR_INVALID_ARG, "FF_SINGLE_LAYER needs one stream per layer (%d, not %d)",
+                n_layers, n_streams);
+  if (n_streams <= 0) return fail(FF_ERR_INVALID_ARG, "n_streams=%d", n_streams);
+  if ((int64_t)2 * n > INT32_MAX) return fail(FF_ERR_UNSUPPORTED, "n too large");
+  if (!x_base || !y_pos || !y_neg_chapters || !streams)
+    return fail(FF_ERR_INVALID_ARG, "NULL pointer argument");
+  Carver size_cv(nullptr);
+  ChapterScratch tmp;
+  carve_chapter(size_cv, tmp, layers, n_layers, n, chunk_pairs, n_streams, hp->dtype);
+  FF_TRY(check_ws(ws, ws_bytes, size_cv.off + kAlign));
+  Carver cv(ws);
+  ChapterScratch cs;
+  carve_chapter(cv, cs, layers, n_layers, n, chunk_pairs, n_streams, hp->dtype);
+
+  const int L = n_layers, S = splits, per = epochs / splits;
+  const int nc = (n + chunk_pairs - 1) / chunk_pairs;
+  const bool bf16 = hp->dtype == FF_BF16;
+  // pub[l][slot]: layer l's version of a chapter is published (its training
+  // done); fwd[l][slot]: layer l's input pass of a chapter is done (its reads
+  // of the published versions of the layers below are over).
+  EventRing pub, fwd;
+  pub.ev.assign((size_t)L * kPubSlots, nullptr);
+  fwd.ev.assign((size_t)L * kPubSlots, nullptr);
+  for (auto &e : pub.ev) FF_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  for (auto &e : fwd.ev) FF_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  auto ev = [&](EventRing &r, int l, int c) { return r.ev[(size_t)l * kPubSlots + c % kPubSlots]; };
+  auto pairs = [&](int c, int start, int b) {
+    ffk::RowMap m{};
+    m.base = x_base;
+    m.lab_a = y_pos;
+    m.lab_b = y_neg_chapters + (size_t)c * n;
+    m.mode = ffk::PAIRS;
+    m.n_pos = b;
+    m.base_off = start;
+    m.n_classes = n_classes;
+    LayerInput in;
+    in.src = m;
+    return in;
+  };
+
+  for (int c = 0; c < S; ++c)
+    for (int l = 0; l < L; ++l) {
+      const int si = assignment == FF_SINGLE_LAYER ? l : c % n_streams;
+      hipStream_t st = static_cast<hipStream_t>(streams[si]);
+      StepScratch &sc = cs.step[si];
+      if (l > 0) FF_HIP(hipStreamWaitEvent(st, ev(pub, l - 1, c), 0));
+      if (c > 0 && assignment == FF_ALL_LAYERS)  // the layer's chapter c-1 ran elsewhere
+        FF_HIP(hipStreamWaitEvent(st, ev(pub, l, c - 1), 0));
+      if (c >= kPubSlots && L > 1)  // the version slot of chapter c-2 has no reader left
+        FF_HIP(hipStreamWaitEvent(st, ev(fwd, L - 1, c - kPubSlots), 0));
+      // input pass: the chapter's pairs through the published layers 0..l-1
+      for (int k = 0; k < l; ++k) {
+        ff_layer P = layers[k];
+        const size_t slot = (size_t)k * kPubSlots + c % kPubSlots;
+        P.W = cs.pub_w[slot];
+        P.b = cs.pub_b[slot];
+        P.W_bf16 = cs.pub_wb[slot];
+        float *out = cs.act[k & 1][si];
+        float *out_s = cs.act_s[k & 1][si];
+        for (int q = 0; q < nc; ++q) {
+          const int start = q * chunk_pairs, b = std::min(chunk_pairs, n - start);
+          const LayerInput in =
+              k == 0 ? pairs(c, start, b)
+                     : raw_rows(cs.act[(k - 1) & 1][si] + (size_t)2 * start * P.d_in,
+                                bf16 ? nullptr : cs.act_s[(k - 1) & 1][si] + (size_t)2 * start);
+          FF_TRY(forward_core(&P, hp, in, 2 * b, out + (size_t)2 * start * P.d_out, nullptr,
+                              bf16 ? nullptr : out_s + (size_t)2 * start, sc, st));
+        }
+      }
+      FF_HIP(hipEventRecord(ev(fwd, l, c), st));
+      // E/S epochs of layer l over the chunks, with the cooled-down rate
+      ff_layer *Ly = &layers[l];
+      for (int m = 0; m < per; ++m) {
+        const int e = c * per + m;
+        ff_hparams hpe = *hp;
+        hpe.lr = cooldown(hp->lr, e, epochs, cooldown_start);
+        for (int q = 0; q < nc; ++q) {
+          const int start = q * chunk_pairs, b = std::min(chunk_pairs, n - start);
+          const LayerInput in =
+              l == 0 ? pairs(c, start, b)
+                     : raw_rows(cs.act[(l - 1) & 1][si] + (size_t)2 * start * Ly->d_in,
+                                bf16 ? nullptr : cs.act_s[(l - 1) & 1][si] + (size_t)2 * start);
+          float *lt = loss_trace ? loss_trace + (size_t)l * epochs * nc + (size_t)e * nc + q
+                                 : nullptr;
+          FF_TRY(step_core(Ly, &hpe, in, b, b, nullptr, nullptr, lt, nullptr, sc, st));
+        }
+      }
+      // publish this chapter's version (read by the layers above)
+      if (l + 1 < L) {
+        const size_t slot = (size_t)l * kPubSlots + c % kPubSlots;
+        const size_t wbytes = (size_t)Ly->d_out * Ly->d_in;
+        FF_HIP(hipMemcpyAsync(cs.pub_w[slot], Ly->W, wbytes * 4, hipMemcpyDeviceToDevice, st));
+        FF_HIP(hipMemcpyAsync(cs.pub_b[slot], Ly->b, (size_t)Ly->d_out * 4,
+                              hipMemcpyDeviceToDevice, st));
+        if (bf16)
+          FF_HIP(hipMemcpyAsync(cs.pub_wb[slot], Ly->W_bf16, wbytes * 2, hipMemcpyDeviceToDevice,
+                                st));
+      }
+      FF_HIP(hipEventRecord(ev(pub, l, c), st));
+    }
+  return FF_OK;
+}
+
 
 // ---------------------------------------------------------------------------
 // Performance-optimised PFF

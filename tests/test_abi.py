@@ -187,6 +187,24 @@ def test_head_rejects_on_host(P):
     assert P.LIB.ff_head_workspace_size(layers, 3, 1, 5, 10, 0) > 5 * (12 + 8 + 8) * 4
 
 
+def test_chapter_rejects_on_host(P):
+    layers = (P._lib.ff_layer * 2)(_layer(P, 16, 8), _layer(P, 8, 8))
+    hp = _hp(P)
+    streams = (ctypes.c_void_p * 2)(None, None)
+
+    def call(epochs=4, splits=2, assignment=0, n_streams=2, ws_bytes=1 << 30):
+        return P.LIB.ff_chapter_train(layers, 2, ctypes.byref(hp), ctypes.c_void_p(4096),
+                                      ctypes.c_void_p(4096), ctypes.c_void_p(4096), 100, 10, 32,
+                                      epochs, splits, 2, assignment, n_streams, streams, None,
+                                      ctypes.c_void_p(1 << 20), ws_bytes)
+
+    assert call(epochs=5) == -1  # not a multiple of splits
+    assert call(assignment=2) == -1
+    assert call(n_streams=1) == -1  # Single-Layer needs one stream per layer
+    assert call(ws_bytes=10) == -3
+    assert layers[0].step == 0 and layers[1].step == 0
+
+
 def test_pipeline_rejects_on_host(P):
     layers = (P._lib.ff_layer * 2)(_layer(P, 16, 8), _layer(P, 8, 8))
     hp = _hp(P)

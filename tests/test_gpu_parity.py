@@ -7,7 +7,7 @@ torch = pytest.importorskip("torch")
 import oracle as O  # noqa: E402
 from ffinputs import WORKLOADS, make_data, make_weights, random_labels, random_matrix  # noqa: E402
 from parity import (assert_acts, assert_goodness, assert_labels, assert_loss,  # noqa: E402
-                    assert_negatives, assert_weights, grad_magnitudes)
+                    assert_negatives, assert_rel_fro, assert_weights, grad_magnitudes)
 
 pytestmark = pytest.mark.gpu
 
@@ -695,3 +695,54 @@ def test_po_predict_parity(P, all_layers):
                                 O.HParams(), all_layers)
     assert_acts(_np(logits), z_ref)
     assert_labels(_np(pred), z_ref, p_ref)
+
+
+# ------------------------------------------------------------------ chapter schedules (Alg. 1 / 2)
+def _chapter(P, assignment, n_streams, dims=(64, 96, 80, 48), n=300, chunk=64, E=4, S=2, cool=2,
+             bf16=False, seed=130):
+    x_base, y, _ = make_data(seed, n, dims[0])
+    negs = np.stack([random_labels(seed + 1 + c, n)[1] for c in range(S)]).astype(np.int32)
+    params = make_weights(seed + 9, dims)
+    layers = [P.Layer(_t(W), _t(b), bf16_shadow=bf16) for W, b in params]
+    nc = -(-n // chunk)
+    trace = torch.zeros(len(layers), E * nc, device=DEV)
+    hp = P.HParams(lr=0.03, dtype=P.FF_BF16 if bf16 else P.FF_F32)
+    P.ff_chapter_train(layers, hp, _t(x_base), _t(y), _t(negs), 10, chunk, E, S, cool, assignment,
+                       n_streams=n_streams, loss_trace=trace)
+    torch.cuda.synchronize()
+    return layers, _np(trace), (x_base, y, negs, params, chunk, E, S, cool)
+
+
+@pytest.mark.parametrize("assignment,n_streams", [(0, None), (1, 2)])
+def test_chapter_parity(P, assignment, n_streams):
+    layers, trace, (x_base, y, negs, params, chunk, E, S, cool) = _chapter(P, assignment,
+                                                                            n_streams)
+    ref = [O.Layer.from_params(W, b) for W, b in params]
+    t_ref = O.chapter_train(ref, x_base, y, list(negs), 10, chunk, E, S, cool, O.HParams(lr=0.03))
+    np.testing.assert_allclose(trace, t_ref, rtol=2e-4)
+    for L, R in zip(layers, ref):
+        assert L.step == R.t
+        np.testing.assert_allclose(_np(L.W), R.W, rtol=1e-3, atol=2e-4)
+
+
+def test_chapter_assignments_agree_bitwise(P):
+    """Single-Layer (one stream per layer) and All-Layers (chapters dealt to 1
+    or 3 streams) run the same (layer, chapter) graph: identical results."""
+    a, ta, _ = _chapter(P, 0, None, E=6, S=3, cool=3)
+    b, tb, _ = _chapter(P, 1, 3, E=6, S=3, cool=3)
+    c, tc, _ = _chapter(P, 1, 1, E=6, S=3, cool=3)
+    np.testing.assert_array_equal(ta, tb)
+    np.testing.assert_array_equal(ta, tc)
+    for x, y_, z in zip(a, b, c):
+        np.testing.assert_array_equal(_np(x.W), _np(y_.W))
+        np.testing.assert_array_equal(_np(x.W), _np(z.W))
+
+
+def test_chapter_parity_bf16(P):
+    layers, trace, (x_base, y, negs, params, chunk, E, S, cool) = _chapter(P, 0, None, bf16=True)
+    ref = [O.Layer.from_params(W, b) for W, b in params]
+    t_ref = O.chapter_train(ref, x_base, y, list(negs), 10, chunk, E, S, cool,
+                            O.HParams(lr=0.03, bf16=True))
+    np.testing.assert_allclose(trace, t_ref, rtol=2e-3)
+    for L, R in zip(layers, ref):
+        assert_rel_fro(_np(L.W), R.W, 1e-2)
