@@ -57,8 +57,14 @@ typedef enum { FF_SEQUENTIAL = 0, FF_PIPELINED = 1 } ff_schedule;
  * c mod n_streams (All-Layers PFF, Alg. 2). */
 typedef enum { FF_SINGLE_LAYER = 0, FF_ALL_LAYERS = 1 } ff_assignment;
 
+/* Largest layer width (d_in, d_out) the kernels take: a 256-row operand tile
+ * of that width stays within a 32-bit buffer range.  Wider layers are
+ * rejected with FF_ERR_UNSUPPORTED. */
+#define FF_MAX_WIDTH (1 << 20)
+
 /* One dense ReLU FF layer, h = max(x_hat W^T + b, 0) (Sec. 3, Sec. 5.1).
- * All buffers are caller-owned device memory. */
+ * d_in and d_out are multiples of 4 (of 8 for d_in in FF_BF16 mode), at most
+ * FF_MAX_WIDTH.  All buffers are caller-owned device memory. */
 typedef struct {
   int32_t d_in, d_out;
   float *W;          /* (device) [d_out][d_in] fp32 master weights           */

@@ -15,6 +15,8 @@
 #include "../../include/ff.h"
 #include "ff_internal.h"
 
+static_assert(FF_MAX_WIDTH == ffk::kMaxWidth, "one width limit");
+
 namespace {
 
 thread_local char g_msg[512] = "";
@@ -159,6 +161,9 @@ ff_status check_layer(const ff_layer *L, const ff_hparams *hp, bool for_update, 
   if (L->d_in % 4 || L->d_out % 4)
     return fail(FF_ERR_UNSUPPORTED, "layer %d: d_in=%d d_out=%d must be multiples of 4", idx,
                 L->d_in, L->d_out);
+  if (L->d_in > FF_MAX_WIDTH || L->d_out > FF_MAX_WIDTH)
+    return fail(FF_ERR_UNSUPPORTED, "layer %d: d_in=%d d_out=%d exceed %d", idx, L->d_in,
+                L->d_out, FF_MAX_WIDTH);
   if (!L->W || !L->b) return fail(FF_ERR_INVALID_ARG, "layer %d: W or b is NULL", idx);
   if (for_update && (!L->mW || !L->vW || !L->mb || !L->vb))
     return fail(FF_ERR_INVALID_ARG, "layer %d: Adam moment buffer is NULL", idx);

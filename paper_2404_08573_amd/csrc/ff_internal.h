@@ -8,6 +8,10 @@
 
 namespace ffk {
 
+// Largest operand row length (layer width) of the forward product: a 256-row
+// tile of it spans under 2^31 bytes, the range of one buffer descriptor.
+constexpr int kMaxWidth = 1 << 20;
+
 // Where row r of a layer-0 input comes from.
 //   ROWS:     row r of `base` (already embedded or a hidden activity).
 //   PAIRS:    rows [0, n_pos) are base rows base_off+r with label lab_a[base_off+r];

@@ -291,13 +291,11 @@ __device__ __forceinline__ void kloop(int nk, Load &gload, Store &sstore, Comput
 // X [M][K], W [N][K] (both K-contiguous), fp32 or bf16 operands, fp32
 // accumulation.  Tile BM x BN, WM x WN waves, each (BM/WM) x (BN/WN) as 32x32
 // MFMA blocks: v_mfma_f32_32x32x2f32 (one fp32 per lane per instruction) or
-// v_mfma_f32_32x32x16_bf16 (eight bf16 per lane).  Within a BK slab the two
-// half-waves take the two halves of the slab's k range, so every lane reads
+// v_mfma_f32_32x32x16_bf16 (eight bf16 per lane).  Within a k-tile the two
+// half-waves take the two halves of its k range, so every lane reads
 // contiguous 16-byte runs from LDS for both operands (the k order inside the
 // contraction is a permutation of the plain order, the same for X and W).
-// Loads are branch-free: out-of-range rows read a clamped valid row whose
-// results are never stored; the k tail is zeroed when written to LDS.  BK is
-// in elements; K must be a multiple of the 16-byte vector (4 fp32 / 8 bf16).
+// K must be a multiple of the 16-byte vector (4 fp32 / 8 bf16).
 // ---------------------------------------------------------------------------
 template <bool BF16>
 struct Operand;
@@ -312,17 +310,57 @@ struct Operand<true> {
   static constexpr int kVec = 8;
 };
 
-// LDS elements of the NT main loop's double-buffered tiles.
-template <bool BF16, int BM, int BN, int BK>
+// A k-tile of the NT main loop is 128 bytes of every operand row.
+template <bool BF16>
+constexpr int nt_bk() {
+  return 128 / (int)sizeof(typename Operand<BF16>::T);
+}
+// LDS elements of the NT main loop's NBUF-stage tiles.
+template <bool BF16, int BM, int BN, int NBUF>
 constexpr int nt_lds_elems() {
-  return 2 * (BM + BN) * (BK + Operand<BF16>::kVec);
+  return NBUF * (BM + BN) * nt_bk<BF16>();
 }
 
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Raw buffer descriptor over `bytes` bytes from `base`: loads at offsets at or
+// past `bytes` return zeros instead of touching memory.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
+constexpr uint32_t kOutOfRange = 0x80000000u;  // a buffer offset past every tile's range
+
+// LDS position of 16-byte chunk c of tile row r in its unpadded 128-byte row.
+// The MFMA fragment reads take one chunk on 16 consecutive rows per group of
+// 16 lanes; this XOR puts them on 16 distinct 16-byte positions modulo 256
+// bytes (two rows share a 256-byte line of the 64 banks, so rows r and r + 8
+// are told apart by bit 3 of r) and on 8 distinct positions within every 8
+// rows.  An involution for each r.
+__device__ __forceinline__ int nt_swz(int r, int c) { return c ^ (r & 7) ^ ((r >> 3) & 1); }
+
+// s_waitcnt operand: at most n vector-memory operations outstanding, no limit
+// on the other counters (gfx9 encoding: vmcnt in bits 3:0 and 15:14).
+constexpr int vmcnt_wait(int n) { return 0x0f70 | (n & 15) | ((n >> 4) << 14); }
+
 // Main loop of C[m][n] = sum_k X[m][k] W[n][k] for the tile at (m0, n0), both
-// operands K-contiguous, into the wave's accumulators.  Shared by the forward
-// product and the bf16 weight-gradient product (whose operands are stored
-// transposed, k-contiguous, for it).
-template <bool BF16, int BM, int BN, int BK, int WM, int WN, int PF>
+// operands K-contiguous, into the wave's accumulators.
+//
+// Operands move from global memory straight into LDS (buffer_load ... lds,
+// 16 bytes per lane): one wave instruction fills 8 unpadded 128-byte tile
+// rows, lane l writing LDS position l % 8 of row l / 8 and fetching the chunk
+// that nt_swz maps to that position.  The buffer descriptors span the tile's
+// valid rows, so rows past M or N and chunks past K (the k tail, given an
+// out-of-range offset) arrive as zeros.  NBUF LDS stages: the loads of tile
+// t + NBUF - 1 are issued right after the barrier that opens tile t (which
+// ends every wave's reads of tile t - 1, whose buffer they refill), and tile
+// t's own loads are waited for by counter before that barrier, so NBUF - 2
+// tiles of loads stay in flight across the MFMAs.  Loads past the last tile
+// are issued all the same (they read zeros), keeping the counter arithmetic
+// exact.  On return every load has landed and every wave has passed a
+// barrier, so the LDS may be reused.  The descriptors' 32-bit range needs
+// min(BM, M - m0) * K and min(BN, N - n0) * K under 2^31 bytes.
+template <bool BF16, int BM, int BN, int WM, int WN, int NBUF>
 __device__ __forceinline__ void nt_mainloop(const typename Operand<BF16>::T *__restrict__ X,
                                             const typename Operand<BF16>::T *__restrict__ W,
                                             int M, int N, int K, int m0, int n0,
@@ -330,54 +368,54 @@ __device__ __forceinline__ void nt_mainloop(const typename Operand<BF16>::T *__r
                                             floatx16 (&acc)[BM / WM / 32][BN / WN / 32]) {
   using T = typename Operand<BF16>::T;
   constexpr int VE = Operand<BF16>::kVec;
-  constexpr int NT = WM * WN * 64;
+  constexpr int ES = sizeof(T);
+  constexpr int BK = nt_bk<BF16>();
+  constexpr int NW = WM * WN;
   constexpr int TM = BM / WM, TN = BN / WN, MB = TM / 32, NB = TN / 32;
-  constexpr int LDK = BK + VE;  // rows padded by 16 bytes: conflict-free 16-byte reads
-  constexpr int KCH = BK / VE;  // 16-byte chunks per tile row
-  constexpr int LDA = BM * KCH / NT, LDB = BN * KCH / NT;  // chunk loads per thread
-  constexpr int RSTEP = NT / KCH;                          // tile rows between them
+  constexpr int IA = BM / 8 / NW, IB = BN / 8 / NW;  // 8-row wave loads per k-tile
+  constexpr int STAGE = (BM + BN) * BK;               // elements per LDS stage
   static_assert(MB * 32 == TM && NB * 32 == TN, "wave tile is whole 32x32 blocks");
-  static_assert(LDA * NT == BM * KCH && LDB * NT == BN * KCH, "tile/threads");
-  static_assert((BK / 2) % VE == 0, "half slab is whole vectors");
-  T *As = sm;                 // [2][BM][LDK]
-  T *Bs = sm + 2 * BM * LDK;  // [2][BN][LDK]
+  static_assert(IA * 8 * NW == BM && IB * 8 * NW == BN, "tile rows split into 8-row wave loads");
+  static_assert(NBUF >= 2 && (NBUF - 2) * (IA + IB) < 64, "stages");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int li = lane & 31, kg = lane >> 5;
 
-  const int srow = tid / KCH, kc = (tid % KCH) * VE;
-  const T *pa[LDA];
-  const T *pb[LDB];
+  const __amdgpu_buffer_rsrc_t ra =
+      buffer_rsrc(X + (size_t)m0 * K, (uint32_t)(min(BM, M - m0) * K * ES));
+  const __amdgpu_buffer_rsrc_t rb =
+      buffer_rsrc(W + (size_t)n0 * K, (uint32_t)(min(BN, N - n0) * K * ES));
+  const int lpos = lane & 7;
+  int kca[IA], kcb[IB];   // element offset of the lane's chunk within a k-tile
+  uint32_t oa[IA], ob[IB];  // byte offset of that chunk in k-tile 0
 #pragma unroll
-  for (int i = 0; i < LDA; ++i) pa[i] = X + (size_t)min(m0 + srow + i * RSTEP, M - 1) * K + kc;
+  for (int i = 0; i < IA; ++i) {
+    const int r = (wave * IA + i) * 8 + (lane >> 3);
+    kca[i] = nt_swz(r, lpos) * VE;
+    oa[i] = (uint32_t)((r * K + kca[i]) * ES);
+  }
 #pragma unroll
-  for (int i = 0; i < LDB; ++i) pb[i] = W + (size_t)min(n0 + srow + i * RSTEP, N - 1) * K + kc;
-
-  // Loaded values are consumed only when written to LDS, after the MFMAs of
-  // the current tile (the k-tail mask is applied there, never right after
-  // the load, which would make the wave wait for it).
-  struct Stage {
-    uint4 a[LDA], b[LDB];
-    int kt;
-  } st[PF];
-  auto gload = [&](Stage &g, int kt) {
+  for (int i = 0; i < IB; ++i) {
+    const int r = (wave * IB + i) * 8 + (lane >> 3);
+    kcb[i] = nt_swz(r, lpos) * VE;
+    ob[i] = (uint32_t)((r * K + kcb[i]) * ES);
+  }
+  auto issue = [&](int kt, int buf) {
+    T *As = sm + buf * STAGE;
+    T *Bs = As + BM * BK;
     const int kb = kt * BK;
-    const int ko = kb + kc < K ? kb : K - VE - kc;  // clamped to a valid address when past K
 #pragma unroll
-    for (int i = 0; i < LDA; ++i) g.a[i] = ld16(pa[i] + ko);
+    for (int i = 0; i < IA; ++i) {
+      const uint32_t o = kb + kca[i] < K ? oa[i] + kb * ES : kOutOfRange;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void *)(As + (wave * IA + i) * 8 * BK), 16,
+                                               o, 0, 0, 0);
+    }
 #pragma unroll
-    for (int i = 0; i < LDB; ++i) g.b[i] = ld16(pb[i] + ko);
-    g.kt = kt;
-  };
-  auto sstore = [&](const Stage &g, int buf) {
-    const bool kok = g.kt * BK + kc < K;
-    const uint4 z = make_uint4(0u, 0u, 0u, 0u);
-#pragma unroll
-    for (int i = 0; i < LDA; ++i)
-      st16(As + (buf * BM + srow + i * RSTEP) * LDK + kc, kok ? g.a[i] : z);
-#pragma unroll
-    for (int i = 0; i < LDB; ++i)
-      st16(Bs + (buf * BN + srow + i * RSTEP) * LDK + kc, kok ? g.b[i] : z);
+    for (int i = 0; i < IB; ++i) {
+      const uint32_t o = kb + kcb[i] < K ? ob[i] + kb * ES : kOutOfRange;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void *)(Bs + (wave * IB + i) * 8 * BK), 16,
+                                               o, 0, 0, 0);
+    }
   };
 
 #pragma unroll
@@ -388,15 +426,22 @@ __device__ __forceinline__ void nt_mainloop(const typename Operand<BF16>::T *__r
       for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.f;
 
   auto compute = [&](int buf) {
-    const T *a0 = As + (buf * BM + wm * TM + li) * LDK + kg * (BK / 2);
-    const T *b0 = Bs + (buf * BN + wn * TN + li) * LDK + kg * (BK / 2);
+    const T *As = sm + buf * STAGE;
+    const T *Bs = As + BM * BK;
 #pragma unroll
     for (int sv = 0; sv < BK / 2; sv += VE) {
+      const int c = (kg * (BK / 2) + sv) / VE;
       uint4 a[MB], b[NB];
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) a[mb] = ld16(a0 + mb * 32 * LDK + sv);
+      for (int mb = 0; mb < MB; ++mb) {
+        const int r = wm * TM + mb * 32 + li;
+        a[mb] = ld16(As + r * BK + nt_swz(r, c) * VE);
+      }
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) b[nb] = ld16(b0 + nb * 32 * LDK + sv);
+      for (int nb = 0; nb < NB; ++nb) {
+        const int r = wn * TN + nb * 32 + li;
+        b[nb] = ld16(Bs + r * BK + nt_swz(r, c) * VE);
+      }
       if constexpr (BF16) {
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
@@ -417,10 +462,20 @@ __device__ __forceinline__ void nt_mainloop(const typename Operand<BF16>::T *__r
     }
   };
 
-  kloop<PF>((K + BK - 1) / BK, gload, sstore, compute, st);
+  const int nk = (K + BK - 1) / BK;
+#pragma unroll
+  for (int j = 0; j < NBUF - 1; ++j) issue(j, j);
+  for (int kt = 0; kt < nk; ++kt) {
+    __builtin_amdgcn_s_waitcnt(vmcnt_wait((NBUF - 2) * (IA + IB)));
+    __builtin_amdgcn_s_barrier();
+    issue(kt + NBUF - 1, (kt + NBUF - 1) % NBUF);
+    compute(kt % NBUF);
+  }
+  __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
+  __builtin_amdgcn_s_barrier();
 }
 
-template <bool BF16, int BM, int BN, int BK, int WM, int WN, int PF, bool STORE_H>
+template <bool BF16, int BM, int BN, int WM, int WN, int NBUF, bool STORE_H>
 __global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16>::T *__restrict__ X,
                                                      const typename Operand<BF16>::T *__restrict__ W,
                                                      const float *__restrict__ bias,
@@ -430,7 +485,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16
   using T = typename Operand<BF16>::T;
   constexpr int NT = WM * WN * 64;
   constexpr int TM = BM / WM, TN = BN / WN, MB = TM / 32, NB = TN / 32;
-  __shared__ __attribute__((aligned(16))) T sm[nt_lds_elems<BF16, BM, BN, BK>()];
+  __shared__ __attribute__((aligned(16))) T sm[nt_lds_elems<BF16, BM, BN, NBUF>()];
   const int nt = (N + BN - 1) / BN;
   int tm, tn;
   tile_of(blockIdx.x, (M + BM - 1) / BM, nt, tm, tn);
@@ -440,7 +495,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16
   const int li = lane & 31, kg = lane >> 5;
 
   floatx16 acc[MB][NB];
-  nt_mainloop<BF16, BM, BN, BK, WM, WN, PF>(X, W, M, N, K, m0, n0, sm, acc);
+  nt_mainloop<BF16, BM, BN, WM, WN, NBUF>(X, W, M, N, K, m0, n0, sm, acc);
 
   // Epilogue: row scale (the input rows' normalisation, when the operand rows
   // are raw), bias, ReLU, H store, goodness partials.
@@ -502,7 +557,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16
 // (converted from bf16 bits in bf16 mode, where s is already bf16-rounded, so
 // s * W_label is exact in fp32).
 // ---------------------------------------------------------------------------
-template <bool BF16, int BM, int BN, int BK, int WM, int WN, int PF, bool STORE_H>
+template <bool BF16, int BM, int BN, int WM, int WN, int NBUF, bool STORE_H>
 __global__ __launch_bounds__(WM *WN * 64) void k_fwd_expand(
     const typename Operand<BF16>::T *__restrict__ X, const typename Operand<BF16>::T *__restrict__ W,
     const float *__restrict__ bias, LabelExpand ex, int M, int N, int K, float *__restrict__ H,
@@ -510,7 +565,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd_expand(
   using T = typename Operand<BF16>::T;
   constexpr int NT = WM * WN * 64;
   constexpr int TM = BM / WM, TN = BN / WN, MB = TM / 32, NB = TN / 32;
-  constexpr int kMain = nt_lds_elems<BF16, BM, BN, BK>() * (int)sizeof(T) / 4;  // in floats
+  constexpr int kMain = nt_lds_elems<BF16, BM, BN, NBUF>() * (int)sizeof(T) / 4;  // in floats
   constexpr int kEpi = kMaxExpand * (WN * BM + BN);
   __shared__ __attribute__((aligned(16))) float smf[kMain > kEpi ? kMain : kEpi];
   const int nt = (N + BN - 1) / BN;
@@ -523,8 +578,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd_expand(
   const int C = ex.n_classes;
 
   floatx16 acc[MB][NB];
-  nt_mainloop<BF16, BM, BN, BK, WM, WN, PF>(X, W, M, N, K, m0, n0, reinterpret_cast<T *>(smf),
-                                            acc);
+  nt_mainloop<BF16, BM, BN, WM, WN, NBUF>(X, W, M, N, K, m0, n0, reinterpret_cast<T *>(smf), acc);
 
   // LDS after the main loop: gs [C][WN][BM] goodness partials, wl [BN][kMaxExpand]
   // the tile's label columns of W.
@@ -652,7 +706,9 @@ __global__ __launch_bounds__(kLossRows) void k_loss_rows(const float *__restrict
 // Half-wave kg takes slab rows 2s+kg.  The loads are issued raw ahead of the
 // MFMAs; the row scale c, the k-tail mask and the db sums are applied when the
 // registers are written to LDS.  With BS the X rows are raw and bscale holds
-// their normalisation (x_hat_k = bscale[k] * X_k), applied there too.
+// their normalisation (x_hat_k = bscale[k] * X_k).  A per-row factor of the
+// contraction can sit on either operand, so it joins c on the c.H rows (after
+// the db sum, which wants c alone) and the X_hat tile is staged as loaded.
 // ---------------------------------------------------------------------------
 template <int BM, int BN, int BK, int WM, int WN, int PF, bool BS>
 __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
@@ -698,7 +754,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
 
   struct Stage {
     float4 a[LDA], b[LDB];
-    float c[LDA], s[BS ? LDB : 1];
+    float c[LDA], s[BS ? LDA : 1];
     int kt;
   } st[PF];
   float4 dbp = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -708,12 +764,12 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
       const int k = min(kt * BK + ka + i * KSA, K - 1);
       g.a[i] = ld4(pa + (size_t)k * M);
       g.c[i] = cvec[k];
+      if constexpr (BS) g.s[i] = bscale[k];
     }
 #pragma unroll
     for (int i = 0; i < LDB; ++i) {
       const int k = min(kt * BK + kb + i * KSB, K - 1);
       g.b[i] = ld4(pb + (size_t)k * N);
-      if constexpr (BS) g.s[i] = bscale[k];
     }
     g.kt = kt;
   };
@@ -732,19 +788,16 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
         dbp.z += v.z;
         dbp.w += v.w;
       }
-      st4(As + (buf * BK + ka + i * KSA) * LDM + ca, v);
-    }
-#pragma unroll
-    for (int i = 0; i < LDB; ++i) {
-      float4 v = g.b[i];
       if constexpr (BS) {
         v.x *= g.s[i];
         v.y *= g.s[i];
         v.z *= g.s[i];
         v.w *= g.s[i];
       }
-      st4(Bs + (buf * BK + kb + i * KSB) * LDN + cb, v);
+      st4(As + (buf * BK + ka + i * KSA) * LDM + ca, v);
     }
+#pragma unroll
+    for (int i = 0; i < LDB; ++i) st4(Bs + (buf * BK + kb + i * KSB) * LDN + cb, g.b[i]);
   };
 
   floatx16 acc[MB][NB];
@@ -1279,8 +1332,9 @@ inline unsigned cdiv(long a, long b) { return (unsigned)((a + b - 1) / b); }
 // Launchers
 // ---------------------------------------------------------------------------
 // GEMM tile configurations: (BM, BN, BK in elements, waves along M, waves
-// along N, register stages of the load pipeline), measured on MI355X over
-// the layer shapes of the workloads.  A weight-gradient launch takes the large
+// along N, stages: register stages of a weight-gradient load pipeline, LDS
+// stages of a forward one), measured on MI355X over the layer shapes of the
+// workloads.  A weight-gradient launch takes the large
 // tile when its tiles alone fill every CU, else the small one.
 template <int BM, int BN, int BK, int WM, int WN, int PF = 1>
 struct Tile {
@@ -1295,9 +1349,14 @@ using DwBigBf16 = Tile<128, 128, 32, 4, 2, 2>;
 using DwSmallBf16 = Tile<64, 64, 64, 2, 2, 2>;
 
 // Forward tile ladder: a launch takes the largest tile whose grid still puts a
-// workgroup on every CU.  bf16 products need the larger tiles for operand
-// reuse (a 128x128 bf16 tile asks about as many operand bytes per cycle as a
-// CU can load at full MFMA rate); fp32 measured no faster above 128x128.
+// workgroup on every CU.  The last parameter of a forward tile is its number
+// of LDS stages (BK is fixed at 128 bytes of a row): two let two 128x128
+// workgroups share a CU.  A bf16 k-tile holds a quarter of the MFMA time of
+// an fp32 one, too little to cover a load's latency with one tile in flight,
+// so a bf16 grid of fewer than two 128x128 workgroups per CU (Full) takes
+// three stages instead, as does the small tile.  bf16 products use the larger
+// tiles for operand reuse when the grid allows; fp32 measured no faster above
+// 128x128.
 template <bool BF16>
 struct FwdTiles;
 template <>
@@ -1305,14 +1364,16 @@ struct FwdTiles<false> {
   using Huge = Tile<128, 128, 32, 4, 2, 2>;
   using Large = Huge;
   using Big = Huge;
-  using Small = Tile<64, 64, 32, 2, 2, 2>;
+  using Full = Huge;
+  using Small = Tile<64, 64, 32, 2, 2, 3>;
 };
 template <>
 struct FwdTiles<true> {
   using Huge = Tile<256, 256, 64, 4, 2, 2>;
   using Large = Tile<256, 192, 64, 4, 2, 2>;
   using Big = Tile<128, 128, 64, 4, 2, 2>;
-  using Small = Tile<64, 64, 64, 2, 2, 2>;
+  using Full = Tile<128, 128, 64, 4, 2, 3>;
+  using Small = Tile<64, 64, 64, 2, 2, 3>;
 };
 template <class T>
 struct TileTag {
@@ -1327,7 +1388,8 @@ void fwd_tile(int M, int N, F &&f) {
     if (L::Huge::tiles(M, N) >= kCUs) return f(TileTag<typename L::Huge>{});
     if (L::Large::tiles(M, N) >= kCUs) return f(TileTag<typename L::Large>{});
   }
-  if (L::Big::tiles(M, N) >= kCUs) return f(TileTag<typename L::Big>{});
+  if (L::Big::tiles(M, N) >= 2 * kCUs) return f(TileTag<typename L::Big>{});
+  if (L::Full::tiles(M, N) >= kCUs) return f(TileTag<typename L::Full>{});
   f(TileTag<typename L::Small>{});
 }
 
@@ -1379,11 +1441,12 @@ void fwd_launch(const void *x, const void *w, const float *bias, const float *ro
   const dim3 grid(T::tiles(M, N));
   const E *xe = static_cast<const E *>(x);
   const E *we = static_cast<const E *>(w);
+  static_assert(T::bk == nt_bk<BF16>(), "forward k-tile is 128 bytes");
   if (H)
-    hipLaunchKernelGGL((k_fwd<BF16, T::bm, T::bn, T::bk, T::wm, T::wn, T::pf, true>), grid,
+    hipLaunchKernelGGL((k_fwd<BF16, T::bm, T::bn, T::wm, T::wn, T::pf, true>), grid,
                        dim3(T::threads), 0, s, xe, we, bias, rowscale, M, N, K, H, gpart);
   else
-    hipLaunchKernelGGL((k_fwd<BF16, T::bm, T::bn, T::bk, T::wm, T::wn, T::pf, false>), grid,
+    hipLaunchKernelGGL((k_fwd<BF16, T::bm, T::bn, T::wm, T::wn, T::pf, false>), grid,
                        dim3(T::threads), 0, s, xe, we, bias, rowscale, M, N, K, H, gpart);
 }
 
@@ -1391,6 +1454,7 @@ hipError_t launch_fwd(int dtype, const void *X, const void *W, const float *bias
                       const float *rowscale, int M, int N, int K, float *H, float *gpart,
                       hipStream_t s) {
   if (M <= 0) return hipSuccess;
+  if (K > kMaxWidth) return hipErrorInvalidValue;
   if (dtype == 0)
     fwd_tile<false>(M, N, [&](auto t) {
       fwd_launch<false, typename decltype(t)::type>(X, W, bias, rowscale, M, N, K, H, gpart, s);
@@ -1409,19 +1473,20 @@ void fwd_expand_launch(const void *x, const void *w, const float *bias, const La
   const dim3 grid(T::tiles(M, N));
   const E *xe = static_cast<const E *>(x);
   const E *we = static_cast<const E *>(w);
+  static_assert(T::bk == nt_bk<BF16>(), "forward k-tile is 128 bytes");
   if (H)
-    hipLaunchKernelGGL((k_fwd_expand<BF16, T::bm, T::bn, T::bk, T::wm, T::wn, T::pf, true>),
-                       grid, dim3(T::threads), 0, s, xe, we, bias, ex, M, N, K, H, gpart);
+    hipLaunchKernelGGL((k_fwd_expand<BF16, T::bm, T::bn, T::wm, T::wn, T::pf, true>), grid,
+                       dim3(T::threads), 0, s, xe, we, bias, ex, M, N, K, H, gpart);
   else
-    hipLaunchKernelGGL((k_fwd_expand<BF16, T::bm, T::bn, T::bk, T::wm, T::wn, T::pf, false>),
-                       grid, dim3(T::threads), 0, s, xe, we, bias, ex, M, N, K, H, gpart);
+    hipLaunchKernelGGL((k_fwd_expand<BF16, T::bm, T::bn, T::wm, T::wn, T::pf, false>), grid,
+                       dim3(T::threads), 0, s, xe, we, bias, ex, M, N, K, H, gpart);
 }
 
 hipError_t launch_fwd_expand(int dtype, const void *X, const void *W, const float *bias,
                              const LabelExpand &ex, int M, int N, int K, float *H, float *gpart,
                              hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  if (ex.n_classes < 1 || ex.n_classes > kMaxExpand || ex.n_classes > K)
+  if (ex.n_classes < 1 || ex.n_classes > kMaxExpand || ex.n_classes > K || K > kMaxWidth)
     return hipErrorInvalidValue;
   if (dtype == 0)
     fwd_tile<false, false>(M, N, [&](auto t) {

@@ -73,7 +73,7 @@ def _hp(P, **kw):
 @pytest.mark.parametrize("case,status", [
     ("n_pos0", -1), ("n_neg0", -1), ("x_null", -1), ("d_in_odd", -2), ("d_out0", -1),
     ("no_moments", -1), ("bad_dtype", -1), ("bf16_no_shadow", -1), ("ws_null", -3),
-    ("ws_small", -3), ("beta_out_of_range", -1)])
+    ("ws_small", -3), ("beta_out_of_range", -1), ("too_wide", -2)])
 def test_layer_step_rejects_on_host(P, case, status):
     L = _layer(P)
     hp = _hp(P)
@@ -101,6 +101,8 @@ def test_layer_step_rejects_on_host(P, case, status):
         ws_bytes = 100
     elif case == "beta_out_of_range":
         hp = _hp(P, beta2=1.0)
+    elif case == "too_wide":
+        L = _layer(P, d_in=(1 << 20) + 4)  # past FF_MAX_WIDTH
     st = P.LIB.ff_layer_step(ctypes.byref(L), ctypes.byref(hp), x, n_pos, n_neg, 0, None, None,
                              None, ws, ws_bytes, None)
     assert st == status, P.LIB.ff_last_error()
