@@ -7,7 +7,8 @@
 //   k_embed_norm   label embedding (Sec. 3 "Negative Data") + row L2 normalisation;
 //                  one wave per row, float4 loads, HBM-bound.
 //   k_fwd          Z = X W^T on MFMA (v_mfma_f32_32x32x2f32 for fp32 operands,
-//                  v_mfma_f32_32x32x16_bf16 for bf16), epilogue fuses bias, ReLU, the
+//                  v_mfma_f32_32x32x16_bf16 for bf16), operands loaded straight into
+//                  LDS (buffer_load ... lds); the epilogue fuses bias, ReLU, the
 //                  H store and the per-row goodness partial sum over the tile's
 //                  columns (Eq. 1) through a lane butterfly and LDS.
 //   k_loss_rows    goodness partials -> g, the per-row gradient coefficient
@@ -406,6 +407,9 @@ __device__ __forceinline__ void nt_mainloop(const typename Operand<BF16>::T *__r
     const int kb = kt * BK;
 #pragma unroll
     for (int i = 0; i < IA; ++i) {
+      // The offset goes through a typed local: with a template-dependent
+      // expression as the argument, hipcc's host pass drops the kernel's
+      // launch stub without a diagnostic (the library then fails to load).
       const uint32_t o = kb + kca[i] < K ? oa[i] + kb * ES : kOutOfRange;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void *)(As + (wave * IA + i) * 8 * BK), 16,
                                                o, 0, 0, 0);
