@@ -352,6 +352,48 @@ def test_pipeline_schedule_invariance_bitwise(P):
         np.testing.assert_array_equal(_np(x.W), _np(z.W))
 
 
+def test_pipeline_full_size_bench_config(P):
+    """The timed training epoch at its full size and launch configuration (60 000
+    pairs, 784->2000x4, chunks of 1024+1024 rows, one stream per layer).  Each
+    layer's step on chunk c depends only on chunks <= c, so the loss trace of
+    the first two chunks of every layer is the oracle's pipelined run on those
+    two chunks; the whole epoch is bitwise the same when run again and when
+    every layer shares one stream."""
+    from ffinputs import make_workload
+    w = WORKLOADS["mnist_784_2000x4_pipelined"]
+    x_base, y, y_neg, params = make_workload(w)
+    hp_kw = dict(theta=w.theta, lr=w.lr, beta1=w.beta1, beta2=w.beta2, adam_eps=w.adam_eps,
+                 norm_eps=w.norm_eps)
+    xd, yd, ynd = _t(x_base), _t(y), _t(y_neg)
+    nc = len(w.chunks())
+
+    def run(streams):
+        layers = [P.Layer(_t(W), _t(b)) for W, b in params]
+        trace = torch.zeros(w.n_layers, nc, device=DEV)
+        P.ff_pipeline_epoch(layers, P.HParams(**hp_kw), xd, yd, ynd, w.n_classes,
+                            w.chunk_pairs, 1, P.FF_PIPELINED, streams=streams, loss_trace=trace)
+        torch.cuda.synchronize()
+        return [_np(L.W) for L in layers], _np(trace)
+
+    cur = torch.cuda.current_stream()
+    four = [cur] + [torch.cuda.Stream() for _ in range(w.n_layers - 1)]
+    Wa, ta = run(four)
+    Wb, tb = run(four)
+    Wc, tc = run([cur] * w.n_layers)
+    np.testing.assert_array_equal(ta, tb)
+    np.testing.assert_array_equal(ta, tc)
+    for a, b, c in zip(Wa, Wb, Wc):
+        np.testing.assert_array_equal(a, b)
+        np.testing.assert_array_equal(a, c)
+        assert np.isfinite(a).all()
+
+    n2 = 2 * w.chunk_pairs
+    ref = [O.Layer.from_params(W, b) for W, b in params]
+    tr_ref = O.train_pipelined(ref, x_base[:n2], y[:n2], y_neg[:n2], w.n_classes,
+                               w.chunk_pairs, 1, O.HParams(**hp_kw))
+    np.testing.assert_allclose(ta[:, :2], tr_ref, rtol=2e-4)
+
+
 def test_tiny_config_end_to_end(P):
     """784->500->500, 512 pairs full batch, 5 steps per layer layer by layer, then scoring."""
     w = WORKLOADS["mnist_tiny_784_500x2"]
