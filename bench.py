@@ -169,6 +169,52 @@ def isolated_roofline(P, torch, w, dtype, kind, peak, punit, reps=20):
             "launches": st["launches"]}
 
 
+def hbm_kernels(P, torch, reps=20):
+    """The row / elementwise kernels alone on one stream at bandwidth-sized
+    launches, each timed by the per-launch HIP events of the library's kernel
+    timing: algorithmic bytes per launch / average launch duration, against
+    the 8 TB/s HBM peak.  Inputs are seeded uniform(0, 1) rows drawn on the
+    device.
+      embed_norm: normalisation of CIFAR-shaped rows (3072 features): one
+        training chunk (4096 rows, bf16 out) and the 49 152-row prefix of the
+        set (bf16 and fp32 out);
+      bf16_shadow: the bf16 weight copy of a 3072 x 3072 layer."""
+    from ffinputs import make_weights
+    dev = torch.device("cuda:0")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(11)
+    out = {}
+
+    def timed(kind, fn):
+        fn()
+        torch.cuda.synchronize()
+        P.ff_profile_start(reps * 4, kinds=[kind])
+        for _ in range(reps):
+            fn()
+        st = P.ff_profile_stop()[kind]
+        gbs = st["bytes"] / (st["total_ms"] * 1e-3) / 1e9
+        return {"avg_us": st["total_ms"] * 1e3 / st["launches"],
+                "bytes_per_launch": st["bytes"] / st["launches"], "GB/s": gbs,
+                "frac": gbs / HBM_PEAK_GBS, "launches": st["launches"]}
+
+    d, d_out = 3072, 16
+    (W, b), = make_weights(12, (d, d_out))
+    x = torch.rand(49152, d, generator=gen, device=dev)
+    for rows, bf16 in ((4096, True), (49152, True), (49152, False)):
+        dt = P.FF_BF16 if bf16 else P.FF_F32
+        L = P.Layer(torch.from_numpy(W).to(dev), torch.from_numpy(b).to(dev), bf16)
+        hp = P.HParams(dtype=dt)
+        ws = P.workspace(P.ff_step_workspace_size(rows, d, d_out, dt), dev)
+        xr = x[:rows]
+        r = timed("embed_norm", lambda: P.ff_layer_forward(L, hp, xr, ws=ws))
+        out[f"embed_norm_{rows}x{d}_{'bf16' if bf16 else 'f32'}_out"] = r
+        del ws
+    Wb = torch.rand(3072, 3072, generator=gen, device=dev) - 0.5
+    Lb = P.Layer(Wb, torch.zeros(3072, device=dev), True)
+    out["bf16_shadow_3072x3072"] = timed("bf16_shadow", lambda: P.ff_refresh_bf16_shadow(Lb))
+    return out
+
+
 def other_workloads(P, torch, names, reps=2):
     """Training epochs of the other training workloads (the sequential fp32
     schedule of the same MNIST-shaped net, its bf16 form, and the CIFAR-shaped
@@ -257,6 +303,14 @@ def softmax_head(P, torch, sw, sxd, slayers, reps=5):
         out[name + "_ms"] = a.elapsed_time(b) / reps
     out["images_per_s"] = sw.n / (out["predict_ms"] * 1e-3)
     out["features"] = D
+    # the softmax layer's logits kernel alone: it reads every feature row once
+    P.ff_profile_start(64, kinds=["head"])
+    P.ff_head_predict(slayers, hp, head, sxd, 1, pred=pred, ws=ws)
+    st = P.ff_profile_stop()["head"]
+    gbs = st["bytes"] / (st["total_ms"] * 1e-3) / 1e9
+    out["head_logits"] = {"avg_us": st["total_ms"] * 1e3 / max(st["launches"], 1),
+                          "bytes_per_launch": st["bytes"] / max(st["launches"], 1),
+                          "GB/s": gbs, "frac": gbs / HBM_PEAK_GBS}
     return out
 
 
@@ -569,6 +623,7 @@ def main():
         "kernels": kernels,
     }
     out["roofline_isolated"] = isolated_roofline(P, torch, w, dtype, dom, peak, punit)
+    out["hbm_kernels_isolated"] = hbm_kernels(P, torch)
     if not args.no_other_workloads:
         out["softmax_head"] = softmax_head(P, torch, sw, sxd, slayers)
         out["performance_optimised_and_adaptive_neg"] = po_and_adaptive(P, torch, w, xd, yd,

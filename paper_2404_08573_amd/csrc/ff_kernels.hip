@@ -28,6 +28,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "ff_internal.h"
 
@@ -176,6 +177,56 @@ __global__ __launch_bounds__(kBlock) void k_embed_norm(RowMap m, int rows, int d
       reinterpret_cast<uint2 *>(out)[(size_t)r * d4 + i] = p;
     } else {
       st4(reinterpret_cast<float *>(out) + (size_t)r * d + 4 * i, v);
+    }
+  }
+}
+
+// The same for rows of at most 256 * NV features, held in registers: each
+// lane issues its NV float4 loads before using any, so a wave keeps NV KB in
+// flight, and the row is read once (the general kernel above reads it twice
+// and waits on each load in turn).
+template <int NV, bool BF16OUT>
+__global__ __launch_bounds__(kBlock) void k_embed_norm_reg(RowMap m, int rows, int d, float eps,
+                                                           int normalise, void *out,
+                                                           float *scale_out) {
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  if (r >= rows) return;  // uniform per wave
+  int src, lab;
+  map_row(m, r, src, lab);
+  const float *xr = m.base + (size_t)src * d;
+  const int d4 = d >> 2;
+  float4 v[NV];
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int i = lane + 64 * j;
+    v[j] = i < d4 ? ld4(xr + 4 * i) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    v[j] = embed4(v[j], 4 * (lane + 64 * j), lab, m.n_classes);
+    ss += v[j].x * v[j].x + v[j].y * v[j].y + v[j].z * v[j].z + v[j].w * v[j].w;
+  }
+  float scale = 1.f;
+  if (normalise) {
+    ss = wave_sum(ss);
+    if (m.mode == MASKED) ss += 1.f;  // the one-hot label feature every embedding carries
+    scale = 1.f / (sqrtf(ss) + eps);
+  }
+  if (scale_out && lane == 0) scale_out[r] = BF16OUT ? bf16_round_f(scale) : scale;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int i = lane + 64 * j;
+    if (i >= d4) break;
+    const float4 t = make_float4(v[j].x * scale, v[j].y * scale, v[j].z * scale, v[j].w * scale);
+    if (BF16OUT) {
+      uint2 p;
+      p.x = pack_bf16(t.x, t.y);
+      p.y = pack_bf16(t.z, t.w);
+      reinterpret_cast<uint2 *>(out)[(size_t)r * d4 + i] = p;
+    } else {
+      st4(reinterpret_cast<float *>(out) + (size_t)r * d + 4 * i, t);
     }
   }
 }
@@ -1094,69 +1145,144 @@ __device__ __forceinline__ int head_block(const HeadFeatures &hf, int f, int &j)
   return blk;
 }
 
-// One wave per row: the C dot products over the row's feature blocks, reduced
-// across the wave, then the softmax on lanes 0..C-1.
+// One wave per kHeadRows rows: the C dot products of each row over its
+// feature blocks, reduced across the wave, then the softmax on lanes 0..C-1.
+// The classifier weights go through LDS in chunks of 256 features (double
+// buffered, one barrier per chunk), so the workgroup's 4 waves share each
+// weight load; each wave prefetches its rows' next chunk before working on
+// the current one.  The feature rows are read from HBM once.  A row's sums
+// run in the same order whatever its wave.
+//
+// CC is a compile-time bound on the class count C (C <= CC): the weights of
+// classes C..CC-1 are class C-1 again and their sums are dropped, so the
+// loops have no per-class branches.
+constexpr int kHeadRows = 2;
+template <int CC>
 __global__ __launch_bounds__(kBlock) void k_head_logits(HeadFeatures hf, int n, int C,
                                                         const int32_t *__restrict__ labels,
                                                         float *__restrict__ logits,
                                                         int32_t *__restrict__ pred,
                                                         float *__restrict__ G,
                                                         float *__restrict__ lrow) {
-  const int lane = threadIdx.x & 63;
-  const int r = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
-  if (r >= n) return;  // uniform per wave
-  float acc[kHeadMaxClasses];
+  constexpr int RW = kHeadRows;
+  constexpr int WL = (CC * 64 + kBlock - 1) / kBlock;  // weight float4 per thread per chunk
+  __shared__ float4 wsh[2][CC * 64];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int r0 = (blockIdx.x * (kBlock / 64) + (tid >> 6)) * RW;
+  const bool active = r0 < n;  // uniform per wave; every wave stages weights
+  float acc[RW][CC];
 #pragma unroll
-  for (int c = 0; c < kHeadMaxClasses; ++c) acc[c] = 0.f;
+  for (int q = 0; q < RW; ++q)
+#pragma unroll
+    for (int c = 0; c < CC; ++c) acc[q][c] = 0.f;
   for (int blk = 0; blk < hf.n_blocks; ++blk) {
-    const int d = hf.d[blk], ldw = hf.ldw[blk];
-    const float *hr = hf.h[blk] + (size_t)r * d;
+    const int d4 = hf.d[blk] >> 2, ldw = hf.ldw[blk];
     const float *wb = hf.w[blk];
-    const float sr = hf.s[blk] ? hf.s[blk][r] : 1.f;
-    for (int i = lane; i < (d >> 2); i += 64) {
-      float4 a = ld4(hr + 4 * i);
-      a.x *= sr;
-      a.y *= sr;
-      a.z *= sr;
-      a.w *= sr;
+    const float *hr[RW];
+    float sr[RW];
 #pragma unroll
-      for (int c = 0; c < kHeadMaxClasses; ++c)
-        if (c < C) {
-          const float4 w = ld4(wb + (size_t)c * ldw + 4 * i);
-          acc[c] += a.x * w.x + a.y * w.y + a.z * w.z + a.w * w.w;
-        }
+    for (int q = 0; q < RW; ++q) {
+      const int r = min(r0 + q, n - 1);  // rows past n: computed, never stored
+      hr[q] = hf.h[blk] + (size_t)r * hf.d[blk];
+      sr[q] = hf.s[blk] ? hf.s[blk][r] : 1.f;
     }
-  }
-  float z = 0.f, zmax = -INFINITY;
-  int arg = 0;
+    const int nch = (d4 + 63) / 64;
+    float4 wreg[WL];
+    auto wload = [&](int ch) {
 #pragma unroll
-  for (int c = 0; c < kHeadMaxClasses; ++c)
-    if (c < C) {
-      float v = wave_sum(acc[c]);
-      for (int k = 0; k < hf.n_bias; ++k) v += hf.bias[k][c];
-      if (lane == c) z = v;
-      if (v > zmax) {
-        zmax = v;
-        arg = c;
+      for (int k = 0; k < WL; ++k) {
+        const int t = tid + k * kBlock, j = ch * 64 + (t & 63);
+        if (t < CC * 64)
+          wreg[k] = j < d4 ? ld4(wb + (size_t)min(t >> 6, C - 1) * ldw + 4 * j)
+                           : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    };
+    auto wstore = [&](int buf) {
+#pragma unroll
+      for (int k = 0; k < WL; ++k) {
+        const int t = tid + k * kBlock;
+        if (t < CC * 64) wsh[buf][t] = wreg[k];
+      }
+    };
+    float4 a[RW];
+    wload(0);
+#pragma unroll
+    for (int q = 0; q < RW; ++q)
+      a[q] = active && lane < d4 ? ld4(hr[q] + 4 * lane) : make_float4(0.f, 0.f, 0.f, 0.f);
+    wstore(0);
+    __syncthreads();
+    for (int ch = 0; ch < nch; ++ch) {
+      const int i = ch * 64 + lane;
+      const bool more = ch + 1 < nch;
+      float4 an[RW];
+      if (more) {
+        wload(ch + 1);
+        const int inext = min(i + 64, d4 - 1);
+#pragma unroll
+        for (int q = 0; q < RW; ++q)
+          an[q] = active ? ld4(hr[q] + 4 * inext) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+      if (active && i < d4) {
+#pragma unroll
+        for (int q = 0; q < RW; ++q) {
+          a[q].x *= sr[q];
+          a[q].y *= sr[q];
+          a[q].z *= sr[q];
+          a[q].w *= sr[q];
+        }
+#pragma unroll
+        for (int c = 0; c < CC; ++c) {
+          const float4 w = wsh[ch & 1][c * 64 + lane];
+#pragma unroll
+          for (int q = 0; q < RW; ++q)
+            acc[q][c] += a[q].x * w.x + a[q].y * w.y + a[q].z * w.z + a[q].w * w.w;
+        }
+      }
+      if (more) wstore((ch + 1) & 1);
+      __syncthreads();  // chunk ch's buffer is free, chunk ch+1's is written
+      if (more) {
+#pragma unroll
+        for (int q = 0; q < RW; ++q) a[q] = an[q];
       }
     }
-  const float e = lane < C ? expf(z - zmax) : 0.f;
-  const float esum = wave_sum(e);
-  // labels outside [0, C) are clamped into it (unspecified result, no stray access)
-  const int y = labels ? min(max(labels[r], 0), C - 1) : 0;
-  const float zy = __shfl(z, y);  // the true class's logit, from its lane (whole wave active)
-  if (lane < C) {
-    if (logits) logits[(size_t)r * C + lane] = z;
-    if (G) G[(size_t)r * C + lane] = (e / esum - (lane == y ? 1.f : 0.f)) / (float)n;
   }
-  if (lane == 0) {
-    if (pred) pred[r] = arg;
-    if (lrow) lrow[r] = logf(esum) - (zy - zmax);  // -log p_y
+  if (!active) return;
+#pragma unroll
+  for (int q = 0; q < RW; ++q) {
+    const int r = r0 + q;
+    if (r >= n) break;  // uniform per wave
+    float z = 0.f, zmax = -INFINITY;
+    int arg = 0;
+#pragma unroll
+    for (int c = 0; c < CC; ++c)
+      if (c < C) {
+        float v = wave_sum(acc[q][c]);
+        for (int k = 0; k < hf.n_bias; ++k) v += hf.bias[k][c];
+        if (lane == c) z = v;
+        if (v > zmax) {
+          zmax = v;
+          arg = c;
+        }
+      }
+    const float e = lane < C ? expf(z - zmax) : 0.f;
+    const float esum = wave_sum(e);
+    // labels outside [0, C) are clamped into it (unspecified result, no stray access)
+    const int y = labels ? min(max(labels[r], 0), C - 1) : 0;
+    const float zy = __shfl(z, y);  // the true class's logit, from its lane (whole wave active)
+    if (lane < C) {
+      if (logits) logits[(size_t)r * C + lane] = z;
+      if (G) G[(size_t)r * C + lane] = (e / esum - (lane == y ? 1.f : 0.f)) / (float)n;
+    }
+    if (lane == 0) {
+      if (pred) pred[r] = arg;
+      if (lrow) lrow[r] = logf(esum) - (zy - zmax);  // -log p_y
+    }
   }
 }
 
 // Backprop of a layer's classifier into the layer: one thread per 4
 // consecutive units of a row.
+template <int CC>  // class-count bound, as in k_head_logits
 __global__ __launch_bounds__(kBlock) void k_po_dz(const float *__restrict__ H,
                                                   const float *__restrict__ G,
                                                   const float *__restrict__ Wc, int R, int D,
@@ -1169,15 +1295,16 @@ __global__ __launch_bounds__(kBlock) void k_po_dz(const float *__restrict__ H,
   const float4 h = ld4(H + (size_t)r * D + j);
   float4 g = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-  for (int c = 0; c < kHeadMaxClasses; ++c)
-    if (c < C) {
-      const float gc = G[(size_t)r * C + c];
-      const float4 w = ld4(Wc + (size_t)c * D + j);
-      g.x += gc * w.x;
-      g.y += gc * w.y;
-      g.z += gc * w.z;
-      g.w += gc * w.w;
-    }
+  for (int c = 0; c < CC; ++c) {
+    const int cc = min(c, C - 1);
+    const float gl = G[(size_t)r * C + cc];
+    const float4 w = ld4(Wc + (size_t)cc * D + j);
+    const float gc = c < C ? gl : 0.f;
+    g.x += gc * w.x;
+    g.y += gc * w.y;
+    g.z += gc * w.z;
+    g.w += gc * w.w;
+  }
   g.x = h.x > 0.f ? g.x : 0.f;  // the ReLU derivative (h = 0 wherever z <= 0)
   g.y = h.y > 0.f ? g.y : 0.f;
   g.z = h.z > 0.f ? g.z : 0.f;
@@ -1187,6 +1314,7 @@ __global__ __launch_bounds__(kBlock) void k_po_dz(const float *__restrict__ H,
 }
 
 // One thread per 4 consecutive features and split of rows: C x 4 partial sums.
+template <int CC>  // class-count bound, as in k_head_logits
 __global__ __launch_bounds__(kBlock) void k_head_grad(HeadFeatures hf,
                                                       const float *__restrict__ G, int n, int C,
                                                       int D, int rows_per_split,
@@ -1199,9 +1327,9 @@ __global__ __launch_bounds__(kBlock) void k_head_grad(HeadFeatures hf,
   const float *h = hf.h[blk] + j;
   const float *sv = hf.s[blk];  // null: scale 1
   const int r0 = blockIdx.y * rows_per_split, r1 = min(n, r0 + rows_per_split);
-  float4 acc[kHeadMaxClasses];
+  float4 acc[CC];
 #pragma unroll
-  for (int c = 0; c < kHeadMaxClasses; ++c) acc[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int c = 0; c < CC; ++c) acc[c] = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int r = r0; r < r1; ++r) {
     float4 a = ld4(h + (size_t)r * d);
     const float sr = sv ? sv[r] : 1.f;
@@ -1210,17 +1338,16 @@ __global__ __launch_bounds__(kBlock) void k_head_grad(HeadFeatures hf,
     a.z *= sr;
     a.w *= sr;
 #pragma unroll
-    for (int c = 0; c < kHeadMaxClasses; ++c)
-      if (c < C) {
-        const float g = G[(size_t)r * C + c];
-        acc[c].x += g * a.x;
-        acc[c].y += g * a.y;
-        acc[c].z += g * a.z;
-        acc[c].w += g * a.w;
-      }
+    for (int c = 0; c < CC; ++c) {
+      const float g = G[(size_t)r * C + min(c, C - 1)];  // classes past C: never stored
+      acc[c].x += g * a.x;
+      acc[c].y += g * a.y;
+      acc[c].z += g * a.z;
+      acc[c].w += g * a.w;
+    }
   }
 #pragma unroll
-  for (int c = 0; c < kHeadMaxClasses; ++c)
+  for (int c = 0; c < CC; ++c)
     if (c < C) st4(part + ((size_t)blockIdx.y * C + c) * D + f, acc[c]);
 }
 
@@ -1322,10 +1449,17 @@ __global__ __launch_bounds__(kBlock) void k_argmax(const float *__restrict__ S, 
   pred[i] = arg;
 }
 
+// Eight weights per thread: two 16-byte loads, one 16-byte store.
 __global__ __launch_bounds__(kBlock) void k_bf16_shadow(const float *__restrict__ W,
                                                         uint16_t *__restrict__ Wb, size_t count) {
-  const size_t i = (size_t)blockIdx.x * kBlock + threadIdx.x;
-  if (i < count) Wb[i] = bf16_of(W[i]);
+  const size_t i = ((size_t)blockIdx.x * kBlock + threadIdx.x) * 8;
+  if (i + 8 <= count) {
+    const float4 a = ld4(W + i), b = ld4(W + i + 4);
+    st16(Wb + i, make_uint4(pack_bf16(a.x, a.y), pack_bf16(a.z, a.w), pack_bf16(b.x, b.y),
+                            pack_bf16(b.z, b.w)));
+  } else {
+    for (size_t j = i; j < count; ++j) Wb[j] = bf16_of(W[j]);
+  }
 }
 
 inline unsigned cdiv(long a, long b) { return (unsigned)((a + b - 1) / b); }
@@ -1425,16 +1559,43 @@ int fwd_col_tiles_max(int n_cols) {
 
 int loss_blocks(int rows) { return (int)cdiv(rows, kLossRows); }
 
+template <int NV>
+void embed_norm_reg(const RowMap &m, int rows, int d, float eps, bool normalise, bool bf16_out,
+                    void *out, float *scale_out, hipStream_t s) {
+  const dim3 grid(cdiv(rows, kBlock / 64));
+  if (bf16_out)
+    hipLaunchKernelGGL((k_embed_norm_reg<NV, true>), grid, dim3(kBlock), 0, s, m, rows, d, eps,
+                       (int)normalise, out, scale_out);
+  else
+    hipLaunchKernelGGL((k_embed_norm_reg<NV, false>), grid, dim3(kBlock), 0, s, m, rows, d, eps,
+                       (int)normalise, out, scale_out);
+}
+
 hipError_t launch_embed_norm(const RowMap &m, int rows, int d, float eps, bool normalise,
                              bool bf16_out, void *out, float *scale_out, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  const dim3 grid(cdiv(rows, kBlock / 64));
-  if (bf16_out)
-    hipLaunchKernelGGL(k_embed_norm<true>, grid, dim3(kBlock), 0, s, m, rows, d, eps,
-                       (int)normalise, out, scale_out);
-  else
-    hipLaunchKernelGGL(k_embed_norm<false>, grid, dim3(kBlock), 0, s, m, rows, d, eps,
-                       (int)normalise, out, scale_out);
+  const int nv = (int)cdiv(d / 4, 64);  // float4 per lane for the whole row
+  if (nv <= 1) {
+    embed_norm_reg<1>(m, rows, d, eps, normalise, bf16_out, out, scale_out, s);
+  } else if (nv <= 2) {
+    embed_norm_reg<2>(m, rows, d, eps, normalise, bf16_out, out, scale_out, s);
+  } else if (nv <= 4) {
+    embed_norm_reg<4>(m, rows, d, eps, normalise, bf16_out, out, scale_out, s);
+  } else if (nv <= 8) {
+    embed_norm_reg<8>(m, rows, d, eps, normalise, bf16_out, out, scale_out, s);
+  } else if (nv <= 12) {
+    embed_norm_reg<12>(m, rows, d, eps, normalise, bf16_out, out, scale_out, s);
+  } else if (nv <= 16) {
+    embed_norm_reg<16>(m, rows, d, eps, normalise, bf16_out, out, scale_out, s);
+  } else {
+    const dim3 grid(cdiv(rows, kBlock / 64));
+    if (bf16_out)
+      hipLaunchKernelGGL(k_embed_norm<true>, grid, dim3(kBlock), 0, s, m, rows, d, eps,
+                         (int)normalise, out, scale_out);
+    else
+      hipLaunchKernelGGL(k_embed_norm<false>, grid, dim3(kBlock), 0, s, m, rows, d, eps,
+                         (int)normalise, out, scale_out);
+  }
   return hipGetLastError();
 }
 
@@ -1566,6 +1727,17 @@ hipError_t launch_argmax(const float *scores, int n, int C, const int32_t *exclu
   return hipGetLastError();
 }
 
+// Calls f with the compile-time class-count bound of the head kernels for C.
+template <class F>
+void head_classes(int C, F &&f) {
+  static_assert(kHeadMaxClasses == 16, "bounds below");
+  if (C <= 2) return f(std::integral_constant<int, 2>{});
+  if (C <= 4) return f(std::integral_constant<int, 4>{});
+  if (C <= 8) return f(std::integral_constant<int, 8>{});
+  if (C <= 10) return f(std::integral_constant<int, 10>{});
+  f(std::integral_constant<int, 16>{});
+}
+
 hipError_t launch_head_logits(const HeadFeatures &f, int n, int C, const int32_t *labels,
                               float *logits, int32_t *pred, float *G, float *lrow,
                               hipStream_t s) {
@@ -1573,8 +1745,10 @@ hipError_t launch_head_logits(const HeadFeatures &f, int n, int C, const int32_t
   if (C < 1 || C > kHeadMaxClasses || f.n_blocks < 1 || f.n_blocks > kHeadMaxBlocks ||
       f.n_bias < 0 || f.n_bias > kHeadMaxBlocks || ((G || lrow) && !labels))
     return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_head_logits, dim3(cdiv(n, kBlock / 64)), dim3(kBlock), 0, s, f, n, C,
-                     labels, logits, pred, G, lrow);
+  head_classes(C, [&](auto cc) {
+    hipLaunchKernelGGL(k_head_logits<decltype(cc)::value>, dim3(cdiv(n, kBlock / 64 * kHeadRows)),
+                       dim3(kBlock), 0, s, f, n, C, labels, logits, pred, G, lrow);
+  });
   return hipGetLastError();
 }
 
@@ -1582,8 +1756,10 @@ hipError_t launch_po_dz(const float *H, const float *G, const float *Wc, int R, 
                         float *dZ, float *ones, hipStream_t s) {
   if (R <= 0) return hipSuccess;
   if (C < 1 || C > kHeadMaxClasses || D % 4) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_po_dz, dim3(cdiv((long)R * (D / 4), kBlock)), dim3(kBlock), 0, s, H, G,
-                     Wc, R, D, C, dZ, ones);
+  head_classes(C, [&](auto cc) {
+    hipLaunchKernelGGL(k_po_dz<decltype(cc)::value>, dim3(cdiv((long)R * (D / 4), kBlock)),
+                       dim3(kBlock), 0, s, H, G, Wc, R, D, C, dZ, ones);
+  });
   return hipGetLastError();
 }
 
@@ -1594,8 +1770,10 @@ hipError_t launch_head_grad(const HeadFeatures &f, const float *G, int n, int C,
   if (n <= 0) return hipSuccess;
   if (C < 1 || C > kHeadMaxClasses || D % 4 || splits < 1) return hipErrorInvalidValue;
   const int rps = (int)cdiv(n, splits);
-  hipLaunchKernelGGL(k_head_grad, dim3(cdiv(D / 4, kBlock), splits), dim3(kBlock), 0, s, f, G, n,
-                     C, D, rps, part);
+  head_classes(C, [&](auto cc) {
+    hipLaunchKernelGGL(k_head_grad<decltype(cc)::value>, dim3(cdiv(D / 4, kBlock), splits),
+                       dim3(kBlock), 0, s, f, G, n, C, D, rps, part);
+  });
   return hipGetLastError();
 }
 
@@ -1612,8 +1790,8 @@ hipError_t launch_head_adam(const float *part, int splits, const float *G, const
 
 hipError_t launch_bf16_shadow(const float *W, uint16_t *Wb, size_t count, hipStream_t s) {
   if (count == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_bf16_shadow, dim3(cdiv((long)count, kBlock)), dim3(kBlock), 0, s, W, Wb,
-                     count);
+  hipLaunchKernelGGL(k_bf16_shadow, dim3(cdiv((long)count, 8 * kBlock)), dim3(kBlock), 0, s, W,
+                     Wb, count);
   return hipGetLastError();
 }
 

@@ -468,6 +468,25 @@ def _run_steps_bf16(P, x, n_pos, W, b, k, hp_kw):
     return L
 
 
+def _bf16_rne(w):
+    """Round-to-nearest-even bf16 bits of fp32 values (finite inputs)."""
+    u = w.view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+@pytest.mark.parametrize("d_out,d_in", [(4, 4), (12, 20), (2000, 784), (3072, 3072)])
+def test_bf16_shadow_refresh_exact(P, d_out, d_in):
+    """ff_refresh_bf16_shadow: every weight rounded to nearest even."""
+    W = random_matrix(d_out * 31 + d_in, d_out, d_in, -2, 2)
+    W[0, 0] = np.float32(1.00390625)  # a tie between two bf16 values: rounds to even
+    L = P.Layer(_t(W), _t(np.zeros(d_out, np.float32)), bf16_shadow=True)
+    L.W_bf16.zero_()
+    P.ff_refresh_bf16_shadow(L)
+    got = _np(L.W_bf16).view(np.uint16)
+    np.testing.assert_array_equal(got, _bf16_rne(W))
+    assert got[0, 0] == 0x3F80
+
+
 @pytest.mark.parametrize("n,d_in,d_out,k", [(24, 16, 12, 2), (150, 200, 260, 3), (1024, 784, 2000, 2)])
 def test_step_parity_bf16(P, n, d_in, d_out, k):
     x_base, y, y_neg = make_data(n + d_out, n, d_in)
