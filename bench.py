@@ -623,8 +623,8 @@ def main():
         "kernels": kernels,
     }
     out["roofline_isolated"] = isolated_roofline(P, torch, w, dtype, dom, peak, punit)
-    out["hbm_kernels_isolated"] = hbm_kernels(P, torch)
     if not args.no_other_workloads:
+        out["hbm_kernels_isolated"] = hbm_kernels(P, torch)
         out["softmax_head"] = softmax_head(P, torch, sw, sxd, slayers)
         out["performance_optimised_and_adaptive_neg"] = po_and_adaptive(P, torch, w, xd, yd,
                                                                         layers)
