@@ -141,6 +141,38 @@ def traffic_summary(fetch_csv, write_csv, cfetch_csv, cwrite_csv, workload, copy
     print(json.dumps(out, indent=1))
 
 
+def counter_summary(csv_paths, n_simd=1024, n_xcd=8):
+    """Per kernel kind, from rocprofv3 --pmc runs over `--focus` steps: MFMA
+    busy fraction = SQ_VALU_MFMA_BUSY_CYCLES / (SIMDs x GPU-active cycles per
+    XCD), with GRBM_GUI_ACTIVE summed over the XCDs; wait and LDS figures per
+    wave cycle.  Prints a markdown table."""
+    import csv
+    import collections
+    print("| run | kernel kind | dispatches | MFMA busy | wave cycles waiting | waiting on LDS "
+          "| LDS bank conflicts / LDS instruction |")
+    print("|---|---|---|---|---|---|---|")
+    for path in csv_paths:
+        agg = collections.defaultdict(lambda: collections.defaultdict(float))
+        ids = collections.defaultdict(set)
+        for r in csv.DictReader(open(path)):
+            kind = next((k for pat, k in KIND_OF if pat in r["Kernel_Name"]), None)
+            if kind is None:
+                continue
+            agg[kind][r["Counter_Name"]] += float(r["Counter_Value"])
+            ids[kind].add(r["Dispatch_Id"])
+        run = os.path.basename(os.path.dirname(path))
+        for kind, c in agg.items():
+            n = len(ids[kind])
+            gui = c.get("GRBM_GUI_ACTIVE", 0.0) / n_xcd
+            busy = c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / n_simd / gui if gui else float("nan")
+            wc = max(c.get("SQ_WAVE_CYCLES", 0.0), 1.0)
+            lds = max(c.get("SQ_INSTS_LDS", 0.0), 1.0)
+            print(f"| {run} | {kind} | {n} | {busy * 100:.1f} % | "
+                  f"{c.get('SQ_WAIT_ANY', 0.0) / wc * 100:.1f} % | "
+                  f"{c.get('SQ_WAIT_INST_LDS', 0.0) / wc * 100:.1f} % | "
+                  f"{c.get('SQ_LDS_BANK_CONFLICT', 0.0) / lds:.3f} |")
+
+
 def isolated_roofline(P, torch, w, dtype, kind, peak, punit, reps=20):
     """The dominant kernel alone on one stream, at the largest layer shape of
     the training step (its chunk rows x the widest layer), timed by the same
@@ -470,6 +502,9 @@ def main():
                     help="FETCH, WRITE, copy FETCH, copy WRITE counter_collection.csv files: "
                          "write profiles/traffic.json for --workload and exit")
     ap.add_argument("--copy-bytes", type=int, default=1 << 30)
+    ap.add_argument("--counter-summary", nargs="+", metavar="CSV",
+                    help="counter_collection.csv files of rocprofv3 --pmc runs over --focus "
+                         "steps: print MFMA-busy and wait fractions per kernel kind and exit")
     ap.add_argument("--focus", nargs=4, type=int, metavar=("ROWS", "D_IN", "D_OUT", "BF16"),
                     help="run a few layer steps of one shape on one stream (for counter runs)")
     args = ap.parse_args()
@@ -478,6 +513,9 @@ def main():
         return
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
+        return
+    if args.counter_summary:
+        counter_summary(args.counter_summary)
         return
     if args.traffic_summary:
         traffic_summary(*args.traffic_summary, args.workload, args.copy_bytes)
