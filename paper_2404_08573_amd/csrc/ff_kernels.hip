@@ -391,6 +391,18 @@ constexpr uint32_t kOutOfRange = 0x80000000u;  // a buffer offset past every til
 // rows.  An involution for each r.
 __device__ __forceinline__ int nt_swz(int r, int c) { return c ^ (r & 7) ^ ((r >> 3) & 1); }
 
+// Workgroup barrier that the compiler may not move memory accesses across.
+// The s_barrier builtin alone is no memory fence, so LDS reads of a tile could
+// be scheduled across it, and __syncthreads' workgroup fence would also wait
+// for every outstanding load into LDS (vmcnt(0)), draining the prefetch.  The
+// empty asm statements with a memory clobber pin the order at the compiler
+// level; the hardware order comes from the explicit s_waitcnt before it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // s_waitcnt operand: at most n vector-memory operations outstanding, no limit
 // on the other counters (gfx9 encoding: vmcnt in bits 3:0 and 15:14).
 constexpr int vmcnt_wait(int n) { return 0x0f70 | (n & 15) | ((n >> 4) << 14); }
@@ -522,12 +534,12 @@ __device__ __forceinline__ void nt_mainloop(const typename Operand<BF16>::T *__r
   for (int j = 0; j < NBUF - 1; ++j) issue(j, j);
   for (int kt = 0; kt < nk; ++kt) {
     __builtin_amdgcn_s_waitcnt(vmcnt_wait((NBUF - 2) * (IA + IB)));
-    __builtin_amdgcn_s_barrier();
+    lds_barrier();
     issue(kt + NBUF - 1, (kt + NBUF - 1) % NBUF);
     compute(kt % NBUF);
   }
   __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
-  __builtin_amdgcn_s_barrier();
+  lds_barrier();
 }
 
 template <bool BF16, int BM, int BN, int WM, int WN, int NBUF, bool STORE_H>
