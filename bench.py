@@ -483,7 +483,52 @@ def cpu_baseline(w, x_base, y, y_neg, params, sw, sx, sparams, budget_s=12.0):
             "sample": f"{steps} layer-steps of {2 * b} rows (chunks 0..{steps // w.n_layers - 1} "
                       f"through all {w.n_layers} layers, {t_train:.1f} s) and label scoring of "
                       f"{n_img} inputs ({t_score:.1f} s); fp64 NumPy, extrapolated to the step",
-            "train_samples_per_s": train_rate, "images_per_s": img_rate}
+            "train_samples_per_s": train_rate, "images_per_s": img_rate,
+            "tiny_config_one_thread_s": tiny_config_one_thread(),
+            "host": host_info()}
+
+
+def tiny_config_one_thread():
+    """The oracle on the tiny configuration (784->500->500, 512 pairs, 5
+    full-batch steps per layer, layer by layer, then scoring all 512 inputs
+    under 10 labels) with one BLAS thread: seconds."""
+    import oracle as O
+    from ffinputs import WORKLOADS, make_workload
+    try:
+        from threadpoolctl import threadpool_limits
+    except Exception:
+        return None
+    w = WORKLOADS["mnist_tiny_784_500x2"]
+    x, y, yn, params = make_workload(w)
+    hp = O.HParams(theta=w.theta, lr=w.lr)
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        layers = [O.Layer.from_params(W, b) for W, b in params]
+        O.train_sequential(layers, x, y, yn, w.n_classes, w.chunk_pairs, w.epochs, hp)
+        O.score_labels(layers, x, w.n_classes, hp, 0)
+        return time.perf_counter() - t0
+
+
+def host_info():
+    """CPU model and the BLAS NumPy uses, for the oracle baseline."""
+    import numpy as np
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    blas = None
+    try:
+        from threadpoolctl import threadpool_info
+        blas = ", ".join(sorted({f"{i.get('internal_api')} {i.get('version')}"
+                                 for i in threadpool_info() if i.get("user_api") == "blas"}))
+    except Exception:
+        pass
+    return {"cpu_model": model, "logical_cpus": os.cpu_count(), "blas": blas,
+            "numpy": np.__version__}
 
 
 def main():
@@ -615,6 +660,10 @@ def main():
     # whole-step algorithmic flops of the training epoch (both products of every layer step)
     train_flops = sum(4.0 * 2 * b * di * do for (_, b) in w.chunks()
                       for di, do in zip(w.dims[:-1], w.dims[1:]))
+    # the algorithmic minimum: layer 0's positive and negative rows share their
+    # base row, so an exact rewrite halves layer 0's products (the scoring pass
+    # already runs that rewrite; training launches the full products)
+    train_min_flops = train_flops - sum(4.0 * b * w.dims[0] * w.dims[1] for (_, b) in w.chunks())
     kernel_ms = sum(v["total_ms"] for v in kstats.values())
     dname = "bf16" if bf16 else "f32"
     bound, peak, punit = PEAK[dname]
@@ -658,6 +707,7 @@ def main():
                              "timed ones)"},
         "concurrency": kernel_ms / profiled_ms,
         "train_mfma_frac": train_flops / (train_ms * 1e-3) / 1e12 / peak,
+        "train_effective_frac": train_min_flops / (train_ms * 1e-3) / 1e12 / peak,
         "kernels": kernels,
     }
     out["roofline_isolated"] = isolated_roofline(P, torch, w, dtype, dom, peak, punit)
