@@ -107,6 +107,7 @@ struct StepScratch {
   float *gpart = nullptr; // [col tiles][rows]
   float *g = nullptr;     // [rows]
   float *c = nullptr;     // [rows]
+  float *cs = nullptr;    // [rows] c times the input row scale (raw fp32 input rows)
   float *lpart = nullptr; // [loss blocks][2]
   float *loss = nullptr;  // [1]
   // Performance-optimised steps (po_classes > 0): the classifier's logit
@@ -131,6 +132,7 @@ void carve_step(Carver &cv, StepScratch &s, int rows, int d_in, int d_out, int d
   s.gpart = static_cast<float *>(cv.take((size_t)ffk::fwd_col_tiles_max(d_out) * rows * 4));
   if (need_g) s.g = static_cast<float *>(cv.take((size_t)rows * 4));
   s.c = static_cast<float *>(cv.take((size_t)rows * 4));
+  s.cs = static_cast<float *>(cv.take((size_t)rows * 4));
   s.lpart = static_cast<float *>(cv.take((size_t)ffk::loss_blocks(rows) * 2 * 4));
   if (need_loss) s.loss = static_cast<float *>(cv.take(4));
 }
@@ -311,10 +313,13 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int
   const int nt = ffk::fwd_col_tiles(R, L->d_out, hp->dtype);
   FF_HIP(fwd(hp->dtype, xop, weight_operand(L, hp->dtype), L->b, in.rowscale, R, L->d_out,
              L->d_in, H, s.gpart, st));
+  float *cs = in.rowscale ? s.cs : nullptr;
   FF_HIP(launch(FF_KERNEL_LOSS, 0.0,
-                (double)nt * R * 4.0 + R * (g ? 8.0 : 4.0) + (s_next ? R * 4.0 : 0.0), st, [&] {
+                (double)nt * R * 4.0 + R * (g ? 8.0 : 4.0) + (s_next ? R * 4.0 : 0.0) +
+                    (cs ? R * 8.0 : 0.0),
+                st, [&] {
                   return ffk::launch_loss(s.gpart, nt, R, n_pos, hp->theta, g, s.c, s.lpart,
-                                          s_next, hp->norm_eps, st);
+                                          s_next, hp->norm_eps, in.rowscale, cs, st);
                 }));
   ffk::LossFinish lf;
   lf.lpart = s.lpart;
@@ -337,7 +342,7 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int
                          R * (in.rowscale ? 8.0 : 4.0) +
                          params * (24.0 + (hp->dtype == FF_BF16 ? 2.0 : 0.0)) + L->d_out * 24.0;
     FF_HIP(launch(FF_KERNEL_DW_ADAM, gemm_flops(L->d_out, L->d_in, R), bytes, st, [&] {
-      return ffk::launch_dw_adam(hp->dtype, H, s.c, xop, in.rowscale, L->d_out, L->d_in, R, L->W,
+      return ffk::launch_dw_adam(hp->dtype, H, s.c, xop, cs, L->d_out, L->d_in, R, L->W,
                                  L->mW, L->vW, hp->dtype == FF_BF16 ? L->W_bf16 : nullptr, L->b,
                                  L->mb, L->vb, a, lf, st);
     }));
@@ -401,7 +406,9 @@ ff_status po_step_core(ff_layer *L, ff_head *head, const ff_hparams *hp, const f
                                                head->mW, head->vW, head->b, head->mb, head->vb,
                                                ah, loss ? loss : s.loss, st);
                 }));
-  // dW = dZ^T x_hat, db = sum dZ: the weight-gradient product with row scale 1
+  // dW = dZ^T x_hat, db = sum dZ: the weight-gradient product with row scale
+  // c = 1, so with raw input rows the product's factor c * s is the input row
+  // scale s itself
   const ffk::AdamArgs a = adam_args(hp, ++L->step);
   ffk::LossFinish lf{};
   const double eb = (double)elem_bytes(hp->dtype);

@@ -142,18 +142,21 @@ hipError_t launch_fwd_expand(int dtype, const void *X, const void *W, const floa
 // g_r = sum_t gpart[t][r] (into g unless null), c_r = 2 dL/dg_r, and loss
 // partials lpart[loss_blocks(R)][2]; s_out (unless null) gets the
 // normalisation 1/(sqrt(g_r) + norm_eps) of the activity rows as the next
-// layer's input (g_r is their squared norm).
+// layer's input (g_r is their squared norm).  With s_in (the layer input's
+// row scales, when its rows are raw), cs_r = c_r * s_in_r.
 hipError_t launch_loss(const float *gpart, int ntiles, int R, int n_pos, float theta, float *g,
-                       float *c, float *lpart, float *s_out, float norm_eps, hipStream_t s);
+                       float *c, float *lpart, float *s_out, float norm_eps, const float *s_in,
+                       float *cs, hipStream_t s);
 
 // dW = (c . H)^T Xh contracted over the R rows, db = sum_r c_r H_r, then one
 // Adam update of W (and its bf16 shadow when Wb != nullptr) and of b; also
-// finishes the loss scalar described by lf.  bscale [R] or null (fp32 only):
-// Xh rows are raw and x_hat_r = bscale[r] * Xh_r.
+// finishes the loss scalar described by lf.  cs [R] or null (fp32 only): Xh
+// rows are raw, x_hat_r = s_r * Xh_r, and cs_r = c_r * s_r is the factor the
+// product applies to H row r (db still uses c).
 hipError_t launch_dw_adam(int dtype, const float *H, const float *c, const void *Xh,
-                          const float *bscale, int M, int N, int K, float *W, float *mW,
-                          float *vW, uint16_t *Wb, float *b, float *mb, float *vb,
-                          const AdamArgs &a, const LossFinish &lf, hipStream_t s);
+                          const float *cs, int M, int N, int K, float *W, float *mW, float *vW,
+                          uint16_t *Wb, float *b, float *mb, float *vb, const AdamArgs &a,
+                          const LossFinish &lf, hipStream_t s);
 
 // g_r = sum_t gpart[t][r] into g (any of the outputs may be null);
 // out[r] = g_r (accumulate == 0) or out[r] += g_r (accumulate == 1);

@@ -728,7 +728,9 @@ __global__ __launch_bounds__(kLossRows) void k_loss_rows(const float *__restrict
                                                           float *__restrict__ c,
                                                           float *__restrict__ lpart,
                                                           float *__restrict__ s_out,
-                                                          float norm_eps) {
+                                                          float norm_eps,
+                                                          const float *__restrict__ s_in,
+                                                          float *__restrict__ cs) {
   __shared__ float sp[kLossRows], sn[kLossRows];
   const int r = blockIdx.x * kLossRows + threadIdx.x;
   float lp = 0.f, ln = 0.f;
@@ -737,15 +739,18 @@ __global__ __launch_bounds__(kLossRows) void k_loss_rows(const float *__restrict
     for (int t = 0; t < nt; ++t) gv += gpart[(size_t)t * R + r];
     if (g) g[r] = gv;
     if (s_out) s_out[r] = 1.f / (sqrtf(gv) + norm_eps);  // g is the row's squared norm
+    float cr;
     if (r < n_pos) {
       const float x = theta - gv;
       lp = softplus_f(x);
-      c[r] = -2.f * sigmoid_f(x) / (float)n_pos;
+      cr = -2.f * sigmoid_f(x) / (float)n_pos;
     } else {
       const float x = gv - theta;
       ln = softplus_f(x);
-      c[r] = 2.f * sigmoid_f(x) / (float)(R - n_pos);
+      cr = 2.f * sigmoid_f(x) / (float)(R - n_pos);
     }
+    c[r] = cr;
+    if (cs) cs[r] = cr * s_in[r];
   }
   sp[threadIdx.x] = lp;
   sn[threadIdx.x] = ln;
@@ -772,15 +777,16 @@ __global__ __launch_bounds__(kLossRows) void k_loss_rows(const float *__restrict
 // row MB*i + mb; likewise NB consecutive X_hat floats give column NB*j + nb.
 // Half-wave kg takes slab rows 2s+kg.  The loads are issued raw ahead of the
 // MFMAs; the row scale c, the k-tail mask and the db sums are applied when the
-// registers are written to LDS.  With BS the X rows are raw and bscale holds
-// their normalisation (x_hat_k = bscale[k] * X_k).  A per-row factor of the
-// contraction can sit on either operand, so it joins c on the c.H rows (after
-// the db sum, which wants c alone) and the X_hat tile is staged as loaded.
+// registers are written to LDS.  With BS the X rows are raw (x_hat_k =
+// s_k * X_k): a per-row factor of the contraction can sit on either operand,
+// so the c.H rows are staged scaled by cs_k = c_k * s_k (one factor, computed
+// with c by the loss kernel), the X tile is staged as loaded, and only the
+// column-tile-0 workgroups, which also sum db = sum_k c_k H_k, load c.
 // ---------------------------------------------------------------------------
 template <int BM, int BN, int BK, int WM, int WN, int PF, bool BS>
 __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
     const float *__restrict__ Hm, const float *__restrict__ cvec, const float *__restrict__ Xh,
-    const float *__restrict__ bscale, int M, int N, int K, float *__restrict__ W, float *__restrict__ mW, float *__restrict__ vW,
+    const float *__restrict__ csvec, int M, int N, int K, float *__restrict__ W, float *__restrict__ mW, float *__restrict__ vW,
     uint16_t *__restrict__ Wb, float *__restrict__ bvec, float *__restrict__ mbv,
     float *__restrict__ vbv, AdamArgs ad, LossFinish lf) {
   constexpr int NT = WM * WN * 64;
@@ -821,7 +827,7 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
 
   struct Stage {
     float4 a[LDA], b[LDB];
-    float c[LDA], s[BS ? LDA : 1];
+    float c[LDA], d[BS ? LDA : 1];  // product factor (c or cs); c for db under BS
     int kt;
   } st[PF];
   float4 dbp = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -830,8 +836,12 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
     for (int i = 0; i < LDA; ++i) {
       const int k = min(kt * BK + ka + i * KSA, K - 1);
       g.a[i] = ld4(pa + (size_t)k * M);
-      g.c[i] = cvec[k];
-      if constexpr (BS) g.s[i] = bscale[k];
+      if constexpr (BS) {
+        g.c[i] = csvec[k];
+        if (do_db) g.d[i] = cvec[k];
+      } else {
+        g.c[i] = cvec[k];
+      }
     }
 #pragma unroll
     for (int i = 0; i < LDB; ++i) {
@@ -843,23 +853,16 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
   auto sstore = [&](const Stage &g, int buf) {
 #pragma unroll
     for (int i = 0; i < LDA; ++i) {
-      const float cc = g.kt * BK + ka + i * KSA < K ? g.c[i] : 0.f;  // rows past K add nothing
-      float4 v = g.a[i];
-      v.x *= cc;
-      v.y *= cc;
-      v.z *= cc;
-      v.w *= cc;
+      const bool kok = g.kt * BK + ka + i * KSA < K;  // rows past K add nothing
+      const float cc = kok ? g.c[i] : 0.f;
+      const float4 a = g.a[i];
+      const float4 v = make_float4(a.x * cc, a.y * cc, a.z * cc, a.w * cc);
       if (do_db) {
-        dbp.x += v.x;
-        dbp.y += v.y;
-        dbp.z += v.z;
-        dbp.w += v.w;
-      }
-      if constexpr (BS) {
-        v.x *= g.s[i];
-        v.y *= g.s[i];
-        v.z *= g.s[i];
-        v.w *= g.s[i];
+        const float cd = BS ? (kok ? g.d[BS ? i : 0] : 0.f) : cc;
+        dbp.x += a.x * cd;
+        dbp.y += a.y * cd;
+        dbp.z += a.z * cd;
+        dbp.w += a.w * cd;
       }
       st4(As + (buf * BK + ka + i * KSA) * LDM + ca, v);
     }
@@ -1677,14 +1680,16 @@ hipError_t launch_fwd_expand(int dtype, const void *X, const void *W, const floa
 }
 
 hipError_t launch_loss(const float *gpart, int ntiles, int R, int n_pos, float theta, float *g,
-                       float *c, float *lpart, float *s_out, float norm_eps, hipStream_t s) {
+                       float *c, float *lpart, float *s_out, float norm_eps, const float *s_in,
+                       float *cs, hipStream_t s) {
+  if (cs && !s_in) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_loss_rows, dim3(loss_blocks(R)), dim3(kLossRows), 0, s, gpart, ntiles, R,
-                     n_pos, theta, g, c, lpart, s_out, norm_eps);
+                     n_pos, theta, g, c, lpart, s_out, norm_eps, s_in, cs);
   return hipGetLastError();
 }
 
 template <bool BF16, class T>
-void dw_launch(const float *H, const float *c, const void *Xh, const float *bscale, int M, int N,
+void dw_launch(const float *H, const float *c, const void *Xh, const float *cs, int M, int N,
                int K, float *W, float *mW, float *vW, uint16_t *Wb, float *b, float *mb,
                float *vb, const AdamArgs &a, const LossFinish &lf, hipStream_t s) {
   const dim3 grid(T::tiles(M, N)), block(T::threads);
@@ -1692,28 +1697,28 @@ void dw_launch(const float *H, const float *c, const void *Xh, const float *bsca
     hipLaunchKernelGGL((k_dw_adam_bf16<T::bm, T::bn, T::bk, T::wm, T::wn, T::pf>), grid, block,
                        0, s, H, c, static_cast<const uint16_t *>(Xh), M, N, K, W, mW, vW, Wb, b,
                        mb, vb, a, lf);
-  else if (bscale)
+  else if (cs)
     hipLaunchKernelGGL((k_dw_adam_f32<T::bm, T::bn, T::bk, T::wm, T::wn, T::pf, true>), grid,
-                       block, 0, s, H, c, static_cast<const float *>(Xh), bscale, M, N, K, W, mW,
+                       block, 0, s, H, c, static_cast<const float *>(Xh), cs, M, N, K, W, mW,
                        vW, Wb, b, mb, vb, a, lf);
   else
     hipLaunchKernelGGL((k_dw_adam_f32<T::bm, T::bn, T::bk, T::wm, T::wn, T::pf, false>), grid,
-                       block, 0, s, H, c, static_cast<const float *>(Xh), bscale, M, N, K, W, mW,
+                       block, 0, s, H, c, static_cast<const float *>(Xh), cs, M, N, K, W, mW,
                        vW, Wb, b, mb, vb, a, lf);
 }
 
 hipError_t launch_dw_adam(int dtype, const float *H, const float *c, const void *Xh,
-                          const float *bscale, int M, int N, int K, float *W, float *mW,
+                          const float *cs, int M, int N, int K, float *W, float *mW,
                           float *vW, uint16_t *Wb, float *b, float *mb, float *vb,
                           const AdamArgs &a, const LossFinish &lf, hipStream_t s) {
   const bool big = dw_big(M, N, dtype);
   if (dtype == 0) {
     if (big)
-      dw_launch<false, DwBig>(H, c, Xh, bscale, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
+      dw_launch<false, DwBig>(H, c, Xh, cs, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
     else
-      dw_launch<false, DwSmall>(H, c, Xh, bscale, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
+      dw_launch<false, DwSmall>(H, c, Xh, cs, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
   } else {
-    if (bscale) return hipErrorInvalidValue;  // bf16 operands arrive normalised
+    if (cs) return hipErrorInvalidValue;  // bf16 operands arrive normalised
     if (big)
       dw_launch<true, DwBigBf16>(H, c, Xh, nullptr, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
     else
