@@ -247,7 +247,12 @@ size_t ff_pipeline_workspace_size(const ff_layer *layers, int32_t n_layers, int3
  * (labels y_neg), embedded as in ff_embed_labels.
  *   FF_SEQUENTIAL (Sec. 3 sequential training): layer l takes all its steps,
  *     then one forward pass with its final weights gives layer l+1's input
- *     (the "x <- layer(x)" step of Alg. 2).  Everything runs on streams[0].
+ *     (the "x <- layer(x)" step of Alg. 2).  The steps run on streams[0]; that
+ *     forward pass runs chunk by chunk on streams[1] (when n_layers > 1 and
+ *     streams[1] is not NULL; else on streams[0]), beside layer l+1's steps,
+ *     each of which waits only for the chunk it reads.  Work on streams[1]
+ *     always ends before the last step on streams[0], and the result is the
+ *     same either way.
  *   FF_PIPELINED (Single-Layer PFF, Sec. 4.1 / Alg. 1, at the per-batch
  *     exchange granularity proposed in Sec. 6): layer l runs on streams[l];
  *     its step on chunk c starts once layer l-1 has emitted the activities of
@@ -257,8 +262,7 @@ size_t ff_pipeline_workspace_size(const ff_layer *layers, int32_t n_layers, int3
  *   layers (host) [n_layers] chained; x_base (device) [n][layers[0].d_in];
  *   y_pos, y_neg (device) [n] int32 in [0, n_classes) (other values give
  *   unspecified results, without out-of-bounds accesses); streams (host)
- *   [n_layers] (only [0] is
- *   read for FF_SEQUENTIAL); loss_trace (device) [n_layers][epochs*n_chunks]
+ *   [n_layers] (only [0] and [1] are read for FF_SEQUENTIAL); loss_trace (device) [n_layers][epochs*n_chunks]
  *   or NULL.  The caller must not touch the layers or ws until all streams
  *   have drained. */
 ff_status ff_pipeline_epoch(ff_layer *layers, int32_t n_layers, const ff_hparams *hp,

@@ -890,7 +890,7 @@ namespace {
 // fp32 hidden inputs travel raw, with their row normalisation beside them
 // (slot_s, act_s); bf16 layers normalise their input into their own scratch.
 struct PipeScratch {
-  std::vector<StepScratch> step;    // per layer (pipelined) or one shared (sequential)
+  std::vector<StepScratch> step;    // per layer (pipelined); sequential: steps, re-forward
   std::vector<float *> slot[2];     // pipelined: [l] input slots of layer l (l >= 1)
   std::vector<float *> slot_s[2];   // pipelined, fp32: [l] row normalisation of slot[.][l]
   float *act[2] = {nullptr, nullptr};    // sequential: whole-set activations, ping-pong
@@ -922,8 +922,10 @@ void carve_pipe(Carver &cv, PipeScratch &p, const ff_layer *layers, int L, int n
       max_in = std::max(max_in, layers[l].d_in);
       max_out = std::max(max_out, layers[l].d_out);
     }
-    p.step.assign(1, StepScratch());
+    p.step.assign(2, StepScratch());
     carve_step(cv, p.step[0], rows, max_in, max_out, dtype, true, false, false, po_classes);
+    // the forward pass with the final weights, run beside the next layer's steps
+    carve_step(cv, p.step[1], rows, max_in, max_out, dtype, false, false, false);
     int max_hidden = 0;
     for (int l = 0; l + 1 < L; ++l) max_hidden = std::max(max_hidden, layers[l].d_out);
     if (L > 1)
@@ -971,34 +973,53 @@ ff_status epoch_core(ff_layer *layers, int n_layers, const ff_hparams *hp, int n
   };
 
   if (schedule == FF_SEQUENTIAL) {
+    // Layer l's steps run on streams[0].  The forward pass with layer l-1's
+    // final weights, which gives layer l its input, runs chunk by chunk on
+    // streams[1] (when there is one) beside layer l's steps: step q waits only
+    // for the chunk it reads, and the pass starts once layer l-1's last step
+    // is done.  The same kernels on the same data as on one stream.
     hipStream_t st = static_cast<hipStream_t>(streams[0]);
+    hipStream_t fs = n_layers > 1 && streams[1] ? static_cast<hipStream_t>(streams[1]) : st;
+    EventRing evs;  // [0]: layer l-1's steps done; [1]: a chunk of its forward pass done
+    if (fs != st) {
+      evs.ev.assign(2, nullptr);
+      for (auto &e : evs.ev) FF_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    }
+    auto input_of = [&](int l, int start, int b) {
+      if (l == 0) return input0(start, b);
+      const float *in_s = p.act_s[(l - 1) & 1];
+      return raw_rows(p.act[(l - 1) & 1] + (size_t)rpp * start * layers[l].d_in,
+                      in_s ? in_s + (size_t)rpp * start : nullptr);
+    };
+    // forward pass of layer l over chunk c into layer l+1's input
+    auto reforward = [&](int l, int c, hipStream_t s) -> ff_status {
+      int start, b;
+      chunk_map(c, start, b);
+      float *out_s = p.act_s[l & 1];
+      return forward_core(&layers[l], hp, input_of(l, start, b), rpp * b,
+                          p.act[l & 1] + (size_t)rpp * start * layers[l].d_out, nullptr,
+                          out_s ? out_s + (size_t)rpp * start : nullptr, p.step[1], s);
+    };
     for (int l = 0; l < n_layers; ++l) {
-      ff_layer *L = &layers[l];
-      const float *in = l == 0 ? nullptr : p.act[(l - 1) & 1];
-      const float *in_s = l == 0 ? nullptr : p.act_s[(l - 1) & 1];
-      auto input = [&](int start, int b) {
-        if (l == 0) return input0(start, b);
-        return raw_rows(in + (size_t)rpp * start * L->d_in,
-                        in_s ? in_s + (size_t)rpp * start : nullptr);
-      };
+      const bool overlap = l > 0 && fs != st;
+      if (overlap) {
+        FF_HIP(hipEventRecord(evs.ev[0], st));  // layer l-1's last step
+        FF_HIP(hipStreamWaitEvent(fs, evs.ev[0], 0));
+      }
       for (int q = 0; q < steps; ++q) {
         int start, b;
         chunk_map(q % nc, start, b);
-        FF_TRY(step(l, input(start, b), start, b, nullptr,
+        if (overlap && q < nc) {
+          FF_TRY(reforward(l - 1, q, fs));
+          FF_HIP(hipEventRecord(evs.ev[1], fs));
+          FF_HIP(hipStreamWaitEvent(st, evs.ev[1], 0));
+        }
+        FF_TRY(step(l, input_of(l, start, b), start, b, nullptr,
                     loss_trace ? loss_trace + (size_t)l * steps + q : nullptr, nullptr, p.step[0],
                     st));
       }
-      if (l + 1 < n_layers) {
-        float *out = p.act[l & 1];
-        float *out_s = p.act_s[l & 1];
-        for (int c = 0; c < nc; ++c) {
-          int start, b;
-          chunk_map(c, start, b);
-          FF_TRY(forward_core(L, hp, input(start, b), rpp * b,
-                              out + (size_t)rpp * start * L->d_out, nullptr,
-                              out_s ? out_s + (size_t)rpp * start : nullptr, p.step[0], st));
-        }
-      }
+      if (l + 1 < n_layers && fs == st)
+        for (int c = 0; c < nc; ++c) FF_TRY(reforward(l, c, st));
     }
     return FF_OK;
   }

@@ -352,6 +352,22 @@ def test_pipeline_schedule_invariance_bitwise(P):
         np.testing.assert_array_equal(_np(x.W), _np(z.W))
 
 
+def test_sequential_reforward_beside_next_layer_bitwise(P):
+    """The sequential schedule's forward pass with a trained layer's final
+    weights runs on a second stream beside the next layer's steps: the same
+    result, bit for bit, as with every layer on one stream (two epochs, so later
+    passes reuse the finished activities)."""
+    hp_kw = dict(theta=2.0, lr=0.03)
+    dims = (784, 256, 256, 256)
+    a, ta, _ = _pipe(P, 0, 1500, dims, 256, 2, 81, hp_kw)
+    s = torch.cuda.current_stream()
+    b, tb, _ = _pipe(P, 0, 1500, dims, 256, 2, 81, hp_kw, streams=[s] * len(dims[1:]))
+    np.testing.assert_array_equal(ta, tb)
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(_np(x.W), _np(y.W))
+        np.testing.assert_array_equal(_np(x.b), _np(y.b))
+
+
 def test_pipeline_full_size_bench_config(P):
     """The timed training epoch at its full size and launch configuration (60 000
     pairs, 784->2000x4, chunks of 1024+1024 rows, one stream per layer).  Each
