@@ -889,10 +889,13 @@ ff_status ff_head_predict(const ff_layer *layers, int32_t n_layers, int32_t firs
 namespace {
 // fp32 hidden inputs travel raw, with their row normalisation beside them
 // (slot_s, act_s); bf16 layers normalise their input into their own scratch.
+// Input slots per layer boundary of the pipelined schedule: layer l may run
+// this many chunks ahead of layer l+1.
+constexpr int kPipeSlots = 3;
 struct PipeScratch {
   std::vector<StepScratch> step;    // per layer (pipelined); sequential: steps, re-forward
-  std::vector<float *> slot[2];     // pipelined: [l] input slots of layer l (l >= 1)
-  std::vector<float *> slot_s[2];   // pipelined, fp32: [l] row normalisation of slot[.][l]
+  std::vector<float *> slot[kPipeSlots];    // pipelined: [l] input slots of layer l (l >= 1)
+  std::vector<float *> slot_s[kPipeSlots];  // pipelined, fp32: row normalisation of slot[.][l]
   float *act[2] = {nullptr, nullptr};    // sequential: whole-set activations, ping-pong
   float *act_s[2] = {nullptr, nullptr};  // sequential, fp32: their row normalisation
 };
@@ -904,7 +907,7 @@ void carve_pipe(Carver &cv, PipeScratch &p, const ff_layer *layers, int L, int n
   const int rows = rpp * std::min(chunk, n);
   if (sched == FF_PIPELINED) {
     p.step.assign(L, StepScratch());
-    for (int k = 0; k < 2; ++k) {
+    for (int k = 0; k < kPipeSlots; ++k) {
       p.slot[k].assign(L, nullptr);
       p.slot_s[k].assign(L, nullptr);
     }
@@ -912,7 +915,7 @@ void carve_pipe(Carver &cv, PipeScratch &p, const ff_layer *layers, int L, int n
       carve_step(cv, p.step[l], rows, l == 0 || dtype == FF_BF16 ? layers[l].d_in : 0,
                  layers[l].d_out, dtype, l + 1 == L, false, false, po_classes);
     for (int l = 1; l < L; ++l)
-      for (int k = 0; k < 2; ++k) {
+      for (int k = 0; k < kPipeSlots; ++k) {
         p.slot[k][l] = static_cast<float *>(cv.take((size_t)rows * layers[l].d_in * 4));
         if (dtype == FF_F32) p.slot_s[k][l] = static_cast<float *>(cv.take((size_t)rows * 4));
       }
@@ -1026,10 +1029,12 @@ ff_status epoch_core(ff_layer *layers, int n_layers, const ff_hparams *hp, int n
 
   // Pipelined: done[l][q % kRing] marks layer l's step q complete.  Layer l's
   // step q waits for layer l-1's step q (its input slot is filled) and, before
-  // it overwrites layer l+1's slot q%2, for layer l+1's step q-2 (the slot's
-  // previous reader).  Both waits are enqueued before the event is recorded
-  // again kRing steps later, so a ring of 4 events per layer suffices.
+  // it overwrites layer l+1's slot q % kPipeSlots, for layer l+1's step
+  // q - kPipeSlots (the slot's previous reader).  Both waits are enqueued
+  // before the event they name is recorded again (kRing >= kPipeSlots steps
+  // later, and layer l+1's record of a step follows layer l's in host order).
   constexpr int kRing = 4;
+  static_assert(kRing >= kPipeSlots, "event ring");
   EventRing ring;
   ring.ev.assign((size_t)n_layers * kRing, nullptr);
   for (auto &e : ring.ev) FF_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
@@ -1040,14 +1045,15 @@ ff_status epoch_core(ff_layer *layers, int n_layers, const ff_hparams *hp, int n
       ff_layer *L = &layers[l];
       hipStream_t st = static_cast<hipStream_t>(streams[l]);
       if (l > 0) FF_HIP(hipStreamWaitEvent(st, ring.ev[(size_t)(l - 1) * kRing + q % kRing], 0));
-      if (l + 1 < n_layers && q >= 2)
-        FF_HIP(hipStreamWaitEvent(st, ring.ev[(size_t)(l + 1) * kRing + (q - 2) % kRing], 0));
-      const LayerInput in = l == 0 ? input0(start, b)
-                                   : raw_rows(p.slot[q & 1][l], p.slot_s[q & 1][l]);
+      if (l + 1 < n_layers && q >= kPipeSlots)
+        FF_HIP(hipStreamWaitEvent(
+            st, ring.ev[(size_t)(l + 1) * kRing + (q - kPipeSlots) % kRing], 0));
+      const int k = q % kPipeSlots;
+      const LayerInput in = l == 0 ? input0(start, b) : raw_rows(p.slot[k][l], p.slot_s[k][l]);
       const bool next = l + 1 < n_layers;
-      FF_TRY(step(l, in, start, b, next ? p.slot[q & 1][l + 1] : nullptr,
+      FF_TRY(step(l, in, start, b, next ? p.slot[k][l + 1] : nullptr,
                   loss_trace ? loss_trace + (size_t)l * steps + q : nullptr,
-                  next ? p.slot_s[q & 1][l + 1] : nullptr, p.step[l], st));
+                  next ? p.slot_s[k][l + 1] : nullptr, p.step[l], st));
       FF_HIP(hipEventRecord(ring.ev[(size_t)l * kRing + q % kRing], st));
     }
   }
