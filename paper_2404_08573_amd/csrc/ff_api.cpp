@@ -439,7 +439,7 @@ ffk::RowMap rows_of(const float *x) {
   return m;
 }
 
-constexpr int kScoreBlockImages = 2048;  // images per scoring pass (rows = images * classes)
+constexpr int kScoreBlockImages = 8192;  // images per scoring pass (rows = images * classes)
 
 }  // namespace
 
