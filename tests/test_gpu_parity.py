@@ -184,11 +184,13 @@ def test_score_parity_tiny_config(P, first):
 
 
 def test_score_ragged_blocks_and_tiny(P):
-    """More images than one scoring pass holds (ragged last pass), odd label count."""
-    x_base, _, _ = make_data(60, 2101, 24, 0.5)
+    """More images than one scoring pass holds (8192 inputs; a ragged last pass of
+    5), odd label count."""
+    n = 8197
+    x_base, _, _ = make_data(60, n, 24, 0.5)
     params = make_weights(61, (24, 36, 20))
     layers = [P.Layer(_t(W), _t(b)) for W, b in params]
-    S = torch.empty(2101, 7, device=DEV)
+    S = torch.empty(n, 7, device=DEV)
     _, pred = P.ff_score_labels(layers, P.HParams(), _t(x_base), 7, 0, scores=S)
     S_ref, p_ref = O.score_labels([O.Layer.from_params(W, b) for W, b in params], x_base, 7,
                                   O.HParams(), 0)
