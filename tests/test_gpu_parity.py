@@ -52,7 +52,8 @@ def test_embed_labels_exact(P, rows, d, C):
 # small shapes take the 64x64 tile, the last two the 128x128 tile (ragged in rows,
 # columns and depth)
 FWD_SHAPES = [(1, 12, 8), (130, 44, 132), (300, 200, 260), (1024, 784, 500), (257, 784, 2000),
-              (129, 2000, 136), (2100, 788, 2004), (2048, 2000, 2000)]
+              (129, 2000, 136), (2100, 788, 2004), (2048, 2000, 2000),
+              (37, 4, 20), (300, 16384, 136)]  # the narrowest input; a wide one (large offsets)
 
 
 @pytest.mark.parametrize("rows,d_in,d_out", FWD_SHAPES)
@@ -199,6 +200,20 @@ def test_score_ragged_blocks_and_tiny(P):
     _, p1 = P.ff_score_labels(layers, P.HParams(), _t(x_base[:1]), 7, 1)
     assert _np(p1)[0] == O.score_labels([O.Layer.from_params(W, b) for W, b in params],
                                         x_base[:1], 7, O.HParams(), 1)[1][0]
+
+
+def test_score_single_label(P):
+    """One candidate label: every prediction is label 0 and each score is the
+    goodness of the one embedding."""
+    x_base, _, _ = make_data(62, 300, 48, 0.5)
+    params = make_weights(63, (48, 64, 40))
+    layers = [P.Layer(_t(W), _t(b)) for W, b in params]
+    S = torch.empty(300, 1, device=DEV)
+    _, pred = P.ff_score_labels(layers, P.HParams(), _t(x_base), 1, 0, scores=S)
+    S_ref, p_ref = O.score_labels([O.Layer.from_params(W, b) for W, b in params], x_base, 1,
+                                  O.HParams(), 0)
+    assert_goodness(_np(S), S_ref, what="scores")
+    assert (_np(pred) == 0).all() and (p_ref == 0).all()
 
 
 @pytest.mark.parametrize("n_classes,first", [(16, 0), (17, 1), (20, 0)])
@@ -437,7 +452,9 @@ def test_tiny_config_end_to_end(P):
 # The last two select the 256x256 and 256x192 bf16 tiles (grids of at least one
 # tile per CU), with ragged row, column and k tails.
 BF16_FWD_SHAPES = [(1, 16, 8), (300, 200, 260), (2048, 784, 2000), (2100, 2000, 2004),
-                   (4200, 72, 4100), (4100, 136, 3000)]
+                   (4200, 72, 4100), (4100, 136, 3000),
+                   (37, 8, 20), (300, 16384, 136),  # the narrowest input; a wide one
+                   (8192, 520, 1000)]  # two 128x128 workgroups per CU (two LDS stages)
 
 
 @pytest.mark.parametrize("rows,d_in,d_out", BF16_FWD_SHAPES)
