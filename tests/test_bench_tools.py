@@ -1,0 +1,108 @@
+"""CPU checks of bench.py's measurement plumbing: the rocprofv3 counter
+summaries, the copy calibration of the traffic counters, the kernel-source gate
+on stored traffic, and the one-GPU guard."""
+import csv
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+FIELDS = ["Correlation_Id", "Dispatch_Id", "Agent_Id", "Queue_Id", "Process_Id", "Thread_Id",
+          "Grid_Size", "Kernel_Id", "Kernel_Name", "Workgroup_Size", "LDS_Block_Size",
+          "Scratch_Size", "VGPR_Count", "Accum_VGPR_Count", "SGPR_Count", "Counter_Name",
+          "Counter_Value", "Start_Timestamp", "End_Timestamp"]
+
+
+def _csv(path, rows):
+    """rows: (dispatch id, kernel name, counter, value)"""
+    with open(path, "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=FIELDS)
+        w.writeheader()
+        for d, name, counter, value in rows:
+            r = {k: 0 for k in FIELDS}
+            r.update(Dispatch_Id=d, Correlation_Id=d, Kernel_Name=name, Counter_Name=counter,
+                     Counter_Value=value, Agent_Id="Agent 1")
+            w.writerow(r)
+    return str(path)
+
+
+FWD = "void ffk::(anonymous namespace)::k_fwd<false, 128, 128, 4, 2, 2, true>(...)"
+DW = "void ffk::(anonymous namespace)::k_dw_adam_f32<64, 128, 32, 2, 4, 3, true>(...)"
+COPY = "__amd_rocclr_copyBuffer"
+
+
+def test_counter_per_dispatch_and_largest(tmp_path):
+    p = _csv(tmp_path / "c.csv", [(1, FWD, "FETCH_SIZE", 100.0), (2, FWD, "FETCH_SIZE", 200.0),
+                                  (3, DW, "FETCH_SIZE", 50.0), (4, COPY, "FETCH_SIZE", 7.0),
+                                  (5, COPY, "FETCH_SIZE", 3000.0), (5, FWD, "WRITE_SIZE", 9.0)])
+    per, n = bench._counter_per_dispatch(p, "FETCH_SIZE")
+    assert per["forward"] == pytest.approx(150.0) and n["forward"] == 2
+    assert per["dw_adam"] == pytest.approx(50.0) and n["dw_adam"] == 1
+    assert bench._largest_dispatch(p, "FETCH_SIZE") == 3000.0
+
+
+def test_traffic_summary_scales_by_the_copy(tmp_path, monkeypatch):
+    """A 1 GiB copy that reads FETCH_SIZE = 0.5 GiB and WRITE_SIZE = 1 GiB
+    scales fetches by 2 and writes by 1."""
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "feedc0de01234567")
+    os.makedirs(tmp_path / "profiles")
+    gib_kib = float(1 << 20)
+    f = _csv(tmp_path / "f.csv", [(1, FWD, "FETCH_SIZE", 1000.0), (2, FWD, "FETCH_SIZE", 3000.0)])
+    w = _csv(tmp_path / "w.csv", [(1, FWD, "WRITE_SIZE", 500.0), (2, FWD, "WRITE_SIZE", 500.0)])
+    cf = _csv(tmp_path / "cf.csv", [(1, COPY, "FETCH_SIZE", gib_kib / 2)])
+    cw = _csv(tmp_path / "cw.csv", [(1, COPY, "WRITE_SIZE", gib_kib)])
+    bench.traffic_summary(f, w, cf, cw, "wl", 1 << 30)
+    t = json.load(open(tmp_path / "profiles" / "traffic.json"))
+    assert t["fetch_factor"] == pytest.approx(2.0) and t["write_factor"] == pytest.approx(1.0)
+    e = t["wl"]["forward"]
+    assert e["fetch_bytes_per_launch"] == pytest.approx(2000.0 * 1024 * 2)
+    assert e["write_bytes_per_launch"] == pytest.approx(500.0 * 1024)
+    assert e["kernel_source_sha256_16"] == "feedc0de01234567"
+
+
+def test_stored_traffic_only_for_the_same_kernel_source(tmp_path, monkeypatch):
+    assert len(bench.kernel_source_hash()) == 16  # of the real kernel file
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "feedc0de01234567")
+    os.makedirs(tmp_path / "profiles")
+    path = tmp_path / "profiles" / "traffic.json"
+    entry = {"bytes_per_launch": 123.0, "kernel_source_sha256_16": bench.kernel_source_hash()}
+    json.dump({"wl": {"forward": entry}}, open(path, "w"))
+    assert bench.load_traffic("forward", "wl") == 123.0
+    entry["kernel_source_sha256_16"] = "0" * 16
+    json.dump({"wl": {"forward": entry}}, open(path, "w"))
+    assert bench.load_traffic("forward", "wl") is None
+    assert bench.load_traffic("dw_adam", "wl") is None
+
+
+def test_counter_summary_mfma_busy(tmp_path, capsys):
+    """Half of the 1024 SIMDs' cycles busy over a GPU-active time of 1000
+    cycles per XCD (8 XCDs summed) reads as 50 % MFMA busy."""
+    d = tmp_path / "focus_1_2_3_0"
+    os.makedirs(d)
+    p = _csv(d / "run_counter_collection.csv",
+             [(1, FWD, "SQ_VALU_MFMA_BUSY_CYCLES", 1024 * 1000 * 0.5),
+              (1, FWD, "GRBM_GUI_ACTIVE", 8 * 1000.0), (1, FWD, "SQ_WAVE_CYCLES", 200.0),
+              (1, FWD, "SQ_WAIT_ANY", 50.0), (1, FWD, "SQ_WAIT_INST_LDS", 10.0),
+              (1, FWD, "SQ_INSTS_LDS", 100.0), (1, FWD, "SQ_LDS_BANK_CONFLICT", 5.0)])
+    bench.counter_summary([p])
+    out = capsys.readouterr().out
+    row = [ln for ln in out.splitlines() if "forward" in ln][0]
+    cells = [c.strip() for c in row.strip("|").split("|")]
+    assert cells[0] == "focus_1_2_3_0" and cells[2] == "1"
+    assert cells[3] == "50.0 %" and cells[4] == "25.0 %" and cells[5] == "5.0 %"
+    assert cells[6] == "0.050"
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
