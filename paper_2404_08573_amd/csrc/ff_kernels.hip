@@ -247,8 +247,14 @@ __device__ __forceinline__ void rowsum_scatter(float (&v)[NV], int lane) {
     const bool hi = (lane & o) != 0;
 #pragma unroll
     for (int q = 0; q < half; ++q) {
-      const float send = hi ? v[q] : v[q + half];
-      const float keep = hi ? v[q + half] : v[q];
+      float lo = v[q], up = v[q + half];
+      // Both halves as register values before the selects: left as selects
+      // between array elements, they were compiled as indexed accesses into
+      // the whole array (a 500-instruction select network per kernel, or the
+      // array moved out of registers).
+      asm volatile("" : "+v"(lo), "+v"(up));
+      const float send = hi ? lo : up;
+      const float keep = hi ? up : lo;
       v[q] = keep + __shfl_xor(send, o);
     }
   }
