@@ -621,6 +621,220 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16
 }
 
 // ---------------------------------------------------------------------------
+// bf16 forward on four waves of 128 x (BN/2) each (one wave per SIMD).
+// The 8-wave tiles above give each wave a 32x64 or 64x96 share, whose MFMA
+// fragments cost more LDS read bytes per flop than the CU's LDS delivers at
+// the bf16 MFMA rate.  A 128x96 wave tile needs 7 fragment reads per 12
+// MFMAs.  Its 192 accumulators live in AGPRs, so one wave fills a SIMD and
+// must hide its own latencies:
+//   * fragments are double-buffered in registers: the reads of k-step s+1
+//     are issued one beside each MFMA of k-step s (sched_group_barrier);
+//   * one barrier per 64-deep k-tile, placed after the first MFMA of its last
+//     k-step, so the MFMA pipe is busy while the waves meet;
+//   * after that barrier, the loads of k-tile t+2 and the first fragments of
+//     k-tile t+1 are issued one slot per MFMA of the rest of that k-step.
+// Same operand layout, k permutation, swizzle and zero-filled tails as
+// nt_mainloop with two LDS stages; same epilogue results as k_fwd.
+// ---------------------------------------------------------------------------
+// s_waitcnt operand: no vector-memory or LDS operation outstanding.
+constexpr int kWaitAll = 0x0070;
+
+template <int BM, int BN>
+__device__ __forceinline__ void nt_mainloop4(const uint16_t *__restrict__ X,
+                                             const uint16_t *__restrict__ W, int M, int N, int K,
+                                             int m0, int n0, uint16_t *sm,
+                                             floatx16 (&acc)[BM / 64][BN / 64]) {
+  constexpr int VE = 8, ES = 2, BK = 64, NW = 4, WN = 2;
+  constexpr int TM = BM / 2, TN = BN / 2, MB = TM / 32, NB = TN / 32;
+  constexpr int IA = BM / 8 / NW, IB = BN / 8 / NW;  // 8-row wave loads per k-tile
+  constexpr int STAGE = (BM + BN) * BK;
+  constexpr int KS = BK / 2 / VE;  // 16-deep k-steps per k-tile
+  constexpr int NM = MB * NB - 1, ND = MB + NB, NV = IA + IB;
+  static_assert(MB * 32 == TM && NB * 32 == TN && IA * 8 * NW == BM && IB * 8 * NW == BN,
+                "tile shape");
+  static_assert(ND <= NM && KS % 2 == 0, "a fragment read per MFMA");
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int li = lane & 31, kg = lane >> 5;
+  const __amdgpu_buffer_rsrc_t ra =
+      buffer_rsrc(X + (size_t)m0 * K, (uint32_t)(min(BM, M - m0) * K * ES));
+  const __amdgpu_buffer_rsrc_t rb =
+      buffer_rsrc(W + (size_t)n0 * K, (uint32_t)(min(BN, N - n0) * K * ES));
+  const int lpos = lane & 7;
+  int kca[IA], kcb[IB];
+  uint32_t oa[IA], ob[IB];
+#pragma unroll
+  for (int i = 0; i < IA; ++i) {
+    const int r = (wave * IA + i) * 8 + (lane >> 3);
+    kca[i] = nt_swz(r, lpos) * VE;
+    oa[i] = (uint32_t)((r * K + kca[i]) * ES);
+  }
+#pragma unroll
+  for (int i = 0; i < IB; ++i) {
+    const int r = (wave * IB + i) * 8 + (lane >> 3);
+    kcb[i] = nt_swz(r, lpos) * VE;
+    ob[i] = (uint32_t)((r * K + kcb[i]) * ES);
+  }
+  // Load j of k-tile kt into stage buf: 8 rows of the X tile for j < IA, else
+  // 8 rows of the W tile.
+  auto issue1 = [&](int kt, int buf, int j) {
+    uint16_t *As = sm + buf * STAGE;
+    const int kb = kt * BK;
+    if (j < IA) {
+      const uint32_t o = kb + kca[j] < K ? oa[j] + kb * ES : kOutOfRange;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void *)(As + (wave * IA + j) * 8 * BK), 16,
+                                               o, 0, 0, 0);
+    } else {
+      const int i = j - IA;
+      const uint32_t o = kb + kcb[i] < K ? ob[i] + kb * ES : kOutOfRange;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rb, (lds_void *)(As + BM * BK + (wave * IB + i) * 8 * BK), 16, o, 0, 0, 0);
+    }
+  };
+  // LDS offsets (elements) of the lane's fragment rows in stage 0.
+  int pa[MB], pb[NB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) pa[mb] = (wm * TM + mb * 32 + li) * BK;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) pb[nb] = BM * BK + (wn * TN + nb * 32 + li) * BK;
+  // Fragment i of k-step ks from stage buf: X block i for i < MB, else W block i - MB.
+  auto rd1 = [&](int buf, int ks, int i, uint4 (&a)[MB], uint4 (&b)[NB]) {
+    const uint16_t *S = sm + buf * STAGE;
+    const int c = kg * KS + ks;
+    if (i < MB)
+      a[i] = ld16(S + pa[i] + nt_swz(i * 32 + li, c) * VE);
+    else
+      b[i - MB] = ld16(S + pb[i - MB] + nt_swz((i - MB) * 32 + li, c) * VE);
+  };
+  auto mm = [&](int mb, int nb, const uint4 &a, const uint4 &b) {
+    acc[mb][nb] =
+        __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf8(a), as_bf8(b), acc[mb][nb], 0, 0, 0);
+  };
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mb][nb][r] = 0.f;
+
+  uint4 fa[2][MB], fb[2][NB];
+  const int nk = (K + BK - 1) / BK;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) issue1(0, 0, j);
+#pragma unroll
+  for (int j = 0; j < NV; ++j) issue1(1, 1, j);
+  __builtin_amdgcn_s_waitcnt(vmcnt_wait(NV));
+  lds_barrier();
+#pragma unroll
+  for (int i = 0; i < ND; ++i) rd1(0, 0, i, fa[0], fb[0]);
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int cur = ks & 1, nxt = cur ^ 1;
+      if (ks + 1 < KS) {
+#pragma unroll
+        for (int i = 0; i < ND; ++i) rd1(buf, ks + 1, i, fa[nxt], fb[nxt]);
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) mm(mb, nb, fa[cur][mb], fb[cur][nb]);
+        // One fragment read beside each MFMA, the rest of the MFMAs after.
+#pragma unroll
+        for (int i = 0; i < ND; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, MB * NB - ND, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      } else {
+        mm(0, 0, fa[cur][0], fb[cur][0]);
+        __builtin_amdgcn_sched_barrier(0);
+        // Every fragment of k-tile kt is in registers and k-tile kt + 1 has
+        // landed: one barrier opens kt + 1 and frees kt's stage for kt + 2.
+        __builtin_amdgcn_s_waitcnt(kWaitAll);
+        lds_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        // Slots of (loads, one fragment read, one MFMA), kept in this order.
+#pragma unroll
+        for (int i = 0; i < NM; ++i) {
+#pragma unroll
+          for (int j = (i * NV) / NM; j < ((i + 1) * NV) / NM; ++j) issue1(kt + 2, buf, j);
+          if (i < ND) rd1(buf ^ 1, 0, i, fa[nxt], fb[nxt]);
+          const int p = i + 1;
+          mm(p / NB, p % NB, fa[cur][p / NB], fb[cur][p % NB]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
+  lds_barrier();
+}
+
+template <int BM, int BN, bool STORE_H>
+__global__ __launch_bounds__(256) void k_fwd4(const uint16_t *__restrict__ X,
+                                              const uint16_t *__restrict__ W,
+                                              const float *__restrict__ bias,
+                                              const float *__restrict__ rowscale, int M, int N,
+                                              int K, float *__restrict__ H,
+                                              float *__restrict__ gpart) {
+  constexpr int WN = 2, TM = BM / 2, TN = BN / 2, MB = TM / 32, NB = TN / 32;
+  __shared__ __attribute__((aligned(16))) uint16_t sm[2 * (BM + BN) * 64];
+  const int nt = (N + BN - 1) / BN;
+  int tm, tn;
+  tile_of(blockIdx.x, (M + BM - 1) / BM, nt, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int li = lane & 31, kg = lane >> 5;
+  floatx16 acc[MB][NB];
+  nt_mainloop4<BM, BN>(X, W, M, N, K, m0, n0, sm, acc);
+
+  // Epilogue as in k_fwd, one 32-row block at a time, so that only 16 row
+  // sums and scales are live beside the accumulators.
+  float bv[NB];
+  bool cok[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int col = n0 + wn * TN + nb * 32 + li;
+    cok[nb] = col < N;
+    bv[nb] = cok[nb] ? bias[col] : 0.f;
+  }
+  float *gs = reinterpret_cast<float *>(sm);  // [WN][BM]; the main-loop buffers are free now
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    float hsq[16], rs[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      hsq[r] = 0.f;
+      rs[r] = rowscale ? rowscale[min(m0 + wm * TM + mb * 32 + acc_row(r, kg), M - 1)] : 1.f;
+    }
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int col = n0 + wn * TN + nb * 32 + li;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float h = cok[nb] ? fmaxf(fmaf(acc[mb][nb][r], rs[r], bv[nb]), 0.f) : 0.f;
+        if (STORE_H) {
+          const int row = m0 + wm * TM + mb * 32 + acc_row(r, kg);
+          if (row < M && cok[nb]) H[(size_t)row * N + col] = h;
+        }
+        hsq[r] += h * h;
+      }
+    }
+    rowsum_scatter(hsq, lane);
+    const int q = (lane & 31) >> 1;
+    if ((lane & 1) == 0) gs[wn * BM + wm * TM + mb * 32 + acc_row(q, kg)] = hsq[0];
+  }
+  __syncthreads();
+  for (int t = tid; t < BM; t += 256) {
+    const int row = m0 + t;
+    if (row < M) gpart[(size_t)tn * M + row] = gs[t] + gs[BM + t];
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Shared-base layer-0 forward.  Every label embedding of an input row has the
 // same norm (one label feature is 1), so with x_hat = s * (masked row + e_label)
 // the product splits into P = X_masked_hat W^T, computed once per base row on
@@ -1514,8 +1728,10 @@ using DwSmallBf16 = Tile<64, 64, 64, 2, 2, 2>;
 // an fp32 one, too little to cover a load's latency with one tile in flight,
 // so a bf16 grid of fewer than two 128x128 workgroups per CU (Full) takes
 // three stages instead, as does the small tile.  bf16 products use the larger
-// tiles for operand reuse when the grid allows; fp32 measured no faster above
-// 128x128.
+// tiles for operand reuse when the grid allows: 256x192 on the four-wave
+// kernel (one workgroup per CU) when its grid fills the CUs, and 256x256 on
+// eight waves only from two of its tiles per CU on, where it measured faster.
+// fp32 measured no faster above 128x128.
 template <bool BF16>
 struct FwdTiles;
 template <>
@@ -1529,7 +1745,7 @@ struct FwdTiles<false> {
 template <>
 struct FwdTiles<true> {
   using Huge = Tile<256, 256, 64, 4, 2, 2>;
-  using Large = Tile<256, 192, 64, 4, 2, 2>;
+  using Large = Tile<256, 192, 64, 2, 2, 2>;  // four-wave kernel (k_fwd4)
   using Big = Tile<128, 128, 64, 4, 2, 2>;
   using Full = Tile<128, 128, 64, 4, 2, 3>;
   using Small = Tile<64, 64, 64, 2, 2, 3>;
@@ -1544,7 +1760,7 @@ template <bool BF16, bool LARGE = true, class F>
 void fwd_tile(int M, int N, F &&f) {
   using L = FwdTiles<BF16>;
   if constexpr (LARGE) {
-    if (L::Huge::tiles(M, N) >= kCUs) return f(TileTag<typename L::Huge>{});
+    if (L::Huge::tiles(M, N) >= (BF16 ? 2 : 1) * kCUs) return f(TileTag<typename L::Huge>{});
     if (L::Large::tiles(M, N) >= kCUs) return f(TileTag<typename L::Large>{});
   }
   if (L::Big::tiles(M, N) >= 2 * kCUs) return f(TileTag<typename L::Big>{});
@@ -1628,12 +1844,21 @@ void fwd_launch(const void *x, const void *w, const float *bias, const float *ro
   const E *xe = static_cast<const E *>(x);
   const E *we = static_cast<const E *>(w);
   static_assert(T::bk == nt_bk<BF16>(), "forward k-tile is 128 bytes");
-  if (H)
+  if constexpr (BF16 && T::threads == 256 && T::bm == 256) {
+    static_assert(T::wm == 2 && T::wn == 2 && T::pf == 2, "four-wave tile");
+    if (H)
+      hipLaunchKernelGGL((k_fwd4<T::bm, T::bn, true>), grid, dim3(256), 0, s, xe, we, bias,
+                         rowscale, M, N, K, H, gpart);
+    else
+      hipLaunchKernelGGL((k_fwd4<T::bm, T::bn, false>), grid, dim3(256), 0, s, xe, we, bias,
+                         rowscale, M, N, K, H, gpart);
+  } else if (H) {
     hipLaunchKernelGGL((k_fwd<BF16, T::bm, T::bn, T::wm, T::wn, T::pf, true>), grid,
                        dim3(T::threads), 0, s, xe, we, bias, rowscale, M, N, K, H, gpart);
-  else
+  } else {
     hipLaunchKernelGGL((k_fwd<BF16, T::bm, T::bn, T::wm, T::wn, T::pf, false>), grid,
                        dim3(T::threads), 0, s, xe, we, bias, rowscale, M, N, K, H, gpart);
+  }
 }
 
 hipError_t launch_fwd(int dtype, const void *X, const void *W, const float *bias,

@@ -159,3 +159,36 @@ def test_planted_po_mistakes_fail(mistake):
         assert_weights(M.mW, L.mW, gW, mW, "mW")
         assert_weights(M.W, L.W, gW, mW, "W", lr=0.01)
         assert_weights(MH.b, Hd.b, [np.ones(10)], [np.ones(10)], "bc", lr=1e-3)
+
+
+def test_r1_slack_covers_fp32_normalisation():
+    """The bf16 goodness allowance for open R1 roundings (rows whose normalised
+    input has an element within 2^-18 of a bf16 rounding change) covers what an
+    fp32 normalisation does to the goodness, row by row, and is zero on every
+    other row.  The input is sparse and narrow, as in the bf16 forward test
+    where an fp32 normalisation moves a row by 1.2e-3."""
+    from parity import r1_goodness_slack
+    from ffinputs import random_matrix
+    rows, d_in, d_out = 4000, 72, 600
+    x = random_matrix(rows + 3 * d_in, rows, d_in, 0, 1, 0.6)
+    (W, b), = make_weights(d_out + 5, (d_in, d_out))
+    xh64 = O.l2_normalise(x, 1e-8)
+    _, _, h_ref, g_ref = O.layer_forward(W, b, x, 1e-8, bf16=True)
+    Wb = O.bf16_round(W)
+    slack = r1_goodness_slack(Wb, xh64, h_ref)
+    # the allowance is confined to rows with an open element
+    lo = O.bf16_round(xh64 * (1 - 2.0 ** -18))
+    hi = O.bf16_round(xh64 * (1 + 2.0 ** -18))
+    open_rows = (lo != hi).any(axis=1)
+    assert np.all(slack[~open_rows] == 0) and np.all(slack[open_rows] > 0)
+    assert 0 < open_rows.sum() < rows // 4
+    # every open element rounded the other way at once stays inside it
+    for other in (lo, hi):
+        _, _, _, g_alt = O.layer_forward(W, b, other, 1e-8, normalised=True, bf16=True)
+        assert np.all(np.abs(g_alt - g_ref) <= slack + 1e-12 * np.abs(g_ref))
+    # an fp32 normalisation (one summation order) passes the bar with it
+    x32 = x.astype(np.float32)
+    s32 = np.float32(1) / (np.sqrt((x32 * x32).sum(axis=1, dtype=np.float32)) + np.float32(1e-8))
+    xh32 = O.bf16_round((x32 * s32[:, None]).astype(np.float64))
+    _, _, _, g32 = O.layer_forward(W, b, xh32, 1e-8, normalised=True, bf16=True)
+    assert_goodness(g32, g_ref, rel=1e-3, slack=slack)
