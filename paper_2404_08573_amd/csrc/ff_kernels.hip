@@ -1548,16 +1548,25 @@ __global__ __launch_bounds__(kBlock) void k_po_dz(const float *__restrict__ H,
   if (j == 0) ones[r] = 1.f;
 }
 
-// One thread per 4 consecutive features and split of rows: C x 4 partial sums.
+// Classifier weight-gradient partials.  A workgroup covers 64 consecutive
+// features (16 float4 lanes) of one split of rows, with 16 row lanes walking
+// the split's rows 16 apart; each thread keeps C float4 sums, and the 16 row
+// lanes are reduced through LDS in a fixed order.  A split of 128 rows leaves
+// each thread 8 independent row loads, and a 1024-row step of 2000 features
+// has 256 workgroups (one thread per feature quad and split had left 16
+// workgroups walking 128 dependent rows each).
+constexpr int kHeadGradQuads = 16, kHeadGradRowLanes = kBlock / kHeadGradQuads;
 template <int CC>  // class-count bound, as in k_head_logits
 __global__ __launch_bounds__(kBlock) void k_head_grad(HeadFeatures hf,
                                                       const float *__restrict__ G, int n, int C,
                                                       int D, int rows_per_split,
                                                       float *__restrict__ part) {
-  const int f = 4 * (blockIdx.x * kBlock + threadIdx.x);
-  if (f >= D) return;
-  int j;
-  const int blk = head_block(hf, f, j);
+  __shared__ float4 red[kHeadGradRowLanes][CC][kHeadGradQuads];
+  const int q = threadIdx.x % kHeadGradQuads, rl = threadIdx.x / kHeadGradQuads;
+  const int f = 4 * (blockIdx.x * kHeadGradQuads + q);
+  const bool fok = f < D;
+  int j = 0;
+  const int blk = fok ? head_block(hf, f, j) : 0;
   const int d = hf.d[blk];
   const float *h = hf.h[blk] + j;
   const float *sv = hf.s[blk];  // null: scale 1
@@ -1565,25 +1574,41 @@ __global__ __launch_bounds__(kBlock) void k_head_grad(HeadFeatures hf,
   float4 acc[CC];
 #pragma unroll
   for (int c = 0; c < CC; ++c) acc[c] = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int r = r0; r < r1; ++r) {
-    float4 a = ld4(h + (size_t)r * d);
-    const float sr = sv ? sv[r] : 1.f;
-    a.x *= sr;
-    a.y *= sr;
-    a.z *= sr;
-    a.w *= sr;
+  if (fok) {
+    for (int r = r0 + rl; r < r1; r += kHeadGradRowLanes) {
+      float4 a = ld4(h + (size_t)r * d);
+      const float sr = sv ? sv[r] : 1.f;
+      a.x *= sr;
+      a.y *= sr;
+      a.z *= sr;
+      a.w *= sr;
 #pragma unroll
-    for (int c = 0; c < CC; ++c) {
-      const float g = G[(size_t)r * C + min(c, C - 1)];  // classes past C: never stored
-      acc[c].x += g * a.x;
-      acc[c].y += g * a.y;
-      acc[c].z += g * a.z;
-      acc[c].w += g * a.w;
+      for (int c = 0; c < CC; ++c) {
+        const float g = G[(size_t)r * C + min(c, C - 1)];  // classes past C: never stored
+        acc[c].x += g * a.x;
+        acc[c].y += g * a.y;
+        acc[c].z += g * a.z;
+        acc[c].w += g * a.w;
+      }
     }
   }
 #pragma unroll
-  for (int c = 0; c < CC; ++c)
-    if (c < C) st4(part + ((size_t)blockIdx.y * C + c) * D + f, acc[c]);
+  for (int c = 0; c < CC; ++c) red[rl][c][q] = acc[c];
+  __syncthreads();
+  for (int o = threadIdx.x; o < CC * kHeadGradQuads; o += kBlock) {
+    const int c = o / kHeadGradQuads, qq = o % kHeadGradQuads;
+    const int ff = 4 * (blockIdx.x * kHeadGradQuads + qq);
+    if (c >= C || ff >= D) continue;
+    float4 sum = red[0][c][qq];
+    for (int k = 1; k < kHeadGradRowLanes; ++k) {
+      const float4 v = red[k][c][qq];
+      sum.x += v.x;
+      sum.y += v.y;
+      sum.z += v.z;
+      sum.w += v.w;
+    }
+    st4(part + ((size_t)blockIdx.y * C + c) * D + ff, sum);
+  }
 }
 
 // Adam on the head.  Block 0 also reduces db and the loss over the rows: each
@@ -2019,8 +2044,9 @@ hipError_t launch_head_grad(const HeadFeatures &f, const float *G, int n, int C,
   if (C < 1 || C > kHeadMaxClasses || D % 4 || splits < 1) return hipErrorInvalidValue;
   const int rps = (int)cdiv(n, splits);
   head_classes(C, [&](auto cc) {
-    hipLaunchKernelGGL(k_head_grad<decltype(cc)::value>, dim3(cdiv(D / 4, kBlock), splits),
-                       dim3(kBlock), 0, s, f, G, n, C, D, rps, part);
+    hipLaunchKernelGGL(k_head_grad<decltype(cc)::value>,
+                       dim3(cdiv(D / 4, kHeadGradQuads), splits), dim3(kBlock), 0, s, f, G, n, C,
+                       D, rps, part);
   });
   return hipGetLastError();
 }
