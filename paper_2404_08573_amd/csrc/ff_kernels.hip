@@ -1752,7 +1752,8 @@ using DwSmallBf16 = Tile<64, 64, 64, 2, 2, 2>;
 // workgroups share a CU.  A bf16 k-tile holds a quarter of the MFMA time of
 // an fp32 one, too little to cover a load's latency with one tile in flight,
 // so a bf16 grid of fewer than two 128x128 workgroups per CU (Full) takes
-// three stages instead, as does the small tile.  bf16 products use the larger
+// three stages instead, as does the bf16 small tile (the fp32 one measured
+// faster with two: 1024x2000x2000, 88 -> 77 us).  bf16 products use the larger
 // tiles for operand reuse when the grid allows: 256x192 on the four-wave
 // kernel (one workgroup per CU) when its grid fills the CUs, and 256x256 on
 // eight waves only from two of its tiles per CU on, where it measured faster.
@@ -1765,7 +1766,7 @@ struct FwdTiles<false> {
   using Large = Huge;
   using Big = Huge;
   using Full = Huge;
-  using Small = Tile<64, 64, 32, 2, 2, 3>;
+  using Small = Tile<64, 64, 32, 2, 2, 2>;
 };
 template <>
 struct FwdTiles<true> {
