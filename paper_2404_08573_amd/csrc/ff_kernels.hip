@@ -303,6 +303,26 @@ __device__ __forceinline__ void lds_vec(const float *p, float (&out)[V]) {
   }
 }
 
+// Workgroup barrier that the compiler may not move memory accesses across.
+// The s_barrier builtin alone is no memory fence, so LDS reads of a tile could
+// be scheduled across it, and __syncthreads' workgroup fence would also wait
+// for every outstanding load into LDS (vmcnt(0)), draining the prefetch.  The
+// empty asm statements with a memory clobber pin the order at the compiler
+// level; the hardware order comes from the explicit s_waitcnt before it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// s_waitcnt operand: at most n vector-memory operations outstanding, no limit
+// on the other counters (gfx9 encoding: vmcnt in bits 3:0 and 15:14).
+constexpr int vmcnt_wait(int n) { return 0x0f70 | (n & 15) | ((n >> 4) << 14); }
+// s_waitcnt operands: nothing outstanding; no LDS (or scalar memory) operation
+// outstanding, any number of vector-memory ones.
+constexpr int kWaitAll = 0x0070;
+constexpr int kWaitLds = 0xc07f;
+
 // Software pipeline over nk k-tiles with double-buffered LDS and PF register
 // stages: the loads of tile t+PF are issued before the MFMAs of tile t, and
 // tile t+1 is written from its register stage to the other LDS buffer after
@@ -315,14 +335,24 @@ __device__ __forceinline__ void lds_vec(const float *p, float (&out)[V]) {
 // lcm(PF, 2) so that register stages and LDS buffers are fixed; each LDS
 // buffer is rewritten only after the barrier that ends the computation
 // reading it, and each register stage only after it has been written to LDS.
+//
+// The barrier after each LDS write waits for the thread's own LDS writes
+// only (lgkmcnt(0)): __syncthreads' workgroup fence would also wait for every
+// outstanding global load, the register stages of the next PF - 1 tiles, and
+// so cut the prefetch to the tile issued in the same iteration.
 template <int PF, class Load, class Store, class Compute, class Stage>
 __device__ __forceinline__ void kloop(int nk, Load &gload, Store &sstore, Compute &compute,
                                       Stage (&st)[PF]) {
   constexpr int U = PF % 2 == 0 ? PF : 2 * PF;
+  auto barrier = [] {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(kWaitLds);
+    lds_barrier();
+  };
 #pragma unroll
   for (int j = 0; j < PF; ++j) gload(st[j], j);
   sstore(st[0], 0);
-  __syncthreads();
+  barrier();
   int kt = 0;
   for (; kt + U <= nk; kt += U) {
 #pragma unroll
@@ -330,7 +360,7 @@ __device__ __forceinline__ void kloop(int nk, Load &gload, Store &sstore, Comput
       gload(st[j % PF], kt + j + PF);
       compute(j % 2);
       sstore(st[(j + 1) % PF], (j + 1) % 2);
-      __syncthreads();
+      barrier();
     }
   }
 #pragma unroll
@@ -339,9 +369,10 @@ __device__ __forceinline__ void kloop(int nk, Load &gload, Store &sstore, Comput
       gload(st[j % PF], kt + j + PF);
       compute(j % 2);
       sstore(st[(j + 1) % PF], (j + 1) % 2);
-      __syncthreads();
+      barrier();
     }
   }
+  __builtin_amdgcn_s_waitcnt(kWaitAll);  // the loads past the last tile, before the LDS is reused
 }
 
 // ---------------------------------------------------------------------------
@@ -397,21 +428,6 @@ constexpr uint32_t kOutOfRange = 0x80000000u;  // a buffer offset past every til
 // rows.  An involution for each r.
 __device__ __forceinline__ int nt_swz(int r, int c) { return c ^ (r & 7) ^ ((r >> 3) & 1); }
 
-// Workgroup barrier that the compiler may not move memory accesses across.
-// The s_barrier builtin alone is no memory fence, so LDS reads of a tile could
-// be scheduled across it, and __syncthreads' workgroup fence would also wait
-// for every outstanding load into LDS (vmcnt(0)), draining the prefetch.  The
-// empty asm statements with a memory clobber pin the order at the compiler
-// level; the hardware order comes from the explicit s_waitcnt before it.
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
-// s_waitcnt operand: at most n vector-memory operations outstanding, no limit
-// on the other counters (gfx9 encoding: vmcnt in bits 3:0 and 15:14).
-constexpr int vmcnt_wait(int n) { return 0x0f70 | (n & 15) | ((n >> 4) << 14); }
 
 // Main loop of C[m][n] = sum_k X[m][k] W[n][k] for the tile at (m0, n0), both
 // operands K-contiguous, into the wave's accumulators.
@@ -636,8 +652,6 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16
 // Same operand layout, k permutation, swizzle and zero-filled tails as
 // nt_mainloop with two LDS stages; same epilogue results as k_fwd.
 // ---------------------------------------------------------------------------
-// s_waitcnt operand: no vector-memory or LDS operation outstanding.
-constexpr int kWaitAll = 0x0070;
 
 template <int BM, int BN>
 __device__ __forceinline__ void nt_mainloop4(const uint16_t *__restrict__ X,
