@@ -69,6 +69,10 @@ def test_forward_parity(P, rows, d_in, d_out):
     _, _, h_ref, g_ref = O.layer_forward(W, b, x, 1e-8)
     assert_acts(_np(h), h_ref)
     assert_goodness(_np(g), g_ref)
+    # goodness only: the kernels' variant without the activity store
+    g2 = torch.empty(rows, device=DEV)
+    P.ff_layer_forward(L, P.HParams(), _t(x), goodness=g2)
+    assert_goodness(_np(g2), g_ref)
 
 
 def test_forward_prenormalised_input(P):
@@ -472,6 +476,10 @@ def test_forward_parity_bf16(P, rows, d_in, d_out):
     slack = r1_goodness_slack(O.bf16_round(W), O.l2_normalise(x, 1e-8), h_ref)
     assert_goodness(_np(g), g_ref, rel=1e-3, slack=slack)
     assert_acts(_np(h), h_ref, rel=1e-3, floor=1e-3)
+    # goodness only: the kernels' variant without the activity store
+    g2 = torch.empty(rows, device=DEV)
+    P.ff_layer_forward(L, P.HParams(dtype=P.FF_BF16), _t(x), goodness=g2)
+    assert_goodness(_np(g2), g_ref, rel=1e-3, slack=slack)
 
 
 def _run_steps_bf16(P, x, n_pos, W, b, k, hp_kw):
