@@ -1759,6 +1759,9 @@ constexpr int kCUs = 256;
 using DwBig = Tile<64, 128, 32, 2, 4, 3>;
 using DwSmall = Tile<64, 64, 32, 2, 2, 2>;
 using DwBigBf16 = Tile<128, 128, 32, 4, 2, 2>;
+// Fewer than two bf16 tiles per CU: one more register stage (2000x2000 over
+// 2048 rows 54 -> 50 us; at 3072x3072 over 4096 rows two stages are faster).
+using DwFullBf16 = Tile<128, 128, 32, 4, 2, 3>;
 using DwSmallBf16 = Tile<64, 64, 64, 2, 2, 2>;
 
 // Forward tile ladder: a launch takes the largest tile whose grid still puts a
@@ -1994,8 +1997,10 @@ hipError_t launch_dw_adam(int dtype, const float *H, const float *c, const void 
       dw_launch<false, DwSmall>(H, c, Xh, cs, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
   } else {
     if (cs) return hipErrorInvalidValue;  // bf16 operands arrive normalised
-    if (big)
+    if (big && DwBigBf16::tiles(M, N) >= 2 * kCUs)
       dw_launch<true, DwBigBf16>(H, c, Xh, nullptr, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
+    else if (big)
+      dw_launch<true, DwFullBf16>(H, c, Xh, nullptr, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf, s);
     else
       dw_launch<true, DwSmallBf16>(H, c, Xh, nullptr, M, N, K, W, mW, vW, Wb, b, mb, vb, a, lf,
                                    s);

@@ -541,9 +541,20 @@ def test_step_parity_bf16(P, n, d_in, d_out, k):
 
 
 def test_step_parity_bf16_large_tiles_ragged(P):
+    # 16 x 16 weight-gradient tiles of 128x128: one per CU (three register stages)
     x = random_matrix(54, 2060, 2008, 0, 1, 0.5)
     (W, b), = make_weights(55, (2008, 2004))
     _run_steps_bf16(P, x, 1031, W, b, 2, dict(theta=2.0, lr=0.01))
+
+
+def test_step_parity_bf16_two_tiles_per_cu(P):
+    # 24 x 24 weight-gradient tiles (two register stages).  The batch is not
+    # tiny: the device takes the R3 rounding of c*h from its fp32 forward, and
+    # over a 70-row batch the rounding differences against the fp64 oracle
+    # exceed the weight bar on the CPU too (1400 of 9e6 weights).
+    x = random_matrix(56, 1024, 3000, 0, 1, 0.5)
+    (W, b), = make_weights(57, (3000, 3000))
+    _run_steps_bf16(P, x, 512, W, b, 2, dict(theta=2.0, lr=0.01))
 
 
 def test_score_parity_bf16(P):
