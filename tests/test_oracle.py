@@ -698,13 +698,114 @@ def test_chunking_ragged_tail():
 
 
 # ---------------------------------------------------------------- bf16 emulation points
-def test_bf16_mode_rounds_operands_only():
-    x_base, y, y_neg = make_data(31, 6, 40)
-    (W, b), = make_weights(32, (40, 8))
-    x = O.embed_labels(x_base, y, 10)
-    xh, z, h, g = O.layer_forward(W, b, x, 1e-8, bf16=True)
-    xr = O.bf16_round(O.l2_normalise(x, 1e-8))
-    np.testing.assert_array_equal(xh, xr)
-    np.testing.assert_allclose(z, xr @ O.bf16_round(W).T + b, rtol=1e-14)
-    _, z32, _, _ = O.layer_forward(W, b, x, 1e-8)
-    assert np.max(np.abs(z - z32)) < 2 ** -7 * np.max(np.abs(z32)) * 4
+# bf16 mode rounds three operands to bfloat16 (round to nearest, ties to even):
+# R1 the normalised layer input, R2 the weights, R3 dZ = 2 dL/dg h before the
+# weight-gradient contraction; db, h, g and the loss stay unrounded.
+def test_bf16_forward_hand_ties():
+    """Ties of R1 and R2 go to the even neighbour, non-ties to the nearest; the
+    bias and the accumulation are not rounded (hand-derived values)."""
+    c = GOLD["bf16_forward_ties"]
+    W, b = _layer(c)
+    xh, z, h, g = O.layer_forward(W, b, np.array(c["x"], float), c["norm_eps"], bf16=True)
+    np.testing.assert_array_equal(xh, c["x_hat"])
+    np.testing.assert_array_equal(h, c["h"])
+    np.testing.assert_allclose(g, c["g"], rtol=1e-15)
+
+
+def test_bf16_step_hand_r3():
+    """R3 rounds dZ = 2 dL/dg h (not dW, not h); db sums the unrounded dZ."""
+    c = GOLD["bf16_step_r3"]
+    W, b = _layer(c)
+    L = O.Layer.from_params(W, b)
+    r = O.layer_step(L, np.array(c["x"], float), c["n_pos"],
+                     O.HParams(theta=c["theta"], norm_eps=c["norm_eps"], bf16=True))
+    np.testing.assert_allclose(r.g, c["g"], rtol=1e-15)
+    assert abs(r.loss - c["loss"]) <= 1e-15 * c["loss"]
+    np.testing.assert_allclose(r.dLdg, c["dLdg"], rtol=1e-14)
+    np.testing.assert_array_equal(r.dW, c["dW"])  # sums of products of bf16 values: exact
+    np.testing.assert_allclose(r.db, c["db"], rtol=1e-14)
+
+
+def _bf16_random_step(seed):
+    x_base, y, y_neg = make_data(seed, 64, 48)
+    (W, b), = make_weights(seed + 1, (48, 40))
+    b = b + np.linspace(-0.05, 0.1, 40)
+    x = np.concatenate([O.embed_labels(x_base, y, 10), O.embed_labels(x_base, y_neg, 10)])
+    r = O.layer_step(O.Layer.from_params(W, b), x, 64, O.HParams(theta=1.0, bf16=True))
+    return x, W, b, r
+
+
+def test_bf16_weight_gradient_within_r3_rounding_bound():
+    """On the same bf16 forward (R1, R2 applied), the weight gradient differs from
+    the exact one only by the rounding of dZ: |dW16 - dW| <= (2^-8 + 2^-16) |dZ|^T
+    |x_hat| elementwise (bf16 unit roundoff 2^-8, after the float32 conversion),
+    and it does differ, so the rounding is applied."""
+    x, W, b, r = _bf16_random_step(150)
+    xh16 = O.bf16_round(O.l2_normalise(x, 1e-8))
+    h16 = np.maximum(xh16 @ O.bf16_round(W).T + b, 0.0)
+    np.testing.assert_array_equal(r.xh, xh16)
+    np.testing.assert_allclose(r.h, h16, rtol=1e-14, atol=1e-16)
+    g = (h16 * h16).sum(axis=1)
+    n = 64
+    s = np.where(np.arange(2 * n) < n, -1.0 / (1.0 + np.exp(g - 1.0)),
+                 1.0 / (1.0 + np.exp(1.0 - g))) / n
+    dz = 2.0 * s[:, None] * h16
+    exact = dz.T @ xh16
+    bound = (2.0 ** -8 + 2.0 ** -16) * (np.abs(dz).T @ np.abs(xh16))
+    assert np.all(np.abs(r.dW - exact) <= bound + 1e-300)
+    assert np.mean(r.dW != exact) > 0.5
+
+
+def test_bf16_bias_gradient_is_unrounded():
+    """db sums dZ before R3: it matches the sum of the unrounded dZ to fp64
+    rounding and not the sum of the bf16-rounded dZ."""
+    x, W, b, r = _bf16_random_step(151)
+    dz = 2.0 * r.dLdg[:, None] * r.h
+    np.testing.assert_allclose(r.db, dz.sum(axis=0), rtol=1e-13, atol=1e-18)
+    rounded = O.bf16_round(dz).sum(axis=0)
+    assert np.max(np.abs(r.db - rounded) / np.abs(r.db)) > 1e-4
+
+
+@pytest.mark.parametrize("mistake", ["none", "round_dW", "round_h_then_scale", "rounded_db",
+                                     "no_R1", "no_R2", "ties_away", "no_R3"])
+def test_planted_bf16_mistakes_fail_the_hand_cases(mistake):
+    """Each plausible mistake in the bf16 step, planted in a copy of it, changes a
+    value of the hand-derived cases; the copy without a mistake matches them."""
+    def rnd(v):
+        if mistake != "ties_away":
+            return O.bf16_round(v)
+        f = np.asarray(v, np.float32).view(np.uint32).astype(np.uint64)
+        return ((f + 0x8000) & 0xFFFF0000).astype(np.uint32).view(np.float32).astype(float)
+
+    def step(case):
+        W, b = _layer(case)
+        x = np.array(case["x"], float)
+        xh = O.l2_normalise(x, case["norm_eps"])
+        xh = xh if mistake == "no_R1" else rnd(xh)
+        Wr = W if mistake == "no_R2" else rnd(W)
+        h = np.maximum(xh @ Wr.T + b, 0.0)
+        g = (h * h).sum(axis=1)
+        if "n_pos" not in case:
+            return h, g, None, None
+        _, dg = O.ff_loss(g, case["n_pos"], case["theta"])
+        dz = 2.0 * dg[:, None] * h
+        if mistake == "round_dW":
+            dW = rnd(dz.T @ xh)
+        elif mistake == "round_h_then_scale":
+            dW = (2.0 * dg[:, None] * rnd(h)).T @ xh
+        elif mistake == "no_R3":
+            dW = dz.T @ xh
+        else:
+            dW = rnd(dz).T @ xh
+        db = rnd(dz).sum(axis=0) if mistake == "rounded_db" else dz.sum(axis=0)
+        return h, g, dW, db
+
+    def matches():
+        fwd, st = GOLD["bf16_forward_ties"], GOLD["bf16_step_r3"]
+        h, g, _, _ = step(fwd)
+        ok = np.array_equal(h, fwd["h"]) and np.allclose(g, fwd["g"], rtol=1e-15)
+        h, g, dW, db = step(st)
+        return (ok and np.allclose(g, st["g"], rtol=1e-15) and np.array_equal(dW, st["dW"])
+                and np.allclose(db, st["db"], rtol=1e-14))
+
+    assert matches() == (mistake == "none")
