@@ -74,8 +74,10 @@ typedef struct {
   uint16_t *W_bf16;  /* (device) [d_out][d_in] bf16 shadow of W; required when
                         dtype == FF_BF16 (kept in sync by every update, see
                         ff_refresh_bf16_shadow), ignored otherwise            */
-  int64_t step;      /* (host) Adam step count t; an update increments it
-                        before use, so the first update runs with t = 1       */
+  int64_t step;      /* (host) Adam step count: an update runs with
+                        t = step + 1 (the first with t = 1) and stores t in
+                        step once its launch is enqueued; a failed launch
+                        leaves it unchanged                                   */
 } ff_layer;
 
 /* Hyper-parameters.  theta: goodness threshold of Eq. 1.  lr, beta1, beta2,
@@ -121,7 +123,7 @@ ff_status ff_layer_forward(const ff_layer *L, const ff_hparams *hp, const float 
  *          (negative log-likelihood of Eq. 1, each half averaged over its rows);
  *   dZ_rj = 2 dL/dg_r h_rj;  dW = dZ^T x_hat;  db = sum_r dZ_r
  *          (local gradient only: FF needs no input gradient);
- *   one Adam update of W and b with t = ++L->step.
+ *   one Adam update of W and b with t = L->step + 1 (then L->step = t).
  *   x (device) [R][d_in]; h_out (device) [R][d_out] or NULL: the activities,
  *   computed with the weights before the update; goodness (device) [R] or
  *   NULL; loss (device) [1] or NULL.  Requires n_pos >= 1 and n_neg >= 1. */
@@ -192,6 +194,33 @@ ff_status ff_chapter_train(ff_layer *layers, int32_t n_layers, const ff_hparams 
                            int32_t chunk_pairs, int32_t epochs, int32_t splits,
                            int32_t cooldown_start, int32_t assignment, int32_t n_streams,
                            void *const *streams, float *loss_trace, void *ws, size_t ws_bytes);
+
+/* AdaptiveNEG chapters (Sec. 5 negative selection; the UpdateXNEG step of
+ * Alg. 1 / Alg. 2): as ff_chapter_train, but chapter c's wrong labels are
+ * computed on the device as the chapter begins,
+ *   y_neg_chapters[c][i] = argmax_{k != y_pos[i]} S[i][k]   (lowest k on ties),
+ * S as in ff_score_labels (first_scored_layer as there) over the whole set,
+ * with every layer's weights as they stand after chapter c-1 (the initial
+ * weights for c = 0): the last network all layers agree on (a reading; the
+ * paper does not say which layer versions regenerate the negatives).  The
+ * scoring runs on the worker stream that trains layer 0 in chapter c, after
+ * every layer has published chapter c-1, so chapter c of any layer starts
+ * after it.
+ *   y_neg_chapters (device) [splits][n] int32: output; n_classes >= 2.
+ *   Workspace: ff_chapter_adaptive_workspace_size.  Other arguments, errors
+ *   and asynchrony as for ff_chapter_train. */
+size_t ff_chapter_adaptive_workspace_size(const ff_layer *layers, int32_t n_layers, int32_t n,
+                                          int32_t n_classes, int32_t chunk_pairs,
+                                          int32_t n_streams, int32_t dtype);
+
+ff_status ff_chapter_train_adaptive(ff_layer *layers, int32_t n_layers, const ff_hparams *hp,
+                                    const float *x_base, const int32_t *y_pos,
+                                    int32_t *y_neg_chapters, int32_t n, int32_t n_classes,
+                                    int32_t chunk_pairs, int32_t epochs, int32_t splits,
+                                    int32_t cooldown_start, int32_t assignment,
+                                    int32_t first_scored_layer, int32_t n_streams,
+                                    void *const *streams, float *loss_trace, void *ws,
+                                    size_t ws_bytes);
 
 /* ---- Softmax prediction layer (Sec. 3 "Prediction": Softmax; Sec. 5.1) ------
  * An input is labelled with the neutral label (0.1 in every label feature) and
@@ -357,6 +386,14 @@ typedef struct {
  * other kinds run without events. */
 ff_status ff_profile_start(int32_t max_launches, uint32_t kind_mask);
 ff_status ff_profile_stop(ff_kernel_stats *stats /* (host) [FF_KERNEL_KINDS] */);
+
+/* ---- Failure injection (testing aid) ---------------------------------------
+ * The next launch of kernel kind `kind` (an ff_kernel_kind) that any entry
+ * point makes enqueues nothing and fails, so the entry point returns
+ * FF_ERR_HIP as for a failed launch; -1 disarms.  Lets tests check that a
+ * failed launch leaves host state (the Adam step counts) as it was.
+ * Process-wide; FF_ERR_INVALID_ARG for a kind outside [-1, FF_KERNEL_KINDS). */
+ff_status ff_fail_next_launch(int32_t kind);
 
 #ifdef __cplusplus
 }

@@ -287,20 +287,28 @@ def cooldown_lr(lr0: float, epoch: int, epochs: int, cooldown_start: int) -> flo
 
 def chapter_train(layers: List[Layer], x_base, y, y_neg_chapters, n_classes: int,
                   chunk_pairs: int, epochs: int, splits: int, cooldown_start: int,
-                  hp: HParams) -> np.ndarray:
+                  hp: HParams, on_step=None) -> np.ndarray:
     """Chapter-granularity PFF training (Alg. 1 Single-Layer; Alg. 2 All-Layers).
 
     The E epochs are split into S chapters of E/S epochs.  In chapter c, layer l
     first takes as input the training set (positives with labels y, negatives
-    with this chapter's wrong labels: RandomNEG redraws them for every chapter,
-    they are inputs here) passed through layers 0..l-1 as published at the end
-    of their chapter c ("x <- layer(x)" with getLayer(k, chapter)); then it
-    trains for E/S epochs over the chunks, starting from its own weights after
-    chapter c-1, with the cooled-down learning rate of each epoch; then it is
-    published.  Single-Layer (one layer per node) and All-Layers (each node
-    trains the whole net for a chapter, handing each layer on) compute this same
-    dependency graph; they differ in which node does which (layer, chapter).
-    Returns the loss trace ``[L, E * n_chunks]``.
+    with this chapter's wrong labels) passed through layers 0..l-1 as published
+    at the end of their chapter c ("x <- layer(x)" with getLayer(k, chapter));
+    then it trains for E/S epochs over the chunks, starting from its own
+    weights after chapter c-1, with the cooled-down learning rate of each
+    epoch; then it is published.  Single-Layer (one layer per node) and
+    All-Layers (each node trains the whole net for a chapter, handing each layer
+    on) compute this same dependency graph; they differ in which node does
+    which (layer, chapter).
+
+    ``y_neg_chapters`` is either the chapters' wrong labels (``[S][n]``: the
+    RandomNEG redraw of every chapter, random numbers being inputs here) or a
+    function ``negatives(c, layers)`` called when chapter c begins, while every
+    layer still holds its weights after chapter c-1 (the initial weights for
+    c = 0), which returns that chapter's wrong labels (AdaptiveNEG:
+    ``adaptive_chapter_negatives``).  Returns the loss trace ``[L, E * n_chunks]``.
+    ``on_step(l, result)``, if given, sees every step's StepResult (test
+    bookkeeping; no effect on results).
     """
     E, S = epochs, splits
     assert E % S == 0
@@ -309,12 +317,13 @@ def chapter_train(layers: List[Layer], x_base, y, y_neg_chapters, n_classes: int
     L = len(layers)
     trace = np.zeros((L, E * len(chunks)))
     for c in range(S):
+        y_neg = y_neg_chapters(c, layers) if callable(y_neg_chapters) else y_neg_chapters[c]
         published = []
         for li, Ly in enumerate(layers):
             # the chapter's input of this layer: every chunk through the published layers
             inputs = []
             for (s, b) in chunks:
-                a = chunk_input(x_base, y, y_neg_chapters[c], s, b, n_classes)
+                a = chunk_input(x_base, y, y_neg, s, b, n_classes)
                 for P in published:
                     a = layer_forward(P[0], P[1], a, hp.norm_eps, False, hp.bf16)[2]
                 inputs.append(a)
@@ -322,9 +331,31 @@ def chapter_train(layers: List[Layer], x_base, y, y_neg_chapters, n_classes: int
                 e = c * per + m
                 hp_e = dataclasses.replace(hp, lr=cooldown_lr(hp.lr, e, E, cooldown_start))
                 for q, (s, b) in enumerate(chunks):
-                    trace[li, e * len(chunks) + q] = layer_step(Ly, inputs[q], b, hp_e).loss
+                    r = layer_step(Ly, inputs[q], b, hp_e)
+                    trace[li, e * len(chunks) + q] = r.loss
+                    if on_step:
+                        on_step(li, r)
             published.append((Ly.W.copy(), Ly.b.copy()))
     return trace
+
+
+def adaptive_chapter_negatives(x_base, y, n_classes: int, hp: HParams,
+                               first_scored_layer: int = 0, record: Optional[list] = None):
+    """AdaptiveNEG negatives for the chapter schedules (Sec. 5 negative selection,
+    the UpdateXNEG step of Alg. 1 / Alg. 2): the function ``negatives(c, layers)``
+    that ``chapter_train`` calls as chapter c begins.  It returns the wrong label
+    the network scores highest for every training sample (``adaptive_negatives``
+    over the whole set), evaluated with every layer's weights after chapter c-1.
+    Reading: the paper regenerates the adaptive negatives between chapters
+    without saying from which layer versions; here they come from the network as
+    it stands when the chapter starts, the last network all layers agree on.
+    ``record``, if given, collects each chapter's labels."""
+    def negatives(c, layers):
+        y_neg = adaptive_negatives(layers, x_base, y, n_classes, hp, first_scored_layer)[1]
+        if record is not None:
+            record.append(y_neg)
+        return y_neg
+    return negatives
 
 
 # ----------------------------------------------------------------------------
@@ -520,13 +551,14 @@ def chunk_input(x_base, y, y_neg, s: int, b: int, n_classes: int) -> np.ndarray:
 
 
 def train_sequential(layers: List[Layer], x_base, y, y_neg, n_classes: int, chunk_pairs: int,
-                     epochs: int, hp: HParams) -> np.ndarray:
+                     epochs: int, hp: HParams, on_step=None) -> np.ndarray:
     """Train the layers one after another ("Sequential Training", Sec. 3).
 
     Layer l runs ``epochs`` passes over all chunks, then its output on the
     whole set -- one forward pass with its final weights, as the ``x <- layer(x)``
     step of Alg. 2 -- becomes layer l+1's input.  Returns the loss trace
-    ``[n_layers, epochs * n_chunks]``.  Mutates ``layers``.
+    ``[n_layers, epochs * n_chunks]``.  Mutates ``layers``.  ``on_step(l, result)``,
+    if given, sees every step's StepResult (test bookkeeping; no effect on results).
     """
     chunks = chunk_bounds(x_base.shape[0], chunk_pairs)
     trace = np.zeros((len(layers), epochs * len(chunks)))
@@ -534,14 +566,18 @@ def train_sequential(layers: List[Layer], x_base, y, y_neg, n_classes: int, chun
     for li, L in enumerate(layers):
         for e in range(epochs):
             for ci, (s, b) in enumerate(chunks):
-                trace[li, e * len(chunks) + ci] = layer_step(L, acts[ci], b, hp).loss
+                r = layer_step(L, acts[ci], b, hp)
+                trace[li, e * len(chunks) + ci] = r.loss
+                if on_step:
+                    on_step(li, r)
         if li + 1 < len(layers):
             acts = [layer_forward(L.W, L.b, a, hp.norm_eps, False, hp.bf16)[2] for a in acts]
     return trace
 
 
 def train_pipelined(layers: List[Layer], x_base, y, y_neg, n_classes: int, chunk_pairs: int,
-                    epochs: int, hp: HParams, order: str = "chunk_major") -> np.ndarray:
+                    epochs: int, hp: HParams, order: str = "chunk_major",
+                    on_step=None) -> np.ndarray:
     """Layer-per-stage pipeline at chunk granularity (Single-Layer PFF, Sec. 4.1, Alg. 1).
 
     Each layer trains on the chunks in order; layer l+1 trains on chunk c once
@@ -554,6 +590,8 @@ def train_pipelined(layers: List[Layer], x_base, y, y_neg, n_classes: int, chunk
     ("chunk_major", "layer_major" or "wavefront") to demonstrate that.  With
     ``epochs > 1`` the chunk stream is the chunk list repeated.  Returns the
     loss trace ``[n_layers, epochs * n_chunks]``.  Mutates ``layers``.
+    ``on_step(l, result)``, if given, sees every step's StepResult (test
+    bookkeeping; no effect on results).
     """
     chunks = chunk_bounds(x_base.shape[0], chunk_pairs) * epochs
     nl, nc = len(layers), len(chunks)
@@ -572,6 +610,8 @@ def train_pipelined(layers: List[Layer], x_base, y, y_neg, n_classes: int, chunk
         x = chunk_input(x_base, y, y_neg, s, b, n_classes) if l == 0 else inputs.pop((l, c))
         r = layer_step(layers[l], x, b, hp)
         trace[l, c] = r.loss
+        if on_step:
+            on_step(l, r)
         if l + 1 < nl:
             inputs[(l + 1, c)] = r.h
     return trace

@@ -28,10 +28,11 @@ EXPORTS = ["ff_status_string", "ff_last_error", "ff_embed_labels", "ff_step_work
            "ff_score_workspace_size", "ff_score_labels", "ff_adaptive_negatives",
            "ff_head_workspace_size", "ff_head_step", "ff_head_predict",
            "ff_chapter_workspace_size", "ff_chapter_train",
+           "ff_chapter_adaptive_workspace_size", "ff_chapter_train_adaptive",
            "ff_po_step_workspace_size", "ff_po_layer_step", "ff_po_epoch_workspace_size",
            "ff_po_epoch", "ff_po_predict_workspace_size", "ff_po_predict",
            "ff_pipeline_workspace_size",
-           "ff_pipeline_epoch", "ff_profile_start", "ff_profile_stop"]
+           "ff_pipeline_epoch", "ff_profile_start", "ff_profile_stop", "ff_fail_next_launch"]
 
 KERNEL_KINDS = ["embed_norm", "forward", "loss", "dw_adam", "goodness", "argmax", "bf16_shadow",
                 "head"]
@@ -100,6 +101,12 @@ def _load() -> ctypes.CDLL:
         "ff_chapter_train": (c_int32, [POINTER(ff_layer), c_int32, POINTER(ff_hparams), P, P, P,
                                        c_int32, c_int32, c_int32, c_int32, c_int32, c_int32,
                                        c_int32, c_int32, POINTER(c_void_p), P, P, c_size_t]),
+        "ff_chapter_adaptive_workspace_size": (c_size_t, [POINTER(ff_layer), c_int32, c_int32,
+                                                          c_int32, c_int32, c_int32, c_int32]),
+        "ff_chapter_train_adaptive": (c_int32, [POINTER(ff_layer), c_int32, POINTER(ff_hparams), P,
+                                                P, P, c_int32, c_int32, c_int32, c_int32,
+                                                c_int32, c_int32, c_int32, c_int32, c_int32,
+                                                POINTER(c_void_p), P, P, c_size_t]),
         "ff_po_step_workspace_size": (c_size_t, [c_int32] * 5),
         "ff_po_layer_step": (c_int32, [POINTER(ff_layer), POINTER(ff_head), POINTER(ff_hparams),
                                        POINTER(ff_hparams), P, P, c_int32, c_int32, P, P, P,
@@ -122,6 +129,7 @@ def _load() -> ctypes.CDLL:
                                         POINTER(c_void_p), P, P, c_size_t]),
         "ff_profile_start": (c_int32, [c_int32, ctypes.c_uint32]),
         "ff_profile_stop": (c_int32, [POINTER(ff_kernel_stats)]),
+        "ff_fail_next_launch": (c_int32, [c_int32]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -154,6 +162,23 @@ def _ptr(t: Optional[torch.Tensor], dtype=None, numel=None, name="tensor"):
 def _stream(stream) -> Optional[int]:
     s = stream if stream is not None else torch.cuda.current_stream()
     return s.cuda_stream if isinstance(s, torch.cuda.Stream) else int(s)
+
+
+def _hold(tensors, streams):
+    """Buffers this binding allocated (on the current stream) and handed to
+    work enqueued on `streams`: mark them in use by every stream other than the
+    current one, so that torch's caching allocator does not hand their memory
+    to a later allocation before that work has finished."""
+    cur = torch.cuda.current_stream().cuda_stream
+    for s in streams:
+        if s is None:
+            continue
+        if not isinstance(s, torch.cuda.Stream):
+            s = torch.cuda.ExternalStream(int(s))
+        if s.cuda_stream != cur:
+            for t in tensors:
+                if t is not None:
+                    t.record_stream(s)
 
 
 @dataclasses.dataclass
@@ -227,7 +252,9 @@ def workspace(nbytes: int, device="cuda") -> torch.Tensor:
 def ff_embed_labels(x_base: torch.Tensor, labels: torch.Tensor, n_classes: int,
                     out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     rows, d = x_base.shape
-    out = torch.empty_like(x_base) if out is None else out
+    mine = [torch.empty_like(x_base)] if out is None else []
+    out = mine[0] if mine else out
+    _hold(mine, [stream])
     _check(LIB.ff_embed_labels(_ptr(x_base, torch.float32, name="x_base"),
                                 _ptr(labels, torch.int32, rows, "labels"), rows, d, n_classes,
                                 _ptr(out, torch.float32, rows * d, "out"), _stream(stream)))
@@ -245,6 +272,7 @@ def ff_layer_forward(layer: Layer, hp: HParams, x: torch.Tensor, x_normalised: b
     if ws is None:
         ws = workspace(ff_step_workspace_size(max(rows, 1), layer.d_in, layer.d_out, hp.dtype),
                        x.device)
+        _hold([ws], [stream])
     Lc = layer.c()
     _check(LIB.ff_layer_forward(ctypes.byref(Lc), ctypes.byref(hp.c()),
                                  _ptr(x, torch.float32, rows * layer.d_in, "x"), rows,
@@ -263,6 +291,7 @@ def ff_layer_step(layer: Layer, hp: HParams, x: torch.Tensor, n_pos: int, n_neg:
     if ws is None:
         ws = workspace(ff_step_workspace_size(max(R, 1), layer.d_in, layer.d_out, hp.dtype),
                        x.device)
+        _hold([ws], [stream])
     Lc = layer.c()
     st = LIB.ff_layer_step(ctypes.byref(Lc), ctypes.byref(hp.c()),
                             _ptr(x, torch.float32, R * layer.d_in, "x"), n_pos, n_neg,
@@ -291,9 +320,12 @@ def ff_score_labels(layers: Sequence[Layer], hp: HParams, x_base: torch.Tensor, 
                     stream=None):
     n = x_base.shape[0]
     dev = x_base.device
-    pred = torch.empty(n, dtype=torch.int32, device=dev) if pred is None else pred
+    if pred is None:
+        pred = torch.empty(n, dtype=torch.int32, device=dev)
+        _hold([pred], [stream])
     if ws is None:
         ws = workspace(ff_score_workspace_size(layers, max(n, 1), n_classes, hp.dtype), dev)
+        _hold([ws], [stream])
     arr = _layers_c(layers)
     _check(LIB.ff_score_labels(arr, len(layers), first_scored_layer, ctypes.byref(hp.c()),
                                 _ptr(x_base, torch.float32, n * layers[0].d_in, "x_base"), n,
@@ -311,9 +343,12 @@ def ff_adaptive_negatives(layers: Sequence[Layer], hp: HParams, x_base: torch.Te
     """AdaptiveNEG: y_neg[n] = argmax over c != labels[n] of the goodness scores."""
     n = x_base.shape[0]
     dev = x_base.device
-    y_neg = torch.empty(n, dtype=torch.int32, device=dev) if y_neg is None else y_neg
+    if y_neg is None:
+        y_neg = torch.empty(n, dtype=torch.int32, device=dev)
+        _hold([y_neg], [stream])
     if ws is None:
         ws = workspace(ff_score_workspace_size(layers, max(n, 1), n_classes, hp.dtype), dev)
+        _hold([ws], [stream])
     arr = _layers_c(layers)
     _check(LIB.ff_adaptive_negatives(
         arr, len(layers), first_scored_layer, ctypes.byref(hp.c()),
@@ -339,6 +374,7 @@ def ff_head_step(layers: Sequence[Layer], hp: HParams, head: Head, head_hp: HPar
     if ws is None:
         ws = workspace(ff_head_workspace_size(layers, first_layer, max(n, 1), head.n_classes,
                                               hp.dtype), x_base.device)
+        _hold([ws], [stream])
     Hc = head.c()
     st = LIB.ff_head_step(_layers_c(layers), len(layers), first_layer, ctypes.byref(hp.c()),
                           ctypes.byref(Hc), ctypes.byref(head_hp.c()),
@@ -358,10 +394,13 @@ def ff_head_predict(layers: Sequence[Layer], hp: HParams, head: Head, x_base: to
     """Softmax prediction: (logits or None, pred)."""
     n = x_base.shape[0]
     dev = x_base.device
-    pred = torch.empty(n, dtype=torch.int32, device=dev) if pred is None else pred
+    if pred is None:
+        pred = torch.empty(n, dtype=torch.int32, device=dev)
+        _hold([pred], [stream])
     if ws is None:
         ws = workspace(ff_head_workspace_size(layers, first_layer, max(n, 1), head.n_classes,
                                               hp.dtype), dev)
+        _hold([ws], [stream])
     _check(LIB.ff_head_predict(_layers_c(layers), len(layers), first_layer, ctypes.byref(hp.c()),
                                ctypes.byref(head.c()),
                                _ptr(x_base, torch.float32, n * layers[0].d_in, "x_base"), n,
@@ -392,6 +431,7 @@ def ff_chapter_train(layers: List[Layer], hp: HParams, x_base: torch.Tensor, y_p
     if ws is None:
         ws = workspace(LIB.ff_chapter_workspace_size(_layers_c(layers), len(layers), n,
                                                      chunk_pairs, len(streams), hp.dtype), dev)
+        _hold([ws], streams)
     sarr = (c_void_p * len(streams))(*[_stream(s) for s in streams])
     arr = _layers_c(layers)
     st = LIB.ff_chapter_train(arr, len(layers), ctypes.byref(hp.c()),
@@ -410,6 +450,53 @@ def ff_chapter_train(layers: List[Layer], hp: HParams, x_base: torch.Tensor, y_p
     _check(st)
 
 
+def ff_chapter_train_adaptive(layers: List[Layer], hp: HParams, x_base: torch.Tensor,
+                              y_pos: torch.Tensor, n_classes: int, chunk_pairs: int, epochs: int,
+                              splits: int, cooldown_start: int,
+                              assignment: int = FF_SINGLE_LAYER, first_scored_layer: int = 0,
+                              y_neg_chapters: Optional[torch.Tensor] = None,
+                              streams: Optional[Sequence] = None, n_streams: Optional[int] = None,
+                              loss_trace: Optional[torch.Tensor] = None,
+                              ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """AdaptiveNEG chapters: as ff_chapter_train, with each chapter's wrong labels
+    computed on the device when the chapter starts; returns them, [splits][n]."""
+    n = x_base.shape[0]
+    dev = x_base.device
+    nc = (n + chunk_pairs - 1) // chunk_pairs
+    ns = len(layers) if assignment == FF_SINGLE_LAYER else (n_streams or len(layers))
+    own = streams is None
+    cur = torch.cuda.current_stream(dev)
+    if own:
+        streams = [torch.cuda.Stream(dev) for _ in range(ns)]
+        for s in streams:
+            s.wait_stream(cur)
+    if y_neg_chapters is None:
+        y_neg_chapters = torch.empty(splits, n, dtype=torch.int32, device=dev)
+        _hold([y_neg_chapters], streams)
+    if ws is None:
+        ws = workspace(LIB.ff_chapter_adaptive_workspace_size(
+            _layers_c(layers), len(layers), n, n_classes, chunk_pairs, len(streams), hp.dtype), dev)
+        _hold([ws], streams)
+    sarr = (c_void_p * len(streams))(*[_stream(s) for s in streams])
+    arr = _layers_c(layers)
+    st = LIB.ff_chapter_train_adaptive(
+        arr, len(layers), ctypes.byref(hp.c()),
+        _ptr(x_base, torch.float32, n * layers[0].d_in, "x_base"),
+        _ptr(y_pos, torch.int32, n, "y_pos"),
+        _ptr(y_neg_chapters, torch.int32, splits * n, "y_neg_chapters"), n, n_classes,
+        chunk_pairs, epochs, splits, cooldown_start, assignment, first_scored_layer,
+        len(streams), sarr,
+        _ptr(loss_trace, torch.float32, len(layers) * epochs * nc, "loss_trace"),
+        _ptr(ws, torch.uint8), ws.numel())
+    for L, Lc in zip(layers, arr):
+        L.step = Lc.step
+    if own:
+        for s in streams:
+            cur.wait_stream(s)
+    _check(st)
+    return y_neg_chapters
+
+
 def _heads_c(heads: Sequence[Head]):
     return (ff_head * len(heads))(*[h.c() for h in heads])
 
@@ -423,6 +510,7 @@ def ff_po_layer_step(layer: Layer, head: Head, hp: HParams, head_hp: HParams, x:
     if ws is None:
         ws = workspace(LIB.ff_po_step_workspace_size(max(rows, 1), layer.d_in, layer.d_out,
                                                      head.n_classes, hp.dtype), x.device)
+        _hold([ws], [stream])
     Lc, Hc = layer.c(), head.c()
     st = LIB.ff_po_layer_step(ctypes.byref(Lc), ctypes.byref(Hc), ctypes.byref(hp.c()),
                               ctypes.byref(head_hp.c()),
@@ -443,15 +531,16 @@ def ff_po_epoch(layers: List[Layer], heads: List[Head], hp: HParams, head_hp: HP
     n = x_base.shape[0]
     dev = x_base.device
     nc = (n + chunk - 1) // chunk
-    if ws is None:
-        ws = workspace(LIB.ff_po_epoch_workspace_size(_layers_c(layers), len(layers), n,
-                                                      n_classes, chunk, schedule, hp.dtype), dev)
     own = streams is None
     cur = torch.cuda.current_stream(dev)
     if own:
         streams = [cur] + [torch.cuda.Stream(dev) for _ in range(len(layers) - 1)]
         for s in streams[1:]:
             s.wait_stream(cur)
+    if ws is None:
+        ws = workspace(LIB.ff_po_epoch_workspace_size(_layers_c(layers), len(layers), n,
+                                                      n_classes, chunk, schedule, hp.dtype), dev)
+        _hold([ws], streams)
     sarr = (c_void_p * len(layers))(*[_stream(s) for s in streams])
     arr, harr = _layers_c(layers), _heads_c(heads)
     st = LIB.ff_po_epoch(arr, harr, len(layers), ctypes.byref(hp.c()), ctypes.byref(head_hp.c()),
@@ -478,10 +567,13 @@ def ff_po_predict(layers: Sequence[Layer], heads: Sequence[Head], hp: HParams,
     n = x_base.shape[0]
     dev = x_base.device
     C = heads[0].n_classes
-    pred = torch.empty(n, dtype=torch.int32, device=dev) if pred is None else pred
+    if pred is None:
+        pred = torch.empty(n, dtype=torch.int32, device=dev)
+        _hold([pred], [stream])
     if ws is None:
         ws = workspace(LIB.ff_po_predict_workspace_size(_layers_c(layers), len(layers),
                                                         max(n, 1), C, hp.dtype), dev)
+        _hold([ws], [stream])
     _check(LIB.ff_po_predict(_layers_c(layers), _heads_c(heads), len(layers),
                              ctypes.byref(hp.c()),
                              _ptr(x_base, torch.float32, n * layers[0].d_in, "x_base"), n,
@@ -507,14 +599,15 @@ def ff_pipeline_epoch(layers: List[Layer], hp: HParams, x_base: torch.Tensor, y_
     n = x_base.shape[0]
     dev = x_base.device
     nc = (n + chunk_pairs - 1) // chunk_pairs
-    if ws is None:
-        ws = workspace(ff_pipeline_workspace_size(layers, n, chunk_pairs, schedule, hp.dtype), dev)
     own = streams is None
     cur = torch.cuda.current_stream(dev)
     if own:
         streams = [cur] + [torch.cuda.Stream(dev) for _ in range(len(layers) - 1)]
         for s in streams[1:]:
             s.wait_stream(cur)
+    if ws is None:
+        ws = workspace(ff_pipeline_workspace_size(layers, n, chunk_pairs, schedule, hp.dtype), dev)
+        _hold([ws], streams)
     sarr = (c_void_p * len(layers))(*[_stream(s) for s in streams])
     arr = _layers_c(layers)
     st = LIB.ff_pipeline_epoch(arr, len(layers), ctypes.byref(hp.c()),
@@ -529,10 +622,14 @@ def ff_pipeline_epoch(layers: List[Layer], hp: HParams, x_base: torch.Tensor, y_
     if own:
         for s in streams[1:]:
             cur.wait_stream(s)
-        for s in streams[1:]:  # the side streams used ws: keep it until they finish
-            ws.record_stream(s)
     _check(st)
     return loss_trace
+
+
+def ff_fail_next_launch(kind: Optional[str]):
+    """Test aid: the next launch of kernel kind `kind` (a KERNEL_KINDS name) fails
+    without enqueuing anything; None disarms."""
+    _check(LIB.ff_fail_next_launch(-1 if kind is None else KERNEL_KINDS.index(kind)))
 
 
 def ff_profile_start(max_launches: int = 65536, kinds=None):

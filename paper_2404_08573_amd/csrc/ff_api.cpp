@@ -9,6 +9,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
 #include <mutex>
 #include <vector>
 
@@ -78,10 +79,17 @@ struct Profiler {
 };
 Profiler g_prof;
 
+// Test aid (ff_fail_next_launch): kernel kind whose next launch fails, or -1.
+std::atomic<int> g_fail_kind{-1};
+
 // Launches `fn` (returning hipError_t), bracketed by timing events when a
 // profile is active and events remain.
 template <class F>
 hipError_t launch(int kind, double flops, double bytes, hipStream_t st, F fn) {
+  int armed = kind;
+  if (g_fail_kind.load(std::memory_order_relaxed) == kind &&
+      g_fail_kind.compare_exchange_strong(armed, -1))
+    return hipErrorLaunchFailure;  // nothing enqueued
   std::unique_lock<std::mutex> lk(g_prof.mu);
   if (!g_prof.on || !((g_prof.mask >> kind) & 1u) || g_prof.used + 2 > g_prof.pool.size()) {
     lk.unlock();
@@ -298,6 +306,18 @@ ff_status forward_core(const ff_layer *L, const ff_hparams *hp, const LayerInput
   return FF_OK;
 }
 
+// Adam arguments of update t.
+ffk::AdamArgs adam_args(const ff_hparams *hp, int64_t t) {
+  ffk::AdamArgs a;
+  a.lr = hp->lr;
+  a.beta1 = hp->beta1;
+  a.beta2 = hp->beta2;
+  a.eps = hp->adam_eps;
+  a.bc1 = (float)(1.0 - pow((double)hp->beta1, (double)t));
+  a.bc2 = (float)(1.0 - pow((double)hp->beta2, (double)t));
+  return a;
+}
+
 // One training step (n_pos positives first); `s_next` as in forward_core.
 ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int n_pos,
                     int n_neg, float *h_out, float *goodness, float *loss, float *s_next,
@@ -327,14 +347,9 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int
   lf.n_pos = n_pos;
   lf.n_neg = n_neg;
   lf.loss = lo;
-  const int64_t t = ++L->step;
-  ffk::AdamArgs a;
-  a.lr = hp->lr;
-  a.beta1 = hp->beta1;
-  a.beta2 = hp->beta2;
-  a.eps = hp->adam_eps;
-  a.bc1 = (float)(1.0 - pow((double)hp->beta1, (double)t));
-  a.bc2 = (float)(1.0 - pow((double)hp->beta2, (double)t));
+  // the update is t = step + 1; the count moves only once its launch is enqueued
+  const int64_t t = L->step + 1;
+  const ffk::AdamArgs a = adam_args(hp, t);
   {
     const double eb = (double)elem_bytes(hp->dtype);
     const double params = (double)L->d_out * L->d_in;
@@ -347,19 +362,8 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int
                                  L->mb, L->vb, a, lf, st);
     }));
   }
+  L->step = t;
   return FF_OK;
-}
-
-// Adam arguments of update t.
-ffk::AdamArgs adam_args(const ff_hparams *hp, int64_t t) {
-  ffk::AdamArgs a;
-  a.lr = hp->lr;
-  a.beta1 = hp->beta1;
-  a.beta2 = hp->beta2;
-  a.eps = hp->adam_eps;
-  a.bc1 = (float)(1.0 - pow((double)hp->beta1, (double)t));
-  a.bc2 = (float)(1.0 - pow((double)hp->beta2, (double)t));
-  return a;
 }
 
 // One performance-optimised step (R rows, labels): the layer and its softmax
@@ -399,17 +403,18 @@ ff_status po_step_core(ff_layer *L, ff_head *head, const ff_hparams *hp, const f
   FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * R * C * D, hbytes + (double)splits * C * D * 4.0, st, [&] {
     return ffk::launch_head_grad(f, s.G, R, C, D, splits, s.part, st);
   }));
-  const ffk::AdamArgs ah = adam_args(head_hp, ++head->step);
+  const ffk::AdamArgs ah = adam_args(head_hp, head->step + 1);
   FF_HIP(launch(FF_KERNEL_HEAD, 0.0, (double)splits * C * D * 4.0 + (double)C * D * 24.0, st,
                 [&] {
                   return ffk::launch_head_adam(s.part, splits, s.G, s.lrow, R, C, D, head->W,
                                                head->mW, head->vW, head->b, head->mb, head->vb,
                                                ah, loss ? loss : s.loss, st);
                 }));
+  ++head->step;
   // dW = dZ^T x_hat, db = sum dZ: the weight-gradient product with row scale
   // c = 1, so with raw input rows the product's factor c * s is the input row
   // scale s itself
-  const ffk::AdamArgs a = adam_args(hp, ++L->step);
+  const ffk::AdamArgs a = adam_args(hp, L->step + 1);
   ffk::LossFinish lf{};
   const double eb = (double)elem_bytes(hp->dtype);
   const double params = (double)D * L->d_in;
@@ -420,6 +425,7 @@ ff_status po_step_core(ff_layer *L, ff_head *head, const ff_hparams *hp, const f
                                L->mW, L->vW, hp->dtype == FF_BF16 ? L->W_bf16 : nullptr, L->b,
                                L->mb, L->vb, a, lf, st);
   }));
+  ++L->step;
   return FF_OK;
 }
 
@@ -584,12 +590,8 @@ size_t ff_score_workspace_size(const ff_layer *layers, int32_t n_layers, int32_t
 }
 
 namespace {
-// Scores every input under every label, then takes the argmax (skipping
-// exclude[i] when exclude is given).
-ff_status score_core(const ff_layer *layers, int32_t n_layers, int32_t first_scored_layer,
-                     const ff_hparams *hp, const float *x_base, int32_t n, int32_t n_classes,
-                     const int32_t *exclude, float *scores, int32_t *pred, void *ws,
-                     size_t ws_bytes, void *stream) {
+ff_status check_score_args(const ff_layer *layers, int32_t n_layers, int32_t first_scored_layer,
+                           const ff_hparams *hp, int32_t n, int32_t n_classes) {
   FF_TRY(check_hp(hp));
   FF_TRY(check_stack(layers, n_layers, hp, false));
   if (first_scored_layer < 0 || first_scored_layer >= n_layers)
@@ -598,18 +600,16 @@ ff_status score_core(const ff_layer *layers, int32_t n_layers, int32_t first_sco
   if (n < 0 || n_classes <= 0) return fail(FF_ERR_INVALID_ARG, "n=%d n_classes=%d", n, n_classes);
   if (n_classes > layers[0].d_in)
     return fail(FF_ERR_INVALID_ARG, "n_classes=%d exceeds d_in=%d", n_classes, layers[0].d_in);
-  if (n == 0) return FF_OK;
-  if (!x_base || !pred) return fail(FF_ERR_INVALID_ARG, "x_base or the output labels are NULL");
   if ((int64_t)n * n_classes > INT32_MAX) return fail(FF_ERR_UNSUPPORTED, "n too large");
-  Carver size_cv(nullptr);
-  ScoreScratch tmp;
-  carve_score(size_cv, tmp, layers, n_layers, n, n_classes, hp->dtype, scores == nullptr);
-  FF_TRY(check_ws(ws, ws_bytes, size_cv.off + kAlign));
-  Carver cv(ws);
-  ScoreScratch s;
-  carve_score(cv, s, layers, n_layers, n, n_classes, hp->dtype, scores == nullptr);
-  float *S = scores ? scores : s.scores;
-  hipStream_t st = static_cast<hipStream_t>(stream);
+  return FF_OK;
+}
+
+// Scores every input under every label into S, then takes the argmax
+// (skipping exclude[i] when exclude is given); arguments already checked.
+ff_status score_run(const ff_layer *layers, int32_t n_layers, int32_t first_scored_layer,
+                    const ff_hparams *hp, const float *x_base, int32_t n, int32_t n_classes,
+                    const int32_t *exclude, float *S, int32_t *pred, ScoreScratch &s,
+                    hipStream_t st) {
   const bool bf16 = hp->dtype == FF_BF16;
   for (int n0 = 0; n0 < n; n0 += kScoreBlockImages) {
     const int nb = std::min(kScoreBlockImages, n - n0);
@@ -653,6 +653,24 @@ ff_status score_core(const ff_layer *layers, int32_t n_layers, int32_t first_sco
   FF_HIP(launch(FF_KERNEL_ARGMAX, 0.0, (double)n * n_classes * 4.0 + n * 4.0, st,
                 [&] { return ffk::launch_argmax(S, n, n_classes, exclude, pred, st); }));
   return FF_OK;
+}
+
+ff_status score_core(const ff_layer *layers, int32_t n_layers, int32_t first_scored_layer,
+                     const ff_hparams *hp, const float *x_base, int32_t n, int32_t n_classes,
+                     const int32_t *exclude, float *scores, int32_t *pred, void *ws,
+                     size_t ws_bytes, void *stream) {
+  FF_TRY(check_score_args(layers, n_layers, first_scored_layer, hp, n, n_classes));
+  if (n == 0) return FF_OK;
+  if (!x_base || !pred) return fail(FF_ERR_INVALID_ARG, "x_base or the output labels are NULL");
+  Carver size_cv(nullptr);
+  ScoreScratch tmp;
+  carve_score(size_cv, tmp, layers, n_layers, n, n_classes, hp->dtype, scores == nullptr);
+  FF_TRY(check_ws(ws, ws_bytes, size_cv.off + kAlign));
+  Carver cv(ws);
+  ScoreScratch s;
+  carve_score(cv, s, layers, n_layers, n, n_classes, hp->dtype, scores == nullptr);
+  return score_run(layers, n_layers, first_scored_layer, hp, x_base, n, n_classes, exclude,
+                   scores ? scores : s.scores, pred, s, static_cast<hipStream_t>(stream));
 }
 }  // namespace
 
@@ -833,14 +851,7 @@ ff_status ff_head_step(const ff_layer *layers, int32_t n_layers, int32_t first_l
   FF_TRY(head_features(layers, n_layers, first_layer, hp, x_base, n, C, hs, st, f));
   head_weights(f, head->W, head->b, D);
   const int splits = ffk::head_grad_splits(n);
-  const int64_t t = ++head->step;
-  ffk::AdamArgs a;
-  a.lr = head_hp->lr;
-  a.beta1 = head_hp->beta1;
-  a.beta2 = head_hp->beta2;
-  a.eps = head_hp->adam_eps;
-  a.bc1 = (float)(1.0 - pow((double)head_hp->beta1, (double)t));
-  a.bc2 = (float)(1.0 - pow((double)head_hp->beta2, (double)t));
+  const ffk::AdamArgs a = adam_args(head_hp, head->step + 1);
   const double feat_bytes = (double)n * D * 4.0 + (double)n * f.n_blocks * 4.0;
   FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * n * C * D, feat_bytes + (double)C * D * 4.0 + n * C * 4.0,
                 st, [&] {
@@ -857,6 +868,7 @@ ff_status ff_head_step(const ff_layer *layers, int32_t n_layers, int32_t first_l
                                                head->W, head->mW, head->vW, head->b, head->mb,
                                                head->vb, a, loss ? loss : hs.loss, st);
                 }));
+  ++head->step;
   return FF_OK;
 }
 
@@ -1122,10 +1134,14 @@ struct ChapterScratch {
   std::vector<float *> act[2], act_s[2];   // per stream: whole-set activities, ping-pong
   std::vector<float *> pub_w, pub_b;       // [l * kPubSlots + slot]
   std::vector<uint16_t *> pub_wb;          // bf16 shadows of the published weights
+  ScoreScratch score;                      // AdaptiveNEG: scoring of the whole set
 };
 
+// score_classes > 0: the AdaptiveNEG variant, which also scores the n samples
+// under that many labels.
 void carve_chapter(Carver &cv, ChapterScratch &c, const ff_layer *layers, int L, int n,
-                   int chunk, int n_streams, int dtype) {
+                   int chunk, int n_streams, int dtype, int score_classes = 0) {
+  if (score_classes > 0) carve_score(cv, c.score, layers, L, n, score_classes, dtype, true);
   const int rows = 2 * std::min(chunk, n);
   int max_in = 0, max_out = 0, max_hidden = 0;
   for (int l = 0; l < L; ++l) {
@@ -1175,12 +1191,29 @@ size_t ff_chapter_workspace_size(const ff_layer *layers, int32_t n_layers, int32
   return cv.off + kAlign;
 }
 
-ff_status ff_chapter_train(ff_layer *layers, int32_t n_layers, const ff_hparams *hp,
-                           const float *x_base, const int32_t *y_pos,
-                           const int32_t *y_neg_chapters, int32_t n, int32_t n_classes,
-                           int32_t chunk_pairs, int32_t epochs, int32_t splits,
-                           int32_t cooldown_start, int32_t assignment, int32_t n_streams,
-                           void *const *streams, float *loss_trace, void *ws, size_t ws_bytes) {
+size_t ff_chapter_adaptive_workspace_size(const ff_layer *layers, int32_t n_layers, int32_t n,
+                                          int32_t n_classes, int32_t chunk_pairs,
+                                          int32_t n_streams, int32_t dtype) {
+  if (!layers || n_layers <= 0 || n <= 0 || n_classes <= 0 || chunk_pairs <= 0 || n_streams <= 0)
+    return 0;
+  Carver cv(nullptr);
+  ChapterScratch c;
+  carve_chapter(cv, c, layers, n_layers, n, chunk_pairs, n_streams, dtype, n_classes);
+  return cv.off + kAlign;
+}
+}  // extern "C"
+
+namespace {
+// Both chapter entry points.  adaptive: chapter c's wrong labels are computed
+// on the device when the chapter starts, from the network as every layer left
+// it after chapter c-1 (AdaptiveNEG), and written to y_neg_chapters[c];
+// otherwise they are read from it.
+ff_status chapter_core(ff_layer *layers, int32_t n_layers, const ff_hparams *hp,
+                       const float *x_base, const int32_t *y_pos, int32_t *y_neg_chapters,
+                       int32_t n, int32_t n_classes, int32_t chunk_pairs, int32_t epochs,
+                       int32_t splits, int32_t cooldown_start, int32_t assignment,
+                       int32_t n_streams, void *const *streams, float *loss_trace, void *ws,
+                       size_t ws_bytes, bool adaptive, int32_t first_scored_layer) {
   FF_TRY(check_hp(hp));
   FF_TRY(check_stack(layers, n_layers, hp, true));
   if (n <= 0 || chunk_pairs <= 0 || splits <= 0 || epochs <= 0 || epochs % splits)
@@ -1197,13 +1230,19 @@ ff_status ff_chapter_train(ff_layer *layers, int32_t n_layers, const ff_hparams 
   if ((int64_t)2 * n > INT32_MAX) return fail(FF_ERR_UNSUPPORTED, "n too large");
   if (!x_base || !y_pos || !y_neg_chapters || !streams)
     return fail(FF_ERR_INVALID_ARG, "NULL pointer argument");
+  if (adaptive) {
+    if (n_classes < 2) return fail(FF_ERR_INVALID_ARG, "n_classes=%d: no wrong label", n_classes);
+    FF_TRY(check_score_args(layers, n_layers, first_scored_layer, hp, n, n_classes));
+  }
+  const int score_classes = adaptive ? n_classes : 0;
   Carver size_cv(nullptr);
   ChapterScratch tmp;
-  carve_chapter(size_cv, tmp, layers, n_layers, n, chunk_pairs, n_streams, hp->dtype);
+  carve_chapter(size_cv, tmp, layers, n_layers, n, chunk_pairs, n_streams, hp->dtype,
+                score_classes);
   FF_TRY(check_ws(ws, ws_bytes, size_cv.off + kAlign));
   Carver cv(ws);
   ChapterScratch cs;
-  carve_chapter(cv, cs, layers, n_layers, n, chunk_pairs, n_streams, hp->dtype);
+  carve_chapter(cv, cs, layers, n_layers, n, chunk_pairs, n_streams, hp->dtype, score_classes);
 
   const int L = n_layers, S = splits, per = epochs / splits;
   const int nc = (n + chunk_pairs - 1) / chunk_pairs;
@@ -1231,7 +1270,19 @@ ff_status ff_chapter_train(ff_layer *layers, int32_t n_layers, const ff_hparams 
     return in;
   };
 
-  for (int c = 0; c < S; ++c)
+  for (int c = 0; c < S; ++c) {
+    if (adaptive) {
+      // UpdateXNEG: on the worker that trains layer 0 in this chapter, once
+      // every layer has finished chapter c-1 (no layer starts chapter c before
+      // layer 0, which follows this on the same stream), score the whole set
+      // with the live weights and take the best wrong label of each sample.
+      const int si = assignment == FF_SINGLE_LAYER ? 0 : c % n_streams;
+      hipStream_t st = static_cast<hipStream_t>(streams[si]);
+      if (c > 0)
+        for (int l = 0; l < L; ++l) FF_HIP(hipStreamWaitEvent(st, ev(pub, l, c - 1), 0));
+      FF_TRY(score_run(layers, L, first_scored_layer, hp, x_base, n, n_classes, y_pos,
+                       cs.score.scores, y_neg_chapters + (size_t)c * n, cs.score, st));
+    }
     for (int l = 0; l < L; ++l) {
       const int si = assignment == FF_SINGLE_LAYER ? l : c % n_streams;
       hipStream_t st = static_cast<hipStream_t>(streams[si]);
@@ -1291,7 +1342,36 @@ ff_status ff_chapter_train(ff_layer *layers, int32_t n_layers, const ff_hparams 
       }
       FF_HIP(hipEventRecord(ev(pub, l, c), st));
     }
+  }
   return FF_OK;
+}
+}  // namespace
+
+extern "C" {
+
+ff_status ff_chapter_train(ff_layer *layers, int32_t n_layers, const ff_hparams *hp,
+                           const float *x_base, const int32_t *y_pos,
+                           const int32_t *y_neg_chapters, int32_t n, int32_t n_classes,
+                           int32_t chunk_pairs, int32_t epochs, int32_t splits,
+                           int32_t cooldown_start, int32_t assignment, int32_t n_streams,
+                           void *const *streams, float *loss_trace, void *ws, size_t ws_bytes) {
+  // given negatives are only read
+  return chapter_core(layers, n_layers, hp, x_base, y_pos, const_cast<int32_t *>(y_neg_chapters),
+                      n, n_classes, chunk_pairs, epochs, splits, cooldown_start, assignment,
+                      n_streams, streams, loss_trace, ws, ws_bytes, false, 0);
+}
+
+ff_status ff_chapter_train_adaptive(ff_layer *layers, int32_t n_layers, const ff_hparams *hp,
+                                    const float *x_base, const int32_t *y_pos,
+                                    int32_t *y_neg_chapters, int32_t n, int32_t n_classes,
+                                    int32_t chunk_pairs, int32_t epochs, int32_t splits,
+                                    int32_t cooldown_start, int32_t assignment,
+                                    int32_t first_scored_layer, int32_t n_streams,
+                                    void *const *streams, float *loss_trace, void *ws,
+                                    size_t ws_bytes) {
+  return chapter_core(layers, n_layers, hp, x_base, y_pos, y_neg_chapters, n, n_classes,
+                      chunk_pairs, epochs, splits, cooldown_start, assignment, n_streams, streams,
+                      loss_trace, ws, ws_bytes, true, first_scored_layer);
 }
 
 
@@ -1452,6 +1532,13 @@ ff_status ff_po_predict(const ff_layer *layers, const ff_head *heads, int32_t n_
   FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * n * C * D, (double)n * D * 4.0 + C * D * 4.0, st, [&] {
     return ffk::launch_head_logits(f, n, C, nullptr, logits, pred, nullptr, nullptr, st);
   }));
+  return FF_OK;
+}
+
+ff_status ff_fail_next_launch(int32_t kind) {
+  if (kind < -1 || kind >= FF_KERNEL_KINDS)
+    return fail(FF_ERR_INVALID_ARG, "kind=%d outside [-1, %d)", kind, (int)FF_KERNEL_KINDS);
+  g_fail_kind.store(kind);
   return FF_OK;
 }
 

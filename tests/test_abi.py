@@ -207,6 +207,45 @@ def test_chapter_rejects_on_host(P):
     assert layers[0].step == 0 and layers[1].step == 0
 
 
+def test_chapter_adaptive_rejects_on_host(P):
+    layers = (P._lib.ff_layer * 2)(_layer(P, 16, 8), _layer(P, 8, 8))
+    hp = _hp(P)
+    streams = (ctypes.c_void_p * 2)(None, None)
+
+    def call(n_classes=10, first=0, epochs=4, ws_bytes=1 << 30, y_neg=ctypes.c_void_p(4096)):
+        return P.LIB.ff_chapter_train_adaptive(layers, 2, ctypes.byref(hp), ctypes.c_void_p(4096),
+                                               ctypes.c_void_p(4096), y_neg, 100, n_classes, 32,
+                                               epochs, 2, 2, 0, first, 2, streams, None,
+                                               ctypes.c_void_p(1 << 20), ws_bytes)
+
+    assert call(n_classes=1) == -1  # no wrong label to choose
+    assert call(first=2) == -1  # first_scored_layer past the last layer
+    assert call(epochs=3) == -1
+    assert call(y_neg=None) == -1
+    need = P.LIB.ff_chapter_adaptive_workspace_size(layers, 2, 100, 10, 32, 2, 0)
+    assert need > P.LIB.ff_chapter_workspace_size(layers, 2, 100, 32, 2, 0)
+    assert call(ws_bytes=need - 512) == -3
+    assert layers[0].step == 0 and layers[1].step == 0
+
+
+def test_failed_launch_leaves_the_step_count(P):
+    """A launch that fails (forced by the test hook before anything is
+    enqueued) makes the entry point return FF_ERR_HIP with the Adam step count
+    unchanged; the hook fires once, and -1 disarms it."""
+    L = _layer(P)
+    hp = _hp(P)
+    assert P.LIB.ff_fail_next_launch(99) == -1
+    assert P.LIB.ff_fail_next_launch(1) == 0  # the forward product
+    try:
+        # normalised fp32 rows: the forward product is the step's first launch
+        st = P.LIB.ff_layer_step(ctypes.byref(L), ctypes.byref(hp), ctypes.c_void_p(4096), 4, 4,
+                                 1, None, None, None, ctypes.c_void_p(1 << 20), 1 << 30, None)
+        assert st == -4 and L.step == 0
+        assert b"failed" in P.LIB.ff_last_error()
+    finally:
+        assert P.LIB.ff_fail_next_launch(-1) == 0
+
+
 def test_pipeline_rejects_on_host(P):
     layers = (P._lib.ff_layer * 2)(_layer(P, 16, 8), _layer(P, 8, 8))
     hp = _hp(P)

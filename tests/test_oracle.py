@@ -395,6 +395,70 @@ def test_chapters_layer_major_order_and_negative_redraw():
     np.testing.assert_array_equal(t_other[0, :len(chunks)], t_ref[0, :len(chunks)])
 
 
+def _hand_adaptive_case(n=40, seed=5):
+    """The hand-designed layer of the AdaptiveNEG test: label c's score rises
+    with data feature d_c, so the hardest wrong label is the largest d_c over
+    the labels other than the true one."""
+    C = 10
+    rng = np.random.default_rng(seed)
+    data = rng.uniform(0, 1, (n, C))
+    x_base = np.concatenate([rng.uniform(0, 1, (n, C)), data], axis=1)
+    W = np.zeros((C, 2 * C))
+    W[np.arange(C), np.arange(C)] = 1.0
+    W[np.arange(C), C + np.arange(C)] = 1.0
+    order = np.argsort(-data, axis=1)
+    y = np.where(np.arange(n) % 2 == 0, order[:, 0], rng.integers(0, C, n)).astype(np.int32)
+    want = np.where(order[:, 0] == y, order[:, 1], order[:, 0])
+    return x_base, y, W, want
+
+
+def test_adaptive_chapters_draw_negatives_from_the_network_at_chapter_start():
+    """AdaptiveNEG chapters: chapter 0 takes the hardest wrong labels of the
+    initial network (known by construction of the hand-designed layer); with
+    the rate 0 the network never changes, so every chapter takes them."""
+    x_base, y, W, want = _hand_adaptive_case()
+    hp = O.HParams(lr=0.03)
+    rec = []
+    O.chapter_train([O.Layer.from_params(W, np.zeros(10))], x_base, y,
+                    O.adaptive_chapter_negatives(x_base, y, 10, hp, record=rec), 10, 16, 4, 2, 4,
+                    hp)
+    assert len(rec) == 2
+    np.testing.assert_array_equal(rec[0], want)
+    assert np.all(rec[1] != y)
+    rec0 = []
+    hp0 = O.HParams(lr=0.0)
+    O.chapter_train([O.Layer.from_params(W, np.zeros(10))], x_base, y,
+                    O.adaptive_chapter_negatives(x_base, y, 10, hp0, record=rec0), 10, 16, 3, 3, 3,
+                    hp0)
+    for r in rec0:
+        np.testing.assert_array_equal(r, want)
+
+
+def test_adaptive_chapters_are_the_given_negatives_of_each_chapter_start():
+    """Chapter c's AdaptiveNEG labels are adaptive_negatives of the network after
+    chapter c-1: training on those labels as given negatives reproduces the run
+    bit for bit, and the labels of chapter 1 are those of the network after a
+    one-chapter run on chapter 0's labels."""
+    x_base, y, _ = make_data(66, 120, 30)
+    params = make_weights(67, (30, 20, 16))
+    hp = O.HParams(lr=0.05)
+    E, S, chunk, cool = 4, 2, 32, 2
+    rec = []
+    A = [O.Layer.from_params(W, b) for W, b in params]
+    ta = O.chapter_train(A, x_base, y, O.adaptive_chapter_negatives(x_base, y, 10, hp, record=rec),
+                         10, chunk, E, S, cool, hp)
+    B = [O.Layer.from_params(W, b) for W, b in params]
+    tb = O.chapter_train(B, x_base, y, rec, 10, chunk, E, S, cool, hp)
+    np.testing.assert_array_equal(ta, tb)
+    for la, lb in zip(A, B):
+        np.testing.assert_array_equal(la.W, lb.W)
+    C0 = [O.Layer.from_params(W, b) for W, b in params]
+    np.testing.assert_array_equal(rec[0], O.adaptive_negatives(C0, x_base, y, 10, hp)[1])
+    O.chapter_train(C0, x_base, y, [rec[0]], 10, chunk, E // S, 1, E, hp)  # chapter 0 only
+    np.testing.assert_array_equal(rec[1], O.adaptive_negatives(C0, x_base, y, 10, hp)[1])
+    assert np.any(rec[1] != rec[0])
+
+
 # ---------------------------------------------------------------- softmax head
 def test_embed_neutral_hand():
     x = np.arange(24, dtype=np.float32).reshape(2, 12) / 10
