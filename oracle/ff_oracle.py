@@ -389,6 +389,10 @@ class Head:
         return Head(W, b, np.zeros_like(W), np.zeros_like(W), np.zeros_like(b),
                     np.zeros_like(b))
 
+    def copy(self) -> "Head":
+        return Head(self.W.copy(), self.b.copy(), self.mW.copy(), self.vW.copy(),
+                    self.mb.copy(), self.vb.copy(), self.t)
+
 
 def head_features(layers: Sequence[Layer], x_base: np.ndarray, n_classes: int, hp: HParams,
                   first_layer: int = 1) -> np.ndarray:
@@ -484,38 +488,49 @@ def po_layer_step(L: Layer, head: Head, x: np.ndarray, y: np.ndarray, hp: HParam
 
 
 def po_train_pipelined(layers: List[Layer], heads: List[Head], x_base, y, n_classes: int,
-                       chunk_pairs: int, epochs: int, hp: HParams, head_hp: HParams) -> np.ndarray:
+                       chunk_pairs: int, epochs: int, hp: HParams, head_hp: HParams,
+                       on_step=None) -> np.ndarray:
     """Performance-Optimised PFF over chunks in the layer-per-stage pipeline: layer
     l trains chunk c on layer l-1's activities of chunk c (computed before that
     step's update), as the FF pipeline does.  Layer 0 sees the neutrally
     labelled input (a reading: no label is given to a network that predicts it).
-    Returns the loss trace ``[L, epochs * n_chunks]``."""
+    Returns the loss trace ``[L, epochs * n_chunks]``.  ``on_step(l, layer,
+    head, x, y, result)``, if given, sees copies of the layer and its classifier
+    before each step, the step's input and labels, and what po_layer_step
+    returned (test bookkeeping; no effect on results)."""
     chunks = chunk_bounds(x_base.shape[0], chunk_pairs)
     trace = np.zeros((len(layers), epochs * len(chunks)))
     for e in range(epochs):
         for ci, (s, b) in enumerate(chunks):
             a = embed_neutral(x_base[s:s + b], n_classes)
             for li, (L, Hd) in enumerate(zip(layers, heads)):
-                loss, a, *_ = po_layer_step(L, Hd, a, y[s:s + b], hp, head_hp)
+                pre = (L.copy(), Hd.copy(), a) if on_step else None
+                res = po_layer_step(L, Hd, a, y[s:s + b], hp, head_hp)
+                if on_step:
+                    on_step(li, pre[0], pre[1], pre[2], y[s:s + b], res)
+                loss, a = res[0], res[1]
                 trace[li, e * len(chunks) + ci] = loss
     return trace
 
 
 def po_train_sequential(layers: List[Layer], heads: List[Head], x_base, y, n_classes: int,
                         chunk_pairs: int, epochs: int, hp: HParams,
-                        head_hp: HParams) -> np.ndarray:
+                        head_hp: HParams, on_step=None) -> np.ndarray:
     """Performance-Optimised training one layer after another (the sequential FF
     schedule of Sec. 3): layer l takes all its steps over the chunks, then its
     output with its final weights is the next layer's input.  Returns the loss
-    trace ``[L, epochs * n_chunks]``."""
+    trace ``[L, epochs * n_chunks]``.  ``on_step`` as for po_train_pipelined."""
     chunks = chunk_bounds(x_base.shape[0], chunk_pairs)
     trace = np.zeros((len(layers), epochs * len(chunks)))
     a_all = embed_neutral(x_base, n_classes)
     for li, (L, Hd) in enumerate(zip(layers, heads)):
         for e in range(epochs):
             for ci, (s, b) in enumerate(chunks):
-                trace[li, e * len(chunks) + ci] = po_layer_step(L, Hd, a_all[s:s + b], y[s:s + b],
-                                                                hp, head_hp)[0]
+                pre = (L.copy(), Hd.copy()) if on_step else None
+                res = po_layer_step(L, Hd, a_all[s:s + b], y[s:s + b], hp, head_hp)
+                if on_step:
+                    on_step(li, pre[0], pre[1], a_all[s:s + b], y[s:s + b], res)
+                trace[li, e * len(chunks) + ci] = res[0]
         a_all = layer_forward(L.W, L.b, a_all, hp.norm_eps, False, hp.bf16)[2]
     return trace
 

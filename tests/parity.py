@@ -72,20 +72,40 @@ def r1_goodness_slack(Wb, xh, h, band=2.0 ** -18):
     return slack
 
 
+def r1_activity_slack(Wb, xh, band=2.0 ** -18):
+    """Per-element activity allowance for open R1 roundings (see
+    r1_goodness_slack): |dh_rj| <= D_rj = sum over row r's open elements i of
+    |W_ji| u_i, since relu moves by at most the shift of z.  Returns [R, d_out]
+    (zero on rows without an open element)."""
+    xh = np.asarray(xh, np.float64)
+    Wa = np.abs(np.asarray(Wb, np.float64))
+    lo = bf16_round(xh * (1.0 - band))
+    hi = bf16_round(xh * (1.0 + band))
+    open_ = lo != hi
+    D = np.zeros((xh.shape[0], Wa.shape[0]))
+    rows = np.nonzero(open_.any(axis=1))[0]
+    if rows.size:
+        D[rows] = np.where(open_[rows], bf16_ulp(hi[rows]), 0.0) @ Wa.T
+    return D
+
+
 def assert_loss(l, ref, rel=1e-4):
     assert abs(float(l) - float(ref)) <= rel * abs(float(ref)), f"loss {l} vs {ref}"
 
 
-def assert_acts(h, ref, rel=1e-4, floor=1e-5):
+def assert_acts(h, ref, rel=1e-4, floor=1e-5, slack=None):
     """|dh| <= rel |h_ref| + floor max|h_ref|.
 
     bf16 operands: a value that lies within fp32 rounding of a bf16 rounding
     boundary can round to neighbouring bf16 values on the two sides (the device
     computes it in fp32, the oracle in fp64); one such operand moves z by one bf16
     ulp (2^-8 relative) of one product term, about 1e-4 of max|h| at these
-    shapes, so the bf16 tests use floor = 1e-3."""
+    shapes.  `slack` (bf16): r1_activity_slack, the per-element bound of that
+    effect, added to the fp32 bar."""
     h = np.asarray(h, np.float64)
     tol = rel * np.abs(ref) + floor * max(np.abs(ref).max(), 1e-30)
+    if slack is not None:
+        tol = tol + slack
     bad = np.abs(h - ref) > tol
     assert not bad.any(), f"activities: {bad.sum()} of {bad.size} off, max abs err " \
                           f"{np.max(np.abs(h - ref)):.3g}"
@@ -123,6 +143,32 @@ def ill_conditioned(grads, mags, lr=None, adam_eps=1e-8, tol=None, split=False):
     return (cond, amp & ~cond) if split else cond | amp
 
 
+class Conditioning:
+    """The flags of ill_conditioned kept step by step, for runs too long to hold
+    every step's gradients: add(grad, mag) per update of one tensor; the
+    sign-flip flags are OR-ed, and for the Adam-amplified set the largest
+    eps 1e-5 mag / (|g| + eps)^2 over the steps is kept, to be scaled by the
+    learning rate when the set is taken."""
+
+    def __init__(self, adam_eps=1e-8):
+        self.eps = adam_eps
+        self.cond = None
+        self.q = None
+
+    def add(self, grad, mag):
+        a = np.abs(np.asarray(grad, np.float64))
+        mg = np.asarray(mag, np.float64)
+        c = (a > 0) & (a < 1e-5 * mg)
+        q = np.where(a > 0, self.eps * 1e-5 * mg / (a + self.eps) ** 2, 0.0)
+        self.cond = c if self.cond is None else self.cond | c
+        self.q = q if self.q is None else np.maximum(self.q, q)
+
+    def masks(self, lr, tol):
+        """(sign-flip set, Adam-amplified set) as ill_conditioned(split=True)."""
+        amp = np.zeros_like(self.cond) if lr is None else (lr * self.q > 0.5 * tol)
+        return self.cond, amp & ~self.cond
+
+
 def assert_weights(W, ref, grads, mags, what="W", rel=1e-3, outliers=0.0, outlier_rel=0.0,
                    lr=None, adam_eps=1e-8):
     """Weights after k Adam steps (see the module docstring).
@@ -140,9 +186,16 @@ def assert_weights(W, ref, grads, mags, what="W", rel=1e-3, outliers=0.0, outlie
     sides may round one operand of a gradient sum one bf16 ulp apart (the value
     sits within fp32 rounding of a bf16 rounding boundary), which moves that sum
     by 2^-8 of one term; Adam's per-element normalisation can turn that into a
-    weight difference above the fp32 bar for the rare elements it touches."""
+    weight difference above the fp32 bar for the rare elements it touches.
+
+    `grads` may instead be a Conditioning that has seen every update (then
+    `mags` is not used)."""
     W = np.asarray(W, np.float64)
-    cond, amp = ill_conditioned(grads, mags, lr, adam_eps, rel * np.abs(ref) + 1e-6, split=True)
+    if isinstance(grads, Conditioning):  # flags kept step by step (mags unused)
+        cond, amp = grads.masks(lr, rel * np.abs(ref) + 1e-6)
+    else:
+        cond, amp = ill_conditioned(grads, mags, lr, adam_eps, rel * np.abs(ref) + 1e-6,
+                                    split=True)
     assert cond.mean() <= 1e-3, f"{what}: ill-conditioned fraction {cond.mean():.2e} > 1e-3"
     assert amp.mean() <= 1e-2, f"{what}: Adam-amplified fraction {amp.mean():.2e} > 1e-2"
     flag = cond | amp
