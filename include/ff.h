@@ -131,6 +131,27 @@ ff_status ff_layer_step(ff_layer *L, const ff_hparams *hp, const float *x, int32
                         int32_t n_neg, int32_t x_normalised, float *h_out, float *goodness,
                         float *loss, void *ws, size_t ws_bytes, void *stream);
 
+/* ---- No-allocation step ------------------------------------------------------
+ * For callers that cannot allocate device memory or take a workspace (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): ff_layer_step with its scratch in a fixed device array of
+ * FF_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on
+ * until the process ends.  No hipMalloc, hipFree or allocating library call.
+ * Arguments and results as ff_layer_step (the same kernels).  The scratch
+ * holds the normalised input and the goodness partials, plus the activities
+ * when h_out is NULL and the goodness and loss when those are NULL;
+ * a request that needs more returns FF_ERR_UNSUPPORTED before anything is
+ * enqueued (784 -> 2000 and 2000 -> 2000 fp32 layers on 2048 rows, and
+ * 3072 -> 3072 bf16 layers on 4096 rows with h_out, fit).  The scratch is
+ * found for the calling thread's current device, which must be the device
+ * of `stream`.  Every call on a GPU shares that GPU's one scratch: calls
+ * that overlap on one GPU (different streams or threads) race, so the
+ * caller must order them. */
+#define FF_NOALLOC_SCRATCH_BYTES (32u << 20)
+ff_status ff_layer_step_noalloc(ff_layer *L, const ff_hparams *hp, const float *x, int32_t n_pos,
+                                int32_t n_neg, int32_t x_normalised, float *h_out,
+                                float *goodness, float *loss, void *stream);
+
 /* Rewrite W_bf16 = bf16(W) (round to nearest even).  Call once after
  * initialising W in FF_BF16 mode; updates keep the shadow in sync after that. */
 ff_status ff_refresh_bf16_shadow(const ff_layer *L, void *stream);

@@ -32,7 +32,8 @@ EXPORTS = ["ff_status_string", "ff_last_error", "ff_embed_labels", "ff_step_work
            "ff_po_step_workspace_size", "ff_po_layer_step", "ff_po_epoch_workspace_size",
            "ff_po_epoch", "ff_po_predict_workspace_size", "ff_po_predict",
            "ff_pipeline_workspace_size",
-           "ff_pipeline_epoch", "ff_profile_start", "ff_profile_stop", "ff_fail_next_launch"]
+           "ff_pipeline_epoch", "ff_profile_start", "ff_profile_stop", "ff_fail_next_launch",
+           "ff_layer_step_noalloc"]
 
 KERNEL_KINDS = ["embed_norm", "forward", "loss", "dw_adam", "goodness", "argmax", "bf16_shadow",
                 "head"]
@@ -130,6 +131,8 @@ def _load() -> ctypes.CDLL:
         "ff_profile_start": (c_int32, [c_int32, ctypes.c_uint32]),
         "ff_profile_stop": (c_int32, [POINTER(ff_kernel_stats)]),
         "ff_fail_next_launch": (c_int32, [c_int32]),
+        "ff_layer_step_noalloc": (c_int32, [POINTER(ff_layer), POINTER(ff_hparams), P, c_int32,
+                                            c_int32, c_int32, P, P, P, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -299,6 +302,28 @@ def ff_layer_step(layer: Layer, hp: HParams, x: torch.Tensor, n_pos: int, n_neg:
                             _ptr(goodness, torch.float32, R, "goodness"),
                             _ptr(loss, torch.float32, 1, "loss"), _ptr(ws, torch.uint8),
                             ws.numel(), _stream(stream))
+    layer.step = Lc.step
+    _check(st)
+    return h_out, goodness, loss
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20  # FF_NOALLOC_SCRATCH_BYTES of include/ff.h
+
+
+def ff_layer_step_noalloc(layer: Layer, hp: HParams, x: torch.Tensor, n_pos: int, n_neg: int,
+                          x_normalised: bool = False, h_out: Optional[torch.Tensor] = None,
+                          goodness: Optional[torch.Tensor] = None,
+                          loss: Optional[torch.Tensor] = None, stream=None):
+    """ff_layer_step without a workspace: the library's fixed device scratch is
+    used (calls overlapping on one GPU race; the caller orders them)."""
+    R = n_pos + n_neg
+    Lc = layer.c()
+    st = LIB.ff_layer_step_noalloc(ctypes.byref(Lc), ctypes.byref(hp.c()),
+                                    _ptr(x, torch.float32, R * layer.d_in, "x"), n_pos, n_neg,
+                                    int(x_normalised),
+                                    _ptr(h_out, torch.float32, R * layer.d_out, "h_out"),
+                                    _ptr(goodness, torch.float32, R, "goodness"),
+                                    _ptr(loss, torch.float32, 1, "loss"), _stream(stream))
     layer.step = Lc.step
     _check(st)
     return h_out, goodness, loss

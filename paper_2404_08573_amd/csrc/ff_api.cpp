@@ -1,7 +1,7 @@
 // Host side of the C ABI declared in include/ff.h: argument validation,
 // workspace carving, launch sequencing, and the one-stream-per-layer pipeline
 // scheduler (Single-Layer PFF, Sec. 4.1 / Alg. 1, emulated on one GPU).
-#include <hip/hip_runtime_api.h>
+#include <hip/hip_runtime.h>
 
 #include <math.h>
 #include <stdarg.h>
@@ -521,6 +521,75 @@ ff_status ff_layer_step(ff_layer *L, const ff_hparams *hp, const float *x, int32
   Carver cv(ws);
   StepScratch s;
   carve_step(cv, s, R, L->d_in, L->d_out, hp->dtype, true, true, true);
+  LayerInput in;
+  in.src = rows_of(x);
+  in.normalised = x_normalised != 0;
+  return step_core(L, hp, in, n_pos, n_neg, h_out, goodness, loss, nullptr, s,
+                   static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// The no-allocation step: its scratch is this file-scope device array (each
+// GPU holds its own copy).  In host code `scratch` only names the symbol; its
+// device address, per device, comes from hipGetSymbolAddress.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[FF_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device, looked up on the first
+// call made with that device current and kept.
+ff_status scratch_of_current_device(void **out) {
+  int dev = -1;
+  FF_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(FF_ERR_UNSUPPORTED, "device %d: the no-allocation scratch table holds %d devices",
+                dev, kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    FF_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(FF_ERR_HIP, "hipGetSymbolAddress gave no address for the scratch");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return FF_OK;
+}
+}  // namespace
+
+extern "C" {
+
+ff_status ff_layer_step_noalloc(ff_layer *L, const ff_hparams *hp, const float *x, int32_t n_pos,
+                                int32_t n_neg, int32_t x_normalised, float *h_out,
+                                float *goodness, float *loss, void *stream) {
+  FF_TRY(check_hp(hp));
+  FF_TRY(check_layer(L, hp, true, 0));
+  if (n_pos < 1 || n_neg < 1)
+    return fail(FF_ERR_INVALID_ARG, "n_pos=%d n_neg=%d: both halves need at least one row",
+                n_pos, n_neg);
+  if (!x) return fail(FF_ERR_INVALID_ARG, "x is NULL");
+  const int R = n_pos + n_neg;
+  // scratch for what the caller does not receive: the activities only when
+  // h_out is NULL, the goodness and loss only when not passed
+  Carver size_cv(nullptr);
+  StepScratch tmp;
+  carve_step(size_cv, tmp, R, L->d_in, L->d_out, hp->dtype, !h_out, !goodness, !loss);
+  const size_t need = size_cv.off;
+  if (need > (size_t)FF_NOALLOC_SCRATCH_BYTES)
+    return fail(FF_ERR_UNSUPPORTED,
+                "%d rows of %d -> %d need %zu bytes of scratch; the no-allocation step holds %zu "
+                "(pass h_out, or use ff_layer_step with a workspace)",
+                R, L->d_in, L->d_out, need, (size_t)FF_NOALLOC_SCRATCH_BYTES);
+  void *base = nullptr;
+  FF_TRY(scratch_of_current_device(&base));
+  Carver cv(base);
+  StepScratch s;
+  carve_step(cv, s, R, L->d_in, L->d_out, hp->dtype, !h_out, !goodness, !loss);
   LayerInput in;
   in.src = rows_of(x);
   in.normalised = x_normalised != 0;
