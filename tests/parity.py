@@ -5,12 +5,14 @@ fp32 path:
   loss:             |dL| <= 1e-4 |L_ref|
   activities h:     |dh| <= 1e-4 |h_ref| + 1e-5 max|h_ref| (fp32 contraction over
                     d_in terms of unit-norm rows)
-  weights after k Adam steps: |dW| <= 1e-3 |W_ref| + 1e-6 outside the
+  weights after k Adam steps: |dW| <= 1e-3 |W_ref| + 1e-6 + 1e-5 lr E outside the
                     ill-conditioned set, i.e. elements whose oracle gradient had
                     0 < |g| < 1e-5 sum|terms| at some step (Adam's first steps move
                     by about lr*sign(g), so a gradient whose sum cancels down to
                     rounding-noise level can flip its update in any fp32
                     implementation); that set must be at most 1e-3 of the tensor.
+                    E (Conditioning) bounds to first order how far the Adam
+                    updates carry a gradient error of sum|terms| per step.
   labels:           bit-exact where the oracle's top-two gap is >= 1e-4 relative.
 bf16 path (compared with the bf16-emulating oracle, which rounds the same three
   operands): goodness, scores and loss within 1e-3 relative (plus, for the
@@ -144,65 +146,99 @@ def ill_conditioned(grads, mags, lr=None, adam_eps=1e-8, tol=None, split=False):
 
 
 class Conditioning:
-    """The flags of ill_conditioned kept step by step, for runs too long to hold
-    every step's gradients: add(grad, mag) per update of one tensor; the
-    sign-flip flags are OR-ed, and for the Adam-amplified set the largest
-    eps 1e-5 mag / (|g| + eps)^2 over the steps is kept, to be scaled by the
-    learning rate when the set is taken."""
+    """Per-element bookkeeping of one Adam-updated tensor over a run, fed every
+    update's oracle gradient g and term magnitudes mag = sum of |terms|:
 
-    def __init__(self, adam_eps=1e-8):
-        self.eps = adam_eps
-        self.cond = None
-        self.q = None
+    * cond: the sign-flip set of ill_conditioned (0 < |g| < 1e-5 mag at some step);
+    * E: a first-order bound on how far a gradient error of at most mag per
+      step can move the parameter through the Adam updates, per unit learning
+      rate (the bar multiplies it by lr and by the gradient allowance 1e-5).
+
+    Adam's step t applies u_t = m_hat/(sqrt(v_hat) + eps), with
+    m = beta1 m + (1 - beta1) g and v = beta2 v + (1 - beta2) g^2.  An error d_s
+    in the gradient of step s <= t moves u_t by
+      d_s [(1-beta1) beta1^(t-s) / (bc1 (sqrt(v_hat) + eps))
+           - m_hat (1-beta2) beta2^(t-s) g_s / (bc2 sqrt(v_hat) (sqrt(v_hat) + eps)^2)]
+    (bc1, bc2 the bias corrections of step t).  The term of the current step is
+    taken with its sign (at t = 1 it is eps/(|g| + eps)^2, so the nearly
+    sign-like first update is insensitive unless |g| is near eps); the terms
+    of earlier steps, carried by the moments, are bounded in absolute value
+    through the running sums A = sum beta1^(t-s) mag_s and
+    B = sum beta2^(t-s) |g_s| mag_s.  E = sum over steps of the resulting bound
+    on |du_t|.  It leaves out the feedback of weight differences into later
+    gradients."""
+
+    def __init__(self, beta1=0.9, beta2=0.999, adam_eps=1e-8):
+        self.b1, self.b2, self.eps = beta1, beta2, adam_eps
+        self.t = 0
+        self.cond = self.E = None
 
     def add(self, grad, mag):
-        a = np.abs(np.asarray(grad, np.float64))
-        mg = np.asarray(mag, np.float64)
-        c = (a > 0) & (a < 1e-5 * mg)
-        q = np.where(a > 0, self.eps * 1e-5 * mg / (a + self.eps) ** 2, 0.0)
-        self.cond = c if self.cond is None else self.cond | c
-        self.q = q if self.q is None else np.maximum(self.q, q)
+        g = np.asarray(grad, np.float64)
+        e = np.asarray(mag, np.float64)
+        b1, b2, eps = self.b1, self.b2, self.eps
+        if self.t == 0:
+            z = np.zeros_like(g)
+            self.cond = np.zeros(g.shape, bool)
+            self.m, self.v, self.A, self.B, self.E = z.copy(), z.copy(), z.copy(), z.copy(), z
+            self.g_prev, self.e_prev = z, z
+        self.t += 1
+        t = self.t
+        self.A = b1 * (self.A + self.e_prev)
+        self.B = b2 * (self.B + np.abs(self.g_prev) * self.e_prev)
+        self.m = b1 * self.m + (1 - b1) * g
+        self.v = b2 * self.v + (1 - b2) * g * g
+        bc1, bc2 = 1 - b1 ** t, 1 - b2 ** t
+        mh = self.m / bc1
+        sv = np.sqrt(self.v / bc2)
+        den = np.where(sv > 0, sv, 1.0) * (sv + eps) ** 2
+        same = np.abs((1 - b1) / (bc1 * (sv + eps)) - mh * (1 - b2) * g / (bc2 * den)) * e
+        carried = ((1 - b1) * self.A / (bc1 * (sv + eps))
+                   + np.abs(mh) * (1 - b2) * self.B / (bc2 * den))
+        self.E = self.E + same + carried
+        a = np.abs(g)
+        self.cond = self.cond | ((a > 0) & (a < 1e-5 * e))
+        self.g_prev, self.e_prev = g, e
 
-    def masks(self, lr, tol):
-        """(sign-flip set, Adam-amplified set) as ill_conditioned(split=True)."""
-        amp = np.zeros_like(self.cond) if lr is None else (lr * self.q > 0.5 * tol)
-        return self.cond, amp & ~self.cond
+    @staticmethod
+    def of(grads, mags, adam_eps=1e-8):
+        c = Conditioning(adam_eps=adam_eps)
+        for g, m in zip(grads, mags):
+            c.add(g, m)
+        return c
 
 
 def assert_weights(W, ref, grads, mags, what="W", rel=1e-3, outliers=0.0, outlier_rel=0.0,
-                   lr=None, adam_eps=1e-8):
-    """Weights after k Adam steps (see the module docstring).
+                   lr=None, adam_eps=1e-8, grad_rel=1e-5):
+    """Weights (or Adam moments) after k Adam steps (see the module docstring).
 
-    `lr`, `adam_eps`: pass them when W is a parameter updated by Adam with
-    those settings (not for the moments), so elements whose update amplifies
-    gradient rounding past the bar are set aside (see ill_conditioned).  The
-    sign-flip set may hold at most 1e-3 of the elements, the amplified set at
-    most 1e-2: the latter grows when gradients are small next to Adam's eps,
-    and callers check the first moments (linear in the gradient, never
-    amplified) beside the weights.
+    The bar is |dW| <= rel |W_ref| + 1e-6 outside the sign-flip set (at most
+    1e-3 of the elements).  For a parameter (`lr` given) it adds
+    grad_rel lr E: the Adam updates' first-order response to a gradient error
+    of grad_rel times the sum of |terms| at every step (Conditioning; grad_rel
+    1e-5 is the gradient allowance of the sign-flip rule).  The moments are
+    linear in the gradients and take no such term.  `grads`, `mags`: the
+    lists of every update's oracle gradient and term magnitudes, or a
+    Conditioning that has seen them (then `mags` is not used).
 
     `outliers` (bf16 comparisons only): the fraction of elements allowed to
-    exceed `rel`, each still within `outlier_rel`.  With bf16 operands the two
+    exceed the bar, each still within `outlier_rel`.  With bf16 operands the two
     sides may round one operand of a gradient sum one bf16 ulp apart (the value
     sits within fp32 rounding of a bf16 rounding boundary), which moves that sum
     by 2^-8 of one term; Adam's per-element normalisation can turn that into a
-    weight difference above the fp32 bar for the rare elements it touches.
-
-    `grads` may instead be a Conditioning that has seen every update (then
-    `mags` is not used)."""
+    weight difference above the fp32 bar for the rare elements it touches."""
     W = np.asarray(W, np.float64)
-    if isinstance(grads, Conditioning):  # flags kept step by step (mags unused)
-        cond, amp = grads.masks(lr, rel * np.abs(ref) + 1e-6)
-    else:
-        cond, amp = ill_conditioned(grads, mags, lr, adam_eps, rel * np.abs(ref) + 1e-6,
-                                    split=True)
+    c = grads if isinstance(grads, Conditioning) else Conditioning.of(grads, mags, adam_eps)
+    cond = c.cond
     assert cond.mean() <= 1e-3, f"{what}: ill-conditioned fraction {cond.mean():.2e} > 1e-3"
-    assert amp.mean() <= 1e-2, f"{what}: Adam-amplified fraction {amp.mean():.2e} > 1e-2"
-    flag = cond | amp
     err = np.abs(W - ref)
-    bad = (err > rel * np.abs(ref) + 1e-6) & ~flag
+    tol = rel * np.abs(ref) + 1e-6
+    if lr is not None:
+        tol = tol + grad_rel * lr * c.E
+    bad = (err > tol) & ~cond
     n_ok = int(outliers * bad.size)
-    msg = f"{what}: {bad.sum()} of {bad.size} off, worst abs {np.max(err[~flag]):.3g}"
+    msg = (f"{what}: {bad.sum()} of {bad.size} off, worst abs {np.max(err[~cond]):.3g}, "
+           f"worst excess over the bar {np.max((err - tol)[~cond]):.3g}")
     assert bad.sum() <= n_ok, msg
     if bad.any():
         assert np.all(err[bad] <= outlier_rel * np.abs(ref[bad]) + 1e-5), msg
@@ -243,3 +279,57 @@ def assert_negatives(y_neg, S_ref, y_ref, labels):
 def assert_rel_fro(W, ref, rel):
     d = np.linalg.norm(np.asarray(W, np.float64) - ref) / np.linalg.norm(ref)
     assert d <= rel, f"relative Frobenius error {d:.3g} > {rel}"
+
+
+def divergence(W, mW, ref, cond, rel=2e-3, lr=None, grad_rel=1e-5):
+    """How far one trained layer lies from the oracle's: the fraction of weights
+    beyond the single-step bar (rel |W_ref| + 1e-6 + grad_rel lr E, outside the
+    sign-flip set), and the relative Frobenius distances of W and of its first
+    Adam moment."""
+    W, mW = np.asarray(W, np.float64), np.asarray(mW, np.float64)
+    tol = rel * np.abs(ref.W) + 1e-6 + (grad_rel * lr * cond.E if lr is not None else 0.0)
+    off = (np.abs(W - ref.W) > tol) & ~cond.cond
+    return {"frac": float(off.mean()),
+            "fro_W": float(np.linalg.norm(W - ref.W) / np.linalg.norm(ref.W)),
+            "fro_mW": float(np.linalg.norm(mW - ref.mW) / max(np.linalg.norm(ref.mW), 1e-300))}
+
+
+def assert_run_like_fp32(dev, f32, refs, conds, trace, trace32, trace_ref, lr, bf16=True,
+                         factor=4.0):
+    """A multi-layer run against the oracle, bounded by what a plain float32
+    evaluation of the same run (tests/fp32_eval.py) does.
+
+    dev, f32: per layer (W, mW) of the device run and of the float32
+    evaluation; refs: the oracle's layers; conds: their Conditioning.  For
+    every layer, each divergence metric of the device (fraction of weights
+    past the single-step bar, 2e-3 relative in bf16 and 1e-3 in fp32 plus the
+    propagated allowance; relative Frobenius distance of W and of the first
+    moment) and the largest relative difference of its loss trace must be at
+    most `factor` times the float32 evaluation's, plus a floor (1e-4 of the
+    elements, 1e-6, 1e-5 for the trace).  Every layer also stays within the
+    workload's weight bar of the oracle as a relative Frobenius distance: 5e-2
+    in bf16, 1e-3 in fp32.
+
+    Why a relative bar: a later layer trains on activities produced by layers
+    that already differ slightly from the oracle's, and in bf16 those
+    activities' roundings go the other way where they sit within evaluation
+    error of a rounding boundary.  Neither is a per-step effect that a
+    single-step bar covers, and both sides move different elements (their
+    summation orders differ), but a correct evaluation moves about as many by
+    about as much."""
+    rel, cap = (2e-3, 5e-2) if bf16 else (1e-3, 1e-3)
+    for i, ((W, mW), (W32, mW32), R, c) in enumerate(zip(dev, f32, refs, conds)):
+        d = divergence(W, mW, R, c, rel=rel, lr=lr)
+        e = divergence(W32, mW32, R, c, rel=rel, lr=lr)
+        floors = {"frac": 1e-4, "fro_W": 1e-6, "fro_mW": 1e-6}
+        for k, fl in floors.items():
+            assert d[k] <= factor * e[k] + fl, \
+                f"layer {i} {k}: device {d[k]:.3g} vs float32 evaluation {e[k]:.3g}"
+        assert d["fro_W"] <= cap, f"layer {i}: relative Frobenius distance {d['fro_W']:.3g}"
+        tr = np.asarray(trace, np.float64)[i]
+        t32 = np.asarray(trace32, np.float64)[i]
+        tref = np.asarray(trace_ref, np.float64)[i]
+        dt = np.max(np.abs(tr - tref) / np.abs(tref))
+        d32 = np.max(np.abs(t32 - tref) / np.abs(tref))
+        assert dt <= factor * d32 + 1e-5, \
+            f"layer {i} loss trace: device {dt:.3g} vs float32 evaluation {d32:.3g}"
