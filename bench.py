@@ -56,9 +56,10 @@ def load_traffic(kernel, workload):
         return None
 
 
-KIND_OF = [("k_fwd", "forward"), ("k_dw_adam", "dw_adam"), ("k_embed_norm", "embed_norm"),
-           ("k_loss_rows", "loss"), ("k_goodness", "goodness"), ("k_argmax", "argmax"),
-           ("k_bf16_shadow", "bf16_shadow")]
+KIND_OF = [("k_fwd", "forward"), ("k_dw_adam", "dw_adam"), ("k_dw4", "dw_adam"),
+           ("k_embed_norm", "embed_norm"), ("k_loss_rows", "loss"), ("k_loss_t", "loss"),
+           ("k_goodness", "goodness"), ("k_argmax", "argmax"), ("k_bf16_shadow", "bf16_shadow"),
+           ("k_transpose_bf16", "transpose")]
 
 
 def focus_steps(rows, d_in, d_out, bf16, steps=3):

@@ -138,16 +138,17 @@ ff_status ff_layer_step(ff_layer *L, const ff_hparams *hp, const float *x, int32
  * FF_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on
  * until the process ends.  No hipMalloc, hipFree or allocating library call.
  * Arguments and results as ff_layer_step (the same kernels).  The scratch
- * holds the normalised input and the goodness partials, plus the activities
- * when h_out is NULL and the goodness and loss when those are NULL;
- * a request that needs more returns FF_ERR_UNSUPPORTED before anything is
- * enqueued (784 -> 2000 and 2000 -> 2000 fp32 layers on 2048 rows, and
- * 3072 -> 3072 bf16 layers on 4096 rows with h_out, fit).  The scratch is
+ * holds the normalised input, the goodness partials and, in bf16, the
+ * weight-gradient operands, plus the activities when h_out is NULL and the
+ * goodness and loss when those are NULL; a request that needs more returns
+ * FF_ERR_UNSUPPORTED before anything is enqueued (784 -> 2000 and
+ * 2000 -> 2000 layers on 2048 rows, and 3072 -> 3072 bf16 layers on 4096 rows
+ * with h_out, fit).  The scratch is
  * found for the calling thread's current device, which must be the device
  * of `stream`.  Every call on a GPU shares that GPU's one scratch: calls
  * that overlap on one GPU (different streams or threads) race, so the
  * caller must order them. */
-#define FF_NOALLOC_SCRATCH_BYTES (32u << 20)
+#define FF_NOALLOC_SCRATCH_BYTES (96u << 20)
 ff_status ff_layer_step_noalloc(ff_layer *L, const ff_hparams *hp, const float *x, int32_t n_pos,
                                 int32_t n_neg, int32_t x_normalised, float *h_out,
                                 float *goodness, float *loss, void *stream);
@@ -393,7 +394,8 @@ typedef enum {
   FF_KERNEL_ARGMAX = 5,      /* label argmax                                  */
   FF_KERNEL_SHADOW = 6,      /* bf16 weight shadow refresh                    */
   FF_KERNEL_HEAD = 7,        /* softmax layer: logits, gradient, Adam         */
-  FF_KERNEL_KINDS = 8
+  FF_KERNEL_TRANSPOSE = 8,   /* bf16 operand transposes of the weight gradient */
+  FF_KERNEL_KINDS = 9
 } ff_kernel_kind;
 
 typedef struct {

@@ -36,7 +36,7 @@ EXPORTS = ["ff_status_string", "ff_last_error", "ff_embed_labels", "ff_step_work
            "ff_layer_step_noalloc"]
 
 KERNEL_KINDS = ["embed_norm", "forward", "loss", "dw_adam", "goodness", "argmax", "bf16_shadow",
-                "head"]
+                "head", "transpose"]
 
 
 class FFError(RuntimeError):
@@ -307,7 +307,7 @@ def ff_layer_step(layer: Layer, hp: HParams, x: torch.Tensor, n_pos: int, n_neg:
     return h_out, goodness, loss
 
 
-NOALLOC_SCRATCH_BYTES = 32 << 20  # FF_NOALLOC_SCRATCH_BYTES of include/ff.h
+NOALLOC_SCRATCH_BYTES = 96 << 20  # FF_NOALLOC_SCRATCH_BYTES of include/ff.h
 
 
 def ff_layer_step_noalloc(layer: Layer, hp: HParams, x: torch.Tensor, n_pos: int, n_neg: int,

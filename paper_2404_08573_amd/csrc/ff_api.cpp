@@ -124,10 +124,17 @@ struct StepScratch {
   float *lrow = nullptr;  // [rows]
   float *part = nullptr;  // [head_grad_splits(rows)][C][d_out]
   float *dz = nullptr;    // [rows][d_out]
+  // bf16 FF training steps: the weight-gradient product's operands, row-major
+  // over the rows padded to Rp = padded_rows(rows), and the db partials
+  uint16_t *xt = nullptr;   // [d_in][Rp] x_hat^T
+  uint16_t *dzt = nullptr;  // [d_out][Rp] bf16(c . H)^T
+  float *dbp = nullptr;     // [Rp / 64][d_out]
 };
 
+// train: the scratch of a training step (the bf16 weight-gradient operands);
+// false for forward passes only.
 void carve_step(Carver &cv, StepScratch &s, int rows, int d_in, int d_out, int dtype, bool need_h,
-                bool need_g, bool need_loss, int po_classes = 0) {
+                bool need_g, bool need_loss, int po_classes = 0, bool train = true) {
   if (po_classes > 0) {
     s.G = static_cast<float *>(cv.take((size_t)rows * po_classes * 4));
     s.lrow = static_cast<float *>(cv.take((size_t)rows * 4));
@@ -143,6 +150,12 @@ void carve_step(Carver &cv, StepScratch &s, int rows, int d_in, int d_out, int d
   s.cs = static_cast<float *>(cv.take((size_t)rows * 4));
   s.lpart = static_cast<float *>(cv.take((size_t)ffk::loss_blocks(rows) * 2 * 4));
   if (need_loss) s.loss = static_cast<float *>(cv.take(4));
+  if (train && dtype == FF_BF16 && po_classes == 0 && d_in > 0) {
+    const size_t rp = (size_t)ffk::padded_rows(rows);
+    s.xt = static_cast<uint16_t *>(cv.take(rp * d_in * 2));
+    s.dzt = static_cast<uint16_t *>(cv.take(rp * d_out * 2));
+    s.dbp = static_cast<float *>(cv.take((size_t)ffk::loss_blocks(rows) * d_out * 4));
+  }
 }
 
 size_t step_ws_bytes(int rows, int d_in, int d_out, int dtype, bool need_h) {
@@ -313,8 +326,8 @@ ffk::AdamArgs adam_args(const ff_hparams *hp, int64_t t) {
   a.beta1 = hp->beta1;
   a.beta2 = hp->beta2;
   a.eps = hp->adam_eps;
-  a.bc1 = (float)(1.0 - pow((double)hp->beta1, (double)t));
-  a.bc2 = (float)(1.0 - pow((double)hp->beta2, (double)t));
+  a.lr_bc1 = (float)((double)hp->lr / (1.0 - pow((double)hp->beta1, (double)t)));
+  a.inv_bc2 = (float)(1.0 / (1.0 - pow((double)hp->beta2, (double)t)));
   return a;
 }
 
@@ -333,6 +346,39 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int
   const int nt = ffk::fwd_col_tiles(R, L->d_out, hp->dtype);
   FF_HIP(fwd(hp->dtype, xop, weight_operand(L, hp->dtype), L->b, in.rowscale, R, L->d_out,
              L->d_in, H, s.gpart, st));
+  if (hp->dtype == FF_BF16 && s.dzt) {
+    // bf16: the weight gradient as an NT product over the rows.  The loss pass
+    // also writes bf16(c . H)^T and the db partials; x_hat^T is transposed from
+    // the normalised bf16 rows.
+    const int Rp = ffk::padded_rows(R), nrb = ffk::loss_blocks(R);
+    const uint16_t *xh = static_cast<const uint16_t *>(xop);
+    FF_HIP(launch(FF_KERNEL_LOSS, 0.0,
+                  (double)nt * R * 4.0 + (double)R * L->d_out * 4.0 + (g ? R * 4.0 : 0.0) +
+                      (double)Rp * L->d_out * 2.0 + (double)nrb * L->d_out * 4.0,
+                  st, [&] {
+                    return ffk::launch_loss_t(s.gpart, nt, R, n_pos, hp->theta, H, L->d_out, g,
+                                              nullptr, s.lpart, s.dzt, s.dbp, st);
+                  }));
+    FF_HIP(launch(FF_KERNEL_TRANSPOSE, 0.0, (double)R * L->d_in * 2.0 + (double)Rp * L->d_in * 2.0,
+                  st, [&] { return ffk::launch_transpose_bf16(xh, R, L->d_in, s.xt, st); }));
+    ffk::LossFinish lf;
+    lf.lpart = s.lpart;
+    lf.nblk = nrb;
+    lf.n_pos = n_pos;
+    lf.n_neg = n_neg;
+    lf.loss = lo;
+    const int64_t t = L->step + 1;
+    const ffk::AdamArgs a = adam_args(hp, t);
+    const double params = (double)L->d_out * L->d_in;
+    const double bytes = (double)Rp * (L->d_out + L->d_in) * 2.0 + params * 26.0 +
+                         (double)nrb * L->d_out * 4.0 + L->d_out * 24.0;
+    FF_HIP(launch(FF_KERNEL_DW_ADAM, gemm_flops(L->d_out, L->d_in, R), bytes, st, [&] {
+      return ffk::launch_dw4(s.dzt, s.xt, L->d_out, L->d_in, R, L->W, L->mW, L->vW, L->W_bf16,
+                             s.dbp, L->b, L->mb, L->vb, a, lf, st);
+    }));
+    L->step = t;
+    return FF_OK;
+  }
   float *cs = in.rowscale ? s.cs : nullptr;
   FF_HIP(launch(FF_KERNEL_LOSS, 0.0,
                 (double)nt * R * 4.0 + R * (g ? 8.0 : 4.0) + (s_next ? R * 4.0 : 0.0) +
@@ -1009,7 +1055,7 @@ void carve_pipe(Carver &cv, PipeScratch &p, const ff_layer *layers, int L, int n
     p.step.assign(2, StepScratch());
     carve_step(cv, p.step[0], rows, max_in, max_out, dtype, true, false, false, po_classes);
     // the forward pass with the final weights, run beside the next layer's steps
-    carve_step(cv, p.step[1], rows, max_in, max_out, dtype, false, false, false);
+    carve_step(cv, p.step[1], rows, max_in, max_out, dtype, false, false, false, 0, false);
     int max_hidden = 0;
     for (int l = 0; l + 1 < L; ++l) max_hidden = std::max(max_hidden, layers[l].d_out);
     if (L > 1)

@@ -47,9 +47,11 @@ struct LabelExpand {
 };
 constexpr int kMaxExpand = 16;  // label counts up to this take the shared-base path
 
+// Adam update t: the bias corrections bc1 = 1 - beta1^t and bc2 = 1 - beta2^t
+// enter as lr / bc1 and 1 / bc2 (computed in double on the host).
 struct AdamArgs {
   float lr, beta1, beta2, eps;
-  float bc1, bc2;  // 1 - beta1^t, 1 - beta2^t
+  float lr_bc1, inv_bc2;
 };
 
 // Loss scalar finished by the dW kernel from the per-workgroup partials of
@@ -157,6 +159,29 @@ hipError_t launch_dw_adam(int dtype, const float *H, const float *c, const void 
                           const float *cs, int M, int N, int K, float *W, float *mW, float *vW,
                           uint16_t *Wb, float *b, float *mb, float *vb, const AdamArgs &a,
                           const LossFinish &lf, hipStream_t s);
+
+// Rows of the transposed bf16 weight-gradient operands: R rounded up to a
+// multiple of 64 (the extra columns are zeros).
+int padded_rows(int rows);
+
+// Loss rows as launch_loss (g, c into g_out, c_out when non-null, loss
+// partials lpart[loss_blocks(R)][2]) for a bf16 layer, plus its weight-gradient
+// operand dZ^T = bf16(c . H)^T [D][padded_rows(R)] (R3) and the fp32 column
+// sums of c . H over each 64-row block, dbp[loss_blocks(R)][D] (for db).
+hipError_t launch_loss_t(const float *gpart, int ntiles, int R, int n_pos, float theta,
+                         const float *H, int D, float *g_out, float *c_out, float *lpart,
+                         uint16_t *dzT, float *dbp, hipStream_t s);
+
+// xT [d][padded_rows(R)] = x^T for bf16 rows x [R][d] (d a multiple of 8),
+// zero in the columns past R.
+hipError_t launch_transpose_bf16(const uint16_t *x, int R, int d, uint16_t *xT, hipStream_t s);
+
+// bf16 weight gradient dW = dZ^T (xT)^T over padded_rows(R) rows (operands from
+// launch_loss_t and launch_transpose_bf16; M = d_out, N = d_in), with the Adam
+// update of W, its shadow Wb and b (db from dbp) fused, and the loss scalar of lf.
+hipError_t launch_dw4(const uint16_t *dzT, const uint16_t *xT, int M, int N, int R, float *W,
+                      float *mW, float *vW, uint16_t *Wb, const float *dbp, float *b, float *mb,
+                      float *vb, const AdamArgs &a, const LossFinish &lf, hipStream_t s);
 
 // g_r = sum_t gpart[t][r] into g (any of the outputs may be null);
 // out[r] = g_r (accumulate == 0) or out[r] += g_r (accumulate == 1);

@@ -85,13 +85,16 @@ __device__ __forceinline__ float sigmoid_f(float x) {
   return x >= 0.f ? 1.f / (1.f + e) : e / (1.f + e);
 }
 
+// One Adam update: m, v moments; p -= lr m_hat / (sqrt(v_hat) + eps).  The
+// square root and the reciprocal are the hardware's (about 1 ulp each, far
+// below what the update's fp32 inputs carry): the IEEE-exact sequences cost
+// several times the instructions, which matters in the one-wave-per-SIMD
+// epilogues that run this for every weight.
 __device__ __forceinline__ void adam_update(float &p, float &m, float &v, float g,
                                             const AdamArgs &a) {
   m = a.beta1 * m + (1.f - a.beta1) * g;
   v = a.beta2 * v + (1.f - a.beta2) * g * g;
-  const float mh = m / a.bc1;
-  const float vh = v / a.bc2;
-  p = p - a.lr * mh / (sqrtf(vh) + a.eps);
+  p = p - a.lr_bc1 * m * __builtin_amdgcn_rcpf(__builtin_amdgcn_sqrtf(v * a.inv_bc2) + a.eps);
 }
 
 // ---------------------------------------------------------------------------
@@ -653,7 +656,11 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd(const typename Operand<BF16
 // nt_mainloop with two LDS stages; same epilogue results as k_fwd.
 // ---------------------------------------------------------------------------
 
-template <int BM, int BN>
+// s_waitcnt operand: at most n vector-memory operations and no LDS operation
+// outstanding.
+constexpr int vmcnt_lgkm0(int n) { return 0x0070 | (n & 15) | ((n >> 4) << 14); }
+
+template <int BM, int BN, int NBUF = 2>
 __device__ __forceinline__ void nt_mainloop4(const uint16_t *__restrict__ X,
                                              const uint16_t *__restrict__ W, int M, int N, int K,
                                              int m0, int n0, uint16_t *sm,
@@ -663,10 +670,13 @@ __device__ __forceinline__ void nt_mainloop4(const uint16_t *__restrict__ X,
   constexpr int IA = BM / 8 / NW, IB = BN / 8 / NW;  // 8-row wave loads per k-tile
   constexpr int STAGE = (BM + BN) * BK;
   constexpr int KS = BK / 2 / VE;  // 16-deep k-steps per k-tile
-  constexpr int NM = MB * NB - 1, ND = MB + NB, NV = IA + IB;
+  // the last k-step of a k-tile has NM MFMAs after its barrier and ND
+  // fragment reads of the next k-tile: NS slots carry them with the loads
+  constexpr int NM = MB * NB - 1, ND = MB + NB, NV = IA + IB, NS = NM > ND ? NM : ND;
   static_assert(MB * 32 == TM && NB * 32 == TN && IA * 8 * NW == BM && IB * 8 * NW == BN,
                 "tile shape");
-  static_assert(ND <= NM && KS % 2 == 0, "a fragment read per MFMA");
+  static_assert(ND <= MB * NB && KS % 2 == 0, "a fragment read per MFMA");
+  static_assert(NBUF >= 2 && (NBUF - 1) * (IA + IB) < 64, "stages");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int li = lane & 31, kg = lane >> 5;
@@ -733,16 +743,19 @@ __device__ __forceinline__ void nt_mainloop4(const uint16_t *__restrict__ X,
 
   uint4 fa[2][MB], fb[2][NB];
   const int nk = (K + BK - 1) / BK;
+  // NBUF LDS stages: k-tiles 0..NBUF-1 are issued up front; k-tile kt + NBUF
+  // goes into k-tile kt's stage after the barrier that ends kt's reads, so
+  // NBUF - 1 k-tiles stay in flight beside the MFMAs.
 #pragma unroll
-  for (int j = 0; j < NV; ++j) issue1(0, 0, j);
+  for (int b = 0; b < NBUF; ++b)
 #pragma unroll
-  for (int j = 0; j < NV; ++j) issue1(1, 1, j);
-  __builtin_amdgcn_s_waitcnt(vmcnt_wait(NV));
+    for (int j = 0; j < NV; ++j) issue1(b, b, j);
+  __builtin_amdgcn_s_waitcnt(vmcnt_wait((NBUF - 1) * NV));
   lds_barrier();
 #pragma unroll
   for (int i = 0; i < ND; ++i) rd1(0, 0, i, fa[0], fb[0]);
   for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
+    const int buf = kt % NBUF, bnext = (kt + 1) % NBUF;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const int cur = ks & 1, nxt = cur ^ 1;
@@ -765,18 +778,21 @@ __device__ __forceinline__ void nt_mainloop4(const uint16_t *__restrict__ X,
         mm(0, 0, fa[cur][0], fb[cur][0]);
         __builtin_amdgcn_sched_barrier(0);
         // Every fragment of k-tile kt is in registers and k-tile kt + 1 has
-        // landed: one barrier opens kt + 1 and frees kt's stage for kt + 2.
-        __builtin_amdgcn_s_waitcnt(kWaitAll);
+        // landed (the loads of the NBUF - 2 tiles after it may still be in
+        // flight): one barrier opens kt + 1 and frees kt's stage for kt + NBUF.
+        __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0((NBUF - 2) * NV));
         lds_barrier();
         __builtin_amdgcn_sched_barrier(0);
         // Slots of (loads, one fragment read, one MFMA), kept in this order.
 #pragma unroll
-        for (int i = 0; i < NM; ++i) {
+        for (int i = 0; i < NS; ++i) {
 #pragma unroll
-          for (int j = (i * NV) / NM; j < ((i + 1) * NV) / NM; ++j) issue1(kt + 2, buf, j);
-          if (i < ND) rd1(buf ^ 1, 0, i, fa[nxt], fb[nxt]);
-          const int p = i + 1;
-          mm(p / NB, p % NB, fa[cur][p / NB], fb[cur][p % NB]);
+          for (int j = (i * NV) / NS; j < ((i + 1) * NV) / NS; ++j) issue1(kt + NBUF, buf, j);
+          if (i < ND) rd1(bnext, 0, i, fa[nxt], fb[nxt]);
+          if (i < NM) {
+            const int p = i + 1;
+            mm(p / NB, p % NB, fa[cur][p / NB], fb[cur][p % NB]);
+          }
           __builtin_amdgcn_sched_barrier(0);
         }
       }
@@ -849,6 +865,132 @@ __global__ __launch_bounds__(256) void k_fwd4(const uint16_t *__restrict__ X,
 }
 
 // ---------------------------------------------------------------------------
+// bf16 weight gradient on the four-wave main loop: dW = dZ^T (x_hat^T)^T over
+// the Rp rows (both operands row-major over the rows, from k_loss_t and
+// k_transpose_bf16), with the Adam update of W, its bf16 shadow and (column
+// tile 0) of b fused in the epilogue; the first workgroup also finishes the
+// loss.  The accumulators go through LDS half a tile at a time (the rows of
+// the waves with wm = 0, then wm = 1), and each thread keeps kAdamBatch
+// float4 updates' loads in flight, so the W, m, v traffic streams instead of
+// waiting on one load at a time.  db sums the 64-row column partials of
+// k_loss_t in a fixed order.
+// ---------------------------------------------------------------------------
+constexpr int kAdamBatch = 6;
+
+template <int BM, int BN, int NBUF>
+__global__ __launch_bounds__(256) void k_dw4(const uint16_t *__restrict__ dzT,
+                                             const uint16_t *__restrict__ xT, int M, int N,
+                                             int K, float *__restrict__ W, float *__restrict__ mW,
+                                             float *__restrict__ vW, uint16_t *__restrict__ Wb,
+                                             const float *__restrict__ dbp, int nrb,
+                                             float *__restrict__ bvec, float *__restrict__ mbv,
+                                             float *__restrict__ vbv, AdamArgs ad, LossFinish lf) {
+  constexpr int WN = 2, TM = BM / 2, TN = BN / 2, MB = TM / 32, NB = TN / 32;
+  constexpr int LDC = BN + 4;
+  constexpr int kMain = NBUF * (BM + BN) * 64;          // bf16 elements
+  constexpr int kEpi = TM * LDC * 2;                    // an fp32 half tile, in bf16 elements
+  __shared__ __attribute__((aligned(16))) uint16_t sm[kMain > kEpi ? kMain : kEpi];
+  const int nt = (N + BN - 1) / BN;
+  int tm, tn;
+  tile_of(blockIdx.x, (M + BM - 1) / BM, nt, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int li = lane & 31, kg = lane >> 5;
+
+  if (lf.loss && blockIdx.x == 0 && tid == 0) {
+    float sp = 0.f, sn = 0.f;
+    for (int i = 0; i < lf.nblk; ++i) {
+      sp += lf.lpart[2 * i];
+      sn += lf.lpart[2 * i + 1];
+    }
+    lf.loss[0] = sp / (float)lf.n_pos + sn / (float)lf.n_neg;
+  }
+
+  floatx16 acc[MB][NB];
+  nt_mainloop4<BM, BN, NBUF>(dzT, xT, M, N, K, m0, n0, sm, acc);
+
+  float *Cs = reinterpret_cast<float *>(sm);  // [TM][LDC]; the main-loop buffers are free
+  constexpr int Q = TM * (BN / 4);            // float4 updates per half tile
+#pragma unroll 1
+  for (int half = 0; half < 2; ++half) {
+    if (wm == half) {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            Cs[(mb * 32 + acc_row(r, kg)) * LDC + wn * TN + nb * 32 + li] = acc[mb][nb][r];
+    }
+    __syncthreads();
+    const int mh = m0 + half * TM;
+#pragma unroll 1
+    for (int i0 = tid; i0 < Q; i0 += 256 * kAdamBatch) {
+      float4 p[kAdamBatch], m[kAdamBatch], v[kAdamBatch];
+      size_t o[kAdamBatch];
+      bool ok[kAdamBatch];
+#pragma unroll
+      for (int u = 0; u < kAdamBatch; ++u) {
+        const int idx = i0 + 256 * u;
+        const int mr = idx / (BN / 4), n4 = (idx % (BN / 4)) * 4;
+        ok[u] = idx < Q && mh + mr < M && n0 + n4 < N;
+        o[u] = ok[u] ? (size_t)(mh + mr) * N + n0 + n4 : 0;
+        if (ok[u]) {
+          p[u] = ld4(W + o[u]);
+          m[u] = ld4(mW + o[u]);
+          v[u] = ld4(vW + o[u]);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kAdamBatch; ++u) {
+        if (!ok[u]) continue;
+        const int idx = i0 + 256 * u;
+        const int mr = idx / (BN / 4), n4 = (idx % (BN / 4)) * 4;
+        const float4 g = ld4(Cs + mr * LDC + n4);
+        adam_update(p[u].x, m[u].x, v[u].x, g.x, ad);
+        adam_update(p[u].y, m[u].y, v[u].y, g.y, ad);
+        adam_update(p[u].z, m[u].z, v[u].z, g.z, ad);
+        adam_update(p[u].w, m[u].w, v[u].w, g.w, ad);
+        st4(W + o[u], p[u]);
+        st4(mW + o[u], m[u]);
+        st4(vW + o[u], v[u]);
+        if (Wb) {
+          uint2 sh;
+          sh.x = pack_bf16(p[u].x, p[u].y);
+          sh.y = pack_bf16(p[u].z, p[u].w);
+          *reinterpret_cast<uint2 *>(Wb + o[u]) = sh;
+        }
+      }
+    }
+    __syncthreads();  // the half tile's reads are done before the next one is written
+  }
+
+  if (tn == 0) {  // db = sum of the 64-row column partials, then Adam on b
+    for (int t = tid; t < BM; t += 256) {
+      const int row = m0 + t;
+      if (row >= M) continue;
+      float sum = 0.f;  // in block order, 16 loads in flight
+      int k = 0;
+      for (; k + 16 <= nrb; k += 16) {
+        float q[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) q[j] = dbp[(size_t)(k + j) * M + row];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) sum += q[j];
+      }
+      for (; k < nrb; ++k) sum += dbp[(size_t)k * M + row];
+      float p = bvec[row], m = mbv[row], v = vbv[row];
+      adam_update(p, m, v, sum, ad);
+      bvec[row] = p;
+      mbv[row] = m;
+      vbv[row] = v;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Shared-base layer-0 forward.// ---------------------------------------------------------------------------
 // Shared-base layer-0 forward.  Every label embedding of an input row has the
 // same norm (one label feature is 1), so with x_hat = s * (masked row + e_label)
 // the product splits into P = X_masked_hat W^T, computed once per base row on
@@ -951,10 +1093,12 @@ __global__ __launch_bounds__(WM *WN * 64) void k_fwd_expand(
 }
 
 // ---------------------------------------------------------------------------
-// Loss rows: g_r, c_r = 2 dL/dg_r, and per-workgroup partial sums of the Eq. 1
-// terms (positives and negatives apart); the dW kernel finishes the scalar.
+// Loss rows: g_r, c_r = 2 dL/dg_r, and per-block partial sums of the Eq. 1
+// terms (positives and negatives apart) over 64-row blocks, one wave per block;
+// the weight-gradient kernel finishes the scalar.  Each row's partials are
+// summed in column-tile order, eight loads in flight.
 // ---------------------------------------------------------------------------
-constexpr int kLossRows = 256;
+constexpr int kLossRows = 64;
 
 __global__ __launch_bounds__(kLossRows) void k_loss_rows(const float *__restrict__ gpart, int nt,
                                                           int R, int n_pos, float theta,
@@ -965,12 +1109,19 @@ __global__ __launch_bounds__(kLossRows) void k_loss_rows(const float *__restrict
                                                           float norm_eps,
                                                           const float *__restrict__ s_in,
                                                           float *__restrict__ cs) {
-  __shared__ float sp[kLossRows], sn[kLossRows];
   const int r = blockIdx.x * kLossRows + threadIdx.x;
   float lp = 0.f, ln = 0.f;
   if (r < R) {
     float gv = 0.f;
-    for (int t = 0; t < nt; ++t) gv += gpart[(size_t)t * R + r];
+    int t = 0;
+    for (; t + 8 <= nt; t += 8) {
+      float p[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) p[j] = gpart[(size_t)(t + j) * R + r];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) gv += p[j];
+    }
+    for (; t < nt; ++t) gv += gpart[(size_t)t * R + r];
     if (g) g[r] = gv;
     if (s_out) s_out[r] = 1.f / (sqrtf(gv) + norm_eps);  // g is the row's squared norm
     float cr;
@@ -986,19 +1137,11 @@ __global__ __launch_bounds__(kLossRows) void k_loss_rows(const float *__restrict
     c[r] = cr;
     if (cs) cs[r] = cr * s_in[r];
   }
-  sp[threadIdx.x] = lp;
-  sn[threadIdx.x] = ln;
-  __syncthreads();
-  for (int s = kLossRows / 2; s > 0; s >>= 1) {
-    if ((int)threadIdx.x < s) {
-      sp[threadIdx.x] += sp[threadIdx.x + s];
-      sn[threadIdx.x] += sn[threadIdx.x + s];
-    }
-    __syncthreads();
-  }
+  lp = wave_sum(lp);
+  ln = wave_sum(ln);
   if (threadIdx.x == 0) {
-    lpart[2 * blockIdx.x] = sp[0];
-    lpart[2 * blockIdx.x + 1] = sn[0];
+    lpart[2 * blockIdx.x] = lp;
+    lpart[2 * blockIdx.x + 1] = ln;
   }
 }
 
@@ -1169,6 +1312,163 @@ __global__ __launch_bounds__(WM *WN * 64) void k_dw_adam_f32(
       vbv[row] = v;
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 weight gradient as an NT product.  The contraction runs over the batch
+// rows, so both operands are wanted row-major over the rows: dZ^T [d_out][Rp]
+// and x_hat^T [d_in][Rp], Rp = R rounded up to 64 with zero columns.  Two
+// passes write them; the product then runs on the four-wave main loop.
+// ---------------------------------------------------------------------------
+constexpr int kTRows = 64;  // batch rows per transposed block
+
+// The transposes below stage a 64 x 64 bf16 tile in LDS as words of two
+// consecutive rows of one column, T[col][row pair] with 33 words per column:
+// the writes of a wave (one column word per lane) then fall on 64 distinct
+// banks, and a lane gathers its 16 rows of a column as 8 words.
+constexpr int kTWords = kTRows / 2 + 1;
+
+// Writes rows r0..r0+63 of column `col` of a transposed tile from T (lane
+// segment seg: rows 16 seg .. 16 seg + 15) to out[col][r0 + ...] (row stride Rp).
+__device__ __forceinline__ void store_tcol(const uint32_t (*T)[kTWords], int c, int seg,
+                                           uint16_t *out_col) {
+  uint32_t w[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) w[j] = T[c][seg * 8 + j];
+  uint4 *dst = reinterpret_cast<uint4 *>(out_col + seg * 16);
+  dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
+  dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
+}
+
+// Loss rows (as k_loss_rows, over 64-row blocks) and dZ^T = bf16(c . H)^T
+// (R3) with the per-block column sums of c . H in fp32 for db:
+//   grid (Rp / 64, ceil(D / 256)); each workgroup takes 64 rows and 256
+//   columns in four 64 x 64 sub-tiles, staged through LDS to transpose.
+//   Column block 0 also writes g, c and the loss partials lpart[2 * block].
+// Rows R..Rp-1 give zero columns of dZ^T.
+__global__ __launch_bounds__(kBlock) void k_loss_t(const float *__restrict__ gpart, int nt, int R,
+                                                   int Rp, int n_pos, float theta,
+                                                   const float *__restrict__ H, int D,
+                                                   float *__restrict__ g_out,
+                                                   float *__restrict__ c_out,
+                                                   float *__restrict__ lpart,
+                                                   uint16_t *__restrict__ dzT,
+                                                   float *__restrict__ dbp) {
+  __shared__ float cs[kTRows];
+  __shared__ float red[16][kTRows + 4];
+  __shared__ uint32_t T[kTRows][kTWords];
+  const int tid = threadIdx.x;
+  const int r0 = blockIdx.x * kTRows;
+  if (tid < kTRows) {  // wave 0: the block's rows
+    const int r = r0 + tid;
+    float cr = 0.f, lp = 0.f, ln = 0.f;
+    if (r < R) {
+      float gv = 0.f;
+      int t = 0;
+      for (; t + 8 <= nt; t += 8) {
+        float p[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) p[j] = gpart[(size_t)(t + j) * R + r];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) gv += p[j];
+      }
+      for (; t < nt; ++t) gv += gpart[(size_t)t * R + r];
+      if (r < n_pos) {
+        const float x = theta - gv;
+        lp = softplus_f(x);
+        cr = -2.f * sigmoid_f(x) / (float)n_pos;
+      } else {
+        const float x = gv - theta;
+        ln = softplus_f(x);
+        cr = 2.f * sigmoid_f(x) / (float)(R - n_pos);
+      }
+      if (blockIdx.y == 0) {
+        if (g_out) g_out[r] = gv;
+        if (c_out) c_out[r] = cr;
+      }
+    }
+    cs[tid] = cr;
+    lp = wave_sum(lp);
+    ln = wave_sum(ln);
+    if (blockIdx.y == 0 && tid == 0) {
+      lpart[2 * blockIdx.x] = lp;
+      lpart[2 * blockIdx.x + 1] = ln;
+    }
+  }
+  __syncthreads();
+  const int q = tid & 15, p = tid >> 4;  // column quad; row pairs p and p + 16
+#pragma unroll 1
+  for (int sub = 0; sub < 4; ++sub) {
+    const int cb = blockIdx.y * 256 + sub * 64;
+    if (cb >= D) break;  // uniform
+    const int col = cb + 4 * q;
+    float4 v[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {  // rows 2p, 2p+1, 2p+32, 2p+33
+      const int row = 2 * p + (i & 1) + 32 * (i >> 1), r = r0 + row;
+      v[i] = (r < R && col < D) ? ld4(H + (size_t)r * D + col) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float cc = cs[2 * p + (i & 1) + 32 * (i >> 1)];
+      v[i] = make_float4(v[i].x * cc, v[i].y * cc, v[i].z * cc, v[i].w * cc);
+      acc.x += v[i].x;
+      acc.y += v[i].y;
+      acc.z += v[i].z;
+      acc.w += v[i].w;
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {  // the word of rows (2p, 2p+1) + 32 h of each column
+      const float4 a = v[2 * h], b = v[2 * h + 1];
+      T[4 * q + 0][p + 16 * h] = pack_bf16(a.x, b.x);
+      T[4 * q + 1][p + 16 * h] = pack_bf16(a.y, b.y);
+      T[4 * q + 2][p + 16 * h] = pack_bf16(a.z, b.z);
+      T[4 * q + 3][p + 16 * h] = pack_bf16(a.w, b.w);
+    }
+    red[p][4 * q + 0] = acc.x;
+    red[p][4 * q + 1] = acc.y;
+    red[p][4 * q + 2] = acc.z;
+    red[p][4 * q + 3] = acc.w;
+    __syncthreads();
+    if (tid < kTRows && cb + tid < D) {
+      float sum = 0.f;
+#pragma unroll
+      for (int k = 0; k < 16; ++k) sum += red[k][tid];
+      dbp[(size_t)blockIdx.x * D + cb + tid] = sum;
+    }
+    const int c = tid >> 2, seg = tid & 3;
+    if (cb + c < D) store_tcol(T, c, seg, dzT + (size_t)(cb + c) * Rp + r0);
+    __syncthreads();
+  }
+}
+
+// x^T [d][Rp] from bf16 rows x [R][d] (d a multiple of 8), zero columns R..Rp-1:
+// 64 x 64 tiles through LDS, grid (Rp / 64, ceil(d / 64)).  A lane loads eight
+// columns of two consecutive rows.
+__global__ __launch_bounds__(kBlock) void k_transpose_bf16(const uint16_t *__restrict__ x, int R,
+                                                           int Rp, int d,
+                                                           uint16_t *__restrict__ xT) {
+  __shared__ uint32_t T[kTRows][kTWords];
+  const int tid = threadIdx.x;
+  const int r0 = blockIdx.x * kTRows, c0 = blockIdx.y * 64;
+  {
+    const int pp = tid >> 3, o = tid & 7, col = c0 + 8 * o;
+    uint4 a = make_uint4(0, 0, 0, 0), b = a;
+    if (col < d) {
+      if (r0 + 2 * pp < R) a = ld16(x + (size_t)(r0 + 2 * pp) * d + col);
+      if (r0 + 2 * pp + 1 < R) b = ld16(x + (size_t)(r0 + 2 * pp + 1) * d + col);
+    }
+    const uint32_t av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {  // columns 8o + 2j (low halves) and 8o + 2j + 1 (high)
+      T[8 * o + 2 * j][pp] = (av[j] & 0xFFFFu) | (bv[j] << 16);
+      T[8 * o + 2 * j + 1][pp] = (av[j] >> 16) | (bv[j] & 0xFFFF0000u);
+    }
+  }
+  __syncthreads();
+  const int c = tid >> 2, seg = tid & 3;
+  if (c0 + c < d) store_tcol(T, c, seg, xT + (size_t)(c0 + c) * Rp + r0);
 }
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
@@ -1749,10 +2049,12 @@ inline unsigned cdiv(long a, long b) { return (unsigned)((a + b - 1) / b); }
 // workloads.  A weight-gradient launch takes the large
 // tile when its tiles fill the CUs (fp32: three quarters of them), else the
 // small one.
-template <int BM, int BN, int BK, int WM, int WN, int PF = 1>
+// FOUR: the bf16 forward runs on the four-wave kernel (k_fwd4) with this tile.
+template <int BM, int BN, int BK, int WM, int WN, int PF = 1, bool FOUR = false>
 struct Tile {
   static constexpr int bm = BM, bn = BN, bk = BK, wm = WM, wn = WN, pf = PF,
                        threads = WM * WN * 64;
+  static constexpr bool four = FOUR;
   static long tiles(int m, int n) { return (long)cdiv(m, BM) * cdiv(n, BN); }
 };
 constexpr int kCUs = 256;
@@ -1789,7 +2091,7 @@ struct FwdTiles<false> {
 template <>
 struct FwdTiles<true> {
   using Huge = Tile<256, 256, 64, 4, 2, 2>;
-  using Large = Tile<256, 192, 64, 2, 2, 2>;  // four-wave kernel (k_fwd4)
+  using Large = Tile<256, 192, 64, 2, 2, 2, true>;  // four-wave kernel (k_fwd4)
   using Big = Tile<128, 128, 64, 4, 2, 2>;
   using Full = Tile<128, 128, 64, 4, 2, 3>;
   using Small = Tile<64, 64, 64, 2, 2, 3>;
@@ -1842,6 +2144,8 @@ int fwd_col_tiles_max(int n_cols) {
 }
 
 int loss_blocks(int rows) { return (int)cdiv(rows, kLossRows); }
+static_assert(kLossRows == kTRows, "the two loss kernels share their row blocks");
+int padded_rows(int rows) { return (int)cdiv(rows, kTRows) * kTRows; }
 
 template <int NV>
 void embed_norm_reg(const RowMap &m, int rows, int d, float eps, bool normalise, bool bf16_out,
@@ -1891,7 +2195,7 @@ void fwd_launch(const void *x, const void *w, const float *bias, const float *ro
   const E *xe = static_cast<const E *>(x);
   const E *we = static_cast<const E *>(w);
   static_assert(T::bk == nt_bk<BF16>(), "forward k-tile is 128 bytes");
-  if constexpr (BF16 && T::threads == 256 && T::bm == 256) {
+  if constexpr (BF16 && T::four) {
     static_assert(T::wm == 2 && T::wn == 2 && T::pf == 2, "four-wave tile");
     if (H)
       hipLaunchKernelGGL((k_fwd4<T::bm, T::bn, true>), grid, dim3(256), 0, s, xe, we, bias,
@@ -1963,6 +2267,47 @@ hipError_t launch_loss(const float *gpart, int ntiles, int R, int n_pos, float t
   if (cs && !s_in) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_loss_rows, dim3(loss_blocks(R)), dim3(kLossRows), 0, s, gpart, ntiles, R,
                      n_pos, theta, g, c, lpart, s_out, norm_eps, s_in, cs);
+  return hipGetLastError();
+}
+
+hipError_t launch_loss_t(const float *gpart, int ntiles, int R, int n_pos, float theta,
+                        const float *H, int D, float *g, float *c, float *lpart, uint16_t *dzT,
+                        float *dbp, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  const int Rp = padded_rows(R);
+  hipLaunchKernelGGL(k_loss_t, dim3(Rp / kTRows, cdiv(D, 256)), dim3(kBlock), 0, s, gpart, ntiles,
+                     R, Rp, n_pos, theta, H, D, g, c, lpart, dzT, dbp);
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose_bf16(const uint16_t *x, int R, int d, uint16_t *xT, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  if (d % 8) return hipErrorInvalidValue;
+  const int Rp = padded_rows(R);
+  hipLaunchKernelGGL(k_transpose_bf16, dim3(Rp / kTRows, cdiv(d, 64)), dim3(kBlock), 0, s, x, R,
+                     Rp, d, xT);
+  return hipGetLastError();
+}
+
+// The bf16 weight-gradient product takes 192x192 tiles when they give every CU
+// one (3072-wide layers), else 128x128.
+template <int BM, int BN, int NBUF>
+void dw4_launch(const uint16_t *dzT, const uint16_t *xT, int M, int N, int K, float *W, float *mW,
+                float *vW, uint16_t *Wb, const float *dbp, int nrb, float *b, float *mb, float *vb,
+                const AdamArgs &a, const LossFinish &lf, hipStream_t s) {
+  hipLaunchKernelGGL((k_dw4<BM, BN, NBUF>), dim3(cdiv(M, BM) * cdiv(N, BN)), dim3(256), 0, s, dzT, xT,
+                     M, N, K, W, mW, vW, Wb, dbp, nrb, b, mb, vb, a, lf);
+}
+
+hipError_t launch_dw4(const uint16_t *dzT, const uint16_t *xT, int M, int N, int R, float *W,
+                      float *mW, float *vW, uint16_t *Wb, const float *dbp, float *b, float *mb,
+                      float *vb, const AdamArgs &a, const LossFinish &lf, hipStream_t s) {
+  const int Rp = padded_rows(R), nrb = Rp / kTRows;
+  if (N % 8 || Rp > kMaxWidth) return hipErrorInvalidValue;
+  if ((long)cdiv(M, 192) * cdiv(N, 192) >= kCUs)
+    dw4_launch<192, 192, 3>(dzT, xT, M, N, Rp, W, mW, vW, Wb, dbp, nrb, b, mb, vb, a, lf, s);
+  else
+    dw4_launch<128, 128, 3>(dzT, xT, M, N, Rp, W, mW, vW, Wb, dbp, nrb, b, mb, vb, a, lf, s);
   return hipGetLastError();
 }
 
