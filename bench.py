@@ -8,11 +8,23 @@ activity handoff), followed by goodness label scoring of the 10 000-vector
 MNIST-shaped set under all 10 labels through a 784->2000x4 net.  Inputs are
 seeded synthetic data resident in HBM before the timed region.
 
-Prints one JSON line.  ``value`` is training pos+neg layer-step samples per
-second of whole step (training rows x layers / ms_per_step); the training and
-scoring parts are also reported on their own (HIP-event timed).  ``roofline``
-is the dominant kernel's algorithmic throughput from live per-launch HIP
-events; ``cpu_baseline`` is the CPU oracle timed on a bounded sample.
+Prints one JSON line.  ``value`` is the step's pos+neg layer-step samples
+per second over the whole train+score step (training rows x layers /
+ms_per_step); the training and scoring parts are also reported on their own
+(HIP-event timed: ``train_samples_per_s``, ``images_per_s``).  ``roofline`` is
+the dominant kernel's one-stream figure: the step replayed with every layer on
+one HIP stream, HIP events around each launch, algorithmic flops over the
+summed durations of all its launches in the step (every shape it runs at,
+weighted by its launches); ``roofline_overlapped`` is the same kernel inside
+the timed, stream-overlapped steps.  ``cpu_baseline`` is the CPU oracle timed
+on a bounded sample.
+
+Profiling modes (for rocprofv3 runs): ``--replay K`` (K one-stream steps),
+``--focus`` (layer steps of one shape) and ``--hbm`` (the row kernels at their
+bench shapes) record every launch and write the list to ``--launch-list``;
+``--rocprof-shapes`` matches a rocprofv3 kernel trace of such a run to that
+list, launch by launch, and prints per-kernel, per-shape durations and
+roofline fractions.
 """
 import argparse
 import hashlib
@@ -59,12 +71,161 @@ def load_traffic(kernel, workload):
 KIND_OF = [("k_fwd", "forward"), ("k_dw_adam", "dw_adam"), ("k_dw4", "dw_adam"),
            ("k_embed_norm", "embed_norm"), ("k_loss_rows", "loss"), ("k_loss_t", "loss"),
            ("k_goodness", "goodness"), ("k_argmax", "argmax"), ("k_bf16_shadow", "bf16_shadow"),
-           ("k_transpose_bf16", "transpose")]
+           ("k_transpose_bf16", "transpose"), ("k_head_", "head"), ("k_po_dz", "head")]
+MFMA_KINDS = ("forward", "dw_adam")
+ROW_MODES = ["rows", "pairs", "expand", "masked", "neutral"]
+HEAD_PARTS = ["", "logits", "layer dZ", "grad partials", "Adam"]
 
 
-def focus_steps(rows, d_in, d_out, bf16, steps=3):
-    """A few training steps of one layer shape on one stream, nothing else timed:
-    the workload of the per-kernel counter runs."""
+def kind_of(kernel_name):
+    return next((k for pat, k in KIND_OF if pat in kernel_name), None)
+
+
+def shape_label(r):
+    """Shape of a recorded launch (sizes by kind as ff_launch_record documents)."""
+    kind, m, n, k, aux = r["kind"], r["m"], r["n"], r["k"], r["aux"]
+    if kind == "forward":
+        return f"{m}x{k}->{n}" + (f" (x{aux} labels)" if aux else "")
+    if kind == "dw_adam":
+        return f"{n}->{m} over {k} rows"
+    if kind == "head":
+        return f"{m}x{k}->{n} classes ({HEAD_PARTS[aux]})"
+    if kind == "loss":
+        return f"{m}x{n}" + (" (+bf16 dZ^T)" if aux else "")
+    if kind == "goodness":
+        return f"{m} rows x {n} partials"
+    if kind == "embed_norm":
+        return f"{m}x{n} ({ROW_MODES[aux & 15]}, {'bf16' if aux & 16 else 'fp32'} out)"
+    return f"{m}x{n}"
+
+
+def by_shape(recs, dname, durations=None):
+    """Per (kernel kind, shape) of the launches: count, average duration,
+    algorithmic work per launch and the rate against its roofline (MFMA peak of
+    the dtype for the two products, 8 TB/s HBM for the rest).  durations (us,
+    one per record) replaces the records' event times."""
+    import collections
+    groups = collections.OrderedDict()
+    for i, r in enumerate(recs):
+        us = durations[i] if durations is not None else r["ms"] * 1e3
+        groups.setdefault((r["kind"], shape_label(r)), []).append((r, us))
+    out = []
+    for (kind, lab), rs in groups.items():
+        n = len(rs)
+        tot_s = sum(us for _, us in rs) * 1e-6
+        fl = sum(r["flops"] for r, _ in rs)
+        by = sum(r["bytes"] for r, _ in rs)
+        e = {"kernel": kind, "shape": lab, "launches": n, "avg_us": tot_s * 1e6 / n,
+             "flops_per_launch": fl / n, "bytes_per_launch": by / n}
+        if kind in MFMA_KINDS:
+            e["TFLOP/s"] = fl / tot_s / 1e12
+            e["frac"] = e["TFLOP/s"] / PEAK[dname][1]
+        else:
+            e["GB/s"] = by / tot_s / 1e9
+            e["frac"] = e["GB/s"] / HBM_PEAK_GBS
+        out.append(e)
+    return out
+
+
+def kind_totals(recs, dname, durations=None):
+    """Per kernel kind over all its launches: summed duration and the rate of
+    its summed algorithmic work over it (the shape-weighted fraction)."""
+    import collections
+    acc = collections.OrderedDict()
+    for i, r in enumerate(recs):
+        us = durations[i] if durations is not None else r["ms"] * 1e3
+        a = acc.setdefault(r["kind"], [0, 0.0, 0.0, 0.0])
+        a[0] += 1
+        a[1] += us
+        a[2] += r["flops"]
+        a[3] += r["bytes"]
+    out = {}
+    for kind, (n, us, fl, by) in acc.items():
+        e = {"launches": n, "total_us": us, "avg_us": us / n}
+        if kind in MFMA_KINDS:
+            e["TFLOP/s"] = fl / (us * 1e-6) / 1e12
+            e["frac"] = e["TFLOP/s"] / PEAK[dname][1]
+        else:
+            e["GB/s"] = by / (us * 1e-6) / 1e9
+            e["frac"] = e["GB/s"] / HBM_PEAK_GBS
+        out[kind] = e
+    return out
+
+
+def write_launch_list(path, recs, timed, dname, about, **extra):
+    """The recorded launches, each marked timed (counted in the summaries) or not."""
+    if path:
+        for r, t in zip(recs, timed):
+            r["timed"] = bool(t)
+        with open(path, "w") as f:
+            json.dump(dict({"about": about, "dtype": dname,
+                            "kernel_source_sha256_16": kernel_source_hash(), "launches": recs},
+                           **extra), f)
+
+
+def rocprof_shapes(trace_csv, list_json):
+    """Match the dispatches of this library's kernels in a rocprofv3 kernel
+    trace (Dispatch_Id order) one to one with a recorded launch list (enqueue
+    order, one stream), then print per-kernel, per-shape rocprof durations and
+    fractions over the launches marked timed (markdown)."""
+    import csv
+    L = json.load(open(list_json))
+    recs, dname = L["launches"], L["dtype"]
+    ours = []
+    for r in csv.DictReader(open(trace_csv)):
+        kind = kind_of(r["Kernel_Name"])
+        if kind is None:
+            continue
+        ours.append((int(r["Dispatch_Id"]), kind,
+                     (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3))
+    ours.sort()
+    # the recorded launches are the trace's last ones (the runs launch nothing of
+    # the library's after their profile stops; set-up, such as a bf16 layer's
+    # first weight shadow, may come before it starts)
+    skip = len(ours) - len(recs)
+    if skip < 0:
+        raise SystemExit(f"{len(ours)} dispatches of the library's kernels in the trace, "
+                         f"{len(recs)} recorded launches")
+    ours = ours[skip:]
+    for i, ((_, kind, _), r) in enumerate(zip(ours, recs)):
+        if kind != r["kind"]:
+            raise SystemExit(f"launch {i}: trace has {kind}, list has {r['kind']}")
+    sel = [i for i, r in enumerate(recs) if r["timed"]]
+    n_all = len(recs)
+    recs, us = [recs[i] for i in sel], [ours[i][2] for i in sel]
+    print(f"Launch list: {L['about']} ({len(recs)} timed launches of {n_all}, matched to the "
+          f"trace's last {n_all} dispatches of the library's kernels after {skip} earlier ones; "
+          f"kernel source {L['kernel_source_sha256_16']}).  Durations: rocprofv3 kernel trace "
+          f"(End - Start); `event avg` is the library's HIP-event time of the same launches.\n")
+    print("| kernel | shape | launches | rocprof avg us | event avg us | work per launch "
+          "| rate | fraction of peak |")
+    print("|---|---|---|---|---|---|---|---|")
+    rows_ev = {(e["kernel"], e["shape"]): e for e in by_shape(recs, dname)}
+    for e in by_shape(recs, dname, us):
+        evr = rows_ev[(e["kernel"], e["shape"])]
+        work = (f"{e['flops_per_launch'] / 1e9:.3f} GFLOP" if e["kernel"] in MFMA_KINDS
+                else f"{e['bytes_per_launch'] / 1e6:.2f} MB")
+        rate = (f"{e['TFLOP/s']:.1f} TFLOP/s" if e["kernel"] in MFMA_KINDS
+                else f"{e['GB/s']:.0f} GB/s")
+        print(f"| {e['kernel']} | {e['shape']} | {e['launches']} | {e['avg_us']:.1f} | "
+              f"{evr['avg_us']:.1f} | {work} | {rate} | {e['frac'] * 100:.1f} % |")
+    print("\nShape-weighted per kernel kind (summed work / summed rocprof duration):\n")
+    print("| kernel | launches | total us | rate | fraction of peak |")
+    print("|---|---|---|---|---|")
+    tot = 0.0
+    for kind, e in kind_totals(recs, dname, us).items():
+        tot += e["total_us"]
+        rate = (f"{e['TFLOP/s']:.1f} TFLOP/s" if kind in MFMA_KINDS else f"{e['GB/s']:.0f} GB/s")
+        print(f"| {kind} | {e['launches']} | {e['total_us']:.1f} | {rate} | "
+              f"{e['frac'] * 100:.1f} % |")
+    print(f"\nSum of the listed kernel durations: {tot / 1e3:.3f} ms"
+          + (f" over {L['steps']} step(s), {tot / 1e3 / L['steps']:.3f} ms per step; "
+             f"event-timed wall time of a step: {L['step_ms']:.3f} ms" if "steps" in L else ""))
+
+
+def focus_steps(rows, d_in, d_out, bf16, steps=3, launch_list=None):
+    """One untimed and `steps` recorded training steps of one layer shape on one
+    stream: the workload of the per-shape rocprofv3 runs."""
     import torch
     import paper_2404_08573_amd as P
     from ffinputs import random_matrix, make_weights
@@ -75,10 +236,24 @@ def focus_steps(rows, d_in, d_out, bf16, steps=3):
     L = P.Layer(torch.from_numpy(W).to(dev), torch.from_numpy(b).to(dev), bool(bf16))
     hp = P.HParams(dtype=dt, lr=0.01)
     ws = P.workspace(P.ff_step_workspace_size(rows, d_in, d_out, dt), dev)
-    for _ in range(steps):
-        P.ff_layer_step(L, hp, x, rows // 2, rows - rows // 2, ws=ws)
     torch.cuda.synchronize()
-    print(json.dumps({"focus": [rows, d_in, d_out, bf16], "steps": steps}))
+    P.ff_profile_start(1 << 14)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for i in range(1 + steps):
+        if i == 1:
+            a.record()
+        P.ff_layer_step(L, hp, x, rows // 2, rows - rows // 2, ws=ws)
+    b.record()
+    torch.cuda.synchronize()
+    _, recs = P.ff_profile_stop(launches=True)
+    t0 = len(recs) // (1 + steps)
+    dname = "bf16" if bf16 else "f32"
+    write_launch_list(launch_list, recs, [i >= t0 for i in range(len(recs))], dname,
+                      f"one untimed and {steps} timed layer steps {rows}x{d_in}->{d_out} "
+                      f"{dname}, one stream", steps=steps, step_ms=a.elapsed_time(b) / steps)
+    print(json.dumps({"focus": [rows, d_in, d_out, bf16], "steps": steps,
+                      "step_ms": a.elapsed_time(b) / steps,
+                      "shapes": by_shape(recs[t0:], dname)}))
 
 
 def copy_calibration(nbytes):
@@ -174,35 +349,7 @@ def counter_summary(csv_paths, n_simd=1024, n_xcd=8):
                   f"{c.get('SQ_LDS_BANK_CONFLICT', 0.0) / lds:.3f} |")
 
 
-def isolated_roofline(P, torch, w, dtype, kind, peak, punit, reps=20):
-    """The dominant kernel alone on one stream, at the largest layer shape of
-    the training step (its chunk rows x the widest layer), timed by the same
-    per-launch HIP events: the kernel's own efficiency, without the time it
-    shares with the other layers' streams in the pipelined step."""
-    from ffinputs import random_matrix, make_weights
-    dev = torch.device("cuda:0")
-    di, do = max(zip(w.dims[:-1], w.dims[1:]), key=lambda t: t[0] * t[1])
-    R = 2 * w.chunk_pairs
-    x = torch.from_numpy(random_matrix(7, R, di, 0, 1, 0.5)).to(dev)
-    (Wt, bt), = make_weights(8, (di, do))
-    L = P.Layer(torch.from_numpy(Wt).to(dev), torch.from_numpy(bt).to(dev),
-                dtype == P.FF_BF16)
-    hp = P.HParams(theta=w.theta, lr=w.lr, dtype=dtype)
-    ws = P.workspace(P.ff_step_workspace_size(R, di, do, dtype), dev)
-    for _ in range(3):
-        P.ff_layer_step(L, hp, x, R // 2, R - R // 2, ws=ws)
-    torch.cuda.synchronize()
-    P.ff_profile_start(reps * 8)
-    for _ in range(reps):
-        P.ff_layer_step(L, hp, x, R // 2, R - R // 2, ws=ws)
-    st = P.ff_profile_stop()[kind]
-    ach = st["flops"] / (st["total_ms"] * 1e-3) / 1e12
-    return {"kernel": kind, "shape": f"{R}x{di}->{do}", "achieved": ach, "peak": peak,
-            "unit": punit, "frac": ach / peak, "avg_launch_us": st["total_ms"] * 1e3 / reps,
-            "launches": st["launches"]}
-
-
-def hbm_kernels(P, torch, reps=20):
+def hbm_kernels(P, torch, reps=20, recorded=False):
     """The row / elementwise kernels alone on one stream at bandwidth-sized
     launches, each timed by the per-launch HIP events of the library's kernel
     timing: algorithmic bytes per launch / average launch duration, against
@@ -211,7 +358,9 @@ def hbm_kernels(P, torch, reps=20):
       embed_norm: normalisation of CIFAR-shaped rows (3072 features): one
         training chunk (4096 rows, bf16 out) and the 49 152-row prefix of the
         set (bf16 and fp32 out);
-      bf16_shadow: the bf16 weight copy of a 3072 x 3072 layer."""
+      bf16_shadow: the bf16 weight copy of a 3072 x 3072 layer.
+    recorded: a profile that records every launch is already active (--hbm):
+    the launches run without a profile of their own and nothing is returned."""
     from ffinputs import make_weights
     dev = torch.device("cuda:0")
     gen = torch.Generator(device=dev)
@@ -221,6 +370,10 @@ def hbm_kernels(P, torch, reps=20):
     def timed(kind, fn):
         fn()
         torch.cuda.synchronize()
+        if recorded:
+            for _ in range(reps):
+                fn()
+            return None
         P.ff_profile_start(reps * 4, kinds=[kind])
         for _ in range(reps):
             fn()
@@ -312,7 +465,7 @@ def other_workloads(P, torch, names, reps=2, trials=3):
     return out
 
 
-def softmax_head(P, torch, sw, sxd, slayers, reps=5):
+def softmax_head(P, torch, sw, sxd, slayers, reps=5, recorded=False):
     """Softmax prediction (one neutral-label pass + the softmax layer over the
     normalised activities of layers 1..) of the scoring set, and one training
     step of the softmax layer on it, each HIP-event timed on its own."""
@@ -328,6 +481,10 @@ def softmax_head(P, torch, sw, sxd, slayers, reps=5):
     ws = P.workspace(P.ff_head_workspace_size(slayers, 1, sw.n, sw.n_classes), dev)
     pred = torch.empty(sw.n, dtype=torch.int32, device=dev)
     loss = torch.empty(1, device=dev)
+    if recorded:  # an outer profile records every launch (--hbm): the predictions only
+        for _ in range(1 + reps):
+            P.ff_head_predict(slayers, hp, head, sxd, 1, pred=pred, ws=ws)
+        return None
     out = {}
     for name, fn in (("predict", lambda: P.ff_head_predict(slayers, hp, head, sxd, 1, pred=pred,
                                                            ws=ws)),
@@ -442,6 +599,36 @@ def chapters(P, torch, w, xd, yd, ynd, params, epochs=2, splits=2):
         ms = a.elapsed_time(b)
         out[name] = {"ms": ms, "streams": ns,
                      "samples_per_s": 2 * w.n * w.n_layers * epochs / (ms * 1e-3)}
+        del layers, ws
+    # AdaptiveNEG: chapter c's wrong labels are the hardest ones under the network
+    # as chapter c starts, scored on the device (chapter 0 takes the scoring of the
+    # fresh weights too)
+    for name, assignment, ns in (("single_layer_adaptive", P.FF_SINGLE_LAYER, w.n_layers),
+                                 ("all_layers_adaptive", P.FF_ALL_LAYERS, 2)):
+        layers = [P.Layer(torch.from_numpy(W).to(dev), torch.from_numpy(b).to(dev), bf16)
+                  for W, b in params]
+        ws = P.workspace(P.LIB.ff_chapter_adaptive_workspace_size(
+            P._lib._layers_c(layers), len(layers), w.n, w.n_classes, w.chunk_pairs, ns, dtype), dev)
+        yneg = torch.empty(splits, w.n, dtype=torch.int32, device=dev)
+        cur = torch.cuda.current_stream(dev)
+        streams = [torch.cuda.Stream(dev) for _ in range(ns)]
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(cur)
+        for s in streams:
+            s.wait_stream(cur)
+        P.ff_chapter_train_adaptive(layers, hp, xd, yd, w.n_classes, w.chunk_pairs, epochs,
+                                    splits, epochs // splits, assignment, 0,
+                                    y_neg_chapters=yneg, streams=streams, ws=ws)
+        for s in streams:
+            cur.wait_stream(s)
+        b.record(cur)
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b)
+        out[name] = {"ms": ms, "streams": ns,
+                     "samples_per_s": 2 * w.n * w.n_layers * epochs / (ms * 1e-3),
+                     "note": "includes scoring the 60 000 inputs under every label at each "
+                             "chapter start"}
         del layers, ws
     out["epochs"], out["splits"] = epochs, splits
     return out
@@ -561,9 +748,24 @@ def main():
                          "steps: print MFMA-busy and wait fractions per kernel kind and exit")
     ap.add_argument("--focus", nargs=4, type=int, metavar=("ROWS", "D_IN", "D_OUT", "BF16"),
                     help="run a few layer steps of one shape on one stream (for counter runs)")
+    ap.add_argument("--replay", type=int, metavar="K", default=0,
+                    help="run one untimed and K recorded one-stream replays of the step "
+                         "(every layer on one HIP stream, then the scoring) and exit")
+    ap.add_argument("--hbm", action="store_true",
+                    help="run the row kernels at their bench shapes (embedding + "
+                         "normalisation, bf16 weight shadow, softmax-layer logits) with every "
+                         "launch recorded and exit")
+    ap.add_argument("--launch-list", metavar="JSON",
+                    help="with --replay, --focus or --hbm: write the recorded launches here")
+    ap.add_argument("--rocprof-shapes", nargs=2, metavar=("KERNEL_TRACE_CSV", "LAUNCH_LIST"),
+                    help="match a rocprofv3 kernel trace of a --replay/--focus/--hbm run to its "
+                         "launch list and print per-kernel, per-shape durations; exit")
     args = ap.parse_args()
+    if args.rocprof_shapes:
+        rocprof_shapes(*args.rocprof_shapes)
+        return
     if args.focus:
-        focus_steps(*args.focus)
+        focus_steps(*args.focus, launch_list=args.launch_list)
         return
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
@@ -616,13 +818,14 @@ def main():
     side = [torch.cuda.Stream(dev) for _ in range(w.n_layers - 1)]
     streams = [cur] + side
 
-    def step(ev=None):
+    def step(ev=None, one_stream=False):
         for s in side:
             s.wait_stream(cur)
         if ev:
             ev[0].record(cur)
         P.ff_pipeline_epoch(layers, hp, xd, yd, ynd, w.n_classes, w.chunk_pairs, 1, sched,
-                            streams=streams, loss_trace=trace, ws=ws)
+                            streams=[cur] * w.n_layers if one_stream else streams,
+                            loss_trace=trace, ws=ws)
         for s in side:
             cur.wait_stream(s)
         if ev:
@@ -631,22 +834,79 @@ def main():
         if ev:
             ev[2].record(cur)
 
+    launches_per_step = 4 * (w.n_layers * nc * 5 + 4 * (sw.n // 1024 + 1) * 4 + 64)
+    dname = "bf16" if bf16 else "f32"
+
+    def replay(k):
+        """k one-stream replays of the step, every launch recorded: (launches, ms per step)."""
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        P.ff_profile_start(launches_per_step * k)
+        ev[0].record(cur)
+        for _ in range(k):
+            step(one_stream=True)
+        ev[1].record(cur)
+        torch.cuda.synchronize()
+        _, recs = P.ff_profile_stop(launches=True)
+        return recs, ev[0].elapsed_time(ev[1]) / k
+
+    if args.replay:
+        if args.hbm:
+            raise SystemExit("--replay and --hbm are separate runs")
+        log(f"bench: one untimed and {args.replay} recorded one-stream replay(s)")
+        P.ff_profile_start(launches_per_step)
+        step(one_stream=True)
+        torch.cuda.synchronize()
+        _, warm = P.ff_profile_stop(launches=True)
+        recs, rms = replay(args.replay)
+        about = (f"one untimed and {args.replay} recorded one-stream replays of the step: the "
+                 f"{w.name} epoch with every layer on one HIP stream, then scoring {sw.name}")
+        write_launch_list(args.launch_list, warm + recs,
+                          [False] * len(warm) + [True] * len(recs), dname, about,
+                          steps=args.replay, step_ms=rms)
+        print(json.dumps({"replay_steps": args.replay, "step_ms": rms,
+                          "kernels": kind_totals(recs, dname)}))
+        return
+    if args.hbm:
+        P.ff_profile_start(1 << 14)
+        hbm_kernels(P, torch, recorded=True)
+        softmax_head(P, torch, sw, sxd, slayers, recorded=True)
+        torch.cuda.synchronize()
+        _, recs = P.ff_profile_stop(launches=True)
+        # each kernel's first launch at a shape is untimed, its repeats are timed
+        seen, timed = set(), []
+        for r in recs:
+            key = (r["kind"], shape_label(r))
+            timed.append(key in seen)
+            seen.add(key)
+        write_launch_list(args.launch_list, recs, timed, dname,
+                          "the row kernels at their bench shapes on one stream (with the "
+                          "products that feed them): each kernel's first launch at a shape "
+                          "untimed, its repeats timed")
+        print(json.dumps({"shapes": by_shape([r for r, t in zip(recs, timed) if t], dname)}))
+        return
+
     log(f"bench: warmup {args.warmup} step(s)")
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    launches_per_step = w.n_layers * nc * 4 + 4 * (sw.n // 2048 + 1) * 4 + 8
 
-    # One untimed step with every launch bracketed by events: the per-kernel
-    # table, and which product dominates.
+    # One-stream replay: each launch runs alone, so its event time is the
+    # kernel's own; the dominant product and its roofline come from here.
+    log("bench: one-stream replay")
+    step(one_stream=True)
+    torch.cuda.synchronize()
+    orecs, replay_ms = replay(1)
+    otot = kind_totals(orecs, dname)
+    dom = max((k for k in MFMA_KINDS if k in otot), key=lambda k: otot[k]["total_us"])
+
+    # One untimed overlapped step with every launch bracketed by events: the
+    # per-kernel table of the pipelined step.
     pev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-    P.ff_profile_start(launches_per_step + 64)
+    P.ff_profile_start(launches_per_step)
     step(pev)
     torch.cuda.synchronize()
     kstats = P.ff_profile_stop()
     profiled_ms = pev[0].elapsed_time(pev[2])
-    gemms = {k: v for k, v in kstats.items() if k in ("forward", "dw_adam") and v["launches"]}
-    dom = max(gemms, key=lambda k: gemms[k]["total_ms"])
 
     # Timed region: events around the dominant kernel's launches only (events
     # at every launch boundary cost the pipelined step about 1 %).
@@ -674,12 +934,11 @@ def main():
     # already runs that rewrite; training launches the full products)
     train_min_flops = train_flops - sum(4.0 * b * w.dims[0] * w.dims[1] for (_, b) in w.chunks())
     kernel_ms = sum(v["total_ms"] for v in kstats.values())
-    dname = "bf16" if bf16 else "f32"
     bound, peak, punit = PEAK[dname]
-    achieved = ds["flops"] / (ds["total_ms"] * 1e-3) / 1e12
-    traffic = load_traffic(dom, w.name)
-    if traffic is not None:
-        traffic *= 1.0  # HBM bytes per launch of the dominant kernel (counter runs)
+    dom_recs = [r for r in orecs if r["kind"] == dom]
+    one = otot[dom]
+    achieved_ov = ds["flops"] / (ds["total_ms"] * 1e-3) / 1e12
+    traffic = load_traffic(dom, w.name)  # HBM bytes per launch (counter runs)
     kernels = {}
     for k, v in kstats.items():
         if not v["launches"]:
@@ -692,7 +951,11 @@ def main():
     out = {
         "metric": METRIC,
         "value": step_rows / (ms_per_step * 1e-3),
-        "unit": "pos+neg samples/s per layer-step",
+        "unit": "pos+neg samples/s per layer-step over the train+score step",
+        "value_definition": "training rows x layers per step / ms_per_step, where the timed "
+                            "step is one training epoch plus scoring the score set; the "
+                            "training part alone is train_samples_per_s, the scoring part "
+                            "images_per_s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": dname, "data": "synthetic",
@@ -704,22 +967,30 @@ def main():
         "train_samples_per_s": step_rows / (train_ms * 1e-3),
         "score_ms_per_step": score_ms,
         "images_per_s": sw.n / (score_ms * 1e-3),
-        "roofline": {"bound": bound, "kernel": dom, "achieved": achieved, "peak": peak,
-                     "unit": punit, "frac": achieved / peak,
-                     "traffic": traffic,
-                     "avg_launch_us": ds["total_ms"] * 1e3 / ds["launches"],
-                     "launches": ds["launches"],
-                     "note": "events around this kernel's launches in the timed steps; "
-                             "per-launch durations include time shared with the other layers' "
-                             "streams: kernel time summed over launches is `concurrency` times "
-                             "the step's wall time (`kernels`: one profiled step before the "
-                             "timed ones)"},
+        "roofline": {"bound": bound, "kernel": dom, "achieved": one["TFLOP/s"], "peak": peak,
+                     "unit": punit, "frac": one["frac"], "traffic": traffic,
+                     "avg_launch_us": one["avg_us"], "launches": one["launches"],
+                     "algorithmic_flops_per_launch": sum(r["flops"] for r in dom_recs)
+                     / len(dom_recs),
+                     "shapes": by_shape(dom_recs, dname),
+                     "replay_ms_per_step": replay_ms,
+                     "method": "one-stream replay of the step (every layer on one HIP stream, "
+                               "then the scoring): HIP events around each launch; achieved = "
+                               "the kernel's algorithmic flops summed over all its launches in "
+                               "the step / their summed durations (`shapes`: per shape)"},
+        "roofline_overlapped": {
+            "kernel": dom, "achieved": achieved_ov, "peak": peak, "unit": punit,
+            "frac": achieved_ov / peak, "avg_launch_us": ds["total_ms"] * 1e3 / ds["launches"],
+            "launches": ds["launches"],
+            "note": "events around this kernel's launches in the timed steps; per-launch "
+                    "durations include time shared with the other layers' streams: kernel time "
+                    "summed over launches is `concurrency` times the step's wall time"},
+        "replay_kernels": otot,
         "concurrency": kernel_ms / profiled_ms,
         "train_mfma_frac": train_flops / (train_ms * 1e-3) / 1e12 / peak,
         "train_effective_frac": train_min_flops / (train_ms * 1e-3) / 1e12 / peak,
         "kernels": kernels,
     }
-    out["roofline_isolated"] = isolated_roofline(P, torch, w, dtype, dom, peak, punit)
     if not args.no_other_workloads:
         out["hbm_kernels_isolated"] = hbm_kernels(P, torch)
         out["softmax_head"] = softmax_head(P, torch, sw, sxd, slayers)

@@ -405,10 +405,39 @@ typedef struct {
   double bytes;       /* algorithmic HBM bytes of those launches             */
 } ff_kernel_stats;
 
+/* One timed launch.  Sizes by kind:
+ *   FORWARD      m rows, n output features, k input features; aux = label
+ *                count of the label-expanding scoring product (m base rows),
+ *                else 0;
+ *   DW_ADAM      m = d_out, n = d_in, k = rows contracted;
+ *   EMBED_NORM   m rows, n features; aux = the row source mode, plus 16
+ *                for bf16 output rows;
+ *   LOSS         m rows, n = d_out, k = goodness partials per row; aux = 1
+ *                when the pass also writes the bf16 weight-gradient operand;
+ *   TRANSPOSE    m rows, n features;
+ *   GOODNESS     m rows, n = partials per row;
+ *   ARGMAX       m rows, n labels;
+ *   SHADOW       m x n weights;
+ *   HEAD         m rows, n classes, k features; aux = 1 logits, 2 layer dZ,
+ *                3 weight-gradient partials, 4 Adam. */
+typedef struct {
+  int32_t kind;       /* ff_kernel_kind                                      */
+  int32_t m, n, k, aux;
+  float ms;           /* event-measured duration                             */
+  double flops;       /* algorithmic flops                                   */
+  double bytes;       /* algorithmic HBM bytes                               */
+} ff_launch_record;
+
 /* kind_mask: bit k selects kernel kind k (0 selects every kind); launches of
  * other kinds run without events. */
 ff_status ff_profile_start(int32_t max_launches, uint32_t kind_mask);
 ff_status ff_profile_stop(ff_kernel_stats *stats /* (host) [FF_KERNEL_KINDS] */);
+/* As ff_profile_stop, and also the timed launches one by one in the order the
+ * host enqueued them: the first min(max_launches, timed) into launches
+ * (host, may be NULL), their number into *n_launches (host, may be NULL). */
+ff_status ff_profile_stop_launches(ff_kernel_stats *stats /* (host) [FF_KERNEL_KINDS] or NULL */,
+                                   ff_launch_record *launches, int32_t max_launches,
+                                   int32_t *n_launches);
 
 /* ---- Failure injection (testing aid) ---------------------------------------
  * The next launch of kernel kind `kind` (an ff_kernel_kind) that any entry

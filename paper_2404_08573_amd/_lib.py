@@ -32,7 +32,8 @@ EXPORTS = ["ff_status_string", "ff_last_error", "ff_embed_labels", "ff_step_work
            "ff_po_step_workspace_size", "ff_po_layer_step", "ff_po_epoch_workspace_size",
            "ff_po_epoch", "ff_po_predict_workspace_size", "ff_po_predict",
            "ff_pipeline_workspace_size",
-           "ff_pipeline_epoch", "ff_profile_start", "ff_profile_stop", "ff_fail_next_launch",
+           "ff_pipeline_epoch", "ff_profile_start", "ff_profile_stop", "ff_profile_stop_launches",
+           "ff_fail_next_launch",
            "ff_layer_step_noalloc"]
 
 KERNEL_KINDS = ["embed_norm", "forward", "loss", "dw_adam", "goodness", "argmax", "bf16_shadow",
@@ -59,6 +60,12 @@ class ff_head(ctypes.Structure):
 
 class ff_kernel_stats(ctypes.Structure):
     _fields_ = [("launches", c_int64), ("total_ms", ctypes.c_double), ("flops", ctypes.c_double),
+                ("bytes", ctypes.c_double)]
+
+
+class ff_launch_record(ctypes.Structure):
+    _fields_ = [("kind", c_int32), ("m", c_int32), ("n", c_int32), ("k", c_int32),
+                ("aux", c_int32), ("ms", c_float), ("flops", ctypes.c_double),
                 ("bytes", ctypes.c_double)]
 
 
@@ -130,6 +137,8 @@ def _load() -> ctypes.CDLL:
                                         POINTER(c_void_p), P, P, c_size_t]),
         "ff_profile_start": (c_int32, [c_int32, ctypes.c_uint32]),
         "ff_profile_stop": (c_int32, [POINTER(ff_kernel_stats)]),
+        "ff_profile_stop_launches": (c_int32, [POINTER(ff_kernel_stats), POINTER(ff_launch_record),
+                                               c_int32, POINTER(c_int32)]),
         "ff_fail_next_launch": (c_int32, [c_int32]),
         "ff_layer_step_noalloc": (c_int32, [POINTER(ff_layer), POINTER(ff_hparams), P, c_int32,
                                             c_int32, c_int32, P, P, P, P]),
@@ -663,9 +672,22 @@ def ff_profile_start(max_launches: int = 65536, kinds=None):
     _check(LIB.ff_profile_start(max_launches, mask))
 
 
-def ff_profile_stop() -> dict:
-    """Per kernel kind: launches, total_ms, flops, bytes (event-timed on each launch's stream)."""
+def ff_profile_stop(launches: bool = False):
+    """Per kernel kind: launches, total_ms, flops, bytes (event-timed on each launch's stream).
+    With launches=True also the list of timed launches in enqueue order, each a dict of
+    kind (name), m, n, k, aux, ms, flops, bytes: returns (stats, launches)."""
     arr = (ff_kernel_stats * len(KERNEL_KINDS))()
-    _check(LIB.ff_profile_stop(arr))
-    return {k: dict(launches=a.launches, total_ms=a.total_ms, flops=a.flops, bytes=a.bytes)
-            for k, a in zip(KERNEL_KINDS, arr)}
+    if not launches:
+        _check(LIB.ff_profile_stop(arr))
+    else:
+        cap = 1 << 20
+        recs = (ff_launch_record * cap)()
+        n = c_int32(0)
+        _check(LIB.ff_profile_stop_launches(arr, recs, cap, ctypes.byref(n)))
+    stats = {k: dict(launches=a.launches, total_ms=a.total_ms, flops=a.flops, bytes=a.bytes)
+             for k, a in zip(KERNEL_KINDS, arr)}
+    if not launches:
+        return stats
+    out = [dict(kind=KERNEL_KINDS[r.kind], m=r.m, n=r.n, k=r.k, aux=r.aux, ms=r.ms,
+                flops=r.flops, bytes=r.bytes) for r in recs[:n.value]]
+    return stats, out

@@ -64,8 +64,13 @@ inline size_t elem_bytes(int dtype) { return dtype == FF_BF16 ? 2 : 4; }
 // ---------------------------------------------------------------------------
 // Kernel timing: event pairs around launches while a profile is active.
 // ---------------------------------------------------------------------------
+// Sizes of a launch, recorded with its timing (ff_launch_record).
+struct Sizes {
+  int32_t m = 0, n = 0, k = 0, aux = 0;
+};
 struct ProfRec {
   int kind;
+  Sizes sz;
   double flops, bytes;
   hipEvent_t a, b;
 };
@@ -85,7 +90,7 @@ std::atomic<int> g_fail_kind{-1};
 // Launches `fn` (returning hipError_t), bracketed by timing events when a
 // profile is active and events remain.
 template <class F>
-hipError_t launch(int kind, double flops, double bytes, hipStream_t st, F fn) {
+hipError_t launch(int kind, Sizes sz, double flops, double bytes, hipStream_t st, F fn) {
   int armed = kind;
   if (g_fail_kind.load(std::memory_order_relaxed) == kind &&
       g_fail_kind.compare_exchange_strong(armed, -1))
@@ -101,7 +106,7 @@ hipError_t launch(int kind, double flops, double bytes, hipStream_t st, F fn) {
   e = fn();
   if (e != hipSuccess) return e;
   e = hipEventRecord(b, st);
-  if (e == hipSuccess) g_prof.recs.push_back(ProfRec{kind, flops, bytes, a, b});
+  if (e == hipSuccess) g_prof.recs.push_back(ProfRec{kind, sz, flops, bytes, a, b});
   return e;
 }
 
@@ -226,7 +231,8 @@ hipError_t embed_norm(const ffk::RowMap &src, int rows, int d, float eps, bool n
                                                     : (double)rows;
   const double bytes = src_rows * d * 4.0 + (double)rows * d * (bf16 ? 2 : 4) +
                        (scale_out ? rows * 4.0 : 0.0);
-  return launch(FF_KERNEL_EMBED_NORM, 0.0, bytes, st, [&] {
+  return launch(FF_KERNEL_EMBED_NORM, Sizes{rows, d, 0, src.mode | (bf16 ? 16 : 0)}, 0.0,
+                bytes, st, [&] {
     return ffk::launch_embed_norm(src, rows, d, eps, normalise, bf16, out, scale_out, st);
   });
 }
@@ -238,7 +244,7 @@ hipError_t fwd(int dtype, const void *X, const void *W, const float *bias, const
   const double bytes = (double)M * K * eb + (double)N * K * eb + N * 4.0 +
                        (rowscale ? M * 4.0 : 0.0) + (H ? (double)M * N * 4.0 : 0.0) +
                        nt * M * 4.0;
-  return launch(FF_KERNEL_FORWARD, gemm_flops(M, N, K), bytes, st, [&] {
+  return launch(FF_KERNEL_FORWARD, Sizes{M, N, K, 0}, gemm_flops(M, N, K), bytes, st, [&] {
     return ffk::launch_fwd(dtype, X, W, bias, rowscale, M, N, K, H, gpart, st);
   });
 }
@@ -253,7 +259,8 @@ hipError_t fwd_expand(int dtype, const void *X, const void *W, const float *bias
   const double nt = ffk::fwd_expand_col_tiles(M, N, dtype);
   const double bytes = (double)M * K * eb + (double)N * K * eb + N * 4.0 + M * 4.0 +
                        (H ? rows_out * N * 4.0 : 0.0) + nt * rows_out * 4.0;
-  return launch(FF_KERNEL_FORWARD, gemm_flops(M, N, K), bytes, st, [&] {
+  return launch(FF_KERNEL_FORWARD, Sizes{M, N, K, ex.n_classes}, gemm_flops(M, N, K), bytes, st,
+                [&] {
     return ffk::launch_fwd_expand(dtype, X, W, bias, ex, M, N, K, H, gpart, st);
   });
 }
@@ -262,7 +269,7 @@ hipError_t goodness_sum(const float *gpart, int nt, int R, float *g, float *out,
                         float *s_out, float norm_eps, hipStream_t st) {
   const double bytes = (double)nt * R * 4.0 + (g ? R * 4.0 : 0.0) +
                        (out ? R * 4.0 * (accumulate ? 2 : 1) : 0.0) + (s_out ? R * 4.0 : 0.0);
-  return launch(FF_KERNEL_GOODNESS, 0.0, bytes, st, [&] {
+  return launch(FF_KERNEL_GOODNESS, Sizes{R, nt, 0, 0}, 0.0, bytes, st, [&] {
     return ffk::launch_goodness(gpart, nt, R, g, out, accumulate, s_out, norm_eps, st);
   });
 }
@@ -352,14 +359,14 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int
     // the normalised bf16 rows.
     const int Rp = ffk::padded_rows(R), nrb = ffk::loss_blocks(R);
     const uint16_t *xh = static_cast<const uint16_t *>(xop);
-    FF_HIP(launch(FF_KERNEL_LOSS, 0.0,
+    FF_HIP(launch(FF_KERNEL_LOSS, Sizes{R, L->d_out, nt, 1}, 0.0,
                   (double)nt * R * 4.0 + (double)R * L->d_out * 4.0 + (g ? R * 4.0 : 0.0) +
                       (double)Rp * L->d_out * 2.0 + (double)nrb * L->d_out * 4.0,
                   st, [&] {
                     return ffk::launch_loss_t(s.gpart, nt, R, n_pos, hp->theta, H, L->d_out, g,
                                               nullptr, s.lpart, s.dzt, s.dbp, st);
                   }));
-    FF_HIP(launch(FF_KERNEL_TRANSPOSE, 0.0, (double)R * L->d_in * 2.0 + (double)Rp * L->d_in * 2.0,
+    FF_HIP(launch(FF_KERNEL_TRANSPOSE, Sizes{R, L->d_in, 0, 0}, 0.0, (double)R * L->d_in * 2.0 + (double)Rp * L->d_in * 2.0,
                   st, [&] { return ffk::launch_transpose_bf16(xh, R, L->d_in, s.xt, st); }));
     ffk::LossFinish lf;
     lf.lpart = s.lpart;
@@ -372,7 +379,8 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int
     const double params = (double)L->d_out * L->d_in;
     const double bytes = (double)Rp * (L->d_out + L->d_in) * 2.0 + params * 26.0 +
                          (double)nrb * L->d_out * 4.0 + L->d_out * 24.0;
-    FF_HIP(launch(FF_KERNEL_DW_ADAM, gemm_flops(L->d_out, L->d_in, R), bytes, st, [&] {
+    FF_HIP(launch(FF_KERNEL_DW_ADAM, Sizes{L->d_out, L->d_in, R, 0},
+                  gemm_flops(L->d_out, L->d_in, R), bytes, st, [&] {
       return ffk::launch_dw4(s.dzt, s.xt, L->d_out, L->d_in, R, L->W, L->mW, L->vW, L->W_bf16,
                              s.dbp, L->b, L->mb, L->vb, a, lf, st);
     }));
@@ -380,7 +388,7 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int
     return FF_OK;
   }
   float *cs = in.rowscale ? s.cs : nullptr;
-  FF_HIP(launch(FF_KERNEL_LOSS, 0.0,
+  FF_HIP(launch(FF_KERNEL_LOSS, Sizes{R, L->d_out, nt, 0}, 0.0,
                 (double)nt * R * 4.0 + R * (g ? 8.0 : 4.0) + (s_next ? R * 4.0 : 0.0) +
                     (cs ? R * 8.0 : 0.0),
                 st, [&] {
@@ -402,7 +410,8 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int
     const double bytes = (double)R * L->d_out * 4.0 + (double)R * L->d_in * eb +
                          R * (in.rowscale ? 8.0 : 4.0) +
                          params * (24.0 + (hp->dtype == FF_BF16 ? 2.0 : 0.0)) + L->d_out * 24.0;
-    FF_HIP(launch(FF_KERNEL_DW_ADAM, gemm_flops(L->d_out, L->d_in, R), bytes, st, [&] {
+    FF_HIP(launch(FF_KERNEL_DW_ADAM, Sizes{L->d_out, L->d_in, R, 0},
+                  gemm_flops(L->d_out, L->d_in, R), bytes, st, [&] {
       return ffk::launch_dw_adam(hp->dtype, H, s.c, xop, cs, L->d_out, L->d_in, R, L->W,
                                  L->mW, L->vW, hp->dtype == FF_BF16 ? L->W_bf16 : nullptr, L->b,
                                  L->mb, L->vb, a, lf, st);
@@ -438,20 +447,23 @@ ff_status po_step_core(ff_layer *L, ff_head *head, const ff_hparams *hp, const f
   f.bias[0] = head->b;
   const int splits = ffk::head_grad_splits(R);
   const double hbytes = (double)R * D * 4.0;
-  FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * R * C * D, hbytes + (double)C * D * 4.0 + R * C * 8.0, st,
+  FF_HIP(launch(FF_KERNEL_HEAD, Sizes{R, C, D, 1}, 2.0 * R * C * D,
+                hbytes + (double)C * D * 4.0 + R * C * 8.0, st,
                 [&] {
                   return ffk::launch_head_logits(f, R, C, labels, nullptr, nullptr, s.G, s.lrow,
                                                  st);
                 }));
-  FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * R * C * D, 2.0 * hbytes + (double)C * D * 4.0, st, [&] {
+  FF_HIP(launch(FF_KERNEL_HEAD, Sizes{R, C, D, 2}, 2.0 * R * C * D,
+                2.0 * hbytes + (double)C * D * 4.0, st, [&] {
     return ffk::launch_po_dz(H, s.G, head->W, R, D, C, s.dz, s.c, st);
   }));
-  FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * R * C * D, hbytes + (double)splits * C * D * 4.0, st, [&] {
+  FF_HIP(launch(FF_KERNEL_HEAD, Sizes{R, C, D, 3}, 2.0 * R * C * D,
+                hbytes + (double)splits * C * D * 4.0, st, [&] {
     return ffk::launch_head_grad(f, s.G, R, C, D, splits, s.part, st);
   }));
   const ffk::AdamArgs ah = adam_args(head_hp, head->step + 1);
-  FF_HIP(launch(FF_KERNEL_HEAD, 0.0, (double)splits * C * D * 4.0 + (double)C * D * 24.0, st,
-                [&] {
+  FF_HIP(launch(FF_KERNEL_HEAD, Sizes{R, C, D, 4}, 0.0,
+                (double)splits * C * D * 4.0 + (double)C * D * 24.0, st, [&] {
                   return ffk::launch_head_adam(s.part, splits, s.G, s.lrow, R, C, D, head->W,
                                                head->mW, head->vW, head->b, head->mb, head->vb,
                                                ah, loss ? loss : s.loss, st);
@@ -466,7 +478,8 @@ ff_status po_step_core(ff_layer *L, ff_head *head, const ff_hparams *hp, const f
   const double params = (double)D * L->d_in;
   const double bytes = hbytes + (double)R * L->d_in * eb + R * (in.rowscale ? 8.0 : 4.0) +
                        params * (24.0 + (hp->dtype == FF_BF16 ? 2.0 : 0.0)) + D * 24.0;
-  FF_HIP(launch(FF_KERNEL_DW_ADAM, gemm_flops(D, L->d_in, R), bytes, st, [&] {
+  FF_HIP(launch(FF_KERNEL_DW_ADAM, Sizes{D, L->d_in, R, 0}, gemm_flops(D, L->d_in, R), bytes,
+                st, [&] {
     return ffk::launch_dw_adam(hp->dtype, s.dz, s.c, xop, in.rowscale, D, L->d_in, R, L->W,
                                L->mW, L->vW, hp->dtype == FF_BF16 ? L->W_bf16 : nullptr, L->b,
                                L->mb, L->vb, a, lf, st);
@@ -648,7 +661,7 @@ ff_status ff_refresh_bf16_shadow(const ff_layer *L, void *stream) {
   if (!L->W_bf16) return fail(FF_ERR_INVALID_ARG, "W_bf16 is NULL");
   const size_t count = (size_t)L->d_out * L->d_in;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  FF_HIP(launch(FF_KERNEL_SHADOW, 0.0, count * 6.0, st,
+  FF_HIP(launch(FF_KERNEL_SHADOW, Sizes{L->d_out, L->d_in, 0, 0}, 0.0, count * 6.0, st,
                 [&] { return ffk::launch_bf16_shadow(L->W, L->W_bf16, count, st); }));
   return FF_OK;
 }
@@ -765,7 +778,8 @@ ff_status score_run(const ff_layer *layers, int32_t n_layers, int32_t first_scor
         FF_HIP(embed_norm(rows_of(H), rows, L->d_out, hp->norm_eps, true, true, s.x, st));
     }
   }
-  FF_HIP(launch(FF_KERNEL_ARGMAX, 0.0, (double)n * n_classes * 4.0 + n * 4.0, st,
+  FF_HIP(launch(FF_KERNEL_ARGMAX, Sizes{n, n_classes, 0, 0}, 0.0,
+                (double)n * n_classes * 4.0 + n * 4.0, st,
                 [&] { return ffk::launch_argmax(S, n, n_classes, exclude, pred, st); }));
   return FF_OK;
 }
@@ -968,17 +982,17 @@ ff_status ff_head_step(const ff_layer *layers, int32_t n_layers, int32_t first_l
   const int splits = ffk::head_grad_splits(n);
   const ffk::AdamArgs a = adam_args(head_hp, head->step + 1);
   const double feat_bytes = (double)n * D * 4.0 + (double)n * f.n_blocks * 4.0;
-  FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * n * C * D, feat_bytes + (double)C * D * 4.0 + n * C * 4.0,
-                st, [&] {
+  FF_HIP(launch(FF_KERNEL_HEAD, Sizes{n, C, D, 1}, 2.0 * n * C * D,
+                feat_bytes + (double)C * D * 4.0 + n * C * 4.0, st, [&] {
                   return ffk::launch_head_logits(f, n, C, labels, nullptr, nullptr, hs.G,
                                                  hs.lrow, st);
                 }));
-  FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * n * C * D,
+  FF_HIP(launch(FF_KERNEL_HEAD, Sizes{n, C, D, 3}, 2.0 * n * C * D,
                 feat_bytes + n * C * 4.0 + (double)splits * C * D * 4.0, st, [&] {
                   return ffk::launch_head_grad(f, hs.G, n, C, D, splits, hs.part, st);
                 }));
-  FF_HIP(launch(FF_KERNEL_HEAD, 0.0, (double)splits * C * D * 4.0 + (double)C * D * 24.0, st,
-                [&] {
+  FF_HIP(launch(FF_KERNEL_HEAD, Sizes{n, C, D, 4}, 0.0,
+                (double)splits * C * D * 4.0 + (double)C * D * 24.0, st, [&] {
                   return ffk::launch_head_adam(hs.part, splits, hs.G, hs.lrow, n, C, D,
                                                head->W, head->mW, head->vW, head->b, head->mb,
                                                head->vb, a, loss ? loss : hs.loss, st);
@@ -1002,7 +1016,7 @@ ff_status ff_head_predict(const ff_layer *layers, int32_t n_layers, int32_t firs
   ffk::HeadFeatures f;
   FF_TRY(head_features(layers, n_layers, first_layer, hp, x_base, n, C, hs, st, f));
   head_weights(f, head->W, head->b, D);
-  FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * n * C * D,
+  FF_HIP(launch(FF_KERNEL_HEAD, Sizes{n, C, D, 1}, 2.0 * n * C * D,
                 (double)n * D * 4.0 + (double)C * D * 4.0 + n * (C + 1) * 4.0, st, [&] {
                   return ffk::launch_head_logits(f, n, C, nullptr, logits, pred, nullptr,
                                                  nullptr, st);
@@ -1644,7 +1658,8 @@ ff_status ff_po_predict(const ff_layer *layers, const ff_head *heads, int32_t n_
   }
   double D = 0;
   for (int l = l0; l < n_layers; ++l) D += layers[l].d_out;
-  FF_HIP(launch(FF_KERNEL_HEAD, 2.0 * n * C * D, (double)n * D * 4.0 + C * D * 4.0, st, [&] {
+  FF_HIP(launch(FF_KERNEL_HEAD, Sizes{n, C, (int32_t)D, 1}, 2.0 * n * C * D,
+                (double)n * D * 4.0 + C * D * 4.0, st, [&] {
     return ffk::launch_head_logits(f, n, C, nullptr, logits, pred, nullptr, nullptr, st);
   }));
   return FF_OK;
@@ -1681,11 +1696,13 @@ ff_status ff_profile_start(int32_t max_launches, uint32_t kind_mask) {
   return FF_OK;
 }
 
-ff_status ff_profile_stop(ff_kernel_stats *stats) {
+ff_status ff_profile_stop_launches(ff_kernel_stats *stats, ff_launch_record *launches,
+                                   int32_t max_launches, int32_t *n_launches) {
   std::lock_guard<std::mutex> lk(g_prof.mu);
   if (!g_prof.on) return fail(FF_ERR_INVALID_ARG, "no active profile");
   g_prof.on = false;
   ff_status st = FF_OK;
+  if (n_launches) *n_launches = 0;
   if (stats)
     for (int k = 0; k < FF_KERNEL_KINDS; ++k) stats[k] = ff_kernel_stats{0, 0.0, 0.0, 0.0};
   for (const ProfRec &r : g_prof.recs) {
@@ -1696,6 +1713,9 @@ ff_status ff_profile_stop(ff_kernel_stats *stats) {
       st = fail(FF_ERR_HIP, "reading kernel timing events: %s", hipGetErrorString(e));
       continue;
     }
+    if (launches && n_launches && *n_launches < max_launches)
+      launches[(*n_launches)++] =
+          ff_launch_record{r.kind, r.sz.m, r.sz.n, r.sz.k, r.sz.aux, ms, r.flops, r.bytes};
     if (stats) {
       ff_kernel_stats &k = stats[r.kind];
       k.launches += 1;
@@ -1709,6 +1729,10 @@ ff_status ff_profile_stop(ff_kernel_stats *stats) {
   g_prof.recs.clear();
   g_prof.used = 0;
   return st;
+}
+
+ff_status ff_profile_stop(ff_kernel_stats *stats) {
+  return ff_profile_stop_launches(stats, nullptr, 0, nullptr);
 }
 
 }  // extern "C"

@@ -802,7 +802,7 @@ __device__ __forceinline__ void nt_mainloop4(const uint16_t *__restrict__ X,
   lds_barrier();
 }
 
-template <int BM, int BN, bool STORE_H>
+template <int BM, int BN, int NBUF, bool STORE_H>
 __global__ __launch_bounds__(256) void k_fwd4(const uint16_t *__restrict__ X,
                                               const uint16_t *__restrict__ W,
                                               const float *__restrict__ bias,
@@ -810,7 +810,7 @@ __global__ __launch_bounds__(256) void k_fwd4(const uint16_t *__restrict__ X,
                                               int K, float *__restrict__ H,
                                               float *__restrict__ gpart) {
   constexpr int WN = 2, TM = BM / 2, TN = BN / 2, MB = TM / 32, NB = TN / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t sm[2 * (BM + BN) * 64];
+  __shared__ __attribute__((aligned(16))) uint16_t sm[NBUF * (BM + BN) * 64];
   const int nt = (N + BN - 1) / BN;
   int tm, tn;
   tile_of(blockIdx.x, (M + BM - 1) / BM, nt, tm, tn);
@@ -819,7 +819,7 @@ __global__ __launch_bounds__(256) void k_fwd4(const uint16_t *__restrict__ X,
   const int wm = wave / WN, wn = wave % WN;
   const int li = lane & 31, kg = lane >> 5;
   floatx16 acc[MB][NB];
-  nt_mainloop4<BM, BN>(X, W, M, N, K, m0, n0, sm, acc);
+  nt_mainloop4<BM, BN, NBUF>(X, W, M, N, K, m0, n0, sm, acc);
 
   // Epilogue as in k_fwd, one 32-row block at a time, so that only 16 row
   // sums and scales are live beside the accumulators.
@@ -1327,6 +1327,8 @@ constexpr int kTRows = 64;  // batch rows per transposed block
 // the writes of a wave (one column word per lane) then fall on 64 distinct
 // banks, and a lane gathers its 16 rows of a column as 8 words.
 constexpr int kTWords = kTRows / 2 + 1;
+// 64-column sub-tiles per workgroup of the loss pass with the bf16 operand.
+constexpr int kLossTSubs = 2;
 
 // Writes rows r0..r0+63 of column `col` of a transposed tile from T (lane
 // segment seg: rows 16 seg .. 16 seg + 15) to out[col][r0 + ...] (row stride Rp).
@@ -1342,10 +1344,13 @@ __device__ __forceinline__ void store_tcol(const uint32_t (*T)[kTWords], int c, 
 
 // Loss rows (as k_loss_rows, over 64-row blocks) and dZ^T = bf16(c . H)^T
 // (R3) with the per-block column sums of c . H in fp32 for db:
-//   grid (Rp / 64, ceil(D / 256)); each workgroup takes 64 rows and 256
-//   columns in four 64 x 64 sub-tiles, staged through LDS to transpose.
-//   Column block 0 also writes g, c and the loss partials lpart[2 * block].
+//   grid (Rp / 64, ceil(D / (64 SUBS))); each workgroup takes 64 rows and
+//   SUBS 64-column sub-tiles, staged through LDS to transpose.  The H loads of
+//   all its sub-tiles are issued beside the goodness partials, before the row
+//   coefficients c are known.  Every workgroup sums its rows' goodness; column
+//   block 0 also writes g, c and the loss partials lpart[2 * block].
 // Rows R..Rp-1 give zero columns of dZ^T.
+template <int SUBS>
 __global__ __launch_bounds__(kBlock) void k_loss_t(const float *__restrict__ gpart, int nt, int R,
                                                    int Rp, int n_pos, float theta,
                                                    const float *__restrict__ H, int D,
@@ -1355,10 +1360,22 @@ __global__ __launch_bounds__(kBlock) void k_loss_t(const float *__restrict__ gpa
                                                    uint16_t *__restrict__ dzT,
                                                    float *__restrict__ dbp) {
   __shared__ float cs[kTRows];
-  __shared__ float red[16][kTRows + 4];
-  __shared__ uint32_t T[kTRows][kTWords];
+  __shared__ float red[SUBS][16][kTRows + 4];
+  __shared__ uint32_t T[SUBS][kTRows][kTWords];
   const int tid = threadIdx.x;
-  const int r0 = blockIdx.x * kTRows;
+  const int r0 = blockIdx.x * kTRows, cb0 = blockIdx.y * 64 * SUBS;
+  const int q = tid & 15, p = tid >> 4;  // column quad; row pairs p and p + 16
+  // rows 2p, 2p+1, 2p+32, 2p+33 of each sub-tile's column quad
+  float4 v[SUBS][4];
+#pragma unroll
+  for (int sub = 0; sub < SUBS; ++sub)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = 2 * p + (i & 1) + 32 * (i >> 1), r = r0 + row;
+      const int col = cb0 + sub * 64 + 4 * q;
+      v[sub][i] = (r < R && col < D) ? ld4(H + (size_t)r * D + col)
+                                     : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
   if (tid < kTRows) {  // wave 0: the block's rows
     const int r = r0 + tid;
     float cr = 0.f, lp = 0.f, ln = 0.f;
@@ -1366,11 +1383,11 @@ __global__ __launch_bounds__(kBlock) void k_loss_t(const float *__restrict__ gpa
       float gv = 0.f;
       int t = 0;
       for (; t + 8 <= nt; t += 8) {
-        float p[8];
+        float pt[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) p[j] = gpart[(size_t)(t + j) * R + r];
+        for (int j = 0; j < 8; ++j) pt[j] = gpart[(size_t)(t + j) * R + r];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) gv += p[j];
+        for (int j = 0; j < 8; ++j) gv += pt[j];
       }
       for (; t < nt; ++t) gv += gpart[(size_t)t * R + r];
       if (r < n_pos) {
@@ -1396,50 +1413,50 @@ __global__ __launch_bounds__(kBlock) void k_loss_t(const float *__restrict__ gpa
     }
   }
   __syncthreads();
-  const int q = tid & 15, p = tid >> 4;  // column quad; row pairs p and p + 16
-#pragma unroll 1
-  for (int sub = 0; sub < 4; ++sub) {
-    const int cb = blockIdx.y * 256 + sub * 64;
-    if (cb >= D) break;  // uniform
-    const int col = cb + 4 * q;
-    float4 v[4];
+  float cc[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {  // rows 2p, 2p+1, 2p+32, 2p+33
-      const int row = 2 * p + (i & 1) + 32 * (i >> 1), r = r0 + row;
-      v[i] = (r < R && col < D) ? ld4(H + (size_t)r * D + col) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
+  for (int i = 0; i < 4; ++i) cc[i] = cs[2 * p + (i & 1) + 32 * (i >> 1)];
+#pragma unroll
+  for (int sub = 0; sub < SUBS; ++sub) {
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float cc = cs[2 * p + (i & 1) + 32 * (i >> 1)];
-      v[i] = make_float4(v[i].x * cc, v[i].y * cc, v[i].z * cc, v[i].w * cc);
-      acc.x += v[i].x;
-      acc.y += v[i].y;
-      acc.z += v[i].z;
-      acc.w += v[i].w;
+      float4 &w = v[sub][i];
+      w = make_float4(w.x * cc[i], w.y * cc[i], w.z * cc[i], w.w * cc[i]);
+      acc.x += w.x;
+      acc.y += w.y;
+      acc.z += w.z;
+      acc.w += w.w;
     }
 #pragma unroll
     for (int h = 0; h < 2; ++h) {  // the word of rows (2p, 2p+1) + 32 h of each column
-      const float4 a = v[2 * h], b = v[2 * h + 1];
-      T[4 * q + 0][p + 16 * h] = pack_bf16(a.x, b.x);
-      T[4 * q + 1][p + 16 * h] = pack_bf16(a.y, b.y);
-      T[4 * q + 2][p + 16 * h] = pack_bf16(a.z, b.z);
-      T[4 * q + 3][p + 16 * h] = pack_bf16(a.w, b.w);
+      const float4 a = v[sub][2 * h], b = v[sub][2 * h + 1];
+      T[sub][4 * q + 0][p + 16 * h] = pack_bf16(a.x, b.x);
+      T[sub][4 * q + 1][p + 16 * h] = pack_bf16(a.y, b.y);
+      T[sub][4 * q + 2][p + 16 * h] = pack_bf16(a.z, b.z);
+      T[sub][4 * q + 3][p + 16 * h] = pack_bf16(a.w, b.w);
     }
-    red[p][4 * q + 0] = acc.x;
-    red[p][4 * q + 1] = acc.y;
-    red[p][4 * q + 2] = acc.z;
-    red[p][4 * q + 3] = acc.w;
-    __syncthreads();
-    if (tid < kTRows && cb + tid < D) {
+    red[sub][p][4 * q + 0] = acc.x;
+    red[sub][p][4 * q + 1] = acc.y;
+    red[sub][p][4 * q + 2] = acc.z;
+    red[sub][p][4 * q + 3] = acc.w;
+  }
+  __syncthreads();
+  // db partials: thread (sub, column) sums its column's 16 row-group sums
+  for (int i = tid; i < SUBS * 64; i += kBlock) {
+    const int sub = i >> 6, c = i & 63, col = cb0 + sub * 64 + c;
+    if (col < D) {
       float sum = 0.f;
 #pragma unroll
-      for (int k = 0; k < 16; ++k) sum += red[k][tid];
-      dbp[(size_t)blockIdx.x * D + cb + tid] = sum;
+      for (int k = 0; k < 16; ++k) sum += red[sub][k][c];
+      dbp[(size_t)blockIdx.x * D + col] = sum;
     }
-    const int c = tid >> 2, seg = tid & 3;
-    if (cb + c < D) store_tcol(T, c, seg, dzT + (size_t)(cb + c) * Rp + r0);
-    __syncthreads();
+  }
+  const int c = tid >> 2, seg = tid & 3;
+#pragma unroll
+  for (int sub = 0; sub < SUBS; ++sub) {
+    const int col = cb0 + sub * 64 + c;
+    if (col < D) store_tcol(T[sub], c, seg, dzT + (size_t)col * Rp + r0);
   }
 }
 
@@ -2196,13 +2213,13 @@ void fwd_launch(const void *x, const void *w, const float *bias, const float *ro
   const E *we = static_cast<const E *>(w);
   static_assert(T::bk == nt_bk<BF16>(), "forward k-tile is 128 bytes");
   if constexpr (BF16 && T::four) {
-    static_assert(T::wm == 2 && T::wn == 2 && T::pf == 2, "four-wave tile");
+    static_assert(T::wm == 2 && T::wn == 2, "four-wave tile");
     if (H)
-      hipLaunchKernelGGL((k_fwd4<T::bm, T::bn, true>), grid, dim3(256), 0, s, xe, we, bias,
+      hipLaunchKernelGGL((k_fwd4<T::bm, T::bn, T::pf, true>), grid, dim3(256), 0, s, xe, we, bias,
                          rowscale, M, N, K, H, gpart);
     else
-      hipLaunchKernelGGL((k_fwd4<T::bm, T::bn, false>), grid, dim3(256), 0, s, xe, we, bias,
-                         rowscale, M, N, K, H, gpart);
+      hipLaunchKernelGGL((k_fwd4<T::bm, T::bn, T::pf, false>), grid, dim3(256), 0, s, xe, we,
+                         bias, rowscale, M, N, K, H, gpart);
   } else if (H) {
     hipLaunchKernelGGL((k_fwd<BF16, T::bm, T::bn, T::wm, T::wn, T::pf, true>), grid,
                        dim3(T::threads), 0, s, xe, we, bias, rowscale, M, N, K, H, gpart);
@@ -2274,9 +2291,11 @@ hipError_t launch_loss_t(const float *gpart, int ntiles, int R, int n_pos, float
                         const float *H, int D, float *g, float *c, float *lpart, uint16_t *dzT,
                         float *dbp, hipStream_t s) {
   if (R <= 0) return hipSuccess;
+  if (D % 4) return hipErrorInvalidValue;
   const int Rp = padded_rows(R);
-  hipLaunchKernelGGL(k_loss_t, dim3(Rp / kTRows, cdiv(D, 256)), dim3(kBlock), 0, s, gpart, ntiles,
-                     R, Rp, n_pos, theta, H, D, g, c, lpart, dzT, dbp);
+  constexpr int subs = kLossTSubs;
+  hipLaunchKernelGGL(k_loss_t<subs>, dim3(Rp / kTRows, cdiv(D, 64 * subs)), dim3(kBlock), 0, s,
+                     gpart, ntiles, R, Rp, n_pos, theta, H, D, g, c, lpart, dzT, dbp);
   return hipGetLastError();
 }
 

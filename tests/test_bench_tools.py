@@ -106,3 +106,76 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+TRACE_FIELDS = ["Kind", "Agent_Id", "Queue_Id", "Stream_Id", "Thread_Id", "Dispatch_Id",
+                "Kernel_Id", "Kernel_Name", "Correlation_Id", "Start_Timestamp", "End_Timestamp",
+                "Grid_Size_X"]
+LOSS = "void ffk::(anonymous namespace)::k_loss_rows(...)"
+
+
+def _trace(path, rows):
+    """rows: (dispatch id, kernel name, duration in ns)"""
+    with open(path, "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=TRACE_FIELDS)
+        w.writeheader()
+        t = 1000
+        for d, name, ns in rows:
+            r = {k: 0 for k in TRACE_FIELDS}
+            r.update(Dispatch_Id=d, Kernel_Name=name, Start_Timestamp=t, End_Timestamp=t + ns)
+            t += ns + 10
+            w.writerow(r)
+    return str(path)
+
+
+def _rec(kind, m, n, k, flops, bytes_, ms, aux=0):
+    return dict(kind=kind, m=m, n=n, k=k, aux=aux, ms=ms, flops=flops, bytes=bytes_)
+
+
+def test_shape_labels_and_weighted_fraction():
+    a = _rec("forward", 2048, 2000, 784, 2.0 * 2048 * 2000 * 784, 1e6, 0.1)
+    b = _rec("forward", 2048, 2000, 2000, 2.0 * 2048 * 2000 * 2000, 1e6, 0.2)
+    assert bench.shape_label(a) == "2048x784->2000"
+    assert bench.shape_label(_rec("forward", 100, 2000, 784, 0, 0, 0, aux=10)) == \
+        "100x784->2000 (x10 labels)"
+    assert bench.shape_label(_rec("dw_adam", 2000, 784, 2048, 0, 0, 0)) == "784->2000 over 2048 rows"
+    assert bench.shape_label(_rec("embed_norm", 4096, 3072, 0, 0, 0, 0, aux=1 | 16)) == \
+        "4096x3072 (pairs, bf16 out)"
+    recs = [a, b, b]
+    shapes = bench.by_shape(recs, "f32")
+    assert [s["launches"] for s in shapes] == [1, 2]
+    assert shapes[1]["avg_us"] == pytest.approx(200.0)
+    tot = bench.kind_totals(recs, "f32")["forward"]
+    # shape-weighted: summed flops over summed time, not the mean of the per-shape fractions
+    want = (a["flops"] + 2 * b["flops"]) / (0.5e-3) / 1e12
+    assert tot["TFLOP/s"] == pytest.approx(want)
+    assert tot["frac"] == pytest.approx(want / bench.PEAK["f32"][1])
+
+
+def test_rocprof_shapes_matches_dispatches_in_order(tmp_path, capsys):
+    recs = [_rec("forward", 64, 64, 64, 2.0 * 64 ** 3, 1.0, 0.005),
+            _rec("loss", 64, 64, 1, 0.0, 4e6, 0.002),
+            _rec("forward", 64, 64, 64, 2.0 * 64 ** 3, 1.0, 0.004),
+            _rec("loss", 64, 64, 1, 0.0, 4e6, 0.001)]
+    lst = tmp_path / "l.json"
+    bench.write_launch_list(str(lst), recs, [False, False, True, True], "f32", "test")
+    # a torch kernel between ours is skipped; durations come from the trace
+    tr = _trace(tmp_path / "t.csv", [(1, FWD, 5000), (2, "at::native::copy", 99), (3, LOSS, 2000),
+                                     (4, FWD, 8000), (5, LOSS, 1000)])
+    bench.rocprof_shapes(tr, str(lst))
+    out = capsys.readouterr().out
+    assert "| forward | 64x64->64 | 1 | 8.0 | 4.0 |" in out
+    assert "| loss | 64x64 | 1 | 1.0 | 1.0 | 4.00 MB | 4000 GB/s | 50.0 % |" in out
+    bad = _trace(tmp_path / "b.csv", [(1, FWD, 5000), (3, FWD, 2000), (4, FWD, 8000),
+                                      (5, LOSS, 1000)])
+    with pytest.raises(SystemExit, match="launch 1"):
+        bench.rocprof_shapes(bad, str(lst))
+    short = _trace(tmp_path / "s.csv", [(1, FWD, 5000)])
+    with pytest.raises(SystemExit, match="dispatches"):
+        bench.rocprof_shapes(short, str(lst))
+    # set-up dispatches before the recorded window are skipped
+    pre = _trace(tmp_path / "p.csv", [(0, "k_bf16_shadow", 700), (1, FWD, 5000), (3, LOSS, 2000),
+                                      (4, FWD, 6000), (5, LOSS, 1000)])
+    bench.rocprof_shapes(pre, str(lst))
+    out = capsys.readouterr().out
+    assert "after 1 earlier ones" in out and "| forward | 64x64->64 | 1 | 6.0 | 4.0 |" in out
