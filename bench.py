@@ -71,7 +71,8 @@ def load_traffic(kernel, workload):
 KIND_OF = [("k_fwd", "forward"), ("k_dw_adam", "dw_adam"), ("k_dw4", "dw_adam"),
            ("k_embed_norm", "embed_norm"), ("k_loss_rows", "loss"), ("k_loss_t", "loss"),
            ("k_goodness", "goodness"), ("k_argmax", "argmax"), ("k_bf16_shadow", "bf16_shadow"),
-           ("k_transpose_bf16", "transpose"), ("k_head_", "head"), ("k_po_dz", "head")]
+           ("k_transpose_bf16", "transpose"), ("k_head_", "head"), ("k_po_dz", "head"),
+           ("k_adam_dense", "adam")]
 MFMA_KINDS = ("forward", "dw_adam")
 ROW_MODES = ["rows", "pairs", "expand", "masked", "neutral"]
 HEAD_PARTS = ["", "logits", "layer dZ", "grad partials", "Adam"]
@@ -87,7 +88,9 @@ def shape_label(r):
     if kind == "forward":
         return f"{m}x{k}->{n}" + (f" (x{aux} labels)" if aux else "")
     if kind == "dw_adam":
-        return f"{n}->{m} over {k} rows"
+        return f"{n}->{m} over {k} rows" + (" (gradient out)" if aux else "")
+    if kind == "adam":
+        return f"{m}x{n}"
     if kind == "head":
         return f"{m}x{k}->{n} classes ({HEAD_PARTS[aux]})"
     if kind == "loss":

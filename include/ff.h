@@ -395,7 +395,8 @@ typedef enum {
   FF_KERNEL_SHADOW = 6,      /* bf16 weight shadow refresh                    */
   FF_KERNEL_HEAD = 7,        /* softmax layer: logits, gradient, Adam         */
   FF_KERNEL_TRANSPOSE = 8,   /* bf16 operand transposes of the weight gradient */
-  FF_KERNEL_KINDS = 9
+  FF_KERNEL_ADAM = 9,        /* Adam update from a stored weight gradient     */
+  FF_KERNEL_KINDS = 10
 } ff_kernel_kind;
 
 typedef struct {
@@ -409,7 +410,9 @@ typedef struct {
  *   FORWARD      m rows, n output features, k input features; aux = label
  *                count of the label-expanding scoring product (m base rows),
  *                else 0;
- *   DW_ADAM      m = d_out, n = d_in, k = rows contracted;
+ *   DW_ADAM      m = d_out, n = d_in, k = rows contracted; aux = 1 when the
+ *                product stores the gradient for a separate ADAM launch;
+ *   ADAM         m = d_out, n = d_in, k = rows of the step;
  *   EMBED_NORM   m rows, n features; aux = the row source mode, plus 16
  *                for bf16 output rows;
  *   LOSS         m rows, n = d_out, k = goodness partials per row; aux = 1

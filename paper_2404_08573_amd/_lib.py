@@ -37,7 +37,7 @@ EXPORTS = ["ff_status_string", "ff_last_error", "ff_embed_labels", "ff_step_work
            "ff_layer_step_noalloc"]
 
 KERNEL_KINDS = ["embed_norm", "forward", "loss", "dw_adam", "goodness", "argmax", "bf16_shadow",
-                "head", "transpose"]
+                "head", "transpose", "adam"]
 
 
 class FFError(RuntimeError):

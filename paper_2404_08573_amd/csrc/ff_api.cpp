@@ -134,12 +134,17 @@ struct StepScratch {
   uint16_t *xt = nullptr;   // [d_in][Rp] x_hat^T
   uint16_t *dzt = nullptr;  // [d_out][Rp] bf16(c . H)^T
   float *dbp = nullptr;     // [Rp / 64][d_out]
+  // bf16 FF training steps of an epoch: the weight gradient, stored for an
+  // Adam launch of its own (which other streams' products can run beside)
+  float *dw = nullptr;      // [d_out][d_in]
 };
 
 // train: the scratch of a training step (the bf16 weight-gradient operands);
-// false for forward passes only.
+// false for forward passes only.  split_adam: a bf16 training step also gets
+// the weight-gradient buffer, and runs its Adam update as a launch of its own.
 void carve_step(Carver &cv, StepScratch &s, int rows, int d_in, int d_out, int dtype, bool need_h,
-                bool need_g, bool need_loss, int po_classes = 0, bool train = true) {
+                bool need_g, bool need_loss, int po_classes = 0, bool train = true,
+                bool split_adam = false) {
   if (po_classes > 0) {
     s.G = static_cast<float *>(cv.take((size_t)rows * po_classes * 4));
     s.lrow = static_cast<float *>(cv.take((size_t)rows * 4));
@@ -160,6 +165,7 @@ void carve_step(Carver &cv, StepScratch &s, int rows, int d_in, int d_out, int d
     s.xt = static_cast<uint16_t *>(cv.take(rp * d_in * 2));
     s.dzt = static_cast<uint16_t *>(cv.take(rp * d_out * 2));
     s.dbp = static_cast<float *>(cv.take((size_t)ffk::loss_blocks(rows) * d_out * 4));
+    if (split_adam) s.dw = static_cast<float *>(cv.take((size_t)d_out * d_in * 4));
   }
 }
 
@@ -377,13 +383,23 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int
     const int64_t t = L->step + 1;
     const ffk::AdamArgs a = adam_args(hp, t);
     const double params = (double)L->d_out * L->d_in;
-    const double bytes = (double)Rp * (L->d_out + L->d_in) * 2.0 + params * 26.0 +
-                         (double)nrb * L->d_out * 4.0 + L->d_out * 24.0;
-    FF_HIP(launch(FF_KERNEL_DW_ADAM, Sizes{L->d_out, L->d_in, R, 0},
+    const double operands = (double)Rp * (L->d_out + L->d_in) * 2.0;
+    const double adam = params * 24.0 + params * 2.0 + (double)nrb * L->d_out * 4.0 +
+                        L->d_out * 24.0;  // W, m, v in and out, Wb out, b
+    // split: the product stores dW, then the Adam launch reads it back
+    const double bytes = s.dw ? operands + params * 4.0 : operands + adam;
+    FF_HIP(launch(FF_KERNEL_DW_ADAM, Sizes{L->d_out, L->d_in, R, s.dw ? 1 : 0},
                   gemm_flops(L->d_out, L->d_in, R), bytes, st, [&] {
-      return ffk::launch_dw4(s.dzt, s.xt, L->d_out, L->d_in, R, L->W, L->mW, L->vW, L->W_bf16,
-                             s.dbp, L->b, L->mb, L->vb, a, lf, st);
+      return ffk::launch_dw4(s.dzt, s.xt, L->d_out, L->d_in, R, s.dw, L->W, L->mW, L->vW,
+                             L->W_bf16, s.dbp, L->b, L->mb, L->vb, a, lf, st);
     }));
+    if (s.dw)
+      FF_HIP(launch(FF_KERNEL_ADAM, Sizes{L->d_out, L->d_in, R, 0}, 0.0, params * 4.0 + adam, st,
+                    [&] {
+                      return ffk::launch_adam_dense(s.dw, L->d_out, L->d_in, L->W, L->mW, L->vW,
+                                                    L->W_bf16, s.dbp, R, L->b, L->mb, L->vb, a,
+                                                    st);
+                    }));
     L->step = t;
     return FF_OK;
   }
@@ -1041,6 +1057,11 @@ struct PipeScratch {
   float *act_s[2] = {nullptr, nullptr};  // sequential, fp32: their row normalisation
 };
 
+// Whether the bf16 steps of an epoch run Adam as a launch of its own (see
+// StepScratch::dw), by schedule.
+constexpr bool kSplitAdamPipelined = true;
+constexpr bool kSplitAdamSequential = false;
+
 // rpp: rows per sample in a chunk (2 for FF: a positive and a negative row;
 // 1 for the performance-optimised variant); po_classes > 0 adds its scratch.
 void carve_pipe(Carver &cv, PipeScratch &p, const ff_layer *layers, int L, int n, int chunk,
@@ -1054,7 +1075,8 @@ void carve_pipe(Carver &cv, PipeScratch &p, const ff_layer *layers, int L, int n
     }
     for (int l = 0; l < L; ++l)
       carve_step(cv, p.step[l], rows, l == 0 || dtype == FF_BF16 ? layers[l].d_in : 0,
-                 layers[l].d_out, dtype, l + 1 == L, false, false, po_classes);
+                 layers[l].d_out, dtype, l + 1 == L, false, false, po_classes, true,
+                 kSplitAdamPipelined);
     for (int l = 1; l < L; ++l)
       for (int k = 0; k < kPipeSlots; ++k) {
         p.slot[k][l] = static_cast<float *>(cv.take((size_t)rows * layers[l].d_in * 4));
@@ -1067,7 +1089,8 @@ void carve_pipe(Carver &cv, PipeScratch &p, const ff_layer *layers, int L, int n
       max_out = std::max(max_out, layers[l].d_out);
     }
     p.step.assign(2, StepScratch());
-    carve_step(cv, p.step[0], rows, max_in, max_out, dtype, true, false, false, po_classes);
+    carve_step(cv, p.step[0], rows, max_in, max_out, dtype, true, false, false, po_classes, true,
+               kSplitAdamSequential);
     // the forward pass with the final weights, run beside the next layer's steps
     carve_step(cv, p.step[1], rows, max_in, max_out, dtype, false, false, false, 0, false);
     int max_hidden = 0;

@@ -179,9 +179,19 @@ hipError_t launch_transpose_bf16(const uint16_t *x, int R, int d, uint16_t *xT, 
 // bf16 weight gradient dW = dZ^T (xT)^T over padded_rows(R) rows (operands from
 // launch_loss_t and launch_transpose_bf16; M = d_out, N = d_in), with the Adam
 // update of W, its shadow Wb and b (db from dbp) fused, and the loss scalar of lf.
-hipError_t launch_dw4(const uint16_t *dzT, const uint16_t *xT, int M, int N, int R, float *W,
-                      float *mW, float *vW, uint16_t *Wb, const float *dbp, float *b, float *mb,
-                      float *vb, const AdamArgs &a, const LossFinish &lf, hipStream_t s);
+// G non-null: dW is stored into G [M][N] instead and W, b are left for
+// launch_adam_dense (the loss scalar is still finished).
+hipError_t launch_dw4(const uint16_t *dzT, const uint16_t *xT, int M, int N, int R, float *G,
+                      float *W, float *mW, float *vW, uint16_t *Wb, const float *dbp, float *b,
+                      float *mb, float *vb, const AdamArgs &a, const LossFinish &lf,
+                      hipStream_t s);
+
+// The Adam update launch_dw4 fuses, from a stored gradient: W, mW, vW, Wb
+// [M][N] from G [M][N] (N a multiple of 4), and b, mb, vb [M] from the db
+// partials dbp [loss_blocks(R)][M] of the R-row step.
+hipError_t launch_adam_dense(const float *G, int M, int N, float *W, float *mW, float *vW,
+                             uint16_t *Wb, const float *dbp, int R, float *b, float *mb,
+                             float *vb, const AdamArgs &a, hipStream_t s);
 
 // g_r = sum_t gpart[t][r] into g (any of the outputs may be null);
 // out[r] = g_r (accumulate == 0) or out[r] += g_r (accumulate == 1);

@@ -874,13 +874,17 @@ __global__ __launch_bounds__(256) void k_fwd4(const uint16_t *__restrict__ X,
 // float4 updates' loads in flight, so the W, m, v traffic streams instead of
 // waiting on one load at a time.  db sums the 64-row column partials of
 // k_loss_t in a fixed order.
+// ADAM = false: the epilogue stores dW (fp32, [M][N]) into G instead, and
+// k_adam_dense applies the same update (and the one of b) in a launch of its
+// own, which holds no LDS and so shares the CUs with other streams' products.
 // ---------------------------------------------------------------------------
 constexpr int kAdamBatch = 6;
 
-template <int BM, int BN, int NBUF>
+template <int BM, int BN, int NBUF, bool ADAM>
 __global__ __launch_bounds__(256) void k_dw4(const uint16_t *__restrict__ dzT,
                                              const uint16_t *__restrict__ xT, int M, int N,
-                                             int K, float *__restrict__ W, float *__restrict__ mW,
+                                             int K, float *__restrict__ G,
+                                             float *__restrict__ W, float *__restrict__ mW,
                                              float *__restrict__ vW, uint16_t *__restrict__ Wb,
                                              const float *__restrict__ dbp, int nrb,
                                              float *__restrict__ bvec, float *__restrict__ mbv,
@@ -936,7 +940,7 @@ __global__ __launch_bounds__(256) void k_dw4(const uint16_t *__restrict__ dzT,
         const int mr = idx / (BN / 4), n4 = (idx % (BN / 4)) * 4;
         ok[u] = idx < Q && mh + mr < M && n0 + n4 < N;
         o[u] = ok[u] ? (size_t)(mh + mr) * N + n0 + n4 : 0;
-        if (ok[u]) {
+        if (ADAM && ok[u]) {
           p[u] = ld4(W + o[u]);
           m[u] = ld4(mW + o[u]);
           v[u] = ld4(vW + o[u]);
@@ -948,6 +952,10 @@ __global__ __launch_bounds__(256) void k_dw4(const uint16_t *__restrict__ dzT,
         const int idx = i0 + 256 * u;
         const int mr = idx / (BN / 4), n4 = (idx % (BN / 4)) * 4;
         const float4 g = ld4(Cs + mr * LDC + n4);
+        if (!ADAM) {
+          st4(G + o[u], g);
+          continue;
+        }
         adam_update(p[u].x, m[u].x, v[u].x, g.x, ad);
         adam_update(p[u].y, m[u].y, v[u].y, g.y, ad);
         adam_update(p[u].z, m[u].z, v[u].z, g.z, ad);
@@ -966,7 +974,7 @@ __global__ __launch_bounds__(256) void k_dw4(const uint16_t *__restrict__ dzT,
     __syncthreads();  // the half tile's reads are done before the next one is written
   }
 
-  if (tn == 0) {  // db = sum of the 64-row column partials, then Adam on b
+  if (ADAM && tn == 0) {  // db = sum of the 64-row column partials, then Adam on b
     for (int t = tid; t < BM; t += 256) {
       const int row = m0 + t;
       if (row >= M) continue;
@@ -985,6 +993,74 @@ __global__ __launch_bounds__(256) void k_dw4(const uint16_t *__restrict__ dzT,
       bvec[row] = p;
       mbv[row] = m;
       vbv[row] = v;
+    }
+  }
+}
+
+// Adam on W [M][N] (and its bf16 shadow Wb) from the weight gradient G, and
+// on b from the 64-row column partials dbp [nrb][M] (summed in block order):
+// the update k_dw4 fuses, as a launch of its own.  The first workgroups take
+// float4 groups of W, kAdamBatch per thread with their loads in flight; the
+// last ceil(M / 256) take one bias row per thread.  N is a multiple of 4.
+__global__ __launch_bounds__(kBlock) void k_adam_dense(const float *__restrict__ G, int M, int N,
+                                                       int nmain, float *__restrict__ W,
+                                                       float *__restrict__ mW,
+                                                       float *__restrict__ vW,
+                                                       uint16_t *__restrict__ Wb,
+                                                       const float *__restrict__ dbp, int nrb,
+                                                       float *__restrict__ bvec,
+                                                       float *__restrict__ mbv,
+                                                       float *__restrict__ vbv, AdamArgs ad) {
+  const int tid = threadIdx.x;
+  if ((int)blockIdx.x >= nmain) {
+    const int row = (blockIdx.x - nmain) * kBlock + tid;
+    if (row >= M) return;
+    float sum = 0.f;  // in block order, 16 loads in flight
+    int k = 0;
+    for (; k + 16 <= nrb; k += 16) {
+      float q[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) q[j] = dbp[(size_t)(k + j) * M + row];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) sum += q[j];
+    }
+    for (; k < nrb; ++k) sum += dbp[(size_t)k * M + row];
+    float p = bvec[row], m = mbv[row], v = vbv[row];
+    adam_update(p, m, v, sum, ad);
+    bvec[row] = p;
+    mbv[row] = m;
+    vbv[row] = v;
+    return;
+  }
+  const size_t n4 = (size_t)M * N / 4;
+  const size_t base = (size_t)blockIdx.x * kBlock * kAdamBatch + tid;
+  float4 p[kAdamBatch], m[kAdamBatch], v[kAdamBatch], g[kAdamBatch];
+#pragma unroll
+  for (int u = 0; u < kAdamBatch; ++u) {
+    const size_t i = base + (size_t)u * kBlock;
+    if (i < n4) {
+      g[u] = ld4(G + 4 * i);
+      p[u] = ld4(W + 4 * i);
+      m[u] = ld4(mW + 4 * i);
+      v[u] = ld4(vW + 4 * i);
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kAdamBatch; ++u) {
+    const size_t i = base + (size_t)u * kBlock;
+    if (i >= n4) continue;
+    adam_update(p[u].x, m[u].x, v[u].x, g[u].x, ad);
+    adam_update(p[u].y, m[u].y, v[u].y, g[u].y, ad);
+    adam_update(p[u].z, m[u].z, v[u].z, g[u].z, ad);
+    adam_update(p[u].w, m[u].w, v[u].w, g[u].w, ad);
+    st4(W + 4 * i, p[u]);
+    st4(mW + 4 * i, m[u]);
+    st4(vW + 4 * i, v[u]);
+    if (Wb) {
+      uint2 sh;
+      sh.x = pack_bf16(p[u].x, p[u].y);
+      sh.y = pack_bf16(p[u].z, p[u].w);
+      *reinterpret_cast<uint2 *>(Wb + 4 * i) = sh;
     }
   }
 }
@@ -2311,22 +2387,41 @@ hipError_t launch_transpose_bf16(const uint16_t *x, int R, int d, uint16_t *xT, 
 // The bf16 weight-gradient product takes 192x192 tiles when they give every CU
 // one (3072-wide layers), else 128x128.
 template <int BM, int BN, int NBUF>
-void dw4_launch(const uint16_t *dzT, const uint16_t *xT, int M, int N, int K, float *W, float *mW,
-                float *vW, uint16_t *Wb, const float *dbp, int nrb, float *b, float *mb, float *vb,
-                const AdamArgs &a, const LossFinish &lf, hipStream_t s) {
-  hipLaunchKernelGGL((k_dw4<BM, BN, NBUF>), dim3(cdiv(M, BM) * cdiv(N, BN)), dim3(256), 0, s, dzT, xT,
-                     M, N, K, W, mW, vW, Wb, dbp, nrb, b, mb, vb, a, lf);
+void dw4_launch(const uint16_t *dzT, const uint16_t *xT, int M, int N, int K, float *G, float *W,
+                float *mW, float *vW, uint16_t *Wb, const float *dbp, int nrb, float *b, float *mb,
+                float *vb, const AdamArgs &a, const LossFinish &lf, hipStream_t s) {
+  const dim3 grid(cdiv(M, BM) * cdiv(N, BN));
+  if (G)
+    hipLaunchKernelGGL((k_dw4<BM, BN, NBUF, false>), grid, dim3(256), 0, s, dzT, xT, M, N, K, G,
+                       W, mW, vW, Wb, dbp, nrb, b, mb, vb, a, lf);
+  else
+    hipLaunchKernelGGL((k_dw4<BM, BN, NBUF, true>), grid, dim3(256), 0, s, dzT, xT, M, N, K, G, W,
+                       mW, vW, Wb, dbp, nrb, b, mb, vb, a, lf);
 }
 
-hipError_t launch_dw4(const uint16_t *dzT, const uint16_t *xT, int M, int N, int R, float *W,
-                      float *mW, float *vW, uint16_t *Wb, const float *dbp, float *b, float *mb,
-                      float *vb, const AdamArgs &a, const LossFinish &lf, hipStream_t s) {
+hipError_t launch_dw4(const uint16_t *dzT, const uint16_t *xT, int M, int N, int R, float *G,
+                      float *W, float *mW, float *vW, uint16_t *Wb, const float *dbp, float *b,
+                      float *mb, float *vb, const AdamArgs &a, const LossFinish &lf,
+                      hipStream_t s) {
   const int Rp = padded_rows(R), nrb = Rp / kTRows;
   if (N % 8 || Rp > kMaxWidth) return hipErrorInvalidValue;
   if ((long)cdiv(M, 192) * cdiv(N, 192) >= kCUs)
-    dw4_launch<192, 192, 3>(dzT, xT, M, N, Rp, W, mW, vW, Wb, dbp, nrb, b, mb, vb, a, lf, s);
+    dw4_launch<192, 192, 3>(dzT, xT, M, N, Rp, G, W, mW, vW, Wb, dbp, nrb, b, mb, vb, a, lf, s);
   else
-    dw4_launch<128, 128, 3>(dzT, xT, M, N, Rp, W, mW, vW, Wb, dbp, nrb, b, mb, vb, a, lf, s);
+    dw4_launch<128, 128, 3>(dzT, xT, M, N, Rp, G, W, mW, vW, Wb, dbp, nrb, b, mb, vb, a, lf, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_adam_dense(const float *G, int M, int N, float *W, float *mW, float *vW,
+                             uint16_t *Wb, const float *dbp, int R, float *b, float *mb,
+                             float *vb, const AdamArgs &a, hipStream_t s) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if (N % 4) return hipErrorInvalidValue;
+  const int nrb = padded_rows(R) / kTRows;
+  const int nmain = (int)cdiv((long)M * N / 4, (long)kBlock * kAdamBatch);
+  const int nbias = (int)cdiv(M, kBlock);
+  hipLaunchKernelGGL(k_adam_dense, dim3(nmain + nbias), dim3(kBlock), 0, s, G, M, N, nmain, W, mW,
+                     vW, Wb, dbp, nrb, b, mb, vb, a);
   return hipGetLastError();
 }
 

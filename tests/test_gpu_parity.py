@@ -424,6 +424,37 @@ def test_pipeline_schedule_invariance_bitwise(P):
         np.testing.assert_array_equal(_np(x.W), _np(z.W))
 
 
+@pytest.mark.parametrize("sched", [0, 1])
+def test_epoch_adam_launch_matches_fused_steps_bitwise(P, sched):
+    """bf16 epochs run each step's Adam update as a launch of its own from the
+    stored weight gradient; single layer steps fuse it into the product's
+    epilogue.  A one-layer epoch (784 -> 256, 128-pair chunks, a ragged 44-pair
+    last chunk) equals the same chunks' embedded rows through ff_layer_step,
+    bit for bit: weights, moments, bias, bf16 shadow and per-chunk losses."""
+    hp = P.HParams(theta=2.0, lr=0.01, dtype=P.FF_BF16)
+    x_base, y, y_neg = make_data(190, 300, 784)
+    (W, b), = make_weights(191, (784, 256))
+    ep = P.Layer(_t(W), _t(b), True)
+    nc = -(-300 // 128)
+    trace = torch.zeros(1, nc, device=DEV)
+    P.ff_pipeline_epoch([ep], hp, _t(x_base), _t(y), _t(y_neg), 10, 128, 1, sched,
+                        loss_trace=trace)
+    st = P.Layer(_t(W), _t(b), True)
+    losses = []
+    for c in range(nc):
+        sl = slice(128 * c, min(300, 128 * (c + 1)))
+        x = np.concatenate([O.embed_labels(x_base[sl], y[sl], 10),
+                            O.embed_labels(x_base[sl], y_neg[sl], 10)]).astype(np.float32)
+        k = sl.stop - sl.start
+        loss = torch.empty(1, device=DEV)
+        P.ff_layer_step(st, hp, _t(x), k, k, loss=loss)
+        losses.append(_np(loss)[0])
+    np.testing.assert_array_equal(_np(trace)[0], np.array(losses, np.float32))
+    assert ep.step == st.step == nc
+    for k in ("W", "b", "mW", "vW", "mb", "vb", "W_bf16"):
+        np.testing.assert_array_equal(_np(getattr(ep, k)), _np(getattr(st, k)), err_msg=k)
+
+
 def test_sequential_reforward_beside_next_layer_bitwise(P):
     """The sequential schedule's forward pass with a trained layer's final
     weights runs on a second stream beside the next layer's steps: the same
