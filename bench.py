@@ -94,7 +94,8 @@ def shape_label(r):
     if kind == "head":
         return f"{m}x{k}->{n} classes ({HEAD_PARTS[aux]})"
     if kind == "loss":
-        return f"{m}x{n}" + (" (+bf16 dZ^T)" if aux else "")
+        return f"{m}x{n}" + (" (+bf16 dZ^T)" if aux & 1 else "") + \
+            (" (+next layer operand)" if aux & 2 else "")
     if kind == "goodness":
         return f"{m} rows x {n} partials"
     if kind == "embed_norm":

@@ -415,8 +415,9 @@ typedef struct {
  *   ADAM         m = d_out, n = d_in, k = rows of the step;
  *   EMBED_NORM   m rows, n features; aux = the row source mode, plus 16
  *                for bf16 output rows;
- *   LOSS         m rows, n = d_out, k = goodness partials per row; aux = 1
- *                when the pass also writes the bf16 weight-gradient operand;
+ *   LOSS         m rows, n = d_out, k = goodness partials per row; aux bit 0:
+ *                the pass also writes the bf16 weight-gradient operand, bit 1:
+ *                and the next layer's normalised bf16 operand;
  *   TRANSPOSE    m rows, n features;
  *   GOODNESS     m rows, n = partials per row;
  *   ARGMAX       m rows, n labels;

@@ -305,6 +305,17 @@ struct LayerInput {
   ffk::RowMap src{};
   bool normalised = false;
   const float *rowscale = nullptr;
+  // bf16 steps: src.base holds the normalised bf16 operand rows [rows][d_in]
+  // and xt their transpose [d_in][padded_rows(rows)], written by the previous
+  // layer's loss pass (NextBf16)
+  const uint16_t *xt = nullptr;
+};
+
+// Where a bf16 training step's loss pass writes the next layer's operand:
+// normalised bf16 rows [rows][d_out] and their transpose [d_out][padded rows].
+struct NextBf16 {
+  uint16_t *rows = nullptr;
+  uint16_t *xt = nullptr;
 };
 
 LayerInput raw_rows(const float *x, const float *rowscale) {
@@ -347,10 +358,12 @@ ffk::AdamArgs adam_args(const ff_hparams *hp, int64_t t) {
 // One training step (n_pos positives first); `s_next` as in forward_core.
 ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int n_pos,
                     int n_neg, float *h_out, float *goodness, float *loss, float *s_next,
-                    StepScratch &s, hipStream_t st) {
+                    StepScratch &s, hipStream_t st, const NextBf16 *nx = nullptr) {
   const int R = n_pos + n_neg;
   const void *xop = in.src.base;
-  if (!in.rowscale)
+  if ((in.xt || nx) && !(hp->dtype == FF_BF16 && s.dzt && !in.rowscale))
+    return fail(FF_ERR_INVALID_ARG, "bf16 operand handoff outside a bf16 training step");
+  if (!in.rowscale && !in.xt)
     FF_TRY(stage_input(in.src, R, L->d_in, in.normalised, hp->dtype, hp->norm_eps, s.xhat, &xop,
                        st));
   float *H = h_out ? h_out : s.h;
@@ -365,15 +378,20 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int
     // the normalised bf16 rows.
     const int Rp = ffk::padded_rows(R), nrb = ffk::loss_blocks(R);
     const uint16_t *xh = static_cast<const uint16_t *>(xop);
-    FF_HIP(launch(FF_KERNEL_LOSS, Sizes{R, L->d_out, nt, 1}, 0.0,
+    FF_HIP(launch(FF_KERNEL_LOSS, Sizes{R, L->d_out, nt, nx ? 3 : 1}, 0.0,
                   (double)nt * R * 4.0 + (double)R * L->d_out * 4.0 + (g ? R * 4.0 : 0.0) +
-                      (double)Rp * L->d_out * 2.0 + (double)nrb * L->d_out * 4.0,
+                      (double)Rp * L->d_out * 2.0 + (double)nrb * L->d_out * 4.0 +
+                      (nx ? ((double)R + Rp) * L->d_out * 2.0 : 0.0),
                   st, [&] {
                     return ffk::launch_loss_t(s.gpart, nt, R, n_pos, hp->theta, H, L->d_out, g,
-                                              nullptr, s.lpart, s.dzt, s.dbp, st);
+                                              nullptr, s.lpart, s.dzt, s.dbp, hp->norm_eps,
+                                              nx ? nx->rows : nullptr, nx ? nx->xt : nullptr, st);
                   }));
-    FF_HIP(launch(FF_KERNEL_TRANSPOSE, Sizes{R, L->d_in, 0, 0}, 0.0, (double)R * L->d_in * 2.0 + (double)Rp * L->d_in * 2.0,
-                  st, [&] { return ffk::launch_transpose_bf16(xh, R, L->d_in, s.xt, st); }));
+    if (!in.xt)
+      FF_HIP(launch(FF_KERNEL_TRANSPOSE, Sizes{R, L->d_in, 0, 0}, 0.0,
+                    (double)R * L->d_in * 2.0 + (double)Rp * L->d_in * 2.0, st,
+                    [&] { return ffk::launch_transpose_bf16(xh, R, L->d_in, s.xt, st); }));
+    const uint16_t *xT = in.xt ? in.xt : s.xt;
     ffk::LossFinish lf;
     lf.lpart = s.lpart;
     lf.nblk = nrb;
@@ -390,7 +408,7 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int
     const double bytes = s.dw ? operands + params * 4.0 : operands + adam;
     FF_HIP(launch(FF_KERNEL_DW_ADAM, Sizes{L->d_out, L->d_in, R, s.dw ? 1 : 0},
                   gemm_flops(L->d_out, L->d_in, R), bytes, st, [&] {
-      return ffk::launch_dw4(s.dzt, s.xt, L->d_out, L->d_in, R, s.dw, L->W, L->mW, L->vW,
+      return ffk::launch_dw4(s.dzt, xT, L->d_out, L->d_in, R, s.dw, L->W, L->mW, L->vW,
                              L->W_bf16, s.dbp, L->b, L->mb, L->vb, a, lf, st);
     }));
     if (s.dw)
@@ -1053,6 +1071,10 @@ struct PipeScratch {
   std::vector<StepScratch> step;    // per layer (pipelined); sequential: steps, re-forward
   std::vector<float *> slot[kPipeSlots];    // pipelined: [l] input slots of layer l (l >= 1)
   std::vector<float *> slot_s[kPipeSlots];  // pipelined, fp32: row normalisation of slot[.][l]
+  // pipelined bf16 FF epochs: layer l's input slots hold its normalised bf16
+  // operand rows and their transpose, written by layer l-1's loss pass
+  bool bf16_handoff = false;
+  std::vector<uint16_t *> slot_b[kPipeSlots], slot_t[kPipeSlots];
   float *act[2] = {nullptr, nullptr};    // sequential: whole-set activations, ping-pong
   float *act_s[2] = {nullptr, nullptr};  // sequential, fp32: their row normalisation
 };
@@ -1061,6 +1083,9 @@ struct PipeScratch {
 // StepScratch::dw), by schedule.
 constexpr bool kSplitAdamPipelined = true;
 constexpr bool kSplitAdamSequential = false;
+// Whether pipelined bf16 FF epochs hand the next layer its operand from the
+// loss pass (PipeScratch::bf16_handoff) instead of the activities.
+constexpr bool kBf16Handoff = true;
 
 // rpp: rows per sample in a chunk (2 for FF: a positive and a negative row;
 // 1 for the performance-optimised variant); po_classes > 0 adds its scratch.
@@ -1068,18 +1093,28 @@ void carve_pipe(Carver &cv, PipeScratch &p, const ff_layer *layers, int L, int n
                 int sched, int dtype, int rpp = 2, int po_classes = 0) {
   const int rows = rpp * std::min(chunk, n);
   if (sched == FF_PIPELINED) {
+    p.bf16_handoff = kBf16Handoff && dtype == FF_BF16 && po_classes == 0;
     p.step.assign(L, StepScratch());
     for (int k = 0; k < kPipeSlots; ++k) {
       p.slot[k].assign(L, nullptr);
       p.slot_s[k].assign(L, nullptr);
+      p.slot_b[k].assign(L, nullptr);
+      p.slot_t[k].assign(L, nullptr);
     }
     for (int l = 0; l < L; ++l)
       carve_step(cv, p.step[l], rows, l == 0 || dtype == FF_BF16 ? layers[l].d_in : 0,
-                 layers[l].d_out, dtype, l + 1 == L, false, false, po_classes, true,
-                 kSplitAdamPipelined);
+                 layers[l].d_out, dtype, l + 1 == L || p.bf16_handoff, false, false, po_classes,
+                 true, kSplitAdamPipelined);
+    const size_t rp = (size_t)ffk::padded_rows(rows);
     for (int l = 1; l < L; ++l)
       for (int k = 0; k < kPipeSlots; ++k) {
-        p.slot[k][l] = static_cast<float *>(cv.take((size_t)rows * layers[l].d_in * 4));
+        const size_t d = (size_t)layers[l].d_in;
+        if (p.bf16_handoff) {
+          p.slot_b[k][l] = static_cast<uint16_t *>(cv.take((size_t)rows * d * 2));
+          p.slot_t[k][l] = static_cast<uint16_t *>(cv.take(rp * d * 2));
+          continue;
+        }
+        p.slot[k][l] = static_cast<float *>(cv.take((size_t)rows * d * 4));
         if (dtype == FF_F32) p.slot_s[k][l] = static_cast<float *>(cv.take((size_t)rows * 4));
       }
   } else {
@@ -1183,7 +1218,7 @@ ff_status epoch_core(ff_layer *layers, int n_layers, const ff_hparams *hp, int n
         }
         FF_TRY(step(l, input_of(l, start, b), start, b, nullptr,
                     loss_trace ? loss_trace + (size_t)l * steps + q : nullptr, nullptr, p.step[0],
-                    st));
+                    st, nullptr));
       }
       if (l + 1 < n_layers && fs == st)
         for (int c = 0; c < nc; ++c) FF_TRY(reforward(l, c, st));
@@ -1213,11 +1248,27 @@ ff_status epoch_core(ff_layer *layers, int n_layers, const ff_hparams *hp, int n
         FF_HIP(hipStreamWaitEvent(
             st, ring.ev[(size_t)(l + 1) * kRing + (q - kPipeSlots) % kRing], 0));
       const int k = q % kPipeSlots;
-      const LayerInput in = l == 0 ? input0(start, b) : raw_rows(p.slot[k][l], p.slot_s[k][l]);
-      const bool next = l + 1 < n_layers;
-      FF_TRY(step(l, in, start, b, next ? p.slot[k][l + 1] : nullptr,
+      const bool next = l + 1 < n_layers, hand = p.bf16_handoff;
+      LayerInput in;
+      if (l == 0) {
+        in = input0(start, b);
+      } else if (hand) {
+        in.src.base = reinterpret_cast<const float *>(p.slot_b[k][l]);  // bf16 rows
+        in.src.mode = ffk::ROWS;
+        in.normalised = true;
+        in.xt = p.slot_t[k][l];
+      } else {
+        in = raw_rows(p.slot[k][l], p.slot_s[k][l]);
+      }
+      NextBf16 nx;
+      if (next && hand) {
+        nx.rows = p.slot_b[k][l + 1];
+        nx.xt = p.slot_t[k][l + 1];
+      }
+      FF_TRY(step(l, in, start, b, next && !hand ? p.slot[k][l + 1] : nullptr,
                   loss_trace ? loss_trace + (size_t)l * steps + q : nullptr,
-                  next ? p.slot_s[k][l + 1] : nullptr, p.step[l], st));
+                  next && !hand ? p.slot_s[k][l + 1] : nullptr, p.step[l], st,
+                  next && hand ? &nx : nullptr));
       FF_HIP(hipEventRecord(ring.ev[(size_t)l * kRing + q % kRing], st));
     }
   }
@@ -1269,8 +1320,8 @@ ff_status ff_pipeline_epoch(ff_layer *layers, int32_t n_layers, const ff_hparams
     return li;
   };
   auto step = [&](int l, const LayerInput &in, int, int b, float *h_out, float *loss,
-                  float *s_next, StepScratch &sc, hipStream_t st) {
-    return step_core(&layers[l], hp, in, b, b, h_out, nullptr, loss, s_next, sc, st);
+                  float *s_next, StepScratch &sc, hipStream_t st, const NextBf16 *nx) {
+    return step_core(&layers[l], hp, in, b, b, h_out, nullptr, loss, s_next, sc, st, nx);
   };
   return epoch_core(layers, n_layers, hp, n, chunk_pairs, epochs, schedule, streams, loss_trace,
                     p, 2, input0, step);
@@ -1626,7 +1677,7 @@ ff_status ff_po_epoch(ff_layer *layers, ff_head *heads, int32_t n_layers, const 
     return li;
   };
   auto step = [&](int l, const LayerInput &in, int start, int b, float *h_out, float *loss,
-                  float *s_next, StepScratch &sc, hipStream_t st) {
+                  float *s_next, StepScratch &sc, hipStream_t st, const NextBf16 *) {
     return po_step_core(&layers[l], &heads[l], hp, head_hp, in, b, labels + start, h_out, loss,
                         s_next, sc, st);
   };

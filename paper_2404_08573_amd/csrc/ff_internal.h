@@ -168,9 +168,12 @@ int padded_rows(int rows);
 // partials lpart[loss_blocks(R)][2]) for a bf16 layer, plus its weight-gradient
 // operand dZ^T = bf16(c . H)^T [D][padded_rows(R)] (R3) and the fp32 column
 // sums of c . H over each 64-row block, dbp[loss_blocks(R)][D] (for db).
+// xn, xnT (both or neither): also the next layer's bf16 operand from H, rows
+// xn [R][D] = bf16(h_r / (sqrt(g_r) + norm_eps)) and xnT [D][padded_rows(R)].
 hipError_t launch_loss_t(const float *gpart, int ntiles, int R, int n_pos, float theta,
                          const float *H, int D, float *g_out, float *c_out, float *lpart,
-                         uint16_t *dzT, float *dbp, hipStream_t s);
+                         uint16_t *dzT, float *dbp, float norm_eps, uint16_t *xn, uint16_t *xnT,
+                         hipStream_t s);
 
 // xT [d][padded_rows(R)] = x^T for bf16 rows x [R][d] (d a multiple of 8),
 // zero in the columns past R.

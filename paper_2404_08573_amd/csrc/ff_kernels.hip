@@ -1426,7 +1426,11 @@ __device__ __forceinline__ void store_tcol(const uint32_t (*T)[kTWords], int c, 
 //   coefficients c are known.  Every workgroup sums its rows' goodness; column
 //   block 0 also writes g, c and the loss partials lpart[2 * block].
 // Rows R..Rp-1 give zero columns of dZ^T.
-template <int SUBS>
+// NEXT: the pass also writes the next layer's bf16 operand from the same H
+// (pre-update activities): its rows xn [R][D] = bf16(h_r / (sqrt(g_r) + eps))
+// (g_r = ||h_r||^2, the goodness) and their transpose xnT [D][Rp] (zero
+// columns past R), so the next layer needs no normalisation or transpose pass.
+template <int SUBS, bool NEXT>
 __global__ __launch_bounds__(kBlock) void k_loss_t(const float *__restrict__ gpart, int nt, int R,
                                                    int Rp, int n_pos, float theta,
                                                    const float *__restrict__ H, int D,
@@ -1434,10 +1438,14 @@ __global__ __launch_bounds__(kBlock) void k_loss_t(const float *__restrict__ gpa
                                                    float *__restrict__ c_out,
                                                    float *__restrict__ lpart,
                                                    uint16_t *__restrict__ dzT,
-                                                   float *__restrict__ dbp) {
+                                                   float *__restrict__ dbp, float norm_eps,
+                                                   uint16_t *__restrict__ xn,
+                                                   uint16_t *__restrict__ xnT) {
   __shared__ float cs[kTRows];
+  __shared__ float ns[NEXT ? kTRows : 1];
   __shared__ float red[SUBS][16][kTRows + 4];
   __shared__ uint32_t T[SUBS][kTRows][kTWords];
+  __shared__ uint32_t TN[NEXT ? SUBS : 1][kTRows][kTWords];
   const int tid = threadIdx.x;
   const int r0 = blockIdx.x * kTRows, cb0 = blockIdx.y * 64 * SUBS;
   const int q = tid & 15, p = tid >> 4;  // column quad; row pairs p and p + 16
@@ -1479,6 +1487,9 @@ __global__ __launch_bounds__(kBlock) void k_loss_t(const float *__restrict__ gpa
         if (g_out) g_out[r] = gv;
         if (c_out) c_out[r] = cr;
       }
+      if (NEXT) ns[tid] = 1.f / (sqrtf(gv) + norm_eps);
+    } else if (NEXT) {
+      ns[tid] = 0.f;
     }
     cs[tid] = cr;
     lp = wave_sum(lp);
@@ -1492,6 +1503,36 @@ __global__ __launch_bounds__(kBlock) void k_loss_t(const float *__restrict__ gpa
   float cc[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) cc[i] = cs[2 * p + (i & 1) + 32 * (i >> 1)];
+  if constexpr (NEXT) {  // the next layer's operand, from the unscaled activities
+    float sn[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) sn[i] = ns[2 * p + (i & 1) + 32 * (i >> 1)];
+#pragma unroll
+    for (int sub = 0; sub < SUBS; ++sub) {
+      float4 t[4];
+      const int col = cb0 + sub * 64 + 4 * q;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float4 w = v[sub][i];
+        t[i] = make_float4(w.x * sn[i], w.y * sn[i], w.z * sn[i], w.w * sn[i]);
+        const int r = r0 + 2 * p + (i & 1) + 32 * (i >> 1);
+        if (r < R && col < D) {
+          uint2 pk;
+          pk.x = pack_bf16(t[i].x, t[i].y);
+          pk.y = pack_bf16(t[i].z, t[i].w);
+          *reinterpret_cast<uint2 *>(xn + (size_t)r * D + col) = pk;
+        }
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const float4 a = t[2 * h], b = t[2 * h + 1];
+        TN[sub][4 * q + 0][p + 16 * h] = pack_bf16(a.x, b.x);
+        TN[sub][4 * q + 1][p + 16 * h] = pack_bf16(a.y, b.y);
+        TN[sub][4 * q + 2][p + 16 * h] = pack_bf16(a.z, b.z);
+        TN[sub][4 * q + 3][p + 16 * h] = pack_bf16(a.w, b.w);
+      }
+    }
+  }
 #pragma unroll
   for (int sub = 0; sub < SUBS; ++sub) {
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -1532,7 +1573,10 @@ __global__ __launch_bounds__(kBlock) void k_loss_t(const float *__restrict__ gpa
 #pragma unroll
   for (int sub = 0; sub < SUBS; ++sub) {
     const int col = cb0 + sub * 64 + c;
-    if (col < D) store_tcol(T[sub], c, seg, dzT + (size_t)col * Rp + r0);
+    if (col < D) {
+      store_tcol(T[sub], c, seg, dzT + (size_t)col * Rp + r0);
+      if constexpr (NEXT) store_tcol(TN[sub], c, seg, xnT + (size_t)col * Rp + r0);
+    }
   }
 }
 
@@ -2365,13 +2409,18 @@ hipError_t launch_loss(const float *gpart, int ntiles, int R, int n_pos, float t
 
 hipError_t launch_loss_t(const float *gpart, int ntiles, int R, int n_pos, float theta,
                         const float *H, int D, float *g, float *c, float *lpart, uint16_t *dzT,
-                        float *dbp, hipStream_t s) {
+                        float *dbp, float norm_eps, uint16_t *xn, uint16_t *xnT, hipStream_t s) {
   if (R <= 0) return hipSuccess;
-  if (D % 4) return hipErrorInvalidValue;
+  if (D % 4 || (xn == nullptr) != (xnT == nullptr)) return hipErrorInvalidValue;
   const int Rp = padded_rows(R);
   constexpr int subs = kLossTSubs;
-  hipLaunchKernelGGL(k_loss_t<subs>, dim3(Rp / kTRows, cdiv(D, 64 * subs)), dim3(kBlock), 0, s,
-                     gpart, ntiles, R, Rp, n_pos, theta, H, D, g, c, lpart, dzT, dbp);
+  const dim3 grid(Rp / kTRows, cdiv(D, 64 * subs));
+  if (xn)
+    hipLaunchKernelGGL((k_loss_t<subs, true>), grid, dim3(kBlock), 0, s, gpart, ntiles, R, Rp,
+                       n_pos, theta, H, D, g, c, lpart, dzT, dbp, norm_eps, xn, xnT);
+  else
+    hipLaunchKernelGGL((k_loss_t<subs, false>), grid, dim3(kBlock), 0, s, gpart, ntiles, R, Rp,
+                       n_pos, theta, H, D, g, c, lpart, dzT, dbp, norm_eps, xn, xnT);
   return hipGetLastError();
 }
 
