@@ -356,9 +356,12 @@ ffk::AdamArgs adam_args(const ff_hparams *hp, int64_t t) {
 }
 
 // One training step (n_pos positives first); `s_next` as in forward_core.
+// out_ready (optional) is recorded on st once the step's outputs for the next
+// layer (h_out, s_next or nx) are written, before the weight update.
 ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int n_pos,
                     int n_neg, float *h_out, float *goodness, float *loss, float *s_next,
-                    StepScratch &s, hipStream_t st, const NextBf16 *nx = nullptr) {
+                    StepScratch &s, hipStream_t st, const NextBf16 *nx = nullptr,
+                    hipEvent_t out_ready = nullptr) {
   const int R = n_pos + n_neg;
   const void *xop = in.src.base;
   if ((in.xt || nx) && !(hp->dtype == FF_BF16 && s.dzt && !in.rowscale))
@@ -387,6 +390,7 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int
                                               nullptr, s.lpart, s.dzt, s.dbp, hp->norm_eps,
                                               nx ? nx->rows : nullptr, nx ? nx->xt : nullptr, st);
                   }));
+    if (out_ready) FF_HIP(hipEventRecord(out_ready, st));
     if (!in.xt)
       FF_HIP(launch(FF_KERNEL_TRANSPOSE, Sizes{R, L->d_in, 0, 0}, 0.0,
                     (double)R * L->d_in * 2.0 + (double)Rp * L->d_in * 2.0, st,
@@ -429,6 +433,7 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int
                   return ffk::launch_loss(s.gpart, nt, R, n_pos, hp->theta, g, s.c, s.lpart,
                                           s_next, hp->norm_eps, in.rowscale, cs, st);
                 }));
+  if (out_ready) FF_HIP(hipEventRecord(out_ready, st));
   ffk::LossFinish lf;
   lf.lpart = s.lpart;
   lf.nblk = ffk::loss_blocks(R);
@@ -1218,7 +1223,7 @@ ff_status epoch_core(ff_layer *layers, int n_layers, const ff_hparams *hp, int n
         }
         FF_TRY(step(l, input_of(l, start, b), start, b, nullptr,
                     loss_trace ? loss_trace + (size_t)l * steps + q : nullptr, nullptr, p.step[0],
-                    st, nullptr));
+                    st, nullptr, nullptr));
       }
       if (l + 1 < n_layers && fs == st)
         for (int c = 0; c < nc; ++c) FF_TRY(reforward(l, c, st));
@@ -1226,24 +1231,28 @@ ff_status epoch_core(ff_layer *layers, int n_layers, const ff_hparams *hp, int n
     return FF_OK;
   }
 
-  // Pipelined: done[l][q % kRing] marks layer l's step q complete.  Layer l's
-  // step q waits for layer l-1's step q (its input slot is filled) and, before
-  // it overwrites layer l+1's slot q % kPipeSlots, for layer l+1's step
-  // q - kPipeSlots (the slot's previous reader).  Both waits are enqueued
-  // before the event they name is recorded again (kRing >= kPipeSlots steps
-  // later, and layer l+1's record of a step follows layer l's in host order).
+  // Pipelined: out[l][q % kRing] marks layer l's step q's output for layer l+1
+  // written (recorded before its weight update), done[l][q % kRing] the whole
+  // step complete.  Layer l's step q waits for out[l-1][q] (its input slot is
+  // filled) and, before it overwrites layer l+1's slot q % kPipeSlots, for
+  // done[l+1][q - kPipeSlots] (the slot's previous reader).  Both waits are
+  // enqueued before the event they name is recorded again (kRing >= kPipeSlots
+  // steps later, and layer l+1's record of a step follows layer l's in host
+  // order).
   constexpr int kRing = 4;
   static_assert(kRing >= kPipeSlots, "event ring");
-  EventRing ring;
+  EventRing ring, out;
   ring.ev.assign((size_t)n_layers * kRing, nullptr);
+  out.ev.assign((size_t)n_layers * kRing, nullptr);
   for (auto &e : ring.ev) FF_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  for (auto &e : out.ev) FF_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
   for (int q = 0; q < steps; ++q) {
     int start, b;
     chunk_map(q % nc, start, b);
     for (int l = 0; l < n_layers; ++l) {
       ff_layer *L = &layers[l];
       hipStream_t st = static_cast<hipStream_t>(streams[l]);
-      if (l > 0) FF_HIP(hipStreamWaitEvent(st, ring.ev[(size_t)(l - 1) * kRing + q % kRing], 0));
+      if (l > 0) FF_HIP(hipStreamWaitEvent(st, out.ev[(size_t)(l - 1) * kRing + q % kRing], 0));
       if (l + 1 < n_layers && q >= kPipeSlots)
         FF_HIP(hipStreamWaitEvent(
             st, ring.ev[(size_t)(l + 1) * kRing + (q - kPipeSlots) % kRing], 0));
@@ -1268,7 +1277,7 @@ ff_status epoch_core(ff_layer *layers, int n_layers, const ff_hparams *hp, int n
       FF_TRY(step(l, in, start, b, next && !hand ? p.slot[k][l + 1] : nullptr,
                   loss_trace ? loss_trace + (size_t)l * steps + q : nullptr,
                   next && !hand ? p.slot_s[k][l + 1] : nullptr, p.step[l], st,
-                  next && hand ? &nx : nullptr));
+                  next && hand ? &nx : nullptr, out.ev[(size_t)l * kRing + q % kRing]));
       FF_HIP(hipEventRecord(ring.ev[(size_t)l * kRing + q % kRing], st));
     }
   }
@@ -1320,8 +1329,10 @@ ff_status ff_pipeline_epoch(ff_layer *layers, int32_t n_layers, const ff_hparams
     return li;
   };
   auto step = [&](int l, const LayerInput &in, int, int b, float *h_out, float *loss,
-                  float *s_next, StepScratch &sc, hipStream_t st, const NextBf16 *nx) {
-    return step_core(&layers[l], hp, in, b, b, h_out, nullptr, loss, s_next, sc, st, nx);
+                  float *s_next, StepScratch &sc, hipStream_t st, const NextBf16 *nx,
+                  hipEvent_t out_ready) {
+    return step_core(&layers[l], hp, in, b, b, h_out, nullptr, loss, s_next, sc, st, nx,
+                     out_ready);
   };
   return epoch_core(layers, n_layers, hp, n, chunk_pairs, epochs, schedule, streams, loss_trace,
                     p, 2, input0, step);
@@ -1677,9 +1688,12 @@ ff_status ff_po_epoch(ff_layer *layers, ff_head *heads, int32_t n_layers, const 
     return li;
   };
   auto step = [&](int l, const LayerInput &in, int start, int b, float *h_out, float *loss,
-                  float *s_next, StepScratch &sc, hipStream_t st, const NextBf16 *) {
-    return po_step_core(&layers[l], &heads[l], hp, head_hp, in, b, labels + start, h_out, loss,
-                        s_next, sc, st);
+                  float *s_next, StepScratch &sc, hipStream_t st, const NextBf16 *,
+                  hipEvent_t out_ready) -> ff_status {
+    FF_TRY(po_step_core(&layers[l], &heads[l], hp, head_hp, in, b, labels + start, h_out, loss,
+                        s_next, sc, st));
+    if (out_ready) FF_HIP(hipEventRecord(out_ready, st));
+    return FF_OK;
   };
   return epoch_core(layers, n_layers, hp, n, chunk, epochs, schedule, streams, loss_trace, p, 1,
                     input0, step);
