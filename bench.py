@@ -28,6 +28,7 @@ roofline fractions.
 """
 import argparse
 import hashlib
+import itertools
 import json
 import os
 import sys
@@ -272,6 +273,70 @@ def copy_calibration(nbytes):
     print(json.dumps({"copy_bytes": nbytes}))
 
 
+COPY_SWEEP_MB = (8, 25, 50, 100, 400, 1024)
+COPY_SWEEP_REPS = 24
+
+
+def _copy_rotation(mb):
+    """Buffers per size: enough distinct ones to cover 600 MB (more than the
+    256 MB last-level cache), at most 12."""
+    return max(1, min(12, 600 // mb))
+
+
+def copy_sweep():
+    """Plain device copies (tensor copy_, which the HIP runtime runs as its own
+    copy kernel) of each size in COPY_SWEEP_MB, COPY_SWEEP_REPS timed launches
+    after one untimed pass over the buffers, each launch on a buffer pair the
+    previous launches did not touch: the HBM rate a copy of that size reaches
+    on this GPU, the calibration for the row kernels' fractions.  Prints the
+    event-timed rate (launch gaps included); --copy-sweep-summary gives each
+    copy's own duration from a rocprofv3 kernel trace of this run."""
+    import torch
+    dev = torch.device("cuda:0")
+    out = {}
+    for mb in COPY_SWEEP_MB:
+        n = mb * (1 << 20) // 4
+        nrot = _copy_rotation(mb)
+        src = [torch.rand(n, device=dev) for _ in range(nrot)]
+        dst = [torch.empty(n, device=dev) for _ in range(nrot)]
+        for i in range(nrot):
+            dst[i].copy_(src[i])
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for k in range(COPY_SWEEP_REPS):
+            dst[k % nrot].copy_(src[k % nrot])
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / COPY_SWEEP_REPS
+        out[f"{mb}MB"] = {"us_per_copy": ms * 1e3, "GB/s": 2 * mb * (1 << 20) / (ms * 1e-3) / 1e9}
+        del src, dst
+        torch.cuda.empty_cache()
+    print(json.dumps(out))
+
+
+def copy_sweep_summary(trace_csv):
+    """Per size of a --copy-sweep run's rocprofv3 kernel trace: the average
+    duration of its timed copies (the runtime's copy-kernel dispatches, in
+    order) and the rate of the bytes read and written against 8 TB/s."""
+    import csv
+    cps = sorted((int(r["Dispatch_Id"]), (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3)
+                 for r in csv.DictReader(open(trace_csv)) if "copyBuffer" in r["Kernel_Name"])
+    need = sum(_copy_rotation(mb) + COPY_SWEEP_REPS for mb in COPY_SWEEP_MB)
+    if len(cps) != need:
+        raise SystemExit(f"{len(cps)} copy dispatches in the trace, {need} expected")
+    print("| copy size | bytes moved (read + write) | rocprof avg us | rate | fraction of 8 TB/s |")
+    print("|---|---|---|---|---|")
+    i = 0
+    for mb in COPY_SWEEP_MB:
+        i += _copy_rotation(mb)
+        us = sum(u for _, u in cps[i:i + COPY_SWEEP_REPS]) / COPY_SWEEP_REPS
+        i += COPY_SWEEP_REPS
+        gbs = 2 * mb * (1 << 20) / (us * 1e-6) / 1e9
+        print(f"| {mb} MiB | {2 * mb} MiB | {us:.1f} | {gbs:.0f} GB/s | "
+              f"{gbs / HBM_PEAK_GBS * 100:.1f} % |")
+
+
 def _counter_per_dispatch(csv_path, counter):
     """Mean value per dispatch of `counter`, by kernel kind and for the copy kernel."""
     import csv
@@ -358,7 +423,10 @@ def hbm_kernels(P, torch, reps=20, recorded=False):
     launches, each timed by the per-launch HIP events of the library's kernel
     timing: algorithmic bytes per launch / average launch duration, against
     the 8 TB/s HBM peak.  Inputs are seeded uniform(0, 1) rows drawn on the
-    device.
+    device; launches rotate over distinct buffers whose total exceeds the
+    256 MB last-level cache, so each reads its inputs from HBM.  (Event pairs
+    add a few microseconds to each launch: the rocprofv3 durations of the
+    same launches, from --hbm, are the kernels' own.)
       embed_norm: normalisation of CIFAR-shaped rows (3072 features): one
         training chunk (4096 rows, bf16 out) and the 49 152-row prefix of the
         set (bf16 and fp32 out);
@@ -390,18 +458,31 @@ def hbm_kernels(P, torch, reps=20, recorded=False):
     d, d_out = 3072, 16
     (W, b), = make_weights(12, (d, d_out))
     x = torch.rand(49152, d, generator=gen, device=dev)
+    # every launch reads rows the previous ones did not: consecutive row blocks
+    # of the 604 MB set (more than the 256 MB last-level cache), round robin
     for rows, bf16 in ((4096, True), (49152, True), (49152, False)):
         dt = P.FF_BF16 if bf16 else P.FF_F32
         L = P.Layer(torch.from_numpy(W).to(dev), torch.from_numpy(b).to(dev), bf16)
         hp = P.HParams(dtype=dt)
-        ws = P.workspace(P.ff_step_workspace_size(rows, d, d_out, dt), dev)
-        xr = x[:rows]
-        r = timed("embed_norm", lambda: P.ff_layer_forward(L, hp, xr, ws=ws))
-        out[f"embed_norm_{rows}x{d}_{'bf16' if bf16 else 'f32'}_out"] = r
-        del ws
-    Wb = torch.rand(3072, 3072, generator=gen, device=dev) - 0.5
-    Lb = P.Layer(Wb, torch.zeros(3072, device=dev), True)
-    out["bf16_shadow_3072x3072"] = timed("bf16_shadow", lambda: P.ff_refresh_bf16_shadow(Lb))
+        nrot = min(49152 // rows, 12)
+        wss = [P.workspace(P.ff_step_workspace_size(rows, d, d_out, dt), dev) for _ in range(nrot)]
+        turn = itertools.count()
+
+        def fwd_next():
+            i = next(turn) % nrot
+            P.ff_layer_forward(L, hp, x[i * rows:(i + 1) * rows], ws=wss[i])
+        r = timed("embed_norm", fwd_next)
+        if r is not None:
+            out[f"embed_norm_{rows}x{d}_{'bf16' if bf16 else 'f32'}_out"] = r
+        del wss
+    del x
+    # 3072 x 3072 layers (37.7 MB of fp32 weights each), round robin over 12
+    shadow = [P.Layer(torch.rand(3072, 3072, generator=gen, device=dev) - 0.5,
+                      torch.zeros(3072, device=dev), True) for _ in range(12)]
+    turn = itertools.count()
+    r = timed("bf16_shadow", lambda: P.ff_refresh_bf16_shadow(shadow[next(turn) % 12]))
+    if r is not None:
+        out["bf16_shadow_3072x3072"] = r
     return out
 
 
@@ -759,12 +840,23 @@ def main():
                     help="run the row kernels at their bench shapes (embedding + "
                          "normalisation, bf16 weight shadow, softmax-layer logits) with every "
                          "launch recorded and exit")
+    ap.add_argument("--copy-sweep", action="store_true",
+                    help="time plain device copies of 8 MiB to 1 GiB on cold buffers and exit "
+                         "(the HBM calibration of the row kernels)")
+    ap.add_argument("--copy-sweep-summary", metavar="KERNEL_TRACE_CSV",
+                    help="per-size copy durations from a rocprofv3 kernel trace of --copy-sweep")
     ap.add_argument("--launch-list", metavar="JSON",
                     help="with --replay, --focus or --hbm: write the recorded launches here")
     ap.add_argument("--rocprof-shapes", nargs=2, metavar=("KERNEL_TRACE_CSV", "LAUNCH_LIST"),
                     help="match a rocprofv3 kernel trace of a --replay/--focus/--hbm run to its "
                          "launch list and print per-kernel, per-shape durations; exit")
     args = ap.parse_args()
+    if args.copy_sweep:
+        copy_sweep()
+        return
+    if args.copy_sweep_summary:
+        copy_sweep_summary(args.copy_sweep_summary)
+        return
     if args.rocprof_shapes:
         rocprof_shapes(*args.rocprof_shapes)
         return

@@ -179,3 +179,21 @@ def test_rocprof_shapes_matches_dispatches_in_order(tmp_path, capsys):
     bench.rocprof_shapes(pre, str(lst))
     out = capsys.readouterr().out
     assert "after 1 earlier ones" in out and "| forward | 64x64->64 | 1 | 6.0 | 4.0 |" in out
+
+
+def test_copy_sweep_summary_reads_the_timed_copies(tmp_path, capsys):
+    rows, d = [], 1
+    for mb in bench.COPY_SWEEP_MB:
+        for k in range(bench._copy_rotation(mb)):  # untimed pass
+            rows.append((d, "__amd_rocclr_copyBuffer", 10 ** 9))
+            d += 1
+        for k in range(bench.COPY_SWEEP_REPS):
+            rows.append((d, "__amd_rocclr_copyBuffer", 2 * mb * (1 << 20) // 4000))  # 4000 B/ns
+            d += 1
+            rows.append((d, "at::native::fill", 5))
+            d += 1
+    bench.copy_sweep_summary(_trace(tmp_path / "c.csv", rows))
+    out = capsys.readouterr().out
+    assert out.count("| 4000 GB/s | 50.0 % |") == len(bench.COPY_SWEEP_MB)
+    with pytest.raises(SystemExit, match="copy dispatches"):
+        bench.copy_sweep_summary(_trace(tmp_path / "s.csv", rows[:5]))
