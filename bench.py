@@ -386,6 +386,82 @@ def traffic_summary(fetch_csv, write_csv, cfetch_csv, cwrite_csv, workload, copy
     print(json.dumps(out, indent=1))
 
 
+def _per_dispatch(csv_path, counter):
+    """[(dispatch id, kind, value)] of the library's kernels for one counter, in dispatch order."""
+    import csv
+    vals = {}
+    for r in csv.DictReader(open(csv_path)):
+        if r["Counter_Name"] != counter:
+            continue
+        kind = kind_of(r["Kernel_Name"])
+        if kind is None:
+            continue
+        d = int(r["Dispatch_Id"])
+        k, v = vals.get(d, (kind, 0.0))
+        vals[d] = (kind, v + float(r["Counter_Value"]))
+    return [(d, k, v) for d, (k, v) in sorted(vals.items())]
+
+
+def traffic_by_shape(fetch_csv, write_csv, cfetch_csv, cwrite_csv, list_json, workload,
+                     copy_bytes):
+    """HBM bytes per launch by kernel and shape: the FETCH_SIZE / WRITE_SIZE runs of a
+    --replay/--focus/--hbm command matched launch by launch to its recorded list (as
+    rocprof_shapes does), each counter scaled by what it reads for a plain device copy
+    of copy_bytes.  Prints a markdown table against the algorithmic bytes and stores
+    the per-kind averages over the timed launches in profiles/traffic.json under
+    `workload`, with the kernel source hash."""
+    L = json.load(open(list_json))
+    recs = L["launches"]
+    kf = copy_bytes / (_largest_dispatch(cfetch_csv, "FETCH_SIZE") * 1024.0)
+    kw = copy_bytes / (_largest_dispatch(cwrite_csv, "WRITE_SIZE") * 1024.0)
+    cols = []
+    for path, counter in ((fetch_csv, "FETCH_SIZE"), (write_csv, "WRITE_SIZE")):
+        d = _per_dispatch(path, counter)
+        skip = len(d) - len(recs)
+        if skip < 0:
+            raise SystemExit(f"{counter}: {len(d)} dispatches, {len(recs)} recorded launches")
+        d = d[skip:]
+        for i, ((_, kind, _), r) in enumerate(zip(d, recs)):
+            if kind != r["kind"]:
+                raise SystemExit(f"{counter} launch {i}: trace has {kind}, list has {r['kind']}")
+        cols.append([v * 1024.0 for _, _, v in d])
+    import collections
+    groups = collections.OrderedDict()
+    kinds = collections.OrderedDict()
+    for i, r in enumerate(recs):
+        if not r["timed"]:
+            continue
+        f, w = cols[0][i] * kf, cols[1][i] * kw
+        for key, acc in (((r["kind"], shape_label(r)), groups), (r["kind"], kinds)):
+            a = acc.setdefault(key, [0, 0.0, 0.0, 0.0])
+            a[0] += 1
+            a[1] += f
+            a[2] += w
+            a[3] += r["bytes"]
+    print(f"Launch list: {L['about']} (kernel source {L['kernel_source_sha256_16']}).  "
+          f"FETCH_SIZE x {kf:.3f}, WRITE_SIZE x {kw:.3f} (the factors a plain device copy of "
+          f"{copy_bytes} bytes reads).\n")
+    print("| kernel | shape | launches | fetched MB / launch | written MB / launch | "
+          "algorithmic MB / launch | measured / algorithmic |")
+    print("|---|---|---|---|---|---|---|")
+    for (kind, lab), (n, f, w, a) in groups.items():
+        print(f"| {kind} | {lab} | {n} | {f / n / 1e6:.1f} | {w / n / 1e6:.1f} | {a / n / 1e6:.1f} | "
+              f"{(f + w) / a:.2f} |")
+    out = {"_about": "HBM bytes per launch from rocprofv3 --pmc FETCH_SIZE and --pmc WRITE_SIZE "
+                     "(KiB per dispatch) scaled by the factor each counter reads for a plain "
+                     f"device copy of {copy_bytes} bytes, averaged over the timed launches of "
+                     "each kernel kind; valid only for the kernel source hash",
+           "fetch_factor": kf, "write_factor": kw}
+    out[workload] = {k: {"bytes_per_launch": (f + w) / n, "fetch_bytes_per_launch": f / n,
+                         "write_bytes_per_launch": w / n, "algorithmic_bytes_per_launch": a / n,
+                         "dispatches": n, "kernel_source_sha256_16": L["kernel_source_sha256_16"]}
+                     for k, (n, f, w, a) in kinds.items()}
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    old = json.load(open(path)) if os.path.exists(path) else {}
+    old.update(out)
+    json.dump(old, open(path, "w"), indent=1)
+
+
 def counter_summary(csv_paths, n_simd=1024, n_xcd=8):
     """Per kernel kind, from rocprofv3 --pmc runs over `--focus` steps: MFMA
     busy fraction = SQ_VALU_MFMA_BUSY_CYCLES / (SIMDs x GPU-active cycles per
@@ -870,7 +946,11 @@ def main():
         counter_summary(args.counter_summary)
         return
     if args.traffic_summary:
-        traffic_summary(*args.traffic_summary, args.workload, args.copy_bytes)
+        if args.launch_list:
+            traffic_by_shape(*args.traffic_summary, args.launch_list, args.workload,
+                             args.copy_bytes)
+        else:
+            traffic_summary(*args.traffic_summary, args.workload, args.copy_bytes)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this build has no multi-GPU path "
@@ -1067,6 +1147,8 @@ def main():
                      "unit": punit, "frac": one["frac"], "traffic": traffic,
                      "avg_launch_us": one["avg_us"], "launches": one["launches"],
                      "algorithmic_flops_per_launch": sum(r["flops"] for r in dom_recs)
+                     / len(dom_recs),
+                     "algorithmic_bytes_per_launch": sum(r["bytes"] for r in dom_recs)
                      / len(dom_recs),
                      "shapes": by_shape(dom_recs, dname),
                      "replay_ms_per_step": replay_ms,

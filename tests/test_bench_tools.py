@@ -197,3 +197,29 @@ def test_copy_sweep_summary_reads_the_timed_copies(tmp_path, capsys):
     assert out.count("| 4000 GB/s | 50.0 % |") == len(bench.COPY_SWEEP_MB)
     with pytest.raises(SystemExit, match="copy dispatches"):
         bench.copy_sweep_summary(_trace(tmp_path / "s.csv", rows[:5]))
+
+
+def test_traffic_by_shape_matches_dispatches_and_scales(tmp_path, monkeypatch, capsys):
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "feedc0de01234567")
+    os.makedirs(tmp_path / "profiles")
+    recs = [_rec("forward", 64, 64, 64, 1.0, 3e6, 0.1), _rec("forward", 64, 64, 64, 1.0, 3e6, 0.1),
+            _rec("loss", 64, 64, 1, 0.0, 1e6, 0.1)]
+    lst = tmp_path / "l.json"
+    bench.write_launch_list(str(lst), recs, [False, True, True], "f32", "test")
+    kib = 1e6 / 1024.0
+    # a torch kernel and a set-up dispatch before the list are skipped
+    f = _csv(tmp_path / "f.csv", [(1, FWD, "FETCH_SIZE", 7.0), (2, FWD, "FETCH_SIZE", 1.0),
+                                  (3, "at::native::x", "FETCH_SIZE", 9.0),
+                                  (4, FWD, "FETCH_SIZE", 2 * kib), (5, LOSS, "FETCH_SIZE", kib)])
+    w = _csv(tmp_path / "w.csv", [(1, FWD, "WRITE_SIZE", 7.0), (2, FWD, "WRITE_SIZE", 1.0),
+                                  (4, FWD, "WRITE_SIZE", kib), (5, LOSS, "WRITE_SIZE", 0.0)])
+    gib_kib = float(1 << 20)
+    cf = _csv(tmp_path / "cf.csv", [(1, COPY, "FETCH_SIZE", gib_kib / 2)])
+    cw = _csv(tmp_path / "cw.csv", [(1, COPY, "WRITE_SIZE", gib_kib)])
+    bench.traffic_by_shape(f, w, cf, cw, str(lst), "wl", 1 << 30)
+    out = capsys.readouterr().out
+    assert "| forward | 64x64->64 | 1 | 4.0 | 1.0 | 3.0 | 1.67 |" in out
+    t = json.load(open(tmp_path / "profiles" / "traffic.json"))["wl"]
+    assert t["forward"]["bytes_per_launch"] == pytest.approx(5e6)
+    assert t["loss"]["fetch_bytes_per_launch"] == pytest.approx(2e6)
