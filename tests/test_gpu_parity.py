@@ -471,6 +471,47 @@ def test_sequential_reforward_beside_next_layer_bitwise(P):
         np.testing.assert_array_equal(_np(x.b), _np(y.b))
 
 
+def test_sequential_reforward_beside_next_layer_bitwise_bf16(P):
+    """bf16: the forward pass with a trained layer's final weights beside the
+    next layer's steps on a second stream (256-pair chunks and a ragged 220-pair
+    last one, two epochs) gives the same result, bit for bit, as on one stream."""
+    hp = P.HParams(theta=2.0, lr=0.01, dtype=P.FF_BF16)
+    dims = (784, 256, 256, 256)
+    x_base, y, y_neg = make_data(82, 1500, dims[0])
+    params = make_weights(83, dims)
+    out = []
+    for streams in (None, [torch.cuda.current_stream()] * 3):
+        layers = [P.Layer(_t(W), _t(b), bf16_shadow=True) for W, b in params]
+        trace = torch.zeros(3, 2 * 6, device=DEV)
+        P.ff_pipeline_epoch(layers, hp, _t(x_base), _t(y), _t(y_neg), 10, 256, 2,
+                            P.FF_SEQUENTIAL, streams=streams, loss_trace=trace)
+        out.append((layers, _np(trace)))
+    np.testing.assert_array_equal(out[0][1], out[1][1])
+    for x, z in zip(out[0][0], out[1][0]):
+        for k in ("W", "b", "mW", "W_bf16"):
+            np.testing.assert_array_equal(_np(getattr(x, k)), _np(getattr(z, k)), err_msg=k)
+
+
+@pytest.mark.parametrize("sched", [0, 1])
+def test_schedule_parity_bf16_three_layers(P, sched):
+    """Three bf16 layers, 230 pairs in 50-pair chunks (a ragged 30-pair last one),
+    both schedules (pipelined: layers 1 and 2 take their normalised bf16 operand
+    and its transpose from the loss pass of the layer before), against the
+    bf16-emulating oracle within what a float32 evaluation of the same run does."""
+    hp_kw = dict(theta=2.0, lr=0.01)
+    dims = (64, 96, 80, 48)
+    x_base, y, y_neg = make_data(92, 230, 64)
+    params = make_weights(93, dims)
+    layers = [P.Layer(_t(W), _t(b), bf16_shadow=True) for W, b in params]
+    trace = torch.zeros(3, 5, device=DEV)
+    P.ff_pipeline_epoch(layers, P.HParams(dtype=P.FF_BF16, **hp_kw), _t(x_base), _t(y),
+                        _t(y_neg), 10, 50, 1, sched, loss_trace=trace)
+    torch.cuda.synchronize()
+    fn = O.train_sequential if sched == 0 else O.train_pipelined
+    _run_check(layers, trace, params, hp_kw["lr"], lambda Ls, obs: fn(
+        Ls, x_base, y, y_neg, 10, 50, 1, O.HParams(bf16=True, **hp_kw), on_step=obs))
+
+
 def test_pipeline_full_size_bench_config(P):
     """The timed training epoch at its full size and launch configuration (60 000
     pairs, 784->2000x4, 58 chunks of 1024+1024 rows and a ragged one of 608+608,
