@@ -284,3 +284,56 @@ def test_graft_build_entry_binds_exports(P, monkeypatch):
     monkeypatch.setattr(B, "build", lambda *a, **k: None)
     entry = importlib.import_module("__graft_entry__")
     entry.build()
+
+
+STRUCTS = {  # C struct -> the binding's ctypes class name
+    "ff_layer": "ff_layer", "ff_head": "ff_head", "ff_hparams": "ff_hparams",
+    "ff_kernel_stats": "ff_kernel_stats", "ff_launch_record": "ff_launch_record"}
+ENUMS = ["FF_F32", "FF_BF16", "FF_SEQUENTIAL", "FF_PIPELINED", "FF_SINGLE_LAYER",
+         "FF_ALL_LAYERS", "FF_KERNEL_EMBED_NORM", "FF_KERNEL_FORWARD", "FF_KERNEL_LOSS",
+         "FF_KERNEL_DW_ADAM", "FF_KERNEL_GOODNESS", "FF_KERNEL_ARGMAX", "FF_KERNEL_SHADOW",
+         "FF_KERNEL_HEAD", "FF_KERNEL_TRANSPOSE", "FF_KERNEL_ADAM", "FF_KERNEL_KINDS"]
+
+
+def test_binding_layouts_match_the_header(P, tmp_path):
+    """Every struct the binding passes has the C header's size and field offsets
+    (a C program compiled against include/ff.h prints them), and the binding's
+    constants and kernel-kind names follow the header's enums."""
+    import json
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("no C compiler")
+    L = P._lib
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "ff.h"', 'int main(void) {',
+             '  printf("{");']
+    for c in STRUCTS:
+        fields = [f for f, _ in getattr(L, STRUCTS[c])._fields_]
+        offs = ", ".join(f'\\"{f}\\": %zu' for f in fields)
+        args = ", ".join(f"offsetof({c}, {f})" for f in fields)
+        lines.append(f'  printf("\\"{c}\\": {{\\"size\\": %zu, {offs}}}, ", sizeof({c}), {args});')
+    for e in ENUMS:
+        lines.append(f'  printf("\\"{e}\\": %d, ", (int){e});')
+    lines += ['  printf("\\"end\\": 0}");', '  return 0;', '}']
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c11", "-I", os.path.join(ROOT, "include"), str(src), "-o",
+                    str(exe)], check=True)
+    got = json.loads(subprocess.run([str(exe)], check=True, capture_output=True,
+                                    text=True).stdout)
+    for c, cls in STRUCTS.items():
+        ct = getattr(L, cls)
+        assert got[c]["size"] == ctypes.sizeof(ct), c
+        for f, _ in ct._fields_:
+            assert got[c][f] == getattr(ct, f).offset, (c, f)
+    assert (got["FF_F32"], got["FF_BF16"]) == (P.FF_F32, P.FF_BF16)
+    assert (got["FF_SEQUENTIAL"], got["FF_PIPELINED"]) == (P.FF_SEQUENTIAL, P.FF_PIPELINED)
+    assert (got["FF_SINGLE_LAYER"], got["FF_ALL_LAYERS"]) == (P.FF_SINGLE_LAYER,
+                                                              P.FF_ALL_LAYERS)
+    names = {"EMBED_NORM": "embed_norm", "FORWARD": "forward", "LOSS": "loss",
+             "DW_ADAM": "dw_adam", "GOODNESS": "goodness", "ARGMAX": "argmax",
+             "SHADOW": "bf16_shadow", "HEAD": "head", "TRANSPOSE": "transpose", "ADAM": "adam"}
+    assert got["FF_KERNEL_KINDS"] == len(L.KERNEL_KINDS) == len(names)
+    for e, n in names.items():
+        assert L.KERNEL_KINDS[got["FF_KERNEL_" + e]] == n, e
