@@ -666,10 +666,14 @@ def ff_fail_next_launch(kind: Optional[str]):
     _check(LIB.ff_fail_next_launch(-1 if kind is None else KERNEL_KINDS.index(kind)))
 
 
+_profile_capacity = [0]  # max_launches of the active profile
+
+
 def ff_profile_start(max_launches: int = 65536, kinds=None):
     """kinds: names from KERNEL_KINDS to time (None: every kind)."""
     mask = 0 if kinds is None else sum(1 << KERNEL_KINDS.index(k) for k in kinds)
     _check(LIB.ff_profile_start(max_launches, mask))
+    _profile_capacity[0] = max_launches
 
 
 def ff_profile_stop(launches: bool = False):
@@ -680,7 +684,7 @@ def ff_profile_stop(launches: bool = False):
     if not launches:
         _check(LIB.ff_profile_stop(arr))
     else:
-        cap = 1 << 20
+        cap = max(_profile_capacity[0], 1)  # no more launches are timed than that
         recs = (ff_launch_record * cap)()
         n = c_int32(0)
         _check(LIB.ff_profile_stop_launches(arr, recs, cap, ctypes.byref(n)))
