@@ -72,7 +72,7 @@ def load_traffic(kernel, workload):
 KIND_OF = [("k_fwd", "forward"), ("k_dw_adam", "dw_adam"), ("k_dw4", "dw_adam"),
            ("k_embed_norm", "embed_norm"), ("k_loss_rows", "loss"), ("k_loss_t", "loss"),
            ("k_goodness", "goodness"), ("k_argmax", "argmax"), ("k_bf16_shadow", "bf16_shadow"),
-           ("k_transpose_bf16", "transpose"), ("k_head_", "head"), ("k_po_dz", "head"),
+           ("k_head_", "head"), ("k_po_dz", "head"),
            ("k_adam_dense", "adam")]
 MFMA_KINDS = ("forward", "dw_adam")
 ROW_MODES = ["rows", "pairs", "expand", "masked", "neutral"]
@@ -96,7 +96,8 @@ def shape_label(r):
         return f"{m}x{k}->{n} classes ({HEAD_PARTS[aux]})"
     if kind == "loss":
         return f"{m}x{n}" + (" (+bf16 dZ^T)" if aux & 1 else "") + \
-            (" (+next layer operand)" if aux & 2 else "")
+            (" (+next layer operand)" if aux & 2 else "") + \
+            (" (+input transpose)" if aux & 4 else "")
     if kind == "goodness":
         return f"{m} rows x {n} partials"
     if kind == "embed_norm":

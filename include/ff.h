@@ -394,7 +394,7 @@ typedef enum {
   FF_KERNEL_ARGMAX = 5,      /* label argmax                                  */
   FF_KERNEL_SHADOW = 6,      /* bf16 weight shadow refresh                    */
   FF_KERNEL_HEAD = 7,        /* softmax layer: logits, gradient, Adam         */
-  FF_KERNEL_TRANSPOSE = 8,   /* bf16 operand transposes of the weight gradient */
+  FF_KERNEL_TRANSPOSE = 8,   /* reserved: the bf16 loss pass writes the transposes */
   FF_KERNEL_ADAM = 9,        /* Adam update from a stored weight gradient     */
   FF_KERNEL_KINDS = 10
 } ff_kernel_kind;
@@ -417,8 +417,8 @@ typedef struct {
  *                for bf16 output rows;
  *   LOSS         m rows, n = d_out, k = goodness partials per row; aux bit 0:
  *                the pass also writes the bf16 weight-gradient operand, bit 1:
- *                and the next layer's normalised bf16 operand;
- *   TRANSPOSE    m rows, n features;
+ *                the next layer's normalised bf16 operand, bit 2: the
+ *                transpose of the layer's bf16 input rows;
  *   GOODNESS     m rows, n = partials per row;
  *   ARGMAX       m rows, n labels;
  *   SHADOW       m x n weights;

@@ -381,20 +381,21 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int
     // the normalised bf16 rows.
     const int Rp = ffk::padded_rows(R), nrb = ffk::loss_blocks(R);
     const uint16_t *xh = static_cast<const uint16_t *>(xop);
-    FF_HIP(launch(FF_KERNEL_LOSS, Sizes{R, L->d_out, nt, nx ? 3 : 1}, 0.0,
+    // without a handed-off transpose the same launch transposes the input rows
+    const bool tr = !in.xt;
+    FF_HIP(launch(FF_KERNEL_LOSS, Sizes{R, L->d_out, nt, 1 | (nx ? 2 : 0) | (tr ? 4 : 0)}, 0.0,
                   (double)nt * R * 4.0 + (double)R * L->d_out * 4.0 + (g ? R * 4.0 : 0.0) +
                       (double)Rp * L->d_out * 2.0 + (double)nrb * L->d_out * 4.0 +
-                      (nx ? ((double)R + Rp) * L->d_out * 2.0 : 0.0),
+                      (nx ? ((double)R + Rp) * L->d_out * 2.0 : 0.0) +
+                      (tr ? ((double)R + Rp) * L->d_in * 2.0 : 0.0),
                   st, [&] {
                     return ffk::launch_loss_t(s.gpart, nt, R, n_pos, hp->theta, H, L->d_out, g,
                                               nullptr, s.lpart, s.dzt, s.dbp, hp->norm_eps,
-                                              nx ? nx->rows : nullptr, nx ? nx->xt : nullptr, st);
+                                              nx ? nx->rows : nullptr, nx ? nx->xt : nullptr,
+                                              tr ? xh : nullptr, L->d_in, tr ? s.xt : nullptr,
+                                              st);
                   }));
     if (out_ready) FF_HIP(hipEventRecord(out_ready, st));
-    if (!in.xt)
-      FF_HIP(launch(FF_KERNEL_TRANSPOSE, Sizes{R, L->d_in, 0, 0}, 0.0,
-                    (double)R * L->d_in * 2.0 + (double)Rp * L->d_in * 2.0, st,
-                    [&] { return ffk::launch_transpose_bf16(xh, R, L->d_in, s.xt, st); }));
     const uint16_t *xT = in.xt ? in.xt : s.xt;
     ffk::LossFinish lf;
     lf.lpart = s.lpart;

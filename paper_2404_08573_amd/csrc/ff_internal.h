@@ -170,17 +170,15 @@ int padded_rows(int rows);
 // sums of c . H over each 64-row block, dbp[loss_blocks(R)][D] (for db).
 // xn, xnT (both or neither): also the next layer's bf16 operand from H, rows
 // xn [R][D] = bf16(h_r / (sqrt(g_r) + norm_eps)) and xnT [D][padded_rows(R)].
+// x, xT (both or neither): also the transpose xT [dx][padded_rows(R)] of the
+// layer's bf16 input rows x [R][dx] (dx a multiple of 8), in the same launch.
 hipError_t launch_loss_t(const float *gpart, int ntiles, int R, int n_pos, float theta,
                          const float *H, int D, float *g_out, float *c_out, float *lpart,
                          uint16_t *dzT, float *dbp, float norm_eps, uint16_t *xn, uint16_t *xnT,
-                         hipStream_t s);
-
-// xT [d][padded_rows(R)] = x^T for bf16 rows x [R][d] (d a multiple of 8),
-// zero in the columns past R.
-hipError_t launch_transpose_bf16(const uint16_t *x, int R, int d, uint16_t *xT, hipStream_t s);
+                         const uint16_t *x, int dx, uint16_t *xT, hipStream_t s);
 
 // bf16 weight gradient dW = dZ^T (xT)^T over padded_rows(R) rows (operands from
-// launch_loss_t and launch_transpose_bf16; M = d_out, N = d_in), with the Adam
+// launch_loss_t; M = d_out, N = d_in), with the Adam
 // update of W, its shadow Wb and b (db from dbp) fused, and the loss scalar of lf.
 // G non-null: dW is stored into G [M][N] instead and W, b are left for
 // launch_adam_dense (the loss scalar is still finished).

@@ -866,10 +866,11 @@ __global__ __launch_bounds__(256) void k_fwd4(const uint16_t *__restrict__ X,
 
 // ---------------------------------------------------------------------------
 // bf16 weight gradient on the four-wave main loop: dW = dZ^T (x_hat^T)^T over
-// the Rp rows (both operands row-major over the rows, from k_loss_t and
-// k_transpose_bf16), with the Adam update of W, its bf16 shadow and (column
-// tile 0) of b fused in the epilogue; the first workgroup also finishes the
-// loss.  The accumulators go through LDS half a tile at a time (the rows of
+// the Rp rows (both operands row-major over the rows, from k_loss_t: its loss
+// workgroups write dZ^T, its transposing ones x_hat^T, or the previous layer's
+// loss pass handed x_hat^T over), with the Adam update of W, its bf16 shadow and
+// (column tile 0) of b fused in the epilogue; the first workgroup also finishes
+// the loss.  The accumulators go through LDS half a tile at a time (the rows of
 // the waves with wm = 0, then wm = 1), and each thread keeps kAdamBatch
 // float4 updates' loads in flight, so the W, m, v traffic streams instead of
 // waiting on one load at a time.  db sums the 64-row column partials of
@@ -1418,6 +1419,32 @@ __device__ __forceinline__ void store_tcol(const uint32_t (*T)[kTWords], int c, 
   dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
 }
 
+// One 64 x 64 tile of x^T [d][Rp] from bf16 rows x [R][d] (d a multiple of 8,
+// zero columns R..Rp-1) through the LDS words T: the tile of rows r0.. and
+// columns c0..  A lane loads eight columns of two consecutive rows.
+__device__ __forceinline__ void transpose_tile(const uint16_t *__restrict__ x, int R, int Rp,
+                                               int d, uint16_t *__restrict__ xT, int r0, int c0,
+                                               uint32_t (*T)[kTWords]) {
+  const int tid = threadIdx.x;
+  {
+    const int pp = tid >> 3, o = tid & 7, col = c0 + 8 * o;
+    uint4 a = make_uint4(0, 0, 0, 0), b = a;
+    if (col < d) {
+      if (r0 + 2 * pp < R) a = ld16(x + (size_t)(r0 + 2 * pp) * d + col);
+      if (r0 + 2 * pp + 1 < R) b = ld16(x + (size_t)(r0 + 2 * pp + 1) * d + col);
+    }
+    const uint32_t av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {  // columns 8o + 2j (low halves) and 8o + 2j + 1 (high)
+      T[8 * o + 2 * j][pp] = (av[j] & 0xFFFFu) | (bv[j] << 16);
+      T[8 * o + 2 * j + 1][pp] = (av[j] >> 16) | (bv[j] & 0xFFFF0000u);
+    }
+  }
+  __syncthreads();
+  const int c = tid >> 2, seg = tid & 3;
+  if (c0 + c < d) store_tcol(T, c, seg, xT + (size_t)(c0 + c) * Rp + r0);
+}
+
 // Loss rows (as k_loss_rows, over 64-row blocks) and dZ^T = bf16(c . H)^T
 // (R3) with the per-block column sums of c . H in fp32 for db:
 //   grid (Rp / 64, ceil(D / (64 SUBS))); each workgroup takes 64 rows and
@@ -1430,6 +1457,9 @@ __device__ __forceinline__ void store_tcol(const uint32_t (*T)[kTWords], int c, 
 // (pre-update activities): its rows xn [R][D] = bf16(h_r / (sqrt(g_r) + eps))
 // (g_r = ||h_r||^2, the goodness) and their transpose xnT [D][Rp] (zero
 // columns past R), so the next layer needs no normalisation or transpose pass.
+// x (optional): the layer's bf16 input rows [R][dx]; the workgroups past the
+// ny loss column blocks write their transpose xT [dx][Rp] (transpose_tile), the
+// other operand of the weight-gradient product, in the same launch.
 template <int SUBS, bool NEXT>
 __global__ __launch_bounds__(kBlock) void k_loss_t(const float *__restrict__ gpart, int nt, int R,
                                                    int Rp, int n_pos, float theta,
@@ -1440,7 +1470,9 @@ __global__ __launch_bounds__(kBlock) void k_loss_t(const float *__restrict__ gpa
                                                    uint16_t *__restrict__ dzT,
                                                    float *__restrict__ dbp, float norm_eps,
                                                    uint16_t *__restrict__ xn,
-                                                   uint16_t *__restrict__ xnT) {
+                                                   uint16_t *__restrict__ xnT,
+                                                   const uint16_t *__restrict__ x, int dx,
+                                                   uint16_t *__restrict__ xT, int ny) {
   __shared__ float cs[kTRows];
   __shared__ float ns[NEXT ? kTRows : 1];
   __shared__ float red[SUBS][16][kTRows + 4];
@@ -1448,6 +1480,10 @@ __global__ __launch_bounds__(kBlock) void k_loss_t(const float *__restrict__ gpa
   __shared__ uint32_t TN[NEXT ? SUBS : 1][kTRows][kTWords];
   const int tid = threadIdx.x;
   const int r0 = blockIdx.x * kTRows, cb0 = blockIdx.y * 64 * SUBS;
+  if ((int)blockIdx.y >= ny) {  // a tile of the input's transpose (uniform per workgroup)
+    transpose_tile(x, R, Rp, dx, xT, r0, (blockIdx.y - ny) * 64, T[0]);
+    return;
+  }
   const int q = tid & 15, p = tid >> 4;  // column quad; row pairs p and p + 16
   // rows 2p, 2p+1, 2p+32, 2p+33 of each sub-tile's column quad
   float4 v[SUBS][4];
@@ -1578,34 +1614,6 @@ __global__ __launch_bounds__(kBlock) void k_loss_t(const float *__restrict__ gpa
       if constexpr (NEXT) store_tcol(TN[sub], c, seg, xnT + (size_t)col * Rp + r0);
     }
   }
-}
-
-// x^T [d][Rp] from bf16 rows x [R][d] (d a multiple of 8), zero columns R..Rp-1:
-// 64 x 64 tiles through LDS, grid (Rp / 64, ceil(d / 64)).  A lane loads eight
-// columns of two consecutive rows.
-__global__ __launch_bounds__(kBlock) void k_transpose_bf16(const uint16_t *__restrict__ x, int R,
-                                                           int Rp, int d,
-                                                           uint16_t *__restrict__ xT) {
-  __shared__ uint32_t T[kTRows][kTWords];
-  const int tid = threadIdx.x;
-  const int r0 = blockIdx.x * kTRows, c0 = blockIdx.y * 64;
-  {
-    const int pp = tid >> 3, o = tid & 7, col = c0 + 8 * o;
-    uint4 a = make_uint4(0, 0, 0, 0), b = a;
-    if (col < d) {
-      if (r0 + 2 * pp < R) a = ld16(x + (size_t)(r0 + 2 * pp) * d + col);
-      if (r0 + 2 * pp + 1 < R) b = ld16(x + (size_t)(r0 + 2 * pp + 1) * d + col);
-    }
-    const uint32_t av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {  // columns 8o + 2j (low halves) and 8o + 2j + 1 (high)
-      T[8 * o + 2 * j][pp] = (av[j] & 0xFFFFu) | (bv[j] << 16);
-      T[8 * o + 2 * j + 1][pp] = (av[j] >> 16) | (bv[j] & 0xFFFF0000u);
-    }
-  }
-  __syncthreads();
-  const int c = tid >> 2, seg = tid & 3;
-  if (c0 + c < d) store_tcol(T, c, seg, xT + (size_t)(c0 + c) * Rp + r0);
 }
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
@@ -2409,27 +2417,24 @@ hipError_t launch_loss(const float *gpart, int ntiles, int R, int n_pos, float t
 
 hipError_t launch_loss_t(const float *gpart, int ntiles, int R, int n_pos, float theta,
                         const float *H, int D, float *g, float *c, float *lpart, uint16_t *dzT,
-                        float *dbp, float norm_eps, uint16_t *xn, uint16_t *xnT, hipStream_t s) {
+                        float *dbp, float norm_eps, uint16_t *xn, uint16_t *xnT,
+                        const uint16_t *x, int dx, uint16_t *xT, hipStream_t s) {
   if (R <= 0) return hipSuccess;
-  if (D % 4 || (xn == nullptr) != (xnT == nullptr)) return hipErrorInvalidValue;
+  if (D % 4 || (xn == nullptr) != (xnT == nullptr) || (x == nullptr) != (xT == nullptr) ||
+      (x && dx % 8))
+    return hipErrorInvalidValue;
   const int Rp = padded_rows(R);
   constexpr int subs = kLossTSubs;
-  const dim3 grid(Rp / kTRows, cdiv(D, 64 * subs));
+  const int ny = (int)cdiv(D, 64 * subs);
+  const dim3 grid(Rp / kTRows, ny + (x ? (int)cdiv(dx, 64) : 0));
   if (xn)
     hipLaunchKernelGGL((k_loss_t<subs, true>), grid, dim3(kBlock), 0, s, gpart, ntiles, R, Rp,
-                       n_pos, theta, H, D, g, c, lpart, dzT, dbp, norm_eps, xn, xnT);
+                       n_pos, theta, H, D, g, c, lpart, dzT, dbp, norm_eps, xn, xnT, x, dx, xT,
+                       ny);
   else
     hipLaunchKernelGGL((k_loss_t<subs, false>), grid, dim3(kBlock), 0, s, gpart, ntiles, R, Rp,
-                       n_pos, theta, H, D, g, c, lpart, dzT, dbp, norm_eps, xn, xnT);
-  return hipGetLastError();
-}
-
-hipError_t launch_transpose_bf16(const uint16_t *x, int R, int d, uint16_t *xT, hipStream_t s) {
-  if (R <= 0) return hipSuccess;
-  if (d % 8) return hipErrorInvalidValue;
-  const int Rp = padded_rows(R);
-  hipLaunchKernelGGL(k_transpose_bf16, dim3(Rp / kTRows, cdiv(d, 64)), dim3(kBlock), 0, s, x, R,
-                     Rp, d, xT);
+                       n_pos, theta, H, D, g, c, lpart, dzT, dbp, norm_eps, xn, xnT, x, dx, xT,
+                       ny);
   return hipGetLastError();
 }
 
