@@ -262,6 +262,48 @@ def focus_steps(rows, d_in, d_out, bf16, steps=3, launch_list=None):
                       "shapes": by_shape(recs[t0:], dname)}))
 
 
+def focus_epoch(rows, d_in, d_out, bf16, chunks=4, launch_list=None):
+    """One untimed and one recorded pipelined epoch of a one-layer net over
+    `chunks` chunks of rows/2 positive + rows/2 negative rows (label-embedded
+    input rows of d_in features): the launch configuration of the pipelined
+    epochs' layer steps (in bf16 the weight-gradient product and Adam run as
+    separate launches), on one stream, for the per-shape rocprofv3 runs."""
+    import torch
+    import paper_2404_08573_amd as P
+    from ffinputs import make_data, make_weights
+    dev = torch.device("cuda:0")
+    dt = P.FF_BF16 if bf16 else P.FF_F32
+    b = rows // 2
+    n = b * chunks
+    x_base, y, y_neg = make_data(3, n, d_in, 0.0)
+    (W, bias), = make_weights(4, (d_in, d_out))
+    xd, yd, ynd = (torch.from_numpy(a).to(dev) for a in (x_base, y, y_neg))
+    P.ff_profile_start(1 << 14)
+    L = P.Layer(torch.from_numpy(W).to(dev), torch.from_numpy(bias).to(dev), bool(bf16))
+    hp = P.HParams(dtype=dt, lr=0.01)
+    ws = P.workspace(P.ff_pipeline_workspace_size([L], n, b, P.FF_PIPELINED, dt), dev)
+    cur = torch.cuda.current_stream(dev)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    for e in range(2):
+        ev[e].record(cur)
+        P.ff_pipeline_epoch([L], hp, xd, yd, ynd, 10, b, 1, P.FF_PIPELINED, streams=[cur],
+                            ws=ws)
+    ev[2].record(cur)
+    torch.cuda.synchronize()
+    _, recs = P.ff_profile_stop(launches=True)
+    half = len(recs) // 2  # the second epoch's launches (the layer's shadow comes first)
+    timed = [i >= len(recs) - half for i in range(len(recs))]
+    dname = "bf16" if bf16 else "f32"
+    step_ms = ev[1].elapsed_time(ev[2]) / chunks
+    write_launch_list(launch_list, recs, timed, dname,
+                      f"one untimed and one timed pipelined epoch of one {d_in}->{d_out} "
+                      f"{dname} layer, {chunks} chunks of {b}+{b} rows, one stream",
+                      steps=chunks, step_ms=step_ms)
+    print(json.dumps({"focus_epoch": [rows, d_in, d_out, bf16], "chunks": chunks,
+                      "step_ms": step_ms,
+                      "shapes": by_shape([r for r, t in zip(recs, timed) if t], dname)}))
+
+
 def copy_calibration(nbytes):
     """One plain device copy of nbytes (read nbytes, write nbytes): the reference
     that scales the FETCH_SIZE / WRITE_SIZE counters to bytes."""
@@ -910,6 +952,9 @@ def main():
                          "steps: print MFMA-busy and wait fractions per kernel kind and exit")
     ap.add_argument("--focus", nargs=4, type=int, metavar=("ROWS", "D_IN", "D_OUT", "BF16"),
                     help="run a few layer steps of one shape on one stream (for counter runs)")
+    ap.add_argument("--focus-epoch", nargs=4, type=int, metavar=("ROWS", "D_IN", "D_OUT", "BF16"),
+                    help="run a one-layer pipelined epoch of that shape on one stream (the "
+                         "pipelined epochs' launch configuration) and exit")
     ap.add_argument("--replay", type=int, metavar="K", default=0,
                     help="run one untimed and K recorded one-stream replays of the step "
                          "(every layer on one HIP stream, then the scoring) and exit")
@@ -939,6 +984,9 @@ def main():
         return
     if args.focus:
         focus_steps(*args.focus, launch_list=args.launch_list)
+        return
+    if args.focus_epoch:
+        focus_epoch(*args.focus_epoch, launch_list=args.launch_list)
         return
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
