@@ -139,7 +139,9 @@ ff_status ff_layer_step(ff_layer *L, const ff_hparams *hp, const float *x, int32
  * until the process ends.  No hipMalloc, hipFree or allocating library call.
  * Arguments and results as ff_layer_step (the same kernels).  The scratch
  * holds the normalised input, the goodness partials and, in bf16, the
- * weight-gradient operands, plus the activities when h_out is NULL and the
+ * weight-gradient operands (and the weight gradient itself where the Adam
+ * update runs as a launch of its own: layers of 3072 x 3072 and up), plus the
+ * activities when h_out is NULL and the
  * goodness and loss when those are NULL; a request that needs more returns
  * FF_ERR_UNSUPPORTED before anything is enqueued (784 -> 2000 and
  * 2000 -> 2000 layers on 2048 rows, and 3072 -> 3072 bf16 layers on 4096 rows
@@ -148,7 +150,7 @@ ff_status ff_layer_step(ff_layer *L, const ff_hparams *hp, const float *x, int32
  * of `stream`.  Every call on a GPU shares that GPU's one scratch: calls
  * that overlap on one GPU (different streams or threads) race, so the
  * caller must order them. */
-#define FF_NOALLOC_SCRATCH_BYTES (96u << 20)
+#define FF_NOALLOC_SCRATCH_BYTES (128u << 20)
 ff_status ff_layer_step_noalloc(ff_layer *L, const ff_hparams *hp, const float *x, int32_t n_pos,
                                 int32_t n_neg, int32_t x_normalised, float *h_out,
                                 float *goodness, float *loss, void *stream);

@@ -316,7 +316,7 @@ def ff_layer_step(layer: Layer, hp: HParams, x: torch.Tensor, n_pos: int, n_neg:
     return h_out, goodness, loss
 
 
-NOALLOC_SCRATCH_BYTES = 96 << 20  # FF_NOALLOC_SCRATCH_BYTES of include/ff.h
+NOALLOC_SCRATCH_BYTES = 128 << 20  # FF_NOALLOC_SCRATCH_BYTES of include/ff.h
 
 
 def ff_layer_step_noalloc(layer: Layer, hp: HParams, x: torch.Tensor, n_pos: int, n_neg: int,

@@ -141,7 +141,9 @@ struct StepScratch {
 
 // train: the scratch of a training step (the bf16 weight-gradient operands);
 // false for forward passes only.  split_adam: a bf16 training step also gets
-// the weight-gradient buffer, and runs its Adam update as a launch of its own.
+// the weight-gradient buffer, and runs its Adam update as a launch of its own;
+// it always does at the sizes where that is faster on one stream
+// (ffk::dw4_split_adam).
 void carve_step(Carver &cv, StepScratch &s, int rows, int d_in, int d_out, int dtype, bool need_h,
                 bool need_g, bool need_loss, int po_classes = 0, bool train = true,
                 bool split_adam = false) {
@@ -165,7 +167,8 @@ void carve_step(Carver &cv, StepScratch &s, int rows, int d_in, int d_out, int d
     s.xt = static_cast<uint16_t *>(cv.take(rp * d_in * 2));
     s.dzt = static_cast<uint16_t *>(cv.take(rp * d_out * 2));
     s.dbp = static_cast<float *>(cv.take((size_t)ffk::loss_blocks(rows) * d_out * 4));
-    if (split_adam) s.dw = static_cast<float *>(cv.take((size_t)d_out * d_in * 4));
+    if (split_adam || ffk::dw4_split_adam(d_out, d_in))
+      s.dw = static_cast<float *>(cv.take((size_t)d_out * d_in * 4));
   }
 }
 

@@ -187,6 +187,13 @@ hipError_t launch_dw4(const uint16_t *dzT, const uint16_t *xT, int M, int N, int
                       float *mb, float *vb, const AdamArgs &a, const LossFinish &lf,
                       hipStream_t s);
 
+// Whether a bf16 training step of a d_out x d_in layer runs its Adam update as
+// a launch of its own: when the product takes one 192x192 tile per CU (every
+// CU would run the fused update after its product at the same time, while
+// launch_adam_dense streams it near the HBM rate; 3072 x 3072 over 4096 rows:
+// 67.5 + 45.2 us against 121.7 us).
+bool dw4_split_adam(int M, int N);
+
 // The Adam update launch_dw4 fuses, from a stored gradient: W, mW, vW, Wb
 // [M][N] from G [M][N] (N a multiple of 4), and b, mb, vb [M] from the db
 // partials dbp [loss_blocks(R)][M] of the R-row step.

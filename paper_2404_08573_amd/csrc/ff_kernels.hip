@@ -2453,13 +2453,15 @@ void dw4_launch(const uint16_t *dzT, const uint16_t *xT, int M, int N, int K, fl
                        mW, vW, Wb, dbp, nrb, b, mb, vb, a, lf);
 }
 
+bool dw4_split_adam(int M, int N) { return (long)cdiv(M, 192) * cdiv(N, 192) >= kCUs; }
+
 hipError_t launch_dw4(const uint16_t *dzT, const uint16_t *xT, int M, int N, int R, float *G,
                       float *W, float *mW, float *vW, uint16_t *Wb, const float *dbp, float *b,
                       float *mb, float *vb, const AdamArgs &a, const LossFinish &lf,
                       hipStream_t s) {
   const int Rp = padded_rows(R), nrb = Rp / kTRows;
   if (N % 8 || Rp > kMaxWidth) return hipErrorInvalidValue;
-  if ((long)cdiv(M, 192) * cdiv(N, 192) >= kCUs)
+  if (dw4_split_adam(M, N))  // the 192x192 rung: one tile per CU
     dw4_launch<192, 192, 3>(dzT, xT, M, N, Rp, G, W, mW, vW, Wb, dbp, nrb, b, mb, vb, a, lf, s);
   else
     dw4_launch<128, 128, 3>(dzT, xT, M, N, Rp, G, W, mW, vW, Wb, dbp, nrb, b, mb, vb, a, lf, s);
