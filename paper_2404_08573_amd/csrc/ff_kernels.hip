@@ -1841,105 +1841,138 @@ __device__ __forceinline__ int head_block(const HeadFeatures &hf, int f, int &j)
 
 // One wave per kHeadRows rows: the C dot products of each row over its
 // feature blocks, reduced across the wave, then the softmax on lanes 0..C-1.
-// The classifier weights go through LDS in chunks of 256 features (double
-// buffered, one barrier per chunk), so the workgroup's 4 waves share each
-// weight load; each wave prefetches its rows' next chunk before working on
-// the current one.  The feature rows are read from HBM once.  A row's sums
-// run in the same order whatever its wave.
+// Lanes run over features, 4 each, so a chunk is 256 consecutive features of
+// one block; the chunks of all blocks form one sequence.  Each wave keeps the
+// loads of the next two chunks in flight while it works on one: three
+// register sets for the feature rows (the loop is unrolled by three, so each
+// set is a fixed set of registers) and three LDS stages for the classifier
+// weights, which go from global memory straight into LDS (buffer_load ...
+// lds), C x 256 features per chunk shared by the workgroup's 4 waves, with
+// one barrier per chunk.  Every chunk step issues the same loads, past the
+// last chunk too (weights out of range, reading zeros; feature rows of the
+// last chunk again), so the wait counts are fixed.  Rows past n are computed
+// on row n-1 and never stored.  A row's sums run in the same order whatever
+// its wave.
 //
-// CC is a compile-time bound on the class count C (C <= CC): the weights of
-// classes C..CC-1 are class C-1 again and their sums are dropped, so the
-// loops have no per-class branches.
+// CC is a compile-time bound on the class count C (C <= CC): classes C..CC-1
+// load class C-1 again and their sums are dropped, so the loops have no
+// per-class branches.
 constexpr int kHeadRows = 2;
+constexpr int kHeadStages = 3;
+constexpr int kHeadBlock = kBlock;
 template <int CC>
-__global__ __launch_bounds__(kBlock) void k_head_logits(HeadFeatures hf, int n, int C,
+__global__ __launch_bounds__(kHeadBlock) void k_head_logits(HeadFeatures hf, int n, int C,
                                                         const int32_t *__restrict__ labels,
                                                         float *__restrict__ logits,
                                                         int32_t *__restrict__ pred,
                                                         float *__restrict__ G,
                                                         float *__restrict__ lrow) {
-  constexpr int RW = kHeadRows;
-  constexpr int WL = (CC * 64 + kBlock - 1) / kBlock;  // weight float4 per thread per chunk
-  __shared__ float4 wsh[2][CC * 64];
+  constexpr int RW = kHeadRows, NWV = kHeadBlock / 64, NS = kHeadStages;
+  // weight loads per wave per chunk: slots past CC reload class CC-1's slot
+  // with the same bytes its own wave writes there
+  constexpr int WL = (CC + NWV - 1) / NWV;
+  constexpr int NV = WL + RW;  // vector-memory operations per wave per chunk
+  static_assert((NS - 2) * NV < 64, "wait count");
+  // one LDS array per stage: the compiler then sees that the weight loads
+  // into one stage do not alias the reads of another, and does not wait for
+  // them before those reads
+  __shared__ float4 wsh0[CC * 64], wsh1[CC * 64], wsh2[CC * 64], wsh3[CC * 64];
+  __shared__ float srow[NWV][kHeadMaxBlocks][RW];
+  static_assert(NS == 3 || NS == 4, "one array per stage");
+  auto stage = [&](auto S) -> float4 * {
+    constexpr int s = decltype(S)::value;
+    return s == 0 ? wsh0 : (s == 1 ? wsh1 : (s == 2 ? wsh2 : wsh3));
+  };
   const int tid = threadIdx.x, lane = tid & 63;
-  const int r0 = (blockIdx.x * (kBlock / 64) + (tid >> 6)) * RW;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform, in scalar registers
+  const int r0 = (blockIdx.x * NWV + wave) * RW;
   const bool active = r0 < n;  // uniform per wave; every wave stages weights
+  int ng = 0;
+  for (int b = 0; b < hf.n_blocks; ++b) ng += (hf.d[b] / 4 + 63) / 64;
+  if (lane < hf.n_blocks * RW) {  // the rows' scale of each block
+    const int b = lane / RW, r = min(r0 + lane % RW, n - 1);
+    srow[wave][b][lane % RW] = hf.s[b] ? hf.s[b][r] : 1.f;
+  }
   float acc[RW][CC];
 #pragma unroll
   for (int q = 0; q < RW; ++q)
 #pragma unroll
     for (int c = 0; c < CC; ++c) acc[q][c] = 0.f;
-  for (int blk = 0; blk < hf.n_blocks; ++blk) {
-    const int d4 = hf.d[blk] >> 2, ldw = hf.ldw[blk];
-    const float *wb = hf.w[blk];
-    const float *hr[RW];
-    float sr[RW];
-#pragma unroll
-    for (int q = 0; q < RW; ++q) {
-      const int r = min(r0 + q, n - 1);  // rows past n: computed, never stored
-      hr[q] = hf.h[blk] + (size_t)r * hf.d[blk];
-      sr[q] = hf.s[blk] ? hf.s[blk][r] : 1.f;
+
+  // chunk cursors (block, chunk within it); the load cursor stops at the last
+  // chunk, whose feature rows the steps past the end load again
+  int lb = 0, lc = 0, cb = 0, cc = 0, lg = 0;
+  auto next = [&](int &b, int &c) {
+    if (++c == (hf.d[b] / 4 + 63) / 64) {
+      ++b;
+      c = 0;
     }
-    const int nch = (d4 + 63) / 64;
-    float4 wreg[WL];
-    auto wload = [&](int ch) {
+  };
+  float4 a[NS][RW];
+  auto issue = [&](auto S) {
+    constexpr int s = decltype(S)::value;
+    const bool past = lg >= ng;
+    const int d4 = hf.d[lb] >> 2, j = lc * 64 + lane;
+    const __amdgpu_buffer_rsrc_t rw =
+        buffer_rsrc(hf.w[lb], (uint32_t)(((C - 1) * hf.ldw[lb] + hf.d[lb]) * 4));
 #pragma unroll
-      for (int k = 0; k < WL; ++k) {
-        const int t = tid + k * kBlock, j = ch * 64 + (t & 63);
-        if (t < CC * 64)
-          wreg[k] = j < d4 ? ld4(wb + (size_t)min(t >> 6, C - 1) * ldw + 4 * j)
-                           : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int i = 0; i < WL; ++i) {
+      const int slot = min(i * NWV + wave, CC - 1);
+      const uint32_t o = !past && j < d4
+                             ? (uint32_t)((min(slot, C - 1) * hf.ldw[lb] + 4 * j) * 4)
+                             : kOutOfRange;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_void *)(stage(S) + slot * 64), 16, o, 0, 0, 0);
+    }
+    const float *h = hf.h[lb] + 4 * min(j, d4 - 1);
+#pragma unroll
+    for (int q = 0; q < RW; ++q) a[s][q] = ld4(h + (size_t)min(r0 + q, n - 1) * hf.d[lb]);
+    ++lg;
+    if (lg < ng) next(lb, lc);
+  };
+  auto compute = [&](auto S) {
+    constexpr int s = decltype(S)::value;
+    const int d4 = hf.d[cb] >> 2, j = cc * 64 + lane;
+    if (active && j < d4) {
+      float4 x[RW];
+#pragma unroll
+      for (int q = 0; q < RW; ++q) {
+        const float sr = srow[wave][cb][q];
+        x[q] = a[s][q];
+        x[q].x *= sr;
+        x[q].y *= sr;
+        x[q].z *= sr;
+        x[q].w *= sr;
       }
-    };
-    auto wstore = [&](int buf) {
 #pragma unroll
-      for (int k = 0; k < WL; ++k) {
-        const int t = tid + k * kBlock;
-        if (t < CC * 64) wsh[buf][t] = wreg[k];
-      }
-    };
-    float4 a[RW];
-    wload(0);
-#pragma unroll
-    for (int q = 0; q < RW; ++q)
-      a[q] = active && lane < d4 ? ld4(hr[q] + 4 * lane) : make_float4(0.f, 0.f, 0.f, 0.f);
-    wstore(0);
-    __syncthreads();
-    for (int ch = 0; ch < nch; ++ch) {
-      const int i = ch * 64 + lane;
-      const bool more = ch + 1 < nch;
-      float4 an[RW];
-      if (more) {
-        wload(ch + 1);
-        const int inext = min(i + 64, d4 - 1);
+      for (int c = 0; c < CC; ++c) {
+        const float4 w = stage(S)[c * 64 + lane];
 #pragma unroll
         for (int q = 0; q < RW; ++q)
-          an[q] = active ? ld4(hr[q] + 4 * inext) : make_float4(0.f, 0.f, 0.f, 0.f);
-      }
-      if (active && i < d4) {
-#pragma unroll
-        for (int q = 0; q < RW; ++q) {
-          a[q].x *= sr[q];
-          a[q].y *= sr[q];
-          a[q].z *= sr[q];
-          a[q].w *= sr[q];
-        }
-#pragma unroll
-        for (int c = 0; c < CC; ++c) {
-          const float4 w = wsh[ch & 1][c * 64 + lane];
-#pragma unroll
-          for (int q = 0; q < RW; ++q)
-            acc[q][c] += a[q].x * w.x + a[q].y * w.y + a[q].z * w.z + a[q].w * w.w;
-        }
-      }
-      if (more) wstore((ch + 1) & 1);
-      __syncthreads();  // chunk ch's buffer is free, chunk ch+1's is written
-      if (more) {
-#pragma unroll
-        for (int q = 0; q < RW; ++q) a[q] = an[q];
+          acc[q][c] += x[q].x * w.x + x[q].y * w.y + x[q].z * w.z + x[q].w * w.w;
       }
     }
+    next(cb, cc);
+  };
+  // Step g: chunk g's loads have landed (only those of the NS - 2 chunks
+  // after it may be in flight) and, past the barrier, every wave has them and
+  // is done with stage g-1, which chunk g+NS-1's weights then refill.
+  auto step = [&](auto S, int g) {
+    constexpr int s = decltype(S)::value;
+    __builtin_amdgcn_s_waitcnt(vmcnt_wait((NS - 2) * NV));
+    lds_barrier();
+    issue(std::integral_constant<int, (s + NS - 1) % NS>{});
+    if (g < ng) compute(S);
+  };
+  issue(std::integral_constant<int, 0>{});
+  issue(std::integral_constant<int, 1>{});
+  if constexpr (NS > 3) issue(std::integral_constant<int, 2>{});
+  for (int g = 0; g < ng; g += NS) {
+    step(std::integral_constant<int, 0>{}, g);
+    step(std::integral_constant<int, 1>{}, g + 1);
+    step(std::integral_constant<int, 2>{}, g + 2);
+    if constexpr (NS > 3) step(std::integral_constant<int, 3>{}, g + 3);
   }
+  __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));  // no weight load outlives the loop
   if (!active) return;
 #pragma unroll
   for (int q = 0; q < RW; ++q) {
@@ -2557,9 +2590,14 @@ hipError_t launch_head_logits(const HeadFeatures &f, int n, int C, const int32_t
   if (C < 1 || C > kHeadMaxClasses || f.n_blocks < 1 || f.n_blocks > kHeadMaxBlocks ||
       f.n_bias < 0 || f.n_bias > kHeadMaxBlocks || ((G || lrow) && !labels))
     return hipErrorInvalidValue;
+  for (int b = 0; b < f.n_blocks; ++b)  // whole float4 of features; weight offsets in 32 bits
+    if (f.d[b] <= 0 || f.d[b] % 4 || f.ldw[b] < f.d[b] ||
+        ((long)(C - 1) * f.ldw[b] + f.d[b]) * 4 >= (1l << 31))
+      return hipErrorInvalidValue;
   head_classes(C, [&](auto cc) {
-    hipLaunchKernelGGL(k_head_logits<decltype(cc)::value>, dim3(cdiv(n, kBlock / 64 * kHeadRows)),
-                       dim3(kBlock), 0, s, f, n, C, labels, logits, pred, G, lrow);
+    hipLaunchKernelGGL(k_head_logits<decltype(cc)::value>,
+                       dim3(cdiv(n, kHeadBlock / 64 * kHeadRows)), dim3(kHeadBlock), 0, s, f, n,
+                       C, labels, logits, pred, G, lrow);
   });
   return hipGetLastError();
 }
