@@ -1878,6 +1878,7 @@ __global__ __launch_bounds__(kHeadBlock) void k_head_logits(HeadFeatures hf, int
   constexpr int WL = (CC + NWV - 1) / NWV;
   constexpr int NV = WL + RW;  // vector-memory operations per wave per chunk
   static_assert((NS - 2) * NV < 64, "wait count");
+  static_assert(kHeadMaxBlocks * RW <= 64, "one lane per row scale");
   // one LDS array per stage: the compiler then sees that the weight loads
   // into one stage do not alias the reads of another, and does not wait for
   // them before those reads

@@ -833,6 +833,8 @@ def _head_case(seed, dims, C, n, first):
 @pytest.mark.parametrize("dims,C,n,first", [((784, 500, 500), 10, 512, 1),
                                             ((64, 96, 80, 48), 10, 37, 1),
                                             ((64, 96, 80, 48), 16, 300, 0),
+                                            ((64, 96, 80, 48), 7, 129, 0),
+                                            ((24, 36, 20), 3, 65, 1),
                                             ((24, 36, 20), 2, 130, 1)])
 def test_head_predict_parity(P, dims, C, n, first):
     x_base, _, params, Wh, bh = _head_case(92, dims, C, n, first)
