@@ -1863,31 +1863,28 @@ __device__ __forceinline__ int head_block(const HeadFeatures &hf, int f, int &j)
 // load class C-1 again and their sums are dropped, so the loops have no
 // per-class branches.
 constexpr int kHeadRows = 2;
-constexpr int kHeadStages = 3;
-constexpr int kHeadBlock = kBlock;
 template <int CC>
-__global__ __launch_bounds__(kHeadBlock) void k_head_logits(HeadFeatures hf, int n, int C,
+__global__ __launch_bounds__(kBlock) void k_head_logits(HeadFeatures hf, int n, int C,
                                                         const int32_t *__restrict__ labels,
                                                         float *__restrict__ logits,
                                                         int32_t *__restrict__ pred,
                                                         float *__restrict__ G,
                                                         float *__restrict__ lrow) {
-  constexpr int RW = kHeadRows, NWV = kHeadBlock / 64, NS = kHeadStages;
+  constexpr int RW = kHeadRows, NWV = kBlock / 64, NS = 3;
   // weight loads per wave per chunk: slots past CC reload class CC-1's slot
   // with the same bytes its own wave writes there
   constexpr int WL = (CC + NWV - 1) / NWV;
   constexpr int NV = WL + RW;  // vector-memory operations per wave per chunk
-  static_assert((NS - 2) * NV < 64, "wait count");
+  static_assert(NV < 64, "wait count");
   static_assert(kHeadMaxBlocks * RW <= 64, "one lane per row scale");
   // one LDS array per stage: the compiler then sees that the weight loads
   // into one stage do not alias the reads of another, and does not wait for
   // them before those reads
-  __shared__ float4 wsh0[CC * 64], wsh1[CC * 64], wsh2[CC * 64], wsh3[CC * 64];
+  __shared__ float4 wsh0[CC * 64], wsh1[CC * 64], wsh2[CC * 64];
   __shared__ float srow[NWV][kHeadMaxBlocks][RW];
-  static_assert(NS == 3 || NS == 4, "one array per stage");
   auto stage = [&](auto S) -> float4 * {
     constexpr int s = decltype(S)::value;
-    return s == 0 ? wsh0 : (s == 1 ? wsh1 : (s == 2 ? wsh2 : wsh3));
+    return s == 0 ? wsh0 : (s == 1 ? wsh1 : wsh2);
   };
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform, in scalar registers
@@ -1959,24 +1956,22 @@ __global__ __launch_bounds__(kHeadBlock) void k_head_logits(HeadFeatures hf, int
     }
     next(cb, cc);
   };
-  // Step g: chunk g's loads have landed (only those of the NS - 2 chunks
-  // after it may be in flight) and, past the barrier, every wave has them and
-  // is done with stage g-1, which chunk g+NS-1's weights then refill.
+  // Step g: chunk g's loads have landed (only chunk g+1's may be in flight)
+  // and, past the barrier, every wave has them and is done with stage g-1,
+  // which chunk g+2's weights then refill.
   auto step = [&](auto S, int g) {
     constexpr int s = decltype(S)::value;
-    __builtin_amdgcn_s_waitcnt(vmcnt_wait((NS - 2) * NV));
+    __builtin_amdgcn_s_waitcnt(vmcnt_wait(NV));
     lds_barrier();
-    issue(std::integral_constant<int, (s + NS - 1) % NS>{});
+    issue(std::integral_constant<int, (s + 2) % NS>{});
     if (g < ng) compute(S);
   };
   issue(std::integral_constant<int, 0>{});
   issue(std::integral_constant<int, 1>{});
-  if constexpr (NS > 3) issue(std::integral_constant<int, 2>{});
   for (int g = 0; g < ng; g += NS) {
     step(std::integral_constant<int, 0>{}, g);
     step(std::integral_constant<int, 1>{}, g + 1);
     step(std::integral_constant<int, 2>{}, g + 2);
-    if constexpr (NS > 3) step(std::integral_constant<int, 3>{}, g + 3);
   }
   __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));  // no weight load outlives the loop
   if (!active) return;
@@ -2601,9 +2596,8 @@ hipError_t launch_head_logits(const HeadFeatures &f, int n, int C, const int32_t
         ((long)(C - 1) * f.ldw[b] + f.d[b]) * 4 >= (1l << 31))
       return hipErrorInvalidValue;
   head_classes(C, [&](auto cc) {
-    hipLaunchKernelGGL(k_head_logits<decltype(cc)::value>,
-                       dim3(cdiv(n, kHeadBlock / 64 * kHeadRows)), dim3(kHeadBlock), 0, s, f, n,
-                       C, labels, logits, pred, G, lrow);
+    hipLaunchKernelGGL(k_head_logits<decltype(cc)::value>, dim3(cdiv(n, kBlock / 64 * kHeadRows)),
+                       dim3(kBlock), 0, s, f, n, C, labels, logits, pred, G, lrow);
   });
   return hipGetLastError();
 }
