@@ -2256,15 +2256,17 @@ using DwSmallBf16 = Tile<64, 64, 64, 2, 2, 2>;
 // tiles for operand reuse when the grid allows: 256x192 on the four-wave
 // kernel (one workgroup per CU) when its grid fills the CUs, and 256x256 on
 // eight waves only from two of its tiles per CU on, where it measured faster.
-// fp32 measured no faster above 128x128.
+// fp32 takes 128x256 on eight waves (one workgroup per CU) only from 16 of its
+// tiles per CU on: 81920x2000x2000 ran 5027 us on it against 5173 us on
+// 128x128, but 18080 rows (1136 such tiles, 4.4 per CU) 1238 against 1108 us.
 template <bool BF16>
 struct FwdTiles;
 template <>
 struct FwdTiles<false> {
-  using Huge = Tile<128, 128, 32, 4, 2, 2>;
-  using Large = Huge;
-  using Big = Huge;
-  using Full = Huge;
+  using Huge = Tile<128, 256, 32, 2, 4, 2>;
+  using Large = Tile<128, 128, 32, 4, 2, 2>;
+  using Big = Large;
+  using Full = Large;
   using Small = Tile<64, 64, 32, 2, 2, 2>;
 };
 template <>
@@ -2285,7 +2287,7 @@ template <bool BF16, bool LARGE = true, class F>
 void fwd_tile(int M, int N, F &&f) {
   using L = FwdTiles<BF16>;
   if constexpr (LARGE) {
-    if (L::Huge::tiles(M, N) >= (BF16 ? 2 : 1) * kCUs) return f(TileTag<typename L::Huge>{});
+    if (L::Huge::tiles(M, N) >= (BF16 ? 2 : 16) * kCUs) return f(TileTag<typename L::Huge>{});
     if (L::Large::tiles(M, N) >= kCUs) return f(TileTag<typename L::Large>{});
   }
   if (L::Big::tiles(M, N) >= 2 * kCUs) return f(TileTag<typename L::Big>{});
