@@ -835,7 +835,10 @@ def _head_case(seed, dims, C, n, first):
                                             ((64, 96, 80, 48), 16, 300, 0),
                                             ((64, 96, 80, 48), 7, 129, 0),
                                             ((24, 36, 20), 3, 65, 1),
-                                            ((24, 36, 20), 2, 130, 1)])
+                                            ((24, 36, 20), 2, 130, 1),
+                                            # the most feature blocks (8), each under one chunk
+                                            ((16, 4, 8, 12, 4, 8, 4, 4, 8), 16, 3, 0),
+                                            ((24, 8, 4), 2, 1, 1)])
 def test_head_predict_parity(P, dims, C, n, first):
     x_base, _, params, Wh, bh = _head_case(92, dims, C, n, first)
     layers = [P.Layer(_t(W), _t(b)) for W, b in params]
