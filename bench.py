@@ -605,6 +605,97 @@ def hbm_kernels(P, torch, reps=20, recorded=False):
     return out
 
 
+def trace_epoch(name):
+    """One untimed and one timed training epoch of workload `name`, launched as
+    other_workloads launches them (fresh streams, one per layer), for a
+    rocprofv3 kernel trace of how the layers' kernels share the GPU
+    (--overlap-summary takes the second epoch's dispatches).  Prints one JSON
+    line with the timed epoch's HIP-event time."""
+    import torch
+    import paper_2404_08573_amd as P
+    from ffinputs import WORKLOADS, make_workload
+    dev = torch.device("cuda:0")
+    w = WORKLOADS[name]
+    x_base, y, y_neg, params = make_workload(w)
+    bf16 = w.dtype == "bf16"
+    dtype = P.FF_BF16 if bf16 else P.FF_F32
+    sched = P.FF_PIPELINED if w.schedule == "pipelined" else P.FF_SEQUENTIAL
+    xd, yd, ynd = (torch.from_numpy(a).to(dev) for a in (x_base, y, y_neg))
+    layers = [P.Layer(torch.from_numpy(W).to(dev), torch.from_numpy(b).to(dev), bf16)
+              for W, b in params]
+    hp = P.HParams(theta=w.theta, lr=w.lr, beta1=w.beta1, beta2=w.beta2, adam_eps=w.adam_eps,
+                   norm_eps=w.norm_eps, dtype=dtype)
+    ws = P.workspace(P.ff_pipeline_workspace_size(layers, w.n, w.chunk_pairs, sched, dtype), dev)
+    cur = torch.cuda.current_stream(dev)
+    streams = [cur] + [torch.cuda.Stream(dev) for _ in range(w.n_layers - 1)]
+
+    def epoch():
+        for s in streams[1:]:
+            s.wait_stream(cur)
+        P.ff_pipeline_epoch(layers, hp, xd, yd, ynd, w.n_classes, w.chunk_pairs, 1, sched,
+                            streams=streams, ws=ws)
+        for s in streams[1:]:
+            cur.wait_stream(s)
+
+    epoch()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(cur)
+    epoch()
+    b.record(cur)
+    torch.cuda.synchronize()
+    print(json.dumps({"workload": name, "schedule": w.schedule, "dtype": w.dtype,
+                      "epoch_ms": a.elapsed_time(b)}), flush=True)
+
+
+def overlap_summary(trace_csv):
+    """From a rocprofv3 kernel trace of a --trace-epoch run, the second epoch
+    (the later half of the library's dispatches; both epochs launch the same
+    kernels): its span, the time any kernel runs, the summed kernel time, each
+    kernel kind's launches and durations, and the time each set of kinds runs
+    together (markdown)."""
+    import csv
+    import collections
+    ev = []
+    for r in csv.DictReader(open(trace_csv)):
+        kind = kind_of(r["Kernel_Name"])
+        if kind is not None:
+            ev.append((int(r["Dispatch_Id"]), int(r["Start_Timestamp"]),
+                       int(r["End_Timestamp"]), kind))
+    ev.sort()
+    if len(ev) % 2:
+        raise SystemExit(f"{len(ev)} dispatches of the library's kernels: not two equal epochs")
+    ev = ev[len(ev) // 2:]
+    t0, t1 = min(e[1] for e in ev), max(e[2] for e in ev)
+    span = (t1 - t0) * 1e-3
+    marks = sorted([(s, 1, k) for _, s, _, k in ev] + [(e, -1, k) for _, _, e, k in ev])
+    active, last, by_mix = collections.Counter(), t0, collections.Counter()
+    for t, d, k in marks:
+        if t > last:
+            mix = " + ".join(sorted(active.elements())) or "(none)"
+            by_mix[mix] += (t - last) * 1e-3
+        active[k] += d
+        last = t
+    busy = span - by_mix.get("(none)", 0.0)
+    per = collections.defaultdict(lambda: [0, 0.0])
+    for _, s, e, k in ev:
+        per[k][0] += 1
+        per[k][1] += (e - s) * 1e-3
+    total = sum(v[1] for v in per.values())
+    print(f"Second epoch: {len(ev)} dispatches of the library's kernels over {span / 1e3:.2f} ms; "
+          f"some kernel runs {busy / span * 100:.1f} % of that time; summed kernel durations "
+          f"{total / 1e3:.2f} ms ({total / span:.2f} kernels at once on average).\n")
+    print("| kernel | launches | summed us | average us (beside the others) |")
+    print("|---|---|---|---|")
+    for k, (n, t) in sorted(per.items(), key=lambda x: -x[1][1]):
+        print(f"| {k} | {n} | {t:.1f} | {t / n:.1f} |")
+    print("\nTime by the set of kernel kinds running together (the 12 largest):\n")
+    print("| kinds running | us | share of the epoch |")
+    print("|---|---|---|")
+    for mix, t in by_mix.most_common(12):
+        print(f"| {mix} | {t:.1f} | {t / span * 100:.1f} % |")
+
+
 def other_workloads(P, torch, names, reps=2, trials=3):
     """Training epochs of the other training workloads (the sequential fp32
     schedule of the same MNIST-shaped net, its bf16 form, and the CIFAR-shaped
@@ -969,6 +1060,11 @@ def main():
                     help="per-size copy durations from a rocprofv3 kernel trace of --copy-sweep")
     ap.add_argument("--launch-list", metavar="JSON",
                     help="with --replay, --focus or --hbm: write the recorded launches here")
+    ap.add_argument("--trace-epoch", metavar="WORKLOAD",
+                    help="run one untimed and one timed training epoch of that workload (as "
+                         "the other workloads run) for a kernel trace, and exit")
+    ap.add_argument("--overlap-summary", metavar="KERNEL_TRACE_CSV",
+                    help="busy time and kernel mixes of a --trace-epoch run's second epoch")
     ap.add_argument("--rocprof-shapes", nargs=2, metavar=("KERNEL_TRACE_CSV", "LAUNCH_LIST"),
                     help="match a rocprofv3 kernel trace of a --replay/--focus/--hbm run to its "
                          "launch list and print per-kernel, per-shape durations; exit")
@@ -981,6 +1077,12 @@ def main():
         return
     if args.rocprof_shapes:
         rocprof_shapes(*args.rocprof_shapes)
+        return
+    if args.overlap_summary:
+        overlap_summary(args.overlap_summary)
+        return
+    if args.trace_epoch:
+        trace_epoch(args.trace_epoch)
         return
     if args.focus:
         focus_steps(*args.focus, launch_list=args.launch_list)

@@ -223,3 +223,30 @@ def test_traffic_by_shape_matches_dispatches_and_scales(tmp_path, monkeypatch, c
     t = json.load(open(tmp_path / "profiles" / "traffic.json"))["wl"]
     assert t["forward"]["bytes_per_launch"] == pytest.approx(5e6)
     assert t["loss"]["fetch_bytes_per_launch"] == pytest.approx(2e6)
+
+
+def test_overlap_summary_of_the_second_epoch(tmp_path, capsys):
+    def trace(path, rows):  # (dispatch id, kernel name, start us, end us)
+        with open(path, "w", newline="") as f:
+            w = csv.DictWriter(f, fieldnames=TRACE_FIELDS)
+            w.writeheader()
+            for d, name, s, e in rows:
+                r = {k: 0 for k in TRACE_FIELDS}
+                r.update(Dispatch_Id=d, Kernel_Name=name, Start_Timestamp=int(s * 1000),
+                         End_Timestamp=int(e * 1000))
+                w.writerow(r)
+        return str(path)
+    first = [(1, FWD, 0, 10), (2, LOSS, 10, 20), (3, FWD, 20, 30)]
+    second = [(4, FWD, 1000, 1100), (5, LOSS, 1050, 1150), (6, FWD, 1200, 1300)]
+    tr = trace(tmp_path / "t.csv", first + [(9, "at::native::copy", 0, 5000)] + second)
+    bench.overlap_summary(tr)
+    out = capsys.readouterr().out
+    assert "3 dispatches of the library's kernels over 0.30 ms" in out
+    assert "some kernel runs 83.3 %" in out and "(1.00 kernels at once" in out
+    assert "| forward | 2 | 200.0 | 100.0 |" in out and "| loss | 1 | 100.0 | 100.0 |" in out
+    assert "| forward | 150.0 | 50.0 % |" in out
+    assert "| forward + loss | 50.0 | 16.7 % |" in out
+    assert "| loss | 50.0 | 16.7 % |" in out and "| (none) | 50.0 | 16.7 % |" in out
+    odd = trace(tmp_path / "o.csv", first + second[:2])
+    with pytest.raises(SystemExit, match="not two equal epochs"):
+        bench.overlap_summary(odd)
