@@ -1871,8 +1871,8 @@ __global__ __launch_bounds__(kBlock) void k_head_logits(HeadFeatures hf, int n, 
                                                         float *__restrict__ G,
                                                         float *__restrict__ lrow) {
   constexpr int RW = kHeadRows, NWV = kBlock / 64, NS = 3;
-  // weight loads per wave per chunk: slots past CC reload class CC-1's slot
-  // with the same bytes its own wave writes there
+  // weight loads per wave per chunk, the same for every wave: the loads past
+  // slot CC-1 write slot CC-1 again, with the bytes its own load writes there
   constexpr int WL = (CC + NWV - 1) / NWV;
   constexpr int NV = WL + RW;  // vector-memory operations per wave per chunk
   static_assert(NV < 64, "wait count");
