@@ -1409,8 +1409,9 @@ constexpr int kTRows = 64;  // batch rows per transposed block
 // the writes of a wave (one column word per lane) then fall on 64 distinct
 // banks, and a lane gathers its 16 rows of a column as 8 words.
 constexpr int kTWords = kTRows / 2 + 1;
-// 64-column sub-tiles per workgroup of the loss pass with the bf16 operand.
-constexpr int kLossTSubs = 2;
+// 64-column sub-tiles per workgroup of the loss pass with the bf16 operand:
+// one (2048 x 2000: 8.4-8.6 against 9.3-9.7 us with two; 4096 x 3072 the same).
+constexpr int kLossTSubs = 1;
 
 // Writes rows r0..r0+63 of column `col` of a transposed tile from T (lane
 // segment seg: rows 16 seg .. 16 seg + 15) to out[col][r0 + ...] (row stride Rp).
