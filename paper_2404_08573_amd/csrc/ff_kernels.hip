@@ -2479,7 +2479,8 @@ hipError_t launch_loss_t(const float *gpart, int ntiles, int R, int n_pos, float
 }
 
 // The bf16 weight-gradient product takes 192x192 tiles when they give every CU
-// one (3072-wide layers), else 128x128.
+// one (3072-wide layers), else 128x128 with four LDS stages (2000x2000 over
+// 2048 rows: 36.3 against 37.1 us with three).
 template <int BM, int BN, int NBUF>
 void dw4_launch(const uint16_t *dzT, const uint16_t *xT, int M, int N, int K, float *G, float *W,
                 float *mW, float *vW, uint16_t *Wb, const float *dbp, int nrb, float *b, float *mb,
@@ -2504,7 +2505,7 @@ hipError_t launch_dw4(const uint16_t *dzT, const uint16_t *xT, int M, int N, int
   if (dw4_split_adam(M, N))  // the 192x192 rung: one tile per CU
     dw4_launch<192, 192, 3>(dzT, xT, M, N, Rp, G, W, mW, vW, Wb, dbp, nrb, b, mb, vb, a, lf, s);
   else
-    dw4_launch<128, 128, 3>(dzT, xT, M, N, Rp, G, W, mW, vW, Wb, dbp, nrb, b, mb, vb, a, lf, s);
+    dw4_launch<128, 128, 4>(dzT, xT, M, N, Rp, G, W, mW, vW, Wb, dbp, nrb, b, mb, vb, a, lf, s);
   return hipGetLastError();
 }
 
