@@ -466,9 +466,12 @@ ff_status step_core(ff_layer *L, const ff_hparams *hp, const LayerInput &in, int
 
 // One performance-optimised step (R rows, labels): the layer and its softmax
 // classifier trained together by backprop through the two, no negatives.
+// out_ready (optional) is recorded on st once h_out and s_next are written,
+// right after the forward: the rest of the step only reads them.
 ff_status po_step_core(ff_layer *L, ff_head *head, const ff_hparams *hp, const ff_hparams *head_hp,
                        const LayerInput &in, int R, const int32_t *labels, float *h_out,
-                       float *loss, float *s_next, StepScratch &s, hipStream_t st) {
+                       float *loss, float *s_next, StepScratch &s, hipStream_t st,
+                       hipEvent_t out_ready = nullptr) {
   const int C = head->n_classes, D = L->d_out;
   const void *xop = in.src.base;
   if (!in.rowscale)
@@ -480,6 +483,7 @@ ff_status po_step_core(ff_layer *L, ff_head *head, const ff_hparams *hp, const f
   if (s_next)
     FF_HIP(goodness_sum(s.gpart, ffk::fwd_col_tiles(R, D, hp->dtype), R, nullptr, nullptr, 0,
                         s_next, hp->norm_eps, st));
+  if (out_ready) FF_HIP(hipEventRecord(out_ready, st));
   ffk::HeadFeatures f{};
   f.n_blocks = 1;
   f.h[0] = H;
@@ -1694,10 +1698,8 @@ ff_status ff_po_epoch(ff_layer *layers, ff_head *heads, int32_t n_layers, const 
   auto step = [&](int l, const LayerInput &in, int start, int b, float *h_out, float *loss,
                   float *s_next, StepScratch &sc, hipStream_t st, const NextBf16 *,
                   hipEvent_t out_ready) -> ff_status {
-    FF_TRY(po_step_core(&layers[l], &heads[l], hp, head_hp, in, b, labels + start, h_out, loss,
-                        s_next, sc, st));
-    if (out_ready) FF_HIP(hipEventRecord(out_ready, st));
-    return FF_OK;
+    return po_step_core(&layers[l], &heads[l], hp, head_hp, in, b, labels + start, h_out, loss,
+                        s_next, sc, st, out_ready);
   };
   return epoch_core(layers, n_layers, hp, n, chunk, epochs, schedule, streams, loss_trace, p, 1,
                     input0, step);
